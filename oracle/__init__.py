@@ -1,0 +1,179 @@
+"""Brute-force fp64 CPU oracle for DISCO spherical convolution.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, ``__graft_entry__.smoke()`` and
+the CPU-baseline leg of ``bench.py`` may import this package.  The GPU library
+never imports, links or calls it, and it shares no code with the GPU library.
+
+The arithmetic lives in ``disco_oracle.c`` (plain C99, fp64, OpenMP): the
+finite DISCO sum of Ocampo, Price & McEwen (ICLR 2023), Sec. 3.2 eq. 4 for the
+forward op and Sec. 3.5 eq. 6 for the transposed op, over every (output, input)
+pixel pair.  This module only compiles it and marshals numpy arrays.
+
+Parity pins (tests/test_oracle_pins.py) check it against closed forms, the
+paper's worked node example (App. E.2), exact invariants and brute force.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+SOURCE = os.path.join(_HERE, "disco_oracle.c")
+LIB_PATH = os.path.join(_HERE, "_build", "libdisco_oracle.so")
+
+QUAD_FEJER1 = 0
+QUAD_CELL_AREA = 1
+
+
+def build(out: str = LIB_PATH, source: str = SOURCE, extra_flags=()) -> str:
+    """Compile the oracle with gcc into a shared library; returns its path."""
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
+           *extra_flags, source, "-o", tmp, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, out)
+    return out
+
+
+_P = ctypes.POINTER
+_dp = _P(ctypes.c_double)
+_i64p = _P(ctypes.c_int64)
+
+
+def _ptr(a: np.ndarray, typ=_dp):
+    return a.ctypes.data_as(typ)
+
+
+class Oracle:
+    """ctypes view of one compiled oracle library (the default, or a variant)."""
+
+    def __init__(self, path: str = LIB_PATH):
+        if not os.path.exists(path) and path == LIB_PATH:
+            build(path)
+        self.path = path
+        lib = ctypes.CDLL(path)
+        lib.oracle_colatitude.restype = ctypes.c_double
+        lib.oracle_colatitude.argtypes = [ctypes.c_int, ctypes.c_int]
+        lib.oracle_longitude.restype = ctypes.c_double
+        lib.oracle_longitude.argtypes = [ctypes.c_int, ctypes.c_int]
+        lib.oracle_quadrature.restype = ctypes.c_int
+        lib.oracle_quadrature.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _dp]
+        lib.oracle_frame_coords.restype = None
+        lib.oracle_frame_coords.argtypes = [ctypes.c_double] * 4 + [_dp] * 3
+        lib.oracle_basis.restype = None
+        lib.oracle_basis.argtypes = [ctypes.c_double] * 3 + [_dp]
+        lib.oracle_psi_dense.restype = ctypes.c_int
+        lib.oracle_psi_dense.argtypes = [ctypes.c_int] * 4 + [ctypes.c_double] * 2 + [_dp]
+        sig = ([ctypes.c_int] * 4 + [ctypes.c_double] * 2 + [ctypes.c_int] * 4 + [_dp] * 3
+               + [ctypes.c_int, ctypes.c_int64, _i64p])
+        for name in ("oracle_forward", "oracle_transpose"):
+            f = getattr(lib, name)
+            f.restype = ctypes.c_int
+            f.argtypes = sig
+        lib.oracle_max_threads.restype = ctypes.c_int
+        self.lib = lib
+
+    # -- grid / quadrature ---------------------------------------------------
+    def colatitudes(self, nlat: int) -> np.ndarray:
+        return np.array([self.lib.oracle_colatitude(t, nlat) for t in range(nlat)])
+
+    def longitudes(self, nlon: int) -> np.ndarray:
+        return np.array([self.lib.oracle_longitude(p, nlon) for p in range(nlon)])
+
+    def quadrature(self, nlat: int, nlon: int, kind: int = QUAD_FEJER1) -> np.ndarray:
+        q = np.zeros(nlat)
+        rc = self.lib.oracle_quadrature(nlat, nlon, kind, _ptr(q))
+        if rc:
+            raise ValueError("oracle_quadrature failed (%d)" % rc)
+        return q
+
+    # -- geometry / basis ------------------------------------------------------
+    def frame_coords(self, theta_j, phi_j, theta_i, phi_i):
+        th, u, v = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+        self.lib.oracle_frame_coords(theta_j, phi_j, theta_i, phi_i,
+                                     ctypes.byref(th), ctypes.byref(u), ctypes.byref(v))
+        return th.value, u.value, v.value
+
+    def basis(self, u: float, v: float, h: float) -> np.ndarray:
+        out = np.zeros(9)
+        self.lib.oracle_basis(u, v, h, _ptr(out))
+        return out
+
+    def psi_dense(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, h=None) -> np.ndarray:
+        h = theta_c / 3.0 if not h else h
+        n_in, n_out = nlat_in * nlon_in, nlat_out * nlon_out
+        psi = np.zeros((n_out, n_in, 9))
+        rc = self.lib.oracle_psi_dense(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, h, _ptr(psi))
+        if rc:
+            raise ValueError("oracle_psi_dense failed (%d)" % rc)
+        return psi
+
+    # -- convolutions --------------------------------------------------------------
+    def _run(self, fn, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, x, w, h, quad, window,
+             pix, out_grid):
+        x = np.ascontiguousarray(x, dtype=np.float64)
+        w = np.ascontiguousarray(w, dtype=np.float64)
+        B, C_x = x.shape[0], x.shape[1]
+        C_y = w.shape[0] if fn == "oracle_forward" else w.shape[1]
+        if pix is None:
+            pix = np.arange(out_grid[0] * out_grid[1], dtype=np.int64)
+        pix = np.ascontiguousarray(pix, dtype=np.int64)
+        y = np.zeros((B, C_y, pix.size))
+        h = theta_c / 3.0 if not h else h
+        rc = getattr(self.lib, fn)(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, h, quad,
+                                   B, C_x, C_y, _ptr(x), _ptr(w), _ptr(y), int(window),
+                                   pix.size, _ptr(pix, _i64p))
+        if rc:
+            raise ValueError("%s failed (%d)" % (fn, rc))
+        return y
+
+    def forward(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, x, w, *, h=None,
+                quad=QUAD_FEJER1, window=True, pix=None):
+        """y[B, Cout, n] for x[B, Cin, nlat_in, nlon_in], w[Cout, Cin, 9].
+
+        ``pix`` selects flat out-grid pixels (default: all, returned reshaped
+        to [B, Cout, nlat_out, nlon_out])."""
+        y = self._run("oracle_forward", nlat_in, nlon_in, nlat_out, nlon_out, theta_c, x, w, h,
+                      quad, window, pix, (nlat_out, nlon_out))
+        if pix is None:
+            y = y.reshape(y.shape[0], y.shape[1], nlat_out, nlon_out)
+        return y
+
+    def transpose(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, x, w, *, h=None,
+                  quad=QUAD_FEJER1, window=True, pix=None):
+        """Transposed op of plan (in-grid, out-grid): x[B, CinT, nlat_out, nlon_out],
+        w[CinT, CoutT, 9] -> y[B, CoutT, nlat_in, nlon_in] (or [B, CoutT, n])."""
+        y = self._run("oracle_transpose", nlat_in, nlon_in, nlat_out, nlon_out, theta_c, x, w, h,
+                      quad, window, pix, (nlat_in, nlon_in))
+        if pix is None:
+            y = y.reshape(y.shape[0], y.shape[1], nlat_in, nlon_in)
+        return y
+
+    def max_threads(self) -> int:
+        return int(self.lib.oracle_max_threads())
+
+
+_default = None
+
+
+def default() -> Oracle:
+    """The oracle built from ``disco_oracle.c`` (compiled on first use)."""
+    global _default
+    if _default is None:
+        if not os.path.exists(LIB_PATH):
+            build()
+        _default = Oracle(LIB_PATH)
+    return _default
+
+
+def default_h(theta_c: float) -> float:
+    """Node spacing of the 3x3 grid: theta_c / 3 (App. E.2 puts the edge nodes at
+    pi/L with a cutoff of 3 pi/L)."""
+    return theta_c / 3.0
+
+
+__all__ = ["Oracle", "build", "default", "default_h", "QUAD_FEJER1", "QUAD_CELL_AREA"]

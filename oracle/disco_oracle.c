@@ -1,0 +1,353 @@
+/*
+ * disco_oracle.c -- brute-force fp64 reference for DISCO spherical convolution.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the oracle that the GPU library is
+ * checked against.  Only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg load it.  It shares no code, header, table or constant with
+ * the GPU library and includes nothing from it.
+ *
+ * What it computes (Ocampo, Price & McEwen, "Scalable and Equivariant
+ * Spherical CNNs by Discrete-Continuous (DISCO) Convolutions", ICLR 2023):
+ *
+ *   forward   (Sec. 3.2, eq. 4 restricted to SO(3)/SO(2); Sec. 4.1 sparse form)
+ *     Z[b,ci,k](j) = sum_i psi_k(R_j^{-1} w_i) q_in(i) x[b,ci,i]
+ *     y[b,co,j]    = sum_{ci,k} W[co,ci,k] Z[b,ci,k](j)
+ *   transpose (Sec. 3.5, eq. 6: the filter is centred at the transposed op's
+ *              input points w_j and weighted by their quadrature)
+ *     Z'[b,c',k](i) = sum_j psi_k(R_j^{-1} w_i) q_out(j) xT[b,c',j]
+ *     yT[b,c,i]     = sum_{c',k} W[c',c,k] Z'[b,c',k](i)
+ *
+ * with R_j = Z(phi_j) Y(theta_j) (Sec. 3.2, zyz Euler angles without gamma).
+ *
+ * It is the plain finite sum over every (output, input) pixel pair: the sparse
+ * form (Sec. 4.1) and the longitude-shift compression (Sec. 4.2) are exact
+ * rewrites of this sum, so none of them appear here.  Geometry goes through
+ * explicit 3x3 rotation matrices in Cartesian coordinates (a different route
+ * from the GPU library's plan).  Everything is double precision.
+ *
+ * Readings of points the paper leaves open (grid, quadrature rule, rotation
+ * handedness, tangent-plane map, node spacing, basis ordering) are stated at
+ * each function.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#ifndef M_PI
+#define M_PI 3.14159265358979323846
+#endif
+
+/* ------------------------------------------------------------------------- */
+/* Grid.  Equiangular, cell-centred: colatitude (t + 1/2) pi / nlat, longitude
+ * 2 pi p / nlon; longitude is the fastest index.  (The paper's own grid keeps
+ * both poles, Sec. 4.2 "Explicit sampling"; this workload's grid does not.)  */
+/* ------------------------------------------------------------------------- */
+double oracle_colatitude(int t, int nlat) { return (t + 0.5) * M_PI / (double)nlat; }
+double oracle_longitude(int p, int nlon) { return 2.0 * M_PI * (double)p / (double)nlon; }
+
+/* ------------------------------------------------------------------------- */
+/* Quadrature weights q(theta_t), one per ring; a pixel's weight is its ring's.
+ * The paper adopts sampling-theorem quadrature without upsampling (Sec. 3.2,
+ * Sec. 4.1, App. A).  App. A gives weights only for its pole-including grid;
+ * on the cell-centred grid the analogous rule that integrates band-limited
+ * signals exactly is Fejer's first rule in x = cos(theta), times 2 pi / nlon
+ * for the longitude sum:
+ *   w_t = (2/n) [ 1 - 2 sum_{m=1}^{floor(n/2)} cos(2 m theta_t) / (4 m^2 - 1) ]
+ * kind 0 = that rule; kind 1 = exact cell areas 2 sin(theta_t) sin(dtheta/2). */
+/* ------------------------------------------------------------------------- */
+int oracle_quadrature(int nlat, int nlon, int kind, double* q)
+{
+    if (nlat < 1 || nlon < 1 || !q) return 1;
+    for (int t = 0; t < nlat; ++t) {
+        double th = oracle_colatitude(t, nlat);
+        double w;
+        if (kind == 0) {
+            double s = 0.0;
+            for (int m = 1; m <= nlat / 2; ++m)
+                s += cos(2.0 * m * th) / (4.0 * (double)m * (double)m - 1.0);
+            w = (2.0 / nlat) * (1.0 - 2.0 * s);
+        } else if (kind == 1) {
+            w = 2.0 * sin(th) * sin(0.5 * M_PI / nlat);
+        } else {
+            return 2;
+        }
+        q[t] = (2.0 * M_PI / nlon) * w;
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Rotations.  Active, right-handed:
+ *   Z(a) = [[cos a, -sin a, 0], [sin a, cos a, 0], [0, 0, 1]]
+ *   Y(b) = [[cos b, 0, sin b], [0, 1, 0], [-sin b, 0, cos b]]
+ * R_j^{-1} = Y(-theta_j) Z(-phi_j) maps the output point to the north pole.  */
+/* ------------------------------------------------------------------------- */
+static void mat_z(double a, double m[9])
+{
+    double c = cos(a), s = sin(a);
+    m[0] = c;   m[1] = -s;  m[2] = 0.0;
+    m[3] = s;   m[4] = c;   m[5] = 0.0;
+    m[6] = 0.0; m[7] = 0.0; m[8] = 1.0;
+}
+static void mat_y(double b, double m[9])
+{
+    double c = cos(b), s = sin(b);
+    m[0] = c;   m[1] = 0.0; m[2] = s;
+    m[3] = 0.0; m[4] = 1.0; m[5] = 0.0;
+    m[6] = -s;  m[7] = 0.0; m[8] = c;
+}
+static void mat_mul(const double a[9], const double b[9], double c[9])
+{
+    for (int r = 0; r < 3; ++r)
+        for (int col = 0; col < 3; ++col) {
+            double s = 0.0;
+            for (int k = 0; k < 3; ++k) s += a[3 * r + k] * b[3 * k + col];
+            c[3 * r + col] = s;
+        }
+}
+/* M = R^{-1} for R = Z(phi) Y(theta). */
+static void inverse_rotation(double theta, double phi, double m[9])
+{
+    double my[9], mz[9];
+    mat_y(-theta, my);
+    mat_z(-phi, mz);
+    mat_mul(my, mz, m);
+}
+static void unit_vector(double theta, double phi, double e[3])
+{
+    e[0] = sin(theta) * cos(phi);
+    e[1] = sin(theta) * sin(phi);
+    e[2] = cos(theta);
+}
+
+/* Filter-frame coordinates of R_j^{-1} w_i.  Theta is the geodesic distance
+ * from the filter centre, taken with atan2 (never acos).  The tangent-plane
+ * map is azimuthal equidistant, (u, v) = Theta (cos Phi, sin Phi): it is the
+ * azimuthal projection that puts the 3x3 grid's edge nodes at Theta = h and
+ * its corner nodes at Theta = sqrt(2) h, as App. E.2 places them.  Phi = 0
+ * points to increasing colatitude (south), Phi = pi/2 to increasing
+ * longitude (east). */
+static void frame_coords_m(const double m[9], const double e[3],
+                           double* Theta, double* u, double* v)
+{
+    double xr = m[0] * e[0] + m[1] * e[1] + m[2] * e[2];
+    double yr = m[3] * e[0] + m[4] * e[1] + m[5] * e[2];
+    double zr = m[6] * e[0] + m[7] * e[1] + m[8] * e[2];
+    double rho = hypot(xr, yr);
+    double th = atan2(rho, zr);
+    *Theta = th;
+    if (rho > 0.0) {
+        *u = th * xr / rho;
+        *v = th * yr / rho;
+    } else {
+        *u = 0.0;
+        *v = 0.0;
+    }
+}
+
+void oracle_frame_coords(double theta_j, double phi_j, double theta_i, double phi_i,
+                         double* Theta, double* u, double* v)
+{
+    double m[9], e[3];
+    inverse_rotation(theta_j, phi_j, m);
+    unit_vector(theta_i, phi_i, e);
+    frame_coords_m(m, e, Theta, u, v);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Filter basis (Sec. 3.4 and App. E.2): a square 3x3 node grid with spacing h
+ * in the tangent plane, nodes at ((a-1) h, (b-1) h), a, b in {0,1,2}, node
+ * index k = 3a + b (a along u = south, b along v = east).  Values between
+ * nodes by bilinear interpolation of a zero-padded node grid, i.e. the tensor
+ * product of hat functions L(s) = max(0, 1 - |s|):
+ *   psi_k(u, v) = L(u/h - (a-1)) L(v/h - (b-1)).
+ * The filter is zero beyond the cutoff Theta > theta_c (Sec. 3.4).           */
+/* ------------------------------------------------------------------------- */
+static double hat(double s)
+{
+    double a = fabs(s);
+    return a < 1.0 ? 1.0 - a : 0.0;
+}
+
+void oracle_basis(double u, double v, double h, double psi[9])
+{
+    for (int a = 0; a < 3; ++a)
+        for (int b = 0; b < 3; ++b)
+            psi[3 * a + b] = hat(u / h - (a - 1)) * hat(v / h - (b - 1));
+}
+
+/* Evaluate all 9 basis functions of the filter centred at (theta_j, phi_j)
+ * at the input point e; returns 0 if the point is beyond the cutoff or all
+ * nine values vanish, 1 otherwise. */
+static int filter_values(const double m[9], const double e[3], double theta_c, double h,
+                         double psi[9])
+{
+    double Th, u, v;
+    frame_coords_m(m, e, &Th, &u, &v);
+    if (Th > theta_c) return 0;
+    oracle_basis(u, v, h, psi);
+    for (int k = 0; k < 9; ++k)
+        if (psi[k] != 0.0) return 1;
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Dense Psi tensor psi[j][i][k] = psi_k(R_j^{-1} w_i) (no quadrature),
+ * j over out-grid pixels, i over in-grid pixels (Sec. 4.1).  Tiny grids only. */
+/* ------------------------------------------------------------------------- */
+int oracle_psi_dense(int nlat_in, int nlon_in, int nlat_out, int nlon_out,
+                     double theta_c, double h, double* psi)
+{
+    if (!psi) return 1;
+    int64_t n_in = (int64_t)nlat_in * nlon_in, n_out = (int64_t)nlat_out * nlon_out;
+    memset(psi, 0, sizeof(double) * (size_t)(n_out * n_in * 9));
+#pragma omp parallel for schedule(dynamic)
+    for (int64_t j = 0; j < n_out; ++j) {
+        double m[9];
+        inverse_rotation(oracle_colatitude((int)(j / nlon_out), nlat_out),
+                         oracle_longitude((int)(j % nlon_out), nlon_out), m);
+        for (int64_t i = 0; i < n_in; ++i) {
+            double e[3], val[9];
+            unit_vector(oracle_colatitude((int)(i / nlon_in), nlat_in),
+                        oracle_longitude((int)(i % nlon_in), nlon_in), e);
+            if (filter_values(m, e, theta_c, h, val))
+                for (int k = 0; k < 9; ++k) psi[(j * n_in + i) * 9 + k] = val[k];
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* The convolution sums.
+ *
+ * `window` = 0 visits every input ring; `window` = 1 visits only rings whose
+ * colatitude is within theta_c of the output point's.  The second is exact:
+ * by the spherical law of cosines the geodesic distance between two points is
+ * at least the difference of their colatitudes, so every skipped ring lies
+ * entirely beyond the cutoff.  Inside a visited ring every longitude is
+ * visited.
+ *
+ * `pix` lists the flat output-pixel indices to compute (t * nlon + p); y is
+ * written as y[b][c][n] for n over that list.                                */
+/* ------------------------------------------------------------------------- */
+typedef struct {
+    int nlat, nlon;
+} grid_t;
+
+/* Shared body: the filter is centred at points of grid `ctr`, evaluated at
+ * points of grid `ev`.  forward: centre = output pixel, sum over input pixels
+ * (the evaluation points), quadrature of the evaluation points' grid.
+ * transpose: centre = each input pixel of the transposed op, evaluation at the
+ * output pixel, quadrature of the centres' grid. */
+static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, double h,
+                     int quad_kind, int B, int Cin, int Cout, const double* x,
+                     const double* w, double* y, int window, int64_t n_pix,
+                     const int64_t* pix)
+{
+    if (!x || !w || !y || !pix || B < 0 || Cin < 1 || Cout < 1) return 1;
+    double* q_in = (double*)malloc(sizeof(double) * (size_t)g_in.nlat);
+    if (!q_in) return 3;
+    if (oracle_quadrature(g_in.nlat, g_in.nlon, quad_kind, q_in)) {
+        free(q_in);
+        return 2;
+    }
+    int64_t n_in = (int64_t)g_in.nlat * g_in.nlon;
+    int64_t n_out_total = (int64_t)g_out.nlat * g_out.nlon;
+    int bad = 0;
+#pragma omp parallel
+    {
+        double* Z = (double*)malloc(sizeof(double) * (size_t)B * Cin * 9);
+#pragma omp for schedule(dynamic)
+        for (int64_t n = 0; n < n_pix; ++n) {
+            int64_t o = pix[n];
+            if (o < 0 || o >= n_out_total || !Z) {
+#pragma omp atomic write
+                bad = 1;
+                continue;
+            }
+            int to = (int)(o / g_out.nlon), po = (int)(o % g_out.nlon);
+            double th_o = oracle_colatitude(to, g_out.nlat), ph_o = oracle_longitude(po, g_out.nlon);
+            memset(Z, 0, sizeof(double) * (size_t)B * Cin * 9);
+            double m_o[9], e_o[3];
+            inverse_rotation(th_o, ph_o, m_o);
+            unit_vector(th_o, ph_o, e_o);
+            for (int t = 0; t < g_in.nlat; ++t) {
+                double th_i = oracle_colatitude(t, g_in.nlat);
+                if (window && fabs(th_i - th_o) > theta_c) continue;
+                for (int p = 0; p < g_in.nlon; ++p) {
+                    double ph_i = oracle_longitude(p, g_in.nlon);
+                    double val[9];
+                    int nz;
+                    if (!transpose) {
+                        double e_i[3];
+                        unit_vector(th_i, ph_i, e_i);
+                        nz = filter_values(m_o, e_i, theta_c, h, val);
+                    } else {
+                        double m_i[9];
+                        inverse_rotation(th_i, ph_i, m_i);
+                        nz = filter_values(m_i, e_o, theta_c, h, val);
+                    }
+                    if (!nz) continue;
+                    double qw = q_in[t];
+                    for (int b = 0; b < B; ++b)
+                        for (int c = 0; c < Cin; ++c) {
+                            double xv = x[((int64_t)b * Cin + c) * n_in + (int64_t)t * g_in.nlon + p];
+                            double* zc = Z + ((size_t)b * Cin + c) * 9;
+                            for (int k = 0; k < 9; ++k) zc[k] += val[k] * qw * xv;
+                        }
+                }
+            }
+            for (int b = 0; b < B; ++b)
+                for (int co = 0; co < Cout; ++co) {
+                    double s = 0.0;
+                    for (int ci = 0; ci < Cin; ++ci)
+                        for (int k = 0; k < 9; ++k) {
+                            /* forward: W[co][ci][k]; transpose: W[ci][co][k]. */
+                            double wv = transpose ? w[((int64_t)ci * Cout + co) * 9 + k]
+                                                  : w[((int64_t)co * Cin + ci) * 9 + k];
+                            s += wv * Z[((size_t)b * Cin + ci) * 9 + k];
+                        }
+                    y[((int64_t)b * Cout + co) * n_pix + n] = s;
+                }
+        }
+        free(Z);
+    }
+    free(q_in);
+    return bad ? 4 : 0;
+}
+
+/* Forward op from the in-grid to the out-grid.
+ * x[B][Cin][nlat_in][nlon_in], w[Cout][Cin][9], y[B][Cout][n_pix]. */
+int oracle_forward(int nlat_in, int nlon_in, int nlat_out, int nlon_out, double theta_c,
+                   double h, int quad_kind, int B, int Cin, int Cout, const double* x,
+                   const double* w, double* y, int window, int64_t n_pix, const int64_t* pix)
+{
+    grid_t gi = {nlat_in, nlon_in}, go = {nlat_out, nlon_out};
+    return disco_sum(0, gi, go, theta_c, h, quad_kind, B, Cin, Cout, x, w, y, window, n_pix, pix);
+}
+
+/* Transposed op of the same plan, from the out-grid back to the in-grid.
+ * xT[B][CinT][nlat_out][nlon_out], w[CinT][CoutT][9], yT[B][CoutT][n_pix]
+ * with pix indexing the in-grid. */
+int oracle_transpose(int nlat_in, int nlon_in, int nlat_out, int nlon_out, double theta_c,
+                     double h, int quad_kind, int B, int CinT, int CoutT, const double* xT,
+                     const double* w, double* yT, int window, int64_t n_pix, const int64_t* pix)
+{
+    /* The transposed op reads the plan's out-grid and writes its in-grid. */
+    grid_t gi = {nlat_out, nlon_out}, go = {nlat_in, nlon_in};
+    return disco_sum(1, gi, go, theta_c, h, quad_kind, B, CinT, CoutT, xT, w, yT, window, n_pix,
+                     pix);
+}
+
+int oracle_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

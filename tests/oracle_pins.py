@@ -1,0 +1,407 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+Each ``pin_*`` function takes an ``oracle.Oracle`` and raises AssertionError
+when the oracle disagrees with an independent fact: a closed form, a library
+routine (scipy's Legendre polynomials, numpy's Gauss-Legendre rule and linear
+solver), the paper's worked node example (App. E.2), an exact invariant of the
+method, or brute force on tiny inputs.  ``test_oracle_pins.py`` runs them on
+the real oracle; ``test_oracle_mutants.py`` runs them on copies of the oracle
+with planted mistakes and requires every mistake to fail at least one pin.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+
+import numpy as np
+from scipy.special import eval_legendre
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def _xw(seed, B, Cin, nlat, nlon, Cout):
+    r = _rng(seed)
+    return r.standard_normal((B, Cin, nlat, nlon)), r.standard_normal((Cout, Cin, 9)) / 6.0
+
+
+def _select_w(nk=9):
+    """W with Cin = 1, Cout = 9 and W[k, 0, k'] = delta(k, k'): y then equals Z."""
+    w = np.zeros((nk, 1, 9))
+    for k in range(9):
+        w[k, 0, k] = 1.0
+    return w
+
+
+def _haversine_dist(th1, ph1, th2, ph2):
+    """Great-circle distance between colatitude/longitude points (haversine)."""
+    h = np.sin((th1 - th2) / 2) ** 2 + np.sin(th1) * np.sin(th2) * np.sin((ph1 - ph2) / 2) ** 2
+    return 2 * np.arcsin(np.sqrt(np.clip(h, 0.0, 1.0)))
+
+
+# --------------------------------------------------------------------------- #
+# Quadrature (Sec. 3.2 / 4.1 adopt sampling-theorem quadrature; App. A)
+# --------------------------------------------------------------------------- #
+def pin_quadrature_total(o):
+    """Weights sum to the area of the unit sphere, 4 pi."""
+    for n in (1, 2, 3, 7, 32, 64, 128, 2048):
+        for nlon in (2, 64, 4096):
+            tot = o.quadrature(n, nlon).sum() * nlon
+            assert abs(tot - 4 * math.pi) <= 1e-13 * 4 * math.pi, (n, nlon, tot)
+
+
+def pin_quadrature_legendre_exact(o):
+    """The rule integrates P_l(cos theta) exactly for l < nlat: the integral over
+    the sphere is 4 pi for l = 0 and 0 otherwise (orthogonality)."""
+    for n in (4, 7, 32, 64, 129, 512):
+        nlon = 8
+        q = o.quadrature(n, nlon)
+        x = np.cos(o.colatitudes(n))
+        for l in range(n):
+            val = nlon * float(np.dot(q, eval_legendre(l, x)))
+            expect = 4 * math.pi if l == 0 else 0.0
+            assert abs(val - expect) <= 1e-12, (n, l, val)
+
+
+def pin_quadrature_unique(o):
+    """n weights that integrate P_0..P_{n-1} exactly on n distinct nodes are
+    unique: solve that linear system with numpy and compare."""
+    for n in (5, 8, 16, 33):
+        x = np.cos(o.colatitudes(n))
+        V = np.stack([eval_legendre(l, x) for l in range(n)])
+        rhs = np.zeros(n)
+        rhs[0] = 2.0
+        w = np.linalg.solve(V, rhs)
+        nlon = 6
+        q = o.quadrature(n, nlon) * nlon / (2 * math.pi)
+        assert np.allclose(q, w, rtol=0, atol=1e-12), (n, np.abs(q - w).max())
+
+
+def pin_grid(o):
+    """Cell-centred equiangular grid: colatitude (t + 1/2) pi / nlat,
+    longitude 2 pi p / nlon."""
+    th = o.colatitudes(8)
+    assert np.allclose(th, (np.arange(8) + 0.5) * math.pi / 8, atol=1e-15)
+    ph = o.longitudes(16)
+    assert np.allclose(ph, np.arange(16) * 2 * math.pi / 16, atol=1e-15)
+
+
+# --------------------------------------------------------------------------- #
+# Geometry of R_j^{-1} w_i (Sec. 3.2, Sec. 4.1 rotated coordinates)
+# --------------------------------------------------------------------------- #
+def pin_geometry_worked_example(o):
+    """App. E.2: with the filter centred on the pole, the 9 node positions map
+    onto the square 3x3 grid {-h, 0, h}^2, and each basis function is 1 at its
+    own node and 0 at the other eight."""
+    with open(os.path.join(GOLDEN, "nodes_3x3.json")) as f:
+        g = json.load(f)
+    for L in (32, 256, 2048):
+        h = math.pi / L
+        seen = set()
+        for node in g["nodes"]:
+            th = node["theta"] * math.pi / L
+            ph = node["phi"] * math.pi
+            Th, u, v = o.frame_coords(0.0, 0.0, th, ph)
+            assert abs(Th - th) <= 1e-15, (node, Th)
+            eu, ev = node["uv"]
+            assert abs(u / h - eu) <= 1e-12 and abs(v / h - ev) <= 1e-12, (node, u / h, v / h)
+            psi = o.basis(u, v, h)
+            k = int(np.argmax(psi))
+            assert abs(psi[k] - 1.0) <= 1e-12 and np.abs(np.delete(psi, k)).max() <= 1e-12
+            seen.add(k)
+        assert seen == set(range(9))
+
+
+def pin_geometry_identity_and_meridian(o):
+    """Filter centred on the input point: Theta = 0.  Same meridian:
+    Theta = |theta_i - theta_j|, u = theta_i - theta_j (south positive), v = 0."""
+    r = _rng(1)
+    for _ in range(200):
+        thj = r.uniform(0.01, math.pi - 0.01)
+        phj = r.uniform(0, 2 * math.pi)
+        Th, u, v = o.frame_coords(thj, phj, thj, phj)
+        assert Th <= 1e-15 and abs(u) <= 1e-15 and abs(v) <= 1e-15
+        d = r.uniform(-0.05, 0.05)
+        thi = min(max(thj + d, 1e-3), math.pi - 1e-3)
+        Th, u, v = o.frame_coords(thj, phj, thi, phj)
+        assert abs(Th - abs(thi - thj)) <= 2e-15, (Th, thi - thj)
+        assert abs(u - (thi - thj)) <= 2e-15 and abs(v) <= 2e-15
+
+
+def pin_geometry_general(o):
+    """Random pairs: Theta equals the haversine great-circle distance; the
+    direction Phi = atan2(v, u) equals pi minus the initial bearing from the
+    centre to the point (bearing clockwise from north, the navigation formula),
+    i.e. Phi = 0 is south and Phi = pi/2 is east."""
+    r = _rng(2)
+    for _ in range(500):
+        thj = r.uniform(0.02, math.pi - 0.02)
+        phj = r.uniform(0, 2 * math.pi)
+        thi = thj + r.uniform(-0.3, 0.3)
+        thi = min(max(thi, 1e-3), math.pi - 1e-3)
+        phi = phj + r.uniform(-0.4, 0.4)
+        Th, u, v = o.frame_coords(thj, phj, thi, phi)
+        d = float(_haversine_dist(thi, phi, thj, phj))
+        assert abs(Th - d) <= 1e-13, (Th, d)
+        assert abs(math.hypot(u, v) - Th) <= 1e-13
+        if d < 1e-4:
+            continue
+        latj, lati = math.pi / 2 - thj, math.pi / 2 - thi
+        dl = phi - phj
+        bearing = math.atan2(math.sin(dl) * math.cos(lati),
+                             math.cos(latj) * math.sin(lati)
+                             - math.sin(latj) * math.cos(lati) * math.cos(dl))
+        Phi = math.atan2(v, u)
+        diff = (Phi - (math.pi - bearing) + math.pi) % (2 * math.pi) - math.pi
+        assert abs(diff) <= 1e-9, (Phi, bearing)
+
+
+def pin_geometry_same_ring(o):
+    """Two points on one ring: sin(Theta/2) = sin(theta) |sin(dphi/2)| and
+    v has the sign of sin(dphi) (east positive)."""
+    r = _rng(3)
+    for _ in range(200):
+        th = r.uniform(0.01, math.pi - 0.01)
+        ph = r.uniform(0, 2 * math.pi)
+        dp = r.uniform(-0.5, 0.5)
+        Th, u, v = o.frame_coords(th, ph, th, ph + dp)
+        assert abs(math.sin(Th / 2) - math.sin(th) * abs(math.sin(dp / 2))) <= 1e-15
+        if abs(dp) > 1e-6:
+            assert np.sign(v) == np.sign(math.sin(dp))
+
+
+# --------------------------------------------------------------------------- #
+# Basis (Sec. 3.4, App. E.2: bilinear interpolation on the 3x3 node grid)
+# --------------------------------------------------------------------------- #
+def pin_basis(o):
+    h = 0.0123
+    # Kronecker delta at the nodes, node k = 3a + b at ((a-1)h, (b-1)h).
+    for a in range(3):
+        for b in range(3):
+            psi = o.basis((a - 1) * h, (b - 1) * h, h)
+            e = np.zeros(9)
+            e[3 * a + b] = 1.0
+            assert np.allclose(psi, e, atol=1e-15), (a, b, psi)
+    r = _rng(4)
+    for _ in range(500):
+        u, v = r.uniform(-h, h, 2)
+        psi = o.basis(u, v, h)
+        # Partition of unity inside the node square.
+        assert abs(psi.sum() - 1.0) <= 1e-14
+        # Bilinear interpolation reproduces any bilinear function exactly.
+        c = r.standard_normal(4)
+        f = lambda uu, vv: c[0] + c[1] * uu / h + c[2] * vv / h + c[3] * uu * vv / h ** 2
+        nodes = [f((k // 3 - 1) * h, (k % 3 - 1) * h) for k in range(9)]
+        assert abs(float(np.dot(psi, nodes)) - f(u, v)) <= 1e-12
+    for _ in range(500):
+        u, v = r.uniform(-3 * h, 3 * h, 2)
+        psi = o.basis(u, v, h)
+        assert (psi >= 0).all() and (psi <= 1).all()
+        assert np.count_nonzero(psi) <= 4
+        if max(abs(u), abs(v)) >= 2 * h:
+            assert not psi.any()
+    # Linear profile along the u axis: the south node's weight at u = s h.
+    for s in (0.0, 0.25, 0.5, 1.0, 1.5, 2.0):
+        psi = o.basis(s * h, 0.0, h)
+        assert abs(psi[7] - max(0.0, 1 - abs(s - 1))) <= 1e-15
+
+
+# --------------------------------------------------------------------------- #
+# The sums (Sec. 3.2 eq. 4, Sec. 3.5 eq. 6, Sec. 4.1-4.2)
+# --------------------------------------------------------------------------- #
+_DENSE_CASES = [(8, 16, 8, 16), (16, 32, 8, 16), (12, 24, 6, 12)]
+
+
+def pin_compressed_tensor_identity(o):
+    """Sec. 4.2: Psi[t',p',t,p] = Psi[t',0,t,p - s p'] (longitude shift)."""
+    for (a, b, c, d) in _DENSE_CASES:
+        tc = 3 * math.pi / min(a, c)
+        psi = o.psi_dense(a, b, c, d, tc).reshape(c, d, a, b, 9)
+        s = b // d
+        assert np.abs(psi).max() > 0.5
+        for pp in range(d):
+            ref = np.roll(psi[:, 0], s * pp, axis=2)
+            assert np.abs(psi[:, pp] - ref).max() <= 1e-13, (a, b, c, d, pp)
+
+
+def pin_dense_vs_loop(o):
+    """The looped forward and transposed sums equal dense products
+    y = W . (Psi diag(q) x) and yT = W^T . (Psi^T diag(q_out) xT)."""
+    for (a, b, c, d) in _DENSE_CASES:
+        tc = 3 * math.pi / min(a, c)
+        psi = o.psi_dense(a, b, c, d, tc)                  # [Nout, Nin, 9]
+        qi = np.repeat(o.quadrature(a, b), b)
+        qo = np.repeat(o.quadrature(c, d), d)
+        x, w = _xw(10, 2, 3, a, b, 4)
+        Z = np.einsum("jik,bci->bckj", psi, x.reshape(2, 3, -1) * qi)
+        y_dense = np.einsum("ock,bckj->boj", w, Z).reshape(2, 4, c, d)
+        y = o.forward(a, b, c, d, tc, x, w)
+        assert np.abs(y - y_dense).max() <= 1e-13 * np.abs(y_dense).max()
+        xT, wT = _xw(11, 2, 4, c, d, 4)
+        wT = wT.reshape(4, 4, 9)[:, :3]                    # [CinT=4, CoutT=3, 9]
+        ZT = np.einsum("jik,bcj->bcki", psi, xT.reshape(2, 4, -1) * qo)
+        yT_dense = np.einsum("cok,bcki->boi", wT, ZT).reshape(2, 3, a, b)
+        yT = o.transpose(a, b, c, d, tc, xT, wT)
+        assert np.abs(yT - yT_dense).max() <= 1e-13 * np.abs(yT_dense).max()
+
+
+def pin_shift_equivariance(o):
+    """Sec. 3.3: rotations about the z axis commute with the convolution; on
+    the grid a shift by whole output pixels is exact (Sec. 4.2)."""
+    for (a, b, c, d) in [(16, 32, 16, 32), (16, 32, 8, 16)]:
+        tc = 3 * math.pi / min(a, c)
+        s = b // d
+        x, w = _xw(12, 1, 2, a, b, 3)
+        y = o.forward(a, b, c, d, tc, x, w)
+        for m in (1, 3):
+            ys = o.forward(a, b, c, d, tc, np.roll(x, s * m, axis=-1), w)
+            assert np.abs(ys - np.roll(y, m, axis=-1)).max() <= 1e-13 * np.abs(y).max()
+        xT, wT = _xw(13, 1, 3, c, d, 2)
+        wT = wT.reshape(2, 3, 9).transpose(1, 0, 2).copy()  # [CinT=3, CoutT=2, 9]
+        yT = o.transpose(a, b, c, d, tc, xT, wT)
+        ysT = o.transpose(a, b, c, d, tc, np.roll(xT, 2, axis=-1), wT)
+        assert np.abs(ysT - np.roll(yT, 2 * s, axis=-1)).max() <= 1e-13 * np.abs(yT).max()
+
+
+def pin_mirror_symmetry(o):
+    """Mirror phi -> -phi swaps east and west (node column b <-> 2 - b); the
+    flip theta -> pi - theta swaps north and south (node row a <-> 2 - a)."""
+    a, b, c, d = 16, 32, 8, 16
+    tc = 3 * math.pi / c
+    x, w = _xw(14, 1, 2, a, b, 2)
+    y = o.forward(a, b, c, d, tc, x, w)
+    perm_b = [3 * (k // 3) + (2 - k % 3) for k in range(9)]
+    perm_a = [3 * (2 - k // 3) + (k % 3) for k in range(9)]
+    xm = x[..., (-np.arange(b)) % b]
+    ym = o.forward(a, b, c, d, tc, xm, w[:, :, perm_b])
+    assert np.abs(ym - y[..., (-np.arange(d)) % d]).max() <= 1e-13 * np.abs(y).max()
+    xf = x[:, :, ::-1, :]
+    yf = o.forward(a, b, c, d, tc, xf, w[:, :, perm_a])
+    assert np.abs(yf - y[:, :, ::-1, :]).max() <= 1e-12 * np.abs(y).max()
+
+
+def pin_compact_support_and_delta(o):
+    """A delta input at pixel i0 reaches only outputs within the basis support
+    radius 2 sqrt(2) h (< theta_c); at the centre only the central node fires
+    with value q(t0), one ring north of it only the south node (u = +h)."""
+    a, b = 16, 32
+    tc = 3 * math.pi / a
+    h = tc / 3
+    q = o.quadrature(a, b)
+    th = o.colatitudes(a)
+    ph = o.longitudes(b)
+    for (t0, p0) in [(7, 5), (0, 3), (15, 30), (2, 0)]:
+        x = np.zeros((1, 1, a, b))
+        x[0, 0, t0, p0] = 1.0
+        Z = o.forward(a, b, a, b, tc, x, _select_w())[0]   # [9, a, b]
+        dist = _haversine_dist(th[:, None], ph[None, :], th[t0], ph[p0])
+        far = dist > 2 * math.sqrt(2) * h + 1e-12
+        assert not Z[:, far].any()
+        assert np.count_nonzero(Z.any(axis=0)) > 1
+        e = np.zeros(9)
+        e[4] = q[t0]
+        assert np.abs(Z[:, t0, p0] - e).max() <= 1e-15
+        if t0 > 0:
+            e = np.zeros(9)
+            e[7] = q[t0]
+            assert np.abs(Z[:, t0 - 1, p0] - e).max() <= 1e-14, Z[:, t0 - 1, p0]
+
+
+def pin_adjoint(o):
+    """Sec. 3.5 with R11: the transposed op is the adjoint of the forward op in
+    the quadrature-weighted inner products, <A x, g>_q_out = <x, B g>_q_in."""
+    for (a, b, c, d) in [(16, 32, 16, 32), (16, 32, 8, 16), (12, 24, 6, 12)]:
+        tc = 3 * math.pi / min(a, c)
+        r = _rng(15)
+        Cin, Cout = 3, 2
+        x = r.standard_normal((2, Cin, a, b))
+        g = r.standard_normal((2, Cout, c, d))
+        w = r.standard_normal((Cout, Cin, 9))
+        Ax = o.forward(a, b, c, d, tc, x, w)
+        Bg = o.transpose(a, b, c, d, tc, g, w)
+        qo = o.quadrature(c, d)[None, None, :, None]
+        qi = o.quadrature(a, b)[None, None, :, None]
+        lhs = float((Ax * g * qo).sum())
+        rhs = float((x * Bg * qi).sum())
+        assert abs(lhs - rhs) <= 1e-12 * max(abs(lhs), 1.0), (lhs, rhs)
+
+
+def filter_integrals(h, n=24):
+    """S_k = integral over the sphere of psi_k, computed in the filter frame:
+    with the azimuthal equidistant map dmu = (sin r / r) du dv, r = |(u, v)|,
+    by Gauss-Legendre on each hat cell."""
+    xg, wg = np.polynomial.legendre.leggauss(n)
+    S = np.zeros(9)
+    for a in range(3):
+        for b in range(3):
+            tot = 0.0
+            for cu in (a - 2, a - 1):
+                for cv in (b - 2, b - 1):
+                    u = (cu + (xg + 1) / 2) * h
+                    v = (cv + (xg + 1) / 2) * h
+                    U, Vv = np.meshgrid(u, v, indexing="ij")
+                    Wt = np.outer(wg, wg) * (h / 2) ** 2
+                    val = np.maximum(0, 1 - np.abs(U / h - (a - 1))) * \
+                        np.maximum(0, 1 - np.abs(Vv / h - (b - 1)))
+                    rr = np.hypot(U, Vv)
+                    tot += float((Wt * val * np.sinc(rr / math.pi)).sum())
+            S[3 * a + b] = tot
+    return S
+
+
+def pin_constant_input(o):
+    """x = 1 everywhere: each Z_k is exactly constant along an output ring
+    (shift invariance) and approximates the filter integral S_k (Sec. 3.2: the
+    only error is quadrature).  With a hat one pixel wide the sampling error
+    is O((pixel / h)^2): at fixed theta_c it must fall by at least 2.5x per
+    doubling of the grid (second order) and be below 2e-3 at 512 x 1024."""
+    tc = 3 * math.pi / 32
+    h = tc / 3
+    S = filter_integrals(h)
+    a, b = 32, 64
+    Z = o.forward(a, b, a, b, tc, np.ones((1, 1, a, b)), _select_w())[0]   # [9, a, b]
+    spread = np.abs(Z - Z[:, :, :1]).max()
+    assert spread <= 1e-14 * np.abs(Z).max(), spread
+    errs = []
+    for a in (32, 64, 128, 256, 512):
+        b = 2 * a
+        pix = np.arange(a) * b            # one pixel per ring: rings are constant
+        Zr = o.forward(a, b, a, b, tc, np.ones((1, 1, a, b)), _select_w(), pix=pix)[0]
+        errs.append(float(np.abs(Zr / S[:, None] - 1).max()))
+    assert errs[0] <= 0.15, errs
+    for e0, e1 in zip(errs, errs[1:]):
+        assert e1 * 2.5 <= e0, errs
+    assert errs[-1] <= 2e-3, errs
+
+
+def pin_window_equals_all_pairs(o):
+    """Skipping rings farther than theta_c in colatitude changes nothing (the
+    geodesic distance is at least the colatitude difference): bitwise."""
+    for (a, b, c, d) in [(32, 64, 32, 64), (32, 64, 16, 32)]:
+        tc = 3 * math.pi / min(a, c)
+        x, w = _xw(16, 1, 2, a, b, 2)
+        y_all = o.forward(a, b, c, d, tc, x, w, window=False)
+        y_win = o.forward(a, b, c, d, tc, x, w, window=True)
+        assert np.array_equal(y_all, y_win)
+        xT, wT = _xw(17, 1, 2, c, d, 2)
+        yT_all = o.transpose(a, b, c, d, tc, xT, wT, window=False)
+        yT_win = o.transpose(a, b, c, d, tc, xT, wT, window=True)
+        assert np.array_equal(yT_all, yT_win)
+
+
+def pin_pixel_subset(o):
+    """Computing a subset of output pixels gives the same values as the full run."""
+    a, b, c, d = 16, 32, 8, 16
+    tc = 3 * math.pi / c
+    x, w = _xw(18, 2, 2, a, b, 3)
+    y = o.forward(a, b, c, d, tc, x, w)
+    pix = np.array([0, 5, 17, 100, c * d - 1])
+    ys = o.forward(a, b, c, d, tc, x, w, pix=pix)
+    assert np.array_equal(ys, y.reshape(2, 3, -1)[:, :, pix])
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -1,0 +1,68 @@
+"""Planted mistakes in a copy of the oracle must each fail at least one pin.
+
+Every mutant is a textual edit of ``oracle/disco_oracle.c`` compiled on the
+CPU into a temporary library; the real oracle is untouched.  The mistakes are
+the plausible ones: a wrong sign, a dropped term, a transposed operand, a
+wrong index or constant.
+"""
+import pytest
+
+import oracle
+import oracle_pins
+
+MUTANTS = {
+    "v_sign": ("*v = th * yr / rho;", "*v = -th * yr / rho;"),
+    "u_sign": ("*u = th * xr / rho;", "*u = -th * xr / rho;"),
+    "rotation_y_sign": ("mat_y(-theta, my);", "mat_y(theta, my);"),
+    "rotation_order": ("mat_mul(my, mz, m);", "mat_mul(mz, my, m);"),
+    "fejer_denominator": ("(4.0 * (double)m * (double)m - 1.0)",
+                          "(4.0 * (double)m * (double)m + 1.0)"),
+    "fejer_last_term": ("m <= nlat / 2;", "m < nlat / 2;"),
+    "colatitude_scale": ("(t + 0.5) * M_PI / (double)nlat", "(t + 0.5) * M_PI / (double)(nlat + 1)"),
+    "longitude_direction": ("2.0 * M_PI * (double)p / (double)nlon",
+                            "-2.0 * M_PI * (double)p / (double)nlon"),
+    "drop_quadrature": ("zc[k] += val[k] * qw * xv;", "zc[k] += val[k] * xv;"),
+    "transpose_drops_quadrature": ("double qw = q_in[t];", "double qw = transpose ? 1.0 : q_in[t];"),
+    "forward_w_transposed": (": w[((int64_t)co * Cin + ci) * 9 + k];",
+                             ": w[((int64_t)ci * Cout + co) * 9 + k];"),
+    "transpose_w_not_transposed": ("double wv = transpose ? w[((int64_t)ci * Cout + co) * 9 + k]",
+                                   "double wv = transpose ? w[((int64_t)co * Cin + ci) * 9 + k]"),
+    "basis_index_order": ("psi[3 * a + b] = hat", "psi[3 * b + a] = hat"),
+    "hat_shape": ("return a < 1.0 ? 1.0 - a : 0.0;", "return a < 1.0 ? 1.0 - a * a : 0.0;"),
+    "cutoff_too_small": ("if (Th > theta_c) return 0;", "if (Th > 0.5 * theta_c) return 0;"),
+    "window_too_narrow": ("if (window && fabs(th_i - th_o) > theta_c) continue;",
+                          "if (window && fabs(th_i - th_o) > 0.5 * theta_c) continue;"),
+    "transpose_centre_swapped": ("nz = filter_values(m_i, e_o, theta_c, h, val);",
+                                 "nz = filter_values(m_o, e_i_t, theta_c, h, val);"),
+    "basis_drops_corner": ("psi[3 * a + b] = hat(u / h - (a - 1)) * hat(v / h - (b - 1));",
+                           "psi[3 * a + b] = (a != 1 && b != 1) ? 0.0 : "
+                           "hat(u / h - (a - 1)) * hat(v / h - (b - 1));"),
+}
+
+
+def _mutant_source(name):
+    with open(oracle.SOURCE) as f:
+        src = f.read()
+    old, new = MUTANTS[name]
+    assert src.count(old) == 1, (name, src.count(old))
+    src = src.replace(old, new)
+    if name == "transpose_centre_swapped":
+        # Evaluate the transposed op's filter centred at the output point.
+        src = src.replace("double m_i[9];", "double m_i[9], e_i_t[3]; unit_vector(th_i, ph_i, e_i_t);")
+    return src
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    src = tmp_path / "mutant.c"
+    src.write_text(_mutant_source(name))
+    lib = oracle.build(out=str(tmp_path / ("lib_%s.so" % name)), source=str(src))
+    o = oracle.Oracle(lib)
+    failed = []
+    for pin in oracle_pins.ALL_PINS:
+        try:
+            pin(o)
+        except AssertionError:
+            failed.append(pin.__name__)
+            break
+    assert failed, "mutant %s passed every pin" % name
