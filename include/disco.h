@@ -1,0 +1,190 @@
+/*
+ * disco.h -- C ABI of libdisco.so: DISCO spherical convolution on one
+ * MI355X (gfx950) GPU.
+ *
+ * The operation is the DISCO spherical convolution of Ocampo, Price & McEwen,
+ * "Scalable and Equivariant Spherical CNNs by Discrete-Continuous (DISCO)
+ * Convolutions" (ICLR 2023), restricted to rotations R = Z(phi) Y(theta) in
+ * SO(3)/SO(2) (Sec. 3.2), written as a sparse-dense product (Sec. 4.1):
+ *
+ *   forward    y[b,co,j] = sum_{ci,k} W[co,ci,k] sum_i psi_k(R_j^{-1} w_i) q_in(i) x[b,ci,i]
+ *   transpose  y[b,c,i]  = sum_{c',k} W[c',c,k] sum_j psi_k(R_j^{-1} w_i) q_out(j) x[b,c',j]
+ *              (Sec. 3.5, eq. 6: the filter is centred at the transposed
+ *               op's input points and weighted by their quadrature)
+ *
+ * Grids are equiangular and cell-centred: colatitude (t + 1/2) pi / nlat,
+ * longitude 2 pi p / nlon, longitude fastest in memory.  A plan fixes one
+ * (in-grid, out-grid) pair: the forward op maps in -> out, the transposed op
+ * maps out -> in with the same filter pairs.  The longitude compression of
+ * Sec. 4.2 (one psi pattern per output latitude ring, reused at every output
+ * longitude by a cyclic shift) requires nlon_in / nlon_out or nlon_out /
+ * nlon_in to be an integer.
+ *
+ * Basis: the 3x3 node grid of App. E.2, projected onto the sphere with the
+ * azimuthal equidistant map (edge nodes at geodesic distance h, corner nodes
+ * at sqrt(2) h), bilinear interpolation between nodes (Sec. 3.4), node index
+ * k = 3a + b with a along increasing colatitude (south) and b along
+ * increasing longitude (east); the filter is zero beyond theta_c.
+ *
+ * Conventions for every call:
+ *   - every call returns a disco_status_t; on failure nothing is enqueued on
+ *     the stream and no output is written; disco_last_error() then holds a
+ *     human-readable reason (thread-local, valid until the next call on the
+ *     same thread);
+ *   - tensors are dense, contiguous, row-major, on the device that created the
+ *     plan; x, w and y must share one dtype (fp32, or bf16 storage with fp32
+ *     accumulation); y must not overlap x or w and is fully overwritten;
+ *   - the caller owns x, w and y and keeps them alive until the work enqueued
+ *     on `stream` has completed; execution errors surface at the caller's next
+ *     synchronisation, as usual in HIP;
+ *   - a plan is immutable after creation and may be used from several host
+ *     threads and streams at once.
+ */
+#ifndef DISCO_H
+#define DISCO_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct disco_plan* disco_plan_t; /* opaque; owns the device psi tensors */
+
+typedef enum {
+    DISCO_OK = 0,
+    DISCO_ERR_INVALID_ARGUMENT = 1, /* bad sizes, cutoff, null pointer, overlap */
+    DISCO_ERR_UNSUPPORTED = 2,      /* valid but not implemented (longitude ratio, basis) */
+    DISCO_ERR_SHAPE = 3,            /* tensor rank or shape does not match the plan */
+    DISCO_ERR_DTYPE = 4,            /* mixed or unknown dtypes */
+    DISCO_ERR_OUT_OF_MEMORY = 5,    /* device or host allocation failed */
+    DISCO_ERR_DEVICE = 6            /* HIP runtime error, or tensor on another device */
+} disco_status_t;
+
+typedef enum { DISCO_FLOAT32 = 0, DISCO_BFLOAT16 = 1 } disco_dtype_t;
+
+enum { DISCO_BASIS_BILINEAR_3X3 = 0 };               /* K = 9 (App. E.2) */
+enum { DISCO_QUAD_FEJER1 = 0, DISCO_QUAD_CELL_AREA = 1 };
+
+/* Execution variants.  AUTO picks the fastest path for the plan and shapes;
+ * the others force one path (all give the same result up to fp32 rounding). */
+typedef enum {
+    DISCO_ALGO_AUTO = 0,
+    DISCO_ALGO_GATHER_THEN_CONTRACT = 1, /* psi gather -> Z workspace -> W contraction */
+    DISCO_ALGO_CONTRACT_THEN_GATHER = 2, /* W contraction on the input grid -> psi gather */
+    DISCO_ALGO_FUSED = 3                 /* gather and contraction in one kernel, no workspace */
+} disco_algo_t;
+
+typedef struct {
+    int32_t kind;        /* DISCO_BASIS_BILINEAR_3X3 */
+    int32_t quadrature;  /* DISCO_QUAD_FEJER1 (default) or DISCO_QUAD_CELL_AREA */
+    double node_spacing; /* h in radians; 0 selects theta_c / 3 */
+} disco_basis_t;
+
+typedef struct {
+    void* data;       /* device pointer (may be NULL only when the tensor is empty) */
+    int32_t dtype;    /* disco_dtype_t */
+    int32_t ndim;     /* x, y: 4 ([B, C, nlat, nlon]); w: 3 ([C0, C1, 9]) */
+    int64_t shape[4];
+} disco_tensor_t;
+
+typedef struct {
+    int32_t K;                 /* basis size (9) */
+    int32_t nlat_in, nlon_in, nlat_out, nlon_out;
+    int32_t phases_forward;    /* longitude phases of the forward op's patterns */
+    int32_t phases_transpose;  /* ... and of the transposed op's */
+    int32_t max_window;        /* widest stored longitude window, in input pixels */
+    int32_t full_ring_windows; /* (pattern, input ring) pairs whose window is a whole ring */
+    int64_t nnz_entries;       /* stored (pattern, input pixel) entries, forward op */
+    int64_t nnz_entries_transpose;
+    int64_t nnz_pairs_total;   /* non-zero (output pixel, input pixel, k) triples, forward */
+    int64_t psi_bytes;         /* device bytes held by the plan */
+    double h;                  /* node spacing actually used */
+} disco_plan_info_t;
+
+/* Builds the sparse psi tensors of the forward and transposed ops on the host
+ * in fp64 (per output ring: neighbour search over input rings within theta_c,
+ * closed-form longitude window, rotation, basis, quadrature; Sec. 4.1 and
+ * 4.2), rounds them to fp32 and uploads them to the current device.
+ *   nlat_* >= 1, nlon_* >= 2, 0 < theta_c <= pi; basis may be NULL (defaults).
+ * Errors: INVALID_ARGUMENT (sizes, cutoff, negative node spacing, NULL
+ * plan_out), UNSUPPORTED (longitude ratio not an integer, unknown basis or
+ * quadrature), OUT_OF_MEMORY, DEVICE.  On success *plan_out owns the device
+ * memory until disco_plan_destroy. */
+disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlon_out,
+                                 double theta_c, const disco_basis_t* basis,
+                                 disco_plan_t* plan_out);
+
+/* Frees the plan and its device memory (NULL is accepted).  The caller
+ * must ensure no enqueued work still uses the plan. */
+disco_status_t disco_plan_destroy(disco_plan_t plan);
+
+/* Fills *info with the plan's sizes and counts (App. B counts the non-zeros
+ * of Psi as the memory figure). */
+disco_status_t disco_plan_query(disco_plan_t plan, disco_plan_info_t* info);
+
+/* Forward op (Sec. 3.2 eq. 4 on SO(3)/SO(2), Sec. 4.2 compressed product):
+ *   x [B, Cin, nlat_in, nlon_in], w [Cout, Cin, 9], y [B, Cout, nlat_out, nlon_out].
+ * B may be 0 (nothing is enqueued).  Errors: INVALID_ARGUMENT, SHAPE, DTYPE,
+ * OUT_OF_MEMORY (workspace), DEVICE. */
+disco_status_t disco_forward(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                             disco_tensor_t* y, hipStream_t stream);
+
+/* Transposed op (Sec. 3.5 eq. 6), used for upsampling:
+ *   x [B, CinT, nlat_out, nlon_out], w [CinT, CoutT, 9] (the same buffer as
+ *   the forward op's W of the adjoint pair), y [B, CoutT, nlat_in, nlon_in].
+ * With quadrature-weighted inner products it is the adjoint of the forward
+ * op.  Errors as disco_forward. */
+disco_status_t disco_transpose(disco_plan_t plan, const disco_tensor_t* x,
+                               const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream);
+
+/* disco_forward / disco_transpose with an explicit execution variant
+ * (disco_algo_t).  Same arguments, errors and results. */
+disco_status_t disco_forward_algo(disco_plan_t plan, const disco_tensor_t* x,
+                                  const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream,
+                                  int32_t algo);
+disco_status_t disco_transpose_algo(disco_plan_t plan, const disco_tensor_t* x,
+                                    const disco_tensor_t* w, disco_tensor_t* y,
+                                    hipStream_t stream, int32_t algo);
+
+/* Host-only export of the stored psi entries of one op, without any device
+ * (Sec. 4.1: Psi is constructed explicitly, only where it is non-zero).
+ * transpose = 0 selects the forward op, 1 the transposed op.  Each entry is
+ * (output ring, phase, input ring, longitude offset d, 9 values); an output
+ * pixel p_out = P * q + phase reads input pixel (stride * q + d) mod nlon of
+ * the op's input grid, with P = phases and stride = nlon_in_op * P /
+ * nlon_out_op.  Values are psi_k times the quadrature weight of the op's
+ * input ring, rounded to fp32.  If capacity < *count the arrays are left
+ * untouched and only *count, *phases and *stride are written (call with
+ * capacity 0 to size the buffers).  Errors as disco_plan_create except
+ * DEVICE, which cannot occur. */
+disco_status_t disco_psi_entries(int nlat_in, int nlon_in, int nlat_out, int nlon_out,
+                                 double theta_c, const disco_basis_t* basis, int32_t transpose,
+                                 int64_t capacity, int32_t* out_ring, int32_t* phase,
+                                 int32_t* in_ring, int32_t* offset, float* values,
+                                 int64_t* count, int32_t* phases, int32_t* stride);
+
+/* Kernel timing for measurement tools.  While enabled (on != 0), every
+ * kernel the library launches from this process is bracketed by HIP events
+ * recorded on the call's stream; disco_kernel_timing_read waits for the
+ * recorded events, returns per-kernel totals (kernel name, launches,
+ * milliseconds) for up to `capacity` kernels, writes the number of distinct
+ * kernels to *count and clears the record.  names receives capacity rows of
+ * 64 chars.  Enabling adds two event records per launch; disable it for
+ * production use.  Errors: INVALID_ARGUMENT (NULL count), DEVICE. */
+disco_status_t disco_kernel_timing_enable(int32_t on);
+disco_status_t disco_kernel_timing_read(int32_t capacity, char* names, int64_t* launches,
+                                        double* total_ms, int32_t* count);
+
+/* Static text for a status code (never NULL). */
+const char* disco_status_string(disco_status_t status);
+
+/* Detail of the last failed call on this thread ("" if none). */
+const char* disco_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DISCO_H */

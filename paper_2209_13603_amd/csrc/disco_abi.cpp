@@ -1,0 +1,427 @@
+// disco_abi.cpp -- the C ABI of libdisco.so (declared in include/disco.h):
+// argument validation, plan construction and upload, workspace management
+// and dispatch to the kernels.  Validation is synchronous and happens before
+// anything is enqueued; a failed call enqueues nothing.
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <new>
+#include <string>
+
+#include "disco.h"
+#include "disco_internal.h"
+
+using namespace disco;
+
+struct disco_plan {
+    int device = 0;
+    PlanParams params{};
+    disco_plan_info_t info{};
+    DeviceOp fwd, tr;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+disco_status_t fail(disco_status_t s, const std::string& msg) {
+    g_last_error = msg;
+    return s;
+}
+
+disco_status_t ok() {
+    g_last_error.clear();
+    return DISCO_OK;
+}
+
+bool fault_inject_alloc() {
+    const char* v = std::getenv("DISCO_FAULT_INJECT");
+    return v && std::strcmp(v, "alloc") == 0;
+}
+
+disco_status_t hip_fail(hipError_t e, const char* what) {
+    if (e == hipErrorOutOfMemory) return fail(DISCO_ERR_OUT_OF_MEMORY, std::string(what) + ": " + hipGetErrorString(e));
+    return fail(DISCO_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+disco_status_t resolve_params(int nlat_in, int nlon_in, int nlat_out, int nlon_out, double theta_c,
+                              const disco_basis_t* basis, PlanParams* p) {
+    if (nlat_in < 1 || nlat_out < 1 || nlon_in < 2 || nlon_out < 2)
+        return fail(DISCO_ERR_INVALID_ARGUMENT, "grid sizes need nlat >= 1 and nlon >= 2");
+    if ((int64_t)nlat_in * nlon_in > (1LL << 30) || (int64_t)nlat_out * nlon_out > (1LL << 30))
+        return fail(DISCO_ERR_INVALID_ARGUMENT, "grid larger than 2^30 pixels");
+    if (!(theta_c > 0.0) || !(theta_c <= 3.14159265358979323846) || !std::isfinite(theta_c))
+        return fail(DISCO_ERR_INVALID_ARGUMENT, "theta_c must lie in (0, pi]");
+    disco_basis_t b{DISCO_BASIS_BILINEAR_3X3, DISCO_QUAD_FEJER1, 0.0};
+    if (basis) b = *basis;
+    if (b.kind != DISCO_BASIS_BILINEAR_3X3) return fail(DISCO_ERR_UNSUPPORTED, "unknown basis kind");
+    if (b.quadrature != DISCO_QUAD_FEJER1 && b.quadrature != DISCO_QUAD_CELL_AREA)
+        return fail(DISCO_ERR_UNSUPPORTED, "unknown quadrature");
+    if (!(b.node_spacing >= 0.0) || !std::isfinite(b.node_spacing))
+        return fail(DISCO_ERR_INVALID_ARGUMENT, "node_spacing must be >= 0");
+    if (nlon_in % nlon_out != 0 && nlon_out % nlon_in != 0)
+        return fail(DISCO_ERR_UNSUPPORTED, "nlon_in / nlon_out or nlon_out / nlon_in must be an integer");
+    p->nlat_in = nlat_in; p->nlon_in = nlon_in; p->nlat_out = nlat_out; p->nlon_out = nlon_out;
+    p->theta_c = theta_c;
+    p->h = b.node_spacing > 0.0 ? b.node_spacing : theta_c / 3.0;
+    p->quadrature = b.quadrature;
+    return DISCO_OK;
+}
+
+disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
+    d->g = h.g;
+    d->n_entries = (int64_t)h.t_in.size();
+    d->nnz_pairs = h.nnz_pairs;
+    std::vector<DevEntry> ent((size_t)d->n_entries);
+    for (int64_t e = 0; e < d->n_entries; ++e) {
+        DevEntry& E = ent[(size_t)e];
+        E.row = h.t_in[(size_t)e] * h.g.nlon_i;
+        E.d = h.d[(size_t)e];
+        for (int k = 0; k < kBasis; ++k) E.v[k] = h.val[(size_t)e * kBasis + k];
+        E.pad = 0;
+    }
+    const size_t pb = sizeof(int32_t) * h.pat_ptr.size();
+    const size_t eb = sizeof(DevEntry) * std::max<size_t>(ent.size(), 1);
+    if (fault_inject_alloc()) return fail(DISCO_ERR_OUT_OF_MEMORY, "allocation failure injected (DISCO_FAULT_INJECT=alloc)");
+    hipError_t e = hipMalloc((void**)&d->pat_ptr, pb);
+    if (e != hipSuccess) { d->pat_ptr = nullptr; return hip_fail(e, "hipMalloc(pattern table)"); }
+    e = hipMalloc((void**)&d->entries, eb);
+    if (e != hipSuccess) { d->entries = nullptr; return hip_fail(e, "hipMalloc(psi entries)"); }
+    e = hipMemcpy(d->pat_ptr, h.pat_ptr.data(), pb, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy(pattern table)");
+    if (!ent.empty()) {
+        e = hipMemcpy(d->entries, ent.data(), sizeof(DevEntry) * ent.size(), hipMemcpyHostToDevice);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpy(psi entries)");
+    }
+    d->bytes = (int64_t)(pb + eb);
+    return DISCO_OK;
+}
+
+void free_op(DeviceOp* d) {
+    if (d->pat_ptr) (void)hipFree(d->pat_ptr);
+    if (d->entries) (void)hipFree(d->entries);
+    d->pat_ptr = nullptr;
+    d->entries = nullptr;
+}
+
+int64_t numel(const disco_tensor_t* t) {
+    int64_t n = 1;
+    for (int i = 0; i < t->ndim; ++i) n *= t->shape[i];
+    return n;
+}
+
+size_t elem_bytes(int dtype) { return dtype == DISCO_BFLOAT16 ? 2 : 4; }
+
+bool overlaps(const disco_tensor_t* a, const disco_tensor_t* b) {
+    const uintptr_t a0 = (uintptr_t)a->data, a1 = a0 + (uintptr_t)numel(a) * elem_bytes(a->dtype);
+    const uintptr_t b0 = (uintptr_t)b->data, b1 = b0 + (uintptr_t)numel(b) * elem_bytes(b->dtype);
+    return a0 < b1 && b0 < a1 && a1 > a0 && b1 > b0;
+}
+
+disco_status_t check_device_ptr(const void* p, int device, const char* name) {
+    hipPointerAttribute_t attr;
+    std::memset(&attr, 0, sizeof(attr));
+    hipError_t e = hipPointerGetAttributes(&attr, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(DISCO_ERR_DEVICE, std::string(name) + " is not a device pointer known to HIP");
+    }
+    if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged)
+        return fail(DISCO_ERR_DEVICE, std::string(name) + " is not device memory");
+    if (attr.device != device)
+        return fail(DISCO_ERR_DEVICE, std::string(name) + " lives on device " + std::to_string(attr.device) +
+                                          ", the plan on device " + std::to_string(device));
+    return DISCO_OK;
+}
+
+// Shared entry of forward and transpose.
+disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                   disco_tensor_t* y, hipStream_t stream, int32_t algo, bool transpose) {
+    if (!plan) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (!x || !w || !y) return fail(DISCO_ERR_INVALID_ARGUMENT, "tensor descriptor is NULL");
+    if (algo < DISCO_ALGO_AUTO || algo > DISCO_ALGO_FUSED) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown algo");
+    const DeviceOp& op = transpose ? plan->tr : plan->fwd;
+    const OpGeom& g = op.g;
+    if (x->ndim != 4 || y->ndim != 4 || w->ndim != 3)
+        return fail(DISCO_ERR_SHAPE, "x and y must be 4-D [B, C, nlat, nlon], w 3-D");
+    for (int i = 0; i < 4; ++i)
+        if (x->shape[i] < 0 || y->shape[i] < 0 || (i < 3 && w->shape[i] < 0))
+            return fail(DISCO_ERR_SHAPE, "negative extent");
+    const int64_t B = x->shape[0], Ci = x->shape[1], Co = y->shape[1];
+    if (x->shape[2] != g.nlat_i || x->shape[3] != g.nlon_i)
+        return fail(DISCO_ERR_SHAPE, "x grid must be [" + std::to_string(g.nlat_i) + ", " + std::to_string(g.nlon_i) + "]");
+    if (y->shape[2] != g.nlat_o || y->shape[3] != g.nlon_o)
+        return fail(DISCO_ERR_SHAPE, "y grid must be [" + std::to_string(g.nlat_o) + ", " + std::to_string(g.nlon_o) + "]");
+    if (y->shape[0] != B) return fail(DISCO_ERR_SHAPE, "x and y batch differ");
+    if (w->shape[2] != kBasis) return fail(DISCO_ERR_SHAPE, "w last extent must be 9");
+    if (!transpose && (w->shape[0] != Co || w->shape[1] != Ci))
+        return fail(DISCO_ERR_SHAPE, "forward w must be [Cout, Cin, 9]");
+    if (transpose && (w->shape[0] != Ci || w->shape[1] != Co))
+        return fail(DISCO_ERR_SHAPE, "transpose w must be [CinT, CoutT, 9]");
+    if (Ci < 1 || Co < 1) return fail(DISCO_ERR_SHAPE, "channel counts must be >= 1");
+    if (B > 65535 || Ci > 4096 || Co > 4096) return fail(DISCO_ERR_SHAPE, "batch or channels too large");
+    if (x->dtype != y->dtype || w->dtype != x->dtype)
+        return fail(DISCO_ERR_DTYPE, "x, w and y must share one dtype");
+    if (x->dtype != DISCO_FLOAT32 && x->dtype != DISCO_BFLOAT16)
+        return fail(DISCO_ERR_DTYPE, "dtype must be DISCO_FLOAT32 or DISCO_BFLOAT16");
+    if (B == 0) return ok();
+    if (!x->data || !w->data || !y->data) return fail(DISCO_ERR_INVALID_ARGUMENT, "NULL data pointer");
+    if (overlaps(y, x) || overlaps(y, w)) return fail(DISCO_ERR_INVALID_ARGUMENT, "y overlaps x or w");
+    // Index arithmetic inside the kernels keeps per-plane offsets in 64 bits;
+    // the grid itself is bounded by 2^30 pixels at plan creation.
+    disco_status_t s;
+    if ((s = check_device_ptr(x->data, plan->device, "x")) != DISCO_OK) return s;
+    if ((s = check_device_ptr(w->data, plan->device, "w")) != DISCO_OK) return s;
+    if ((s = check_device_ptr(y->data, plan->device, "y")) != DISCO_OK) return s;
+
+    ExecArgs a{};
+    a.op = &op; a.x = x->data; a.w = w->data; a.y = y->data; a.dtype = x->dtype;
+    a.B = (int)B; a.Ci = (int)Ci; a.Co = (int)Co; a.w_trans = transpose; a.stream = stream;
+
+    if (algo == DISCO_ALGO_AUTO || algo == DISCO_ALGO_FUSED) {
+        // Channel mixing goes to the grid with fewer (pixels x channels) of
+        // intermediate planes.
+        const double gtc = (double)Ci * g.nlat_o * g.nlon_o;
+        const double ctg = (double)Co * g.nlat_i * g.nlon_i;
+        algo = ctg < gtc ? DISCO_ALGO_CONTRACT_THEN_GATHER : DISCO_ALGO_GATHER_THEN_CONTRACT;
+    }
+    const size_t ws = algo == DISCO_ALGO_CONTRACT_THEN_GATHER ? workspace_bytes_contract_then_gather(a)
+                                                              : workspace_bytes_gather_then_contract(a);
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return fail(DISCO_ERR_DEVICE, "hipGetDevice failed");
+    if (cur != plan->device && hipSetDevice(plan->device) != hipSuccess)
+        return fail(DISCO_ERR_DEVICE, "hipSetDevice failed");
+    struct Restore { int d; bool on; ~Restore() { if (on) (void)hipSetDevice(d); } } restore{cur, cur != plan->device};
+
+    if (fault_inject_alloc()) return fail(DISCO_ERR_OUT_OF_MEMORY, "allocation failure injected (DISCO_FAULT_INJECT=alloc)");
+    float* ws_ptr = nullptr;
+    hipError_t e = hipMallocAsync((void**)&ws_ptr, std::max<size_t>(ws, 256), stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(workspace)");
+    e = algo == DISCO_ALGO_CONTRACT_THEN_GATHER ? launch_contract_then_gather(a, ws_ptr)
+                                                : launch_gather_then_contract(a, ws_ptr);
+    hipError_t e2 = hipFreeAsync(ws_ptr, stream);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    if (e2 != hipSuccess) return hip_fail(e2, "hipFreeAsync(workspace)");
+    return ok();
+}
+
+// ---- kernel timing (measurement tools only) --------------------------------
+struct TimedLaunch {
+    std::string name;
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+std::atomic<bool> g_timing_on{false};
+std::mutex g_timing_mu;
+std::vector<TimedLaunch> g_timed;
+
+}  // namespace
+
+namespace disco {
+
+int timing_begin(const char* name, hipStream_t s) {
+    if (!g_timing_on.load(std::memory_order_relaxed)) return -1;
+    TimedLaunch t;
+    t.name = name;
+    if (hipEventCreate(&t.start) != hipSuccess || hipEventCreate(&t.stop) != hipSuccess) return -1;
+    (void)hipEventRecord(t.start, s);
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    g_timed.push_back(t);
+    return (int)g_timed.size() - 1;
+}
+
+void timing_end(int token, hipStream_t s) {
+    if (token < 0) return;
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    if (token < (int)g_timed.size()) (void)hipEventRecord(g_timed[(size_t)token].stop, s);
+}
+
+}  // namespace disco
+
+extern "C" {
+
+disco_status_t disco_kernel_timing_enable(int32_t on) {
+    g_timing_on.store(on != 0);
+    return ok();
+}
+
+disco_status_t disco_kernel_timing_read(int32_t capacity, char* names, int64_t* launches,
+                                        double* total_ms, int32_t* count) {
+    if (!count) return fail(DISCO_ERR_INVALID_ARGUMENT, "count is NULL");
+    std::vector<TimedLaunch> rec;
+    {
+        std::lock_guard<std::mutex> lk(g_timing_mu);
+        rec.swap(g_timed);
+    }
+    std::map<std::string, std::pair<int64_t, double>> agg;
+    std::vector<std::string> order;
+    disco_status_t st = DISCO_OK;
+    for (auto& t : rec) {
+        float ms = 0.0f;
+        if (hipEventSynchronize(t.stop) != hipSuccess || hipEventElapsedTime(&ms, t.start, t.stop) != hipSuccess)
+            st = DISCO_ERR_DEVICE;
+        if (!agg.count(t.name)) order.push_back(t.name);
+        auto& a = agg[t.name];
+        a.first += 1;
+        a.second += ms;
+        (void)hipEventDestroy(t.start);
+        (void)hipEventDestroy(t.stop);
+    }
+    *count = (int32_t)order.size();
+    for (int32_t i = 0; i < capacity && i < (int32_t)order.size(); ++i) {
+        if (names) {
+            std::strncpy(names + 64 * (size_t)i, order[(size_t)i].c_str(), 63);
+            names[64 * (size_t)i + 63] = 0;
+        }
+        if (launches) launches[i] = agg[order[(size_t)i]].first;
+        if (total_ms) total_ms[i] = agg[order[(size_t)i]].second;
+    }
+    if (st != DISCO_OK) return fail(st, "event timing failed");
+    return ok();
+}
+
+disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlon_out, double theta_c,
+                                 const disco_basis_t* basis, disco_plan_t* plan_out) {
+    if (!plan_out) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan_out is NULL");
+    *plan_out = nullptr;
+    PlanParams p{};
+    disco_status_t s = resolve_params(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, basis, &p);
+    if (s != DISCO_OK) return s;
+    HostOp hf, ht;
+    std::string err;
+    try {
+        int rc = build_host_op(p, false, &hf, &err);
+        if (rc == DISCO_OK) rc = build_host_op(p, true, &ht, &err);
+        if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
+    } catch (const std::bad_alloc&) {
+        return fail(DISCO_ERR_OUT_OF_MEMORY, "host allocation failed while building psi");
+    }
+    disco_plan* plan = new (std::nothrow) disco_plan();
+    if (!plan) return fail(DISCO_ERR_OUT_OF_MEMORY, "host allocation failed");
+    if (hipGetDevice(&plan->device) != hipSuccess) {
+        (void)hipGetLastError();
+        delete plan;
+        return fail(DISCO_ERR_DEVICE, "no HIP device available");
+    }
+    plan->params = p;
+    if ((s = upload_op(hf, &plan->fwd)) != DISCO_OK || (s = upload_op(ht, &plan->tr)) != DISCO_OK) {
+        free_op(&plan->fwd);
+        free_op(&plan->tr);
+        delete plan;
+        return s;
+    }
+    // Keep freed workspace in the device's pool rather than returning it to
+    // the driver at every synchronisation.
+    hipMemPool_t pool;
+    if (hipDeviceGetDefaultMemPool(&pool, plan->device) == hipSuccess) {
+        uint64_t thr = UINT64_MAX;
+        (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+    }
+    (void)hipGetLastError();
+    disco_plan_info_t& I = plan->info;
+    I.K = kBasis;
+    I.nlat_in = nlat_in; I.nlon_in = nlon_in; I.nlat_out = nlat_out; I.nlon_out = nlon_out;
+    I.phases_forward = hf.g.P;
+    I.phases_transpose = ht.g.P;
+    I.max_window = std::max(hf.max_window, ht.max_window);
+    I.full_ring_windows = hf.full_ring_windows;
+    I.nnz_entries = (int64_t)hf.t_in.size();
+    I.nnz_entries_transpose = (int64_t)ht.t_in.size();
+    I.nnz_pairs_total = hf.nnz_pairs;
+    I.psi_bytes = plan->fwd.bytes + plan->tr.bytes;
+    I.h = p.h;
+    *plan_out = plan;
+    return ok();
+}
+
+disco_status_t disco_plan_destroy(disco_plan_t plan) {
+    if (!plan) return ok();
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    if (cur != plan->device) (void)hipSetDevice(plan->device);
+    free_op(&plan->fwd);
+    free_op(&plan->tr);
+    if (cur != plan->device) (void)hipSetDevice(cur);
+    delete plan;
+    return ok();
+}
+
+disco_status_t disco_plan_query(disco_plan_t plan, disco_plan_info_t* info) {
+    if (!plan || !info) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan or info is NULL");
+    *info = plan->info;
+    return ok();
+}
+
+disco_status_t disco_forward(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                             disco_tensor_t* y, hipStream_t stream) {
+    return run(plan, x, w, y, stream, DISCO_ALGO_AUTO, false);
+}
+
+disco_status_t disco_transpose(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                               disco_tensor_t* y, hipStream_t stream) {
+    return run(plan, x, w, y, stream, DISCO_ALGO_AUTO, true);
+}
+
+disco_status_t disco_forward_algo(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                                  disco_tensor_t* y, hipStream_t stream, int32_t algo) {
+    return run(plan, x, w, y, stream, algo, false);
+}
+
+disco_status_t disco_transpose_algo(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                                    disco_tensor_t* y, hipStream_t stream, int32_t algo) {
+    return run(plan, x, w, y, stream, algo, true);
+}
+
+disco_status_t disco_psi_entries(int nlat_in, int nlon_in, int nlat_out, int nlon_out, double theta_c,
+                                 const disco_basis_t* basis, int32_t transpose, int64_t capacity,
+                                 int32_t* out_ring, int32_t* phase, int32_t* in_ring, int32_t* offset,
+                                 float* values, int64_t* count, int32_t* phases, int32_t* stride) {
+    if (!count) return fail(DISCO_ERR_INVALID_ARGUMENT, "count is NULL");
+    PlanParams p{};
+    disco_status_t s = resolve_params(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, basis, &p);
+    if (s != DISCO_OK) return s;
+    HostOp op;
+    std::string err;
+    try {
+        int rc = build_host_op(p, transpose != 0, &op, &err);
+        if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
+    } catch (const std::bad_alloc&) {
+        return fail(DISCO_ERR_OUT_OF_MEMORY, "host allocation failed while building psi");
+    }
+    const int64_t n = (int64_t)op.t_in.size();
+    *count = n;
+    if (phases) *phases = op.g.P;
+    if (stride) *stride = op.g.stride;
+    if (capacity < n) return ok();
+    if (!out_ring || !phase || !in_ring || !offset || !values)
+        return fail(DISCO_ERR_INVALID_ARGUMENT, "output array is NULL");
+    for (int pat = 0; pat < op.g.n_patterns(); ++pat)
+        for (int32_t e = op.pat_ptr[(size_t)pat]; e < op.pat_ptr[(size_t)pat + 1]; ++e) {
+            out_ring[e] = pat / op.g.P;
+            phase[e] = pat % op.g.P;
+            in_ring[e] = op.t_in[(size_t)e];
+            offset[e] = op.d[(size_t)e];
+            std::memcpy(values + (size_t)e * kBasis, &op.val[(size_t)e * kBasis], sizeof(float) * kBasis);
+        }
+    return ok();
+}
+
+const char* disco_status_string(disco_status_t status) {
+    switch (status) {
+        case DISCO_OK: return "DISCO_OK";
+        case DISCO_ERR_INVALID_ARGUMENT: return "DISCO_ERR_INVALID_ARGUMENT";
+        case DISCO_ERR_UNSUPPORTED: return "DISCO_ERR_UNSUPPORTED";
+        case DISCO_ERR_SHAPE: return "DISCO_ERR_SHAPE";
+        case DISCO_ERR_DTYPE: return "DISCO_ERR_DTYPE";
+        case DISCO_ERR_OUT_OF_MEMORY: return "DISCO_ERR_OUT_OF_MEMORY";
+        case DISCO_ERR_DEVICE: return "DISCO_ERR_DEVICE";
+    }
+    return "DISCO_ERR_UNKNOWN";
+}
+
+const char* disco_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,94 @@
+// disco_internal.h -- shared declarations of libdisco's plan builder, kernels
+// and C ABI layer.  Not installed; the public interface is include/disco.h.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include <hip/hip_runtime.h>
+
+namespace disco {
+
+constexpr int kBasis = 9;
+
+// Parameters of a plan: the forward op maps the in-grid to the out-grid.
+struct PlanParams {
+    int nlat_in, nlon_in, nlat_out, nlon_out;
+    double theta_c;  // filter cutoff (radians)
+    double h;        // node spacing of the 3x3 grid (radians)
+    int quadrature;  // DISCO_QUAD_*
+};
+
+// Longitude structure of one op (forward or transposed) as a gather:
+// output pixel p_o = P * q + r (q in [0, nq), phase r in [0, P)) reads input
+// pixel (stride * q + d) mod nlon_i for each stored entry (t_i, d) of the
+// pattern of (output ring, r).  One of nlon_i / nlon_o and nlon_o / nlon_i is
+// an integer s: then (P, stride) = (1, s) or (s, 1).
+struct OpGeom {
+    int nlat_o, nlon_o;  // op output grid
+    int nlat_i, nlon_i;  // op input grid
+    int P, stride, nq;
+    bool centre_at_input;  // transposed op: the filter sits on the op's input points
+    int n_patterns() const { return nlat_o * P; }
+};
+
+// Host-built sparse psi of one op, patterns in (output ring, phase) order,
+// entries of a pattern ordered by input ring then by longitude offset.
+struct HostOp {
+    OpGeom g{};
+    std::vector<int32_t> pat_ptr;  // n_patterns + 1
+    std::vector<int32_t> t_in;     // per entry: input ring
+    std::vector<int32_t> d;        // per entry: offset in [0, nlon_i)
+    std::vector<float> val;        // per entry: 9 values, psi_k * q(input ring)
+    int32_t max_window = 0;
+    int32_t full_ring_windows = 0;
+    int64_t nnz_pairs = 0;  // non-zero (output pixel, input pixel, k) triples
+};
+
+// Returns 0 on success, otherwise a disco_status_t with *err set.
+int make_op_geom(const PlanParams& p, bool transpose, OpGeom* g, std::string* err);
+int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* err);
+
+// Device-side layout of one op (see disco_kernels.hip).
+struct DevEntry {
+    int32_t row;  // input ring * nlon_i
+    int32_t d;    // longitude offset in [0, nlon_i)
+    float v[kBasis];
+    int32_t pad;
+};
+static_assert(sizeof(DevEntry) == 48, "DevEntry is 12 dwords");
+
+struct DeviceOp {
+    OpGeom g{};
+    int32_t* pat_ptr = nullptr;  // device, n_patterns + 1
+    DevEntry* entries = nullptr;  // device
+    int64_t n_entries = 0;
+    int64_t nnz_pairs = 0;
+    int64_t bytes = 0;
+};
+
+// Kernel launchers (disco_kernels.hip).  All return a hipError_t.
+// dtype: 0 = fp32, 1 = bf16 (raw uint16 storage).
+struct ExecArgs {
+    const DeviceOp* op;
+    const void* x;
+    const void* w;
+    void* y;
+    int dtype;
+    int B, Ci, Co;   // op's input / output channels
+    bool w_trans;    // W is [Ci][Co][9] (transposed op) instead of [Co][Ci][9]
+    hipStream_t stream;
+};
+
+// Kernel timing hook: when enabled, brackets a launch with events on `s`.
+// Returns the token to pass to timing_end (or -1 when disabled).
+int timing_begin(const char* name, hipStream_t s);
+void timing_end(int token, hipStream_t s);
+
+hipError_t launch_gather_then_contract(const ExecArgs& a, float* z_ws);
+hipError_t launch_contract_then_gather(const ExecArgs& a, float* xc_ws);
+size_t workspace_bytes_gather_then_contract(const ExecArgs& a);
+size_t workspace_bytes_contract_then_gather(const ExecArgs& a);
+
+}  // namespace disco

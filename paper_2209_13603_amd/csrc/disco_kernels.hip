@@ -1,0 +1,265 @@
+// disco_kernels.hip -- gfx950 kernels of the DISCO forward and transposed ops.
+//
+// The sparse-dense product of Sec. 4.1, in the compressed form of Sec. 4.2
+// (eq. "memory_compression"): each output ring r_o (and longitude phase) owns
+// one list of (input ring, longitude offset, 9 values) entries; the output at
+// longitude q reads the input at (stride * q + offset) mod nlon.  Lanes of a
+// wavefront own consecutive output longitudes, so every entry is one
+// wave-uniform set of 9 scalars applied to a contiguous, coalesced row
+// segment of the input; the reduction order over entries is the same for
+// every output longitude, which makes whole-pixel longitude shifts commute
+// with the op bitwise.
+//
+// Two orderings of the channel contraction:
+//   gather-then-contract:  Z[b,ci,k,n_o] = sum_e v_k x[b,ci,pix_e]
+//                          y[b,co,n_o]   = sum_{ci,k} W[co,ci,k] Z[b,ci,k,n_o]
+//   contract-then-gather:  X[b,co,k,n_i] = sum_ci W[co,ci,k] x[b,ci,n_i]
+//                          y[b,co,n_o]   = sum_e sum_k v_k X[b,co,k,pix_e]
+// The second moves the channel mixing to the coarser grid when the op
+// upsamples.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "disco_internal.h"
+
+namespace disco {
+
+namespace {
+
+constexpr int kBlock = 256;
+
+// Storage types: fp32, or bf16 held as raw uint16.
+__device__ __forceinline__ float load_val(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float load_val(const uint16_t* p, int64_t i) {
+    return __uint_as_float((uint32_t)p[i] << 16);
+}
+
+// fp32 -> bf16 with round-to-nearest-even (NaN stays a quiet NaN).
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ void store_val(float* p, int64_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void store_val(uint16_t* p, int64_t i, float v) { p[i] = to_bf16(v); }
+
+// W element for (op output channel co, op input channel ci, basis k):
+// [Co][Ci][9] for the forward op, [Ci][Co][9] for the transposed op.
+template <typename T>
+__device__ __forceinline__ float w_at(const T* w, int co, int ci, int k, int Ci, int Co, bool w_trans) {
+    const int64_t idx = w_trans ? ((int64_t)ci * Co + co) * kBasis + k : ((int64_t)co * Ci + ci) * kBasis + k;
+    return load_val(w, idx);
+}
+
+// ---------------------------------------------------------------------------
+// Gather of x into Z (9 planes per input channel).
+// grid: (ceil(nq / 256), n_patterns, B * ceil(C / CG)); one lane per output
+// longitude q of the pattern's ring and phase.
+template <typename T, int CG>
+__global__ __launch_bounds__(kBlock) void k_gather_z(const int32_t* __restrict__ pat_ptr,
+                                                     const DevEntry* __restrict__ ent, OpGeom g,
+                                                     const T* __restrict__ x, float* __restrict__ z,
+                                                     int C, int n_cgroups) {
+    const int q = blockIdx.x * kBlock + threadIdx.x;
+    const int pat = blockIdx.y;
+    const int b = blockIdx.z / n_cgroups;
+    const int c0 = (blockIdx.z % n_cgroups) * CG;
+    if (q >= g.nq) return;
+    const int to = pat / g.P, r = pat - to * g.P;
+    const int64_t n_in = (int64_t)g.nlat_i * g.nlon_i;
+    const int64_t n_out = (int64_t)g.nlat_o * g.nlon_o;
+    const int base = g.stride * q;
+    float acc[CG][kBasis];
+#pragma unroll
+    for (int c = 0; c < CG; ++c)
+#pragma unroll
+        for (int k = 0; k < kBasis; ++k) acc[c][k] = 0.0f;
+    const int e0 = pat_ptr[pat], e1 = pat_ptr[pat + 1];
+    for (int e = e0; e < e1; ++e) {
+        const DevEntry E = ent[e];
+        int idx = base + E.d;
+        if (idx >= g.nlon_i) idx -= g.nlon_i;
+#pragma unroll
+        for (int c = 0; c < CG; ++c) {
+            const int cc = c0 + c < C ? c0 + c : C - 1;
+            const float xv = load_val(x, ((int64_t)b * C + cc) * n_in + E.row + idx);
+#pragma unroll
+            for (int k = 0; k < kBasis; ++k) acc[c][k] = fmaf(E.v[k], xv, acc[c][k]);
+        }
+    }
+    const int64_t pix = (int64_t)to * g.nlon_o + (int64_t)q * g.P + r;
+#pragma unroll
+    for (int c = 0; c < CG; ++c) {
+        if (c0 + c < C) {
+#pragma unroll
+            for (int k = 0; k < kBasis; ++k)
+                z[(((int64_t)b * C + c0 + c) * kBasis + k) * n_out + pix] = acc[c][k];
+        }
+    }
+}
+
+// Channel contraction of Z: y[b,co,n] = sum_{ci,k} W(co,ci,k) Z[b,ci,k,n].
+// grid: (ceil(N / 256), B, ceil(Co / COT)).
+template <typename T, int COT>
+__global__ __launch_bounds__(kBlock) void k_contract_z(const float* __restrict__ z,
+                                                       const T* __restrict__ w, T* __restrict__ y,
+                                                       int Ci, int Co, int64_t N, bool w_trans) {
+    const int64_t n = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int b = blockIdx.y;
+    const int co0 = blockIdx.z * COT;
+    if (n >= N) return;
+    float acc[COT];
+#pragma unroll
+    for (int j = 0; j < COT; ++j) acc[j] = 0.0f;
+    for (int ci = 0; ci < Ci; ++ci) {
+#pragma unroll
+        for (int k = 0; k < kBasis; ++k) {
+            const float zv = z[(((int64_t)b * Ci + ci) * kBasis + k) * N + n];
+#pragma unroll
+            for (int j = 0; j < COT; ++j) {
+                const int co = co0 + j < Co ? co0 + j : Co - 1;
+                acc[j] = fmaf(w_at(w, co, ci, k, Ci, Co, w_trans), zv, acc[j]);
+            }
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < COT; ++j) {
+        if (co0 + j < Co) store_val(y, ((int64_t)b * Co + co0 + j) * N + n, acc[j]);
+    }
+}
+
+// Channel contraction on the input grid: X[b,co,k,n] = sum_ci W(co,ci,k) x[b,ci,n].
+// grid: (ceil(N / 256), B, ceil(Co * 9 / MT)).
+template <typename T, int MT>
+__global__ __launch_bounds__(kBlock) void k_contract_x(const T* __restrict__ x,
+                                                       const T* __restrict__ w,
+                                                       float* __restrict__ xc, int Ci, int Co,
+                                                       int64_t N, bool w_trans) {
+    const int64_t n = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int b = blockIdx.y;
+    const int m0 = blockIdx.z * MT;
+    const int M = Co * kBasis;
+    if (n >= N) return;
+    float acc[MT];
+#pragma unroll
+    for (int j = 0; j < MT; ++j) acc[j] = 0.0f;
+    for (int ci = 0; ci < Ci; ++ci) {
+        const float xv = load_val(x, ((int64_t)b * Ci + ci) * N + n);
+#pragma unroll
+        for (int j = 0; j < MT; ++j) {
+            const int m = m0 + j < M ? m0 + j : M - 1;
+            acc[j] = fmaf(w_at(w, m / kBasis, ci, m % kBasis, Ci, Co, w_trans), xv, acc[j]);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+        if (m0 + j < M) xc[((int64_t)b * M + m0 + j) * N + n] = acc[j];
+    }
+}
+
+// Gather of the contracted planes: y[b,co,n_o] = sum_e sum_k v_k X[b,co,k,pix_e].
+// grid: (ceil(nq / 256), n_patterns, B * ceil(Co / CG)).
+template <typename T, int CG>
+__global__ __launch_bounds__(kBlock) void k_gather_y(const int32_t* __restrict__ pat_ptr,
+                                                     const DevEntry* __restrict__ ent, OpGeom g,
+                                                     const float* __restrict__ xc,
+                                                     T* __restrict__ y, int Co, int n_cgroups) {
+    const int q = blockIdx.x * kBlock + threadIdx.x;
+    const int pat = blockIdx.y;
+    const int b = blockIdx.z / n_cgroups;
+    const int c0 = (blockIdx.z % n_cgroups) * CG;
+    if (q >= g.nq) return;
+    const int to = pat / g.P, r = pat - to * g.P;
+    const int64_t n_in = (int64_t)g.nlat_i * g.nlon_i;
+    const int64_t n_out = (int64_t)g.nlat_o * g.nlon_o;
+    const int base = g.stride * q;
+    float acc[CG];
+#pragma unroll
+    for (int c = 0; c < CG; ++c) acc[c] = 0.0f;
+    const int e0 = pat_ptr[pat], e1 = pat_ptr[pat + 1];
+    for (int e = e0; e < e1; ++e) {
+        const DevEntry E = ent[e];
+        int idx = base + E.d;
+        if (idx >= g.nlon_i) idx -= g.nlon_i;
+#pragma unroll
+        for (int c = 0; c < CG; ++c) {
+            const int cc = c0 + c < Co ? c0 + c : Co - 1;
+            const float* plane = xc + ((int64_t)b * Co + cc) * kBasis * n_in + E.row + idx;
+#pragma unroll
+            for (int k = 0; k < kBasis; ++k) acc[c] = fmaf(E.v[k], plane[k * n_in], acc[c]);
+        }
+    }
+    const int64_t pix = (int64_t)to * g.nlon_o + (int64_t)q * g.P + r;
+#pragma unroll
+    for (int c = 0; c < CG; ++c) {
+        if (c0 + c < Co) store_val(y, ((int64_t)b * Co + c0 + c) * n_out + pix, acc[c]);
+    }
+}
+
+template <typename T>
+hipError_t gather_then_contract(const ExecArgs& a, float* z) {
+    const OpGeom& g = a.op->g;
+    constexpr int CG = 4;
+    const int ncg = (a.Ci + CG - 1) / CG;
+    dim3 grid1((g.nq + kBlock - 1) / kBlock, g.n_patterns(), a.B * ncg);
+    int tk = timing_begin("gather_z", a.stream);
+    hipLaunchKernelGGL((k_gather_z<T, CG>), grid1, dim3(kBlock), 0, a.stream, a.op->pat_ptr,
+                       a.op->entries, g, (const T*)a.x, z, a.Ci, ncg);
+    timing_end(tk, a.stream);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t N = (int64_t)g.nlat_o * g.nlon_o;
+    constexpr int COT = 8;
+    dim3 grid2((unsigned)((N + kBlock - 1) / kBlock), a.B, (a.Co + COT - 1) / COT);
+    tk = timing_begin("contract_z", a.stream);
+    hipLaunchKernelGGL((k_contract_z<T, COT>), grid2, dim3(kBlock), 0, a.stream, z,
+                       (const T*)a.w, (T*)a.y, a.Ci, a.Co, N, a.w_trans);
+    timing_end(tk, a.stream);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t contract_then_gather(const ExecArgs& a, float* xc) {
+    const OpGeom& g = a.op->g;
+    const int64_t N = (int64_t)g.nlat_i * g.nlon_i;
+    constexpr int MT = 9;
+    dim3 grid1((unsigned)((N + kBlock - 1) / kBlock), a.B, (a.Co * kBasis + MT - 1) / MT);
+    int tk = timing_begin("contract_x", a.stream);
+    hipLaunchKernelGGL((k_contract_x<T, MT>), grid1, dim3(kBlock), 0, a.stream, (const T*)a.x,
+                       (const T*)a.w, xc, a.Ci, a.Co, N, a.w_trans);
+    timing_end(tk, a.stream);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    constexpr int CG = 4;
+    const int ncg = (a.Co + CG - 1) / CG;
+    dim3 grid2((g.nq + kBlock - 1) / kBlock, g.n_patterns(), a.B * ncg);
+    tk = timing_begin("gather_y", a.stream);
+    hipLaunchKernelGGL((k_gather_y<T, CG>), grid2, dim3(kBlock), 0, a.stream, a.op->pat_ptr,
+                       a.op->entries, g, xc, (T*)a.y, a.Co, ncg);
+    timing_end(tk, a.stream);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t workspace_bytes_gather_then_contract(const ExecArgs& a) {
+    const OpGeom& g = a.op->g;
+    return sizeof(float) * (size_t)a.B * a.Ci * kBasis * (size_t)g.nlat_o * g.nlon_o;
+}
+
+size_t workspace_bytes_contract_then_gather(const ExecArgs& a) {
+    const OpGeom& g = a.op->g;
+    return sizeof(float) * (size_t)a.B * a.Co * kBasis * (size_t)g.nlat_i * g.nlon_i;
+}
+
+hipError_t launch_gather_then_contract(const ExecArgs& a, float* z_ws) {
+    return a.dtype == 1 ? gather_then_contract<uint16_t>(a, z_ws) : gather_then_contract<float>(a, z_ws);
+}
+
+hipError_t launch_contract_then_gather(const ExecArgs& a, float* xc_ws) {
+    return a.dtype == 1 ? contract_then_gather<uint16_t>(a, xc_ws) : contract_then_gather<float>(a, xc_ws);
+}
+
+}  // namespace disco

@@ -1,0 +1,201 @@
+// disco_plan.cpp -- host construction of the sparse psi tensor (fp64).
+//
+// Sec. 4.1: Psi_ji = psi(R_j^{-1} w_i) is evaluated only where it can be
+// non-zero, using the cutoff theta_c to limit the rotated coordinates that are
+// computed.  Sec. 4.2: on an equiangular grid a rotation about z is a cyclic
+// longitude shift, so the pattern of one output ring (per longitude phase) is
+// stored once and reused at every output longitude.
+//
+// Per output ring the builder visits only input rings whose colatitude is
+// within the search radius (the geodesic distance is at least the colatitude
+// difference) and, on each, only the closed-form longitude window where the
+// distance can be within the radius (spherical law of cosines), plus one
+// pixel of margin.  Each candidate pair is evaluated in fp64 with the
+// half-angle form of R_j^{-1} w_i, which keeps full relative precision for
+// nearby points (the colatitude difference comes from integer ring indices,
+// the longitude difference from an integer residue):
+//   x' = sin(ti - tj) - 2 sin(ti) cos(tj) sin^2(dphi/2)
+//   y' = sin(ti) sin(dphi)
+//   z' = cos(ti - tj) - 2 sin(ti) sin(tj) sin^2(dphi/2)
+// Theta = atan2(|(x', y')|, z'), (u, v) = Theta (x', y') / |(x', y')|
+// (azimuthal equidistant tangent plane: u south, v east).  Entries whose nine
+// basis values are all zero are dropped.  Values absorb the quadrature weight
+// of the op's input ring (Sec. 4.1: quadrature absorbed into f) and are then
+// rounded to fp32.
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <numeric>
+
+#include "disco.h"
+#include "disco_internal.h"
+
+namespace disco {
+
+namespace {
+
+constexpr double kPi = 3.14159265358979323846;
+
+double colat(int t, int nlat) { return (t + 0.5) * kPi / nlat; }
+
+// Quadrature weight per ring (a pixel's weight is its ring's).  Fejer's first
+// rule in cos(theta) on the cell-centred colatitudes, times 2 pi / nlon, is
+// exact for band-limited signals on this grid (the sampling-theorem
+// quadrature the paper adopts, Sec. 3.2 and App. A); cell areas are offered as
+// the alternative.
+std::vector<double> ring_weights(int nlat, int nlon, int kind) {
+    std::vector<double> q(nlat);
+    const double dphi = 2.0 * kPi / nlon;
+    for (int t = 0; t < nlat; ++t) {
+        const double th = colat(t, nlat);
+        double w;
+        if (kind == DISCO_QUAD_CELL_AREA) {
+            const double half = 0.5 * kPi / nlat;
+            w = std::cos(th - half) - std::cos(th + half);
+        } else {
+            double acc = 0.0;
+            for (int m = 1; 2 * m <= nlat; ++m)
+                acc += std::cos(2.0 * m * th) / ((2.0 * m - 1.0) * (2.0 * m + 1.0));
+            w = 2.0 / nlat * (1.0 - 2.0 * acc);
+        }
+        q[t] = w * dphi;
+    }
+    return q;
+}
+
+double hat(double s) {
+    const double a = std::fabs(s);
+    return a < 1.0 ? 1.0 - a : 0.0;
+}
+
+}  // namespace
+
+int make_op_geom(const PlanParams& p, bool transpose, OpGeom* g, std::string* err) {
+    OpGeom o{};
+    o.centre_at_input = transpose;
+    if (!transpose) {
+        o.nlat_o = p.nlat_out; o.nlon_o = p.nlon_out;
+        o.nlat_i = p.nlat_in;  o.nlon_i = p.nlon_in;
+    } else {
+        o.nlat_o = p.nlat_in;  o.nlon_o = p.nlon_in;
+        o.nlat_i = p.nlat_out; o.nlon_i = p.nlon_out;
+    }
+    if (o.nlon_i % o.nlon_o == 0) {
+        o.P = 1;
+        o.stride = o.nlon_i / o.nlon_o;
+    } else if (o.nlon_o % o.nlon_i == 0) {
+        o.P = o.nlon_o / o.nlon_i;
+        o.stride = 1;
+    } else {
+        if (err) *err = "longitude counts must divide one another (nlon_in=" +
+                        std::to_string(p.nlon_in) + ", nlon_out=" + std::to_string(p.nlon_out) + ")";
+        return DISCO_ERR_UNSUPPORTED;
+    }
+    o.nq = o.nlon_o / o.P;
+    *g = o;
+    return DISCO_OK;
+}
+
+int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* err) {
+    OpGeom g;
+    int rc = make_op_geom(p, transpose, &g, err);
+    if (rc) return rc;
+    op->g = g;
+    // Quadrature of the op's input grid: the forward op sums over plan
+    // in-grid points; the transposed op over plan out-grid points, its centres.
+    const std::vector<double> q = ring_weights(g.nlat_i, g.nlon_i, p.quadrature);
+    const double h = p.h;
+    // Basis support radius: the hats vanish for max(|u|, |v|) >= 2h.
+    const double radius = std::min(p.theta_c, 2.0 * std::sqrt(2.0) * h);
+    const int64_t M = (int64_t)g.nlon_i * g.nlon_o;  // longitude residues per 2 pi
+
+    std::vector<double> sin_o(g.nlat_o), cos_o(g.nlat_o), sin_i(g.nlat_i), cos_i(g.nlat_i);
+    for (int t = 0; t < g.nlat_o; ++t) { sin_o[t] = std::sin(colat(t, g.nlat_o)); cos_o[t] = std::cos(colat(t, g.nlat_o)); }
+    for (int t = 0; t < g.nlat_i; ++t) { sin_i[t] = std::sin(colat(t, g.nlat_i)); cos_i[t] = std::cos(colat(t, g.nlat_i)); }
+
+    op->pat_ptr.assign(1, 0);
+    op->t_in.clear(); op->d.clear(); op->val.clear();
+    op->max_window = 0; op->full_ring_windows = 0; op->nnz_pairs = 0;
+
+    for (int to = 0; to < g.nlat_o; ++to) {
+        for (int r = 0; r < g.P; ++r) {
+            for (int ti = 0; ti < g.nlat_i; ++ti) {
+                // Colatitude difference (input - output) from integers:
+                // pi * ((2ti+1) nlat_o - (2to+1) nlat_i) / (2 nlat_i nlat_o).
+                const int64_t dnum = (int64_t)(2 * ti + 1) * g.nlat_o - (int64_t)(2 * to + 1) * g.nlat_i;
+                const double dth_io = kPi * (double)dnum / (2.0 * (double)g.nlat_i * g.nlat_o);
+                if (std::fabs(dth_io) > radius * (1.0 + 1e-12)) continue;
+                // Centre ring c and evaluation ring e of the filter.
+                double sc, cc, se, ce, dth;  // dth = theta_e - theta_c
+                if (!g.centre_at_input) {
+                    sc = sin_o[to]; cc = cos_o[to]; se = sin_i[ti]; ce = cos_i[ti]; dth = dth_io;
+                } else {
+                    sc = sin_i[ti]; cc = cos_i[ti]; se = sin_o[to]; ce = cos_o[to]; dth = -dth_io;
+                }
+                // Longitude window: distance <= radius  <=>  |dphi| <= dphi_max.
+                const double den = sc * se;
+                const double cmax = den > 0 ? (std::cos(radius) - cc * ce) / den : -2.0;
+                // Residue n = d * nlon_o - r * nlon_i of phi_i - phi_o = 2 pi n / M.
+                int64_t d_lo, d_hi;
+                bool full = false;
+                if (cmax <= -1.0) {
+                    full = true;
+                } else {
+                    const double dphi_max = std::acos(std::min(1.0, cmax));
+                    const double nmax = dphi_max * (double)M / (2.0 * kPi);
+                    d_lo = (int64_t)std::floor(((double)r * g.nlon_i - nmax) / g.nlon_o) - 1;
+                    d_hi = (int64_t)std::ceil(((double)r * g.nlon_i + nmax) / g.nlon_o) + 1;
+                    if (d_hi - d_lo + 1 >= g.nlon_i) full = true;
+                }
+                if (full) {
+                    // Exactly one full turn, centred on the output longitude.
+                    d_lo = (int64_t)std::ceil(((double)r * g.nlon_i - 0.5 * (double)M) / g.nlon_o);
+                    d_hi = d_lo + g.nlon_i - 1;
+                }
+                int32_t kept = 0;
+                for (int64_t dd = d_lo; dd <= d_hi; ++dd) {
+                    int64_t n = dd * g.nlon_o - (int64_t)r * g.nlon_i;
+                    n %= M;
+                    if (n > M / 2) n -= M;
+                    if (n < -M / 2) n += M;
+                    // phi_e - phi_c: input minus output for the forward op.
+                    const double dphi = 2.0 * kPi * (double)n / (double)M * (g.centre_at_input ? -1.0 : 1.0);
+                    const double s2 = std::sin(0.5 * dphi);
+                    const double xs = std::sin(dth) - 2.0 * se * cc * s2 * s2;
+                    const double ys = se * std::sin(dphi);
+                    const double zs = std::cos(dth) - 2.0 * se * sc * s2 * s2;
+                    const double rho = std::hypot(xs, ys);
+                    const double Th = std::atan2(rho, zs);
+                    if (Th > p.theta_c) continue;
+                    double u = 0.0, v = 0.0;
+                    if (rho > 0.0) { u = Th * xs / rho; v = Th * ys / rho; }
+                    float vals[kBasis];
+                    bool any = false;
+                    int nzk = 0;
+                    for (int a = 0; a < 3; ++a) {
+                        const double ha = hat(u / h - (a - 1));
+                        for (int b = 0; b < 3; ++b) {
+                            const double psi = ha * hat(v / h - (b - 1));
+                            vals[3 * a + b] = (float)(psi * q[ti]);
+                            if (psi != 0.0) { any = true; ++nzk; }
+                        }
+                    }
+                    if (!any) continue;
+                    int64_t dnorm = dd % g.nlon_i;
+                    if (dnorm < 0) dnorm += g.nlon_i;
+                    op->t_in.push_back(ti);
+                    op->d.push_back((int32_t)dnorm);
+                    op->val.insert(op->val.end(), vals, vals + kBasis);
+                    op->nnz_pairs += (int64_t)nzk * g.nq;
+                    ++kept;
+                }
+                if (kept > 0 && full) ++op->full_ring_windows;
+                op->max_window = std::max(op->max_window, kept);
+            }
+            op->pat_ptr.push_back((int32_t)op->t_in.size());
+        }
+    }
+    return DISCO_OK;
+}
+
+}  // namespace disco

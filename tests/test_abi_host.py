@@ -1,0 +1,171 @@
+"""Host-side checks of libdisco.so that need no GPU: the library loads, exports
+every function include/disco.h declares, validates arguments, and its plan
+builder's psi entries equal the oracle's dense Psi entry by entry."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2209_13603_amd import disco
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    with open(os.path.join(ROOT, "include", "disco.h")) as f:
+        src = f.read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(disco_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    lib = disco.library()
+    declared = _declared_functions()
+    assert declared, "no declarations parsed"
+    assert set(declared) == set(disco.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    lib = disco.library()
+    for s in range(7):
+        assert lib.disco_status_string(s).decode() == disco._status_name(s)
+    assert lib.disco_status_string(99).decode() == "DISCO_ERR_UNKNOWN"
+
+
+def _create(*args, basis=None):
+    lib = disco.library()
+    h = ctypes.c_void_p()
+    b = ctypes.byref(basis) if basis is not None else None
+    return lib.disco_plan_create(*args, b, ctypes.byref(h)), h
+
+
+@pytest.mark.parametrize("args,status", [
+    ((0, 64, 32, 64, 0.3), disco.DISCO_ERR_INVALID_ARGUMENT),
+    ((32, 1, 32, 64, 0.3), disco.DISCO_ERR_INVALID_ARGUMENT),
+    ((32, 64, 32, 64, 0.0), disco.DISCO_ERR_INVALID_ARGUMENT),
+    ((32, 64, 32, 64, -1.0), disco.DISCO_ERR_INVALID_ARGUMENT),
+    ((32, 64, 32, 64, 3.5), disco.DISCO_ERR_INVALID_ARGUMENT),
+    ((32, 64, 32, 64, float("nan")), disco.DISCO_ERR_INVALID_ARGUMENT),
+    ((32, 64, 32, 48, 0.3), disco.DISCO_ERR_UNSUPPORTED),
+])
+def test_plan_create_validation(args, status):
+    rc, h = _create(*args)
+    assert rc == status
+    assert not h.value
+    assert disco.library().disco_last_error().decode()
+
+
+def test_basis_validation():
+    rc, _ = _create(32, 64, 32, 64, 0.3, basis=disco.Basis(7, 0, 0.0))
+    assert rc == disco.DISCO_ERR_UNSUPPORTED
+    rc, _ = _create(32, 64, 32, 64, 0.3, basis=disco.Basis(0, 5, 0.0))
+    assert rc == disco.DISCO_ERR_UNSUPPORTED
+    rc, _ = _create(32, 64, 32, 64, 0.3, basis=disco.Basis(0, 0, -0.1))
+    assert rc == disco.DISCO_ERR_INVALID_ARGUMENT
+    lib = disco.library()
+    assert lib.disco_plan_create(32, 64, 32, 64, 0.3, None, None) == disco.DISCO_ERR_INVALID_ARGUMENT
+
+
+def test_null_plan_calls():
+    lib = disco.library()
+    t = disco.Tensor()
+    assert lib.disco_forward(None, ctypes.byref(t), ctypes.byref(t), ctypes.byref(t), None) == \
+        disco.DISCO_ERR_INVALID_ARGUMENT
+    assert lib.disco_transpose(None, ctypes.byref(t), ctypes.byref(t), ctypes.byref(t), None) == \
+        disco.DISCO_ERR_INVALID_ARGUMENT
+    assert lib.disco_plan_query(None, None) == disco.DISCO_ERR_INVALID_ARGUMENT
+    assert lib.disco_plan_destroy(None) == disco.DISCO_OK
+
+
+# --------------------------------------------------------------------------- #
+# Plan entries against the oracle's dense Psi (fp64 oracle, fp32 entries).
+# --------------------------------------------------------------------------- #
+PLAN_CASES = [
+    (8, 16, 8, 16),       # same grid
+    (16, 32, 8, 16),      # stride-2 downsampling forward
+    (12, 24, 6, 12),      # odd ring counts
+    (8, 16, 16, 32),      # forward that upsamples (2 longitude phases)
+    (32, 64, 32, 64),     # the 32 x 64 workload
+    (10, 20, 5, 20),      # latitude-only change
+]
+
+
+def _dense_check(case, transpose):
+    a, b, c, d = case
+    tc = 3 * math.pi / min(a, c)
+    o = oracle.default()
+    psi = o.psi_dense(a, b, c, d, tc)      # [Nout_plan, Nin_plan, 9]
+    if not transpose:
+        nlat_o, nlon_o, nlat_i, nlon_i = c, d, a, b
+        q = o.quadrature(a, b)
+        dense = psi                           # [op out pixel, op in pixel, 9]
+    else:
+        nlat_o, nlon_o, nlat_i, nlon_i = a, b, c, d
+        q = o.quadrature(c, d)
+        dense = psi.transpose(1, 0, 2)        # filter centred at the op's input points
+    ent = disco.psi_entries(a, b, c, d, tc, transpose=transpose)
+    P, s = ent["phases"], ent["stride"]
+    assert (P, s) == ((1, nlon_i // nlon_o) if nlon_i % nlon_o == 0 else (nlon_o // nlon_i, 1))
+    n = ent["values"].shape[0]
+    assert n > 0
+    seen = set()
+    for e in range(n):
+        to, r, ti, dd = (int(ent[k][e]) for k in ("out_ring", "phase", "in_ring", "offset"))
+        key = (to, r, ti, dd)
+        assert key not in seen
+        seen.add(key)
+        jo = to * nlon_o + r                  # output pixel q = 0 of the pattern
+        ii = ti * nlon_i + dd % nlon_i        # input pixel (stride * 0 + d) mod nlon
+        ref = dense[jo, ii] * q[ti]
+        got = ent["values"][e].astype(np.float64)
+        assert np.abs(got - ref).max() <= 2e-7 * abs(q[ti]) + 1e-30, (key, got, ref)
+    # Completeness: every non-zero dense element of the q = 0 outputs is stored
+    # (the two geometry routes may disagree on exact zeros at hat edges by
+    # ~1e-16, a difference the continuity of the basis keeps harmless).
+    for to in range(nlat_o):
+        for r in range(P):
+            jo = to * nlon_o + r
+            nz = np.nonzero(np.abs(dense[jo]).sum(axis=1) > 1e-12)[0]
+            for ii in nz:
+                assert (to, r, int(ii // nlon_i), int(ii % nlon_i)) in seen, (to, r, ii)
+    # Shift structure (Sec. 4.2): output q > 0 of the pattern reads pixel
+    # (stride q + d) mod nlon with the same values.
+    for to in range(nlat_o):
+        for r in range(P):
+            for qq in (1, nlon_o // P - 1):
+                jo = to * nlon_o + P * qq + r
+                jr = to * nlon_o + r
+                shifted = np.roll(dense[jr].reshape(nlat_i, nlon_i, 9), s * qq, axis=1)
+                assert np.abs(dense[jo] - shifted.reshape(-1, 9)).max() <= 1e-13
+
+
+@pytest.mark.parametrize("case", PLAN_CASES)
+def test_plan_entries_forward_match_dense_psi(case):
+    _dense_check(case, False)
+
+
+@pytest.mark.parametrize("case", PLAN_CASES)
+def test_plan_entries_transpose_match_dense_psi(case):
+    _dense_check(case, True)
+
+
+def test_psi_entries_validation():
+    lib = disco.library()
+    cnt = ctypes.c_int64()
+    null = ctypes.POINTER(ctypes.c_int32)()
+    nullf = ctypes.POINTER(ctypes.c_float)()
+    rc = lib.disco_psi_entries(0, 16, 8, 16, 0.3, None, 0, 0, null, null, null, null, nullf,
+                               ctypes.byref(cnt), None, None)
+    assert rc == disco.DISCO_ERR_INVALID_ARGUMENT
+    rc = lib.disco_psi_entries(8, 16, 8, 12, 0.3, None, 0, 0, null, null, null, null, nullf,
+                               ctypes.byref(cnt), None, None)
+    assert rc == disco.DISCO_ERR_UNSUPPORTED
+    rc = lib.disco_psi_entries(8, 16, 8, 16, 0.3, None, 0, 0, null, null, null, null, nullf,
+                               None, None, None)
+    assert rc == disco.DISCO_ERR_INVALID_ARGUMENT
