@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB_PATH = os.path.join(BUILD_DIR, "libdisco.so")
 
-SOURCES = ["disco_plan.cpp", "disco_abi.cpp", "disco_kernels.hip"]
+SOURCES = ["disco_plan.cpp", "disco_pack.cpp", "disco_abi.cpp", "disco_kernels.hip", "disco_fused.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -39,7 +39,7 @@ def _run(cmd, verbose):
         print(out)
 
 
-def build(verbose: bool = False, jobs: int = 3) -> str:
+def build(verbose: bool = False, jobs: int = 5) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
     objs, procs = [], []
     with tempfile.TemporaryDirectory(dir=BUILD_DIR) as tmp:

@@ -72,6 +72,56 @@ disco_status_t resolve_params(int nlat_in, int nlon_in, int nlat_out, int nlon_o
     return DISCO_OK;
 }
 
+template <typename V>
+disco_status_t upload_vec(const std::vector<V>& v, V** dst, int64_t* bytes, const char* what) {
+    const size_t n = sizeof(V) * std::max<size_t>(v.size(), 1);
+    hipError_t e = hipMalloc((void**)dst, n);
+    if (e != hipSuccess) { *dst = nullptr; return hip_fail(e, what); }
+    if (!v.empty()) {
+        e = hipMemcpy(*dst, v.data(), sizeof(V) * v.size(), hipMemcpyHostToDevice);
+        if (e != hipSuccess) return hip_fail(e, what);
+    }
+    *bytes += (int64_t)n;
+    return DISCO_OK;
+}
+
+// Entries per work item of the fused kernel (balances workgroups).
+constexpr int kTargetEntries = 512;
+
+disco_status_t upload_packed(const HostOp& h, PackedDev* d) {
+    PackedHost P;
+    std::string err;
+    int rc = pack_op(h, kTargetEntries, &P, &err);
+    if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
+    disco_status_t s;
+    if ((s = upload_vec(P.spans, &d->spans, &d->bytes, "hipMalloc(spans)")) != DISCO_OK) return s;
+    if ((s = upload_vec(P.chunks, &d->chunks, &d->bytes, "hipMalloc(chunks)")) != DISCO_OK) return s;
+    std::vector<int32_t> offs(P.entries.size());
+    std::vector<PVal> vals(P.entries.size());
+    for (size_t i = 0; i < P.entries.size(); ++i) {
+        offs[i] = P.entries[i].off;
+        for (int k = 0; k < 4; ++k) vals[i].v[k] = P.entries[i].v[k];
+    }
+    if ((s = upload_vec(offs, &d->offs, &d->bytes, "hipMalloc(entry offsets)")) != DISCO_OK) return s;
+    if ((s = upload_vec(vals, &d->vals, &d->bytes, "hipMalloc(entry values)")) != DISCO_OK) return s;
+    if ((s = upload_vec(P.segs, &d->segs, &d->bytes, "hipMalloc(segments)")) != DISCO_OK) return s;
+    if ((s = upload_vec(P.items, &d->items, &d->bytes, "hipMalloc(items)")) != DISCO_OK) return s;
+    if ((s = upload_vec(P.red_pattern, &d->red_pattern, &d->bytes, "hipMalloc(reduce)")) != DISCO_OK) return s;
+    if ((s = upload_vec(P.red_ptr, &d->red_ptr, &d->bytes, "hipMalloc(reduce)")) != DISCO_OK) return s;
+    if ((s = upload_vec(P.red_slots, &d->red_slots, &d->bytes, "hipMalloc(reduce)")) != DISCO_OK) return s;
+    d->n_items = (int32_t)P.items.size();
+    d->n_split = (int32_t)P.red_pattern.size();
+    d->n_slots = P.n_slots;
+    return DISCO_OK;
+}
+
+void free_packed(PackedDev* d) {
+    void* ptrs[] = {d->spans, d->chunks, d->offs, d->vals, d->segs, d->items, d->red_pattern, d->red_ptr, d->red_slots};
+    for (void* p : ptrs)
+        if (p) (void)hipFree(p);
+    *d = PackedDev{};
+}
+
 disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
     d->g = h.g;
     d->n_entries = (int64_t)h.t_in.size();
@@ -98,6 +148,9 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
         if (e != hipSuccess) return hip_fail(e, "hipMemcpy(psi entries)");
     }
     d->bytes = (int64_t)(pb + eb);
+    disco_status_t s = upload_packed(h, &d->packed);
+    if (s != DISCO_OK) return s;
+    d->bytes += d->packed.bytes;
     return DISCO_OK;
 }
 
@@ -106,6 +159,7 @@ void free_op(DeviceOp* d) {
     if (d->entries) (void)hipFree(d->entries);
     d->pat_ptr = nullptr;
     d->entries = nullptr;
+    free_packed(&d->packed);
 }
 
 int64_t numel(const disco_tensor_t* t) {
@@ -182,14 +236,15 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
     a.op = &op; a.x = x->data; a.w = w->data; a.y = y->data; a.dtype = x->dtype;
     a.B = (int)B; a.Ci = (int)Ci; a.Co = (int)Co; a.w_trans = transpose; a.stream = stream;
 
-    if (algo == DISCO_ALGO_AUTO || algo == DISCO_ALGO_FUSED) {
-        // Channel mixing goes to the grid with fewer (pixels x channels) of
-        // intermediate planes.
+    if (algo == DISCO_ALGO_AUTO) {
+        // Channel mixing goes first when the op upsamples into more (pixels x
+        // channels) than it reads; otherwise the fused gather + contraction.
         const double gtc = (double)Ci * g.nlat_o * g.nlon_o;
         const double ctg = (double)Co * g.nlat_i * g.nlon_i;
-        algo = ctg < gtc ? DISCO_ALGO_CONTRACT_THEN_GATHER : DISCO_ALGO_GATHER_THEN_CONTRACT;
+        algo = ctg < gtc ? DISCO_ALGO_CONTRACT_THEN_GATHER : DISCO_ALGO_FUSED;
     }
     const size_t ws = algo == DISCO_ALGO_CONTRACT_THEN_GATHER ? workspace_bytes_contract_then_gather(a)
+                      : algo == DISCO_ALGO_FUSED              ? workspace_bytes_fused(a)
                                                               : workspace_bytes_gather_then_contract(a);
     int cur = 0;
     if (hipGetDevice(&cur) != hipSuccess) return fail(DISCO_ERR_DEVICE, "hipGetDevice failed");
@@ -199,11 +254,15 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
 
     if (fault_inject_alloc()) return fail(DISCO_ERR_OUT_OF_MEMORY, "allocation failure injected (DISCO_FAULT_INJECT=alloc)");
     float* ws_ptr = nullptr;
-    hipError_t e = hipMallocAsync((void**)&ws_ptr, std::max<size_t>(ws, 256), stream);
-    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(workspace)");
+    hipError_t e = hipSuccess;
+    if (ws > 0) {
+        e = hipMallocAsync((void**)&ws_ptr, ws, stream);
+        if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(workspace)");
+    }
     e = algo == DISCO_ALGO_CONTRACT_THEN_GATHER ? launch_contract_then_gather(a, ws_ptr)
+        : algo == DISCO_ALGO_FUSED              ? launch_fused(a, ws_ptr)
                                                 : launch_gather_then_contract(a, ws_ptr);
-    hipError_t e2 = hipFreeAsync(ws_ptr, stream);
+    hipError_t e2 = ws_ptr ? hipFreeAsync(ws_ptr, stream) : hipSuccess;
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     if (e2 != hipSuccess) return hip_fail(e2, "hipFreeAsync(workspace)");
     return ok();

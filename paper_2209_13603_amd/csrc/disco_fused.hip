@@ -1,0 +1,325 @@
+// disco_fused.hip -- the LDS-staged sparse gather of Sec. 4.2's compressed
+// product (eq. "memory_compression") fused with the channel contraction.
+//
+// One workgroup = 256 lanes = 256 consecutive output longitudes q of one
+// pattern (output ring, phase) of a work item, for one batch element and one
+// tile of output channels.  For each pass over kCIC input channels and each
+// chunk of the pattern:
+//   1. the chunk's spans of input-ring longitudes are copied from HBM into LDS
+//      as float4 groups of 4 channels (coalesced along longitude, wrapping at
+//      the 0 / 2 pi seam once per span, bf16 widened to fp32);
+//   2. entries are visited in hat-cell order; an entry's offset and its (at
+//      most four) non-zero basis values are wave-uniform, so each lane reads
+//      its input with ds_read_b128 at (stride * lane + offset) and does
+//      exactly the FMAs of the basis functions that can be non-zero in that
+//      cell, into Z[c][k] registers;
+//   3. after the pass, Z is contracted with W (staged in LDS) into the output
+//      channel accumulators.
+// The accumulation order of a lane depends only on the pattern, never on q, so
+// whole-pixel longitude shifts commute with the op bitwise, and runs are
+// deterministic.  Patterns cut into several segments write partial outputs
+// to workspace slots; k_reduce_partials sums them in slot order.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "disco_internal.h"
+
+namespace disco {
+
+namespace {
+
+constexpr int kBlock = kTileQ;
+constexpr int kNCQ = kCIC / 4;  // float4 channel groups per pass
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float load_val(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float load_val(const uint16_t* p, int64_t i) {
+    return __uint_as_float((uint32_t)p[i] << 16);
+}
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ void store_val(float* p, int64_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void store_val(uint16_t* p, int64_t i, float v) { p[i] = to_bf16(v); }
+
+__host__ __device__ constexpr int cell_first(int c) { return c == 0 ? 0 : c - 1; }
+__host__ __device__ constexpr int cell_count(int c) { return (c == 0 || c == 3) ? 1 : 2; }
+
+// Blocks are dispatched round-robin over the 8 XCDs; remap so that each XCD
+// walks a contiguous range of work items (neighbouring output rings share
+// input rings, which then stay in that XCD's L2).
+__device__ __forceinline__ int xcd_remap(int bid, int nb) {
+    const int xcd = bid & 7, local = bid >> 3;
+    const int per = nb >> 3, rem = nb & 7;
+    return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
+}
+
+// FMAs of one entry of hat cell CELL: z[c][k] += v_n * x[c] for the cell's
+// (at most four) nodes k, all indices compile-time.
+template <int CELL>
+__device__ __forceinline__ void fma_cell(const float4& v, const float4 (&xv)[kNCQ],
+                                         float (&z)[kCIC][kBasis]) {
+    constexpr int CU = CELL / 4, CV = CELL % 4;
+    constexpr int A0 = cell_first(CU), NA = cell_count(CU);
+    constexpr int B0 = cell_first(CV), NB = cell_count(CV);
+    const float vn[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int ia = 0; ia < NA; ++ia)
+#pragma unroll
+        for (int ib = 0; ib < NB; ++ib) {
+            const float vv = vn[ia * NB + ib];
+            const int k = 3 * (A0 + ia) + (B0 + ib);
+#pragma unroll
+            for (int g = 0; g < kNCQ; ++g) {
+                z[4 * g + 0][k] = fmaf(vv, xv[g].x, z[4 * g + 0][k]);
+                z[4 * g + 1][k] = fmaf(vv, xv[g].y, z[4 * g + 1][k]);
+                z[4 * g + 2][k] = fmaf(vv, xv[g].z, z[4 * g + 2][k]);
+                z[4 * g + 3][k] = fmaf(vv, xv[g].w, z[4 * g + 3][k]);
+            }
+        }
+}
+
+// Entries [eb, ee) of one cell, all staged in LDS; four at a time so that
+// the LDS reads of several entries are in flight together.
+template <int CELL>
+__device__ __forceinline__ void run_cell(int eb, int ee, const int* __restrict__ eoffs,
+                                         const float4* __restrict__ evs,
+                                         const float4* __restrict__ xs, int lane_col,
+                                         float (&z)[kCIC][kBasis]) {
+    int e = eb;
+    for (; e + 4 <= ee; e += 4) {
+        int o[4];
+        float4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            o[u] = eoffs[e + u];
+            v[u] = evs[e + u];
+        }
+        float4 xv[4][kNCQ];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int g = 0; g < kNCQ; ++g) xv[u][g] = xs[g * kLdsCols + lane_col + o[u]];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) fma_cell<CELL>(v[u], xv[u], z);
+    }
+    for (; e < ee; ++e) {
+        const int o = eoffs[e];
+        const float4 v = evs[e];
+        float4 xv[kNCQ];
+#pragma unroll
+        for (int g = 0; g < kNCQ; ++g) xv[g] = xs[g * kLdsCols + lane_col + o];
+        fma_cell<CELL>(v, xv, z);
+    }
+}
+
+template <typename T, int COT>
+__global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ items,
+                                                  const PSeg* __restrict__ segs,
+                                                  const PChunk* __restrict__ chunks,
+                                                  const PSpan* __restrict__ spans,
+                                                  const int32_t* __restrict__ offs,
+                                                  const PVal* __restrict__ vals, OpGeom g,
+                                                  const T* __restrict__ x, const T* __restrict__ w,
+                                                  T* __restrict__ y, float* __restrict__ partial,
+                                                  int Ci, int Co, int n_qtiles, int n_cotiles,
+                                                  bool w_trans) {
+    __shared__ float4 xs[kNCQ * kLdsCols];
+    __shared__ float4 evs[kChunkEntries];
+    __shared__ int eoffs[kChunkEntries];
+    __shared__ float ws[kCIC * kBasis * COT];
+
+    const int tid = threadIdx.x;
+    const int bid = xcd_remap(blockIdx.x, gridDim.x);
+    const int item = bid / n_qtiles;
+    const int qt = bid - item * n_qtiles;
+    const int b = blockIdx.y / n_cotiles;
+    const int co0 = (blockIdx.y - b * n_cotiles) * COT;
+    const int q0 = qt * kBlock;
+    const int q = q0 + tid;
+    const int lane_col = g.stride * tid;
+    const int64_t n_in = (int64_t)g.nlat_i * g.nlon_i;
+    const int64_t n_out = (int64_t)g.nlat_o * g.nlon_o;
+    const PItem it = items[item];
+
+    for (int si = it.seg_begin; si < it.seg_end; ++si) {
+        const PSeg sg = segs[si];
+        v4f yacc[COT / 4];
+#pragma unroll
+        for (int j = 0; j < COT / 4; ++j) yacc[j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int ci0 = 0; ci0 < Ci; ci0 += kCIC) {
+            float z[kCIC][kBasis];
+#pragma unroll
+            for (int c = 0; c < kCIC; ++c)
+#pragma unroll
+                for (int k = 0; k < kBasis; ++k) z[c][k] = 0.0f;
+            __syncthreads();  // previous users of ws / xs are done
+            for (int i = tid; i < kCIC * kBasis * COT; i += kBlock) {
+                // ws[j][c][k]: output channel j of the tile, pass channel c, basis k.
+                const int j = i / (kCIC * kBasis), ck = i % (kCIC * kBasis), c = ck / kBasis, k = ck % kBasis;
+                const int co = co0 + j, ci = ci0 + c;
+                float v = 0.0f;
+                if (co < Co && ci < Ci) {
+                    const int64_t idx = w_trans ? ((int64_t)ci * Co + co) * kBasis + k
+                                                : ((int64_t)co * Ci + ci) * kBasis + k;
+                    v = load_val(w, idx);
+                }
+                ws[i] = v;
+            }
+            for (int ch = sg.chunk_begin; ch < sg.chunk_end; ++ch) {
+                const PChunk C = chunks[ch];
+                if (ch != sg.chunk_begin) __syncthreads();  // readers of the previous chunk
+                for (int sp = C.span_begin; sp < C.span_end; ++sp) {
+                    const PSpan S = spans[sp];
+                    int start = (g.stride * q0 + S.dstart) % g.nlon_i;
+                    if (start < 0) start += g.nlon_i;
+                    for (int j = tid; j < S.len; j += kBlock) {
+                        int idx = start + j;
+                        if (idx >= g.nlon_i) idx = idx % g.nlon_i;
+#pragma unroll
+                        for (int gq = 0; gq < kNCQ; ++gq) {
+                            float4 v;
+                            const int c = ci0 + 4 * gq;
+                            const T* xp = x + ((int64_t)b * Ci) * n_in + S.row + idx;
+                            v.x = c + 0 < Ci ? load_val(xp, (int64_t)(c + 0) * n_in) : 0.0f;
+                            v.y = c + 1 < Ci ? load_val(xp, (int64_t)(c + 1) * n_in) : 0.0f;
+                            v.z = c + 2 < Ci ? load_val(xp, (int64_t)(c + 2) * n_in) : 0.0f;
+                            v.w = c + 3 < Ci ? load_val(xp, (int64_t)(c + 3) * n_in) : 0.0f;
+                            xs[gq * kLdsCols + S.lds_base + j] = v;
+                        }
+                    }
+                }
+                {
+                    const int ebase = C.cls[0], ne = C.cls[kCells] - C.cls[0];
+                    for (int i = tid; i < ne; i += kBlock) {
+                        eoffs[i] = offs[ebase + i];
+                        const PVal pv = vals[ebase + i];
+                        evs[i] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
+                    }
+                }
+                __syncthreads();
+                run_cell<0>(C.cls[0] - C.cls[0], C.cls[1] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<1>(C.cls[1] - C.cls[0], C.cls[2] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<2>(C.cls[2] - C.cls[0], C.cls[3] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<3>(C.cls[3] - C.cls[0], C.cls[4] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<4>(C.cls[4] - C.cls[0], C.cls[5] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<5>(C.cls[5] - C.cls[0], C.cls[6] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<6>(C.cls[6] - C.cls[0], C.cls[7] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<7>(C.cls[7] - C.cls[0], C.cls[8] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<8>(C.cls[8] - C.cls[0], C.cls[9] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<9>(C.cls[9] - C.cls[0], C.cls[10] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<10>(C.cls[10] - C.cls[0], C.cls[11] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<11>(C.cls[11] - C.cls[0], C.cls[12] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<12>(C.cls[12] - C.cls[0], C.cls[13] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<13>(C.cls[13] - C.cls[0], C.cls[14] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<14>(C.cls[14] - C.cls[0], C.cls[15] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                run_cell<15>(C.cls[15] - C.cls[0], C.cls[16] - C.cls[0], eoffs, evs, xs, lane_col, z);
+            }
+            if (sg.chunk_begin == sg.chunk_end) __syncthreads();  // ws visible
+            // Contraction of this pass on the matrix cores:
+            //   y[co][q] += sum_{c,k} W(co, ci0 + c, k) Z[c][k][q].
+            // v_mfma_f32_4x4x1_16b_f32 treats the wave as 16 blocks of 4
+            // lanes; block b computes D[i][j] += A[i] B[j] with lane 4b + i
+            // supplying A[i] and lane 4b + j supplying B[j].  With A[i] =
+            // W(co0 + 4 quad + i, kk) and B[j] = Z[kk] of lane 4b + j's own
+            // pixel, lane l ends with y[co0 + 4 quad + r][its pixel] in
+            // register r: one instruction per (kk, 4 output channels).
+            {
+                const int li = tid & 3;
+#pragma unroll
+                for (int qd = 0; qd < COT / 4; ++qd) {
+                    const float* wrow = ws + (4 * qd + li) * (kCIC * kBasis);
+#pragma unroll
+                    for (int c = 0; c < kCIC; ++c)
+#pragma unroll
+                        for (int k = 0; k < kBasis; ++k)
+                            yacc[qd] = __builtin_amdgcn_mfma_f32_4x4x1f32(wrow[c * kBasis + k], z[c][k],
+                                                                         yacc[qd], 0, 0, 0);
+                }
+            }
+        }
+        if (q < g.nq) {
+            const int to = sg.pattern / g.P, r = sg.pattern - (sg.pattern / g.P) * g.P;
+            if (sg.slot < 0) {
+                const int64_t pix = (int64_t)to * g.nlon_o + (int64_t)q * g.P + r;
+#pragma unroll
+                for (int j = 0; j < COT; ++j)
+                    if (co0 + j < Co) store_val(y, ((int64_t)b * Co + co0 + j) * n_out + pix, yacc[j / 4][j % 4]);
+            } else {
+                const int B = gridDim.y / n_cotiles;
+#pragma unroll
+                for (int j = 0; j < COT; ++j)
+                    if (co0 + j < Co)
+                        partial[(((int64_t)sg.slot * B + b) * Co + co0 + j) * g.nq + q] = yacc[j / 4][j % 4];
+            }
+        }
+    }
+}
+
+// y of split patterns = sum of their partial slots, in slot order.
+// grid: (ceil(nq / 256), n_split, B * Co)
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_reduce_partials(const int32_t* __restrict__ red_pattern,
+                                                            const int32_t* __restrict__ red_ptr,
+                                                            const int32_t* __restrict__ red_slots,
+                                                            const float* __restrict__ partial,
+                                                            OpGeom g, T* __restrict__ y, int B, int Co) {
+    const int q = blockIdx.x * kBlock + threadIdx.x;
+    const int sp = blockIdx.y;
+    const int b = blockIdx.z / Co, co = blockIdx.z - (blockIdx.z / Co) * Co;
+    if (q >= g.nq) return;
+    const int pat = red_pattern[sp];
+    const int to = pat / g.P, r = pat - (pat / g.P) * g.P;
+    const int s0 = red_ptr[sp], s1 = red_ptr[sp + 1];
+    const int64_t n_out = (int64_t)g.nlat_o * g.nlon_o;
+    const int64_t pix = (int64_t)to * g.nlon_o + (int64_t)q * g.P + r;
+    float acc = 0.0f;
+    for (int s = s0; s < s1; ++s) acc += partial[(((int64_t)red_slots[s] * B + b) * Co + co) * g.nq + q];
+    store_val(y, ((int64_t)b * Co + co) * n_out + pix, acc);
+}
+
+template <typename T, int COT>
+hipError_t fused_launch(const ExecArgs& a, float* partial) {
+    const OpGeom& g = a.op->g;
+    const PackedDev& P = a.op->packed;
+    const int n_qtiles = (g.nq + kBlock - 1) / kBlock;
+    const int n_cot = (a.Co + COT - 1) / COT;
+    dim3 grid((unsigned)(P.n_items * n_qtiles), (unsigned)(a.B * n_cot));
+    int tk = timing_begin("fused_gather_contract", a.stream);
+    hipLaunchKernelGGL((k_fused<T, COT>), grid, dim3(kBlock), 0, a.stream, P.items, P.segs, P.chunks,
+                       P.spans, P.offs, P.vals, g, (const T*)a.x, (const T*)a.w, (T*)a.y, partial, a.Ci,
+                       a.Co, n_qtiles, n_cot, a.w_trans);
+    timing_end(tk, a.stream);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || P.n_split == 0) return e;
+    dim3 grid2((unsigned)((g.nq + kBlock - 1) / kBlock), (unsigned)P.n_split, (unsigned)(a.B * a.Co));
+    tk = timing_begin("reduce_partials", a.stream);
+    hipLaunchKernelGGL((k_reduce_partials<T>), grid2, dim3(kBlock), 0, a.stream, P.red_pattern,
+                       P.red_ptr, P.red_slots, partial, g, (T*)a.y, a.B, a.Co);
+    timing_end(tk, a.stream);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t fused_dispatch(const ExecArgs& a, float* partial) {
+    if (a.Co <= 4) return fused_launch<T, 4>(a, partial);
+    if (a.Co <= 8) return fused_launch<T, 8>(a, partial);
+    if (a.Co <= 16) return fused_launch<T, 16>(a, partial);
+    return fused_launch<T, 32>(a, partial);
+}
+
+}  // namespace
+
+size_t workspace_bytes_fused(const ExecArgs& a) {
+    return sizeof(float) * (size_t)a.op->packed.n_slots * a.B * a.Co * a.op->g.nq;
+}
+
+hipError_t launch_fused(const ExecArgs& a, float* partial_ws) {
+    return a.dtype == 1 ? fused_dispatch<uint16_t>(a, partial_ws) : fused_dispatch<float>(a, partial_ws);
+}
+
+}  // namespace disco

@@ -40,6 +40,8 @@ struct HostOp {
     std::vector<int32_t> pat_ptr;  // n_patterns + 1
     std::vector<int32_t> t_in;     // per entry: input ring
     std::vector<int32_t> d;        // per entry: offset in [0, nlon_i)
+    std::vector<int32_t> d_raw;    // per entry: unwrapped offset (contiguous along a window)
+    std::vector<uint8_t> cell;     // per entry: hat cell 4 * cu + cv, cu, cv in [0, 4)
     std::vector<float> val;        // per entry: 9 values, psi_k * q(input ring)
     int32_t max_window = 0;
     int32_t full_ring_windows = 0;
@@ -49,6 +51,60 @@ struct HostOp {
 // Returns 0 on success, otherwise a disco_status_t with *err set.
 int make_op_geom(const PlanParams& p, bool transpose, OpGeom* g, std::string* err);
 int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* err);
+
+// ---------------------------------------------------------------------------
+// Packed layout for the LDS-staged fused kernel (disco_fused.hip).
+//
+// A workgroup owns kTileQ consecutive output longitudes q of one pattern
+// (output ring, phase), one lane per q.  The pattern's entries are cut into
+// chunks; a chunk lists spans of input-ring longitudes that are staged into
+// LDS together (channel-interleaved), and its entries are sorted by hat cell
+// so that each entry touches exactly the basis functions that can be non-zero
+// there.  Consecutive chunks of a pattern form a segment; a pattern with
+// several segments ("split") accumulates partial outputs in a workspace slot
+// per segment that a second kernel sums in a fixed order.  Work items are runs
+// of consecutive segments with a bounded number of entries.
+constexpr int kTileQ = 256;    // output longitudes per workgroup
+constexpr int kCIC = 8;        // input channels per staging pass
+constexpr int kLdsCols = 1024; // staged input longitudes per chunk (per channel)
+constexpr int kChunkEntries = 512;  // entries staged in LDS per chunk
+constexpr int kCells = 16;
+
+struct PSpan { int32_t row, dstart, len, lds_base; };            // row = ring * nlon_i
+struct PChunk { int32_t span_begin, span_end, cls[kCells + 1], pad; };
+struct PEntry { int32_t off; float v[4]; };                       // off: LDS column at lane 0
+struct PVal { float v[4]; };                                      // device: values, SoA with offsets
+struct PSeg { int32_t pattern, chunk_begin, chunk_end, slot; };   // slot -1: writes y
+struct PItem { int32_t seg_begin, seg_end; };
+static_assert(sizeof(PChunk) == 80, "PChunk layout");
+static_assert(sizeof(PEntry) == 20, "PEntry layout");
+
+struct PackedHost {
+    std::vector<PSpan> spans;
+    std::vector<PChunk> chunks;
+    std::vector<PEntry> entries;
+    std::vector<PSeg> segs;
+    std::vector<PItem> items;
+    std::vector<int32_t> red_pattern;   // split patterns
+    std::vector<int32_t> red_ptr;       // CSR over red_slots, size red_pattern + 1
+    std::vector<int32_t> red_slots;     // slots of each split pattern, in summation order
+    int32_t n_slots = 0;
+};
+int pack_op(const HostOp& op, int target_entries, PackedHost* out, std::string* err);
+
+struct PackedDev {
+    PSpan* spans = nullptr;
+    PChunk* chunks = nullptr;
+    int32_t* offs = nullptr;     // per entry: LDS column at lane 0
+    PVal* vals = nullptr;        // per entry: non-zero basis values of its cell
+    PSeg* segs = nullptr;
+    PItem* items = nullptr;
+    int32_t* red_pattern = nullptr;
+    int32_t* red_ptr = nullptr;
+    int32_t* red_slots = nullptr;
+    int32_t n_items = 0, n_split = 0, n_slots = 0;
+    int64_t bytes = 0;
+};
 
 // Device-side layout of one op (see disco_kernels.hip).
 struct DevEntry {
@@ -61,6 +117,7 @@ static_assert(sizeof(DevEntry) == 48, "DevEntry is 12 dwords");
 
 struct DeviceOp {
     OpGeom g{};
+    PackedDev packed;
     int32_t* pat_ptr = nullptr;  // device, n_patterns + 1
     DevEntry* entries = nullptr;  // device
     int64_t n_entries = 0;
@@ -90,5 +147,7 @@ hipError_t launch_gather_then_contract(const ExecArgs& a, float* z_ws);
 hipError_t launch_contract_then_gather(const ExecArgs& a, float* xc_ws);
 size_t workspace_bytes_gather_then_contract(const ExecArgs& a);
 size_t workspace_bytes_contract_then_gather(const ExecArgs& a);
+hipError_t launch_fused(const ExecArgs& a, float* partial_ws);
+size_t workspace_bytes_fused(const ExecArgs& a);
 
 }  // namespace disco

@@ -114,7 +114,7 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
     for (int t = 0; t < g.nlat_i; ++t) { sin_i[t] = std::sin(colat(t, g.nlat_i)); cos_i[t] = std::cos(colat(t, g.nlat_i)); }
 
     op->pat_ptr.assign(1, 0);
-    op->t_in.clear(); op->d.clear(); op->val.clear();
+    op->t_in.clear(); op->d.clear(); op->d_raw.clear(); op->cell.clear(); op->val.clear();
     op->max_window = 0; op->full_ring_windows = 0; op->nnz_pairs = 0;
 
     for (int to = 0; to < g.nlat_o; ++to) {
@@ -183,8 +183,14 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
                     if (!any) continue;
                     int64_t dnorm = dd % g.nlon_i;
                     if (dnorm < 0) dnorm += g.nlon_i;
+                    // Hat cell containing (u, v): cell c spans [(c-2) h, (c-1) h);
+                    // only the nodes on its corners can be non-zero there.
+                    const int cu = std::min(3, std::max(0, (int)std::floor(u / h) + 2));
+                    const int cv = std::min(3, std::max(0, (int)std::floor(v / h) + 2));
                     op->t_in.push_back(ti);
                     op->d.push_back((int32_t)dnorm);
+                    op->d_raw.push_back((int32_t)dd);
+                    op->cell.push_back((uint8_t)(4 * cu + cv));
                     op->val.insert(op->val.end(), vals, vals + kBasis);
                     op->nnz_pairs += (int64_t)nzk * g.nq;
                     ++kept;

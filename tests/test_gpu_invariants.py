@@ -13,7 +13,7 @@ from paper_2209_13603_amd import disco, synth
 
 pytestmark = pytest.mark.gpu
 
-ALGOS = ["gather_then_contract", "contract_then_gather"]
+ALGOS = ["gather_then_contract", "contract_then_gather", "fused"]
 
 
 @pytest.mark.parametrize("algo", ALGOS)

@@ -28,7 +28,7 @@ SMALL = [
     (40, 80, 40, 80),       # not a multiple of the 256-lane tile
     (33, 300, 33, 300),     # ragged tail over two tiles
 ]
-ALGOS = ["gather_then_contract", "contract_then_gather"]
+ALGOS = ["gather_then_contract", "contract_then_gather", "fused"]
 
 
 @pytest.mark.parametrize("algo", ALGOS)
