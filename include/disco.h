@@ -73,7 +73,9 @@ typedef enum {
     DISCO_ALGO_AUTO = 0,
     DISCO_ALGO_GATHER_THEN_CONTRACT = 1, /* psi gather -> Z workspace -> W contraction */
     DISCO_ALGO_CONTRACT_THEN_GATHER = 2, /* W contraction on the input grid -> psi gather */
-    DISCO_ALGO_FUSED = 3                 /* gather and contraction in one kernel, no workspace */
+    DISCO_ALGO_FUSED = 3,       /* gather and contraction in one kernel; rings whose windows
+                                   wrap whole input rings take the exact spectral (DFT) form */
+    DISCO_ALGO_FUSED_DIRECT = 4 /* the fused kernel for every ring (no spectral form) */
 } disco_algo_t;
 
 typedef struct {
@@ -101,6 +103,8 @@ typedef struct {
     int64_t nnz_pairs_total;   /* non-zero (output pixel, input pixel, k) triples, forward */
     int64_t psi_bytes;         /* device bytes held by the plan */
     double h;                  /* node spacing actually used */
+    int32_t spectral_rings_forward;   /* output rings of the forward op on the spectral path */
+    int32_t spectral_rings_transpose; /* ... of the transposed op */
 } disco_plan_info_t;
 
 /* Builds the sparse psi tensors of the forward and transposed ops on the host

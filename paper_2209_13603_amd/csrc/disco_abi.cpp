@@ -88,10 +88,41 @@ disco_status_t upload_vec(const std::vector<V>& v, V** dst, int64_t* bytes, cons
 // Entries per work item of the fused kernel (balances workgroups).
 constexpr int kTargetEntries = 512;
 
-disco_status_t upload_packed(const HostOp& h, PackedDev* d) {
+// Output rings with at least this many entries take the spectral path
+// (environment DISCO_SPECTRAL_MIN_ENTRIES overrides, for tuning).
+int spectral_min_entries() {
+    const char* v = std::getenv("DISCO_SPECTRAL_MIN_ENTRIES");
+    if (v && *v) return std::max(1, std::atoi(v));
+    return 128;
+}
+
+disco_status_t upload_spectral(const SpectralHost& S, SpectralDev* d) {
+    disco_status_t s;
+    if ((s = upload_vec(S.rings, &d->rings, &d->bytes, "hipMalloc(spectral rings)")) != DISCO_OK) return s;
+    if ((s = upload_vec(S.pair_ptr, &d->pair_ptr, &d->bytes, "hipMalloc(spectral pairs)")) != DISCO_OK) return s;
+    if ((s = upload_vec(S.pair_slot, &d->pair_slot, &d->bytes, "hipMalloc(spectral pairs)")) != DISCO_OK) return s;
+    if ((s = upload_vec(S.slot_ring, &d->slot_ring, &d->bytes, "hipMalloc(spectral slots)")) != DISCO_OK) return s;
+    if ((s = upload_vec(S.vs, &d->vs, &d->bytes, "hipMalloc(spectral psi)")) != DISCO_OK) return s;
+    if ((s = upload_vec(S.tw, &d->tw, &d->bytes, "hipMalloc(twiddles)")) != DISCO_OK) return s;
+    d->N = S.N;
+    d->M = S.M;
+    d->n_rings = (int)S.rings.size();
+    d->n_pairs = (int)S.pair_slot.size();
+    d->n_slots = (int)S.slot_ring.size();
+    return DISCO_OK;
+}
+
+void free_spectral(SpectralDev* d) {
+    void* ptrs[] = {d->rings, d->pair_ptr, d->pair_slot, d->slot_ring, d->vs, d->tw};
+    for (void* p : ptrs)
+        if (p) (void)hipFree(p);
+    *d = SpectralDev{};
+}
+
+disco_status_t upload_packed(const HostOp& h, const std::vector<uint8_t>& skip, PackedDev* d) {
     PackedHost P;
     std::string err;
-    int rc = pack_op(h, kTargetEntries, &P, &err);
+    int rc = pack_op(h, kTargetEntries, skip, &P, &err);
     if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
     disco_status_t s;
     if ((s = upload_vec(P.spans, &d->spans, &d->bytes, "hipMalloc(spans)")) != DISCO_OK) return s;
@@ -148,9 +179,19 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
         if (e != hipSuccess) return hip_fail(e, "hipMemcpy(psi entries)");
     }
     d->bytes = (int64_t)(pb + eb);
-    disco_status_t s = upload_packed(h, &d->packed);
+    disco_status_t s = upload_packed(h, {}, &d->packed);
     if (s != DISCO_OK) return s;
     d->bytes += d->packed.bytes;
+    SpectralHost sp;
+    std::vector<uint8_t> heavy;
+    std::string err;
+    int rc = build_spectral(h, spectral_min_entries(), &sp, &heavy, &err);
+    if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
+    if (!sp.rings.empty()) {
+        if ((s = upload_spectral(sp, &d->spectral)) != DISCO_OK) return s;
+        if ((s = upload_packed(h, heavy, &d->packed_light)) != DISCO_OK) return s;
+        d->bytes += d->spectral.bytes + d->packed_light.bytes;
+    }
     return DISCO_OK;
 }
 
@@ -160,6 +201,8 @@ void free_op(DeviceOp* d) {
     d->pat_ptr = nullptr;
     d->entries = nullptr;
     free_packed(&d->packed);
+    free_packed(&d->packed_light);
+    free_spectral(&d->spectral);
 }
 
 int64_t numel(const disco_tensor_t* t) {
@@ -197,7 +240,7 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
                    disco_tensor_t* y, hipStream_t stream, int32_t algo, bool transpose) {
     if (!plan) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (!x || !w || !y) return fail(DISCO_ERR_INVALID_ARGUMENT, "tensor descriptor is NULL");
-    if (algo < DISCO_ALGO_AUTO || algo > DISCO_ALGO_FUSED) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown algo");
+    if (algo < DISCO_ALGO_AUTO || algo > DISCO_ALGO_FUSED_DIRECT) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown algo");
     const DeviceOp& op = transpose ? plan->tr : plan->fwd;
     const OpGeom& g = op.g;
     if (x->ndim != 4 || y->ndim != 4 || w->ndim != 3)
@@ -243,9 +286,17 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
         const double ctg = (double)Co * g.nlat_i * g.nlon_i;
         algo = ctg < gtc ? DISCO_ALGO_CONTRACT_THEN_GATHER : DISCO_ALGO_FUSED;
     }
-    const size_t ws = algo == DISCO_ALGO_CONTRACT_THEN_GATHER ? workspace_bytes_contract_then_gather(a)
-                      : algo == DISCO_ALGO_FUSED              ? workspace_bytes_fused(a)
-                                                              : workspace_bytes_gather_then_contract(a);
+    const bool spectral = algo == DISCO_ALGO_FUSED && op.spectral.n_rings > 0;
+    const PackedDev& packed = spectral ? op.packed_light : op.packed;
+    size_t ws_spec = 0, ws = 0;
+    if (algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {
+        ws = workspace_bytes_contract_then_gather(a);
+    } else if (algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
+        ws = workspace_bytes_gather_then_contract(a);
+    } else {
+        ws_spec = spectral ? (workspace_bytes_spectral(a) + 255) / 256 * 256 : 0;
+        ws = ws_spec + workspace_bytes_fused(a, packed);
+    }
     int cur = 0;
     if (hipGetDevice(&cur) != hipSuccess) return fail(DISCO_ERR_DEVICE, "hipGetDevice failed");
     if (cur != plan->device && hipSetDevice(plan->device) != hipSuccess)
@@ -259,9 +310,14 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
         e = hipMallocAsync((void**)&ws_ptr, ws, stream);
         if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(workspace)");
     }
-    e = algo == DISCO_ALGO_CONTRACT_THEN_GATHER ? launch_contract_then_gather(a, ws_ptr)
-        : algo == DISCO_ALGO_FUSED              ? launch_fused(a, ws_ptr)
-                                                : launch_gather_then_contract(a, ws_ptr);
+    if (algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {
+        e = launch_contract_then_gather(a, ws_ptr);
+    } else if (algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
+        e = launch_gather_then_contract(a, ws_ptr);
+    } else {
+        e = spectral ? launch_spectral(a, ws_ptr) : hipSuccess;
+        if (e == hipSuccess) e = launch_fused(a, packed, (float*)((char*)ws_ptr + ws_spec));
+    }
     hipError_t e2 = ws_ptr ? hipFreeAsync(ws_ptr, stream) : hipSuccess;
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     if (e2 != hipSuccess) return hip_fail(e2, "hipFreeAsync(workspace)");
@@ -392,6 +448,8 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
     I.nnz_pairs_total = hf.nnz_pairs;
     I.psi_bytes = plan->fwd.bytes + plan->tr.bytes;
     I.h = p.h;
+    I.spectral_rings_forward = plan->fwd.spectral.n_rings;
+    I.spectral_rings_transpose = plan->tr.spectral.n_rings;
     *plan_out = plan;
     return ok();
 }

@@ -283,9 +283,9 @@ __global__ __launch_bounds__(kBlock) void k_reduce_partials(const int32_t* __res
 }
 
 template <typename T, int COT>
-hipError_t fused_launch(const ExecArgs& a, float* partial) {
+hipError_t fused_launch(const ExecArgs& a, const PackedDev& P, float* partial) {
     const OpGeom& g = a.op->g;
-    const PackedDev& P = a.op->packed;
+    if (P.n_items == 0) return hipSuccess;
     const int n_qtiles = (g.nq + kBlock - 1) / kBlock;
     const int n_cot = (a.Co + COT - 1) / COT;
     dim3 grid((unsigned)(P.n_items * n_qtiles), (unsigned)(a.B * n_cot));
@@ -305,21 +305,21 @@ hipError_t fused_launch(const ExecArgs& a, float* partial) {
 }
 
 template <typename T>
-hipError_t fused_dispatch(const ExecArgs& a, float* partial) {
-    if (a.Co <= 4) return fused_launch<T, 4>(a, partial);
-    if (a.Co <= 8) return fused_launch<T, 8>(a, partial);
-    if (a.Co <= 16) return fused_launch<T, 16>(a, partial);
-    return fused_launch<T, 32>(a, partial);
+hipError_t fused_dispatch(const ExecArgs& a, const PackedDev& P, float* partial) {
+    if (a.Co <= 4) return fused_launch<T, 4>(a, P, partial);
+    if (a.Co <= 8) return fused_launch<T, 8>(a, P, partial);
+    if (a.Co <= 16) return fused_launch<T, 16>(a, P, partial);
+    return fused_launch<T, 32>(a, P, partial);
 }
 
 }  // namespace
 
-size_t workspace_bytes_fused(const ExecArgs& a) {
-    return sizeof(float) * (size_t)a.op->packed.n_slots * a.B * a.Co * a.op->g.nq;
+size_t workspace_bytes_fused(const ExecArgs& a, const PackedDev& P) {
+    return sizeof(float) * (size_t)P.n_slots * a.B * a.Co * a.op->g.nq;
 }
 
-hipError_t launch_fused(const ExecArgs& a, float* partial_ws) {
-    return a.dtype == 1 ? fused_dispatch<uint16_t>(a, partial_ws) : fused_dispatch<float>(a, partial_ws);
+hipError_t launch_fused(const ExecArgs& a, const PackedDev& P, float* partial_ws) {
+    return a.dtype == 1 ? fused_dispatch<uint16_t>(a, P, partial_ws) : fused_dispatch<float>(a, P, partial_ws);
 }
 
 }  // namespace disco

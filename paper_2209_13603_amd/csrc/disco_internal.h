@@ -43,6 +43,7 @@ struct HostOp {
     std::vector<int32_t> d_raw;    // per entry: unwrapped offset (contiguous along a window)
     std::vector<uint8_t> cell;     // per entry: hat cell 4 * cu + cv, cu, cv in [0, 4)
     std::vector<float> val;        // per entry: 9 values, psi_k * q(input ring)
+    std::vector<double> val64;     // the same values before rounding to fp32
     int32_t max_window = 0;
     int32_t full_ring_windows = 0;
     int64_t nnz_pairs = 0;  // non-zero (output pixel, input pixel, k) triples
@@ -90,7 +91,45 @@ struct PackedHost {
     std::vector<int32_t> red_slots;     // slots of each split pattern, in summation order
     int32_t n_slots = 0;
 };
-int pack_op(const HostOp& op, int target_entries, PackedHost* out, std::string* err);
+// skip[pattern] != 0 leaves the pattern out of the segments and work items
+// (its output is produced elsewhere); skip may be empty.
+int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& skip, PackedHost* out,
+            std::string* err);
+
+// ---------------------------------------------------------------------------
+// Spectral path for heavy output rings (disco_spectral_plan.cpp, disco_spectral.hip).
+//
+// When an output ring's windows wrap whole input rings, its sum over one
+// input ring is a circular cross-correlation along longitude (Sec. 4.2: the
+// pattern is shift invariant), computed exactly through the discrete Fourier
+// transform:  Yhat[co][m] = sum_{t_i, ci} Xhat[t_i][ci][m]
+//   * sum_k W[co][ci][k] conj(Vhat_k[t_o, t_i][m]).
+// East-west mirror symmetry of the 3x3 basis gives Vhat_{3a+2} =
+// conj(Vhat_{3a}) and a real Vhat_{3a+1}, so each (ring pair, frequency)
+// stores 9 floats: Re/Im Vhat_{3a} and Re Vhat_{3a+1} for a = 0, 1, 2.
+struct SpectralHost {
+    int N = 0, M = 0;                 // ring length and M = N / 2
+    std::vector<int32_t> rings;       // heavy output rings
+    std::vector<int32_t> pair_ptr;    // CSR over pairs, size rings + 1
+    std::vector<int32_t> pair_slot;   // input-ring slot of each pair
+    std::vector<int32_t> slot_ring;   // input ring of each slot
+    std::vector<float> vs;            // [pair][9][M + 1], scaled by 1 / N
+    std::vector<float> tw;            // [N / 2][2]: exp(-2 pi i t / N)
+};
+// Fills *sp (possibly with no rings) and marks heavy patterns in *heavy.
+int build_spectral(const HostOp& op, int min_entries, SpectralHost* sp, std::vector<uint8_t>* heavy,
+                   std::string* err);
+
+struct SpectralDev {
+    int N = 0, M = 0, n_rings = 0, n_pairs = 0, n_slots = 0;
+    int32_t* rings = nullptr;
+    int32_t* pair_ptr = nullptr;
+    int32_t* pair_slot = nullptr;
+    int32_t* slot_ring = nullptr;
+    float* vs = nullptr;
+    float* tw = nullptr;
+    int64_t bytes = 0;
+};
 
 struct PackedDev {
     PSpan* spans = nullptr;
@@ -117,7 +156,9 @@ static_assert(sizeof(DevEntry) == 48, "DevEntry is 12 dwords");
 
 struct DeviceOp {
     OpGeom g{};
-    PackedDev packed;
+    PackedDev packed;        // every pattern through the direct kernel
+    PackedDev packed_light;  // patterns not handled by the spectral path
+    SpectralDev spectral;
     int32_t* pat_ptr = nullptr;  // device, n_patterns + 1
     DevEntry* entries = nullptr;  // device
     int64_t n_entries = 0;
@@ -147,7 +188,9 @@ hipError_t launch_gather_then_contract(const ExecArgs& a, float* z_ws);
 hipError_t launch_contract_then_gather(const ExecArgs& a, float* xc_ws);
 size_t workspace_bytes_gather_then_contract(const ExecArgs& a);
 size_t workspace_bytes_contract_then_gather(const ExecArgs& a);
-hipError_t launch_fused(const ExecArgs& a, float* partial_ws);
-size_t workspace_bytes_fused(const ExecArgs& a);
+hipError_t launch_fused(const ExecArgs& a, const PackedDev& P, float* partial_ws);
+size_t workspace_bytes_fused(const ExecArgs& a, const PackedDev& P);
+hipError_t launch_spectral(const ExecArgs& a, float* ws);
+size_t workspace_bytes_spectral(const ExecArgs& a);
 
 }  // namespace disco

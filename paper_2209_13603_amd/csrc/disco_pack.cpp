@@ -23,7 +23,8 @@ struct Piece {
 
 }  // namespace
 
-int pack_op(const HostOp& op, int target_entries, PackedHost* out, std::string* err) {
+int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& skip, PackedHost* out,
+            std::string* err) {
     const OpGeom& g = op.g;
     const int s = g.stride;
     const int halo = s * (kTileQ - 1);  // extra columns a tile reads beyond one entry
@@ -36,6 +37,7 @@ int pack_op(const HostOp& op, int target_entries, PackedHost* out, std::string* 
     std::vector<int32_t> pattern_seg_count(g.n_patterns(), 0);
 
     for (int pat = 0; pat < g.n_patterns(); ++pat) {
+        if (!skip.empty() && skip[(size_t)pat]) continue;
         const int32_t e0 = op.pat_ptr[(size_t)pat], e1 = op.pat_ptr[(size_t)pat + 1];
         // 1. Pieces: runs of one input ring with a bounded offset extent.
         std::vector<Piece> pieces;

@@ -114,7 +114,7 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
     for (int t = 0; t < g.nlat_i; ++t) { sin_i[t] = std::sin(colat(t, g.nlat_i)); cos_i[t] = std::cos(colat(t, g.nlat_i)); }
 
     op->pat_ptr.assign(1, 0);
-    op->t_in.clear(); op->d.clear(); op->d_raw.clear(); op->cell.clear(); op->val.clear();
+    op->t_in.clear(); op->d.clear(); op->d_raw.clear(); op->cell.clear(); op->val.clear(); op->val64.clear();
     op->max_window = 0; op->full_ring_windows = 0; op->nnz_pairs = 0;
 
     for (int to = 0; to < g.nlat_o; ++to) {
@@ -170,13 +170,15 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
                     double u = 0.0, v = 0.0;
                     if (rho > 0.0) { u = Th * xs / rho; v = Th * ys / rho; }
                     float vals[kBasis];
+                    double vals64[kBasis];
                     bool any = false;
                     int nzk = 0;
                     for (int a = 0; a < 3; ++a) {
                         const double ha = hat(u / h - (a - 1));
                         for (int b = 0; b < 3; ++b) {
                             const double psi = ha * hat(v / h - (b - 1));
-                            vals[3 * a + b] = (float)(psi * q[ti]);
+                            vals64[3 * a + b] = psi * q[ti];
+                            vals[3 * a + b] = (float)vals64[3 * a + b];
                             if (psi != 0.0) { any = true; ++nzk; }
                         }
                     }
@@ -192,6 +194,7 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
                     op->d_raw.push_back((int32_t)dd);
                     op->cell.push_back((uint8_t)(4 * cu + cv));
                     op->val.insert(op->val.end(), vals, vals + kBasis);
+                    op->val64.insert(op->val64.end(), vals64, vals64 + kBasis);
                     op->nnz_pairs += (int64_t)nzk * g.nq;
                     ++kept;
                 }

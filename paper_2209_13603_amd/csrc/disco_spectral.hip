@@ -1,0 +1,256 @@
+// disco_spectral.hip -- the spectral path for heavy output rings.
+//
+// Near the poles an output ring's windows span whole input rings, so its sum
+// over one input ring is a circular cross-correlation along longitude
+// (Sec. 4.2: one pattern reused at every output longitude).  Three kernels
+// evaluate it exactly through the DFT (N = nlon, M = N / 2, power of two):
+//   k_rfft_rings : Xhat of every input ring a heavy ring reads (real N-point
+//                  DFT as an M-point complex Stockham FFT in LDS + split),
+//   k_spectral   : Yhat[co][m] = sum_{t_i, ci} Xhat[t_i][ci][m] sum_k W[co][ci][k]
+//                  conj(Vhat_k[m]), using Vhat_{3a+2} = conj(Vhat_{3a}) and
+//                  real Vhat_{3a+1} (9 stored floats per pair and frequency),
+//   k_irfft_rings: y of each heavy ring from Yhat (inverse real DFT).
+// Vhat is precomputed on the host in fp64 and scaled by 1 / N; the device
+// transforms are unnormalised.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "disco_internal.h"
+
+namespace disco {
+
+namespace {
+
+constexpr int kFftBlock = 256;
+constexpr int kSpecC = 2;  // input channels per accumulation pass of k_spectral
+
+__device__ __forceinline__ float load_val(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float load_val(const uint16_t* p, int64_t i) {
+    return __uint_as_float((uint32_t)p[i] << 16);
+}
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ void store_val(float* p, int64_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void store_val(uint16_t* p, int64_t i, float v) { p[i] = to_bf16(v); }
+
+__device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
+__device__ __forceinline__ float2 csub(float2 a, float2 b) { return make_float2(a.x - b.x, a.y - b.y); }
+__device__ __forceinline__ float2 cmul(float2 a, float2 b) {
+    return make_float2(fmaf(a.x, b.x, -a.y * b.y), fmaf(a.x, b.y, a.y * b.x));
+}
+__device__ __forceinline__ float2 conjf2(float2 a) { return make_float2(a.x, -a.y); }
+
+// M-point complex FFT (M a power of two) in LDS, radix-2 Stockham autosort
+// between buffers a and b; sign -1 (forward) or +1 (inverse, unnormalised).
+// tw[t] = exp(-2 pi i t / (2M)); stage with sub-transform length Ls uses
+// exp(-2 pi i k / (2 Ls)) = tw[k M / Ls].  Returns the buffer with the result.
+__device__ float2* fft_lds(float2* a, float2* b, int M, const float2* __restrict__ tw, bool inverse) {
+    const int half = M >> 1;
+    for (int Ls = 1; Ls < M; Ls <<= 1) {
+        const int tstep = M / Ls;
+        for (int j = threadIdx.x; j < half; j += blockDim.x) {
+            const int k = j & (Ls - 1);
+            float2 w = tw[k * tstep];
+            if (inverse) w.y = -w.y;
+            const float2 c0 = a[j];
+            const float2 c1 = cmul(a[j + half], w);
+            const int o = ((j - k) << 1) + k;
+            b[o] = cadd(c0, c1);
+            b[o + Ls] = csub(c0, c1);
+        }
+        __syncthreads();
+        float2* t = a;
+        a = b;
+        b = t;
+    }
+    return a;
+}
+
+// Xhat[slot][b][ci][m], m in [0, M]: real DFT of ring slot_ring[slot] of x.
+// grid: (n_slots, B * Ci)
+template <typename T>
+__global__ __launch_bounds__(kFftBlock) void k_rfft_rings(const int32_t* __restrict__ slot_ring,
+                                                         const T* __restrict__ x, const float2* __restrict__ tw,
+                                                         float2* __restrict__ xh, int B, int Ci, int nlat, int M) {
+    extern __shared__ float2 sm[];
+    float2* a = sm;
+    float2* bb = sm + M;
+    const int slot = blockIdx.x;
+    const int b = blockIdx.y / Ci, ci = blockIdx.y - (blockIdx.y / Ci) * Ci;
+    const int N = 2 * M;
+    const T* row = x + (((int64_t)b * Ci + ci) * nlat + slot_ring[slot]) * N;
+    for (int j = threadIdx.x; j < M; j += blockDim.x)
+        a[j] = make_float2(load_val(row, 2 * j), load_val(row, 2 * j + 1));
+    __syncthreads();
+    const float2* Z = fft_lds(a, bb, M, tw, false);
+    float2* out = xh + (((int64_t)slot * B + b) * Ci + ci) * (M + 1);
+    for (int m = threadIdx.x; m <= M; m += blockDim.x) {
+        const float2 zm = Z[m & (M - 1)];
+        const float2 zc = conjf2(Z[(M - m) & (M - 1)]);
+        const float2 e = make_float2(0.5f * (zm.x + zc.x), 0.5f * (zm.y + zc.y));
+        const float2 dif = csub(zm, zc);
+        const float2 o = make_float2(0.5f * dif.y, -0.5f * dif.x);  // (zm - zc) / (2i)
+        const float2 w = m < M ? tw[m] : make_float2(-1.0f, 0.0f);
+        out[m] = cadd(e, cmul(w, o));
+    }
+}
+
+// Yhat[h][b][co][m] for heavy ring h.  grid: (ceil((M+1)/256), n_rings, B * n_cotiles)
+template <typename T, int COT>
+__global__ __launch_bounds__(kFftBlock) void k_spectral(const int32_t* __restrict__ pair_ptr,
+                                                       const int32_t* __restrict__ pair_slot,
+                                                       const float* __restrict__ vs,
+                                                       const float2* __restrict__ xh,
+                                                       const T* __restrict__ w, float2* __restrict__ yh,
+                                                       int B, int Ci, int Co, int M, int n_cotiles,
+                                                       bool w_trans) {
+    const int m = blockIdx.x * kFftBlock + threadIdx.x;
+    const int h = blockIdx.y;
+    const int b = blockIdx.z / n_cotiles;
+    const int co0 = (blockIdx.z - b * n_cotiles) * COT;
+    if (m > M) return;
+    const int p0 = pair_ptr[h], p1 = pair_ptr[h + 1];
+    const int64_t vstride = (int64_t)(M + 1);
+    float2 Y[COT];
+#pragma unroll
+    for (int j = 0; j < COT; ++j) Y[j] = make_float2(0.0f, 0.0f);
+    for (int ci0 = 0; ci0 < Ci; ci0 += kSpecC) {
+        float2 E[kSpecC][3], F[kSpecC][3], G[kSpecC][3];
+#pragma unroll
+        for (int c = 0; c < kSpecC; ++c)
+#pragma unroll
+            for (int a = 0; a < 3; ++a) {
+                E[c][a] = make_float2(0.0f, 0.0f);
+                F[c][a] = make_float2(0.0f, 0.0f);
+                G[c][a] = make_float2(0.0f, 0.0f);
+            }
+        for (int p = p0; p < p1; ++p) {
+            const float* v = vs + (int64_t)p * 9 * vstride + m;
+            float V[9];
+#pragma unroll
+            for (int i = 0; i < 9; ++i) V[i] = v[i * vstride];
+            const float2* xr = xh + (((int64_t)pair_slot[p] * B + b) * Ci) * vstride + m;
+#pragma unroll
+            for (int c = 0; c < kSpecC; ++c) {
+                const float2 X = ci0 + c < Ci ? xr[(int64_t)(ci0 + c) * vstride] : make_float2(0.0f, 0.0f);
+#pragma unroll
+                for (int a = 0; a < 3; ++a) {
+                    E[c][a].x = fmaf(V[3 * a + 0], X.x, E[c][a].x);
+                    E[c][a].y = fmaf(V[3 * a + 0], X.y, E[c][a].y);
+                    F[c][a].x = fmaf(V[3 * a + 1], X.x, F[c][a].x);
+                    F[c][a].y = fmaf(V[3 * a + 1], X.y, F[c][a].y);
+                    G[c][a].x = fmaf(V[3 * a + 2], X.x, G[c][a].x);
+                    G[c][a].y = fmaf(V[3 * a + 2], X.y, G[c][a].y);
+                }
+            }
+        }
+        // Yhat[co] += sum_{c,a} (W_3a + W_3a+2) E + i (W_3a+2 - W_3a) F + W_3a+1 G
+#pragma unroll
+        for (int j = 0; j < COT; ++j) {
+            const int co = co0 + j < Co ? co0 + j : Co - 1;
+#pragma unroll
+            for (int c = 0; c < kSpecC; ++c) {
+                const int ci = ci0 + c < Ci ? ci0 + c : Ci - 1;  // E, F, G are zero past Ci
+                const int64_t base = w_trans ? ((int64_t)ci * Co + co) * kBasis : ((int64_t)co * Ci + ci) * kBasis;
+#pragma unroll
+                for (int a = 0; a < 3; ++a) {
+                    const float w0 = load_val(w, base + 3 * a), w1 = load_val(w, base + 3 * a + 1),
+                                w2 = load_val(w, base + 3 * a + 2);
+                    const float S = w0 + w2, D = w2 - w0;
+                    Y[j].x = fmaf(S, E[c][a].x, fmaf(-D, F[c][a].y, fmaf(w1, G[c][a].x, Y[j].x)));
+                    Y[j].y = fmaf(S, E[c][a].y, fmaf(D, F[c][a].x, fmaf(w1, G[c][a].y, Y[j].y)));
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < COT; ++j)
+        if (co0 + j < Co) yh[(((int64_t)h * B + b) * Co + co0 + j) * vstride + m] = Y[j];
+}
+
+// y[b][co][ring][:] = inverse real DFT of Yhat[h][b][co][:].  grid: (n_rings, B * Co)
+template <typename T>
+__global__ __launch_bounds__(kFftBlock) void k_irfft_rings(const int32_t* __restrict__ rings,
+                                                          const float2* __restrict__ yh,
+                                                          const float2* __restrict__ tw, T* __restrict__ y,
+                                                          int B, int Co, int nlat_o, int M) {
+    extern __shared__ float2 sm[];
+    float2* a = sm;
+    float2* bb = sm + M;
+    const int h = blockIdx.x;
+    const int b = blockIdx.y / Co, co = blockIdx.y - (blockIdx.y / Co) * Co;
+    const float2* Y = yh + (((int64_t)h * B + b) * Co + co) * (M + 1);
+    for (int m = threadIdx.x; m < M; m += blockDim.x) {
+        const float2 xm = Y[m];
+        const float2 xc = conjf2(Y[M - m]);
+        const float2 e = cadd(xm, xc);
+        const float2 o = cmul(csub(xm, xc), conjf2(tw[m]));
+        a[m] = make_float2(e.x - o.y, e.y + o.x);  // e + i o
+    }
+    __syncthreads();
+    const float2* z = fft_lds(a, bb, M, tw, true);
+    const int N = 2 * M;
+    const int64_t base = (((int64_t)b * Co + co) * nlat_o + rings[h]) * N;
+    for (int j = threadIdx.x; j < M; j += blockDim.x) {
+        const float2 v = z[j];
+        store_val(y, base + 2 * j, v.x);
+        store_val(y, base + 2 * j + 1, v.y);
+    }
+}
+
+template <typename T, int COT>
+hipError_t spectral_launch(const ExecArgs& a, float* ws) {
+    const SpectralDev& S = a.op->spectral;
+    const OpGeom& g = a.op->g;
+    const int M = S.M;
+    float2* xh = (float2*)ws;
+    float2* yh = xh + (size_t)S.n_slots * a.B * a.Ci * (M + 1);
+    const size_t lds = sizeof(float2) * 2 * (size_t)M;
+    int tk = timing_begin("spectral_rfft", a.stream);
+    hipLaunchKernelGGL((k_rfft_rings<T>), dim3(S.n_slots, a.B * a.Ci), dim3(kFftBlock), lds, a.stream,
+                       S.slot_ring, (const T*)a.x, (const float2*)S.tw, xh, a.B, a.Ci, g.nlat_i, M);
+    timing_end(tk, a.stream);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int n_cot = (a.Co + COT - 1) / COT;
+    tk = timing_begin("spectral_mac", a.stream);
+    hipLaunchKernelGGL((k_spectral<T, COT>), dim3((M + 1 + kFftBlock - 1) / kFftBlock, S.n_rings, a.B * n_cot),
+                       dim3(kFftBlock), 0, a.stream, S.pair_ptr, S.pair_slot, S.vs, xh, (const T*)a.w, yh,
+                       a.B, a.Ci, a.Co, M, n_cot, a.w_trans);
+    timing_end(tk, a.stream);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    tk = timing_begin("spectral_irfft", a.stream);
+    hipLaunchKernelGGL((k_irfft_rings<T>), dim3(S.n_rings, a.B * a.Co), dim3(kFftBlock), lds, a.stream,
+                       S.rings, yh, (const float2*)S.tw, (T*)a.y, a.B, a.Co, g.nlat_o, M);
+    timing_end(tk, a.stream);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t spectral_dispatch(const ExecArgs& a, float* ws) {
+    if (a.Co <= 4) return spectral_launch<T, 4>(a, ws);
+    if (a.Co <= 8) return spectral_launch<T, 8>(a, ws);
+    if (a.Co <= 16) return spectral_launch<T, 16>(a, ws);
+    return spectral_launch<T, 32>(a, ws);
+}
+
+}  // namespace
+
+size_t workspace_bytes_spectral(const ExecArgs& a) {
+    const SpectralDev& S = a.op->spectral;
+    if (S.n_rings == 0) return 0;
+    return sizeof(float2) * (size_t)(S.M + 1) * a.B * ((size_t)S.n_slots * a.Ci + (size_t)S.n_rings * a.Co);
+}
+
+hipError_t launch_spectral(const ExecArgs& a, float* ws) {
+    if (a.op->spectral.n_rings == 0) return hipSuccess;
+    return a.dtype == 1 ? spectral_dispatch<uint16_t>(a, ws) : spectral_dispatch<float>(a, ws);
+}
+
+}  // namespace disco

@@ -33,8 +33,10 @@ ALGO_AUTO = 0
 ALGO_GATHER_THEN_CONTRACT = 1
 ALGO_CONTRACT_THEN_GATHER = 2
 ALGO_FUSED = 3
+ALGO_FUSED_DIRECT = 4
 ALGOS = {"auto": ALGO_AUTO, "gather_then_contract": ALGO_GATHER_THEN_CONTRACT,
-         "contract_then_gather": ALGO_CONTRACT_THEN_GATHER, "fused": ALGO_FUSED}
+         "contract_then_gather": ALGO_CONTRACT_THEN_GATHER, "fused": ALGO_FUSED,
+         "fused_direct": ALGO_FUSED_DIRECT}
 
 # Every exported symbol declared in include/disco.h.
 EXPORTS = ("disco_plan_create", "disco_plan_destroy", "disco_plan_query", "disco_forward",
@@ -67,7 +69,8 @@ class PlanInfo(ctypes.Structure):
                 ("max_window", ctypes.c_int32), ("full_ring_windows", ctypes.c_int32),
                 ("nnz_entries", ctypes.c_int64), ("nnz_entries_transpose", ctypes.c_int64),
                 ("nnz_pairs_total", ctypes.c_int64), ("psi_bytes", ctypes.c_int64),
-                ("h", ctypes.c_double)]
+                ("h", ctypes.c_double), ("spectral_rings_forward", ctypes.c_int32),
+                ("spectral_rings_transpose", ctypes.c_int32)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

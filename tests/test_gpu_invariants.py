@@ -13,12 +13,21 @@ from paper_2209_13603_amd import disco, synth
 
 pytestmark = pytest.mark.gpu
 
-ALGOS = ["gather_then_contract", "contract_then_gather", "fused"]
+ALGOS = ["gather_then_contract", "contract_then_gather", "fused", "fused_direct"]
+
+
+def _same(got, ref, algo):
+    """Direct gathers commute with whole-pixel shifts bitwise; the spectral
+    (DFT) form of the fused path does so in exact arithmetic, to fp32 rounding."""
+    if algo == "fused":
+        return np.abs(got - ref).max() <= 1e-6 * np.abs(ref).max()
+    return np.array_equal(got, ref)
 
 
 @pytest.mark.parametrize("algo", ALGOS)
 @pytest.mark.parametrize("case", [(32, 64, 32, 64), (64, 128, 32, 64), (32, 64, 64, 128)])
-def test_shift_equivariance_bitwise(case, algo):
+def test_shift_equivariance_bitwise(case, algo, monkeypatch):
+    monkeypatch.setenv("DISCO_SPECTRAL_MIN_ENTRIES", "8")
     a, b, c, d = case
     tc = 3 * math.pi / min(a, c)
     plan = disco.Plan(a, b, c, d, tc)
@@ -30,14 +39,14 @@ def test_shift_equivariance_bitwise(case, algo):
     else:
         s, m_in, m_out = d // b, 3, 3 * (d // b)
     ys, _ = run_gpu(None, np.roll(x, m_in, axis=-1), w, "forward", algo=algo, plan=plan)
-    assert np.array_equal(ys, np.roll(y, m_out, axis=-1))
+    assert _same(ys, np.roll(y, m_out, axis=-1), algo)
     # Transposed op: a shift of its input by m shifts its output by the ratio.
     xT, wT = synth.random_inputs(22, (2, 4, c, d), (4, 3, 9))
     yT, _ = run_gpu(None, xT, wT, "transpose", algo=algo, plan=plan)
     m_in = 2 if b % d == 0 else 2 * (d // b)
     m_out = 2 * (b // d) if b % d == 0 else 2
     ysT, _ = run_gpu(None, np.roll(xT, m_in, axis=-1), wT, "transpose", algo=algo, plan=plan)
-    assert np.array_equal(ysT, np.roll(yT, m_out, axis=-1))
+    assert _same(ysT, np.roll(yT, m_out, axis=-1), algo)
     plan.close()
 
 

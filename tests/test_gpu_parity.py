@@ -28,7 +28,7 @@ SMALL = [
     (40, 80, 40, 80),       # not a multiple of the 256-lane tile
     (33, 300, 33, 300),     # ragged tail over two tiles
 ]
-ALGOS = ["gather_then_contract", "contract_then_gather", "fused"]
+ALGOS = ["gather_then_contract", "contract_then_gather", "fused", "fused_direct"]
 
 
 @pytest.mark.parametrize("algo", ALGOS)
@@ -89,3 +89,32 @@ def test_workload_up256x512_to_512x1024_bf16():
 
 def test_workload_sphere2048x4096():
     _workload_check("sphere2048x4096", pix_per_ring=4)
+
+
+SPECTRAL = [(32, 64, 32, 64), (64, 128, 64, 128), (48, 128, 48, 128), (20, 256, 20, 256)]
+
+
+@pytest.mark.parametrize("case", SPECTRAL, ids=lambda c: "%dx%d" % c[:2])
+@pytest.mark.parametrize("op", ["forward", "transpose"])
+def test_spectral_path_small_grids(case, op, monkeypatch):
+    """Rings on the spectral (DFT) path, forced down to 8 entries so that most
+    rings of these small grids take it, against the oracle in full."""
+    monkeypatch.setenv("DISCO_SPECTRAL_MIN_ENTRIES", "8")
+    a, b, c, d = case
+    tc = 3 * math.pi / min(a, c)
+    plan = disco.Plan(a, b, c, d, tc)
+    info = plan.info()
+    key = "spectral_rings_forward" if op == "forward" else "spectral_rings_transpose"
+    assert info[key] > 0
+    B, Ci, Co = 2, 3, 5
+    xs = (B, Ci, a, b) if op == "forward" else (B, Ci, c, d)
+    ws = (Co, Ci, 9) if op == "forward" else (Ci, Co, 9)
+    x, w = synth.random_inputs(8, xs, ws)
+    say("spectral", case, op, info[key], "rings")
+    y, _ = run_gpu(None, x, w, op, algo="fused", plan=plan)
+    ref = run_oracle((a, b, c, d, tc), x, w, op)
+    err = rel_l2(y, ref)
+    say("  rel_l2 %.3e" % err)
+    assert err <= FP32_TOL
+    assert np.abs(y - ref).max() <= 1e-5 * np.abs(ref).max()
+    plan.close()
