@@ -146,6 +146,33 @@ disco_status_t upload_packed(const HostOp& h, const std::vector<uint8_t>& skip, 
     return DISCO_OK;
 }
 
+// Cost of one sweep run (entries plus fixed per-pattern work).
+constexpr int kSweepTarget = 768;
+
+disco_status_t upload_sweep(const SweepHost& H, SweepDev* d) {
+    disco_status_t s;
+    std::vector<int32_t> offs(H.entries.size());
+    std::vector<PVal> vals(H.entries.size());
+    for (size_t i = 0; i < H.entries.size(); ++i) {
+        offs[i] = H.entries[i].off;
+        for (int k = 0; k < 4; ++k) vals[i].v[k] = H.entries[i].v[k];
+    }
+    if ((s = upload_vec(H.runs, &d->runs, &d->bytes, "hipMalloc(sweep runs)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.pats, &d->pats, &d->bytes, "hipMalloc(sweep patterns)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.acts, &d->acts, &d->bytes, "hipMalloc(sweep spans)")) != DISCO_OK) return s;
+    if ((s = upload_vec(offs, &d->offs, &d->bytes, "hipMalloc(sweep offsets)")) != DISCO_OK) return s;
+    if ((s = upload_vec(vals, &d->vals, &d->bytes, "hipMalloc(sweep values)")) != DISCO_OK) return s;
+    d->n_runs = (int32_t)H.runs.size();
+    return DISCO_OK;
+}
+
+void free_sweep(SweepDev* d) {
+    void* ptrs[] = {d->runs, d->pats, d->acts, d->offs, d->vals};
+    for (void* p : ptrs)
+        if (p) (void)hipFree(p);
+    *d = SweepDev{};
+}
+
 void free_packed(PackedDev* d) {
     void* ptrs[] = {d->spans, d->chunks, d->offs, d->vals, d->segs, d->items, d->red_pattern, d->red_ptr, d->red_slots};
     for (void* p : ptrs)
@@ -192,6 +219,17 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
         if ((s = upload_packed(h, heavy, &d->packed_light)) != DISCO_OK) return s;
         d->bytes += d->spectral.bytes + d->packed_light.bytes;
     }
+    // Sweep runs over the light patterns; the rest go to the general kernel.
+    SweepHost sw;
+    rc = pack_sweep(h, kSweepTarget, heavy, &sw, &err);
+    if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
+    if (!sw.runs.empty()) {
+        std::vector<uint8_t> rest_skip(sw.covered);
+        for (size_t i = 0; i < rest_skip.size() && i < heavy.size(); ++i) rest_skip[i] |= heavy[i];
+        if ((s = upload_sweep(sw, &d->sweep)) != DISCO_OK) return s;
+        if ((s = upload_packed(h, rest_skip, &d->packed_rest)) != DISCO_OK) return s;
+        d->bytes += d->sweep.bytes + d->packed_rest.bytes;
+    }
     return DISCO_OK;
 }
 
@@ -202,7 +240,9 @@ void free_op(DeviceOp* d) {
     d->entries = nullptr;
     free_packed(&d->packed);
     free_packed(&d->packed_light);
+    free_packed(&d->packed_rest);
     free_spectral(&d->spectral);
+    free_sweep(&d->sweep);
 }
 
 int64_t numel(const disco_tensor_t* t) {
@@ -287,7 +327,8 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
         algo = ctg < gtc ? DISCO_ALGO_CONTRACT_THEN_GATHER : DISCO_ALGO_FUSED;
     }
     const bool spectral = algo == DISCO_ALGO_FUSED && op.spectral.n_rings > 0;
-    const PackedDev& packed = spectral ? op.packed_light : op.packed;
+    const bool sweep = algo == DISCO_ALGO_FUSED && op.sweep.n_runs > 0 && Ci <= kCIC;
+    const PackedDev& packed = sweep ? op.packed_rest : spectral ? op.packed_light : op.packed;
     size_t ws_spec = 0, ws = 0;
     if (algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {
         ws = workspace_bytes_contract_then_gather(a);
@@ -316,6 +357,7 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
         e = launch_gather_then_contract(a, ws_ptr);
     } else {
         e = spectral ? launch_spectral(a, ws_ptr) : hipSuccess;
+        if (e == hipSuccess && sweep) e = launch_sweep(a);
         if (e == hipSuccess) e = launch_fused(a, packed, (float*)((char*)ws_ptr + ws_spec));
     }
     hipError_t e2 = ws_ptr ? hipFreeAsync(ws_ptr, stream) : hipSuccess;

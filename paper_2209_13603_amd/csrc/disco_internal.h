@@ -97,6 +97,44 @@ int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& sk
             std::string* err);
 
 // ---------------------------------------------------------------------------
+// Sweep layout (disco_sweep.hip): a workgroup walks a run of consecutive
+// patterns for one 256-longitude tile, keeping the spans of the input rings
+// the run reads resident in LDS slots; before each pattern it stages only the
+// rings first needed there (into slots whose previous ring is no longer
+// read).  Used for patterns with at most kChunkEntries entries when every
+// input channel fits one staging pass (Ci <= kCIC).
+constexpr int kSweepCols = 1280;  // LDS columns (per channel) of all slots of a run
+constexpr int kSweepEntries = 256;  // entries of one pattern on the sweep path
+
+struct SRun { int32_t pat_begin, pat_end; };             // [begin, end) into SPat
+struct SPat {
+    int32_t pattern;
+    int32_t act_begin, act_end;  // spans to stage before this pattern (PSpan)
+    int32_t cls[kCells + 1];     // entries, sorted by hat cell
+};
+static_assert(sizeof(SPat) == 80, "SPat layout");
+
+struct SweepHost {
+    std::vector<SRun> runs;
+    std::vector<SPat> pats;
+    std::vector<PSpan> acts;
+    std::vector<PEntry> entries;
+    std::vector<uint8_t> covered;  // per pattern: handled by a run
+};
+int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& skip, SweepHost* out,
+               std::string* err);
+
+struct SweepDev {
+    SRun* runs = nullptr;
+    SPat* pats = nullptr;
+    PSpan* acts = nullptr;
+    int32_t* offs = nullptr;
+    PVal* vals = nullptr;
+    int32_t n_runs = 0;
+    int64_t bytes = 0;
+};
+
+// ---------------------------------------------------------------------------
 // Spectral path for heavy output rings (disco_spectral_plan.cpp, disco_spectral.hip).
 //
 // When an output ring's windows wrap whole input rings, its sum over one
@@ -159,6 +197,8 @@ struct DeviceOp {
     PackedDev packed;        // every pattern through the direct kernel
     PackedDev packed_light;  // patterns not handled by the spectral path
     SpectralDev spectral;
+    SweepDev sweep;          // light patterns walked by the sweep kernel (Ci <= kCIC)
+    PackedDev packed_rest;   // light patterns the sweep runs do not cover
     int32_t* pat_ptr = nullptr;  // device, n_patterns + 1
     DevEntry* entries = nullptr;  // device
     int64_t n_entries = 0;
@@ -191,6 +231,7 @@ size_t workspace_bytes_contract_then_gather(const ExecArgs& a);
 hipError_t launch_fused(const ExecArgs& a, const PackedDev& P, float* partial_ws);
 size_t workspace_bytes_fused(const ExecArgs& a, const PackedDev& P);
 hipError_t launch_spectral(const ExecArgs& a, float* ws);
+hipError_t launch_sweep(const ExecArgs& a);
 size_t workspace_bytes_spectral(const ExecArgs& a);
 
 }  // namespace disco

@@ -174,3 +174,156 @@ int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& sk
 }
 
 }  // namespace disco
+
+namespace disco {
+
+int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& skip, SweepHost* out,
+               std::string* err) {
+    (void)err;
+    const OpGeom& g = op.g;
+    const int s = g.stride;
+    const int halo = s * (kTileQ - 1);
+    SweepHost H;
+    H.covered.assign((size_t)g.n_patterns(), 0);
+
+    // Per pattern: the input rings it reads with their raw offset ranges.
+    struct RingUse { int32_t ti, dmin, dmax; };
+    auto ring_uses = [&](int pat) {
+        std::vector<RingUse> u;
+        for (int32_t e = op.pat_ptr[(size_t)pat]; e < op.pat_ptr[(size_t)pat + 1]; ++e) {
+            const int32_t ti = op.t_in[(size_t)e], dr = op.d_raw[(size_t)e];
+            if (!u.empty() && u.back().ti == ti) {
+                u.back().dmin = std::min(u.back().dmin, dr);
+                u.back().dmax = std::max(u.back().dmax, dr);
+            } else {
+                u.push_back(RingUse{ti, dr, dr});
+            }
+        }
+        return u;
+    };
+    auto eligible = [&](int pat) {
+        if (!skip.empty() && skip[(size_t)pat]) return false;
+        const int n = op.pat_ptr[(size_t)pat + 1] - op.pat_ptr[(size_t)pat];
+        return n > 0 && n <= kSweepEntries;
+    };
+
+    int pat = 0;
+    const int np = g.n_patterns();
+    while (pat < np) {
+        if (!eligible(pat)) { ++pat; continue; }
+        // Grow a run [pat, end) while its slots fit in kSweepCols and its cost
+        // stays under the target.
+        std::vector<std::vector<RingUse>> uses;
+        int end = pat, cost = 0;
+        for (; end < np && eligible(end); ++end) {
+            std::vector<RingUse> u = ring_uses(end);
+            uses.push_back(u);
+            // Ring ranges over the run so far and live intervals.
+            std::vector<int32_t> first(g.nlat_i, -1), last(g.nlat_i, -1), dmin(g.nlat_i, 0), dmax(g.nlat_i, 0);
+            for (size_t i = 0; i < uses.size(); ++i)
+                for (auto& r : uses[i]) {
+                    if (first[(size_t)r.ti] < 0) { first[(size_t)r.ti] = (int)i; dmin[(size_t)r.ti] = r.dmin; dmax[(size_t)r.ti] = r.dmax; }
+                    last[(size_t)r.ti] = (int)i;
+                    dmin[(size_t)r.ti] = std::min(dmin[(size_t)r.ti], r.dmin);
+                    dmax[(size_t)r.ti] = std::max(dmax[(size_t)r.ti], r.dmax);
+                }
+            int cap = 0, live_max = 0;
+            for (int t = 0; t < g.nlat_i; ++t)
+                if (first[(size_t)t] >= 0) cap = std::max(cap, halo + dmax[(size_t)t] - dmin[(size_t)t] + 1);
+            for (size_t i = 0; i < uses.size(); ++i) {
+                int live = 0;
+                for (int t = 0; t < g.nlat_i; ++t)
+                    if (first[(size_t)t] >= 0 && first[(size_t)t] <= (int)i && last[(size_t)t] >= (int)i) ++live;
+                live_max = std::max(live_max, live);
+            }
+            const int n_e = op.pat_ptr[(size_t)end + 1] - op.pat_ptr[(size_t)end];
+            const int c = n_e + 24 + (int)u.size() * 2;
+            if (end > pat && ((int64_t)live_max * cap > kSweepCols || cost + c > target_cost)) {
+                uses.pop_back();
+                break;
+            }
+            if ((int64_t)live_max * cap > kSweepCols) {  // a lone pattern that does not fit
+                uses.pop_back();
+                break;
+            }
+            cost += c;
+        }
+        if (end == pat) { ++pat; continue; }  // not even one pattern fits: left to the general kernel
+        // Final slot layout of the run [pat, end).
+        const int n = end - pat;
+        std::vector<int32_t> first(g.nlat_i, -1), last(g.nlat_i, -1), dmin(g.nlat_i, 0), dmax(g.nlat_i, 0);
+        for (int i = 0; i < n; ++i)
+            for (auto& r : uses[(size_t)i]) {
+                if (first[(size_t)r.ti] < 0) { first[(size_t)r.ti] = i; dmin[(size_t)r.ti] = r.dmin; dmax[(size_t)r.ti] = r.dmax; }
+                last[(size_t)r.ti] = i;
+                dmin[(size_t)r.ti] = std::min(dmin[(size_t)r.ti], r.dmin);
+                dmax[(size_t)r.ti] = std::max(dmax[(size_t)r.ti], r.dmax);
+            }
+        int cap = 0;
+        for (int t = 0; t < g.nlat_i; ++t)
+            if (first[(size_t)t] >= 0) cap = std::max(cap, halo + dmax[(size_t)t] - dmin[(size_t)t] + 1);
+        std::vector<int32_t> slot(g.nlat_i, -1);
+        std::vector<int32_t> slot_ring;  // ring currently in each slot (-1: free)
+        SRun R{(int32_t)H.pats.size(), 0};
+        for (int i = 0; i < n; ++i) {
+            const int p = pat + i;
+            // Free slots whose ring is no longer read.
+            for (auto& sr : slot_ring)
+                if (sr >= 0 && last[(size_t)sr] < i) sr = -1;
+            SPat SP{};
+            SP.pattern = p;
+            SP.act_begin = (int32_t)H.acts.size();
+            for (auto& r : uses[(size_t)i]) {
+                if (first[(size_t)r.ti] != i) continue;
+                int sl = -1;
+                for (size_t k = 0; k < slot_ring.size(); ++k)
+                    if (slot_ring[k] < 0) { sl = (int)k; break; }
+                if (sl < 0) { sl = (int)slot_ring.size(); slot_ring.push_back(-1); }
+                slot_ring[(size_t)sl] = r.ti;
+                slot[(size_t)r.ti] = sl;
+                H.acts.push_back(PSpan{r.ti * g.nlon_i, dmin[(size_t)r.ti], halo + dmax[(size_t)r.ti] - dmin[(size_t)r.ti] + 1, sl * cap});
+            }
+            SP.act_end = (int32_t)H.acts.size();
+            // Entries, sorted by cell.
+            std::vector<std::pair<int, PEntry>> ents;
+            for (int32_t e = op.pat_ptr[(size_t)p]; e < op.pat_ptr[(size_t)p + 1]; ++e) {
+                const int32_t ti = op.t_in[(size_t)e];
+                const int cell = op.cell[(size_t)e];
+                const int cu = cell / 4, cv = cell % 4;
+                PEntry E{};
+                E.off = slot[(size_t)ti] * cap + (op.d_raw[(size_t)e] - dmin[(size_t)ti]);
+                int k = 0;
+                const float* v9 = &op.val[(size_t)e * kBasis];
+                for (int a = 0; a < 3; ++a)
+                    for (int b = 0; b < 3; ++b) {
+                        const int fa = cu == 0 ? 0 : cu - 1, na = (cu == 0 || cu == 3) ? 1 : 2;
+                        const int fb = cv == 0 ? 0 : cv - 1, nb = (cv == 0 || cv == 3) ? 1 : 2;
+                        if (a >= fa && a < fa + na && b >= fb && b < fb + nb) E.v[k++] = v9[3 * a + b];
+                    }
+                ents.push_back({cell, E});
+            }
+            std::stable_sort(ents.begin(), ents.end(),
+                             [](const std::pair<int, PEntry>& x, const std::pair<int, PEntry>& y) { return x.first < y.first; });
+            const int32_t base = (int32_t)H.entries.size();
+            int k = 0;
+            for (int c = 0; c <= kCells; ++c) {
+                while (k < (int)ents.size() && ents[(size_t)k].first < c) ++k;
+                SP.cls[c] = base + k;
+            }
+            for (auto& pe : ents) H.entries.push_back(pe.second);
+            H.pats.push_back(SP);
+            H.covered[(size_t)p] = 1;
+        }
+        R.pat_end = (int32_t)H.pats.size();
+        if ((int64_t)slot_ring.size() * cap > kSweepCols) {
+            if (err) *err = "internal: sweep slots exceed the LDS budget";
+            return DISCO_ERR_DEVICE;
+        }
+        H.runs.push_back(R);
+        pat = end;
+    }
+    *out = std::move(H);
+    return DISCO_OK;
+}
+
+}  // namespace disco

@@ -18,8 +18,9 @@
 //   y' = sin(ti) sin(dphi)
 //   z' = cos(ti - tj) - 2 sin(ti) sin(tj) sin^2(dphi/2)
 // Theta = atan2(|(x', y')|, z'), (u, v) = Theta (x', y') / |(x', y')|
-// (azimuthal equidistant tangent plane: u south, v east).  Entries whose nine
-// basis values are all zero are dropped.  Values absorb the quadrature weight
+// (azimuthal equidistant tangent plane: u south, v east).  Basis values below
+// 1e-12 (rounding noise where a hat is evaluated at its own zero) are set to
+// zero, and entries whose nine basis values are all zero are dropped.  Values absorb the quadrature weight
 // of the op's input ring (Sec. 4.1: quadrature absorbed into f) and are then
 // rounded to fp32.
 #include <algorithm>
@@ -35,6 +36,8 @@ namespace disco {
 namespace {
 
 constexpr double kPi = 3.14159265358979323846;
+// Basis values below this (the hats are at most 1) are treated as zero.
+constexpr double kPsiFloor = 1e-12;
 
 double colat(int t, int nlat) { return (t + 0.5) * kPi / nlat; }
 
@@ -176,7 +179,11 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
                     for (int a = 0; a < 3; ++a) {
                         const double ha = hat(u / h - (a - 1));
                         for (int b = 0; b < 3; ++b) {
-                            const double psi = ha * hat(v / h - (b - 1));
+                            double psi = ha * hat(v / h - (b - 1));
+                            // A hat evaluated at its own zero (e.g. a point exactly
+                            // two node spacings away) comes out as rounding noise of
+                            // the fp64 geometry (~1e-16); such values are exact zeros.
+                            if (psi < kPsiFloor) psi = 0.0;
                             vals64[3 * a + b] = psi * q[ti];
                             vals[3 * a + b] = (float)vals64[3 * a + b];
                             if (psi != 0.0) { any = true; ++nzk; }

@@ -1,0 +1,345 @@
+// disco_sweep.hip -- the fused gather + contraction walking runs of output
+// rings with the input-ring spans kept resident in LDS.
+//
+// Same arithmetic as disco_fused.hip (Sec. 4.2's compressed product, hat-cell
+// sorted entries, MFMA 4x4x1 channel contraction), organised for light rings:
+// a workgroup owns 256 consecutive output longitudes of every pattern of one
+// run; each input ring the run reads is staged once, into an LDS slot chosen
+// at plan time, and stays there while consecutive patterns read it.  Before
+// each pattern only the rings it reads first are loaded, so an output ring
+// costs one new input-ring span instead of the ~7 its window covers.  All
+// input channels are resident (Ci <= kCIC), so a pattern needs one pass.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "disco_internal.h"
+
+namespace disco {
+
+namespace {
+
+constexpr int kBlock = kTileQ;
+constexpr int kNCQ = kCIC / 4;
+constexpr int kPF = 2;   // prefetched span columns per lane (512 columns)
+static_assert(kSweepEntries % kTileQ == 0, "entry prefetch covers whole lanes");
+constexpr int kPFE = kSweepEntries / kTileQ;  // prefetched entries per lane
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float load_val(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float load_val(const uint16_t* p, int64_t i) {
+    return __uint_as_float((uint32_t)p[i] << 16);
+}
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ void store_val(float* p, int64_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void store_val(uint16_t* p, int64_t i, float v) { p[i] = to_bf16(v); }
+
+__host__ __device__ constexpr int cell_first(int c) { return c == 0 ? 0 : c - 1; }
+__host__ __device__ constexpr int cell_count(int c) { return (c == 0 || c == 3) ? 1 : 2; }
+
+__device__ __forceinline__ int xcd_remap(int bid, int nb) {
+    const int xcd = bid & 7, local = bid >> 3;
+    const int per = nb >> 3, rem = nb & 7;
+    return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
+}
+
+template <int CELL>
+__device__ __forceinline__ void fma_cell(const float4& v, const float4 (&xv)[kNCQ], float (&z)[kCIC][kBasis]) {
+    constexpr int CU = CELL / 4, CV = CELL % 4;
+    constexpr int A0 = cell_first(CU), NA = cell_count(CU);
+    constexpr int B0 = cell_first(CV), NB = cell_count(CV);
+    const float vn[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int ia = 0; ia < NA; ++ia)
+#pragma unroll
+        for (int ib = 0; ib < NB; ++ib) {
+            const float vv = vn[ia * NB + ib];
+            const int k = 3 * (A0 + ia) + (B0 + ib);
+#pragma unroll
+            for (int g = 0; g < kNCQ; ++g) {
+                z[4 * g + 0][k] = fmaf(vv, xv[g].x, z[4 * g + 0][k]);
+                z[4 * g + 1][k] = fmaf(vv, xv[g].y, z[4 * g + 1][k]);
+                z[4 * g + 2][k] = fmaf(vv, xv[g].z, z[4 * g + 2][k]);
+                z[4 * g + 3][k] = fmaf(vv, xv[g].w, z[4 * g + 3][k]);
+            }
+        }
+}
+
+// Entries of one cell, software-pipelined across the flat entry array (cells
+// are contiguous in it, so the entry after e is always e + 1): while the FMAs
+// of entry e run, the input of e + 1 and the offset and values of e + 2 are
+// already in flight.  (o1, v1, x1) hold entry e + 1, (o2, v2) entry e + 2.
+struct Pipe {
+    int o2;
+    float4 v0, v1, v2;
+    float4 x0[kNCQ], x1[kNCQ];
+};
+
+__device__ __forceinline__ void pipe_load(Pipe& p, int e, int ne, const int* __restrict__ eoffs,
+                                          const float4* __restrict__ evs, const float4* __restrict__ xs, int lane_col) {
+    // Advance: entry e + 1 becomes current, e + 2 becomes next.
+    p.v0 = p.v1;
+#pragma unroll
+    for (int g = 0; g < kNCQ; ++g) p.x0[g] = p.x1[g];
+    p.v1 = p.v2;
+    if (e + 1 < ne) {
+#pragma unroll
+        for (int g = 0; g < kNCQ; ++g) p.x1[g] = xs[g * kSweepCols + lane_col + p.o2];
+    }
+    if (e + 2 < ne) {
+        p.o2 = eoffs[e + 2];
+        p.v2 = evs[e + 2];
+    }
+}
+
+template <int CELL>
+__device__ __forceinline__ void run_cell(int& e, int ee, int ne, Pipe& p, const int* __restrict__ eoffs,
+                                         const float4* __restrict__ evs, const float4* __restrict__ xs,
+                                         int lane_col, float (&z)[kCIC][kBasis]) {
+    for (; e < ee; ++e) {
+        pipe_load(p, e, ne, eoffs, evs, xs, lane_col);
+        fma_cell<CELL>(p.v0, p.x0, z);
+    }
+}
+
+constexpr int kKK = kCIC * kBasis;    // contraction length of one pass (72)
+constexpr int kWG = (kKK + 15) / 16;  // W registers per 4 output channels
+
+// y[co][pixel] += sum_kk W(co, kk) Z[kk][pixel] for kk = KK.., one
+// v_mfma_f32_4x4x1_16b_f32 per (kk, 4 output channels); A is broadcast from
+// block kk % 16 (CBSZ = 4, ABID = kk % 16) of register wv[qd][kk / 16].
+template <int KK, int NQ>
+__device__ __forceinline__ void mfma_contract(v4f (&yacc)[NQ], const float (&wv)[NQ][kWG],
+                                              const float (&z)[kCIC][kBasis]) {
+    if constexpr (KK < kKK) {
+#pragma unroll
+        for (int qd = 0; qd < NQ; ++qd)
+            yacc[qd] = __builtin_amdgcn_mfma_f32_4x4x1f32(wv[qd][KK / 16], z[KK / kBasis][KK % kBasis], yacc[qd], 4,
+                                                         KK % 16, 0);
+        mfma_contract<KK + 1, NQ>(yacc, wv, z);
+    }
+}
+
+// grid: (n_runs * n_qtiles, B * n_cotiles); requires Ci <= kCIC.
+template <typename T, int COT>
+__global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs, const SPat* __restrict__ pats,
+                                                  const PSpan* __restrict__ acts, const int32_t* __restrict__ offs,
+                                                  const PVal* __restrict__ vals, OpGeom g,
+                                                  const T* __restrict__ x, const T* __restrict__ w,
+                                                  T* __restrict__ y, int Ci, int Co, int n_qtiles, int n_cotiles,
+                                                  bool w_trans) {
+    __shared__ float4 xs[kNCQ * kSweepCols];
+    __shared__ float4 evs[kSweepEntries];
+    __shared__ int eoffs[kSweepEntries];
+
+    const int tid = threadIdx.x;
+    const int bid = xcd_remap(blockIdx.x, gridDim.x);
+    const int run = bid / n_qtiles;
+    const int qt = bid - run * n_qtiles;
+    const int b = blockIdx.y / n_cotiles;
+    const int co0 = (blockIdx.y - b * n_cotiles) * COT;
+    const int q0 = qt * kBlock;
+    const int q = q0 + tid;
+    const int lane_col = g.stride * tid;
+    const int64_t n_in = (int64_t)g.nlat_i * g.nlon_i;
+    const int64_t n_out = (int64_t)g.nlat_o * g.nlon_o;
+    const T* xb = x + (int64_t)b * Ci * n_in;
+    const SRun R = runs[run];
+
+    // W in registers for the MFMA contraction: with CBSZ = 4 the A operand of
+    // v_mfma_f32_4x4x1_16b_f32 is taken from block ABID and broadcast to all
+    // 16 blocks, so wv[qd][g] at lane 4b + i holds W(co0 + 4 qd + i, kk =
+    // 16 g + b) and one register serves 16 values of kk.
+    float wv[COT / 4][kWG];
+    {
+        const int li = tid & 3, blk = (tid & 63) >> 2;
+#pragma unroll
+        for (int qd = 0; qd < COT / 4; ++qd)
+#pragma unroll
+            for (int gg = 0; gg < kWG; ++gg) {
+                const int kk = 16 * gg + blk, co = co0 + 4 * qd + li;
+                const int c = kk / kBasis, k = kk % kBasis;
+                float v = 0.0f;
+                if (kk < kKK && co < Co && c < Ci) {
+                    const int64_t idx = w_trans ? ((int64_t)c * Co + co) * kBasis + k : ((int64_t)co * Ci + c) * kBasis + k;
+                    v = load_val(w, idx);
+                }
+                wv[qd][gg] = v;
+            }
+    }
+
+    // Staging of pattern pi's new spans and entries.  Columns j = tid + 256 i
+    // for i < kPF of the first span of the next pattern, and its entries, are
+    // loaded into registers while the current pattern computes; anything
+    // beyond that (the first pattern of a run, or a second new span) is
+    // loaded directly.
+    float4 pf[kPF][kNCQ];
+    int pf_off[kPFE];
+    float4 pf_val[kPFE];
+    auto load_col = [&](const PSpan& S, int start, int j, float4 (&v)[kNCQ]) {
+        int idx = start + j;
+        if (idx >= g.nlon_i) idx = idx % g.nlon_i;
+        const T* xp = xb + S.row + idx;
+#pragma unroll
+        for (int gq = 0; gq < kNCQ; ++gq) {
+            const int c = 4 * gq;
+            v[gq].x = c + 0 < Ci ? load_val(xp, (int64_t)(c + 0) * n_in) : 0.0f;
+            v[gq].y = c + 1 < Ci ? load_val(xp, (int64_t)(c + 1) * n_in) : 0.0f;
+            v[gq].z = c + 2 < Ci ? load_val(xp, (int64_t)(c + 2) * n_in) : 0.0f;
+            v[gq].w = c + 3 < Ci ? load_val(xp, (int64_t)(c + 3) * n_in) : 0.0f;
+        }
+    };
+    auto span_start = [&](const PSpan& S) {
+        int start = (g.stride * q0 + S.dstart) % g.nlon_i;
+        return start < 0 ? start + g.nlon_i : start;
+    };
+    auto prefetch = [&](const SPat& P) {
+        if (P.act_end > P.act_begin) {
+            const PSpan S = acts[P.act_begin];
+            const int start = span_start(S);
+#pragma unroll
+            for (int i = 0; i < kPF; ++i) {
+                const int j = tid + i * kBlock;
+                if (j < S.len) load_col(S, start, j, pf[i]);
+            }
+        }
+        const int ne = P.cls[kCells] - P.cls[0];
+#pragma unroll
+        for (int i = 0; i < kPFE; ++i) {
+            const int k = tid + i * kBlock;
+            if (k < ne) {
+                pf_off[i] = offs[P.cls[0] + k];
+                const PVal pv = vals[P.cls[0] + k];
+                pf_val[i] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
+            }
+        }
+    };
+    bool have_pf = false;
+    for (int pi = R.pat_begin; pi < R.pat_end; ++pi) {
+        const SPat SP = pats[pi];
+        __syncthreads();  // the previous pattern's reads of LDS are done
+        for (int ai = SP.act_begin; ai < SP.act_end; ++ai) {
+            const PSpan S = acts[ai];
+            const int start = span_start(S);
+            const bool first = have_pf && ai == SP.act_begin;
+            for (int j = tid; j < S.len; j += kBlock) {
+                const int i = (j - tid) / kBlock;
+                float4 v[kNCQ];
+                if (first && i < kPF) {
+#pragma unroll
+                    for (int ii = 0; ii < kPF; ++ii)
+                        if (ii == i) {
+#pragma unroll
+                            for (int gq = 0; gq < kNCQ; ++gq) v[gq] = pf[ii][gq];
+                        }
+                } else {
+                    load_col(S, start, j, v);
+                }
+#pragma unroll
+                for (int gq = 0; gq < kNCQ; ++gq) xs[gq * kSweepCols + S.lds_base + j] = v[gq];
+            }
+        }
+        {
+            const int ebase = SP.cls[0], ne = SP.cls[kCells] - SP.cls[0];
+            for (int k = tid; k < ne; k += kBlock) {
+                const int i = (k - tid) / kBlock;
+                if (have_pf && i < kPFE) {
+#pragma unroll
+                    for (int ii = 0; ii < kPFE; ++ii)
+                        if (ii == i) {
+                            eoffs[k] = pf_off[ii];
+                            evs[k] = pf_val[ii];
+                        }
+                } else {
+                    eoffs[k] = offs[ebase + k];
+                    const PVal pv = vals[ebase + k];
+                    evs[k] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
+                }
+            }
+        }
+        __syncthreads();
+        have_pf = pi + 1 < R.pat_end;
+        if (have_pf) prefetch(pats[pi + 1]);
+        float z[kCIC][kBasis];
+#pragma unroll
+        for (int c = 0; c < kCIC; ++c)
+#pragma unroll
+            for (int k = 0; k < kBasis; ++k) z[c][k] = 0.0f;
+        const int c0 = SP.cls[0], ne = SP.cls[kCells] - SP.cls[0];
+        Pipe pp;
+        // Prime: entry 0 in (v1, x1), entry 1's offset and values in (o2, v2).
+        if (ne > 0) {
+            const int o0 = eoffs[0];
+            pp.v2 = evs[0];
+            pp.o2 = o0;
+            pipe_load(pp, -1, ne, eoffs, evs, xs, lane_col);
+        }
+        int e = 0;
+        run_cell<0>(e, SP.cls[1] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<1>(e, SP.cls[2] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<2>(e, SP.cls[3] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<3>(e, SP.cls[4] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<4>(e, SP.cls[5] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<5>(e, SP.cls[6] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<6>(e, SP.cls[7] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<7>(e, SP.cls[8] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<8>(e, SP.cls[9] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<9>(e, SP.cls[10] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<10>(e, SP.cls[11] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<11>(e, SP.cls[12] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<12>(e, SP.cls[13] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<13>(e, SP.cls[14] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<14>(e, SP.cls[15] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<15>(e, SP.cls[16] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        // Contraction on the matrix cores (see disco_fused.hip): lane l ends
+        // with y[co0 + 4 quad + r][its pixel] in register r of yacc[quad].
+        v4f yacc[COT / 4];
+#pragma unroll
+        for (int j = 0; j < COT / 4; ++j) yacc[j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+        mfma_contract<0, COT / 4>(yacc, wv, z);
+        if (q < g.nq) {
+            const int to = SP.pattern / g.P, r = SP.pattern - (SP.pattern / g.P) * g.P;
+            const int64_t pix = (int64_t)to * g.nlon_o + (int64_t)q * g.P + r;
+#pragma unroll
+            for (int j = 0; j < COT; ++j)
+                if (co0 + j < Co) store_val(y, ((int64_t)b * Co + co0 + j) * n_out + pix, yacc[j / 4][j % 4]);
+        }
+    }
+}
+
+template <typename T, int COT>
+hipError_t sweep_launch(const ExecArgs& a) {
+    const OpGeom& g = a.op->g;
+    const SweepDev& S = a.op->sweep;
+    if (S.n_runs == 0) return hipSuccess;
+    const int n_qtiles = (g.nq + kBlock - 1) / kBlock;
+    const int n_cot = (a.Co + COT - 1) / COT;
+    dim3 grid((unsigned)(S.n_runs * n_qtiles), (unsigned)(a.B * n_cot));
+    int tk = timing_begin("sweep_gather_contract", a.stream);
+    hipLaunchKernelGGL((k_sweep<T, COT>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats, S.acts, S.offs, S.vals,
+                       g, (const T*)a.x, (const T*)a.w, (T*)a.y, a.Ci, a.Co, n_qtiles, n_cot, a.w_trans);
+    timing_end(tk, a.stream);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t sweep_dispatch(const ExecArgs& a) {
+    if (a.Co <= 4) return sweep_launch<T, 4>(a);
+    if (a.Co <= 8) return sweep_launch<T, 8>(a);
+    if (a.Co <= 16) return sweep_launch<T, 16>(a);
+    return sweep_launch<T, 32>(a);
+}
+
+}  // namespace
+
+hipError_t launch_sweep(const ExecArgs& a) {
+    if (a.Ci > kCIC) return hipErrorInvalidValue;
+    return a.dtype == 1 ? sweep_dispatch<uint16_t>(a) : sweep_dispatch<float>(a);
+}
+
+}  // namespace disco
