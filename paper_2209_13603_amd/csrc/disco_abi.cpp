@@ -22,6 +22,7 @@ struct disco_plan {
     PlanParams params{};
     disco_plan_info_t info{};
     DeviceOp fwd, tr;
+    hipStream_t aux = nullptr;  // runs the spectral rings beside the direct kernels
 };
 
 namespace {
@@ -356,9 +357,31 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
     } else if (algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
         e = launch_gather_then_contract(a, ws_ptr);
     } else {
-        e = spectral ? launch_spectral(a, ws_ptr) : hipSuccess;
+        // The spectral rings run on the plan's helper stream, forked from and
+        // joined back into the caller's stream, beside the direct kernels.
+        hipEvent_t fork = nullptr, join = nullptr;
+        if (spectral && plan->aux) {
+            e = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
+            if (e == hipSuccess) e = hipEventCreateWithFlags(&join, hipEventDisableTiming);
+            if (e == hipSuccess) e = hipEventRecord(fork, stream);
+            if (e == hipSuccess) e = hipStreamWaitEvent(plan->aux, fork, 0);
+            if (e == hipSuccess) {
+                ExecArgs as = a;
+                as.stream = plan->aux;
+                e = launch_spectral(as, ws_ptr);
+            }
+            if (e == hipSuccess) e = hipEventRecord(join, plan->aux);
+        } else if (spectral) {
+            e = launch_spectral(a, ws_ptr);
+        }
         if (e == hipSuccess && sweep) e = launch_sweep(a);
         if (e == hipSuccess) e = launch_fused(a, packed, (float*)((char*)ws_ptr + ws_spec));
+        if (join) {
+            hipError_t ej = hipStreamWaitEvent(stream, join, 0);
+            if (e == hipSuccess) e = ej;
+        }
+        if (fork) (void)hipEventDestroy(fork);
+        if (join) (void)hipEventDestroy(join);
     }
     hipError_t e2 = ws_ptr ? hipFreeAsync(ws_ptr, stream) : hipSuccess;
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
@@ -470,6 +493,9 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
         delete plan;
         return s;
     }
+    if (plan->fwd.spectral.n_rings > 0 || plan->tr.spectral.n_rings > 0) {
+        if (hipStreamCreateWithFlags(&plan->aux, hipStreamNonBlocking) != hipSuccess) plan->aux = nullptr;
+    }
     // Keep freed workspace in the device's pool rather than returning it to
     // the driver at every synchronisation.
     hipMemPool_t pool;
@@ -501,6 +527,10 @@ disco_status_t disco_plan_destroy(disco_plan_t plan) {
     int cur = 0;
     (void)hipGetDevice(&cur);
     if (cur != plan->device) (void)hipSetDevice(plan->device);
+    if (plan->aux) {
+        (void)hipStreamSynchronize(plan->aux);
+        (void)hipStreamDestroy(plan->aux);
+    }
     free_op(&plan->fwd);
     free_op(&plan->tr);
     if (cur != plan->device) (void)hipSetDevice(cur);
