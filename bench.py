@@ -29,7 +29,15 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 FP32_VALU_PEAK_TFLOPS = 157.3  # MI355X fp32 vector (published)
 FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2209_13603_amd", "csrc", "disco_kernels.hip")
+SOURCE_DIRS = [os.path.join(ROOT, "paper_2209_13603_amd", "csrc"), os.path.join(ROOT, "include")]
+# Library kernel name (as the kernel timing reports it) -> device function name.
+DEVICE_KERNEL = {"gather_z": "k_gather_z", "contract_z": "k_contract_z", "contract_x": "k_contract_x",
+                 "gather_y": "k_gather_y", "fused_gather_contract": "k_fused",
+                 "reduce_partials": "k_reduce_partials", "sweep_gather_contract": "k_sweep",
+                 "spectral_rfft": "k_rfft_rings", "spectral_mac": "k_spectral",
+                 "spectral_irfft": "k_irfft_rings"}
+COPY_PROBE_BYTES = 256 << 20   # per direction, fp32 negation used as the plain copy kernel
+COPY_PROBE_KERNEL = "neg"
 
 
 def log(*a):
@@ -37,53 +45,124 @@ def log(*a):
 
 
 def kernel_source_digest() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Digest of every library source with comments and blank space removed:
+    counter figures go stale when any code changes, not when comments do."""
+    import re
+    strip = re.compile(r"//[^\n]*|/\*.*?\*/", re.S)
+    h = hashlib.sha256()
+    for d in SOURCE_DIRS:
+        for fn in sorted(os.listdir(d)):
+            if fn.endswith((".hip", ".cpp", ".h")):
+                with open(os.path.join(d, fn)) as f:
+                    code = " ".join(strip.sub(" ", f.read()).split())
+                h.update(fn.encode() + b"\0" + code.encode())
+    return h.hexdigest()[:16]
 
 
-def kernel_model(name, wl, info, es):
+def kernel_model(name, wl, work, es):
     """Algorithmic (bytes, flops, bound) of one launch of kernel `name`.
 
-    Per unit figures (one unit = one output pixel x one channel of the
-    kernel's output): gather_z reads x once and writes 9 fp32 Z planes;
-    contract_z reads Z and writes y; contract_x reads x and writes 9 fp32
-    planes per output channel; gather_y reads those planes and writes y; a
-    fused kernel reads x once and writes y once.
+    `work` = (out_pixels, in_pixels, pairs) per batch item and channel, as
+    the library reports it for this kernel.  Per unit figures: every output
+    pixel x channel written costs es bytes, every input pixel x channel read
+    es bytes; the sparse gather costs 2 flop per non-zero (pixel pair, k) per
+    gathered channel, the channel contraction 2 * 9 * Cin flop per output
+    pixel x output channel.  The two-kernel path also moves its fp32
+    intermediate (9 planes per channel), which its kernels must write and
+    read.
     """
-    B = wl.batch
-    Ci, Co = wl.c_in, wl.c_out
-    if wl.op == "forward":
-        n_in, n_out = wl.nlat_in * wl.nlon_in, wl.nlat_out * wl.nlon_out
-    else:
-        n_in, n_out = wl.nlat_out * wl.nlon_out, wl.nlat_in * wl.nlon_in
-    pairs = info["nnz_pairs_total"] if wl.op == "forward" else None
-    if pairs is None:
-        # The transposed op visits the same (pixel, pixel, k) triples.
-        pairs = info["nnz_pairs_total"]
+    B, Ci, Co = wl.batch, wl.c_in, wl.c_out
+    outp, inp, pairs = work
     if name == "gather_z":
-        return (B * Ci * n_in * es + B * Ci * 9 * n_out * 4, 2.0 * pairs * B * Ci, "hbm")
+        return (B * Ci * inp * es + B * Ci * 9 * outp * 4, 2.0 * pairs * B * Ci, "hbm")
     if name == "contract_z":
-        return (B * Ci * 9 * n_out * 4 + B * Co * n_out * es, 2.0 * B * Ci * 9 * Co * n_out, "hbm")
+        return (B * Ci * 9 * outp * 4 + B * Co * outp * es, 2.0 * B * Ci * 9 * Co * outp, "hbm")
     if name == "contract_x":
-        return (B * Ci * n_in * es + B * Co * 9 * n_in * 4, 2.0 * B * Ci * 9 * Co * n_in, "hbm")
+        return (B * Ci * inp * es + B * Co * 9 * inp * 4, 2.0 * B * Ci * 9 * Co * inp, "hbm")
     if name == "gather_y":
-        return (B * Co * 9 * n_in * 4 + B * Co * n_out * es, 2.0 * pairs * B * Co, "hbm")
-    # fused kernels: x in, y out
-    fl = 2.0 * pairs * B * min(Ci, Co) + 2.0 * B * Ci * 9 * Co * min(n_in, n_out)
-    return (B * Ci * n_in * es + B * Co * n_out * es, fl, "alu")
+        return (B * Co * 9 * inp * 4 + B * Co * outp * es, 2.0 * pairs * B * Co, "hbm")
+    # fused kernels: x in, y out, gather over the input channels, contraction per output
+    fl = 2.0 * pairs * B * Ci + 2.0 * B * Ci * 9 * Co * outp
+    return (B * Ci * inp * es + B * Co * outp * es, fl, "alu")
+
+
+def traffic_path(kernel, workload):
+    return os.path.join(ROOT, "profiles", "traffic_%s_%s.txt" % (kernel, workload))
 
 
 def load_traffic(kernel, workload):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when absent or taken on a different kernel source."""
-    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (kernel, workload))
+    """Calibrated HBM bytes per launch from the committed counter summary, or
+    None when absent or taken on different library sources."""
+    path = traffic_path(kernel, workload)
     if not os.path.exists(path):
         return None
+    kv = {}
     with open(path) as f:
-        t = json.load(f)
-    if t.get("kernel_source_sha256_16") != kernel_source_digest():
+        for line in f:
+            if ":" in line and not line.startswith((" ", "#", "-")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("library_source_sha256_16") != kernel_source_digest():
         return None
-    return float(t["hbm_bytes_per_launch"])
+    return float(kv["hbm_bytes_per_launch"])
+
+
+def _pmc_rows(path):
+    """{dispatch id: (kernel name, {counter: value})} from a rocprofv3 counter CSV."""
+    import csv
+    per = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            d = int(r["Dispatch_Id"])
+            name, cs = per.setdefault(d, (r["Kernel_Name"], {}))
+            cs[r["Counter_Name"]] = cs.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return per
+
+
+def traffic_summary(fetch_csv, write_csv, kernel, workload, commands):
+    """Write the calibrated traffic summary of `kernel` from two counter runs
+    (FETCH_SIZE, then WRITE_SIZE) that each also ran the copy probe."""
+    dev = DEVICE_KERNEL[kernel]
+    out = {}
+    for ctr, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = _pmc_rows(path)
+        kv = [cs[ctr] for n, cs in rows.values() if (dev + "<") in n or n.split("(")[0].endswith(dev)]
+        cp = [cs[ctr] for n, cs in rows.values() if COPY_PROBE_KERNEL in n.split("(")[0]]
+        if not kv or not cp:
+            raise SystemExit("%s: no %s dispatch (%d) or copy probe (%d)" % (path, dev, len(kv), len(cp)))
+        kib = sum(kv) / len(kv)
+        cal = (sum(cp) / len(cp)) * 1024.0 / COPY_PROBE_BYTES
+        out[ctr] = (kib, len(kv), sum(cp) / len(cp), cal)
+    fetch = out["FETCH_SIZE"][0] * 1024.0 / out["FETCH_SIZE"][3]
+    write = out["WRITE_SIZE"][0] * 1024.0 / out["WRITE_SIZE"][3]
+    lines = ["# HBM traffic of %s (%s) on %s, from rocprofv3 counters" % (kernel, dev, workload),
+             "# Each counter is scaled by what it reads for a plain copy kernel (fp32 negation)",
+             "# moving %d bytes each way in the same process." % COPY_PROBE_BYTES,
+             "kernel: %s" % kernel, "workload: %s" % workload,
+             "library_source_sha256_16: %s" % kernel_source_digest()]
+    for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
+        kib, n, ckib, cal = out[ctr]
+        lines.append("%s_kib_per_dispatch: %.1f   (mean of %d dispatches)" % (ctr, kib, n))
+        lines.append("%s_copy_probe_kib: %.1f   (calibration factor %.4f)" % (ctr, ckib, cal))
+    lines += ["fetch_bytes_per_launch: %.0f" % fetch, "write_bytes_per_launch: %.0f" % write,
+              "hbm_bytes_per_launch: %.0f" % (fetch + write), "commands:"]
+    lines += ["    " + c for c in commands]
+    path = traffic_path(kernel, workload)
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(path)
+    print("\n".join(lines))
+
+
+def copy_probe(torch, dev, reps=3):
+    """A plain streaming kernel of known size, for counter calibration."""
+    n = COPY_PROBE_BYTES // 4
+    a = torch.ones(n, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    del a, b
 
 
 def cpu_baseline(wl, x, w, seconds=15.0):
@@ -96,16 +175,17 @@ def cpu_baseline(wl, x, w, seconds=15.0):
     args = wl.plan_args()
     fn = o.forward if wl.op == "forward" else o.transpose
     x64, w64 = x.astype(np.float64), w.astype(np.float64)
-    n = 64
-    pix = rng.choice(nlat * nlon, size=n, replace=False)
-    t0 = time.perf_counter()
-    fn(*args, x64, w64, pix=pix)
-    t_cal = time.perf_counter() - t0
-    n = int(min(nlat * nlon, max(64, n * seconds / max(t_cal, 1e-6))))
-    pix = rng.choice(nlat * nlon, size=n, replace=False)
-    t0 = time.perf_counter()
-    fn(*args, x64, w64, pix=pix)
-    dt = time.perf_counter() - t0
+    # Grow the sample until one timed call takes at least half the budget
+    # (the first calls also pay thread start-up, so one calibration is short).
+    n, dt = 256, 0.0
+    for _ in range(6):
+        pix = rng.choice(nlat * nlon, size=n, replace=False)
+        t0 = time.perf_counter()
+        fn(*args, x64, w64, pix=pix)
+        dt = time.perf_counter() - t0
+        if dt >= 0.5 * seconds or n == nlat * nlon:
+            break
+        n = int(min(nlat * nlon, max(2 * n, n * seconds / max(dt, 1e-6))))
     return {"value": n * wl.batch * wl.c_out / dt, "unit": UNIT, "cores": o.max_threads(),
             "kind": "oracle", "seconds": round(dt, 3),
             "sample": "%d output pixels drawn uniformly (seed 12345) of %s, all %d batch x %d "
@@ -121,7 +201,24 @@ def main(argv=None):
     ap.add_argument("--algo", default="auto")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="after the timed steps, run a plain copy kernel of known size "
+                         "(counter calibration for the traffic summary)")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/traffic_<kernel>_<workload>.txt from two rocprofv3 "
+                         "counter runs (FETCH_SIZE, then WRITE_SIZE) of --copy-probe benches; "
+                         "no GPU needed")
+    ap.add_argument("--kernel", default="sweep_gather_contract",
+                    help="library kernel name for --traffic-summary")
+    ap.add_argument("--command", action="append", default=[],
+                    help="the command that produced each counter run (recorded verbatim)")
     args = ap.parse_args(argv)
+
+    if args.traffic_summary:
+        from paper_2209_13603_amd import synth
+        wl = synth.WORKLOADS[args.workload or synth.HEADLINE]
+        traffic_summary(*args.traffic_summary, args.kernel, wl.name, args.command)
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -182,10 +279,26 @@ def main(argv=None):
     log("step %.4f ms (with kernel events %.4f ms); kernels: %s"
         % (ms_per_step, ms_total / args.steps, kt))
 
-    dom = max(kt.items(), key=lambda kv: kv[1][1])
-    name, (launches, tot_ms) = dom
+    if args.copy_probe:
+        copy_probe(torch, dev)
+
+    transpose = wl.op != "forward"
+    work = plan.kernel_work(transpose, args.algo, wl.c_in, wl.c_out)
+    missing = sorted(set(kt) - set(work))
+    if missing:
+        raise SystemExit("no work figures for kernels %s" % missing)
+    per_kernel = {}
+    for k, (launches, tot_ms) in kt.items():
+        avg_ms = tot_ms / launches
+        b_, f_, bd = kernel_model(k, wl, work[k], es)
+        per_kernel[k] = {"launches": launches, "avg_us": round(avg_ms * 1e3, 2),
+                         "alg_bytes": int(b_), "alg_flops": f_, "bound": bd,
+                         "alg_gbs": round(b_ / (avg_ms / 1e3) / 1e9, 1),
+                         "alg_tflops": round(f_ / (avg_ms / 1e3) / 1e12, 2)}
+    name = max(kt, key=lambda k: kt[k][1])
+    launches, tot_ms = kt[name]
     avg_ms = tot_ms / launches
-    bytes_, flops, bound = kernel_model(name, wl, info, es)
+    bytes_, flops, bound = kernel_model(name, wl, work[name], es)
     if bound == "hbm":
         achieved = bytes_ / (avg_ms / 1e3) / 1e9
         peak, unit = HBM_PEAK_GBS, "GB/s"
@@ -196,8 +309,9 @@ def main(argv=None):
     roof = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
             "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": name,
             "kernel_avg_us": round(avg_ms * 1e3, 2), "algorithmic_bytes": int(bytes_),
-            "algorithmic_flops": flops}
-    per_kernel = {k: {"launches": v[0], "avg_us": round(v[1] / v[0] * 1e3, 2)} for k, v in kt.items()}
+            "algorithmic_flops": flops,
+            "algorithmic_gbs": round(bytes_ / (avg_ms / 1e3) / 1e9, 1),
+            "work_per_launch": dict(zip(("out_pixels", "in_pixels", "pairs"), work[name]))}
     op_bytes = wl.batch * (wl.c_in * (wl.nlat_in * wl.nlon_in if wl.op == "forward" else
                                       wl.nlat_out * wl.nlon_out)
                            + wl.c_out * wl.y_shape[2] * wl.y_shape[3]) * es

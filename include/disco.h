@@ -105,6 +105,9 @@ typedef struct {
     double h;                  /* node spacing actually used */
     int32_t spectral_rings_forward;   /* output rings of the forward op on the spectral path */
     int32_t spectral_rings_transpose; /* ... of the transposed op */
+    int32_t sweep_patterns_forward;   /* (ring, phase) patterns of the forward op walked by the
+                                         ring-sweep kernel (used when Cin <= 8) */
+    int32_t sweep_patterns_transpose; /* ... of the transposed op */
 } disco_plan_info_t;
 
 /* Builds the sparse psi tensors of the forward and transposed ops on the host
@@ -180,6 +183,24 @@ disco_status_t disco_psi_entries(int nlat_in, int nlon_in, int nlat_out, int nlo
 disco_status_t disco_kernel_timing_enable(int32_t on);
 disco_status_t disco_kernel_timing_read(int32_t capacity, char* names, int64_t* launches,
                                         double* total_ms, int32_t* count);
+
+/* Algorithmic work of the kernels that one call of disco_forward_algo
+ * (transpose == 0) or disco_transpose_algo (transpose != 0) with `algo`,
+ * c_in input and c_out output channels launches on this plan, for
+ * measurement tools (the dispatch is the one those calls make).  Row i
+ * names the kernel as disco_kernel_timing_read does (64 chars per row in
+ * `names`) and gives, per batch item and per channel: out_pixels[i], the
+ * output pixels the kernel writes; in_pixels[i], the distinct input pixels
+ * it reads; pairs[i], the non-zero (output pixel, input pixel, k) triples of
+ * the sparse tensor (Sec. 4.1 eq. 7, of the forward or the transposed op)
+ * whose products it accounts for.  A kernel that only moves intermediate data reports zeros where it
+ * touches neither x nor y.  Up to `capacity` rows are written (any output
+ * pointer may be NULL) and *count receives the number of kernels.  Host
+ * only, no device call.  Errors: INVALID_ARGUMENT (NULL plan or count,
+ * unknown algo), SHAPE (channel count < 1). */
+disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t algo, int32_t c_in,
+                                 int32_t c_out, int32_t capacity, char* names, int64_t* out_pixels,
+                                 int64_t* in_pixels, int64_t* pairs, int32_t* count);
 
 /* Static text for a status code (never NULL). */
 const char* disco_status_string(disco_status_t status);

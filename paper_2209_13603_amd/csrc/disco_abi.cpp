@@ -164,6 +164,7 @@ disco_status_t upload_sweep(const SweepHost& H, SweepDev* d) {
     if ((s = upload_vec(offs, &d->offs, &d->bytes, "hipMalloc(sweep offsets)")) != DISCO_OK) return s;
     if ((s = upload_vec(vals, &d->vals, &d->bytes, "hipMalloc(sweep values)")) != DISCO_OK) return s;
     d->n_runs = (int32_t)H.runs.size();
+    d->n_pats = (int32_t)H.pats.size();
     return DISCO_OK;
 }
 
@@ -207,6 +208,7 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
         if (e != hipSuccess) return hip_fail(e, "hipMemcpy(psi entries)");
     }
     d->bytes = (int64_t)(pb + eb);
+    d->work_all = pattern_work(h, {});
     disco_status_t s = upload_packed(h, {}, &d->packed);
     if (s != DISCO_OK) return s;
     d->bytes += d->packed.bytes;
@@ -219,6 +221,12 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
         if ((s = upload_spectral(sp, &d->spectral)) != DISCO_OK) return s;
         if ((s = upload_packed(h, heavy, &d->packed_light)) != DISCO_OK) return s;
         d->bytes += d->spectral.bytes + d->packed_light.bytes;
+        std::vector<uint8_t> light(heavy.size());
+        for (size_t i = 0; i < heavy.size(); ++i) light[i] = !heavy[i];
+        d->work_spectral = pattern_work(h, heavy);
+        d->work_light = pattern_work(h, light);
+    } else {
+        d->work_light = d->work_all;
     }
     // Sweep runs over the light patterns; the rest go to the general kernel.
     SweepHost sw;
@@ -230,6 +238,9 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
         if ((s = upload_sweep(sw, &d->sweep)) != DISCO_OK) return s;
         if ((s = upload_packed(h, rest_skip, &d->packed_rest)) != DISCO_OK) return s;
         d->bytes += d->sweep.bytes + d->packed_rest.bytes;
+        for (size_t i = 0; i < rest_skip.size(); ++i) rest_skip[i] = !rest_skip[i];
+        d->work_sweep = pattern_work(h, sw.covered);
+        d->work_rest = pattern_work(h, rest_skip);
     }
     return DISCO_OK;
 }
@@ -277,6 +288,36 @@ disco_status_t check_device_ptr(const void* p, int device, const char* name) {
 }
 
 // Shared entry of forward and transpose.
+// Which kernels one call runs, given the requested algorithm and channels.
+struct Dispatch {
+    int32_t algo;
+    bool spectral, sweep;
+    const PackedDev* packed;  // pattern set of the general fused kernel
+    const Work* packed_work;
+};
+
+Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co) {
+    const OpGeom& g = op.g;
+    if (algo == DISCO_ALGO_AUTO) {
+        // Channel mixing goes first when the op upsamples into more (pixels x
+        // channels) than it reads; otherwise the fused gather + contraction.
+        const double gtc = (double)Ci * g.nlat_o * g.nlon_o;
+        const double ctg = (double)Co * g.nlat_i * g.nlon_i;
+        algo = ctg < gtc ? DISCO_ALGO_CONTRACT_THEN_GATHER : DISCO_ALGO_FUSED;
+    }
+    Dispatch d{algo, false, false, &op.packed, &op.work_all};
+    d.spectral = algo == DISCO_ALGO_FUSED && op.spectral.n_rings > 0;
+    d.sweep = algo == DISCO_ALGO_FUSED && op.sweep.n_runs > 0 && Ci <= kCIC;
+    if (d.sweep) {
+        d.packed = &op.packed_rest;
+        d.packed_work = &op.work_rest;
+    } else if (d.spectral) {
+        d.packed = &op.packed_light;
+        d.packed_work = &op.work_light;
+    }
+    return d;
+}
+
 disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
                    disco_tensor_t* y, hipStream_t stream, int32_t algo, bool transpose) {
     if (!plan) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan is NULL");
@@ -320,16 +361,10 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
     a.op = &op; a.x = x->data; a.w = w->data; a.y = y->data; a.dtype = x->dtype;
     a.B = (int)B; a.Ci = (int)Ci; a.Co = (int)Co; a.w_trans = transpose; a.stream = stream;
 
-    if (algo == DISCO_ALGO_AUTO) {
-        // Channel mixing goes first when the op upsamples into more (pixels x
-        // channels) than it reads; otherwise the fused gather + contraction.
-        const double gtc = (double)Ci * g.nlat_o * g.nlon_o;
-        const double ctg = (double)Co * g.nlat_i * g.nlon_i;
-        algo = ctg < gtc ? DISCO_ALGO_CONTRACT_THEN_GATHER : DISCO_ALGO_FUSED;
-    }
-    const bool spectral = algo == DISCO_ALGO_FUSED && op.spectral.n_rings > 0;
-    const bool sweep = algo == DISCO_ALGO_FUSED && op.sweep.n_runs > 0 && Ci <= kCIC;
-    const PackedDev& packed = sweep ? op.packed_rest : spectral ? op.packed_light : op.packed;
+    const Dispatch dp = dispatch(op, algo, (int)Ci, (int)Co);
+    algo = dp.algo;
+    const bool spectral = dp.spectral, sweep = dp.sweep;
+    const PackedDev& packed = *dp.packed;
     size_t ws_spec = 0, ws = 0;
     if (algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {
         ws = workspace_bytes_contract_then_gather(a);
@@ -518,6 +553,8 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
     I.h = p.h;
     I.spectral_rings_forward = plan->fwd.spectral.n_rings;
     I.spectral_rings_transpose = plan->tr.spectral.n_rings;
+    I.sweep_patterns_forward = plan->fwd.sweep.n_pats;
+    I.sweep_patterns_transpose = plan->tr.sweep.n_pats;
     *plan_out = plan;
     return ok();
 }
@@ -541,6 +578,48 @@ disco_status_t disco_plan_destroy(disco_plan_t plan) {
 disco_status_t disco_plan_query(disco_plan_t plan, disco_plan_info_t* info) {
     if (!plan || !info) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan or info is NULL");
     *info = plan->info;
+    return ok();
+}
+
+disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t algo, int32_t c_in,
+                                 int32_t c_out, int32_t capacity, char* names, int64_t* out_pixels,
+                                 int64_t* in_pixels, int64_t* pairs, int32_t* count) {
+    if (!plan || !count) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan or count is NULL");
+    if (algo < DISCO_ALGO_AUTO || algo > DISCO_ALGO_FUSED_DIRECT) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown algo");
+    if (c_in < 1 || c_out < 1) return fail(DISCO_ERR_SHAPE, "channel counts must be >= 1");
+    const DeviceOp& op = transpose ? plan->tr : plan->fwd;
+    const Dispatch dp = dispatch(op, algo, c_in, c_out);
+    struct Row { const char* name; Work w; };
+    std::vector<Row> rows;
+    const Work& all = op.work_all;
+    if (dp.algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
+        rows.push_back({"gather_z", all});
+        rows.push_back({"contract_z", Work{all.out_pixels, 0, 0}});
+    } else if (dp.algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {
+        rows.push_back({"contract_x", Work{0, all.in_pixels, 0}});
+        rows.push_back({"gather_y", all});
+    } else {
+        if (dp.spectral) {
+            const Work& sw = op.work_spectral;
+            rows.push_back({"spectral_rfft", Work{0, sw.in_pixels, 0}});
+            rows.push_back({"spectral_mac", Work{0, 0, sw.pairs}});
+            rows.push_back({"spectral_irfft", Work{sw.out_pixels, 0, 0}});
+        }
+        if (dp.sweep) rows.push_back({"sweep_gather_contract", op.work_sweep});
+        if (dp.packed->n_items > 0) rows.push_back({"fused_gather_contract", *dp.packed_work});
+        if (dp.packed->n_items > 0 && dp.packed->n_split > 0)
+            rows.push_back({"reduce_partials", Work{0, 0, 0}});
+    }
+    *count = (int32_t)rows.size();
+    for (int32_t i = 0; i < capacity && i < (int32_t)rows.size(); ++i) {
+        if (names) {
+            std::strncpy(names + 64 * (size_t)i, rows[(size_t)i].name, 63);
+            names[64 * (size_t)i + 63] = 0;
+        }
+        if (out_pixels) out_pixels[i] = rows[(size_t)i].w.out_pixels;
+        if (in_pixels) in_pixels[i] = rows[(size_t)i].w.in_pixels;
+        if (pairs) pairs[i] = rows[(size_t)i].w.pairs;
+    }
     return ok();
 }
 

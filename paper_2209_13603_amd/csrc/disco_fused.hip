@@ -1,5 +1,5 @@
 // disco_fused.hip -- the LDS-staged sparse gather of Sec. 4.2's compressed
-// product (eq. "memory_compression") fused with the channel contraction.
+// product (eq. 9) fused with the channel contraction.
 //
 // One workgroup = 256 lanes = 256 consecutive output longitudes q of one
 // pattern (output ring, phase) of a work item, for one batch element and one

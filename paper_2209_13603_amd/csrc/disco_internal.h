@@ -49,6 +49,14 @@ struct HostOp {
     int64_t nnz_pairs = 0;  // non-zero (output pixel, input pixel, k) triples
 };
 
+// Algorithmic work of a set of an op's patterns, per batch item and channel:
+// output pixels written, distinct input pixels read, non-zero (output pixel,
+// input pixel, k) triples of psi.  `include` empty selects every pattern.
+struct Work {
+    int64_t out_pixels = 0, in_pixels = 0, pairs = 0;
+};
+Work pattern_work(const HostOp& op, const std::vector<uint8_t>& include);
+
 // Returns 0 on success, otherwise a disco_status_t with *err set.
 int make_op_geom(const PlanParams& p, bool transpose, OpGeom* g, std::string* err);
 int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* err);
@@ -131,6 +139,7 @@ struct SweepDev {
     int32_t* offs = nullptr;
     PVal* vals = nullptr;
     int32_t n_runs = 0;
+    int32_t n_pats = 0;
     int64_t bytes = 0;
 };
 
@@ -204,6 +213,9 @@ struct DeviceOp {
     int64_t n_entries = 0;
     int64_t nnz_pairs = 0;
     int64_t bytes = 0;
+    // Work of the pattern sets above: all, spectral rings, the rest of them,
+    // sweep-walked, and what the general kernel keeps beside the sweep.
+    Work work_all, work_spectral, work_light, work_sweep, work_rest;
 };
 
 // Kernel launchers (disco_kernels.hip).  All return a hipError_t.

@@ -1,7 +1,7 @@
 // disco_kernels.hip -- gfx950 kernels of the DISCO forward and transposed ops.
 //
 // The sparse-dense product of Sec. 4.1, in the compressed form of Sec. 4.2
-// (eq. "memory_compression"): each output ring r_o (and longitude phase) owns
+// (eq. 9): each output ring r_o (and longitude phase) owns
 // one list of (input ring, longitude offset, 9 values) entries; the output at
 // longitude q reads the input at (stride * q + offset) mod nlon.  Lanes of a
 // wavefront own consecutive output longitudes, so every entry is one

@@ -214,4 +214,28 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
     return DISCO_OK;
 }
 
+Work pattern_work(const HostOp& op, const std::vector<uint8_t>& include) {
+    const OpGeom& g = op.g;
+    Work w;
+    // Output step q reads input longitude (stride * q + d) mod nlon_i, so an
+    // entry of offset d touches the nq longitudes congruent to d modulo the
+    // stride: distinct input pixels per ring = residues seen * nq.
+    std::vector<std::vector<uint8_t>> residues((size_t)g.nlat_i);
+    for (int pat = 0; pat < g.n_patterns(); ++pat) {
+        if (!include.empty() && !include[(size_t)pat]) continue;
+        w.out_pixels += g.nq;
+        for (int32_t e = op.pat_ptr[(size_t)pat]; e < op.pat_ptr[(size_t)pat + 1]; ++e) {
+            int nz = 0;
+            for (int k = 0; k < kBasis; ++k) nz += op.val[(size_t)e * kBasis + k] != 0.0f;
+            w.pairs += (int64_t)nz * g.nq;
+            std::vector<uint8_t>& r = residues[(size_t)op.t_in[(size_t)e]];
+            if (r.empty()) r.assign((size_t)g.stride, 0);
+            r[(size_t)(op.d[(size_t)e] % g.stride)] = 1;
+        }
+    }
+    for (const std::vector<uint8_t>& r : residues)
+        for (uint8_t v : r) w.in_pixels += v ? g.nq : 0;
+    return w;
+}
+
 }  // namespace disco

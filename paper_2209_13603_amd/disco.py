@@ -41,8 +41,8 @@ ALGOS = {"auto": ALGO_AUTO, "gather_then_contract": ALGO_GATHER_THEN_CONTRACT,
 # Every exported symbol declared in include/disco.h.
 EXPORTS = ("disco_plan_create", "disco_plan_destroy", "disco_plan_query", "disco_forward",
            "disco_transpose", "disco_forward_algo", "disco_transpose_algo", "disco_psi_entries",
-           "disco_kernel_timing_enable", "disco_kernel_timing_read", "disco_status_string",
-           "disco_last_error")
+           "disco_kernel_timing_enable", "disco_kernel_timing_read", "disco_kernel_work",
+           "disco_status_string", "disco_last_error")
 
 
 class DiscoError(RuntimeError):
@@ -70,7 +70,9 @@ class PlanInfo(ctypes.Structure):
                 ("nnz_entries", ctypes.c_int64), ("nnz_entries_transpose", ctypes.c_int64),
                 ("nnz_pairs_total", ctypes.c_int64), ("psi_bytes", ctypes.c_int64),
                 ("h", ctypes.c_double), ("spectral_rings_forward", ctypes.c_int32),
-                ("spectral_rings_transpose", ctypes.c_int32)]
+                ("spectral_rings_transpose", ctypes.c_int32),
+                ("sweep_patterns_forward", ctypes.c_int32),
+                ("sweep_patterns_transpose", ctypes.c_int32)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -119,6 +121,11 @@ def library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.disco_kernel_timing_read.argtypes = [ctypes.c_int32, ctypes.c_char_p, P(ctypes.c_int64),
                                              P(ctypes.c_double), P(ctypes.c_int32)]
     lib.disco_kernel_timing_read.restype = ctypes.c_int
+    lib.disco_kernel_work.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.c_int32, ctypes.c_int32, ctypes.c_char_p,
+                                      P(ctypes.c_int64), P(ctypes.c_int64), P(ctypes.c_int64),
+                                      P(ctypes.c_int32)]
+    lib.disco_kernel_work.restype = ctypes.c_int
     lib.disco_status_string.argtypes = [ctypes.c_int]
     lib.disco_status_string.restype = ctypes.c_char_p
     lib.disco_last_error.argtypes = []
@@ -194,6 +201,23 @@ class Plan:
         inf = PlanInfo()
         _check(library().disco_plan_query(self._h, ctypes.byref(inf)))
         return inf.as_dict()
+
+    def kernel_work(self, transpose: bool, algo, c_in: int, c_out: int, capacity: int = 16) -> dict:
+        """{kernel name: (out_pixels, in_pixels, pairs)} per batch item and channel
+        for the kernels one call with these arguments launches."""
+        algo = ALGOS[algo] if isinstance(algo, str) else int(algo)
+        names = ctypes.create_string_buffer(64 * capacity)
+        outp = (ctypes.c_int64 * capacity)()
+        inp = (ctypes.c_int64 * capacity)()
+        pairs = (ctypes.c_int64 * capacity)()
+        count = ctypes.c_int32()
+        _check(library().disco_kernel_work(self._h, int(bool(transpose)), algo, c_in, c_out, capacity,
+                                           names, outp, inp, pairs, ctypes.byref(count)))
+        out = {}
+        for i in range(min(count.value, capacity)):
+            nm = names.raw[64 * i: 64 * i + 64].split(b"\0", 1)[0].decode()
+            out[nm] = (int(outp[i]), int(inp[i]), int(pairs[i]))
+        return out
 
     def _run(self, fn, x, w, y, algo, stream):
         algo = ALGOS[algo] if isinstance(algo, str) else int(algo)

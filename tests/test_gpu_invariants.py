@@ -155,3 +155,62 @@ def test_fault_injection_alloc(monkeypatch):
     torch.cuda.synchronize()
     assert bool((y == 7.0).all())   # a failed call writes nothing
     plan.close()
+
+
+@pytest.mark.parametrize("name", ["sphere32x64", "down128x256_to_64x128", "sphere512x1024",
+                                  "up256x512_to_512x1024_bf16", "sphere2048x4096"])
+def test_kernel_work_covers_the_op(name):
+    """The per-kernel work the library reports for the timing tools splits
+    the op exactly: every output pixel written once, every non-zero triple
+    of psi counted once, whichever kernels the dispatch picks."""
+    wl = synth.WORKLOADS[name]
+    plan = disco.Plan(*wl.plan_args())
+    info = plan.info()
+    for transpose in (False, True):
+        # The transposed op visits the same triples, up to fp64 rounding of
+        # its own geometry exactly at the cutoff.
+        total = plan.kernel_work(transpose, "gather_then_contract", 1, 1)["gather_z"][2]
+        if not transpose:
+            assert total == info["nnz_pairs_total"]
+        assert abs(total - info["nnz_pairs_total"]) <= 1e-4 * info["nnz_pairs_total"]
+        n_out = (wl.nlat_in * wl.nlon_in) if transpose else (wl.nlat_out * wl.nlon_out)
+        n_in = (wl.nlat_out * wl.nlon_out) if transpose else (wl.nlat_in * wl.nlon_in)
+        for algo in ("gather_then_contract", "contract_then_gather", "fused", "fused_direct", "auto"):
+            for ci, co in ((wl.c_in, wl.c_out), (32, 8), (4, 64)):
+                work = plan.kernel_work(transpose, algo, ci, co)
+                say(name, transpose, algo, ci, co, work)
+                gather = [k for k in work if k in ("gather_z", "gather_y", "spectral_mac",
+                                                    "sweep_gather_contract", "fused_gather_contract")]
+                assert sum(work[k][2] for k in gather) == total
+                writers = [k for k in work if k in ("contract_z", "gather_y", "spectral_irfft",
+                                                     "sweep_gather_contract", "fused_gather_contract")]
+                assert sum(work[k][0] for k in writers) == n_out
+                for k, (o, i, p) in work.items():
+                    assert 0 <= o <= n_out and 0 <= i <= n_in and p >= 0
+                if algo == "fused":
+                    assert ("spectral_mac" in work) == (info["spectral_rings_transpose" if transpose
+                                                              else "spectral_rings_forward"] > 0)
+                    assert ("sweep_gather_contract" in work) == (
+                        ci <= 8 and info["sweep_patterns_transpose" if transpose
+                                         else "sweep_patterns_forward"] > 0)
+    plan.close()
+
+
+def test_kernel_work_names_match_timing():
+    """Every kernel the timing records for a call has a work row."""
+    import torch
+    a, b = 32, 64
+    plan = disco.Plan(a, b, a, b, 3 * math.pi / a)
+    dev = torch.device("cuda:0")
+    for algo in ("gather_then_contract", "contract_then_gather", "fused", "fused_direct"):
+        x = torch.randn(1, 4, a, b, device=dev)
+        w = torch.randn(4, 4, 9, device=dev)
+        disco.kernel_timing(True)
+        disco.kernel_timing_read()
+        plan.forward(x, w, algo=algo)
+        kt = disco.kernel_timing_read()
+        disco.kernel_timing(False)
+        work = plan.kernel_work(False, algo, 4, 4)
+        say(algo, sorted(kt), sorted(work))
+        assert set(kt) <= set(work) and kt
+    plan.close()
