@@ -283,7 +283,7 @@ def main(argv=None):
         copy_probe(torch, dev)
 
     transpose = wl.op != "forward"
-    work = plan.kernel_work(transpose, args.algo, wl.c_in, wl.c_out)
+    work = plan.kernel_work(transpose, args.algo, wl.c_in, wl.c_out, wl.dtype)
     missing = sorted(set(kt) - set(work))
     if missing:
         raise SystemExit("no work figures for kernels %s" % missing)

@@ -186,21 +186,22 @@ disco_status_t disco_kernel_timing_read(int32_t capacity, char* names, int64_t* 
 
 /* Algorithmic work of the kernels that one call of disco_forward_algo
  * (transpose == 0) or disco_transpose_algo (transpose != 0) with `algo`,
- * c_in input and c_out output channels launches on this plan, for
- * measurement tools (the dispatch is the one those calls make).  Row i
- * names the kernel as disco_kernel_timing_read does (64 chars per row in
- * `names`) and gives, per batch item and per channel: out_pixels[i], the
- * output pixels the kernel writes; in_pixels[i], the distinct input pixels
- * it reads; pairs[i], the non-zero (output pixel, input pixel, k) triples of
- * the sparse tensor (Sec. 4.1 eq. 7, of the forward or the transposed op)
- * whose products it accounts for.  A kernel that only moves intermediate data reports zeros where it
- * touches neither x nor y.  Up to `capacity` rows are written (any output
- * pointer may be NULL) and *count receives the number of kernels.  Host
- * only, no device call.  Errors: INVALID_ARGUMENT (NULL plan or count,
- * unknown algo), SHAPE (channel count < 1). */
+ * c_in input and c_out output channels and element type `dtype` launches on
+ * this plan, for measurement tools (the dispatch is the one those calls
+ * make).  Row i names the kernel as disco_kernel_timing_read does (64 chars
+ * per row in `names`) and gives, per batch item and per channel:
+ * out_pixels[i], the output pixels the kernel writes; in_pixels[i], the
+ * distinct input pixels it reads; pairs[i], the non-zero (output pixel,
+ * input pixel, k) triples of the sparse tensor (Sec. 4.1 eq. 7, of the
+ * forward or the transposed op) whose products it accounts for.  A kernel
+ * that only moves intermediate data reports zeros where it touches neither
+ * x nor y.  Up to `capacity` rows are written (any output pointer may be
+ * NULL) and *count receives the number of kernels.  Host only, no device
+ * call.  Errors: INVALID_ARGUMENT (NULL plan or count, unknown algo), SHAPE
+ * (channel count < 1), DTYPE (unknown dtype). */
 disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t algo, int32_t c_in,
-                                 int32_t c_out, int32_t capacity, char* names, int64_t* out_pixels,
-                                 int64_t* in_pixels, int64_t* pairs, int32_t* count);
+                                 int32_t c_out, int32_t dtype, int32_t capacity, char* names,
+                                 int64_t* out_pixels, int64_t* in_pixels, int64_t* pairs, int32_t* count);
 
 /* Static text for a status code (never NULL). */
 const char* disco_status_string(disco_status_t status);

@@ -296,7 +296,7 @@ struct Dispatch {
     const Work* packed_work;
 };
 
-Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co) {
+Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co, int32_t dtype) {
     const OpGeom& g = op.g;
     if (algo == DISCO_ALGO_AUTO) {
         // Channel mixing goes first when the op upsamples into more (pixels x
@@ -308,6 +308,7 @@ Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co) {
     Dispatch d{algo, false, false, &op.packed, &op.work_all};
     d.spectral = algo == DISCO_ALGO_FUSED && op.spectral.n_rings > 0;
     d.sweep = algo == DISCO_ALGO_FUSED && op.sweep.n_runs > 0 && Ci <= kCIC;
+    (void)dtype;  // every kernel takes both storage types
     if (d.sweep) {
         d.packed = &op.packed_rest;
         d.packed_work = &op.work_rest;
@@ -361,7 +362,7 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
     a.op = &op; a.x = x->data; a.w = w->data; a.y = y->data; a.dtype = x->dtype;
     a.B = (int)B; a.Ci = (int)Ci; a.Co = (int)Co; a.w_trans = transpose; a.stream = stream;
 
-    const Dispatch dp = dispatch(op, algo, (int)Ci, (int)Co);
+    const Dispatch dp = dispatch(op, algo, (int)Ci, (int)Co, x->dtype);
     algo = dp.algo;
     const bool spectral = dp.spectral, sweep = dp.sweep;
     const PackedDev& packed = *dp.packed;
@@ -393,24 +394,26 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
         e = launch_gather_then_contract(a, ws_ptr);
     } else {
         // The spectral rings run on the plan's helper stream, forked from and
-        // joined back into the caller's stream, beside the direct kernels.
+        // joined back into the caller's stream, beside the direct kernels;
+        // when the sweep kernel takes the light rings, the general kernel's
+        // remaining rings follow the spectral ones there.
         hipEvent_t fork = nullptr, join = nullptr;
-        if (spectral && plan->aux) {
+        const bool fork_aux = spectral && plan->aux;
+        ExecArgs as = a;
+        if (fork_aux) {
+            as.stream = plan->aux;
             e = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
             if (e == hipSuccess) e = hipEventCreateWithFlags(&join, hipEventDisableTiming);
             if (e == hipSuccess) e = hipEventRecord(fork, stream);
             if (e == hipSuccess) e = hipStreamWaitEvent(plan->aux, fork, 0);
-            if (e == hipSuccess) {
-                ExecArgs as = a;
-                as.stream = plan->aux;
-                e = launch_spectral(as, ws_ptr);
-            }
+            if (e == hipSuccess) e = launch_spectral(as, ws_ptr);
+            if (e == hipSuccess && sweep) e = launch_fused(as, packed, (float*)((char*)ws_ptr + ws_spec));
             if (e == hipSuccess) e = hipEventRecord(join, plan->aux);
         } else if (spectral) {
             e = launch_spectral(a, ws_ptr);
         }
         if (e == hipSuccess && sweep) e = launch_sweep(a);
-        if (e == hipSuccess) e = launch_fused(a, packed, (float*)((char*)ws_ptr + ws_spec));
+        if (e == hipSuccess && !(fork_aux && sweep)) e = launch_fused(a, packed, (float*)((char*)ws_ptr + ws_spec));
         if (join) {
             hipError_t ej = hipStreamWaitEvent(stream, join, 0);
             if (e == hipSuccess) e = ej;
@@ -582,13 +585,14 @@ disco_status_t disco_plan_query(disco_plan_t plan, disco_plan_info_t* info) {
 }
 
 disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t algo, int32_t c_in,
-                                 int32_t c_out, int32_t capacity, char* names, int64_t* out_pixels,
-                                 int64_t* in_pixels, int64_t* pairs, int32_t* count) {
+                                 int32_t c_out, int32_t dtype, int32_t capacity, char* names,
+                                 int64_t* out_pixels, int64_t* in_pixels, int64_t* pairs, int32_t* count) {
     if (!plan || !count) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan or count is NULL");
     if (algo < DISCO_ALGO_AUTO || algo > DISCO_ALGO_FUSED_DIRECT) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown algo");
     if (c_in < 1 || c_out < 1) return fail(DISCO_ERR_SHAPE, "channel counts must be >= 1");
+    if (dtype != DISCO_FLOAT32 && dtype != DISCO_BFLOAT16) return fail(DISCO_ERR_DTYPE, "unknown dtype");
     const DeviceOp& op = transpose ? plan->tr : plan->fwd;
-    const Dispatch dp = dispatch(op, algo, c_in, c_out);
+    const Dispatch dp = dispatch(op, algo, c_in, c_out, dtype);
     struct Row { const char* name; Work w; };
     std::vector<Row> rows;
     const Work& all = op.work_all;

@@ -111,6 +111,7 @@ int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& sk
 // rings first needed there (into slots whose previous ring is no longer
 // read).  Used for patterns with at most kChunkEntries entries when every
 // input channel fits one staging pass (Ci <= kCIC).
+constexpr int kSweepTile = 256;   // output longitudes (lanes) of a sweep workgroup
 constexpr int kSweepCols = 1280;  // LDS columns (per channel) of all slots of a run
 constexpr int kSweepEntries = 256;  // entries of one pattern on the sweep path
 

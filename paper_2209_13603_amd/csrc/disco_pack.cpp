@@ -182,7 +182,7 @@ int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& sk
     (void)err;
     const OpGeom& g = op.g;
     const int s = g.stride;
-    const int halo = s * (kTileQ - 1);
+    const int halo = s * (kSweepTile - 1);
     SweepHost H;
     H.covered.assign((size_t)g.n_patterns(), 0);
 

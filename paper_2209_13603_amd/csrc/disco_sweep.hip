@@ -3,7 +3,7 @@
 //
 // Same arithmetic as disco_fused.hip (Sec. 4.2's compressed product, hat-cell
 // sorted entries, MFMA 4x4x1 channel contraction), organised for light rings:
-// a workgroup owns 256 consecutive output longitudes of every pattern of one
+// a workgroup owns kSweepTile consecutive output longitudes of every pattern of one
 // run; each input ring the run reads is staged once, into an LDS slot chosen
 // at plan time, and stays there while consecutive patterns read it.  Before
 // each pattern only the rings it reads first are loaded, so an output ring
@@ -19,11 +19,11 @@ namespace disco {
 
 namespace {
 
-constexpr int kBlock = kTileQ;
+constexpr int kBlock = kSweepTile;
 constexpr int kNCQ = kCIC / 4;
-constexpr int kPF = 2;   // prefetched span columns per lane (512 columns)
-static_assert(kSweepEntries % kTileQ == 0, "entry prefetch covers whole lanes");
-constexpr int kPFE = kSweepEntries / kTileQ;  // prefetched entries per lane
+constexpr int kPF = (kBlock + 8 + kBlock - 1) / kBlock;  // prefetched span columns per lane
+static_assert(kSweepEntries % kBlock == 0, "entry prefetch covers whole lanes");
+constexpr int kPFE = kSweepEntries / kBlock;  // prefetched entries per lane
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float load_val(const float* p, int64_t i) { return p[i]; }
@@ -70,40 +70,21 @@ __device__ __forceinline__ void fma_cell(const float4& v, const float4 (&xv)[kNC
         }
 }
 
-// Entries of one cell, software-pipelined across the flat entry array (cells
-// are contiguous in it, so the entry after e is always e + 1): while the FMAs
-// of entry e run, the input of e + 1 and the offset and values of e + 2 are
-// already in flight.  (o1, v1, x1) hold entry e + 1, (o2, v2) entry e + 2.
-struct Pipe {
-    int o2;
-    float4 v0, v1, v2;
-    float4 x0[kNCQ], x1[kNCQ];
-};
-
-__device__ __forceinline__ void pipe_load(Pipe& p, int e, int ne, const int* __restrict__ eoffs,
-                                          const float4* __restrict__ evs, const float4* __restrict__ xs, int lane_col) {
-    // Advance: entry e + 1 becomes current, e + 2 becomes next.
-    p.v0 = p.v1;
-#pragma unroll
-    for (int g = 0; g < kNCQ; ++g) p.x0[g] = p.x1[g];
-    p.v1 = p.v2;
-    if (e + 1 < ne) {
-#pragma unroll
-        for (int g = 0; g < kNCQ; ++g) p.x1[g] = xs[g * kSweepCols + lane_col + p.o2];
-    }
-    if (e + 2 < ne) {
-        p.o2 = eoffs[e + 2];
-        p.v2 = evs[e + 2];
-    }
-}
-
+// Entries [e, ee) of one cell.  The LDS column offset of the next entry is
+// read one step ahead (o carries it across cells, which are contiguous in
+// the entry array), so each step issues its input and value reads at once;
+// the reads of one wave overlap the FMAs of the other waves on the SIMD.
 template <int CELL>
-__device__ __forceinline__ void run_cell(int& e, int ee, int ne, Pipe& p, const int* __restrict__ eoffs,
+__device__ __forceinline__ void run_cell(int& e, int ee, int ne, int& o, const int* __restrict__ eoffs,
                                          const float4* __restrict__ evs, const float4* __restrict__ xs,
                                          int lane_col, float (&z)[kCIC][kBasis]) {
     for (; e < ee; ++e) {
-        pipe_load(p, e, ne, eoffs, evs, xs, lane_col);
-        fma_cell<CELL>(p.v0, p.x0, z);
+        const int o_next = e + 1 < ne ? eoffs[e + 1] : 0;
+        float4 xv[kNCQ];
+#pragma unroll
+        for (int g = 0; g < kNCQ; ++g) xv[g] = xs[g * kSweepCols + lane_col + o];
+        fma_cell<CELL>(evs[e], xv, z);
+        o = o_next;
     }
 }
 
@@ -271,31 +252,24 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
 #pragma unroll
             for (int k = 0; k < kBasis; ++k) z[c][k] = 0.0f;
         const int c0 = SP.cls[0], ne = SP.cls[kCells] - SP.cls[0];
-        Pipe pp;
-        // Prime: entry 0 in (v1, x1), entry 1's offset and values in (o2, v2).
-        if (ne > 0) {
-            const int o0 = eoffs[0];
-            pp.v2 = evs[0];
-            pp.o2 = o0;
-            pipe_load(pp, -1, ne, eoffs, evs, xs, lane_col);
-        }
+        int o = ne > 0 ? eoffs[0] : 0;
         int e = 0;
-        run_cell<0>(e, SP.cls[1] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<1>(e, SP.cls[2] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<2>(e, SP.cls[3] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<3>(e, SP.cls[4] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<4>(e, SP.cls[5] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<5>(e, SP.cls[6] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<6>(e, SP.cls[7] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<7>(e, SP.cls[8] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<8>(e, SP.cls[9] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<9>(e, SP.cls[10] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<10>(e, SP.cls[11] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<11>(e, SP.cls[12] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<12>(e, SP.cls[13] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<13>(e, SP.cls[14] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<14>(e, SP.cls[15] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
-        run_cell<15>(e, SP.cls[16] - c0, ne, pp, eoffs, evs, xs, lane_col, z);
+        run_cell<0>(e, SP.cls[1] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<1>(e, SP.cls[2] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<2>(e, SP.cls[3] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<3>(e, SP.cls[4] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<4>(e, SP.cls[5] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<5>(e, SP.cls[6] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<6>(e, SP.cls[7] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<7>(e, SP.cls[8] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<8>(e, SP.cls[9] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<9>(e, SP.cls[10] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<10>(e, SP.cls[11] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<11>(e, SP.cls[12] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<12>(e, SP.cls[13] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<13>(e, SP.cls[14] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<14>(e, SP.cls[15] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<15>(e, SP.cls[16] - c0, ne, o, eoffs, evs, xs, lane_col, z);
         // Contraction on the matrix cores (see disco_fused.hip): lane l ends
         // with y[co0 + 4 quad + r][its pixel] in register r of yacc[quad].
         v4f yacc[COT / 4];

@@ -122,7 +122,7 @@ def library(path: str = LIB_PATH) -> ctypes.CDLL:
                                              P(ctypes.c_double), P(ctypes.c_int32)]
     lib.disco_kernel_timing_read.restype = ctypes.c_int
     lib.disco_kernel_work.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
-                                      ctypes.c_int32, ctypes.c_int32, ctypes.c_char_p,
+                                      ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_char_p,
                                       P(ctypes.c_int64), P(ctypes.c_int64), P(ctypes.c_int64),
                                       P(ctypes.c_int32)]
     lib.disco_kernel_work.restype = ctypes.c_int
@@ -202,16 +202,18 @@ class Plan:
         _check(library().disco_plan_query(self._h, ctypes.byref(inf)))
         return inf.as_dict()
 
-    def kernel_work(self, transpose: bool, algo, c_in: int, c_out: int, capacity: int = 16) -> dict:
+    def kernel_work(self, transpose: bool, algo, c_in: int, c_out: int, dtype: str = "fp32",
+                    capacity: int = 16) -> dict:
         """{kernel name: (out_pixels, in_pixels, pairs)} per batch item and channel
         for the kernels one call with these arguments launches."""
         algo = ALGOS[algo] if isinstance(algo, str) else int(algo)
+        dt = DISCO_BFLOAT16 if dtype == "bf16" else DISCO_FLOAT32
         names = ctypes.create_string_buffer(64 * capacity)
         outp = (ctypes.c_int64 * capacity)()
         inp = (ctypes.c_int64 * capacity)()
         pairs = (ctypes.c_int64 * capacity)()
         count = ctypes.c_int32()
-        _check(library().disco_kernel_work(self._h, int(bool(transpose)), algo, c_in, c_out, capacity,
+        _check(library().disco_kernel_work(self._h, int(bool(transpose)), algo, c_in, c_out, dt, capacity,
                                            names, outp, inp, pairs, ctypes.byref(count)))
         out = {}
         for i in range(min(count.value, capacity)):

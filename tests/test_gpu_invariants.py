@@ -176,9 +176,9 @@ def test_kernel_work_covers_the_op(name):
         n_out = (wl.nlat_in * wl.nlon_in) if transpose else (wl.nlat_out * wl.nlon_out)
         n_in = (wl.nlat_out * wl.nlon_out) if transpose else (wl.nlat_in * wl.nlon_in)
         for algo in ("gather_then_contract", "contract_then_gather", "fused", "fused_direct", "auto"):
-            for ci, co in ((wl.c_in, wl.c_out), (32, 8), (4, 64)):
-                work = plan.kernel_work(transpose, algo, ci, co)
-                say(name, transpose, algo, ci, co, work)
+            for ci, co, dt in ((wl.c_in, wl.c_out, wl.dtype), (32, 8, "fp32"), (4, 64, "fp32"), (4, 4, "bf16")):
+                work = plan.kernel_work(transpose, algo, ci, co, dt)
+                say(name, transpose, algo, ci, co, dt, work)
                 gather = [k for k in work if k in ("gather_z", "gather_y", "spectral_mac",
                                                     "sweep_gather_contract", "fused_gather_contract")]
                 assert sum(work[k][2] for k in gather) == total

@@ -118,3 +118,23 @@ def test_spectral_path_small_grids(case, op, monkeypatch):
     assert err <= FP32_TOL
     assert np.abs(y - ref).max() <= 1e-5 * np.abs(ref).max()
     plan.close()
+
+
+@pytest.mark.parametrize("algo", ["auto", "fused_direct", "gather_then_contract"])
+@pytest.mark.parametrize("op", ["forward", "transpose"])
+def test_sphere2048x4096_both_ops(op, algo):
+    """Forward and transpose on the 2048 x 4096 sphere (8 -> 8 channels), every
+    kernel schedule, on sampled output pixels against the oracle."""
+    wl = synth.WORKLOADS["sphere2048x4096"]
+    a, b = wl.nlat_in, wl.nlon_in
+    x, w = synth.random_inputs(21 if op == "forward" else 22, (1, 8, a, b), (8, 8, 9))
+    say("2048x4096", op, algo)
+    y, plan = run_gpu(wl.plan_args(), x, w, op, algo=algo)
+    pix = sample_pixels(a, b, 3, seed=5)
+    ref = run_oracle(wl.plan_args(), x, w, op, pix=pix)
+    got = y.reshape(1, 8, -1)[:, :, pix]
+    err = rel_l2(got, ref)
+    say("  rel_l2 %.3e over %d outputs" % (err, ref.size))
+    assert err <= FP32_TOL
+    assert np.isfinite(y).all()
+    plan.close()
