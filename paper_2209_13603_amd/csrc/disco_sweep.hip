@@ -48,6 +48,18 @@ __device__ __forceinline__ int xcd_remap(int bid, int nb) {
     return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
+// Where lanes write outputs that do not exist (longitudes past the ring,
+// channels past Cout).
+__device__ __align__(16) float g_sweep_sink[kBlock];
+
+// Workgroup barrier that orders LDS only: global loads in flight (the next
+// pattern's prefetch) and stores stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 template <int CELL>
 __device__ __forceinline__ void fma_cell(const float4& v, const float4 (&xv)[kNCQ], float (&z)[kCIC][kBasis]) {
     constexpr int CU = CELL / 4, CV = CELL % 4;
@@ -153,6 +165,10 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
                 wv[qd][gg] = v;
             }
     }
+    // Let the W loads land before the pattern loop (s_waitcnt vmcnt(0)):
+    // otherwise the compiler waits for them inside the loop, before every
+    // contraction, and that wait also drains the next pattern's prefetch.
+    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8));
 
     // Staging of pattern pi's new spans and entries.  Columns j = tid + 256 i
     // for i < kPF of the first span of the next pattern, and its entries, are
@@ -203,47 +219,51 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
     bool have_pf = false;
     for (int pi = R.pat_begin; pi < R.pat_end; ++pi) {
         const SPat SP = pats[pi];
-        __syncthreads();  // the previous pattern's reads of LDS are done
+        lds_barrier();  // the previous pattern's reads of LDS are done
+        const int ne = SP.cls[kCells] - SP.cls[0];
+        if (have_pf) {
+            // The prefetched columns of the first new span and the entries go
+            // in first, in straight-line code, so that their wait counts only
+            // the loads before the stores of the previous pattern.  (A pattern
+            // may read no new ring: the other phases of an output ring.)
+            if (SP.act_end > SP.act_begin) {
+                const PSpan S = acts[SP.act_begin];
+#pragma unroll
+                for (int i = 0; i < kPF; ++i) {
+                    const int j = tid + i * kBlock;
+                    if (j < S.len) {
+#pragma unroll
+                        for (int gq = 0; gq < kNCQ; ++gq) xs[gq * kSweepCols + S.lds_base + j] = pf[i][gq];
+                    }
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < kPFE; ++i) {
+                const int k = tid + i * kBlock;
+                if (k < ne) {
+                    eoffs[k] = pf_off[i];
+                    evs[k] = pf_val[i];
+                }
+            }
+        }
+        // Whatever the prefetch did not cover is loaded directly.
         for (int ai = SP.act_begin; ai < SP.act_end; ++ai) {
             const PSpan S = acts[ai];
             const int start = span_start(S);
-            const bool first = have_pf && ai == SP.act_begin;
-            for (int j = tid; j < S.len; j += kBlock) {
-                const int i = (j - tid) / kBlock;
+            const int j0 = (have_pf && ai == SP.act_begin) ? kPF * kBlock : 0;
+            for (int j = j0 + tid; j < S.len; j += kBlock) {
                 float4 v[kNCQ];
-                if (first && i < kPF) {
-#pragma unroll
-                    for (int ii = 0; ii < kPF; ++ii)
-                        if (ii == i) {
-#pragma unroll
-                            for (int gq = 0; gq < kNCQ; ++gq) v[gq] = pf[ii][gq];
-                        }
-                } else {
-                    load_col(S, start, j, v);
-                }
+                load_col(S, start, j, v);
 #pragma unroll
                 for (int gq = 0; gq < kNCQ; ++gq) xs[gq * kSweepCols + S.lds_base + j] = v[gq];
             }
         }
-        {
-            const int ebase = SP.cls[0], ne = SP.cls[kCells] - SP.cls[0];
-            for (int k = tid; k < ne; k += kBlock) {
-                const int i = (k - tid) / kBlock;
-                if (have_pf && i < kPFE) {
-#pragma unroll
-                    for (int ii = 0; ii < kPFE; ++ii)
-                        if (ii == i) {
-                            eoffs[k] = pf_off[ii];
-                            evs[k] = pf_val[ii];
-                        }
-                } else {
-                    eoffs[k] = offs[ebase + k];
-                    const PVal pv = vals[ebase + k];
-                    evs[k] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
-                }
-            }
+        for (int k = (have_pf ? kPFE * kBlock : 0) + tid; k < ne; k += kBlock) {
+            eoffs[k] = offs[SP.cls[0] + k];
+            const PVal pv = vals[SP.cls[0] + k];
+            evs[k] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
         }
-        __syncthreads();
+        lds_barrier();
         have_pf = pi + 1 < R.pat_end;
         if (have_pf) prefetch(pats[pi + 1]);
         float z[kCIC][kBasis];
@@ -251,7 +271,7 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
         for (int c = 0; c < kCIC; ++c)
 #pragma unroll
             for (int k = 0; k < kBasis; ++k) z[c][k] = 0.0f;
-        const int c0 = SP.cls[0], ne = SP.cls[kCells] - SP.cls[0];
+        const int c0 = SP.cls[0];
         int o = ne > 0 ? eoffs[0] : 0;
         int e = 0;
         run_cell<0>(e, SP.cls[1] - c0, ne, o, eoffs, evs, xs, lane_col, z);
@@ -276,12 +296,16 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
 #pragma unroll
         for (int j = 0; j < COT / 4; ++j) yacc[j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
         mfma_contract<0, COT / 4>(yacc, wv, z);
-        if (q < g.nq) {
-            const int to = SP.pattern / g.P, r = SP.pattern - (SP.pattern / g.P) * g.P;
-            const int64_t pix = (int64_t)to * g.nlon_o + (int64_t)q * g.P + r;
+        // Every lane issues the same COT stores (outputs that do not exist go
+        // to a sink), so the number of memory operations after the prefetch
+        // is fixed and its wait does not cover the stores.
+        const int to = SP.pattern / g.P, r = SP.pattern - (SP.pattern / g.P) * g.P;
+        const int64_t pix = (int64_t)to * g.nlon_o + (int64_t)q * g.P + r;
 #pragma unroll
-            for (int j = 0; j < COT; ++j)
-                if (co0 + j < Co) store_val(y, ((int64_t)b * Co + co0 + j) * n_out + pix, yacc[j / 4][j % 4]);
+        for (int j = 0; j < COT; ++j) {
+            T* dst = (q < g.nq && co0 + j < Co) ? y + ((int64_t)b * Co + co0 + j) * n_out + pix
+                                                 : (T*)g_sweep_sink + tid;
+            store_val(dst, 0, yacc[j / 4][j % 4]);
         }
     }
 }
