@@ -322,6 +322,20 @@ int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& sk
         H.runs.push_back(R);
         pat = end;
     }
+    // Longest runs first: workgroups start roughly in grid order, so the
+    // tail of the launch is made of the short runs.
+    std::vector<int64_t> cost(H.runs.size(), 0);
+    for (size_t r = 0; r < H.runs.size(); ++r)
+        for (int32_t p = H.runs[r].pat_begin; p < H.runs[r].pat_end; ++p) {
+            const SPat& P = H.pats[(size_t)p];
+            cost[r] += (P.cls[kCells] - P.cls[0]) + 24 + 2 * (P.act_end - P.act_begin);
+        }
+    std::vector<size_t> order(H.runs.size());
+    for (size_t r = 0; r < order.size(); ++r) order[r] = r;
+    std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) { return cost[a] > cost[b]; });
+    std::vector<SRun> sorted;
+    for (size_t r : order) sorted.push_back(H.runs[r]);
+    H.runs.swap(sorted);
     *out = std::move(H);
     return DISCO_OK;
 }

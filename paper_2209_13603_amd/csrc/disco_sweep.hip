@@ -48,6 +48,8 @@ __device__ __forceinline__ int xcd_remap(int bid, int nb) {
     return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
+constexpr int kEntryPad = 3;  // padding entries after a pattern's entries (lookahead reads)
+
 // Where lanes write outputs that do not exist (longitudes past the ring,
 // channels past Cout).
 __device__ __align__(16) float g_sweep_sink[kBlock];
@@ -82,21 +84,38 @@ __device__ __forceinline__ void fma_cell(const float4& v, const float4 (&xv)[kNC
         }
 }
 
-// Entries [e, ee) of one cell.  The LDS column offset of the next entry is
-// read one step ahead (o carries it across cells, which are contiguous in
-// the entry array), so each step issues its input and value reads at once;
-// the reads of one wave overlap the FMAs of the other waves on the SIMD.
+// Entries [e, ee) of one cell, with the input and values of the next entry
+// already in flight while an entry's FMAs run.  On entry (and on return) x0
+// and v0 hold the input and values of entry e and o1 the LDS column offset of
+// entry e + 1; entries are taken in pairs so that the two register sets swap
+// roles statically instead of being copied.  Cells are contiguous in the
+// entry array, so the lookahead runs across cell boundaries; the array ends
+// with two padding entries (offset 0, values 0), so the lookahead reads need
+// no bounds test.
 template <int CELL>
-__device__ __forceinline__ void run_cell(int& e, int ee, int ne, int& o, const int* __restrict__ eoffs,
-                                         const float4* __restrict__ evs, const float4* __restrict__ xs,
-                                         int lane_col, float (&z)[kCIC][kBasis]) {
-    for (; e < ee; ++e) {
-        const int o_next = e + 1 < ne ? eoffs[e + 1] : 0;
-        float4 xv[kNCQ];
+__device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], float4& v0, int& o1,
+                                         const int* __restrict__ eoffs, const float4* __restrict__ evs,
+                                         const float4* __restrict__ xs, int lane_col, float (&z)[kCIC][kBasis]) {
+    for (; e + 1 < ee; e += 2) {
+        float4 x1[kNCQ];
 #pragma unroll
-        for (int g = 0; g < kNCQ; ++g) xv[g] = xs[g * kSweepCols + lane_col + o];
-        fma_cell<CELL>(evs[e], xv, z);
-        o = o_next;
+        for (int g = 0; g < kNCQ; ++g) x1[g] = xs[g * kSweepCols + lane_col + o1];
+        const float4 v1 = evs[e + 1];
+        const int o2 = eoffs[e + 2];
+        fma_cell<CELL>(v0, x0, z);
+#pragma unroll
+        for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kSweepCols + lane_col + o2];
+        v0 = evs[e + 2];
+        o1 = eoffs[e + 3];
+        fma_cell<CELL>(v1, x1, z);
+    }
+    if (e < ee) {
+        fma_cell<CELL>(v0, x0, z);
+#pragma unroll
+        for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kSweepCols + lane_col + o1];
+        v0 = evs[e + 1];
+        o1 = eoffs[e + 2];
+        ++e;
     }
 }
 
@@ -127,8 +146,8 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
                                                   T* __restrict__ y, int Ci, int Co, int n_qtiles, int n_cotiles,
                                                   bool w_trans) {
     __shared__ float4 xs[kNCQ * kSweepCols];
-    __shared__ float4 evs[kSweepEntries];
-    __shared__ int eoffs[kSweepEntries];
+    __shared__ float4 evs[kSweepEntries + kEntryPad];
+    __shared__ int eoffs[kSweepEntries + kEntryPad];
 
     const int tid = threadIdx.x;
     const int bid = xcd_remap(blockIdx.x, gridDim.x);
@@ -263,6 +282,10 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
             const PVal pv = vals[SP.cls[0] + k];
             evs[k] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
         }
+        if (tid < kEntryPad) {
+            eoffs[ne + tid] = 0;
+            evs[ne + tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        }
         lds_barrier();
         have_pf = pi + 1 < R.pat_end;
         if (have_pf) prefetch(pats[pi + 1]);
@@ -272,24 +295,31 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
 #pragma unroll
             for (int k = 0; k < kBasis; ++k) z[c][k] = 0.0f;
         const int c0 = SP.cls[0];
-        int o = ne > 0 ? eoffs[0] : 0;
+        // Prime: entry 0 in (x0, v0), the offset of entry 1 in o1 (padding
+        // entries when the pattern has fewer).
+        float4 x0[kNCQ];
+        const int o0 = eoffs[0];
+#pragma unroll
+        for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kSweepCols + lane_col + o0];
+        float4 v0 = evs[0];
+        int o1 = eoffs[1];
         int e = 0;
-        run_cell<0>(e, SP.cls[1] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<1>(e, SP.cls[2] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<2>(e, SP.cls[3] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<3>(e, SP.cls[4] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<4>(e, SP.cls[5] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<5>(e, SP.cls[6] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<6>(e, SP.cls[7] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<7>(e, SP.cls[8] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<8>(e, SP.cls[9] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<9>(e, SP.cls[10] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<10>(e, SP.cls[11] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<11>(e, SP.cls[12] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<12>(e, SP.cls[13] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<13>(e, SP.cls[14] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<14>(e, SP.cls[15] - c0, ne, o, eoffs, evs, xs, lane_col, z);
-        run_cell<15>(e, SP.cls[16] - c0, ne, o, eoffs, evs, xs, lane_col, z);
+        run_cell<0>(e, SP.cls[1] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<1>(e, SP.cls[2] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<2>(e, SP.cls[3] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<3>(e, SP.cls[4] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<4>(e, SP.cls[5] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<5>(e, SP.cls[6] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<6>(e, SP.cls[7] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<7>(e, SP.cls[8] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<8>(e, SP.cls[9] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<9>(e, SP.cls[10] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<10>(e, SP.cls[11] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<11>(e, SP.cls[12] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<12>(e, SP.cls[13] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<13>(e, SP.cls[14] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<14>(e, SP.cls[15] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        run_cell<15>(e, SP.cls[16] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         // Contraction on the matrix cores (see disco_fused.hip): lane l ends
         // with y[co0 + 4 quad + r][its pixel] in register r of yacc[quad].
         v4f yacc[COT / 4];
