@@ -299,11 +299,12 @@ struct Dispatch {
 Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co, int32_t dtype) {
     const OpGeom& g = op.g;
     if (algo == DISCO_ALGO_AUTO) {
-        // Channel mixing goes first when the op upsamples into more (pixels x
-        // channels) than it reads; otherwise the fused gather + contraction.
-        const double gtc = (double)Ci * g.nlat_o * g.nlon_o;
-        const double ctg = (double)Co * g.nlat_i * g.nlon_i;
-        algo = ctg < gtc ? DISCO_ALGO_CONTRACT_THEN_GATHER : DISCO_ALGO_FUSED;
+        // Small ops are bound by launch latency: one direct fused kernel.
+        // Otherwise the fused schedule (spectral polar rings, ring sweep,
+        // general kernel for the rest).
+        const double out_pix_chan = (double)Co * g.nlat_o * g.nlon_o;
+        algo = out_pix_chan < (double)(1 << 18) ? DISCO_ALGO_FUSED_DIRECT : DISCO_ALGO_FUSED;
+        (void)Ci;
     }
     Dispatch d{algo, false, false, &op.packed, &op.work_all};
     d.spectral = algo == DISCO_ALGO_FUSED && op.spectral.n_rings > 0;
