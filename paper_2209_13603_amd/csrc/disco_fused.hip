@@ -32,6 +32,9 @@ namespace {
 constexpr int kBlock = kTileQ;
 constexpr int kNCQ = kCIC / 4;  // float4 channel groups per pass
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef short v4s __attribute__((ext_vector_type(4)));
+constexpr int kKK = kCIC * kBasis;  // contraction length of one channel pass (72)
+static_assert(kKK % 4 == 0, "bf16 contraction takes four kk per instruction");
 
 __device__ __forceinline__ float load_val(const float* p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float load_val(const uint16_t* p, int64_t i) {
@@ -132,6 +135,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
     __shared__ float4 evs[kChunkEntries];
     __shared__ int eoffs[kChunkEntries];
     __shared__ float ws[kCIC * kBasis * COT];
+    constexpr bool kBf16 = sizeof(T) == 2;
 
     const int tid = threadIdx.x;
     const int bid = xcd_remap(blockIdx.x, gridDim.x);
@@ -159,16 +163,17 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
                 for (int k = 0; k < kBasis; ++k) z[c][k] = 0.0f;
             __syncthreads();  // previous users of ws / xs are done
             for (int i = tid; i < kCIC * kBasis * COT; i += kBlock) {
-                // ws[j][c][k]: output channel j of the tile, pass channel c, basis k.
+                // ws[j][c][k]: output channel j of the tile, pass channel c, basis k
+                // (bf16 storage: the raw bf16 values, packed two per word).
                 const int j = i / (kCIC * kBasis), ck = i % (kCIC * kBasis), c = ck / kBasis, k = ck % kBasis;
                 const int co = co0 + j, ci = ci0 + c;
-                float v = 0.0f;
-                if (co < Co && ci < Ci) {
-                    const int64_t idx = w_trans ? ((int64_t)ci * Co + co) * kBasis + k
-                                                : ((int64_t)co * Ci + ci) * kBasis + k;
-                    v = load_val(w, idx);
+                const bool in = co < Co && ci < Ci;
+                const int64_t idx = w_trans ? ((int64_t)ci * Co + co) * kBasis + k : ((int64_t)co * Ci + ci) * kBasis + k;
+                if constexpr (kBf16) {
+                    ((uint16_t*)ws)[i] = in ? w[idx] : (uint16_t)0;
+                } else {
+                    ws[i] = in ? load_val(w, idx) : 0.0f;
                 }
-                ws[i] = v;
             }
             for (int ch = sg.chunk_begin; ch < sg.chunk_end; ++ch) {
                 const PChunk C = chunks[ch];
@@ -228,8 +233,29 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
             // W(co0 + 4 quad + i, kk) and B[j] = Z[kk] of lane 4b + j's own
             // pixel, lane l ends with y[co0 + 4 quad + r][its pixel] in
             // register r: one instruction per (kk, 4 output channels).
-            {
-                const int li = tid & 3;
+            // With bf16 storage, v_mfma_f32_4x4x4_16b_bf16 takes four kk per
+            // instruction (block b: D[i][j] += sum_kk A[i][kk] B[kk][j], lane
+            // 4b + i holding A[i][.], lane 4b + j holding B[.][j]); W is
+            // exact in bf16 and Z is rounded to bf16 for it (fp32
+            // accumulation), an error of the order of the bf16 output's own.
+            const int li = tid & 3;
+            if constexpr (kBf16) {
+                const uint16_t* ws16 = (const uint16_t*)ws;
+#pragma unroll
+                for (int g4 = 0; g4 < kKK / 4; ++g4) {
+                    v4s zb;
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int kk = 4 * g4 + u;
+                        zb[u] = (short)to_bf16(z[kk / kBasis][kk % kBasis]);
+                    }
+#pragma unroll
+                    for (int qd = 0; qd < COT / 4; ++qd) {
+                        const v4s wa = *(const v4s*)(ws16 + (4 * qd + li) * kKK + 4 * g4);
+                        yacc[qd] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(wa, zb, yacc[qd], 0, 0, 0);
+                    }
+                }
+            } else {
 #pragma unroll
                 for (int qd = 0; qd < COT / 4; ++qd) {
                     const float* wrow = ws + (4 * qd + li) * (kCIC * kBasis);

@@ -138,3 +138,26 @@ def test_sphere2048x4096_both_ops(op, algo):
     assert err <= FP32_TOL
     assert np.isfinite(y).all()
     plan.close()
+
+
+@pytest.mark.parametrize("algo", ALGOS)
+@pytest.mark.parametrize("op", ["forward", "transpose"])
+@pytest.mark.parametrize("chans", [(3, 5), (12, 6), (20, 9)], ids=lambda c: "%dto%d" % c)
+def test_bf16_small_grids(chans, op, algo):
+    """bf16 storage (fp32 accumulation; the general kernel contracts with bf16
+    matrix instructions): element-wise against the oracle on the stored
+    bf16 inputs, within the bf16 tolerance."""
+    a, b, c, d = 16, 32, 8, 16
+    tc = 3 * math.pi / c
+    Ci, Co = chans
+    xs = (2, Ci, a, b) if op == "forward" else (2, Ci, c, d)
+    ws = (Co, Ci, 9) if op == "forward" else (Ci, Co, 9)
+    x, w = synth.random_inputs(9, xs, ws, dtype="bf16")
+    say("bf16", chans, op, algo)
+    y, plan = run_gpu((a, b, c, d, tc), x, w, op, dtype="bf16", algo=algo)
+    ref = run_oracle((a, b, c, d, tc), x, w, op)
+    err = rel_l2(y, ref)
+    say("  rel_l2 %.3e" % err)
+    assert err <= BF16_TOL
+    assert np.abs(y - ref).max() <= 3e-2 * np.abs(ref).max()
+    plan.close()
