@@ -45,28 +45,62 @@ __device__ __forceinline__ float2 cmul(float2 a, float2 b) {
 }
 __device__ __forceinline__ float2 conjf2(float2 a) { return make_float2(a.x, -a.y); }
 
-// M-point complex FFT (M a power of two) in LDS, radix-2 Stockham autosort
-// between buffers a and b; sign -1 (forward) or +1 (inverse, unnormalised).
-// tw[t] = exp(-2 pi i t / (2M)); stage with sub-transform length Ls uses
-// exp(-2 pi i k / (2 Ls)) = tw[k M / Ls].  Returns the buffer with the result.
+// exp(-/+ 2 pi i t / (2M)) for t in [0, 2M), from the table tw[t] =
+// exp(-2 pi i t / (2M)), t < M (the upper half is its negative).
+__device__ __forceinline__ float2 tw_at(const float2* __restrict__ tw, int t, int M, bool inverse) {
+    float2 w = t < M ? tw[t] : make_float2(-tw[t - M].x, -tw[t - M].y);
+    if (inverse) w.y = -w.y;
+    return w;
+}
+
+// M-point complex FFT (M a power of two) in LDS, Stockham autosort between
+// buffers a and b: radix-4 stages, then one radix-2 stage if log2 M is odd;
+// sign -1 (forward) or +1 (inverse, unnormalised).  A stage combining
+// sub-transforms of length Ls reads a[j + r M / R] (r < R), twiddles input
+// r by exp(-/+ 2 pi i r k / (R Ls)) with k = j mod Ls, takes the R-point DFT
+// and writes output s to b[R (j - k) + k + s Ls].  Returns the buffer with
+// the result.
 __device__ float2* fft_lds(float2* a, float2* b, int M, const float2* __restrict__ tw, bool inverse) {
-    const int half = M >> 1;
-    for (int Ls = 1; Ls < M; Ls <<= 1) {
-        const int tstep = M / Ls;
+    int Ls = 1;
+    const int q = M >> 2;
+    for (; 4 * Ls <= M; Ls <<= 2) {
+        const int tstep = M / (2 * Ls);
+        for (int j = threadIdx.x; j < q; j += blockDim.x) {
+            const int k = j & (Ls - 1);
+            const int t = k * tstep;
+            const float2 v0 = a[j];
+            const float2 v1 = cmul(a[j + q], tw_at(tw, t, M, inverse));
+            const float2 v2 = cmul(a[j + 2 * q], tw_at(tw, 2 * t, M, inverse));
+            const float2 v3 = cmul(a[j + 3 * q], tw_at(tw, 3 * t, M, inverse));
+            const float2 s02 = cadd(v0, v2), d02 = csub(v0, v2);
+            const float2 s13 = cadd(v1, v3), d13 = csub(v1, v3);
+            // -i d13 (forward) or +i d13 (inverse)
+            const float2 jd13 = inverse ? make_float2(-d13.y, d13.x) : make_float2(d13.y, -d13.x);
+            const int o = ((j - k) << 2) + k;
+            b[o] = cadd(s02, s13);
+            b[o + Ls] = cadd(d02, jd13);
+            b[o + 2 * Ls] = csub(s02, s13);
+            b[o + 3 * Ls] = csub(d02, jd13);
+        }
+        __syncthreads();
+        float2* tmp = a;
+        a = b;
+        b = tmp;
+    }
+    if (2 * Ls == M) {
+        const int half = M >> 1, tstep = M / Ls;
         for (int j = threadIdx.x; j < half; j += blockDim.x) {
             const int k = j & (Ls - 1);
-            float2 w = tw[k * tstep];
-            if (inverse) w.y = -w.y;
             const float2 c0 = a[j];
-            const float2 c1 = cmul(a[j + half], w);
+            const float2 c1 = cmul(a[j + half], tw_at(tw, k * tstep, M, inverse));
             const int o = ((j - k) << 1) + k;
             b[o] = cadd(c0, c1);
             b[o + Ls] = csub(c0, c1);
         }
         __syncthreads();
-        float2* t = a;
+        float2* tmp = a;
         a = b;
-        b = t;
+        b = tmp;
     }
     return a;
 }
