@@ -109,11 +109,14 @@ int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& sk
 // patterns for one 256-longitude tile, keeping the spans of the input rings
 // the run reads resident in LDS slots; before each pattern it stages only the
 // rings first needed there (into slots whose previous ring is no longer
-// read).  Used for patterns with at most kChunkEntries entries when every
+// read).  Used for patterns with at most kSweepEntries entries when every
 // input channel fits one staging pass (Ci <= kCIC).
 constexpr int kSweepTile = 256;   // output longitudes (lanes) of a sweep workgroup
-constexpr int kSweepCols = 1280;  // LDS columns (per channel) of all slots of a run
-constexpr int kSweepEntries = 256;  // entries of one pattern on the sweep path
+// LDS of a sweep workgroup: 2 x kSweepCols float4 of input plus the entry
+// table, 39.5 KB, so that four workgroups (one wave per SIMD each) share a
+// CU's 160 KB.  Rings with 128 entries or more are the spectral path's.
+constexpr int kSweepCols = 1152;  // LDS columns (per channel) of all slots of a run
+constexpr int kSweepEntries = 128;  // entries of one pattern on the sweep path
 
 struct SRun { int32_t pat_begin, pat_end; };             // [begin, end) into SPat
 struct SPat {

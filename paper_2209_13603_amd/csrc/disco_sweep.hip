@@ -22,8 +22,7 @@ namespace {
 constexpr int kBlock = kSweepTile;
 constexpr int kNCQ = kCIC / 4;
 constexpr int kPF = (kBlock + 8 + kBlock - 1) / kBlock;  // prefetched span columns per lane
-static_assert(kSweepEntries % kBlock == 0, "entry prefetch covers whole lanes");
-constexpr int kPFE = kSweepEntries / kBlock;  // prefetched entries per lane
+constexpr int kPFE = (kSweepEntries + kBlock - 1) / kBlock;  // prefetched entries per lane
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float load_val(const float* p, int64_t i) { return p[i]; }
@@ -122,18 +121,21 @@ __device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], flo
 constexpr int kKK = kCIC * kBasis;    // contraction length of one pass (72)
 constexpr int kWG = (kKK + 15) / 16;  // W registers per 4 output channels
 
-// y[co][pixel] += sum_kk W(co, kk) Z[kk][pixel] for kk = KK.., one
-// v_mfma_f32_4x4x1_16b_f32 per (kk, 4 output channels); A is broadcast from
-// block kk % 16 (CBSZ = 4, ABID = kk % 16) of register wv[qd][kk / 16].
-template <int KK, int NQ>
-__device__ __forceinline__ void mfma_contract(v4f (&yacc)[NQ], const float (&wv)[NQ][kWG],
-                                              const float (&z)[kCIC][kBasis]) {
-    if constexpr (KK < kKK) {
+// y[co][pixel] += sum_ci W(co, ci, K) Z[ci][K][pixel] for one basis function
+// K: one v_mfma_f32_4x4x1_16b_f32 per (ci, 4 output channels); A is
+// broadcast from block kk % 16 (CBSZ = 4, ABID = kk % 16, kk = 9 ci + K) of
+// register wv[qd][kk / 16].  Called as soon as the gather has finished every
+// cell that touches K, so the matrix cores work while the VALU gathers the
+// remaining cells and the registers of Z[.][K] are free again.
+template <int K, int CI, int NQ>
+__device__ __forceinline__ void mfma_contract_k(v4f (&yacc)[NQ], const float (&wv)[NQ][kWG],
+                                                const float (&z)[kCIC][kBasis]) {
+    if constexpr (CI < kCIC) {
+        constexpr int KK = CI * kBasis + K;
 #pragma unroll
         for (int qd = 0; qd < NQ; ++qd)
-            yacc[qd] = __builtin_amdgcn_mfma_f32_4x4x1f32(wv[qd][KK / 16], z[KK / kBasis][KK % kBasis], yacc[qd], 4,
-                                                         KK % 16, 0);
-        mfma_contract<KK + 1, NQ>(yacc, wv, z);
+            yacc[qd] = __builtin_amdgcn_mfma_f32_4x4x1f32(wv[qd][KK / 16], z[CI][K], yacc[qd], 4, KK % 16, 0);
+        mfma_contract_k<K, CI + 1, NQ>(yacc, wv, z);
     }
 }
 
@@ -304,28 +306,38 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
         float4 v0 = evs[0];
         int o1 = eoffs[1];
         int e = 0;
+        // Contraction on the matrix cores: lane l ends with y[co0 + 4 quad +
+        // r][its pixel] in register r of yacc[quad].  Cells are walked row by
+        // row over the 4 x 4 grid, so basis function (a, b) is complete after
+        // cell (a + 1, b + 1) and is contracted right there.
+        v4f yacc[COT / 4];
+#pragma unroll
+        for (int j = 0; j < COT / 4; ++j) yacc[j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
         run_cell<0>(e, SP.cls[1] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         run_cell<1>(e, SP.cls[2] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         run_cell<2>(e, SP.cls[3] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         run_cell<3>(e, SP.cls[4] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         run_cell<4>(e, SP.cls[5] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         run_cell<5>(e, SP.cls[6] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        mfma_contract_k<0, 0, COT / 4>(yacc, wv, z);
         run_cell<6>(e, SP.cls[7] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        mfma_contract_k<1, 0, COT / 4>(yacc, wv, z);
         run_cell<7>(e, SP.cls[8] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        mfma_contract_k<2, 0, COT / 4>(yacc, wv, z);
         run_cell<8>(e, SP.cls[9] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         run_cell<9>(e, SP.cls[10] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        mfma_contract_k<3, 0, COT / 4>(yacc, wv, z);
         run_cell<10>(e, SP.cls[11] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        mfma_contract_k<4, 0, COT / 4>(yacc, wv, z);
         run_cell<11>(e, SP.cls[12] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        mfma_contract_k<5, 0, COT / 4>(yacc, wv, z);
         run_cell<12>(e, SP.cls[13] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         run_cell<13>(e, SP.cls[14] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        mfma_contract_k<6, 0, COT / 4>(yacc, wv, z);
         run_cell<14>(e, SP.cls[15] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        mfma_contract_k<7, 0, COT / 4>(yacc, wv, z);
         run_cell<15>(e, SP.cls[16] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        // Contraction on the matrix cores (see disco_fused.hip): lane l ends
-        // with y[co0 + 4 quad + r][its pixel] in register r of yacc[quad].
-        v4f yacc[COT / 4];
-#pragma unroll
-        for (int j = 0; j < COT / 4; ++j) yacc[j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-        mfma_contract<0, COT / 4>(yacc, wv, z);
+        mfma_contract_k<8, 0, COT / 4>(yacc, wv, z);
         // Every lane issues the same COT stores (outputs that do not exist go
         // to a sink), so the number of memory operations after the prefetch
         // is fixed and its wait does not cover the stores.
