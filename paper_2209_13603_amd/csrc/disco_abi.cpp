@@ -308,8 +308,14 @@ Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co, int32_t dtyp
     }
     Dispatch d{algo, false, false, &op.packed, &op.work_all};
     d.spectral = algo == DISCO_ALGO_FUSED && op.spectral.n_rings > 0;
-    d.sweep = algo == DISCO_ALGO_FUSED && op.sweep.n_runs > 0 && Ci <= kCIC;
-    (void)dtype;  // every kernel takes both storage types
+    // The sweep kernel addresses x and y through 32-bit buffer offsets: all
+    // kCIC input channel planes and one output plane must stay below 2^31
+    // bytes (2048 x 4096 fp32: 268 MB and 34 MB); larger grids take the
+    // general kernel.
+    const int64_t es = (int64_t)elem_bytes(dtype);
+    const bool sweep_offsets_fit = (int64_t)kCIC * g.nlat_i * g.nlon_i * es < ((int64_t)1 << 31) &&
+                                   (int64_t)g.nlat_o * g.nlon_o * es < ((int64_t)1 << 31);
+    d.sweep = algo == DISCO_ALGO_FUSED && op.sweep.n_runs > 0 && Ci <= kCIC && sweep_offsets_fit;
     if (d.sweep) {
         d.packed = &op.packed_rest;
         d.packed_work = &op.work_rest;

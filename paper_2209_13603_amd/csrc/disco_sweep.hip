@@ -35,8 +35,27 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
     u += 0x7fffu + ((u >> 16) & 1u);
     return (uint16_t)(u >> 16);
 }
-__device__ __forceinline__ void store_val(float* p, int64_t i, float v) { p[i] = v; }
-__device__ __forceinline__ void store_val(uint16_t* p, int64_t i, float v) { p[i] = to_bf16(v); }
+// Raw buffer access (word 3 of the descriptor for gfx9 raw dword access): an
+// offset at or past num_records reads 0 and drops a store, which replaces the
+// bounds tests of the channel loads and output stores, and the channel
+// stride rides in the scalar offset instead of a 64-bit VALU address add.
+constexpr int kRawBufferFlags = 0x00020000;
+constexpr int kBufferOutOfRange = (int)0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void* p, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, kRawBufferFlags);
+}
+__device__ __forceinline__ float buffer_load_val(const float*, __amdgpu_buffer_rsrc_t r, int off, int soff) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, soff, 0));
+}
+__device__ __forceinline__ float buffer_load_val(const uint16_t*, __amdgpu_buffer_rsrc_t r, int off, int soff) {
+    return __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, off, soff, 0) << 16);
+}
+__device__ __forceinline__ void buffer_store_val(float*, __amdgpu_buffer_rsrc_t r, int off, float v) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, off, 0, 0);
+}
+__device__ __forceinline__ void buffer_store_val(uint16_t*, __amdgpu_buffer_rsrc_t r, int off, float v) {
+    __builtin_amdgcn_raw_buffer_store_b16(to_bf16(v), r, off, 0, 0);
+}
 
 __host__ __device__ constexpr int cell_first(int c) { return c == 0 ? 0 : c - 1; }
 __host__ __device__ constexpr int cell_count(int c) { return (c == 0 || c == 3) ? 1 : 2; }
@@ -48,10 +67,6 @@ __device__ __forceinline__ int xcd_remap(int bid, int nb) {
 }
 
 constexpr int kEntryPad = 3;  // padding entries after a pattern's entries (lookahead reads)
-
-// Where lanes write outputs that do not exist (longitudes past the ring,
-// channels past Cout).
-__device__ __align__(16) float g_sweep_sink[kBlock];
 
 // Workgroup barrier that orders LDS only: global loads in flight (the next
 // pattern's prefetch) and stores stay in flight across it.
@@ -89,8 +104,10 @@ __device__ __forceinline__ void fma_cell(const float4& v, const float4 (&xv)[kNC
 // entry e + 1; entries are taken in pairs so that the two register sets swap
 // roles statically instead of being copied.  Cells are contiguous in the
 // entry array, so the lookahead runs across cell boundaries; the array ends
-// with two padding entries (offset 0, values 0), so the lookahead reads need
-// no bounds test.
+// with kEntryPad padding entries (offset 0, values 0), so the lookahead reads need
+// no bounds test.  The scheduling barriers keep the compiler from sinking
+// the next entry's LDS reads below the current entry's FMAs (which it does to
+// save registers, leaving the read latency exposed).
 template <int CELL>
 __device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], float4& v0, int& o1,
                                          const int* __restrict__ eoffs, const float4* __restrict__ evs,
@@ -101,12 +118,16 @@ __device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], flo
         for (int g = 0; g < kNCQ; ++g) x1[g] = xs[g * kSweepCols + lane_col + o1];
         const float4 v1 = evs[e + 1];
         const int o2 = eoffs[e + 2];
+        __builtin_amdgcn_sched_barrier(0);
         fma_cell<CELL>(v0, x0, z);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kSweepCols + lane_col + o2];
         v0 = evs[e + 2];
         o1 = eoffs[e + 3];
+        __builtin_amdgcn_sched_barrier(0);
         fma_cell<CELL>(v1, x1, z);
+        __builtin_amdgcn_sched_barrier(0);
     }
     if (e < ee) {
         fma_cell<CELL>(v0, x0, z);
@@ -162,7 +183,12 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
     const int lane_col = g.stride * tid;
     const int64_t n_in = (int64_t)g.nlat_i * g.nlon_i;
     const int64_t n_out = (int64_t)g.nlat_o * g.nlon_o;
-    const T* xb = x + (int64_t)b * Ci * n_in;
+    // x of batch item b as one buffer of Ci channel planes: channel c of a
+    // column is read at scalar offset c * plane, and channels past Ci read 0
+    // (the host keeps Ci * n_in * sizeof(T) below 2^31).
+    const int plane = (int)(n_in * (int64_t)sizeof(T));
+    const __amdgpu_buffer_rsrc_t xr = buffer_of(x + (int64_t)b * Ci * n_in, Ci * plane);
+    const int out_plane = (int)(n_out * (int64_t)sizeof(T));  // bytes of one output channel plane
     const SRun R = runs[run];
 
     // W in registers for the MFMA contraction: with CBSZ = 4 the A operand of
@@ -202,14 +228,14 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
     auto load_col = [&](const PSpan& S, int start, int j, float4 (&v)[kNCQ]) {
         int idx = start + j;
         if (idx >= g.nlon_i) idx = idx % g.nlon_i;
-        const T* xp = xb + S.row + idx;
+        const int off = (S.row + idx) * (int)sizeof(T);
 #pragma unroll
         for (int gq = 0; gq < kNCQ; ++gq) {
             const int c = 4 * gq;
-            v[gq].x = c + 0 < Ci ? load_val(xp, (int64_t)(c + 0) * n_in) : 0.0f;
-            v[gq].y = c + 1 < Ci ? load_val(xp, (int64_t)(c + 1) * n_in) : 0.0f;
-            v[gq].z = c + 2 < Ci ? load_val(xp, (int64_t)(c + 2) * n_in) : 0.0f;
-            v[gq].w = c + 3 < Ci ? load_val(xp, (int64_t)(c + 3) * n_in) : 0.0f;
+            v[gq].x = buffer_load_val(x, xr, off, (c + 0) * plane);
+            v[gq].y = buffer_load_val(x, xr, off, (c + 1) * plane);
+            v[gq].z = buffer_load_val(x, xr, off, (c + 2) * plane);
+            v[gq].w = buffer_load_val(x, xr, off, (c + 3) * plane);
         }
     };
     auto span_start = [&](const PSpan& S) {
@@ -338,16 +364,18 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
         mfma_contract_k<7, 0, COT / 4>(yacc, wv, z);
         run_cell<15>(e, SP.cls[16] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         mfma_contract_k<8, 0, COT / 4>(yacc, wv, z);
-        // Every lane issues the same COT stores (outputs that do not exist go
-        // to a sink), so the number of memory operations after the prefetch
-        // is fixed and its wait does not cover the stores.
+        // Every lane issues the same COT stores (outputs that do not exist are
+        // dropped by the buffer range check: an out-of-range offset for
+        // longitudes past the ring, an empty buffer for channels past Cout),
+        // so the number of memory operations after the prefetch is fixed and
+        // its wait does not cover the stores.
         const int to = SP.pattern / g.P, r = SP.pattern - (SP.pattern / g.P) * g.P;
-        const int64_t pix = (int64_t)to * g.nlon_o + (int64_t)q * g.P + r;
+        const int pix_off = q < g.nq ? (to * g.nlon_o + q * g.P + r) * (int)sizeof(T) : kBufferOutOfRange;
 #pragma unroll
         for (int j = 0; j < COT; ++j) {
-            T* dst = (q < g.nq && co0 + j < Co) ? y + ((int64_t)b * Co + co0 + j) * n_out + pix
-                                                 : (T*)g_sweep_sink + tid;
-            store_val(dst, 0, yacc[j / 4][j % 4]);
+            const __amdgpu_buffer_rsrc_t yr =
+                buffer_of(y + ((int64_t)b * Co + co0 + j) * n_out, co0 + j < Co ? out_plane : 0);
+            buffer_store_val(y, yr, pix_off, yacc[j / 4][j % 4]);
         }
     }
 }
