@@ -119,12 +119,22 @@ constexpr int kSweepCols = 1152;  // LDS columns (per channel) of all slots of a
 constexpr int kSweepEntries = 128;  // entries of one pattern on the sweep path
 
 struct SRun { int32_t pat_begin, pat_end; };             // [begin, end) into SPat
+// One pattern of a run, 12 dwords (the kernel keeps two in scalar registers):
+// the entries are [ent, ent + nent), sorted by hat cell, ncell[c / 4] byte
+// c % 4 = entries in cell c; the spans first read here are acts[act_begin,
+// act_begin + nact), the first of them copied inline.
 struct SPat {
     int32_t pattern;
-    int32_t act_begin, act_end;  // spans to stage before this pattern (PSpan)
-    int32_t cls[kCells + 1];     // entries, sorted by hat cell
+    int32_t act_begin;
+    int32_t nact_nent;           // nact in bits 0..7, nent in bits 8..23
+    int32_t ent;
+    uint32_t ncell[4];
+    PSpan first;                 // acts[act_begin] (zeros when nact == 0)
 };
-static_assert(sizeof(SPat) == 80, "SPat layout");
+static_assert(sizeof(SPat) == 48, "SPat layout");
+static_assert(kSweepEntries <= 255, "per-cell entry counts are bytes");
+constexpr int spat_nact(const SPat& P) { return P.nact_nent & 255; }
+constexpr int spat_nent(const SPat& P) { return (P.nact_nent >> 8) & 0xffff; }
 
 struct SweepHost {
     std::vector<SRun> runs;

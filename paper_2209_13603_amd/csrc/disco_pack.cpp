@@ -283,7 +283,8 @@ int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& sk
                 slot[(size_t)r.ti] = sl;
                 H.acts.push_back(PSpan{r.ti * g.nlon_i, dmin[(size_t)r.ti], halo + dmax[(size_t)r.ti] - dmin[(size_t)r.ti] + 1, sl * cap});
             }
-            SP.act_end = (int32_t)H.acts.size();
+            const int nact = (int)H.acts.size() - SP.act_begin;
+            if (nact > 0) SP.first = H.acts[(size_t)SP.act_begin];
             // Entries, sorted by cell.
             std::vector<std::pair<int, PEntry>> ents;
             for (int32_t e = op.pat_ptr[(size_t)p]; e < op.pat_ptr[(size_t)p + 1]; ++e) {
@@ -304,13 +305,13 @@ int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& sk
             }
             std::stable_sort(ents.begin(), ents.end(),
                              [](const std::pair<int, PEntry>& x, const std::pair<int, PEntry>& y) { return x.first < y.first; });
-            const int32_t base = (int32_t)H.entries.size();
-            int k = 0;
-            for (int c = 0; c <= kCells; ++c) {
-                while (k < (int)ents.size() && ents[(size_t)k].first < c) ++k;
-                SP.cls[c] = base + k;
+            SP.ent = (int32_t)H.entries.size();
+            SP.nact_nent = nact | ((int32_t)ents.size() << 8);
+            for (auto& pe : ents) {
+                const int c = pe.first;
+                SP.ncell[c / 4] += 1u << (8 * (c % 4));
+                H.entries.push_back(pe.second);
             }
-            for (auto& pe : ents) H.entries.push_back(pe.second);
             H.pats.push_back(SP);
             H.covered[(size_t)p] = 1;
         }
@@ -328,7 +329,7 @@ int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& sk
     for (size_t r = 0; r < H.runs.size(); ++r)
         for (int32_t p = H.runs[r].pat_begin; p < H.runs[r].pat_end; ++p) {
             const SPat& P = H.pats[(size_t)p];
-            cost[r] += (P.cls[kCells] - P.cls[0]) + 24 + 2 * (P.act_end - P.act_begin);
+            cost[r] += spat_nent(P) + 24 + 2 * spat_nact(P);
         }
     std::vector<size_t> order(H.runs.size());
     for (size_t r = 0; r < order.size(); ++r) order[r] = r;

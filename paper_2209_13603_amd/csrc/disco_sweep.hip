@@ -243,8 +243,8 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
         return start < 0 ? start + g.nlon_i : start;
     };
     auto prefetch = [&](const SPat& P) {
-        if (P.act_end > P.act_begin) {
-            const PSpan S = acts[P.act_begin];
+        if (spat_nact(P) > 0) {
+            const PSpan S = P.first;
             const int start = span_start(S);
 #pragma unroll
             for (int i = 0; i < kPF; ++i) {
@@ -252,29 +252,36 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
                 if (j < S.len) load_col(S, start, j, pf[i]);
             }
         }
-        const int ne = P.cls[kCells] - P.cls[0];
+        const int ne = spat_nent(P);
 #pragma unroll
         for (int i = 0; i < kPFE; ++i) {
             const int k = tid + i * kBlock;
             if (k < ne) {
-                pf_off[i] = offs[P.cls[0] + k];
-                const PVal pv = vals[P.cls[0] + k];
+                pf_off[i] = offs[P.ent + k];
+                const PVal pv = vals[P.ent + k];
                 pf_val[i] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
             }
         }
     };
+    // Pattern descriptors are read one pattern ahead (SPn), and each carries
+    // its first new span inline, so the scalar loads on the way from one
+    // pattern to the next are a single request issued before the previous
+    // pattern's last contraction rather than a chain of dependent ones.
+    SPat SP = pats[R.pat_begin];
+    SPat SPn = pats[R.pat_begin + 1 < R.pat_end ? R.pat_begin + 1 : R.pat_begin];
     bool have_pf = false;
     for (int pi = R.pat_begin; pi < R.pat_end; ++pi) {
-        const SPat SP = pats[pi];
         lds_barrier();  // the previous pattern's reads of LDS are done
-        const int ne = SP.cls[kCells] - SP.cls[0];
+        const int ne = spat_nent(SP);
+        const int act_end = SP.act_begin + spat_nact(SP);
+        int ai0 = SP.act_begin;
         if (have_pf) {
             // The prefetched columns of the first new span and the entries go
             // in first, in straight-line code, so that their wait counts only
             // the loads before the stores of the previous pattern.  (A pattern
             // may read no new ring: the other phases of an output ring.)
-            if (SP.act_end > SP.act_begin) {
-                const PSpan S = acts[SP.act_begin];
+            if (act_end > SP.act_begin) {
+                const PSpan S = SP.first;
 #pragma unroll
                 for (int i = 0; i < kPF; ++i) {
                     const int j = tid + i * kBlock;
@@ -283,6 +290,15 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
                         for (int gq = 0; gq < kNCQ; ++gq) xs[gq * kSweepCols + S.lds_base + j] = pf[i][gq];
                     }
                 }
+                // Columns of the first span past the prefetch, if any.
+                const int start = span_start(S);
+                for (int j = kPF * kBlock + tid; j < S.len; j += kBlock) {
+                    float4 v[kNCQ];
+                    load_col(S, start, j, v);
+#pragma unroll
+                    for (int gq = 0; gq < kNCQ; ++gq) xs[gq * kSweepCols + S.lds_base + j] = v[gq];
+                }
+                ai0 = SP.act_begin + 1;
             }
 #pragma unroll
             for (int i = 0; i < kPFE; ++i) {
@@ -293,12 +309,11 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
                 }
             }
         }
-        // Whatever the prefetch did not cover is loaded directly.
-        for (int ai = SP.act_begin; ai < SP.act_end; ++ai) {
+        // Spans and entries the prefetch did not cover are loaded directly.
+        for (int ai = ai0; ai < act_end; ++ai) {
             const PSpan S = acts[ai];
             const int start = span_start(S);
-            const int j0 = (have_pf && ai == SP.act_begin) ? kPF * kBlock : 0;
-            for (int j = j0 + tid; j < S.len; j += kBlock) {
+            for (int j = tid; j < S.len; j += kBlock) {
                 float4 v[kNCQ];
                 load_col(S, start, j, v);
 #pragma unroll
@@ -306,8 +321,8 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
             }
         }
         for (int k = (have_pf ? kPFE * kBlock : 0) + tid; k < ne; k += kBlock) {
-            eoffs[k] = offs[SP.cls[0] + k];
-            const PVal pv = vals[SP.cls[0] + k];
+            eoffs[k] = offs[SP.ent + k];
+            const PVal pv = vals[SP.ent + k];
             evs[k] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
         }
         if (tid < kEntryPad) {
@@ -316,13 +331,12 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
         }
         lds_barrier();
         have_pf = pi + 1 < R.pat_end;
-        if (have_pf) prefetch(pats[pi + 1]);
+        if (have_pf) prefetch(SPn);
         float z[kCIC][kBasis];
 #pragma unroll
         for (int c = 0; c < kCIC; ++c)
 #pragma unroll
             for (int k = 0; k < kBasis; ++k) z[c][k] = 0.0f;
-        const int c0 = SP.cls[0];
         // Prime: entry 0 in (x0, v0), the offset of entry 1 in o1 (padding
         // entries when the pattern has fewer).
         float4 x0[kNCQ];
@@ -339,37 +353,57 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
         v4f yacc[COT / 4];
 #pragma unroll
         for (int j = 0; j < COT / 4; ++j) yacc[j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-        run_cell<0>(e, SP.cls[1] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        run_cell<1>(e, SP.cls[2] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        run_cell<2>(e, SP.cls[3] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        run_cell<3>(e, SP.cls[4] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        run_cell<4>(e, SP.cls[5] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        run_cell<5>(e, SP.cls[6] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        int ce = 0;  // end of the current cell in the pattern's entries
+        ce += (int)((SP.ncell[0] >> 0) & 255u);
+        run_cell<0>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[0] >> 8) & 255u);
+        run_cell<1>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[0] >> 16) & 255u);
+        run_cell<2>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[0] >> 24) & 255u);
+        run_cell<3>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[1] >> 0) & 255u);
+        run_cell<4>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[1] >> 8) & 255u);
+        run_cell<5>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         mfma_contract_k<0, 0, COT / 4>(yacc, wv, z);
-        run_cell<6>(e, SP.cls[7] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[1] >> 16) & 255u);
+        run_cell<6>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         mfma_contract_k<1, 0, COT / 4>(yacc, wv, z);
-        run_cell<7>(e, SP.cls[8] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[1] >> 24) & 255u);
+        run_cell<7>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         mfma_contract_k<2, 0, COT / 4>(yacc, wv, z);
-        run_cell<8>(e, SP.cls[9] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        run_cell<9>(e, SP.cls[10] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[2] >> 0) & 255u);
+        run_cell<8>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[2] >> 8) & 255u);
+        run_cell<9>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         mfma_contract_k<3, 0, COT / 4>(yacc, wv, z);
-        run_cell<10>(e, SP.cls[11] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[2] >> 16) & 255u);
+        run_cell<10>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         mfma_contract_k<4, 0, COT / 4>(yacc, wv, z);
-        run_cell<11>(e, SP.cls[12] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[2] >> 24) & 255u);
+        run_cell<11>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         mfma_contract_k<5, 0, COT / 4>(yacc, wv, z);
-        run_cell<12>(e, SP.cls[13] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        run_cell<13>(e, SP.cls[14] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[3] >> 0) & 255u);
+        run_cell<12>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[3] >> 8) & 255u);
+        run_cell<13>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         mfma_contract_k<6, 0, COT / 4>(yacc, wv, z);
-        run_cell<14>(e, SP.cls[15] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[3] >> 16) & 255u);
+        run_cell<14>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         mfma_contract_k<7, 0, COT / 4>(yacc, wv, z);
-        run_cell<15>(e, SP.cls[16] - c0, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        ce += (int)((SP.ncell[3] >> 24) & 255u);
+        run_cell<15>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        const int pattern = SP.pattern;
+        SP = SPn;
+        SPn = pats[pi + 2 < R.pat_end ? pi + 2 : pi];
         mfma_contract_k<8, 0, COT / 4>(yacc, wv, z);
         // Every lane issues the same COT stores (outputs that do not exist are
         // dropped by the buffer range check: an out-of-range offset for
         // longitudes past the ring, an empty buffer for channels past Cout),
         // so the number of memory operations after the prefetch is fixed and
         // its wait does not cover the stores.
-        const int to = SP.pattern / g.P, r = SP.pattern - (SP.pattern / g.P) * g.P;
+        const int to = pattern / g.P, r = pattern - (pattern / g.P) * g.P;
         const int pix_off = q < g.nq ? (to * g.nlon_o + q * g.P + r) * (int)sizeof(T) : kBufferOutOfRange;
 #pragma unroll
         for (int j = 0; j < COT; ++j) {
