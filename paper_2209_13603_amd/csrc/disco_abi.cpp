@@ -400,10 +400,13 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
     } else if (algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
         e = launch_gather_then_contract(a, ws_ptr);
     } else {
-        // The spectral rings run on the plan's helper stream, forked from and
-        // joined back into the caller's stream, beside the direct kernels;
-        // when the sweep kernel takes the light rings, the general kernel's
-        // remaining rings follow the spectral ones there.
+        // The spectral rings' input transforms run first on the caller's
+        // stream; their products and inverse transforms then run on the
+        // plan's helper stream, forked from and joined back into the
+        // caller's stream, beside the direct kernels (they take the slots the
+        // sweep's last workgroups leave free); when the sweep kernel takes
+        // the light rings, the general kernel's remaining rings follow the
+        // spectral ones there.
         hipEvent_t fork = nullptr, join = nullptr;
         const bool fork_aux = spectral && plan->aux;
         ExecArgs as = a;
@@ -411,9 +414,10 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
             as.stream = plan->aux;
             e = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
             if (e == hipSuccess) e = hipEventCreateWithFlags(&join, hipEventDisableTiming);
+            if (e == hipSuccess) e = launch_spectral(a, ws_ptr, 1);
             if (e == hipSuccess) e = hipEventRecord(fork, stream);
             if (e == hipSuccess) e = hipStreamWaitEvent(plan->aux, fork, 0);
-            if (e == hipSuccess) e = launch_spectral(as, ws_ptr);
+            if (e == hipSuccess) e = launch_spectral(as, ws_ptr, kSpectralAll & ~1);
             if (e == hipSuccess && sweep) e = launch_fused(as, packed, (float*)((char*)ws_ptr + ws_spec));
             if (e == hipSuccess) e = hipEventRecord(join, plan->aux);
         } else if (spectral) {

@@ -256,7 +256,10 @@ size_t workspace_bytes_gather_then_contract(const ExecArgs& a);
 size_t workspace_bytes_contract_then_gather(const ExecArgs& a);
 hipError_t launch_fused(const ExecArgs& a, const PackedDev& P, float* partial_ws);
 size_t workspace_bytes_fused(const ExecArgs& a, const PackedDev& P);
-hipError_t launch_spectral(const ExecArgs& a, float* ws);
+// stages: bit 0 the input-ring transforms, bit 1 the frequency-domain
+// products, bit 2 the inverse transforms (in that order on one stream).
+constexpr int kSpectralAll = 7;
+hipError_t launch_spectral(const ExecArgs& a, float* ws, int stages = kSpectralAll);
 hipError_t launch_sweep(const ExecArgs& a);
 size_t workspace_bytes_spectral(const ExecArgs& a);
 

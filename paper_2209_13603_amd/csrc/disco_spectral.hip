@@ -23,7 +23,8 @@ namespace disco {
 namespace {
 
 constexpr int kFftBlock = 256;
-constexpr int kSpecC = 2;  // input channels per accumulation pass of k_spectral
+constexpr int kFftBatch = 8;  // global loads per thread in flight while staging a ring
+constexpr int kSpecC = 4;  // input channels per accumulation pass of k_spectral
 
 __device__ __forceinline__ float load_val(const float* p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float load_val(const uint16_t* p, int64_t i) {
@@ -46,7 +47,8 @@ __device__ __forceinline__ float2 cmul(float2 a, float2 b) {
 __device__ __forceinline__ float2 conjf2(float2 a) { return make_float2(a.x, -a.y); }
 
 // exp(-/+ 2 pi i t / (2M)) for t in [0, 2M), from the table tw[t] =
-// exp(-2 pi i t / (2M)), t < M (the upper half is its negative).
+// exp(-2 pi i t / (2M)), t < M (the upper half is its negative); the FFT
+// kernels read it from an LDS copy.
 __device__ __forceinline__ float2 tw_at(const float2* __restrict__ tw, int t, int M, bool inverse) {
     float2 w = t < M ? tw[t] : make_float2(-tw[t - M].x, -tw[t - M].y);
     if (inverse) w.y = -w.y;
@@ -60,7 +62,7 @@ __device__ __forceinline__ float2 tw_at(const float2* __restrict__ tw, int t, in
 // r by exp(-/+ 2 pi i r k / (R Ls)) with k = j mod Ls, takes the R-point DFT
 // and writes output s to b[R (j - k) + k + s Ls].  Returns the buffer with
 // the result.
-__device__ float2* fft_lds(float2* a, float2* b, int M, const float2* __restrict__ tw, bool inverse) {
+__device__ __forceinline__ float2* fft_lds(float2* a, float2* b, int M, const float2* __restrict__ tw, bool inverse) {
     int Ls = 1;
     const int q = M >> 2;
     for (; 4 * Ls <= M; Ls <<= 2) {
@@ -114,14 +116,35 @@ __global__ __launch_bounds__(kFftBlock) void k_rfft_rings(const int32_t* __restr
     extern __shared__ float2 sm[];
     float2* a = sm;
     float2* bb = sm + M;
+    float2* tws = sm + 2 * M;
     const int slot = blockIdx.x;
     const int b = blockIdx.y / Ci, ci = blockIdx.y - (blockIdx.y / Ci) * Ci;
     const int N = 2 * M;
     const T* row = x + (((int64_t)b * Ci + ci) * nlat + slot_ring[slot]) * N;
-    for (int j = threadIdx.x; j < M; j += blockDim.x)
-        a[j] = make_float2(load_val(row, 2 * j), load_val(row, 2 * j + 1));
+    // Loads in batches of kFftBatch per thread, all issued before the LDS
+    // writes (a loop with a run-time trip count would otherwise wait for
+    // each load in turn).
+    for (int j0 = threadIdx.x; j0 < M; j0 += kFftBatch * kFftBlock) {
+        float2 v[kFftBatch], t[kFftBatch];
+#pragma unroll
+        for (int u = 0; u < kFftBatch; ++u) {
+            const int j = j0 + u * kFftBlock;
+            if (j < M) {
+                v[u] = make_float2(load_val(row, 2 * j), load_val(row, 2 * j + 1));
+                t[u] = tw[j];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kFftBatch; ++u) {
+            const int j = j0 + u * kFftBlock;
+            if (j < M) {
+                a[j] = v[u];
+                tws[j] = t[u];
+            }
+        }
+    }
     __syncthreads();
-    const float2* Z = fft_lds(a, bb, M, tw, false);
+    const float2* Z = fft_lds(a, bb, M, tws, false);
     float2* out = xh + (((int64_t)slot * B + b) * Ci + ci) * (M + 1);
     for (int m = threadIdx.x; m <= M; m += blockDim.x) {
         const float2 zm = Z[m & (M - 1)];
@@ -129,7 +152,7 @@ __global__ __launch_bounds__(kFftBlock) void k_rfft_rings(const int32_t* __restr
         const float2 e = make_float2(0.5f * (zm.x + zc.x), 0.5f * (zm.y + zc.y));
         const float2 dif = csub(zm, zc);
         const float2 o = make_float2(0.5f * dif.y, -0.5f * dif.x);  // (zm - zc) / (2i)
-        const float2 w = m < M ? tw[m] : make_float2(-1.0f, 0.0f);
+        const float2 w = m < M ? tws[m] : make_float2(-1.0f, 0.0f);
         out[m] = cadd(e, cmul(w, o));
     }
 }
@@ -216,18 +239,34 @@ __global__ __launch_bounds__(kFftBlock) void k_irfft_rings(const int32_t* __rest
     extern __shared__ float2 sm[];
     float2* a = sm;
     float2* bb = sm + M;
+    float2* tws = sm + 2 * M;
     const int h = blockIdx.x;
     const int b = blockIdx.y / Co, co = blockIdx.y - (blockIdx.y / Co) * Co;
     const float2* Y = yh + (((int64_t)h * B + b) * Co + co) * (M + 1);
-    for (int m = threadIdx.x; m < M; m += blockDim.x) {
-        const float2 xm = Y[m];
-        const float2 xc = conjf2(Y[M - m]);
-        const float2 e = cadd(xm, xc);
-        const float2 o = cmul(csub(xm, xc), conjf2(tw[m]));
-        a[m] = make_float2(e.x - o.y, e.y + o.x);  // e + i o
+    for (int m0 = threadIdx.x; m0 < M; m0 += kFftBatch * kFftBlock) {
+        float2 xm[kFftBatch], xc[kFftBatch], twm[kFftBatch];
+#pragma unroll
+        for (int u = 0; u < kFftBatch; ++u) {
+            const int m = m0 + u * kFftBlock;
+            if (m < M) {
+                xm[u] = Y[m];
+                xc[u] = conjf2(Y[M - m]);
+                twm[u] = tw[m];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kFftBatch; ++u) {
+            const int m = m0 + u * kFftBlock;
+            if (m < M) {
+                tws[m] = twm[u];
+                const float2 e = cadd(xm[u], xc[u]);
+                const float2 o = cmul(csub(xm[u], xc[u]), conjf2(twm[u]));
+                a[m] = make_float2(e.x - o.y, e.y + o.x);  // e + i o
+            }
+        }
     }
     __syncthreads();
-    const float2* z = fft_lds(a, bb, M, tw, true);
+    const float2* z = fft_lds(a, bb, M, tws, true);
     const int N = 2 * M;
     const int64_t base = (((int64_t)b * Co + co) * nlat_o + rings[h]) * N;
     for (int j = threadIdx.x; j < M; j += blockDim.x) {
@@ -238,40 +277,47 @@ __global__ __launch_bounds__(kFftBlock) void k_irfft_rings(const int32_t* __rest
 }
 
 template <typename T, int COT>
-hipError_t spectral_launch(const ExecArgs& a, float* ws) {
+hipError_t spectral_launch(const ExecArgs& a, float* ws, int stages) {
     const SpectralDev& S = a.op->spectral;
     const OpGeom& g = a.op->g;
     const int M = S.M;
     float2* xh = (float2*)ws;
     float2* yh = xh + (size_t)S.n_slots * a.B * a.Ci * (M + 1);
-    const size_t lds = sizeof(float2) * 2 * (size_t)M;
-    int tk = timing_begin("spectral_rfft", a.stream);
-    hipLaunchKernelGGL((k_rfft_rings<T>), dim3(S.n_slots, a.B * a.Ci), dim3(kFftBlock), lds, a.stream,
-                       S.slot_ring, (const T*)a.x, (const float2*)S.tw, xh, a.B, a.Ci, g.nlat_i, M);
-    timing_end(tk, a.stream);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const int n_cot = (a.Co + COT - 1) / COT;
-    tk = timing_begin("spectral_mac", a.stream);
-    hipLaunchKernelGGL((k_spectral<T, COT>), dim3((M + 1 + kFftBlock - 1) / kFftBlock, S.n_rings, a.B * n_cot),
-                       dim3(kFftBlock), 0, a.stream, S.pair_ptr, S.pair_slot, S.vs, xh, (const T*)a.w, yh,
-                       a.B, a.Ci, a.Co, M, n_cot, a.w_trans);
-    timing_end(tk, a.stream);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    tk = timing_begin("spectral_irfft", a.stream);
-    hipLaunchKernelGGL((k_irfft_rings<T>), dim3(S.n_rings, a.B * a.Co), dim3(kFftBlock), lds, a.stream,
-                       S.rings, yh, (const float2*)S.tw, (T*)a.y, a.B, a.Co, g.nlat_o, M);
-    timing_end(tk, a.stream);
-    return hipGetLastError();
+    const size_t lds = sizeof(float2) * 3 * (size_t)M;  // two FFT buffers and the twiddle table
+    if (stages & 1) {
+        const int tk = timing_begin("spectral_rfft", a.stream);
+        hipLaunchKernelGGL((k_rfft_rings<T>), dim3(S.n_slots, a.B * a.Ci), dim3(kFftBlock), lds, a.stream,
+                           S.slot_ring, (const T*)a.x, (const float2*)S.tw, xh, a.B, a.Ci, g.nlat_i, M);
+        timing_end(tk, a.stream);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (stages & 2) {
+        const int n_cot = (a.Co + COT - 1) / COT;
+        const int tk = timing_begin("spectral_mac", a.stream);
+        hipLaunchKernelGGL((k_spectral<T, COT>), dim3((M + 1 + kFftBlock - 1) / kFftBlock, S.n_rings, a.B * n_cot),
+                           dim3(kFftBlock), 0, a.stream, S.pair_ptr, S.pair_slot, S.vs, xh, (const T*)a.w, yh,
+                           a.B, a.Ci, a.Co, M, n_cot, a.w_trans);
+        timing_end(tk, a.stream);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (stages & 4) {
+        const int tk = timing_begin("spectral_irfft", a.stream);
+        hipLaunchKernelGGL((k_irfft_rings<T>), dim3(S.n_rings, a.B * a.Co), dim3(kFftBlock), lds, a.stream,
+                           S.rings, yh, (const float2*)S.tw, (T*)a.y, a.B, a.Co, g.nlat_o, M);
+        timing_end(tk, a.stream);
+        return hipGetLastError();
+    }
+    return hipSuccess;
 }
 
 template <typename T>
-hipError_t spectral_dispatch(const ExecArgs& a, float* ws) {
-    if (a.Co <= 4) return spectral_launch<T, 4>(a, ws);
-    if (a.Co <= 8) return spectral_launch<T, 8>(a, ws);
-    if (a.Co <= 16) return spectral_launch<T, 16>(a, ws);
-    return spectral_launch<T, 32>(a, ws);
+hipError_t spectral_dispatch(const ExecArgs& a, float* ws, int stages) {
+    if (a.Co <= 4) return spectral_launch<T, 4>(a, ws, stages);
+    if (a.Co <= 8) return spectral_launch<T, 8>(a, ws, stages);
+    if (a.Co <= 16) return spectral_launch<T, 16>(a, ws, stages);
+    return spectral_launch<T, 32>(a, ws, stages);
 }
 
 }  // namespace
@@ -282,9 +328,9 @@ size_t workspace_bytes_spectral(const ExecArgs& a) {
     return sizeof(float2) * (size_t)(S.M + 1) * a.B * ((size_t)S.n_slots * a.Ci + (size_t)S.n_rings * a.Co);
 }
 
-hipError_t launch_spectral(const ExecArgs& a, float* ws) {
+hipError_t launch_spectral(const ExecArgs& a, float* ws, int stages) {
     if (a.op->spectral.n_rings == 0) return hipSuccess;
-    return a.dtype == 1 ? spectral_dispatch<uint16_t>(a, ws) : spectral_dispatch<float>(a, ws);
+    return a.dtype == 1 ? spectral_dispatch<uint16_t>(a, ws, stages) : spectral_dispatch<float>(a, ws, stages);
 }
 
 }  // namespace disco
