@@ -24,7 +24,6 @@ namespace {
 
 constexpr int kFftBlock = 256;
 constexpr int kFftBatch = 8;  // global loads per thread in flight while staging a ring
-constexpr int kSpecC = 4;  // input channels per accumulation pass of k_spectral
 
 __device__ __forceinline__ float load_val(const float* p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float load_val(const uint16_t* p, int64_t i) {
@@ -166,20 +165,42 @@ __global__ __launch_bounds__(kFftBlock) void k_spectral(const int32_t* __restric
                                                        const T* __restrict__ w, float2* __restrict__ yh,
                                                        int B, int Ci, int Co, int M, int n_cotiles,
                                                        bool w_trans) {
+    // Input channels per accumulation pass: four for up to 8 output
+    // channels, two above (the accumulators would cost occupancy).
+    constexpr int SC = COT <= 8 ? 4 : 2;
+    // This pass's weights as (W_3a + W_3a+2, W_3a+2 - W_3a, W_3a+1) for each
+    // (input channel, output channel, a), staged in LDS and read back by
+    // broadcast (as uniform scalar loads they would need more SGPRs than
+    // there are and spill).
+    __shared__ float wsd[SC * COT * 9];
     const int m = blockIdx.x * kFftBlock + threadIdx.x;
     const int h = blockIdx.y;
     const int b = blockIdx.z / n_cotiles;
     const int co0 = (blockIdx.z - b * n_cotiles) * COT;
-    if (m > M) return;
+    const bool active = m <= M;  // lanes past M still take part in the barriers
     const int p0 = pair_ptr[h], p1 = pair_ptr[h + 1];
     const int64_t vstride = (int64_t)(M + 1);
     float2 Y[COT];
 #pragma unroll
     for (int j = 0; j < COT; ++j) Y[j] = make_float2(0.0f, 0.0f);
-    for (int ci0 = 0; ci0 < Ci; ci0 += kSpecC) {
-        float2 E[kSpecC][3], F[kSpecC][3], G[kSpecC][3];
+    for (int ci0 = 0; ci0 < Ci; ci0 += SC) {
+        __syncthreads();  // the previous pass's reads of wsd are done
+        for (int idx = threadIdx.x; idx < SC * COT * 3; idx += kFftBlock) {
+            const int c = idx / (COT * 3), r = idx - c * (COT * 3), j = r / 3, a = r - j * 3;
+            const int ci = ci0 + c < Ci ? ci0 + c : Ci - 1;  // E, F, G are zero past Ci
+            const int co = co0 + j < Co ? co0 + j : Co - 1;
+            const int64_t base = w_trans ? ((int64_t)ci * Co + co) * kBasis : ((int64_t)co * Ci + ci) * kBasis;
+            const float w0 = load_val(w, base + 3 * a), w1 = load_val(w, base + 3 * a + 1),
+                        w2 = load_val(w, base + 3 * a + 2);
+            wsd[3 * idx + 0] = w0 + w2;
+            wsd[3 * idx + 1] = w2 - w0;
+            wsd[3 * idx + 2] = w1;
+        }
+        __syncthreads();
+        if (!active) continue;
+        float2 E[SC][3], F[SC][3], G[SC][3];
 #pragma unroll
-        for (int c = 0; c < kSpecC; ++c)
+        for (int c = 0; c < SC; ++c)
 #pragma unroll
             for (int a = 0; a < 3; ++a) {
                 E[c][a] = make_float2(0.0f, 0.0f);
@@ -193,7 +214,7 @@ __global__ __launch_bounds__(kFftBlock) void k_spectral(const int32_t* __restric
             for (int i = 0; i < 9; ++i) V[i] = v[i * vstride];
             const float2* xr = xh + (((int64_t)pair_slot[p] * B + b) * Ci) * vstride + m;
 #pragma unroll
-            for (int c = 0; c < kSpecC; ++c) {
+            for (int c = 0; c < SC; ++c) {
                 const float2 X = ci0 + c < Ci ? xr[(int64_t)(ci0 + c) * vstride] : make_float2(0.0f, 0.0f);
 #pragma unroll
                 for (int a = 0; a < 3; ++a) {
@@ -209,22 +230,19 @@ __global__ __launch_bounds__(kFftBlock) void k_spectral(const int32_t* __restric
         // Yhat[co] += sum_{c,a} (W_3a + W_3a+2) E + i (W_3a+2 - W_3a) F + W_3a+1 G
 #pragma unroll
         for (int j = 0; j < COT; ++j) {
-            const int co = co0 + j < Co ? co0 + j : Co - 1;
 #pragma unroll
-            for (int c = 0; c < kSpecC; ++c) {
-                const int ci = ci0 + c < Ci ? ci0 + c : Ci - 1;  // E, F, G are zero past Ci
-                const int64_t base = w_trans ? ((int64_t)ci * Co + co) * kBasis : ((int64_t)co * Ci + ci) * kBasis;
+            for (int c = 0; c < SC; ++c) {
 #pragma unroll
                 for (int a = 0; a < 3; ++a) {
-                    const float w0 = load_val(w, base + 3 * a), w1 = load_val(w, base + 3 * a + 1),
-                                w2 = load_val(w, base + 3 * a + 2);
-                    const float S = w0 + w2, D = w2 - w0;
+                    const float* wd = wsd + 3 * ((c * COT + j) * 3 + a);
+                    const float S = wd[0], D = wd[1], w1 = wd[2];
                     Y[j].x = fmaf(S, E[c][a].x, fmaf(-D, F[c][a].y, fmaf(w1, G[c][a].x, Y[j].x)));
                     Y[j].y = fmaf(S, E[c][a].y, fmaf(D, F[c][a].x, fmaf(w1, G[c][a].y, Y[j].y)));
                 }
             }
         }
     }
+    if (!active) return;
 #pragma unroll
     for (int j = 0; j < COT; ++j)
         if (co0 + j < Co) yh[(((int64_t)h * B + b) * Co + co0 + j) * vstride + m] = Y[j];
