@@ -45,11 +45,33 @@ __device__ __forceinline__ float2 cmul(float2 a, float2 b) {
 }
 __device__ __forceinline__ float2 conjf2(float2 a) { return make_float2(a.x, -a.y); }
 
-// exp(-/+ 2 pi i t / (2M)) for t in [0, 2M), from the table tw[t] =
-// exp(-2 pi i t / (2M)), t < M (the upper half is its negative); the FFT
-// kernels read it from an LDS copy.
-__device__ __forceinline__ float2 tw_at(const float2* __restrict__ tw, int t, int M, bool inverse) {
-    float2 w = t < M ? tw[t] : make_float2(-tw[t - M].x, -tw[t - M].y);
+// Twiddles in LDS as two short tables, hi[t >> 6] = tw[64 (t >> 6)] and
+// lo[t & 63] = tw[t & 63], whose product is tw[t] = exp(-2 pi i t / (2M))
+// (t < M) to a few ulp: 33.5 KB of LDS per FFT workgroup at M = 2048
+// instead of 48 KB with the whole table, so four workgroups share a CU.
+constexpr int kTwLo = 64;
+__host__ __device__ constexpr int tw_hi_len(int M) { return M > kTwLo ? M / kTwLo : 1; }
+
+// Fills the two tables from the global table tw (t < M); all threads.
+__device__ __forceinline__ void load_twiddles(const float2* __restrict__ tw, float2* __restrict__ thi,
+                                              float2* __restrict__ tlo, int M) {
+    for (int i = threadIdx.x; i < kTwLo + tw_hi_len(M); i += blockDim.x) {
+        if (i < kTwLo) {
+            if (i < M) tlo[i] = tw[i];
+        } else {
+            thi[i - kTwLo] = tw[kTwLo * (i - kTwLo)];
+        }
+    }
+}
+
+// exp(-/+ 2 pi i t / (2M)) for t in [0, 2M) (the upper half is the negative
+// of the lower).
+__device__ __forceinline__ float2 tw_at(const float2* __restrict__ thi, const float2* __restrict__ tlo, int t,
+                                        int M, bool inverse) {
+    const bool upper = t >= M;
+    const int tt = upper ? t - M : t;
+    float2 w = cmul(thi[tt >> 6], tlo[tt & (kTwLo - 1)]);
+    if (upper) w = make_float2(-w.x, -w.y);
     if (inverse) w.y = -w.y;
     return w;
 }
@@ -61,7 +83,8 @@ __device__ __forceinline__ float2 tw_at(const float2* __restrict__ tw, int t, in
 // r by exp(-/+ 2 pi i r k / (R Ls)) with k = j mod Ls, takes the R-point DFT
 // and writes output s to b[R (j - k) + k + s Ls].  Returns the buffer with
 // the result.
-__device__ __forceinline__ float2* fft_lds(float2* a, float2* b, int M, const float2* __restrict__ tw, bool inverse) {
+__device__ __forceinline__ float2* fft_lds(float2* a, float2* b, int M, const float2* __restrict__ thi,
+                                          const float2* __restrict__ tlo, bool inverse) {
     int Ls = 1;
     const int q = M >> 2;
     for (; 4 * Ls <= M; Ls <<= 2) {
@@ -70,9 +93,9 @@ __device__ __forceinline__ float2* fft_lds(float2* a, float2* b, int M, const fl
             const int k = j & (Ls - 1);
             const int t = k * tstep;
             const float2 v0 = a[j];
-            const float2 v1 = cmul(a[j + q], tw_at(tw, t, M, inverse));
-            const float2 v2 = cmul(a[j + 2 * q], tw_at(tw, 2 * t, M, inverse));
-            const float2 v3 = cmul(a[j + 3 * q], tw_at(tw, 3 * t, M, inverse));
+            const float2 v1 = cmul(a[j + q], tw_at(thi, tlo, t, M, inverse));
+            const float2 v2 = cmul(a[j + 2 * q], tw_at(thi, tlo, 2 * t, M, inverse));
+            const float2 v3 = cmul(a[j + 3 * q], tw_at(thi, tlo, 3 * t, M, inverse));
             const float2 s02 = cadd(v0, v2), d02 = csub(v0, v2);
             const float2 s13 = cadd(v1, v3), d13 = csub(v1, v3);
             // -i d13 (forward) or +i d13 (inverse)
@@ -93,7 +116,7 @@ __device__ __forceinline__ float2* fft_lds(float2* a, float2* b, int M, const fl
         for (int j = threadIdx.x; j < half; j += blockDim.x) {
             const int k = j & (Ls - 1);
             const float2 c0 = a[j];
-            const float2 c1 = cmul(a[j + half], tw_at(tw, k * tstep, M, inverse));
+            const float2 c1 = cmul(a[j + half], tw_at(thi, tlo, k * tstep, M, inverse));
             const int o = ((j - k) << 1) + k;
             b[o] = cadd(c0, c1);
             b[o + Ls] = csub(c0, c1);
@@ -115,7 +138,8 @@ __global__ __launch_bounds__(kFftBlock) void k_rfft_rings(const int32_t* __restr
     extern __shared__ float2 sm[];
     float2* a = sm;
     float2* bb = sm + M;
-    float2* tws = sm + 2 * M;
+    float2* tlo = sm + 2 * M;
+    float2* thi = tlo + kTwLo;
     const int slot = blockIdx.x;
     const int b = blockIdx.y / Ci, ci = blockIdx.y - (blockIdx.y / Ci) * Ci;
     const int N = 2 * M;
@@ -123,27 +147,22 @@ __global__ __launch_bounds__(kFftBlock) void k_rfft_rings(const int32_t* __restr
     // Loads in batches of kFftBatch per thread, all issued before the LDS
     // writes (a loop with a run-time trip count would otherwise wait for
     // each load in turn).
+    load_twiddles(tw, thi, tlo, M);
     for (int j0 = threadIdx.x; j0 < M; j0 += kFftBatch * kFftBlock) {
-        float2 v[kFftBatch], t[kFftBatch];
+        float2 v[kFftBatch];
 #pragma unroll
         for (int u = 0; u < kFftBatch; ++u) {
             const int j = j0 + u * kFftBlock;
-            if (j < M) {
-                v[u] = make_float2(load_val(row, 2 * j), load_val(row, 2 * j + 1));
-                t[u] = tw[j];
-            }
+            if (j < M) v[u] = make_float2(load_val(row, 2 * j), load_val(row, 2 * j + 1));
         }
 #pragma unroll
         for (int u = 0; u < kFftBatch; ++u) {
             const int j = j0 + u * kFftBlock;
-            if (j < M) {
-                a[j] = v[u];
-                tws[j] = t[u];
-            }
+            if (j < M) a[j] = v[u];
         }
     }
     __syncthreads();
-    const float2* Z = fft_lds(a, bb, M, tws, false);
+    const float2* Z = fft_lds(a, bb, M, thi, tlo, false);
     float2* out = xh + (((int64_t)slot * B + b) * Ci + ci) * (M + 1);
     for (int m = threadIdx.x; m <= M; m += blockDim.x) {
         const float2 zm = Z[m & (M - 1)];
@@ -151,7 +170,7 @@ __global__ __launch_bounds__(kFftBlock) void k_rfft_rings(const int32_t* __restr
         const float2 e = make_float2(0.5f * (zm.x + zc.x), 0.5f * (zm.y + zc.y));
         const float2 dif = csub(zm, zc);
         const float2 o = make_float2(0.5f * dif.y, -0.5f * dif.x);  // (zm - zc) / (2i)
-        const float2 w = m < M ? tws[m] : make_float2(-1.0f, 0.0f);
+        const float2 w = tw_at(thi, tlo, m, M, false);  // m = M gives -1
         out[m] = cadd(e, cmul(w, o));
     }
 }
@@ -257,10 +276,12 @@ __global__ __launch_bounds__(kFftBlock) void k_irfft_rings(const int32_t* __rest
     extern __shared__ float2 sm[];
     float2* a = sm;
     float2* bb = sm + M;
-    float2* tws = sm + 2 * M;
+    float2* tlo = sm + 2 * M;
+    float2* thi = tlo + kTwLo;
     const int h = blockIdx.x;
     const int b = blockIdx.y / Co, co = blockIdx.y - (blockIdx.y / Co) * Co;
     const float2* Y = yh + (((int64_t)h * B + b) * Co + co) * (M + 1);
+    load_twiddles(tw, thi, tlo, M);
     for (int m0 = threadIdx.x; m0 < M; m0 += kFftBatch * kFftBlock) {
         float2 xm[kFftBatch], xc[kFftBatch], twm[kFftBatch];
 #pragma unroll
@@ -276,7 +297,6 @@ __global__ __launch_bounds__(kFftBlock) void k_irfft_rings(const int32_t* __rest
         for (int u = 0; u < kFftBatch; ++u) {
             const int m = m0 + u * kFftBlock;
             if (m < M) {
-                tws[m] = twm[u];
                 const float2 e = cadd(xm[u], xc[u]);
                 const float2 o = cmul(csub(xm[u], xc[u]), conjf2(twm[u]));
                 a[m] = make_float2(e.x - o.y, e.y + o.x);  // e + i o
@@ -284,7 +304,7 @@ __global__ __launch_bounds__(kFftBlock) void k_irfft_rings(const int32_t* __rest
         }
     }
     __syncthreads();
-    const float2* z = fft_lds(a, bb, M, tws, true);
+    const float2* z = fft_lds(a, bb, M, thi, tlo, true);
     const int N = 2 * M;
     const int64_t base = (((int64_t)b * Co + co) * nlat_o + rings[h]) * N;
     for (int j = threadIdx.x; j < M; j += blockDim.x) {
@@ -301,7 +321,7 @@ hipError_t spectral_launch(const ExecArgs& a, float* ws, int stages) {
     const int M = S.M;
     float2* xh = (float2*)ws;
     float2* yh = xh + (size_t)S.n_slots * a.B * a.Ci * (M + 1);
-    const size_t lds = sizeof(float2) * 3 * (size_t)M;  // two FFT buffers and the twiddle table
+    const size_t lds = sizeof(float2) * (2 * (size_t)M + kTwLo + tw_hi_len(M));  // two FFT buffers, twiddle tables
     if (stages & 1) {
         const int tk = timing_begin("spectral_rfft", a.stream);
         hipLaunchKernelGGL((k_rfft_rings<T>), dim3(S.n_slots, a.B * a.Ci), dim3(kFftBlock), lds, a.stream,

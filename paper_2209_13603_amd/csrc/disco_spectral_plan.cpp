@@ -55,8 +55,8 @@ int build_spectral(const HostOp& op, int min_entries, SpectralHost* sp, std::vec
     heavy->assign((size_t)g.n_patterns(), 0);
     *sp = SpectralHost{};
     const int N = g.nlon_i;
-    // N <= 8192: the device FFTs keep two M-point buffers and the M-entry
-    // twiddle table in LDS (24 M bytes, 96 KB at M = 4096).
+    // N <= 8192: the device FFTs keep two M-point buffers and two short
+    // twiddle tables in LDS (about 16 M bytes, 65 KB at M = 4096).
     if (g.P != 1 || g.stride != 1 || g.nlon_o != N || !is_pow2(N) || N < 64 || N > 8192) return DISCO_OK;
     const int M = N / 2;
 
