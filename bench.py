@@ -34,6 +34,7 @@ SOURCE_DIRS = [os.path.join(ROOT, "paper_2209_13603_amd", "csrc"), os.path.join(
 DEVICE_KERNEL = {"gather_z": "k_gather_z", "contract_z": "k_contract_z", "contract_x": "k_contract_x",
                  "gather_y": "k_gather_y", "fused_gather_contract": "k_fused",
                  "reduce_partials": "k_reduce_partials", "sweep_gather_contract": "k_sweep",
+                 "sweep_gather_z": "k_sweep",
                  "spectral_rfft": "k_rfft_rings", "spectral_mac": "k_spectral",
                  "spectral_irfft": "k_irfft_rings"}
 COPY_PROBE_BYTES = 256 << 20   # per direction, fp32 negation used as the plain copy kernel
@@ -73,7 +74,7 @@ def kernel_model(name, wl, work, es):
     """
     B, Ci, Co = wl.batch, wl.c_in, wl.c_out
     outp, inp, pairs = work
-    if name == "gather_z":
+    if name in ("gather_z", "sweep_gather_z"):
         return (B * Ci * inp * es + B * Ci * 9 * outp * 4, 2.0 * pairs * B * Ci, "hbm")
     if name == "contract_z":
         return (B * Ci * 9 * outp * 4 + B * Co * outp * es, 2.0 * B * Ci * 9 * Co * outp, "hbm")

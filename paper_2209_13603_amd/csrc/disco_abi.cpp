@@ -219,6 +219,13 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
     if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
     if (!sp.rings.empty()) {
         if ((s = upload_spectral(sp, &d->spectral)) != DISCO_OK) return s;
+        std::vector<uint8_t> flag((size_t)h.g.nlat_o, 0);
+        for (int32_t r : sp.rings) flag[(size_t)r] = 1;
+        e = hipMalloc((void**)&d->spectral_ring, flag.size());
+        if (e != hipSuccess) { d->spectral_ring = nullptr; return hip_fail(e, "hipMalloc(spectral ring flags)"); }
+        e = hipMemcpy(d->spectral_ring, flag.data(), flag.size(), hipMemcpyHostToDevice);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpy(spectral ring flags)");
+        d->bytes += (int64_t)flag.size();
         if ((s = upload_packed(h, heavy, &d->packed_light)) != DISCO_OK) return s;
         d->bytes += d->spectral.bytes + d->packed_light.bytes;
         std::vector<uint8_t> light(heavy.size());
@@ -241,6 +248,17 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
         for (size_t i = 0; i < rest_skip.size(); ++i) rest_skip[i] = !rest_skip[i];
         d->work_sweep = pattern_work(h, sw.covered);
         d->work_rest = pattern_work(h, rest_skip);
+        std::vector<int32_t> rest;
+        for (size_t i = 0; i < rest_skip.size(); ++i)
+            if (rest_skip[i]) rest.push_back((int32_t)i);
+        if (!rest.empty()) {
+            e = hipMalloc((void**)&d->rest_pats, sizeof(int32_t) * rest.size());
+            if (e != hipSuccess) { d->rest_pats = nullptr; return hip_fail(e, "hipMalloc(rest patterns)"); }
+            e = hipMemcpy(d->rest_pats, rest.data(), sizeof(int32_t) * rest.size(), hipMemcpyHostToDevice);
+            if (e != hipSuccess) return hip_fail(e, "hipMemcpy(rest patterns)");
+            d->n_rest_pats = (int32_t)rest.size();
+            d->bytes += (int64_t)(sizeof(int32_t) * rest.size());
+        }
     }
     return DISCO_OK;
 }
@@ -248,8 +266,13 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
 void free_op(DeviceOp* d) {
     if (d->pat_ptr) (void)hipFree(d->pat_ptr);
     if (d->entries) (void)hipFree(d->entries);
+    if (d->rest_pats) (void)hipFree(d->rest_pats);
+    if (d->spectral_ring) (void)hipFree(d->spectral_ring);
+    d->spectral_ring = nullptr;
     d->pat_ptr = nullptr;
     d->entries = nullptr;
+    d->rest_pats = nullptr;
+    d->n_rest_pats = 0;
     free_packed(&d->packed);
     free_packed(&d->packed_light);
     free_packed(&d->packed_rest);
@@ -607,7 +630,23 @@ disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t a
     struct Row { const char* name; Work w; };
     std::vector<Row> rows;
     const Work& all = op.work_all;
-    if (dp.algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
+    ExecArgs ea{};
+    ea.op = &op;
+    ea.dtype = dtype;
+    ea.B = 1;
+    ea.Ci = c_in;
+    ea.Co = c_out;
+    if (dp.algo == DISCO_ALGO_GATHER_THEN_CONTRACT && gather_z_split(ea)) {
+        rows.push_back({"sweep_gather_z", op.work_sweep});
+        if (op.n_rest_pats > 0) rows.push_back({"gather_z", op.work_rest});
+        rows.push_back({"contract_z", Work{all.out_pixels - op.work_spectral.out_pixels, 0, 0}});
+        if (op.spectral.n_rings > 0) {
+            const Work& sw = op.work_spectral;
+            rows.push_back({"spectral_rfft", Work{0, sw.in_pixels, 0}});
+            rows.push_back({"spectral_mac", Work{0, 0, sw.pairs}});
+            rows.push_back({"spectral_irfft", Work{sw.out_pixels, 0, 0}});
+        }
+    } else if (dp.algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
         rows.push_back({"gather_z", all});
         rows.push_back({"contract_z", Work{all.out_pixels, 0, 0}});
     } else if (dp.algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {

@@ -222,6 +222,9 @@ struct DeviceOp {
     SpectralDev spectral;
     SweepDev sweep;          // light patterns walked by the sweep kernel (Ci <= kCIC)
     PackedDev packed_rest;   // light patterns the sweep runs do not cover
+    int32_t* rest_pats = nullptr;  // device: those patterns' indices (gather-then-contract schedule)
+    int32_t n_rest_pats = 0;
+    uint8_t* spectral_ring = nullptr;  // device, nlat_o: 1 for output rings the spectral path writes
     int32_t* pat_ptr = nullptr;  // device, n_patterns + 1
     DevEntry* entries = nullptr;  // device
     int64_t n_entries = 0;
@@ -251,6 +254,8 @@ int timing_begin(const char* name, hipStream_t s);
 void timing_end(int token, hipStream_t s);
 
 hipError_t launch_gather_then_contract(const ExecArgs& a, float* z_ws);
+hipError_t launch_sweep_z(const ExecArgs& a, float* z);   // disco_sweep.hip
+bool gather_z_split(const ExecArgs& a);                   // sweep + spectral Z schedule usable
 hipError_t launch_contract_then_gather(const ExecArgs& a, float* xc_ws);
 size_t workspace_bytes_gather_then_contract(const ExecArgs& a);
 size_t workspace_bytes_contract_then_gather(const ExecArgs& a);

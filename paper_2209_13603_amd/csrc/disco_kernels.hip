@@ -55,15 +55,16 @@ __device__ __forceinline__ float w_at(const T* w, int co, int ci, int k, int Ci,
 
 // ---------------------------------------------------------------------------
 // Gather of x into Z (9 planes per input channel).
-// grid: (ceil(nq / 256), n_patterns, B * ceil(C / CG)); one lane per output
-// longitude q of the pattern's ring and phase.
+// grid: (ceil(nq / 256), number of patterns, B * ceil(C / CG)); one lane per
+// output longitude q of the pattern's ring and phase; the patterns are all of
+// them, or the list pat_list when it is given.
 template <typename T, int CG>
 __global__ __launch_bounds__(kBlock) void k_gather_z(const int32_t* __restrict__ pat_ptr,
                                                      const DevEntry* __restrict__ ent, OpGeom g,
                                                      const T* __restrict__ x, float* __restrict__ z,
-                                                     int C, int n_cgroups) {
+                                                     int C, int n_cgroups, const int32_t* __restrict__ pat_list) {
     const int q = blockIdx.x * kBlock + threadIdx.x;
-    const int pat = blockIdx.y;
+    const int pat = pat_list ? pat_list[blockIdx.y] : (int)blockIdx.y;
     const int b = blockIdx.z / n_cgroups;
     const int c0 = (blockIdx.z % n_cgroups) * CG;
     if (q >= g.nq) return;
@@ -100,16 +101,19 @@ __global__ __launch_bounds__(kBlock) void k_gather_z(const int32_t* __restrict__
     }
 }
 
-// Channel contraction of Z: y[b,co,n] = sum_{ci,k} W(co,ci,k) Z[b,ci,k,n].
-// grid: (ceil(N / 256), B, ceil(Co / COT)).
+// Channel contraction of Z: y[b,co,n] = sum_{ci,k} W(co,ci,k) Z[b,ci,k,n],
+// except on the output rings flagged in skip_ring (when given), whose y
+// another kernel writes.  grid: (ceil(N / 256), B, ceil(Co / COT)).
 template <typename T, int COT>
 __global__ __launch_bounds__(kBlock) void k_contract_z(const float* __restrict__ z,
                                                        const T* __restrict__ w, T* __restrict__ y,
-                                                       int Ci, int Co, int64_t N, bool w_trans) {
+                                                       int Ci, int Co, int64_t N, bool w_trans,
+                                                       const uint8_t* __restrict__ skip_ring, int nlon_o) {
     const int64_t n = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     const int b = blockIdx.y;
     const int co0 = blockIdx.z * COT;
     if (n >= N) return;
+    if (skip_ring && skip_ring[n / nlon_o]) return;
     float acc[COT];
 #pragma unroll
     for (int j = 0; j < COT; ++j) acc[j] = 0.0f;
@@ -198,26 +202,53 @@ __global__ __launch_bounds__(kBlock) void k_gather_y(const int32_t* __restrict__
     }
 }
 
+// The gather writes Z for every pattern the contraction then reads.  When
+// the op has sweep runs (gather_z_split), the sweep kernel's Z mode gathers
+// the patterns it covers, k_gather_z the light ones it does not, and the
+// heavy polar rings, whose windows are whole rings (a Z there would take nine
+// inverse FFTs per input channel and ring), keep the spectral path, which
+// writes their y; the contraction skips those rings.
 template <typename T>
-hipError_t gather_then_contract(const ExecArgs& a, float* z) {
+hipError_t gather_then_contract(const ExecArgs& a, float* z, float* spec_ws) {
     const OpGeom& g = a.op->g;
+    const DeviceOp& op = *a.op;
+    const bool split = gather_z_split(a);
     constexpr int CG = 4;
     const int ncg = (a.Ci + CG - 1) / CG;
-    dim3 grid1((g.nq + kBlock - 1) / kBlock, g.n_patterns(), a.B * ncg);
-    int tk = timing_begin("gather_z", a.stream);
-    hipLaunchKernelGGL((k_gather_z<T, CG>), grid1, dim3(kBlock), 0, a.stream, a.op->pat_ptr,
-                       a.op->entries, g, (const T*)a.x, z, a.Ci, ncg);
-    timing_end(tk, a.stream);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    hipError_t e = hipSuccess;
+    if (split) {
+        e = launch_sweep_z(a, z);
+        if (e != hipSuccess) return e;
+        if (op.n_rest_pats > 0) {
+            dim3 grid1((g.nq + kBlock - 1) / kBlock, op.n_rest_pats, a.B * ncg);
+            const int tk = timing_begin("gather_z", a.stream);
+            hipLaunchKernelGGL((k_gather_z<T, CG>), grid1, dim3(kBlock), 0, a.stream, op.pat_ptr, op.entries, g,
+                               (const T*)a.x, z, a.Ci, ncg, (const int32_t*)op.rest_pats);
+            timing_end(tk, a.stream);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+    } else {
+        dim3 grid1((g.nq + kBlock - 1) / kBlock, g.n_patterns(), a.B * ncg);
+        const int tk = timing_begin("gather_z", a.stream);
+        hipLaunchKernelGGL((k_gather_z<T, CG>), grid1, dim3(kBlock), 0, a.stream, op.pat_ptr, op.entries, g,
+                           (const T*)a.x, z, a.Ci, ncg, (const int32_t*)nullptr);
+        timing_end(tk, a.stream);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     const int64_t N = (int64_t)g.nlat_o * g.nlon_o;
     constexpr int COT = 8;
     dim3 grid2((unsigned)((N + kBlock - 1) / kBlock), a.B, (a.Co + COT - 1) / COT);
-    tk = timing_begin("contract_z", a.stream);
+    const int tk = timing_begin("contract_z", a.stream);
+    const uint8_t* skip = split && op.spectral.n_rings > 0 ? op.spectral_ring : nullptr;
     hipLaunchKernelGGL((k_contract_z<T, COT>), grid2, dim3(kBlock), 0, a.stream, z,
-                       (const T*)a.w, (T*)a.y, a.Ci, a.Co, N, a.w_trans);
+                       (const T*)a.w, (T*)a.y, a.Ci, a.Co, N, a.w_trans, skip, g.nlon_o);
     timing_end(tk, a.stream);
-    return hipGetLastError();
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (skip) e = launch_spectral(a, spec_ws);
+    return e;
 }
 
 template <typename T>
@@ -244,9 +275,25 @@ hipError_t contract_then_gather(const ExecArgs& a, float* xc) {
 
 }  // namespace
 
-size_t workspace_bytes_gather_then_contract(const ExecArgs& a) {
+static size_t z_bytes(const ExecArgs& a) {
     const OpGeom& g = a.op->g;
-    return sizeof(float) * (size_t)a.B * a.Ci * kBasis * (size_t)g.nlat_o * g.nlon_o;
+    const size_t b = sizeof(float) * (size_t)a.B * a.Ci * kBasis * (size_t)g.nlat_o * g.nlon_o;
+    return (b + 255) & ~(size_t)255;
+}
+
+bool gather_z_split(const ExecArgs& a) {
+    // Z mode of the sweep: x channel groups and 36 Z planes addressed with
+    // 32-bit buffer offsets.
+    const OpGeom& g = a.op->g;
+    const int64_t es = a.dtype == 1 ? 2 : 4;
+    return a.op->sweep.n_runs > 0 && (int64_t)kCIC * g.nlat_i * g.nlon_i * es < ((int64_t)1 << 31) &&
+           (int64_t)4 * kBasis * g.nlat_o * g.nlon_o * 4 < ((int64_t)1 << 31);
+}
+
+size_t workspace_bytes_gather_then_contract(const ExecArgs& a) {
+    size_t b = z_bytes(a);
+    if (gather_z_split(a) && a.op->spectral.n_rings > 0) b += workspace_bytes_spectral(a);
+    return b;
 }
 
 size_t workspace_bytes_contract_then_gather(const ExecArgs& a) {
@@ -255,7 +302,8 @@ size_t workspace_bytes_contract_then_gather(const ExecArgs& a) {
 }
 
 hipError_t launch_gather_then_contract(const ExecArgs& a, float* z_ws) {
-    return a.dtype == 1 ? gather_then_contract<uint16_t>(a, z_ws) : gather_then_contract<float>(a, z_ws);
+    float* spec_ws = (float*)((char*)z_ws + z_bytes(a));
+    return a.dtype == 1 ? gather_then_contract<uint16_t>(a, z_ws, spec_ws) : gather_then_contract<float>(a, z_ws, spec_ws);
 }
 
 hipError_t launch_contract_then_gather(const ExecArgs& a, float* xc_ws) {

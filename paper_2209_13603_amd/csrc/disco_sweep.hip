@@ -9,6 +9,10 @@
 // each pattern only the rings it reads first are loaded, so an output ring
 // costs one new input-ring span instead of the ~7 its window covers.  All
 // input channels are resident (Ci <= kCIC), so a pattern needs one pass.
+//
+// With ZOUT the same walk writes the gathered sums Z[b, c, k, pixel] (fp32)
+// instead of contracting them: the gather half of the gather-then-contract
+// schedule, one launch per group of kCIC input channels.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -148,6 +152,18 @@ constexpr int kWG = (kKK + 15) / 16;  // W registers per 4 output channels
 // register wv[qd][kk / 16].  Called as soon as the gather has finished every
 // cell that touches K, so the matrix cores work while the VALU gathers the
 // remaining cells and the registers of Z[.][K] are free again.
+// Z[.][K] of the lane's pixel for the kCIC channels of this launch: channels
+// 4 h .. 4 h + 3 go through buffer zr[h] (9 planes per channel, plane bytes
+// zplane), channel c at scalar offset (9 (c % 4) + K) zplane.
+template <int K>
+__device__ __forceinline__ void store_z_k(const __amdgpu_buffer_rsrc_t (&zr)[kNCQ], int off, int zplane,
+                                          const float (&z)[kCIC][kBasis]) {
+#pragma unroll
+    for (int c = 0; c < kCIC; ++c)
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(z[c][K]), zr[c / 4], off, (kBasis * (c % 4) + K) * zplane,
+                                              0);
+}
+
 template <int K, int CI, int NQ>
 __device__ __forceinline__ void mfma_contract_k(v4f (&yacc)[NQ], const float (&wv)[NQ][kWG],
                                                 const float (&z)[kCIC][kBasis]) {
@@ -160,14 +176,17 @@ __device__ __forceinline__ void mfma_contract_k(v4f (&yacc)[NQ], const float (&w
     }
 }
 
-// grid: (n_runs * n_qtiles, B * n_cotiles); requires Ci <= kCIC.
-template <typename T, int COT>
+// grid: (n_runs * n_qtiles, B * n_cotiles); requires Ci <= kCIC.  With ZOUT
+// the second grid dimension runs over (batch item, group of kCIC input
+// channels) instead (n_cotiles = number of channel groups) and z receives
+// Z[b, c, k, pixel] for the group's channels; w and y are not used.
+template <typename T, int COT, bool ZOUT>
 __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs, const SPat* __restrict__ pats,
                                                   const PSpan* __restrict__ acts, const int32_t* __restrict__ offs,
                                                   const PVal* __restrict__ vals, OpGeom g,
                                                   const T* __restrict__ x, const T* __restrict__ w,
-                                                  T* __restrict__ y, int Ci, int Co, int n_qtiles, int n_cotiles,
-                                                  bool w_trans) {
+                                                  T* __restrict__ y, float* __restrict__ zout, int Ci, int Co,
+                                                  int n_qtiles, int n_cotiles, bool w_trans) {
     __shared__ float4 xs[kNCQ * kSweepCols];
     __shared__ float4 evs[kSweepEntries + kEntryPad];
     __shared__ int eoffs[kSweepEntries + kEntryPad];
@@ -177,18 +196,33 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
     const int run = bid / n_qtiles;
     const int qt = bid - run * n_qtiles;
     const int b = blockIdx.y / n_cotiles;
-    const int co0 = (blockIdx.y - b * n_cotiles) * COT;
+    const int co0 = (blockIdx.y - b * n_cotiles) * COT;          // output channel tile
+    const int c0 = ZOUT ? (blockIdx.y - b * n_cotiles) * kCIC : 0;  // input channel group
     const int q0 = qt * kBlock;
     const int q = q0 + tid;
     const int lane_col = g.stride * tid;
     const int64_t n_in = (int64_t)g.nlat_i * g.nlon_i;
     const int64_t n_out = (int64_t)g.nlat_o * g.nlon_o;
-    // x of batch item b as one buffer of Ci channel planes: channel c of a
-    // column is read at scalar offset c * plane, and channels past Ci read 0
-    // (the host keeps Ci * n_in * sizeof(T) below 2^31).
+    // The input channels c0 .. c0 + kCIC - 1 of batch item b as one buffer of
+    // channel planes: channel c0 + c of a column is read at scalar offset
+    // c * plane, and channels past Ci read 0 (the host keeps kCIC * n_in *
+    // sizeof(T) below 2^31).
     const int plane = (int)(n_in * (int64_t)sizeof(T));
-    const __amdgpu_buffer_rsrc_t xr = buffer_of(x + (int64_t)b * Ci * n_in, Ci * plane);
+    const int nch = Ci - c0 < kCIC ? Ci - c0 : kCIC;
+    const __amdgpu_buffer_rsrc_t xr = buffer_of(x + ((int64_t)b * Ci + c0) * n_in, nch * plane);
     const int out_plane = (int)(n_out * (int64_t)sizeof(T));  // bytes of one output channel plane
+    // Z output (ZOUT): channels c0 + 4 h .. c0 + 4 h + 3 as buffer zr[h]; a
+    // buffer ends after its last existing channel (the host keeps 36 planes
+    // below 2^31 bytes).
+    const int zplane = (int)(n_out * (int64_t)sizeof(float));
+    __amdgpu_buffer_rsrc_t zr[kNCQ];
+    if constexpr (ZOUT) {
+#pragma unroll
+        for (int h = 0; h < kNCQ; ++h) {
+            const int nv = nch - 4 * h < 0 ? 0 : (nch - 4 * h < 4 ? nch - 4 * h : 4);
+            zr[h] = buffer_of(zout + ((int64_t)b * Ci + c0 + 4 * h) * kBasis * n_out, nv * kBasis * zplane);
+        }
+    }
     const SRun R = runs[run];
 
     // W in registers for the MFMA contraction: with CBSZ = 4 the A operand of
@@ -196,7 +230,7 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
     // 16 blocks, so wv[qd][g] at lane 4b + i holds W(co0 + 4 qd + i, kk =
     // 16 g + b) and one register serves 16 values of kk.
     float wv[COT / 4][kWG];
-    {
+    if constexpr (!ZOUT) {
         const int li = tid & 3, blk = (tid & 63) >> 2;
 #pragma unroll
         for (int qd = 0; qd < COT / 4; ++qd)
@@ -346,6 +380,11 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
         float4 v0 = evs[0];
         int o1 = eoffs[1];
         int e = 0;
+        int zoff = 0;
+        if constexpr (ZOUT) {
+            const int pt = SP.pattern, tz = pt / g.P, pz = pt - tz * g.P;
+            zoff = q < g.nq ? (tz * g.nlon_o + q * g.P + pz) * (int)sizeof(float) : kBufferOutOfRange;
+        }
         // Contraction on the matrix cores: lane l ends with y[co0 + 4 quad +
         // r][its pixel] in register r of yacc[quad].  Cells are walked row by
         // row over the 4 x 4 grid, so basis function (a, b) is complete after
@@ -366,43 +405,44 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
         run_cell<4>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         ce += (int)((SP.ncell[1] >> 8) & 255u);
         run_cell<5>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        mfma_contract_k<0, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<0>(zr, zoff, zplane, z); else mfma_contract_k<0, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[1] >> 16) & 255u);
         run_cell<6>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        mfma_contract_k<1, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<1>(zr, zoff, zplane, z); else mfma_contract_k<1, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[1] >> 24) & 255u);
         run_cell<7>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        mfma_contract_k<2, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<2>(zr, zoff, zplane, z); else mfma_contract_k<2, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[2] >> 0) & 255u);
         run_cell<8>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         ce += (int)((SP.ncell[2] >> 8) & 255u);
         run_cell<9>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        mfma_contract_k<3, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<3>(zr, zoff, zplane, z); else mfma_contract_k<3, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[2] >> 16) & 255u);
         run_cell<10>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        mfma_contract_k<4, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<4>(zr, zoff, zplane, z); else mfma_contract_k<4, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[2] >> 24) & 255u);
         run_cell<11>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        mfma_contract_k<5, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<5>(zr, zoff, zplane, z); else mfma_contract_k<5, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[3] >> 0) & 255u);
         run_cell<12>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         ce += (int)((SP.ncell[3] >> 8) & 255u);
         run_cell<13>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        mfma_contract_k<6, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<6>(zr, zoff, zplane, z); else mfma_contract_k<6, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[3] >> 16) & 255u);
         run_cell<14>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        mfma_contract_k<7, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<7>(zr, zoff, zplane, z); else mfma_contract_k<7, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[3] >> 24) & 255u);
         run_cell<15>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         const int pattern = SP.pattern;
         SP = SPn;
         SPn = pats[pi + 2 < R.pat_end ? pi + 2 : pi];
-        mfma_contract_k<8, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<8>(zr, zoff, zplane, z); else mfma_contract_k<8, 0, COT / 4>(yacc, wv, z);
         // Every lane issues the same COT stores (outputs that do not exist are
         // dropped by the buffer range check: an out-of-range offset for
         // longitudes past the ring, an empty buffer for channels past Cout),
         // so the number of memory operations after the prefetch is fixed and
         // its wait does not cover the stores.
+        if constexpr (ZOUT) continue;
         const int to = pattern / g.P, r = pattern - (pattern / g.P) * g.P;
         const int pix_off = q < g.nq ? (to * g.nlon_o + q * g.P + r) * (int)sizeof(T) : kBufferOutOfRange;
 #pragma unroll
@@ -423,8 +463,9 @@ hipError_t sweep_launch(const ExecArgs& a) {
     const int n_cot = (a.Co + COT - 1) / COT;
     dim3 grid((unsigned)(S.n_runs * n_qtiles), (unsigned)(a.B * n_cot));
     int tk = timing_begin("sweep_gather_contract", a.stream);
-    hipLaunchKernelGGL((k_sweep<T, COT>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats, S.acts, S.offs, S.vals,
-                       g, (const T*)a.x, (const T*)a.w, (T*)a.y, a.Ci, a.Co, n_qtiles, n_cot, a.w_trans);
+    hipLaunchKernelGGL((k_sweep<T, COT, false>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats, S.acts, S.offs,
+                       S.vals, g, (const T*)a.x, (const T*)a.w, (T*)a.y, (float*)nullptr, a.Ci, a.Co, n_qtiles, n_cot,
+                       a.w_trans);
     timing_end(tk, a.stream);
     return hipGetLastError();
 }
@@ -442,6 +483,26 @@ hipError_t sweep_dispatch(const ExecArgs& a) {
 hipError_t launch_sweep(const ExecArgs& a) {
     if (a.Ci > kCIC) return hipErrorInvalidValue;
     return a.dtype == 1 ? sweep_dispatch<uint16_t>(a) : sweep_dispatch<float>(a);
+}
+
+hipError_t launch_sweep_z(const ExecArgs& a, float* z) {
+    const OpGeom& g = a.op->g;
+    const SweepDev& S = a.op->sweep;
+    if (S.n_runs == 0) return hipSuccess;
+    const int n_qtiles = (g.nq + kBlock - 1) / kBlock;
+    const int n_cg = (a.Ci + kCIC - 1) / kCIC;
+    dim3 grid((unsigned)(S.n_runs * n_qtiles), (unsigned)(a.B * n_cg));
+    const int tk = timing_begin("sweep_gather_z", a.stream);
+    if (a.dtype == 1)
+        hipLaunchKernelGGL((k_sweep<uint16_t, 4, true>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats, S.acts,
+                           S.offs, S.vals, g, (const uint16_t*)a.x, (const uint16_t*)nullptr, (uint16_t*)nullptr, z,
+                           a.Ci, a.Co, n_qtiles, n_cg, a.w_trans);
+    else
+        hipLaunchKernelGGL((k_sweep<float, 4, true>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats, S.acts, S.offs,
+                           S.vals, g, (const float*)a.x, (const float*)nullptr, (float*)nullptr, z, a.Ci, a.Co,
+                           n_qtiles, n_cg, a.w_trans);
+    timing_end(tk, a.stream);
+    return hipGetLastError();
 }
 
 }  // namespace disco

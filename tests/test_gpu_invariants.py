@@ -169,7 +169,7 @@ def test_kernel_work_covers_the_op(name):
     for transpose in (False, True):
         # The transposed op visits the same triples, up to fp64 rounding of
         # its own geometry exactly at the cutoff.
-        total = plan.kernel_work(transpose, "gather_then_contract", 1, 1)["gather_z"][2]
+        total = plan.kernel_work(transpose, "fused_direct", 1, 1)["fused_gather_contract"][2]
         if not transpose:
             assert total == info["nnz_pairs_total"]
         assert abs(total - info["nnz_pairs_total"]) <= 1e-4 * info["nnz_pairs_total"]
@@ -179,7 +179,7 @@ def test_kernel_work_covers_the_op(name):
             for ci, co, dt in ((wl.c_in, wl.c_out, wl.dtype), (32, 8, "fp32"), (4, 64, "fp32"), (4, 4, "bf16")):
                 work = plan.kernel_work(transpose, algo, ci, co, dt)
                 say(name, transpose, algo, ci, co, dt, work)
-                gather = [k for k in work if k in ("gather_z", "gather_y", "spectral_mac",
+                gather = [k for k in work if k in ("gather_z", "gather_y", "spectral_mac", "sweep_gather_z",
                                                     "sweep_gather_contract", "fused_gather_contract")]
                 assert sum(work[k][2] for k in gather) == total
                 writers = [k for k in work if k in ("contract_z", "gather_y", "spectral_irfft",
