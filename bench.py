@@ -37,6 +37,8 @@ DEVICE_KERNEL = {"gather_z": "k_gather_z", "contract_z": "k_contract_z", "contra
                  "sweep_gather_z": "k_sweep",
                  "spectral_rfft": "k_rfft_rings", "spectral_mac": "k_spectral",
                  "spectral_irfft": "k_irfft_rings"}
+# Template argument that tells two schedules' launches of one device function apart.
+KERNEL_VARIANT = {"sweep_gather_contract": ", false>", "sweep_gather_z": ", true>"}
 COPY_PROBE_BYTES = 256 << 20   # per direction, fp32 negation used as the plain copy kernel
 COPY_PROBE_KERNEL = "neg"
 
@@ -124,10 +126,12 @@ def traffic_summary(fetch_csv, write_csv, kernel, workload, commands):
     """Write the calibrated traffic summary of `kernel` from two counter runs
     (FETCH_SIZE, then WRITE_SIZE) that each also ran the copy probe."""
     dev = DEVICE_KERNEL[kernel]
+    sel = KERNEL_VARIANT.get(kernel, "")
     out = {}
     for ctr, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
         rows = _pmc_rows(path)
-        kv = [cs[ctr] for n, cs in rows.values() if (dev + "<") in n or n.split("(")[0].endswith(dev)]
+        kv = [cs[ctr] for n, cs in rows.values()
+              if ((dev + "<") in n or n.split("(")[0].endswith(dev)) and sel in n]
         cp = [cs[ctr] for n, cs in rows.values() if COPY_PROBE_KERNEL in n.split("(")[0]]
         if not kv or not cp:
             raise SystemExit("%s: no %s dispatch (%d) or copy probe (%d)" % (path, dev, len(kv), len(cp)))
@@ -193,6 +197,49 @@ def cpu_baseline(wl, x, w, seconds=15.0):
                       "channels, fp64 ring-window mode" % (n, wl.name, wl.batch, wl.c_out)}
 
 
+def kernel_report(plan, kt, wl, transpose, algo, es):
+    """Per-kernel figures of one timed pass and the roofline object of the
+    kernel with the largest total time (achieved against HBM peak for
+    HBM-bound kernels, against the fp32 peak otherwise)."""
+    work = plan.kernel_work(transpose, algo, wl.c_in, wl.c_out, wl.dtype)
+    missing = sorted(set(kt) - set(work))
+    if missing:
+        raise SystemExit("no work figures for kernels %s" % missing)
+    per_kernel = {}
+    for k, (launches, tot_ms) in kt.items():
+        avg_ms = tot_ms / launches
+        b_, f_, bd = kernel_model(k, wl, work[k], es)
+        per_kernel[k] = {"launches": launches, "avg_us": round(avg_ms * 1e3, 2),
+                         "alg_bytes": int(b_), "alg_flops": f_, "bound": bd,
+                         "alg_gbs": round(b_ / (avg_ms / 1e3) / 1e9, 1),
+                         "alg_tflops": round(f_ / (avg_ms / 1e3) / 1e12, 2)}
+        if bd == "hbm":
+            per_kernel[k]["hbm_frac"] = round(b_ / (avg_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)
+    # The roofline names the direct kernel with the largest total time: the
+    # spectral kernels stand in for part of the direct product (their flops
+    # above are the direct method's they replace) and share the GPU with the
+    # sweep from the helper stream, which stretches their event-timed spans.
+    direct = [k for k in kt if not k.startswith("spectral_")] or list(kt)
+    name = max(direct, key=lambda k: kt[k][1])
+    launches, tot_ms = kt[name]
+    avg_ms = tot_ms / launches
+    bytes_, flops, bound = kernel_model(name, wl, work[name], es)
+    if bound == "hbm":
+        achieved = bytes_ / (avg_ms / 1e3) / 1e9
+        peak, unit = HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved = flops / (avg_ms / 1e3) / 1e12
+        peak, unit = FP32_VALU_PEAK_TFLOPS, "TFLOP/s"
+    traffic = load_traffic(name, wl.name)
+    roof = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": name,
+            "kernel_avg_us": round(avg_ms * 1e3, 2), "algorithmic_bytes": int(bytes_),
+            "algorithmic_flops": flops,
+            "algorithmic_gbs": round(bytes_ / (avg_ms / 1e3) / 1e9, 1),
+            "work_per_launch": dict(zip(("out_pixels", "in_pixels", "pairs"), work[name]))}
+    return per_kernel, roof
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -213,6 +260,9 @@ def main(argv=None):
                     help="library kernel name for --traffic-summary")
     ap.add_argument("--command", action="append", default=[],
                     help="the command that produced each counter run (recorded verbatim)")
+    ap.add_argument("--no-hbm-schedule", action="store_true",
+                    help="skip the extra pass over the gather-then-contract schedule (whose "
+                         "kernels are HBM-bound) that the JSON line reports as hbm_schedule")
     args = ap.parse_args(argv)
 
     if args.traffic_summary:
@@ -284,35 +334,35 @@ def main(argv=None):
         copy_probe(torch, dev)
 
     transpose = wl.op != "forward"
-    work = plan.kernel_work(transpose, args.algo, wl.c_in, wl.c_out, wl.dtype)
-    missing = sorted(set(kt) - set(work))
-    if missing:
-        raise SystemExit("no work figures for kernels %s" % missing)
-    per_kernel = {}
-    for k, (launches, tot_ms) in kt.items():
-        avg_ms = tot_ms / launches
-        b_, f_, bd = kernel_model(k, wl, work[k], es)
-        per_kernel[k] = {"launches": launches, "avg_us": round(avg_ms * 1e3, 2),
-                         "alg_bytes": int(b_), "alg_flops": f_, "bound": bd,
-                         "alg_gbs": round(b_ / (avg_ms / 1e3) / 1e9, 1),
-                         "alg_tflops": round(f_ / (avg_ms / 1e3) / 1e12, 2)}
-    name = max(kt, key=lambda k: kt[k][1])
-    launches, tot_ms = kt[name]
-    avg_ms = tot_ms / launches
-    bytes_, flops, bound = kernel_model(name, wl, work[name], es)
-    if bound == "hbm":
-        achieved = bytes_ / (avg_ms / 1e3) / 1e9
-        peak, unit = HBM_PEAK_GBS, "GB/s"
-    else:
-        achieved = flops / (avg_ms / 1e3) / 1e12
-        peak, unit = FP32_VALU_PEAK_TFLOPS, "TFLOP/s"
-    traffic = load_traffic(name, wl.name)
-    roof = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-            "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": name,
-            "kernel_avg_us": round(avg_ms * 1e3, 2), "algorithmic_bytes": int(bytes_),
-            "algorithmic_flops": flops,
-            "algorithmic_gbs": round(bytes_ / (avg_ms / 1e3) / 1e9, 1),
-            "work_per_launch": dict(zip(("out_pixels", "in_pixels", "pairs"), work[name]))}
+    per_kernel, roof = kernel_report(plan, kt, wl, transpose, args.algo, es)
+
+    # The same op through the gather-then-contract schedule, whose kernels
+    # move the gathered sums through HBM: their achieved GB/s against the
+    # HBM peak (the default schedule's kernels are bound by arithmetic).
+    hbm = None
+    if not args.no_hbm_schedule and args.algo != "gather_then_contract":
+        step2 = (lambda: plan.forward(x, w, y, algo="gather_then_contract")) if wl.op == "forward" else \
+            (lambda: plan.transpose(x, w, y, algo="gather_then_contract"))
+        for _ in range(2):
+            step2()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(args.steps):
+            step2()
+        end.record()
+        torch.cuda.synchronize()
+        ms2 = start.elapsed_time(end) / args.steps
+        disco.kernel_timing(True)
+        disco.kernel_timing_read()
+        for _ in range(args.steps):
+            step2()
+        torch.cuda.synchronize()
+        kt2 = disco.kernel_timing_read()
+        disco.kernel_timing(False)
+        log("gather-then-contract step %.4f ms; kernels: %s" % (ms2, kt2))
+        pk2, roof2 = kernel_report(plan, kt2, wl, transpose, "gather_then_contract", es)
+        hbm = {"algo": "gather_then_contract", "ms_per_step": ms2,
+               "value": wl.out_pix_chan / (ms2 / 1e3), "kernels": pk2, "roofline": roof2}
     op_bytes = wl.batch * (wl.c_in * (wl.nlat_in * wl.nlon_in if wl.op == "forward" else
                                       wl.nlat_out * wl.nlon_out)
                            + wl.c_out * wl.y_shape[2] * wl.y_shape[3]) * es
@@ -328,6 +378,7 @@ def main(argv=None):
         "op_algorithmic_gbs": round(op_bytes / (ms_per_step / 1e3) / 1e9, 2),
         "kernels": per_kernel,
         "roofline": roof,
+        "hbm_schedule": hbm,
         "plan_seconds": round(plan_s, 3),
     }
     if not args.no_cpu_baseline:
