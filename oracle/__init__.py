@@ -26,6 +26,10 @@ LIB_PATH = os.path.join(_HERE, "_build", "libdisco_oracle.so")
 
 QUAD_FEJER1 = 0
 QUAD_CELL_AREA = 1
+SAMPLING_CELL_CENTRED = 0
+SAMPLING_MW = 1        # pole-including (L + 1) x 2L grid of Sec. 4.2 / App. A
+BASIS_BILINEAR = 0     # 3x3 node grid, K = 9
+BASIS_AXISYM = 1       # 4 nodes along theta, K = 4
 
 
 def build(out: str = LIB_PATH, source: str = SOURCE, extra_flags=()) -> str:
@@ -58,6 +62,14 @@ class Oracle:
         lib = ctypes.CDLL(path)
         lib.oracle_colatitude.restype = ctypes.c_double
         lib.oracle_colatitude.argtypes = [ctypes.c_int, ctypes.c_int]
+        lib.oracle_colatitude_s.restype = ctypes.c_double
+        lib.oracle_colatitude_s.argtypes = [ctypes.c_int] * 3
+        lib.oracle_quadrature_s.restype = ctypes.c_int
+        lib.oracle_quadrature_s.argtypes = [ctypes.c_int] * 4 + [_dp]
+        lib.oracle_basis_axisym.restype = None
+        lib.oracle_basis_axisym.argtypes = [ctypes.c_double] * 2 + [_dp]
+        lib.oracle_psi_dense_ex.restype = ctypes.c_int
+        lib.oracle_psi_dense_ex.argtypes = [ctypes.c_int] * 6 + [ctypes.c_double] * 2 + [_dp]
         lib.oracle_longitude.restype = ctypes.c_double
         lib.oracle_longitude.argtypes = [ctypes.c_int, ctypes.c_int]
         lib.oracle_quadrature.restype = ctypes.c_int
@@ -74,19 +86,31 @@ class Oracle:
             f = getattr(lib, name)
             f.restype = ctypes.c_int
             f.argtypes = sig
+        sig_ex = ([ctypes.c_int] * 6 + [ctypes.c_double] * 2 + [ctypes.c_int] * 4 + [_dp] * 3
+                  + [ctypes.c_int, ctypes.c_int64, _i64p])
+        for name in ("oracle_forward_ex", "oracle_transpose_ex"):
+            f = getattr(lib, name)
+            f.restype = ctypes.c_int
+            f.argtypes = sig_ex
         lib.oracle_max_threads.restype = ctypes.c_int
         self.lib = lib
 
     # -- grid / quadrature ---------------------------------------------------
-    def colatitudes(self, nlat: int) -> np.ndarray:
-        return np.array([self.lib.oracle_colatitude(t, nlat) for t in range(nlat)])
+    def colatitudes(self, nlat: int, sampling: int = SAMPLING_CELL_CENTRED) -> np.ndarray:
+        if sampling == SAMPLING_CELL_CENTRED:
+            return np.array([self.lib.oracle_colatitude(t, nlat) for t in range(nlat)])
+        return np.array([self.lib.oracle_colatitude_s(t, nlat, sampling) for t in range(nlat)])
 
     def longitudes(self, nlon: int) -> np.ndarray:
         return np.array([self.lib.oracle_longitude(p, nlon) for p in range(nlon)])
 
-    def quadrature(self, nlat: int, nlon: int, kind: int = QUAD_FEJER1) -> np.ndarray:
+    def quadrature(self, nlat: int, nlon: int, kind: int = QUAD_FEJER1,
+                   sampling: int = SAMPLING_CELL_CENTRED) -> np.ndarray:
         q = np.zeros(nlat)
-        rc = self.lib.oracle_quadrature(nlat, nlon, kind, _ptr(q))
+        if sampling == SAMPLING_CELL_CENTRED:
+            rc = self.lib.oracle_quadrature(nlat, nlon, kind, _ptr(q))
+        else:
+            rc = self.lib.oracle_quadrature_s(nlat, nlon, sampling, kind, _ptr(q))
         if rc:
             raise ValueError("oracle_quadrature failed (%d)" % rc)
         return q
@@ -103,52 +127,72 @@ class Oracle:
         self.lib.oracle_basis(u, v, h, _ptr(out))
         return out
 
-    def psi_dense(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, h=None) -> np.ndarray:
-        h = theta_c / 3.0 if not h else h
+    def basis_axisym(self, Theta: float, h: float) -> np.ndarray:
+        out = np.zeros(4)
+        self.lib.oracle_basis_axisym(Theta, h, _ptr(out))
+        return out
+
+    def psi_dense(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, h=None, *,
+                  sampling=SAMPLING_CELL_CENTRED, basis=BASIS_BILINEAR) -> np.ndarray:
+        h = default_h(theta_c, basis) if not h else h
         n_in, n_out = nlat_in * nlon_in, nlat_out * nlon_out
-        psi = np.zeros((n_out, n_in, 9))
-        rc = self.lib.oracle_psi_dense(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, h, _ptr(psi))
+        psi = np.zeros((n_out, n_in, basis_size(basis)))
+        if sampling == SAMPLING_CELL_CENTRED and basis == BASIS_BILINEAR:
+            rc = self.lib.oracle_psi_dense(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, h, _ptr(psi))
+        else:
+            rc = self.lib.oracle_psi_dense_ex(nlat_in, nlon_in, nlat_out, nlon_out, sampling, basis,
+                                              theta_c, h, _ptr(psi))
         if rc:
             raise ValueError("oracle_psi_dense failed (%d)" % rc)
         return psi
 
     # -- convolutions --------------------------------------------------------------
     def _run(self, fn, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, x, w, h, quad, window,
-             pix, out_grid):
+             pix, out_grid, sampling=SAMPLING_CELL_CENTRED, basis=BASIS_BILINEAR):
         x = np.ascontiguousarray(x, dtype=np.float64)
         w = np.ascontiguousarray(w, dtype=np.float64)
         B, C_x = x.shape[0], x.shape[1]
         C_y = w.shape[0] if fn == "oracle_forward" else w.shape[1]
+        if w.shape[2] != basis_size(basis):
+            raise ValueError("w last extent must be %d" % basis_size(basis))
         if pix is None:
             pix = np.arange(out_grid[0] * out_grid[1], dtype=np.int64)
         pix = np.ascontiguousarray(pix, dtype=np.int64)
         y = np.zeros((B, C_y, pix.size))
-        h = theta_c / 3.0 if not h else h
-        rc = getattr(self.lib, fn)(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, h, quad,
-                                   B, C_x, C_y, _ptr(x), _ptr(w), _ptr(y), int(window),
-                                   pix.size, _ptr(pix, _i64p))
+        h = default_h(theta_c, basis) if not h else h
+        if sampling == SAMPLING_CELL_CENTRED and basis == BASIS_BILINEAR:
+            rc = getattr(self.lib, fn)(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, h, quad,
+                                       B, C_x, C_y, _ptr(x), _ptr(w), _ptr(y), int(window),
+                                       pix.size, _ptr(pix, _i64p))
+        else:
+            rc = getattr(self.lib, fn + "_ex")(nlat_in, nlon_in, nlat_out, nlon_out, sampling,
+                                               basis, theta_c, h, quad, B, C_x, C_y, _ptr(x),
+                                               _ptr(w), _ptr(y), int(window), pix.size,
+                                               _ptr(pix, _i64p))
         if rc:
             raise ValueError("%s failed (%d)" % (fn, rc))
         return y
 
     def forward(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, x, w, *, h=None,
-                quad=QUAD_FEJER1, window=True, pix=None):
-        """y[B, Cout, n] for x[B, Cin, nlat_in, nlon_in], w[Cout, Cin, 9].
+                quad=QUAD_FEJER1, window=True, pix=None, sampling=SAMPLING_CELL_CENTRED,
+                basis=BASIS_BILINEAR):
+        """y[B, Cout, n] for x[B, Cin, nlat_in, nlon_in], w[Cout, Cin, K].
 
         ``pix`` selects flat out-grid pixels (default: all, returned reshaped
         to [B, Cout, nlat_out, nlon_out])."""
         y = self._run("oracle_forward", nlat_in, nlon_in, nlat_out, nlon_out, theta_c, x, w, h,
-                      quad, window, pix, (nlat_out, nlon_out))
+                      quad, window, pix, (nlat_out, nlon_out), sampling, basis)
         if pix is None:
             y = y.reshape(y.shape[0], y.shape[1], nlat_out, nlon_out)
         return y
 
     def transpose(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, x, w, *, h=None,
-                  quad=QUAD_FEJER1, window=True, pix=None):
+                  quad=QUAD_FEJER1, window=True, pix=None, sampling=SAMPLING_CELL_CENTRED,
+                  basis=BASIS_BILINEAR):
         """Transposed op of plan (in-grid, out-grid): x[B, CinT, nlat_out, nlon_out],
-        w[CinT, CoutT, 9] -> y[B, CoutT, nlat_in, nlon_in] (or [B, CoutT, n])."""
+        w[CinT, CoutT, K] -> y[B, CoutT, nlat_in, nlon_in] (or [B, CoutT, n])."""
         y = self._run("oracle_transpose", nlat_in, nlon_in, nlat_out, nlon_out, theta_c, x, w, h,
-                      quad, window, pix, (nlat_in, nlon_in))
+                      quad, window, pix, (nlat_in, nlon_in), sampling, basis)
         if pix is None:
             y = y.reshape(y.shape[0], y.shape[1], nlat_in, nlon_in)
         return y
@@ -170,10 +214,17 @@ def default() -> Oracle:
     return _default
 
 
-def default_h(theta_c: float) -> float:
-    """Node spacing of the 3x3 grid: theta_c / 3 (App. E.2 puts the edge nodes at
-    pi/L with a cutoff of 3 pi/L)."""
-    return theta_c / 3.0
+def default_h(theta_c: float, basis: int = BASIS_BILINEAR) -> float:
+    """Node spacing.  3x3 grid: theta_c / 3 (App. E.2 puts the edge nodes at
+    pi/L with a cutoff of 3 pi/L).  Axisymmetric: theta_c / 4, four nodes at
+    0, h, 2h, 3h whose last hat vanishes at the cutoff."""
+    return theta_c / 4.0 if basis == BASIS_AXISYM else theta_c / 3.0
 
 
-__all__ = ["Oracle", "build", "default", "default_h", "QUAD_FEJER1", "QUAD_CELL_AREA"]
+def basis_size(basis: int) -> int:
+    return 4 if basis == BASIS_AXISYM else 9
+
+
+__all__ = ["Oracle", "build", "default", "default_h", "basis_size", "QUAD_FEJER1",
+           "QUAD_CELL_AREA", "SAMPLING_CELL_CENTRED", "SAMPLING_MW", "BASIS_BILINEAR",
+           "BASIS_AXISYM"]

@@ -25,6 +25,11 @@
  * explicit 3x3 rotation matrices in Cartesian coordinates (a different route
  * from the GPU library's plan).  Everything is double precision.
  *
+ * Two grids (the cell-centred equiangular grid, and the paper's own
+ * pole-including grid of Sec. 4.2 with App. A's quadrature) and two bases
+ * (the 3x3 node grid of App. E.2, K = 9, and the axisymmetric filter with four
+ * nodes along theta that App. B times, K = 4) are offered.
+ *
  * Readings of points the paper leaves open (grid, quadrature rule, rotation
  * handedness, tangent-plane map, node spacing, basis ordering) are stated at
  * each function.
@@ -48,6 +53,17 @@
 /* ------------------------------------------------------------------------- */
 double oracle_colatitude(int t, int nlat) { return (t + 0.5) * M_PI / (double)nlat; }
 double oracle_longitude(int p, int nlon) { return 2.0 * M_PI * (double)p / (double)nlon; }
+
+/* The paper's own grid (Sec. 4.2, "Explicit sampling"; the antipodal variant
+ * of the McEwen-Wiaux sampling, App. A): with L = nlat - 1, colatitude
+ * pi t / L for t = 0..L, both poles included, and longitude pi p / L for
+ * p = 0..2L-1, i.e. nlon = 2L.  Each pole ring holds 2L samples of one point.
+ * sampling 0 = cell-centred (above), 1 = this grid. */
+double oracle_colatitude_s(int t, int nlat, int sampling)
+{
+    if (sampling == 1) return M_PI * (double)t / (double)(nlat - 1);
+    return oracle_colatitude(t, nlat);
+}
 
 /* ------------------------------------------------------------------------- */
 /* Quadrature weights q(theta_t), one per ring; a pixel's weight is its ring's.
@@ -78,6 +94,69 @@ int oracle_quadrature(int nlat, int nlon, int kind, double* q)
         q[t] = (2.0 * M_PI / nlon) * w;
     }
     return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Quadrature of the pole-including grid (App. A), taken in the appendix's
+ * steps.  The colatitude integral of a band-limited signal is extended to the
+ * torus: sin(theta) on [0, pi], zero on (pi, 2 pi), has the Fourier
+ * coefficients
+ *   w(m) = int_0^pi sin(t) e^{i m t} dt = +-i pi/2 (m = +-1), 0 (other odd m),
+ *          2 / (1 - m^2) (even m);
+ * its band-limited version is w_r(t) = sum_{m=-L}^{L-1} w(m) e^{i m t}; the
+ * torus sample at colatitude theta_{2L-t} = 2 pi - theta_t is the sphere's
+ * sample at (theta_t, phi + pi), so its weight folds back onto ring t (not for
+ * the poles, t = 0 and t = L, which are their own images):
+ *   q(theta_t) = 2 pi / (2L)^2 [ w_r(theta_t) + (1 - d_{t0})(1 - d_{tL}) w_r(theta_{2L-t}) ]
+ * (spin s = 0).  The first factor 2 pi / (2L) is the longitude step of the
+ * 2L samples per ring, the second 1 / (2L) the normalisation of the 2L-point
+ * transform along the extended colatitude; the rule is stated for nlon = 2L
+ * and is only offered there.  w_r is real at the sample points (conjugate
+ * pairs m, -m; e^{-i L theta_t} = (-1)^t), its real part is taken.          */
+/* ------------------------------------------------------------------------- */
+static void sin_fourier(int m, double* re, double* im)
+{
+    *re = 0.0;
+    *im = 0.0;
+    if (m == 1) {
+        *im = 0.5 * M_PI;
+    } else if (m == -1) {
+        *im = -0.5 * M_PI;
+    } else if (m % 2 == 0) {
+        *re = 2.0 / (1.0 - (double)m * (double)m);
+    }
+}
+
+static double band_limited_sin(int L, double theta)
+{
+    double acc = 0.0;
+    for (int m = -L; m <= L - 1; ++m) {
+        double re, im;
+        sin_fourier(m, &re, &im);
+        /* Re(w(m) e^{i m theta}) */
+        acc += re * cos(m * theta) - im * sin(m * theta);
+    }
+    return acc;
+}
+
+static int quadrature_mw(int nlat, int nlon, double* q)
+{
+    int L = nlat - 1;
+    if (L < 1 || nlon != 2 * L) return 1;
+    for (int t = 0; t <= L; ++t) {
+        double s = band_limited_sin(L, M_PI * (double)t / (double)L);
+        if (t != 0 && t != L) s += band_limited_sin(L, M_PI * (double)(2 * L - t) / (double)L);
+        q[t] = 2.0 * M_PI / ((2.0 * L) * (2.0 * L)) * s;
+    }
+    return 0;
+}
+
+/* Weights of either grid: sampling 1 takes App. A's rule (kind must be 0). */
+int oracle_quadrature_s(int nlat, int nlon, int sampling, int kind, double* q)
+{
+    if (sampling == 0) return oracle_quadrature(nlat, nlon, kind, q);
+    if (sampling != 1 || kind != 0 || !q) return 2;
+    return quadrature_mw(nlat, nlon, q);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -180,17 +259,34 @@ void oracle_basis(double u, double v, double h, double psi[9])
             psi[3 * a + b] = hat(u / h - (a - 1)) * hat(v / h - (b - 1));
 }
 
-/* Evaluate all 9 basis functions of the filter centred at (theta_j, phi_j)
+/* Axisymmetric basis (Sec. 3.4: filters psi(theta) with equally spaced nodes
+ * along theta and linear interpolation, zero above the cutoff), the one the
+ * paper times (App. B: 4 nodes, cutoff 3 pi / L).  Nodes at k h, k = 0..3,
+ * with h = theta_c / 4 by default, so that the last hat reaches zero exactly
+ * at the cutoff and the filter is continuous:
+ *   psi_k(Theta) = L(Theta / h - k).                                          */
+void oracle_basis_axisym(double Theta, double h, double psi[4])
+{
+    for (int k = 0; k < 4; ++k) psi[k] = hat(Theta / h - k);
+}
+
+/* basis 0 = the 3x3 grid (K = 9), 1 = axisymmetric (K = 4). */
+static int basis_size(int basis) { return basis == 1 ? 4 : 9; }
+
+/* Evaluate the K basis functions of the filter centred at (theta_j, phi_j)
  * at the input point e; returns 0 if the point is beyond the cutoff or all
- * nine values vanish, 1 otherwise. */
-static int filter_values(const double m[9], const double e[3], double theta_c, double h,
-                         double psi[9])
+ * values vanish, 1 otherwise. */
+static int filter_values(int basis, const double m[9], const double e[3], double theta_c,
+                         double h, double psi[9])
 {
     double Th, u, v;
     frame_coords_m(m, e, &Th, &u, &v);
     if (Th > theta_c) return 0;
-    oracle_basis(u, v, h, psi);
-    for (int k = 0; k < 9; ++k)
+    if (basis == 1)
+        oracle_basis_axisym(Th, h, psi);
+    else
+        oracle_basis(u, v, h, psi);
+    for (int k = 0; k < basis_size(basis); ++k)
         if (psi[k] != 0.0) return 1;
     return 0;
 }
@@ -199,26 +295,33 @@ static int filter_values(const double m[9], const double e[3], double theta_c, d
 /* Dense Psi tensor psi[j][i][k] = psi_k(R_j^{-1} w_i) (no quadrature),
  * j over out-grid pixels, i over in-grid pixels (Sec. 4.1).  Tiny grids only. */
 /* ------------------------------------------------------------------------- */
-int oracle_psi_dense(int nlat_in, int nlon_in, int nlat_out, int nlon_out,
-                     double theta_c, double h, double* psi)
+int oracle_psi_dense_ex(int nlat_in, int nlon_in, int nlat_out, int nlon_out, int sampling,
+                        int basis, double theta_c, double h, double* psi)
 {
     if (!psi) return 1;
+    int K = basis_size(basis);
     int64_t n_in = (int64_t)nlat_in * nlon_in, n_out = (int64_t)nlat_out * nlon_out;
-    memset(psi, 0, sizeof(double) * (size_t)(n_out * n_in * 9));
+    memset(psi, 0, sizeof(double) * (size_t)(n_out * n_in * K));
 #pragma omp parallel for schedule(dynamic)
     for (int64_t j = 0; j < n_out; ++j) {
         double m[9];
-        inverse_rotation(oracle_colatitude((int)(j / nlon_out), nlat_out),
+        inverse_rotation(oracle_colatitude_s((int)(j / nlon_out), nlat_out, sampling),
                          oracle_longitude((int)(j % nlon_out), nlon_out), m);
         for (int64_t i = 0; i < n_in; ++i) {
             double e[3], val[9];
-            unit_vector(oracle_colatitude((int)(i / nlon_in), nlat_in),
+            unit_vector(oracle_colatitude_s((int)(i / nlon_in), nlat_in, sampling),
                         oracle_longitude((int)(i % nlon_in), nlon_in), e);
-            if (filter_values(m, e, theta_c, h, val))
-                for (int k = 0; k < 9; ++k) psi[(j * n_in + i) * 9 + k] = val[k];
+            if (filter_values(basis, m, e, theta_c, h, val))
+                for (int k = 0; k < K; ++k) psi[(j * n_in + i) * K + k] = val[k];
         }
     }
     return 0;
+}
+
+int oracle_psi_dense(int nlat_in, int nlon_in, int nlat_out, int nlon_out,
+                     double theta_c, double h, double* psi)
+{
+    return oracle_psi_dense_ex(nlat_in, nlon_in, nlat_out, nlon_out, 0, 0, theta_c, h, psi);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -238,20 +341,28 @@ typedef struct {
     int nlat, nlon;
 } grid_t;
 
+typedef struct {
+    int sampling;  /* 0 cell-centred, 1 pole-including */
+    int basis;     /* 0 the 3x3 grid, 1 axisymmetric */
+    int quad_kind; /* 0 the grid's sampling-theorem rule, 1 cell areas */
+} config_t;
+
 /* Shared body: the filter is centred at points of grid `ctr`, evaluated at
  * points of grid `ev`.  forward: centre = output pixel, sum over input pixels
  * (the evaluation points), quadrature of the evaluation points' grid.
  * transpose: centre = each input pixel of the transposed op, evaluation at the
  * output pixel, quadrature of the centres' grid. */
 static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, double h,
-                     int quad_kind, int B, int Cin, int Cout, const double* x,
+                     config_t cfg, int B, int Cin, int Cout, const double* x,
                      const double* w, double* y, int window, int64_t n_pix,
                      const int64_t* pix)
 {
     if (!x || !w || !y || !pix || B < 0 || Cin < 1 || Cout < 1) return 1;
+    const int K = basis_size(cfg.basis);
+    const int smp = cfg.sampling;
     double* q_in = (double*)malloc(sizeof(double) * (size_t)g_in.nlat);
     if (!q_in) return 3;
-    if (oracle_quadrature(g_in.nlat, g_in.nlon, quad_kind, q_in)) {
+    if (oracle_quadrature_s(g_in.nlat, g_in.nlon, smp, cfg.quad_kind, q_in)) {
         free(q_in);
         return 2;
     }
@@ -270,13 +381,13 @@ static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, d
                 continue;
             }
             int to = (int)(o / g_out.nlon), po = (int)(o % g_out.nlon);
-            double th_o = oracle_colatitude(to, g_out.nlat), ph_o = oracle_longitude(po, g_out.nlon);
+            double th_o = oracle_colatitude_s(to, g_out.nlat, smp), ph_o = oracle_longitude(po, g_out.nlon);
             memset(Z, 0, sizeof(double) * (size_t)B * Cin * 9);
             double m_o[9], e_o[3];
             inverse_rotation(th_o, ph_o, m_o);
             unit_vector(th_o, ph_o, e_o);
             for (int t = 0; t < g_in.nlat; ++t) {
-                double th_i = oracle_colatitude(t, g_in.nlat);
+                double th_i = oracle_colatitude_s(t, g_in.nlat, smp);
                 if (window && fabs(th_i - th_o) > theta_c) continue;
                 for (int p = 0; p < g_in.nlon; ++p) {
                     double ph_i = oracle_longitude(p, g_in.nlon);
@@ -285,11 +396,11 @@ static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, d
                     if (!transpose) {
                         double e_i[3];
                         unit_vector(th_i, ph_i, e_i);
-                        nz = filter_values(m_o, e_i, theta_c, h, val);
+                        nz = filter_values(cfg.basis, m_o, e_i, theta_c, h, val);
                     } else {
                         double m_i[9];
                         inverse_rotation(th_i, ph_i, m_i);
-                        nz = filter_values(m_i, e_o, theta_c, h, val);
+                        nz = filter_values(cfg.basis, m_i, e_o, theta_c, h, val);
                     }
                     if (!nz) continue;
                     double qw = q_in[t];
@@ -297,7 +408,7 @@ static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, d
                         for (int c = 0; c < Cin; ++c) {
                             double xv = x[((int64_t)b * Cin + c) * n_in + (int64_t)t * g_in.nlon + p];
                             double* zc = Z + ((size_t)b * Cin + c) * 9;
-                            for (int k = 0; k < 9; ++k) zc[k] += val[k] * qw * xv;
+                            for (int k = 0; k < K; ++k) zc[k] += val[k] * qw * xv;
                         }
                 }
             }
@@ -305,10 +416,10 @@ static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, d
                 for (int co = 0; co < Cout; ++co) {
                     double s = 0.0;
                     for (int ci = 0; ci < Cin; ++ci)
-                        for (int k = 0; k < 9; ++k) {
+                        for (int k = 0; k < K; ++k) {
                             /* forward: W[co][ci][k]; transpose: W[ci][co][k]. */
-                            double wv = transpose ? w[((int64_t)ci * Cout + co) * 9 + k]
-                                                  : w[((int64_t)co * Cin + ci) * 9 + k];
+                            double wv = transpose ? w[((int64_t)ci * Cout + co) * K + k]
+                                                  : w[((int64_t)co * Cin + ci) * K + k];
                             s += wv * Z[((size_t)b * Cin + ci) * 9 + k];
                         }
                     y[((int64_t)b * Cout + co) * n_pix + n] = s;
@@ -321,26 +432,46 @@ static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, d
 }
 
 /* Forward op from the in-grid to the out-grid.
- * x[B][Cin][nlat_in][nlon_in], w[Cout][Cin][9], y[B][Cout][n_pix]. */
+ * x[B][Cin][nlat_in][nlon_in], w[Cout][Cin][K], y[B][Cout][n_pix]. */
+int oracle_forward_ex(int nlat_in, int nlon_in, int nlat_out, int nlon_out, int sampling,
+                      int basis, double theta_c, double h, int quad_kind, int B, int Cin,
+                      int Cout, const double* x, const double* w, double* y, int window,
+                      int64_t n_pix, const int64_t* pix)
+{
+    grid_t gi = {nlat_in, nlon_in}, go = {nlat_out, nlon_out};
+    config_t cfg = {sampling, basis, quad_kind};
+    return disco_sum(0, gi, go, theta_c, h, cfg, B, Cin, Cout, x, w, y, window, n_pix, pix);
+}
+
+/* Transposed op of the same plan, from the out-grid back to the in-grid.
+ * xT[B][CinT][nlat_out][nlon_out], w[CinT][CoutT][K], yT[B][CoutT][n_pix]
+ * with pix indexing the in-grid. */
+int oracle_transpose_ex(int nlat_in, int nlon_in, int nlat_out, int nlon_out, int sampling,
+                        int basis, double theta_c, double h, int quad_kind, int B, int CinT,
+                        int CoutT, const double* xT, const double* w, double* yT, int window,
+                        int64_t n_pix, const int64_t* pix)
+{
+    /* The transposed op reads the plan's out-grid and writes its in-grid. */
+    grid_t gi = {nlat_out, nlon_out}, go = {nlat_in, nlon_in};
+    config_t cfg = {sampling, basis, quad_kind};
+    return disco_sum(1, gi, go, theta_c, h, cfg, B, CinT, CoutT, xT, w, yT, window, n_pix, pix);
+}
+
+/* The cell-centred grid with the 3x3 basis. */
 int oracle_forward(int nlat_in, int nlon_in, int nlat_out, int nlon_out, double theta_c,
                    double h, int quad_kind, int B, int Cin, int Cout, const double* x,
                    const double* w, double* y, int window, int64_t n_pix, const int64_t* pix)
 {
-    grid_t gi = {nlat_in, nlon_in}, go = {nlat_out, nlon_out};
-    return disco_sum(0, gi, go, theta_c, h, quad_kind, B, Cin, Cout, x, w, y, window, n_pix, pix);
+    return oracle_forward_ex(nlat_in, nlon_in, nlat_out, nlon_out, 0, 0, theta_c, h, quad_kind,
+                             B, Cin, Cout, x, w, y, window, n_pix, pix);
 }
 
-/* Transposed op of the same plan, from the out-grid back to the in-grid.
- * xT[B][CinT][nlat_out][nlon_out], w[CinT][CoutT][9], yT[B][CoutT][n_pix]
- * with pix indexing the in-grid. */
 int oracle_transpose(int nlat_in, int nlon_in, int nlat_out, int nlon_out, double theta_c,
                      double h, int quad_kind, int B, int CinT, int CoutT, const double* xT,
                      const double* w, double* yT, int window, int64_t n_pix, const int64_t* pix)
 {
-    /* The transposed op reads the plan's out-grid and writes its in-grid. */
-    grid_t gi = {nlat_out, nlon_out}, go = {nlat_in, nlon_in};
-    return disco_sum(1, gi, go, theta_c, h, quad_kind, B, CinT, CoutT, xT, w, yT, window, n_pix,
-                     pix);
+    return oracle_transpose_ex(nlat_in, nlon_in, nlat_out, nlon_out, 0, 0, theta_c, h, quad_kind,
+                               B, CinT, CoutT, xT, w, yT, window, n_pix, pix);
 }
 
 int oracle_max_threads(void)

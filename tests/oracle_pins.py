@@ -404,4 +404,202 @@ def pin_pixel_subset(o):
     assert np.array_equal(ys, y.reshape(2, 3, -1)[:, :, pix])
 
 
+# --------------------------------------------------------------------------- #
+# The paper's own timed configuration: the pole-including grid of Sec. 4.2
+# with App. A's quadrature, and the axisymmetric basis of Sec. 3.4 / App. B.
+# --------------------------------------------------------------------------- #
+_MW, _AX = 1, 1
+
+
+def _select_w4():
+    """W with Cin = 1, Cout = 4 and W[k, 0, k'] = delta(k, k'): y then equals Z."""
+    w = np.zeros((4, 1, 4))
+    for k in range(4):
+        w[k, 0, k] = 1.0
+    return w
+
+
+def pin_mw_grid(o):
+    """(theta_t, phi_p) = (pi t / L, pi p / L), 0 <= t <= L, 0 <= p < 2L."""
+    for L in (1, 4, 8, 33):
+        th = o.colatitudes(L + 1, sampling=_MW)
+        assert np.allclose(th, np.arange(L + 1) * math.pi / L, rtol=0, atol=1e-15)
+        assert th[0] == 0.0 and abs(th[-1] - math.pi) <= 1e-15
+        assert np.allclose(o.longitudes(2 * L), np.arange(2 * L) * math.pi / L, rtol=0, atol=1e-15)
+
+
+def pin_mw_quadrature_total_and_symmetry(o):
+    """App. A weights: total 4 pi, antipodally symmetric (q_t = q_{L-t}), positive."""
+    for L in (1, 2, 3, 8, 9, 64, 1024, 2048):
+        q = o.quadrature(L + 1, 2 * L, sampling=_MW)
+        assert abs(q.sum() * 2 * L - 4 * math.pi) <= 1e-12 * 4 * math.pi, (L, q.sum())
+        assert np.abs(q - q[::-1]).max() <= 1e-13 * q.max(), L
+        assert (q > 0).all(), L
+
+
+def pin_mw_quadrature_interpolatory(o):
+    """On the L + 1 distinct nodes x_t = cos(theta_t) exactly one rule
+    integrates every polynomial of degree <= L.  The Chebyshev moments
+    int_{-1}^{1} T_n dx = 2 / (1 - n^2) (n even), 0 (n odd) fix it (numpy's
+    Chebyshev Vandermonde matrix and linear solver); App. A's weights, folded
+    from the band-limited transform of sin(theta), must be that rule times the
+    longitude step 2 pi / (2L)."""
+    for L in (2, 3, 4, 8, 15, 16, 33, 64):
+        x = np.cos(np.arange(L + 1) * math.pi / L)
+        V = np.polynomial.chebyshev.chebvander(x, L).T
+        mom = np.array([2.0 / (1 - n * n) if n % 2 == 0 else 0.0 for n in range(L + 1)])
+        w = np.linalg.solve(V, mom)
+        q = o.quadrature(L + 1, 2 * L, sampling=_MW) * (2 * L) / (2 * math.pi)
+        assert np.abs(q - w).max() <= 1e-13, (L, np.abs(q - w).max())
+
+
+def pin_mw_quadrature_legendre_exact(o):
+    """Band-limited signals integrate exactly (the sampling theorem the grid
+    comes with): P_l(cos theta) over the sphere is 4 pi for l = 0, else 0,
+    for every l < L."""
+    for L in (4, 7, 32, 65, 256):
+        q = o.quadrature(L + 1, 2 * L, sampling=_MW)
+        x = np.cos(o.colatitudes(L + 1, sampling=_MW))
+        for l in range(L):
+            val = 2 * L * float(np.dot(q, eval_legendre(l, x)))
+            expect = 4 * math.pi if l == 0 else 0.0
+            assert abs(val - expect) <= 1e-12, (L, l, val)
+
+
+def pin_axisym_basis(o):
+    """Four hats along Theta at nodes 0, h, 2h, 3h (Sec. 3.4, linear
+    interpolation): Kronecker delta at the nodes, partition of unity on
+    [0, 3h], linear functions reproduced there, only the last hat (falling to
+    zero at 4h) on [3h, 4h], nothing beyond."""
+    h = 0.0123
+    for j in range(4):
+        e = np.zeros(4)
+        e[j] = 1.0
+        assert np.abs(o.basis_axisym(j * h, h) - e).max() <= 1e-15, j
+    assert np.abs(o.basis_axisym(1.5 * h, h) - [0, 0.5, 0.5, 0]).max() <= 1e-15
+    assert np.abs(o.basis_axisym(3.5 * h, h) - [0, 0, 0, 0.5]).max() <= 1e-15
+    assert not o.basis_axisym(4 * h, h).any() and not o.basis_axisym(5.2 * h, h).any()
+    r = _rng(40)
+    for _ in range(300):
+        t = r.uniform(0, 3 * h)
+        psi = o.basis_axisym(t, h)
+        assert abs(psi.sum() - 1.0) <= 1e-14
+        c0, c1 = r.standard_normal(2)
+        assert abs(float(np.dot(psi, c0 + c1 * np.arange(4))) - (c0 + c1 * t / h)) <= 1e-12
+        assert np.count_nonzero(psi) <= 2
+        t = r.uniform(3 * h, 4 * h)
+        psi = o.basis_axisym(t, h)
+        assert np.abs(psi[:3]).max() == 0.0 and abs(psi[3] - (4 - t / h)) <= 1e-14
+
+
+def pin_axisym_pole_closed_form(o):
+    """At a pole every input point of ring t lies at geodesic distance theta_t
+    (north) or pi - theta_t (south), so the 2-D sum collapses to a 1-D sum over
+    rings: Z_k(pole) = sum_t psi_k(dist_t) q_t sum_p x[t, p], the same at every
+    longitude of the pole ring (the ring is one point)."""
+    for L, tc_pix in ((16, 3), (12, 5)):
+        tc = tc_pix * math.pi / L
+        h = tc / 4
+        x = _rng(41).standard_normal((1, 1, L + 1, 2 * L))
+        Z = o.forward(L + 1, 2 * L, L + 1, 2 * L, tc, x, _select_w4(), sampling=_MW, basis=_AX)[0]
+        q = o.quadrature(L + 1, 2 * L, sampling=_MW)
+        th = np.arange(L + 1) * math.pi / L
+        rows = x[0, 0].sum(axis=1)
+        for tp, dist in ((0, th), (L, math.pi - th)):
+            expect = np.zeros(4)
+            for t in range(L + 1):
+                if dist[t] <= tc:
+                    expect += o.basis_axisym(float(dist[t]), h) * q[t] * rows[t]
+            got = Z[:, tp, :]
+            scale = np.abs(expect).max()
+            assert np.abs(got - expect[:, None]).max() <= 1e-13 * scale, (L, tp, got[:, 0], expect)
+
+
+def pin_axisym_grid_isometries(o):
+    """An axisymmetric filter sees only the geodesic distance, so the op
+    commutes with every isometry that maps the grid onto itself: whole-pixel
+    longitude shifts, the mirror phi -> -phi and the flip theta -> pi - theta
+    (all exact up to rounding), for the forward and the transposed op, with
+    and without 2x downsampling."""
+    for (L, Lo) in ((12, 12), (12, 6)):
+        a, b, c, d = L + 1, 2 * L, Lo + 1, 2 * Lo
+        tc = 3 * math.pi / Lo
+        s = b // d
+        r = _rng(42)
+        x = r.standard_normal((1, 2, a, b))
+        w = r.standard_normal((2, 2, 4))
+        kw = dict(sampling=_MW, basis=_AX)
+        y = o.forward(a, b, c, d, tc, x, w, **kw)
+        sc = np.abs(y).max()
+        ys = o.forward(a, b, c, d, tc, np.roll(x, s, axis=-1), w, **kw)
+        assert np.abs(ys - np.roll(y, 1, axis=-1)).max() <= 1e-13 * sc
+        ym = o.forward(a, b, c, d, tc, x[..., (-np.arange(b)) % b], w, **kw)
+        assert np.abs(ym - y[..., (-np.arange(d)) % d]).max() <= 1e-13 * sc
+        yf = o.forward(a, b, c, d, tc, x[:, :, ::-1, :], w, **kw)
+        assert np.abs(yf - y[:, :, ::-1, :]).max() <= 1e-12 * sc
+        for tp in (0, c - 1):
+            assert np.abs(y[:, :, tp, :] - y[:, :, tp, :1]).max() <= 1e-13 * sc
+        xT = r.standard_normal((1, 2, c, d))
+        yT = o.transpose(a, b, c, d, tc, xT, w, **kw)
+        scT = np.abs(yT).max()
+        yTf = o.transpose(a, b, c, d, tc, xT[:, :, ::-1, :], w, **kw)
+        assert np.abs(yTf - yT[:, :, ::-1, :]).max() <= 1e-12 * scT
+        yTm = o.transpose(a, b, c, d, tc, xT[..., (-np.arange(d)) % d], w, **kw)
+        assert np.abs(yTm - yT[..., (-np.arange(b)) % b]).max() <= 1e-13 * scT
+
+
+def pin_axisym_adjoint(o):
+    """The transposed op is the adjoint of the forward op in the
+    quadrature-weighted inner products, on the pole-including grid too."""
+    for (L, Lo) in ((12, 12), (16, 8)):
+        a, b, c, d = L + 1, 2 * L, Lo + 1, 2 * Lo
+        tc = 3 * math.pi / Lo
+        r = _rng(43)
+        x = r.standard_normal((2, 3, a, b))
+        g = r.standard_normal((2, 2, c, d))
+        w = r.standard_normal((2, 3, 4))
+        kw = dict(sampling=_MW, basis=_AX)
+        Ax = o.forward(a, b, c, d, tc, x, w, **kw)
+        Bg = o.transpose(a, b, c, d, tc, g, w, **kw)
+        qo = o.quadrature(c, d, sampling=_MW)[None, None, :, None]
+        qi = o.quadrature(a, b, sampling=_MW)[None, None, :, None]
+        lhs = float((Ax * g * qo).sum())
+        rhs = float((x * Bg * qi).sum())
+        assert abs(lhs - rhs) <= 1e-12 * max(abs(lhs), 1.0), (lhs, rhs)
+
+
+def axisym_filter_integrals(h, n=24):
+    """S_k = integral over the sphere of psi_k(Theta) = 2 pi int psi_k(t) sin t dt,
+    Gauss-Legendre on each side of the hat."""
+    xg, wg = np.polynomial.legendre.leggauss(n)
+    S = np.zeros(4)
+    for k in range(4):
+        for lo, hi in (((k - 1) * h, k * h), (k * h, (k + 1) * h)):
+            lo = max(lo, 0.0)
+            if hi <= lo:
+                continue
+            t = lo + (xg + 1) / 2 * (hi - lo)
+            f = np.maximum(0.0, 1 - np.abs(t / h - k)) * np.sin(t)
+            S[k] += 2 * math.pi * float(((hi - lo) / 2 * wg * f).sum())
+    return S
+
+
+def pin_axisym_constant_input(o):
+    """x = 1 on the pole-including grid: every Z_k approximates the filter
+    integral S_k (the only error is quadrature, Sec. 3.2), at second order in
+    the pixel size at fixed theta_c: from L = 128 on the error falls at least
+    3x per doubling and is below 4e-3 at L = 512."""
+    tc = 3 * math.pi / 32
+    S = axisym_filter_integrals(tc / 4)
+    errs = []
+    for L in (128, 256, 512):
+        pix = np.arange(L + 1) * 2 * L        # one pixel per ring: rings are constant
+        Z = o.forward(L + 1, 2 * L, L + 1, 2 * L, tc, np.ones((1, 1, L + 1, 2 * L)), _select_w4(),
+                      pix=pix, sampling=_MW, basis=_AX)[0]
+        errs.append(float(np.abs(Z / S[:, None] - 1).max()))
+    for e0, e1 in zip(errs, errs[1:]):
+        assert e1 * 3 <= e0, errs
+    assert errs[-1] <= 4e-3, errs
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -23,20 +23,35 @@ MUTANTS = {
                             "-2.0 * M_PI * (double)p / (double)nlon"),
     "drop_quadrature": ("zc[k] += val[k] * qw * xv;", "zc[k] += val[k] * xv;"),
     "transpose_drops_quadrature": ("double qw = q_in[t];", "double qw = transpose ? 1.0 : q_in[t];"),
-    "forward_w_transposed": (": w[((int64_t)co * Cin + ci) * 9 + k];",
-                             ": w[((int64_t)ci * Cout + co) * 9 + k];"),
-    "transpose_w_not_transposed": ("double wv = transpose ? w[((int64_t)ci * Cout + co) * 9 + k]",
-                                   "double wv = transpose ? w[((int64_t)co * Cin + ci) * 9 + k]"),
+    "forward_w_transposed": (": w[((int64_t)co * Cin + ci) * K + k];",
+                             ": w[((int64_t)ci * Cout + co) * K + k];"),
+    "transpose_w_not_transposed": ("double wv = transpose ? w[((int64_t)ci * Cout + co) * K + k]",
+                                   "double wv = transpose ? w[((int64_t)co * Cin + ci) * K + k]"),
     "basis_index_order": ("psi[3 * a + b] = hat", "psi[3 * b + a] = hat"),
     "hat_shape": ("return a < 1.0 ? 1.0 - a : 0.0;", "return a < 1.0 ? 1.0 - a * a : 0.0;"),
     "cutoff_too_small": ("if (Th > theta_c) return 0;", "if (Th > 0.5 * theta_c) return 0;"),
     "window_too_narrow": ("if (window && fabs(th_i - th_o) > theta_c) continue;",
                           "if (window && fabs(th_i - th_o) > 0.5 * theta_c) continue;"),
-    "transpose_centre_swapped": ("nz = filter_values(m_i, e_o, theta_c, h, val);",
-                                 "nz = filter_values(m_o, e_i_t, theta_c, h, val);"),
+    "transpose_centre_swapped": ("nz = filter_values(cfg.basis, m_i, e_o, theta_c, h, val);",
+                                 "nz = filter_values(cfg.basis, m_o, e_i_t, theta_c, h, val);"),
     "basis_drops_corner": ("psi[3 * a + b] = hat(u / h - (a - 1)) * hat(v / h - (b - 1));",
                            "psi[3 * a + b] = (a != 1 && b != 1) ? 0.0 : "
                            "hat(u / h - (a - 1)) * hat(v / h - (b - 1));"),
+    # The pole-including grid, App. A's quadrature and the axisymmetric basis.
+    "mw_colatitude": ("return M_PI * (double)t / (double)(nlat - 1);",
+                      "return M_PI * (double)t / (double)nlat;"),
+    "mw_fold_dropped": ("if (t != 0 && t != L) s += band_limited_sin",
+                        "if (0) s += band_limited_sin"),
+    "mw_fold_at_poles": ("if (t != 0 && t != L) s += band_limited_sin",
+                         "s += band_limited_sin"),
+    "mw_sum_range": ("for (int m = -L; m <= L - 1; ++m)", "for (int m = -L + 1; m <= L - 1; ++m)"),
+    "mw_even_coefficient": ("*re = 2.0 / (1.0 - (double)m * (double)m);",
+                            "*re = 2.0 / (1.0 + (double)m * (double)m);"),
+    "mw_normalisation": ("2.0 * M_PI / ((2.0 * L) * (2.0 * L))",
+                         "2.0 * M_PI / ((2.0 * L) * (2.0 * L + 1.0))"),
+    "axisym_node_shift": ("psi[k] = hat(Theta / h - k);", "psi[k] = hat(Theta / h - k - 1);"),
+    "axisym_signed_coordinate": ("oracle_basis_axisym(Th, h, psi);", "oracle_basis_axisym(u, h, psi);"),
+    "axisym_drops_last_node": ("return basis == 1 ? 4 : 9;", "return basis == 1 ? 3 : 9;"),
 }
 
 
