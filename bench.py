@@ -36,7 +36,13 @@ DEVICE_KERNEL = {"gather_z": "k_gather_z", "contract_z": "k_contract_z", "contra
                  "reduce_partials": "k_reduce_partials", "sweep_gather_contract": "k_sweep",
                  "sweep_gather_z": "k_sweep",
                  "spectral_rfft": "k_rfft_rings", "spectral_mac": "k_spectral",
-                 "spectral_irfft": "k_irfft_rings"}
+                 "spectral_irfft": "k_irfft_rings", "stencil": "k_stencil",
+                 "stencil_blocked": "k_stencil_blocked"}
+# The paper's wall-clock for its timed layer (App. B: one channel, batch 1,
+# axisymmetric four-node filter, theta_c = 3 pi / L, (L + 1) x 2L pixels; NVIDIA
+# RTX 3090, TensorFlow sparse-dense products, mean of 10 runs), in seconds.
+PAPER_SECONDS = {"poles_axisym_L1024": 0.0302, "poles_axisym_L2048": 0.0898,
+                 "poles_axisym_L4096": 0.3255}
 # Template argument that tells two schedules' launches of one device function apart.
 KERNEL_VARIANT = {"sweep_gather_contract": ", false>", "sweep_gather_z": ", true>"}
 COPY_PROBE_BYTES = 256 << 20   # per direction, fp32 negation used as the plain copy kernel
@@ -76,6 +82,13 @@ def kernel_model(name, wl, work, es):
     """
     B, Ci, Co = wl.batch, wl.c_in, wl.c_out
     outp, inp, pairs = work
+    if name in ("stencil", "stencil_blocked"):
+        # W folded into psi: 2 flop per stored (output pixel, input pixel)
+        # pair per channel pair; bound by whichever roof is lower.
+        b_ = B * Ci * inp * es + B * Co * outp * es
+        f_ = 2.0 * pairs * B * Ci * Co
+        bound = "hbm" if b_ / (HBM_PEAK_GBS * 1e9) > f_ / (FP32_VALU_PEAK_TFLOPS * 1e12) else "alu"
+        return (b_, f_, bound)
     if name in ("gather_z", "sweep_gather_z"):
         return (B * Ci * inp * es + B * Ci * 9 * outp * 4, 2.0 * pairs * B * Ci, "hbm")
     if name == "contract_z":
@@ -179,6 +192,7 @@ def cpu_baseline(wl, x, w, seconds=15.0):
     rng = np.random.default_rng(12345)
     args = wl.plan_args()
     fn = o.forward if wl.op == "forward" else o.transpose
+    kw = wl.oracle_kwargs()
     x64, w64 = x.astype(np.float64), w.astype(np.float64)
     # Grow the sample until one timed call takes at least half the budget
     # (the first calls also pay thread start-up, so one calibration is short).
@@ -186,7 +200,7 @@ def cpu_baseline(wl, x, w, seconds=15.0):
     for _ in range(6):
         pix = rng.choice(nlat * nlon, size=n, replace=False)
         t0 = time.perf_counter()
-        fn(*args, x64, w64, pix=pix)
+        fn(*args, x64, w64, pix=pix, **kw)
         dt = time.perf_counter() - t0
         if dt >= 0.5 * seconds or n == nlat * nlon:
             break
@@ -295,7 +309,7 @@ def main(argv=None):
     w = torch.from_numpy(w_np).to(dev).to(tdt)
     y = torch.empty(wl.y_shape, dtype=tdt, device=dev)
     t0 = time.time()
-    plan = disco.Plan(*wl.plan_args())
+    plan = disco.Plan(*wl.plan_args(), **wl.plan_kwargs())
     plan_s = time.time() - t0
     info = plan.info()
     log("plan built in %.2fs: %s" % (plan_s, info))
@@ -340,7 +354,7 @@ def main(argv=None):
     # move the gathered sums through HBM: their achieved GB/s against the
     # HBM peak (the default schedule's kernels are bound by arithmetic).
     hbm = None
-    if not args.no_hbm_schedule and args.algo != "gather_then_contract":
+    if not args.no_hbm_schedule and args.algo != "gather_then_contract" and wl.basis == "bilinear3x3":
         step2 = (lambda: plan.forward(x, w, y, algo="gather_then_contract")) if wl.op == "forward" else \
             (lambda: plan.transpose(x, w, y, algo="gather_then_contract"))
         for _ in range(2):
@@ -366,15 +380,25 @@ def main(argv=None):
     op_bytes = wl.batch * (wl.c_in * (wl.nlat_in * wl.nlon_in if wl.op == "forward" else
                                       wl.nlat_out * wl.nlon_out)
                            + wl.c_out * wl.y_shape[2] * wl.y_shape[3]) * es
+    metric = METRIC if wl.name == synth.HEADLINE else \
+        "DISCO %s output pix*chan/s on %s" % ("fwd" if wl.op == "forward" else "transpose", wl.name)
+    vs_baseline, baseline = None, None
+    if wl.name in PAPER_SECONDS:
+        paper = wl.out_pix_chan / PAPER_SECONDS[wl.name]
+        vs_baseline = value / paper
+        baseline = {"value": paper, "unit": UNIT, "seconds": PAPER_SECONDS[wl.name],
+                    "hardware": "NVIDIA RTX 3090 (the paper's App. B; other hardware, context)"}
     out = {
-        "metric": METRIC, "value": value, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
+        "metric": metric, "value": value, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32" if wl.dtype == "fp32" else "bf16",
+        "scaling": "weak", "vs_baseline": vs_baseline,
+        "dtype": "f32" if wl.dtype == "fp32" else "bf16",
         "data": "synthetic",
         "config": {"workload": wl.name, "op": wl.op, "nlat_in": wl.nlat_in, "nlon_in": wl.nlon_in,
                    "nlat_out": wl.nlat_out, "nlon_out": wl.nlon_out, "theta_c": wl.theta_c,
-                   "batch": wl.batch, "c_in": wl.c_in, "c_out": wl.c_out, "basis": "bilinear3x3",
-                   "algo": args.algo, "storage": wl.dtype},
+                   "batch": wl.batch, "c_in": wl.c_in, "c_out": wl.c_out, "basis": wl.basis,
+                   "sampling": wl.sampling, "algo": args.algo, "storage": wl.dtype},
+        "paper_baseline": baseline,
         "op_algorithmic_gbs": round(op_bytes / (ms_per_step / 1e3) / 1e9, 2),
         "kernels": per_kernel,
         "roofline": roof,

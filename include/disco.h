@@ -12,19 +12,29 @@
  *              (Sec. 3.5, eq. 6: the filter is centred at the transposed
  *               op's input points and weighted by their quadrature)
  *
- * Grids are equiangular and cell-centred: colatitude (t + 1/2) pi / nlat,
- * longitude 2 pi p / nlon, longitude fastest in memory.  A plan fixes one
+ * Grids are equiangular, longitude fastest in memory, longitude 2 pi p / nlon,
+ * in one of two samplings: cell-centred, colatitude (t + 1/2) pi / nlat (the
+ * default), or the paper's own pole-including grid (Sec. 4.2 "Explicit
+ * sampling", the antipodal McEwen-Wiaux variant of App. A): with
+ * L = nlat - 1, colatitude pi t / L for t = 0..L and nlon = 2L, each pole ring
+ * holding 2L samples of one point.  A plan fixes one
  * (in-grid, out-grid) pair: the forward op maps in -> out, the transposed op
  * maps out -> in with the same filter pairs.  The longitude compression of
  * Sec. 4.2 (one psi pattern per output latitude ring, reused at every output
  * longitude by a cyclic shift) requires nlon_in / nlon_out or nlon_out /
  * nlon_in to be an integer.
  *
- * Basis: the 3x3 node grid of App. E.2, projected onto the sphere with the
- * azimuthal equidistant map (edge nodes at geodesic distance h, corner nodes
- * at sqrt(2) h), bilinear interpolation between nodes (Sec. 3.4), node index
- * k = 3a + b with a along increasing colatitude (south) and b along
- * increasing longitude (east); the filter is zero beyond theta_c.
+ * Bases (Sec. 3.4: equally spaced nodes, linear interpolation, zero beyond
+ * theta_c):
+ *   DISCO_BASIS_BILINEAR_3X3 (K = 9): the 3x3 node grid of App. E.2,
+ *     projected onto the sphere with the azimuthal equidistant map (edge nodes
+ *     at geodesic distance h, corner nodes at sqrt(2) h), bilinear
+ *     interpolation between nodes, node index k = 3a + b with a along
+ *     increasing colatitude (south) and b along increasing longitude (east);
+ *   DISCO_BASIS_AXISYMMETRIC_4 (K = 4): the axisymmetric filter psi(theta)
+ *     that App. B times, four nodes at geodesic distance k h, k = 0..3,
+ *     psi_k(Theta) = max(0, 1 - |Theta / h - k|); the default h = theta_c / 4
+ *     makes the last hat vanish at the cutoff.
  *
  * Conventions for every call:
  *   - every call returns a disco_status_t; on failure nothing is enqueued on
@@ -64,8 +74,13 @@ typedef enum {
 
 typedef enum { DISCO_FLOAT32 = 0, DISCO_BFLOAT16 = 1 } disco_dtype_t;
 
-enum { DISCO_BASIS_BILINEAR_3X3 = 0 };               /* K = 9 (App. E.2) */
-enum { DISCO_QUAD_FEJER1 = 0, DISCO_QUAD_CELL_AREA = 1 };
+enum { DISCO_BASIS_BILINEAR_3X3 = 0,                /* K = 9 (App. E.2) */
+       DISCO_BASIS_AXISYMMETRIC_4 = 1 };             /* K = 4 (Sec. 3.4, App. B) */
+/* Quadrature: 0 = the sampling-theorem weights of the grid (Sec. 4.1): Fejer's
+ * first rule in cos(theta) on the cell-centred grid, App. A's weights on the
+ * pole-including grid; 1 = cell areas (cell-centred grid only). */
+enum { DISCO_QUAD_FEJER1 = 0, DISCO_QUAD_SAMPLING_THEOREM = 0, DISCO_QUAD_CELL_AREA = 1 };
+enum { DISCO_SAMPLING_CELL_CENTRED = 0, DISCO_SAMPLING_POLES = 1 };
 
 /* Execution variants.  AUTO picks the fastest path for the plan and shapes;
  * the others force one path (all give the same result up to fp32 rounding). */
@@ -79,20 +94,22 @@ typedef enum {
 } disco_algo_t;
 
 typedef struct {
-    int32_t kind;        /* DISCO_BASIS_BILINEAR_3X3 */
-    int32_t quadrature;  /* DISCO_QUAD_FEJER1 (default) or DISCO_QUAD_CELL_AREA */
-    double node_spacing; /* h in radians; 0 selects theta_c / 3 */
+    int32_t kind;        /* DISCO_BASIS_BILINEAR_3X3 or DISCO_BASIS_AXISYMMETRIC_4 */
+    int32_t quadrature;  /* DISCO_QUAD_SAMPLING_THEOREM (default) or DISCO_QUAD_CELL_AREA */
+    double node_spacing; /* h in radians; 0 selects theta_c / 3 (3x3) or theta_c / 4 (axisymmetric) */
+    int32_t sampling;    /* DISCO_SAMPLING_CELL_CENTRED (default) or DISCO_SAMPLING_POLES */
+    int32_t reserved;    /* must be 0 */
 } disco_basis_t;
 
 typedef struct {
     void* data;       /* device pointer (may be NULL only when the tensor is empty) */
     int32_t dtype;    /* disco_dtype_t */
-    int32_t ndim;     /* x, y: 4 ([B, C, nlat, nlon]); w: 3 ([C0, C1, 9]) */
+    int32_t ndim;     /* x, y: 4 ([B, C, nlat, nlon]); w: 3 ([C0, C1, K]) */
     int64_t shape[4];
 } disco_tensor_t;
 
 typedef struct {
-    int32_t K;                 /* basis size (9) */
+    int32_t K;                 /* basis size (9 or 4) */
     int32_t nlat_in, nlon_in, nlat_out, nlon_out;
     int32_t phases_forward;    /* longitude phases of the forward op's patterns */
     int32_t phases_transpose;  /* ... and of the transposed op's */
@@ -115,9 +132,12 @@ typedef struct {
  * closed-form longitude window, rotation, basis, quadrature; Sec. 4.1 and
  * 4.2), rounds them to fp32 and uploads them to the current device.
  *   nlat_* >= 1, nlon_* >= 2, 0 < theta_c <= pi; basis may be NULL (defaults).
- * Errors: INVALID_ARGUMENT (sizes, cutoff, negative node spacing, NULL
- * plan_out), UNSUPPORTED (longitude ratio not an integer, unknown basis or
- * quadrature), OUT_OF_MEMORY, DEVICE.  On success *plan_out owns the device
+ *   The pole-including sampling needs nlat >= 2 and nlon = 2 (nlat - 1) on
+ *   both grids.
+ * Errors: INVALID_ARGUMENT (sizes, cutoff, negative node spacing, nonzero
+ * reserved field, NULL plan_out), UNSUPPORTED (longitude ratio not an
+ * integer, unknown basis, sampling or quadrature, cell areas on the
+ * pole-including grid), OUT_OF_MEMORY, DEVICE.  On success *plan_out owns the device
  * memory until disco_plan_destroy. */
 disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlon_out,
                                  double theta_c, const disco_basis_t* basis,
@@ -132,14 +152,14 @@ disco_status_t disco_plan_destroy(disco_plan_t plan);
 disco_status_t disco_plan_query(disco_plan_t plan, disco_plan_info_t* info);
 
 /* Forward op (Sec. 3.2 eq. 4 on SO(3)/SO(2), Sec. 4.2 compressed product):
- *   x [B, Cin, nlat_in, nlon_in], w [Cout, Cin, 9], y [B, Cout, nlat_out, nlon_out].
+ *   x [B, Cin, nlat_in, nlon_in], w [Cout, Cin, K], y [B, Cout, nlat_out, nlon_out].
  * B may be 0 (nothing is enqueued).  Errors: INVALID_ARGUMENT, SHAPE, DTYPE,
  * OUT_OF_MEMORY (workspace), DEVICE. */
 disco_status_t disco_forward(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
                              disco_tensor_t* y, hipStream_t stream);
 
 /* Transposed op (Sec. 3.5 eq. 6), used for upsampling:
- *   x [B, CinT, nlat_out, nlon_out], w [CinT, CoutT, 9] (the same buffer as
+ *   x [B, CinT, nlat_out, nlon_out], w [CinT, CoutT, K] (the same buffer as
  *   the forward op's W of the adjoint pair), y [B, CoutT, nlat_in, nlon_in].
  * With quadrature-weighted inner products it is the adjoint of the forward
  * op.  Errors as disco_forward. */
@@ -147,7 +167,10 @@ disco_status_t disco_transpose(disco_plan_t plan, const disco_tensor_t* x,
                                const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream);
 
 /* disco_forward / disco_transpose with an explicit execution variant
- * (disco_algo_t).  Same arguments, errors and results. */
+ * (disco_algo_t).  Same arguments, errors and results.  With the
+ * axisymmetric basis every variant runs the one schedule that basis has (W
+ * folded into psi per call, see disco_kernel_work's "stencil" row) except
+ * GATHER_THEN_CONTRACT and CONTRACT_THEN_GATHER, which return UNSUPPORTED. */
 disco_status_t disco_forward_algo(disco_plan_t plan, const disco_tensor_t* x,
                                   const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream,
                                   int32_t algo);
@@ -158,7 +181,8 @@ disco_status_t disco_transpose_algo(disco_plan_t plan, const disco_tensor_t* x,
 /* Host-only export of the stored psi entries of one op, without any device
  * (Sec. 4.1: Psi is constructed explicitly, only where it is non-zero).
  * transpose = 0 selects the forward op, 1 the transposed op.  Each entry is
- * (output ring, phase, input ring, longitude offset d, 9 values); an output
+ * (output ring, phase, input ring, longitude offset d, 9 values: psi_0..8 for
+ * the 3x3 basis, psi_0..3 then five zeros for the axisymmetric one); an output
  * pixel p_out = P * q + phase reads input pixel (stride * q + d) mod nlon of
  * the op's input grid, with P = phases and stride = nlon_in_op * P /
  * nlon_out_op.  Values are psi_k times the quadrature weight of the op's
@@ -193,7 +217,10 @@ disco_status_t disco_kernel_timing_read(int32_t capacity, char* names, int64_t* 
  * out_pixels[i], the output pixels the kernel writes; in_pixels[i], the
  * distinct input pixels it reads; pairs[i], the non-zero (output pixel,
  * input pixel, k) triples of the sparse tensor (Sec. 4.1 eq. 7, of the
- * forward or the transposed op) whose products it accounts for.  A kernel
+ * forward or the transposed op) whose products it accounts for (for the
+ * axisymmetric basis's "stencil" and "stencil_blocked" rows, whose psi has
+ * W folded in, the
+ * (output pixel, input pixel) pairs instead).  A kernel
  * that only moves intermediate data reports zeros where it touches neither
  * x nor y.  Up to `capacity` rows are written (any output pointer may be
  * NULL) and *count receives the number of kernels.  Host only, no device

@@ -57,19 +57,32 @@ disco_status_t resolve_params(int nlat_in, int nlon_in, int nlat_out, int nlon_o
         return fail(DISCO_ERR_INVALID_ARGUMENT, "grid larger than 2^30 pixels");
     if (!(theta_c > 0.0) || !(theta_c <= 3.14159265358979323846) || !std::isfinite(theta_c))
         return fail(DISCO_ERR_INVALID_ARGUMENT, "theta_c must lie in (0, pi]");
-    disco_basis_t b{DISCO_BASIS_BILINEAR_3X3, DISCO_QUAD_FEJER1, 0.0};
+    disco_basis_t b{DISCO_BASIS_BILINEAR_3X3, DISCO_QUAD_SAMPLING_THEOREM, 0.0, DISCO_SAMPLING_CELL_CENTRED, 0};
     if (basis) b = *basis;
-    if (b.kind != DISCO_BASIS_BILINEAR_3X3) return fail(DISCO_ERR_UNSUPPORTED, "unknown basis kind");
-    if (b.quadrature != DISCO_QUAD_FEJER1 && b.quadrature != DISCO_QUAD_CELL_AREA)
+    if (b.reserved != 0) return fail(DISCO_ERR_INVALID_ARGUMENT, "basis.reserved must be 0");
+    if (b.kind != DISCO_BASIS_BILINEAR_3X3 && b.kind != DISCO_BASIS_AXISYMMETRIC_4)
+        return fail(DISCO_ERR_UNSUPPORTED, "unknown basis kind");
+    if (b.sampling != DISCO_SAMPLING_CELL_CENTRED && b.sampling != DISCO_SAMPLING_POLES)
+        return fail(DISCO_ERR_UNSUPPORTED, "unknown sampling");
+    if (b.quadrature != DISCO_QUAD_SAMPLING_THEOREM && b.quadrature != DISCO_QUAD_CELL_AREA)
         return fail(DISCO_ERR_UNSUPPORTED, "unknown quadrature");
+    if (b.sampling == DISCO_SAMPLING_POLES) {
+        if (b.quadrature != DISCO_QUAD_SAMPLING_THEOREM)
+            return fail(DISCO_ERR_UNSUPPORTED, "the pole-including grid takes its sampling-theorem weights only");
+        if (nlat_in < 2 || nlat_out < 2 || nlon_in != 2 * (nlat_in - 1) || nlon_out != 2 * (nlat_out - 1))
+            return fail(DISCO_ERR_INVALID_ARGUMENT, "the pole-including grid needs nlat >= 2 and nlon = 2 (nlat - 1)");
+    }
     if (!(b.node_spacing >= 0.0) || !std::isfinite(b.node_spacing))
         return fail(DISCO_ERR_INVALID_ARGUMENT, "node_spacing must be >= 0");
     if (nlon_in % nlon_out != 0 && nlon_out % nlon_in != 0)
         return fail(DISCO_ERR_UNSUPPORTED, "nlon_in / nlon_out or nlon_out / nlon_in must be an integer");
     p->nlat_in = nlat_in; p->nlon_in = nlon_in; p->nlat_out = nlat_out; p->nlon_out = nlon_out;
     p->theta_c = theta_c;
-    p->h = b.node_spacing > 0.0 ? b.node_spacing : theta_c / 3.0;
+    const double h_default = b.kind == DISCO_BASIS_AXISYMMETRIC_4 ? theta_c / 4.0 : theta_c / 3.0;
+    p->h = b.node_spacing > 0.0 ? b.node_spacing : h_default;
     p->quadrature = b.quadrature;
+    p->basis = b.kind;
+    p->sampling = b.sampling;
     return DISCO_OK;
 }
 
@@ -175,6 +188,32 @@ void free_sweep(SweepDev* d) {
     *d = SweepDev{};
 }
 
+disco_status_t upload_stencil(const HostOp& h, StencilDev* d) {
+    // Entries per work item: enough workgroups (items x longitude tiles) to
+    // fill the chip several times over, within [128, 1024].
+    const int64_t n_qt = (h.g.nq + kStencilTile - 1) / kStencilTile;
+    const int target = (int)std::min<int64_t>(1024, std::max<int64_t>(128, (int64_t)h.t_in.size() * n_qt / 4096));
+    StencilHost H;
+    std::string err;
+    int rc = pack_stencil(h, target, &H, &err);
+    if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
+    disco_status_t s;
+    if ((s = upload_vec(H.pieces, &d->pieces, &d->bytes, "hipMalloc(stencil pieces)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.chunks, &d->chunks, &d->bytes, "hipMalloc(stencil chunks)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.vals, &d->vals, &d->bytes, "hipMalloc(stencil values)")) != DISCO_OK) return s;
+    PackedDev& P = d->P;
+    if ((s = upload_vec(H.segs, &P.segs, &d->bytes, "hipMalloc(segments)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.items, &P.items, &d->bytes, "hipMalloc(items)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.red_pattern, &P.red_pattern, &d->bytes, "hipMalloc(reduce)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.red_ptr, &P.red_ptr, &d->bytes, "hipMalloc(reduce)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.red_slots, &P.red_slots, &d->bytes, "hipMalloc(reduce)")) != DISCO_OK) return s;
+    P.n_items = (int32_t)H.items.size();
+    P.n_split = (int32_t)H.red_pattern.size();
+    P.n_slots = H.n_slots;
+    d->n_padded = (int64_t)H.vals.size();
+    return DISCO_OK;
+}
+
 void free_packed(PackedDev* d) {
     void* ptrs[] = {d->spans, d->chunks, d->offs, d->vals, d->segs, d->items, d->red_pattern, d->red_ptr, d->red_slots};
     for (void* p : ptrs)
@@ -209,9 +248,21 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
     }
     d->bytes = (int64_t)(pb + eb);
     d->work_all = pattern_work(h, {});
+    d->basis = h.basis;
     disco_status_t s = upload_packed(h, {}, &d->packed);
     if (s != DISCO_OK) return s;
     d->bytes += d->packed.bytes;
+    // The axisymmetric basis has its stencil kernels (the blocked one when the
+    // longitude stride is 1); the spectral and sweep layouts are built for the
+    // 3x3 basis.
+    if (h.basis == DISCO_BASIS_AXISYMMETRIC_4) {
+        d->work_light = d->work_all;
+        if (h.g.stride == 1) {
+            if ((s = upload_stencil(h, &d->stencil)) != DISCO_OK) return s;
+            d->bytes += d->stencil.bytes;
+        }
+        return DISCO_OK;
+    }
     SpectralHost sp;
     std::vector<uint8_t> heavy;
     std::string err;
@@ -278,6 +329,11 @@ void free_op(DeviceOp* d) {
     free_packed(&d->packed_rest);
     free_spectral(&d->spectral);
     free_sweep(&d->sweep);
+    void* sp[] = {d->stencil.pieces, d->stencil.chunks, d->stencil.vals};
+    for (void* p : sp)
+        if (p) (void)hipFree(p);
+    free_packed(&d->stencil.P);
+    d->stencil = StencilDev{};
 }
 
 int64_t numel(const disco_tensor_t* t) {
@@ -330,6 +386,7 @@ Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co, int32_t dtyp
         (void)Ci;
     }
     Dispatch d{algo, false, false, &op.packed, &op.work_all};
+    if (op.basis == DISCO_BASIS_AXISYMMETRIC_4) return d;
     d.spectral = algo == DISCO_ALGO_FUSED && op.spectral.n_rings > 0;
     // The sweep kernel addresses x and y through 32-bit buffer offsets: all
     // kCIC input channel planes and one output plane must stay below 2^31
@@ -367,11 +424,16 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
     if (y->shape[2] != g.nlat_o || y->shape[3] != g.nlon_o)
         return fail(DISCO_ERR_SHAPE, "y grid must be [" + std::to_string(g.nlat_o) + ", " + std::to_string(g.nlon_o) + "]");
     if (y->shape[0] != B) return fail(DISCO_ERR_SHAPE, "x and y batch differ");
-    if (w->shape[2] != kBasis) return fail(DISCO_ERR_SHAPE, "w last extent must be 9");
+    const int K = basis_size(op.basis);
+    const std::string ks = std::to_string(K);
+    if (w->shape[2] != K) return fail(DISCO_ERR_SHAPE, "w last extent must be " + ks);
     if (!transpose && (w->shape[0] != Co || w->shape[1] != Ci))
-        return fail(DISCO_ERR_SHAPE, "forward w must be [Cout, Cin, 9]");
+        return fail(DISCO_ERR_SHAPE, "forward w must be [Cout, Cin, " + ks + "]");
     if (transpose && (w->shape[0] != Ci || w->shape[1] != Co))
-        return fail(DISCO_ERR_SHAPE, "transpose w must be [CinT, CoutT, 9]");
+        return fail(DISCO_ERR_SHAPE, "transpose w must be [CinT, CoutT, " + ks + "]");
+    const bool axisym = op.basis == DISCO_BASIS_AXISYMMETRIC_4;
+    if (axisym && (algo == DISCO_ALGO_GATHER_THEN_CONTRACT || algo == DISCO_ALGO_CONTRACT_THEN_GATHER))
+        return fail(DISCO_ERR_UNSUPPORTED, "the axisymmetric basis has no two-kernel schedule");
     if (Ci < 1 || Co < 1) return fail(DISCO_ERR_SHAPE, "channel counts must be >= 1");
     if (B > 65535 || Ci > 4096 || Co > 4096) return fail(DISCO_ERR_SHAPE, "batch or channels too large");
     if (x->dtype != y->dtype || w->dtype != x->dtype)
@@ -396,8 +458,14 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
     algo = dp.algo;
     const bool spectral = dp.spectral, sweep = dp.sweep;
     const PackedDev& packed = *dp.packed;
+    // One output channel on a stride-1 op takes the blocked stencil kernel.
+    const bool blocked = axisym && op.stencil.P.n_items > 0 && Co == 1;
     size_t ws_spec = 0, ws = 0;
-    if (algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {
+    if (blocked) {
+        ws = workspace_bytes_fused(a, op.stencil.P);
+    } else if (axisym) {
+        ws = workspace_bytes_fused(a, packed);
+    } else if (algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {
         ws = workspace_bytes_contract_then_gather(a);
     } else if (algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
         ws = workspace_bytes_gather_then_contract(a);
@@ -418,7 +486,11 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
         e = hipMallocAsync((void**)&ws_ptr, ws, stream);
         if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(workspace)");
     }
-    if (algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {
+    if (blocked) {
+        e = launch_stencil_blocked(a, op.stencil, ws_ptr);
+    } else if (axisym) {
+        e = launch_stencil(a, packed, ws_ptr);
+    } else if (algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {
         e = launch_contract_then_gather(a, ws_ptr);
     } else if (algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
         e = launch_gather_then_contract(a, ws_ptr);
@@ -577,7 +649,7 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
     }
     (void)hipGetLastError();
     disco_plan_info_t& I = plan->info;
-    I.K = kBasis;
+    I.K = basis_size(p.basis);
     I.nlat_in = nlat_in; I.nlon_in = nlon_in; I.nlat_out = nlat_out; I.nlon_out = nlon_out;
     I.phases_forward = hf.g.P;
     I.phases_transpose = ht.g.P;
@@ -636,7 +708,16 @@ disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t a
     ea.B = 1;
     ea.Ci = c_in;
     ea.Co = c_out;
-    if (dp.algo == DISCO_ALGO_GATHER_THEN_CONTRACT && gather_z_split(ea)) {
+    if (op.basis == DISCO_BASIS_AXISYMMETRIC_4) {
+        if (dp.algo != DISCO_ALGO_GATHER_THEN_CONTRACT && dp.algo != DISCO_ALGO_CONTRACT_THEN_GATHER) {
+            // Folded psi: one value per (output pixel, input pixel) pair.
+            const Work fw{all.out_pixels, all.in_pixels, op.n_entries * op.g.nq};
+            const bool blocked = op.stencil.P.n_items > 0 && c_out == 1;
+            rows.push_back({blocked ? "stencil_blocked" : "stencil", fw});
+            if ((blocked ? op.stencil.P.n_split : op.packed.n_split) > 0)
+                rows.push_back({"reduce_partials", Work{0, 0, 0}});
+        }
+    } else if (dp.algo == DISCO_ALGO_GATHER_THEN_CONTRACT && gather_z_split(ea)) {
         rows.push_back({"sweep_gather_z", op.work_sweep});
         if (op.n_rest_pats > 0) rows.push_back({"gather_z", op.work_rest});
         rows.push_back({"contract_z", Work{all.out_pixels - op.work_spectral.out_pixels, 0, 0}});

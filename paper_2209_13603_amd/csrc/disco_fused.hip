@@ -321,13 +321,8 @@ hipError_t fused_launch(const ExecArgs& a, const PackedDev& P, float* partial) {
                        a.Co, n_qtiles, n_cot, a.w_trans);
     timing_end(tk, a.stream);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || P.n_split == 0) return e;
-    dim3 grid2((unsigned)((g.nq + kBlock - 1) / kBlock), (unsigned)P.n_split, (unsigned)(a.B * a.Co));
-    tk = timing_begin("reduce_partials", a.stream);
-    hipLaunchKernelGGL((k_reduce_partials<T>), grid2, dim3(kBlock), 0, a.stream, P.red_pattern,
-                       P.red_ptr, P.red_slots, partial, g, (T*)a.y, a.B, a.Co);
-    timing_end(tk, a.stream);
-    return hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_reduce_partials(a, P, partial);
 }
 
 template <typename T>
@@ -339,6 +334,21 @@ hipError_t fused_dispatch(const ExecArgs& a, const PackedDev& P, float* partial)
 }
 
 }  // namespace
+
+hipError_t launch_reduce_partials(const ExecArgs& a, const PackedDev& P, const float* partial) {
+    const OpGeom& g = a.op->g;
+    if (P.n_items == 0 || P.n_split == 0) return hipSuccess;
+    dim3 grid((unsigned)((g.nq + kBlock - 1) / kBlock), (unsigned)P.n_split, (unsigned)(a.B * a.Co));
+    const int tk = timing_begin("reduce_partials", a.stream);
+    if (a.dtype == 1)
+        hipLaunchKernelGGL((k_reduce_partials<uint16_t>), grid, dim3(kBlock), 0, a.stream, P.red_pattern,
+                           P.red_ptr, P.red_slots, partial, g, (uint16_t*)a.y, a.B, a.Co);
+    else
+        hipLaunchKernelGGL((k_reduce_partials<float>), grid, dim3(kBlock), 0, a.stream, P.red_pattern,
+                           P.red_ptr, P.red_slots, partial, g, (float*)a.y, a.B, a.Co);
+    timing_end(tk, a.stream);
+    return hipGetLastError();
+}
 
 size_t workspace_bytes_fused(const ExecArgs& a, const PackedDev& P) {
     return sizeof(float) * (size_t)P.n_slots * a.B * a.Co * a.op->g.nq;

@@ -10,15 +10,23 @@
 
 namespace disco {
 
+// Values stored per psi entry: the nine functions of the 3x3 basis, or the
+// four of the axisymmetric basis followed by zeros.
 constexpr int kBasis = 9;
+constexpr int kAxisymBasis = 4;
 
 // Parameters of a plan: the forward op maps the in-grid to the out-grid.
 struct PlanParams {
     int nlat_in, nlon_in, nlat_out, nlon_out;
     double theta_c;  // filter cutoff (radians)
-    double h;        // node spacing of the 3x3 grid (radians)
+    double h;        // node spacing (radians)
     int quadrature;  // DISCO_QUAD_*
+    int basis;       // DISCO_BASIS_*
+    int sampling;    // DISCO_SAMPLING_*
 };
+
+// Basis size K of a DISCO_BASIS_* kind.
+inline int basis_size(int basis) { return basis == 1 ? kAxisymBasis : kBasis; }
 
 // Longitude structure of one op (forward or transposed) as a gather:
 // output pixel p_o = P * q + r (q in [0, nq), phase r in [0, P)) reads input
@@ -37,12 +45,13 @@ struct OpGeom {
 // entries of a pattern ordered by input ring then by longitude offset.
 struct HostOp {
     OpGeom g{};
+    int basis = 0;                 // DISCO_BASIS_*
     std::vector<int32_t> pat_ptr;  // n_patterns + 1
     std::vector<int32_t> t_in;     // per entry: input ring
     std::vector<int32_t> d;        // per entry: offset in [0, nlon_i)
     std::vector<int32_t> d_raw;    // per entry: unwrapped offset (contiguous along a window)
-    std::vector<uint8_t> cell;     // per entry: hat cell 4 * cu + cv, cu, cv in [0, 4)
-    std::vector<float> val;        // per entry: 9 values, psi_k * q(input ring)
+    std::vector<uint8_t> cell;     // per entry: hat cell 4 * cu + cv, cu, cv in [0, 4) (3x3 basis; 0 otherwise)
+    std::vector<float> val;        // per entry: 9 values, psi_k * q(input ring) (axisymmetric: k < 4, then zeros)
     std::vector<double> val64;     // the same values before rounding to fp32
     int32_t max_window = 0;
     int32_t full_ring_windows = 0;
@@ -103,6 +112,40 @@ struct PackedHost {
 // (its output is produced elsewhere); skip may be empty.
 int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& skip, PackedHost* out,
             std::string* err);
+
+// ---------------------------------------------------------------------------
+// Blocked layout of the axisymmetric stencil kernel for ops with longitude
+// stride 1 and one output channel (disco_stencil.hip): a workgroup owns
+// kStencilTile consecutive output longitudes (four per lane) of one pattern.
+// A pattern's entries on one input ring form runs of consecutive offsets
+// (the filter's disc meets a ring in one arc); each run ("piece") is padded
+// with zero entries to whole blocks of four, so a lane's four outputs take
+// the block's four weights against seven consecutive inputs read as two
+// aligned float4 (one of them kept from the previous block).  A chunk's
+// pieces are staged in LDS together (each span kStencilTile + 4 nblk
+// floats, 16-byte aligned); chunks form segments and work items as in the
+// fused layout (PSeg / PItem, split patterns summed by k_reduce_partials).
+// Each span carries one more block of columns than its entries read, and
+// the weight table four more entries, for the kernel's one-block-ahead reads.
+constexpr int kStencilTile = 1024;      // output longitudes per workgroup
+constexpr int kStencilCols = 8192;      // LDS floats staged per chunk
+constexpr int kStencilEntries = 1024;   // padded entries (weights) per chunk
+constexpr int kStencilMaxRun = 512;     // entries of one piece
+constexpr int kStencilSpan(int nblk) { return kStencilTile + 4 * nblk + 4; }
+
+struct SPiece { int32_t row, dstart, lds_base, nblk; };           // row = ring * nlon_i; kStencilSpan(nblk) columns
+struct SChunk { int32_t piece_begin, piece_end, ent_begin, ent_end; };
+
+struct StencilHost {
+    std::vector<SPiece> pieces;
+    std::vector<SChunk> chunks;
+    std::vector<PVal> vals;             // per padded entry: psi_0..3 * q (zeros for padding)
+    std::vector<PSeg> segs;             // chunk_begin / chunk_end index chunks
+    std::vector<PItem> items;
+    std::vector<int32_t> red_pattern, red_ptr, red_slots;
+    int32_t n_slots = 0;
+};
+int pack_stencil(const HostOp& op, int target_entries, StencilHost* out, std::string* err);
 
 // ---------------------------------------------------------------------------
 // Sweep layout (disco_sweep.hip): a workgroup walks a run of consecutive
@@ -206,6 +249,15 @@ struct PackedDev {
     int64_t bytes = 0;
 };
 
+struct StencilDev {
+    SPiece* pieces = nullptr;
+    SChunk* chunks = nullptr;
+    PVal* vals = nullptr;
+    PackedDev P;                        // segs, items and the reduction tables (no spans)
+    int64_t n_padded = 0;
+    int64_t bytes = 0;
+};
+
 // Device-side layout of one op (see disco_kernels.hip).
 struct DevEntry {
     int32_t row;  // input ring * nlon_i
@@ -217,10 +269,12 @@ static_assert(sizeof(DevEntry) == 48, "DevEntry is 12 dwords");
 
 struct DeviceOp {
     OpGeom g{};
+    int basis = 0;           // DISCO_BASIS_*: the axisymmetric basis runs only launch_stencil
     PackedDev packed;        // every pattern through the direct kernel
     PackedDev packed_light;  // patterns not handled by the spectral path
     SpectralDev spectral;
     SweepDev sweep;          // light patterns walked by the sweep kernel (Ci <= kCIC)
+    StencilDev stencil;      // axisymmetric basis, longitude stride 1: the blocked layout
     PackedDev packed_rest;   // light patterns the sweep runs do not cover
     int32_t* rest_pats = nullptr;  // device: those patterns' indices (gather-then-contract schedule)
     int32_t n_rest_pats = 0;
@@ -267,5 +321,14 @@ constexpr int kSpectralAll = 7;
 hipError_t launch_spectral(const ExecArgs& a, float* ws, int stages = kSpectralAll);
 hipError_t launch_sweep(const ExecArgs& a);
 size_t workspace_bytes_spectral(const ExecArgs& a);
+// Sums the partial outputs of split patterns (the fused and stencil kernels' slots).
+hipError_t launch_reduce_partials(const ExecArgs& a, const PackedDev& P, const float* partial);
+// Axisymmetric basis (disco_stencil.hip): W folded into the packed psi values
+// per call, one scalar weight per entry and channel pair, gathered directly
+// into y.  Workspace as launch_fused.
+hipError_t launch_stencil(const ExecArgs& a, const PackedDev& P, float* partial_ws);
+// The blocked kernel (one output channel, longitude stride 1); workspace
+// sizeof(float) * n_slots * B * nq.
+hipError_t launch_stencil_blocked(const ExecArgs& a, const StencilDev& S, float* partial_ws);
 
 }  // namespace disco

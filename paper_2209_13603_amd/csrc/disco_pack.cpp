@@ -85,6 +85,12 @@ int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& sk
                     E.off = lds + (op.d_raw[(size_t)e] - pc.d_first);
                     int n = 0;
                     const float* v9 = &op.val[(size_t)e * kBasis];
+                    if (op.basis == DISCO_BASIS_AXISYMMETRIC_4) {
+                        // All four values (one hat cell): the stencil kernel folds W into them.
+                        for (int k = 0; k < kAxisymBasis; ++k) E.v[k] = v9[k];
+                        ents.push_back({0, E});
+                        continue;
+                    }
                     for (int a = 0; a < 3; ++a)
                         for (int b = 0; b < 3; ++b) {
                             const bool in_cell = a >= cell_first(cu) && a < cell_first(cu) + cell_count(cu) &&
@@ -337,6 +343,120 @@ int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& sk
     std::vector<SRun> sorted;
     for (size_t r : order) sorted.push_back(H.runs[r]);
     H.runs.swap(sorted);
+    *out = std::move(H);
+    return DISCO_OK;
+}
+
+}  // namespace disco
+
+namespace disco {
+
+int pack_stencil(const HostOp& op, int target_entries, StencilHost* out, std::string* err) {
+    const OpGeom& g = op.g;
+    if (g.stride != 1) {
+        if (err) *err = "the blocked stencil layout needs longitude stride 1";
+        return DISCO_ERR_UNSUPPORTED;
+    }
+    StencilHost H;
+    struct Run {
+        int32_t ti, d_first, d_last;
+        std::vector<PVal> v;
+    };
+    for (int pat = 0; pat < g.n_patterns(); ++pat) {
+        const int32_t e0 = op.pat_ptr[(size_t)pat], e1 = op.pat_ptr[(size_t)pat + 1];
+        // 1. Runs of consecutive offsets on one input ring (gaps of up to
+        //    three offsets filled with zero entries), padded to whole blocks.
+        std::vector<Run> runs;
+        for (int32_t e = e0; e < e1; ++e) {
+            const int32_t ti = op.t_in[(size_t)e], dr = op.d_raw[(size_t)e];
+            PVal pv{};
+            for (int k = 0; k < kAxisymBasis; ++k) pv.v[k] = op.val[(size_t)e * kBasis + k];
+            if (!runs.empty() && runs.back().ti == ti && dr > runs.back().d_last &&
+                dr - runs.back().d_last <= 4 && dr - runs.back().d_first + 1 <= kStencilMaxRun) {
+                Run& r = runs.back();
+                for (int32_t gap = r.d_last + 1; gap < dr; ++gap) r.v.push_back(PVal{});
+                r.v.push_back(pv);
+                r.d_last = dr;
+            } else {
+                runs.push_back(Run{ti, dr, dr, {pv}});
+            }
+        }
+        for (Run& r : runs)
+            while (r.v.size() % 4) r.v.push_back(PVal{});
+        // 2. Chunks: runs packed greedily under the LDS column and entry budgets.
+        const int32_t chunk_first = (int32_t)H.chunks.size();
+        std::vector<int32_t> chunk_entries;
+        int used = 0, used_e = 0;
+        for (size_t i = 0; i < runs.size(); ++i) {
+            const int ne = (int)runs[i].v.size();
+            const int len = kStencilSpan(ne / 4);  // staged columns, a multiple of 4
+            if (H.chunks.size() == (size_t)chunk_first || used + len > kStencilCols ||
+                used_e + ne > kStencilEntries) {
+                const int32_t pb = (int32_t)H.pieces.size(), eb = (int32_t)H.vals.size();
+                H.chunks.push_back(SChunk{pb, pb, eb, eb});
+                chunk_entries.push_back(0);
+                used = 0;
+                used_e = 0;
+            }
+            SChunk& C = H.chunks.back();
+            H.pieces.push_back(SPiece{runs[i].ti * g.nlon_i, runs[i].d_first, used, ne / 4});
+            H.vals.insert(H.vals.end(), runs[i].v.begin(), runs[i].v.end());
+            C.piece_end = (int32_t)H.pieces.size();
+            C.ent_end = (int32_t)H.vals.size();
+            chunk_entries.back() += ne;
+            used += len;
+            used_e += ne;
+        }
+        // 3. Segments of consecutive chunks with at most target_entries entries.
+        const int32_t nch = (int32_t)H.chunks.size() - chunk_first;
+        std::vector<std::pair<int32_t, int32_t>> segs;
+        if (nch == 0) {
+            segs.push_back({chunk_first, chunk_first});  // empty pattern: writes zeros
+        } else {
+            int acc = 0;
+            for (int32_t c = 0; c < nch; ++c) {
+                if (segs.empty() || acc + chunk_entries[(size_t)c] > target_entries) {
+                    segs.push_back({chunk_first + c, chunk_first + c + 1});
+                    acc = chunk_entries[(size_t)c];
+                } else {
+                    segs.back().second = chunk_first + c + 1;
+                    acc += chunk_entries[(size_t)c];
+                }
+            }
+        }
+        if (segs.size() > 1) {
+            H.red_pattern.push_back(pat);
+            if (H.red_ptr.empty()) H.red_ptr.push_back(0);
+        }
+        for (auto& sg : segs) {
+            int32_t slot = -1;
+            if (segs.size() > 1) {
+                slot = H.n_slots++;
+                H.red_slots.push_back(slot);
+            }
+            H.segs.push_back(PSeg{pat, sg.first, sg.second, slot});
+        }
+        if (segs.size() > 1) H.red_ptr.push_back((int32_t)H.red_slots.size());
+    }
+    // Work items: runs of consecutive segments with a bounded cost (entries,
+    // staged columns, fixed per-segment work) and at most 64 segments.
+    int acc = 0;
+    for (int32_t i = 0; i < (int32_t)H.segs.size(); ++i) {
+        const PSeg& sg = H.segs[(size_t)i];
+        int n = 16;
+        for (int32_t c = sg.chunk_begin; c < sg.chunk_end; ++c) {
+            const SChunk& C = H.chunks[(size_t)c];
+            n += C.ent_end - C.ent_begin;
+            n += (C.piece_end - C.piece_begin) * kStencilTile / 32;
+        }
+        if (H.items.empty() || acc + n > target_entries || H.items.back().seg_end - H.items.back().seg_begin >= 64) {
+            H.items.push_back(PItem{i, i + 1});
+            acc = n;
+        } else {
+            H.items.back().seg_end = i + 1;
+            acc += n;
+        }
+    }
     *out = std::move(H);
     return DISCO_OK;
 }

@@ -18,11 +18,17 @@
 //   y' = sin(ti) sin(dphi)
 //   z' = cos(ti - tj) - 2 sin(ti) sin(tj) sin^2(dphi/2)
 // Theta = atan2(|(x', y')|, z'), (u, v) = Theta (x', y') / |(x', y')|
-// (azimuthal equidistant tangent plane: u south, v east).  Basis values below
-// 1e-12 (rounding noise where a hat is evaluated at its own zero) are set to
-// zero, and entries whose nine basis values are all zero are dropped.  Values absorb the quadrature weight
-// of the op's input ring (Sec. 4.1: quadrature absorbed into f) and are then
-// rounded to fp32.
+// (azimuthal equidistant tangent plane: u south, v east); the axisymmetric
+// basis needs Theta only.  Basis values below 1e-12 (rounding noise where a
+// hat is evaluated at its own zero) are set to zero, and entries whose basis
+// values are all zero are dropped.  Values absorb the quadrature weight of the
+// op's input ring (Sec. 4.1: quadrature absorbed into f) and are then rounded
+// to fp32.
+//
+// On the pole-including grid (Sec. 4.2 explicit sampling) a pole ring is one
+// point: its sine is taken as exactly zero, which makes every window that
+// touches it a whole ring, and the distance to it is the colatitude
+// difference alone.
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
@@ -39,18 +45,72 @@ constexpr double kPi = 3.14159265358979323846;
 // Basis values below this (the hats are at most 1) are treated as zero.
 constexpr double kPsiFloor = 1e-12;
 
-double colat(int t, int nlat) { return (t + 0.5) * kPi / nlat; }
+bool poles(int sampling) { return sampling == DISCO_SAMPLING_POLES; }
+
+// Colatitude of ring t: cell-centred (t + 1/2) pi / nlat, or pi t / (nlat - 1)
+// on the pole-including grid.
+double colat(int t, int nlat, int sampling) {
+    return poles(sampling) ? kPi * t / (nlat - 1) : (t + 0.5) * kPi / nlat;
+}
+
+// sin and cos of ring t's colatitude, exactly (0, +-1) at the poles.
+void ring_trig(int t, int nlat, int sampling, double* s, double* c) {
+    if (poles(sampling) && (t == 0 || t == nlat - 1)) {
+        *s = 0.0;
+        *c = t == 0 ? 1.0 : -1.0;
+        return;
+    }
+    const double th = colat(t, nlat, sampling);
+    *s = std::sin(th);
+    *c = std::cos(th);
+}
+
+// theta(ti on the op's input grid) - theta(to on its output grid), from
+// integers.
+double colat_diff(int ti, int nlat_i, int to, int nlat_o, int sampling) {
+    if (poles(sampling)) {
+        const int64_t num = (int64_t)ti * (nlat_o - 1) - (int64_t)to * (nlat_i - 1);
+        return kPi * (double)num / ((double)(nlat_i - 1) * (nlat_o - 1));
+    }
+    const int64_t num = (int64_t)(2 * ti + 1) * nlat_o - (int64_t)(2 * to + 1) * nlat_i;
+    return kPi * (double)num / (2.0 * (double)nlat_i * nlat_o);
+}
+
+// App. A weights of the pole-including grid (L = nlat - 1, nlon = 2L):
+// q(theta_t) = 2 pi / (2L)^2 [w_r(theta_t) + w_r(theta_{2L-t})] inside and
+// 2 pi / (2L)^2 w_r(theta_t) at the poles, w_r the band-limited (|m| <= L,
+// m = -L included) Fourier series of sin(theta) on [0, pi], zero on
+// (pi, 2 pi).  Taken in real form: the coefficients of m and -m are complex
+// conjugates, the odd ones vanish except m = +-1, whose sine terms cancel in
+// the fold and vanish at the poles, and e^{-i L theta_t} = cos(L theta_t), so
+//   w_r + fold = c_t [2 + sum_{even 2 <= m < L} 4 cos(m theta_t) / (1 - m^2)
+//                + (L even) 2 cos(L theta_t) / (1 - L^2)],
+// c_t = 2 inside and 1 at the poles.
+std::vector<double> weights_poles(int nlat) {
+    const int L = nlat - 1;
+    std::vector<double> q((size_t)nlat);
+    for (int t = 0; t <= L; ++t) {
+        const double th = kPi * t / L;
+        double acc = 2.0;
+        for (int m = 2; m < L; m += 2) acc += 4.0 * std::cos(m * th) / (1.0 - (double)m * m);
+        if (L % 2 == 0) acc += 2.0 * std::cos(L * th) / (1.0 - (double)L * L);
+        const double ct = (t == 0 || t == L) ? 1.0 : 2.0;
+        q[(size_t)t] = 2.0 * kPi / (4.0 * (double)L * L) * ct * acc;
+    }
+    return q;
+}
 
 // Quadrature weight per ring (a pixel's weight is its ring's).  Fejer's first
 // rule in cos(theta) on the cell-centred colatitudes, times 2 pi / nlon, is
 // exact for band-limited signals on this grid (the sampling-theorem
 // quadrature the paper adopts, Sec. 3.2 and App. A); cell areas are offered as
-// the alternative.
-std::vector<double> ring_weights(int nlat, int nlon, int kind) {
+// the alternative.  The pole-including grid takes App. A's own weights.
+std::vector<double> ring_weights(int nlat, int nlon, int kind, int sampling) {
+    if (poles(sampling)) return weights_poles(nlat);
     std::vector<double> q(nlat);
     const double dphi = 2.0 * kPi / nlon;
     for (int t = 0; t < nlat; ++t) {
-        const double th = colat(t, nlat);
+        const double th = colat(t, nlat, sampling);
         double w;
         if (kind == DISCO_QUAD_CELL_AREA) {
             const double half = 0.5 * kPi / nlat;
@@ -104,17 +164,20 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
     int rc = make_op_geom(p, transpose, &g, err);
     if (rc) return rc;
     op->g = g;
+    op->basis = p.basis;
+    const bool axisym = p.basis == DISCO_BASIS_AXISYMMETRIC_4;
     // Quadrature of the op's input grid: the forward op sums over plan
     // in-grid points; the transposed op over plan out-grid points, its centres.
-    const std::vector<double> q = ring_weights(g.nlat_i, g.nlon_i, p.quadrature);
+    const std::vector<double> q = ring_weights(g.nlat_i, g.nlon_i, p.quadrature, p.sampling);
     const double h = p.h;
-    // Basis support radius: the hats vanish for max(|u|, |v|) >= 2h.
-    const double radius = std::min(p.theta_c, 2.0 * std::sqrt(2.0) * h);
+    // Basis support radius: the 3x3 hats vanish for max(|u|, |v|) >= 2h, the
+    // axisymmetric ones for Theta >= 4h.
+    const double radius = std::min(p.theta_c, axisym ? 4.0 * h : 2.0 * std::sqrt(2.0) * h);
     const int64_t M = (int64_t)g.nlon_i * g.nlon_o;  // longitude residues per 2 pi
 
     std::vector<double> sin_o(g.nlat_o), cos_o(g.nlat_o), sin_i(g.nlat_i), cos_i(g.nlat_i);
-    for (int t = 0; t < g.nlat_o; ++t) { sin_o[t] = std::sin(colat(t, g.nlat_o)); cos_o[t] = std::cos(colat(t, g.nlat_o)); }
-    for (int t = 0; t < g.nlat_i; ++t) { sin_i[t] = std::sin(colat(t, g.nlat_i)); cos_i[t] = std::cos(colat(t, g.nlat_i)); }
+    for (int t = 0; t < g.nlat_o; ++t) ring_trig(t, g.nlat_o, p.sampling, &sin_o[t], &cos_o[t]);
+    for (int t = 0; t < g.nlat_i; ++t) ring_trig(t, g.nlat_i, p.sampling, &sin_i[t], &cos_i[t]);
 
     op->pat_ptr.assign(1, 0);
     op->t_in.clear(); op->d.clear(); op->d_raw.clear(); op->cell.clear(); op->val.clear(); op->val64.clear();
@@ -123,10 +186,8 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
     for (int to = 0; to < g.nlat_o; ++to) {
         for (int r = 0; r < g.P; ++r) {
             for (int ti = 0; ti < g.nlat_i; ++ti) {
-                // Colatitude difference (input - output) from integers:
-                // pi * ((2ti+1) nlat_o - (2to+1) nlat_i) / (2 nlat_i nlat_o).
-                const int64_t dnum = (int64_t)(2 * ti + 1) * g.nlat_o - (int64_t)(2 * to + 1) * g.nlat_i;
-                const double dth_io = kPi * (double)dnum / (2.0 * (double)g.nlat_i * g.nlat_o);
+                // Colatitude difference (input - output) from integers.
+                const double dth_io = colat_diff(ti, g.nlat_i, to, g.nlat_o, p.sampling);
                 if (std::fabs(dth_io) > radius * (1.0 + 1e-12)) continue;
                 // Centre ring c and evaluation ring e of the filter.
                 double sc, cc, se, ce, dth;  // dth = theta_e - theta_c
@@ -170,12 +231,34 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
                     const double rho = std::hypot(xs, ys);
                     const double Th = std::atan2(rho, zs);
                     if (Th > p.theta_c) continue;
-                    double u = 0.0, v = 0.0;
-                    if (rho > 0.0) { u = Th * xs / rho; v = Th * ys / rho; }
                     float vals[kBasis];
                     double vals64[kBasis];
                     bool any = false;
                     int nzk = 0;
+                    if (axisym) {
+                        // psi_k(Theta) = hat(Theta / h - k), k = 0..3 (Sec. 3.4).
+                        for (int k = 0; k < kBasis; ++k) {
+                            double psi = k < kAxisymBasis ? hat(Th / h - k) : 0.0;
+                            if (psi < kPsiFloor) psi = 0.0;
+                            vals64[k] = psi * q[ti];
+                            vals[k] = (float)vals64[k];
+                            if (psi != 0.0) { any = true; ++nzk; }
+                        }
+                        if (!any) continue;
+                        int64_t dnorm = dd % g.nlon_i;
+                        if (dnorm < 0) dnorm += g.nlon_i;
+                        op->t_in.push_back(ti);
+                        op->d.push_back((int32_t)dnorm);
+                        op->d_raw.push_back((int32_t)dd);
+                        op->cell.push_back(0);
+                        op->val.insert(op->val.end(), vals, vals + kBasis);
+                        op->val64.insert(op->val64.end(), vals64, vals64 + kBasis);
+                        op->nnz_pairs += (int64_t)nzk * g.nq;
+                        ++kept;
+                        continue;
+                    }
+                    double u = 0.0, v = 0.0;
+                    if (rho > 0.0) { u = Th * xs / rho; v = Th * ys / rho; }
                     for (int a = 0; a < 3; ++a) {
                         const double ha = hat(u / h - (a - 1));
                         for (int b = 0; b < 3; ++b) {

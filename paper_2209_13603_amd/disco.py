@@ -26,8 +26,14 @@ DISCO_FLOAT32 = 0
 DISCO_BFLOAT16 = 1
 
 DISCO_BASIS_BILINEAR_3X3 = 0
+DISCO_BASIS_AXISYMMETRIC_4 = 1
 DISCO_QUAD_FEJER1 = 0
+DISCO_QUAD_SAMPLING_THEOREM = 0
 DISCO_QUAD_CELL_AREA = 1
+DISCO_SAMPLING_CELL_CENTRED = 0
+DISCO_SAMPLING_POLES = 1
+BASES = {"bilinear3x3": DISCO_BASIS_BILINEAR_3X3, "axisym4": DISCO_BASIS_AXISYMMETRIC_4}
+SAMPLINGS = {"cell_centred": DISCO_SAMPLING_CELL_CENTRED, "poles": DISCO_SAMPLING_POLES}
 
 ALGO_AUTO = 0
 ALGO_GATHER_THEN_CONTRACT = 1
@@ -54,7 +60,8 @@ class DiscoError(RuntimeError):
 
 class Basis(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("quadrature", ctypes.c_int32),
-                ("node_spacing", ctypes.c_double)]
+                ("node_spacing", ctypes.c_double), ("sampling", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class Tensor(ctypes.Structure):
@@ -140,8 +147,11 @@ def _check(status: int):
         raise DiscoError(status, msg)
 
 
-def _basis(node_spacing=0.0, quadrature=DISCO_QUAD_FEJER1, kind=DISCO_BASIS_BILINEAR_3X3):
-    return Basis(kind, quadrature, float(node_spacing))
+def _basis(node_spacing=0.0, quadrature=DISCO_QUAD_FEJER1, kind=DISCO_BASIS_BILINEAR_3X3,
+           sampling=DISCO_SAMPLING_CELL_CENTRED):
+    kind = BASES[kind] if isinstance(kind, str) else int(kind)
+    sampling = SAMPLINGS[sampling] if isinstance(sampling, str) else int(sampling)
+    return Basis(kind, quadrature, float(node_spacing), sampling, 0)
 
 
 def _tensor(t) -> Tensor:
@@ -169,10 +179,11 @@ class Plan:
     """A DISCO plan for one (in-grid, out-grid) pair (``disco_plan_create``)."""
 
     def __init__(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, node_spacing=0.0,
-                 quadrature=DISCO_QUAD_FEJER1):
+                 quadrature=DISCO_QUAD_FEJER1, basis=DISCO_BASIS_BILINEAR_3X3,
+                 sampling=DISCO_SAMPLING_CELL_CENTRED):
         lib = library()
         h = ctypes.c_void_p()
-        b = _basis(node_spacing, quadrature)
+        b = _basis(node_spacing, quadrature, basis, sampling)
         _check(lib.disco_plan_create(nlat_in, nlon_in, nlat_out, nlon_out, float(theta_c),
                                      ctypes.byref(b), ctypes.byref(h)))
         self._h = h
@@ -229,7 +240,7 @@ class Plan:
         return y
 
     def forward(self, x, w, y=None, algo="auto", stream=None):
-        """y[B, Cout, nlat_out, nlon_out] = DISCO(x[B, Cin, nlat_in, nlon_in]; w[Cout, Cin, 9])."""
+        """y[B, Cout, nlat_out, nlon_out] = DISCO(x[B, Cin, nlat_in, nlon_in]; w[Cout, Cin, K])."""
         if y is None:
             import torch
             y = torch.empty((x.shape[0], w.shape[0]) + self.grid_out, dtype=x.dtype,
@@ -237,7 +248,7 @@ class Plan:
         return self._run("disco_forward_algo", x, w, y, algo, stream)
 
     def transpose(self, x, w, y=None, algo="auto", stream=None):
-        """y[B, CoutT, nlat_in, nlon_in] = DISCO^T(x[B, CinT, nlat_out, nlon_out]; w[CinT, CoutT, 9])."""
+        """y[B, CoutT, nlat_in, nlon_in] = DISCO^T(x[B, CinT, nlat_out, nlon_out]; w[CinT, CoutT, K])."""
         if y is None:
             import torch
             y = torch.empty((x.shape[0], w.shape[1]) + self.grid_in, dtype=x.dtype,
@@ -266,10 +277,11 @@ def kernel_timing_read(capacity: int = 16) -> dict:
 
 
 def psi_entries(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, transpose=False, node_spacing=0.0,
-                quadrature=DISCO_QUAD_FEJER1) -> dict:
+                quadrature=DISCO_QUAD_FEJER1, basis=DISCO_BASIS_BILINEAR_3X3,
+                sampling=DISCO_SAMPLING_CELL_CENTRED) -> dict:
     """Host-only export of the stored psi entries of the forward (or transposed) op."""
     lib = library()
-    b = _basis(node_spacing, quadrature)
+    b = _basis(node_spacing, quadrature, basis, sampling)
     count = ctypes.c_int64()
     phases = ctypes.c_int32()
     stride = ctypes.c_int32()

@@ -15,7 +15,11 @@ Recipe (per workload, one ``numpy.random.default_rng(seed)`` stream, PCG64):
   * the 2048 x 4096 workload replaces x by a smooth band-limited field: per
     channel, 64 real spherical harmonics (l, m) drawn without replacement from
     1 <= l <= 16, 0 <= m <= l, random phases and N(0, 1) amplitudes,
-    normalised to unit area-weighted RMS, plus N(0, 0.1^2) white noise.
+    normalised to unit area-weighted RMS, plus N(0, 0.1^2) white noise;
+  * the paper's own timed layer (one channel, batch 1, the axisymmetric
+    four-node basis, theta_c = 3 pi / L on the pole-including (L + 1) x 2L
+    grid, L = 1024, 2048, 4096) takes the same field evaluated on that grid,
+    and w ~ N(0, 1 / 4).
 """
 from __future__ import annotations
 
@@ -25,6 +29,7 @@ from dataclasses import dataclass
 import numpy as np
 
 K_BASIS = 9
+BASIS_K = {"bilinear3x3": 9, "axisym4": 4}
 
 
 @dataclass(frozen=True)
@@ -47,6 +52,21 @@ class Workload:
     op: str             # "forward" or "transpose"
     seed: int
     field: str = "normal"  # "normal" or "sh_field"
+    basis: str = "bilinear3x3"     # "bilinear3x3" (K = 9) or "axisym4" (K = 4)
+    sampling: str = "cell_centred"  # "cell_centred" or "poles" ((L + 1) x 2L with both poles)
+
+    @property
+    def K(self) -> int:
+        return BASIS_K[self.basis]
+
+    def plan_kwargs(self) -> dict:
+        """Keyword arguments of ``disco.Plan`` beyond the grid and cutoff."""
+        return {"basis": self.basis, "sampling": self.sampling}
+
+    def oracle_kwargs(self) -> dict:
+        """The same choice in the oracle's integer codes."""
+        return {"basis": 1 if self.basis == "axisym4" else 0,
+                "sampling": 1 if self.sampling == "poles" else 0}
 
     @property
     def x_shape(self):
@@ -62,11 +82,11 @@ class Workload:
 
     @property
     def w_shape(self):
-        # forward: W[Cout][Cin][9]; transpose: W[CinT][CoutT][9] (the adjoint
+        # forward: W[Cout][Cin][K]; transpose: W[CinT][CoutT][K] (the adjoint
         # pair shares one buffer).
         if self.op == "forward":
-            return (self.c_out, self.c_in, K_BASIS)
-        return (self.c_in, self.c_out, K_BASIS)
+            return (self.c_out, self.c_in, self.K)
+        return (self.c_in, self.c_out, self.K)
 
     @property
     def out_pix_chan(self) -> int:
@@ -90,6 +110,11 @@ WORKLOADS = {
     "sphere2048x4096": Workload("sphere2048x4096", 2048, 4096, 2048, 4096, 3 * math.pi / 2048,
                                 1, 8, 8, "fp32", "forward", 4, "sh_field"),
 }
+# The paper's own timed layer (App. B), L = 1024, 2048, 4096.
+for _i, _L in enumerate((1024, 2048, 4096)):
+    _n = "poles_axisym_L%d" % _L
+    WORKLOADS[_n] = Workload(_n, _L + 1, 2 * _L, _L + 1, 2 * _L, 3 * math.pi / _L, 1, 1, 1, "fp32",
+                             "forward", 5 + _i, "sh_field", "axisym4", "poles")
 
 # The headline workload: forward on the 2048 x 4096 sphere.
 HEADLINE = "sphere2048x4096"
@@ -132,14 +157,21 @@ def _assoc_legendre(lmax: int, x: np.ndarray) -> dict:
     return P
 
 
+def colatitudes(nlat: int, sampling: str = "cell_centred") -> np.ndarray:
+    """Ring colatitudes of either grid (cell-centred, or both poles included)."""
+    if sampling == "poles":
+        return np.arange(nlat) * math.pi / (nlat - 1)
+    return (np.arange(nlat) + 0.5) * math.pi / nlat
+
+
 def sh_field(rng: np.random.Generator, nlat: int, nlon: int, n_terms: int = 64,
-             lmax: int = 16, noise: float = 0.1) -> np.ndarray:
+             lmax: int = 16, noise: float = 0.1, sampling: str = "cell_centred") -> np.ndarray:
     """One channel of the smooth random field (see module docstring)."""
     pairs = [(l, m) for l in range(1, lmax + 1) for m in range(0, l + 1)]
     pick = rng.choice(len(pairs), size=n_terms, replace=False)
     alpha = rng.uniform(0.0, 2.0 * math.pi, size=n_terms)
     amp = rng.standard_normal(n_terms)
-    theta = (np.arange(nlat) + 0.5) * math.pi / nlat
+    theta = colatitudes(nlat, sampling)
     phi = 2.0 * math.pi * np.arange(nlon) / nlon
     P = _assoc_legendre(lmax, np.cos(theta))
     # f = sum_m A_m(theta) cos(m phi) + B_m(theta) sin(m phi)
@@ -171,17 +203,18 @@ def make_inputs(wl: Workload, batch: int | None = None):
         x = np.empty(xs)
         for b in range(xs[0]):
             for c in range(xs[1]):
-                x[b, c] = sh_field(rng, xs[2], xs[3])
+                x[b, c] = sh_field(rng, xs[2], xs[3], sampling=wl.sampling)
     else:
         x = rng.standard_normal(xs)
-    w = rng.standard_normal(wl.w_shape) * math.sqrt(1.0 / (wl.c_in * K_BASIS))
+    w = rng.standard_normal(wl.w_shape) * math.sqrt(1.0 / (wl.c_in * wl.K))
     return to_storage(x, wl.dtype), to_storage(w, wl.dtype)
 
 
 def random_inputs(seed: int, x_shape, w_shape, dtype: str = "fp32", c_in: int | None = None):
-    """Generic seeded N(0,1) x and N(0, 1/(C_in*9)) w for ad-hoc test shapes."""
+    """Generic seeded N(0,1) x and N(0, 1/(C_in*K)) w for ad-hoc test shapes
+    (K = the last extent of w)."""
     rng = np.random.default_rng(seed)
     x = rng.standard_normal(x_shape)
     c_in = x_shape[1] if c_in is None else c_in
-    w = rng.standard_normal(w_shape) * math.sqrt(1.0 / (c_in * K_BASIS))
+    w = rng.standard_normal(w_shape) * math.sqrt(1.0 / (c_in * w_shape[-1]))
     return to_storage(x, dtype), to_storage(w, dtype)

@@ -45,18 +45,19 @@ def sample_pixels(nlat: int, nlon: int, per_ring: int = 6, seed: int = 0) -> np.
 
 
 def run_gpu(wl_or_args, x: np.ndarray, w: np.ndarray, op: str, dtype: str = "fp32",
-            algo="auto", plan=None):
+            algo="auto", plan=None, plan_kw=None):
     """Run forward/transpose through the C ABI; returns (y as float64 numpy, plan)."""
     import torch
     if plan is None:
-        plan = disco.Plan(*wl_or_args)
+        plan = disco.Plan(*wl_or_args, **(plan_kw or {}))
     xt, wt = torch_dev(x, dtype), torch_dev(w, dtype)
     y = plan.forward(xt, wt, algo=algo) if op == "forward" else plan.transpose(xt, wt, algo=algo)
     torch.cuda.synchronize()
     return to_numpy(y), plan
 
 
-def run_oracle(args, x, w, op, pix=None):
+def run_oracle(args, x, w, op, pix=None, **kw):
+    """kw: the oracle's ``sampling`` and ``basis`` codes."""
     o = oracle.default()
     fn = o.forward if op == "forward" else o.transpose
-    return fn(*args, x.astype(np.float64), w.astype(np.float64), pix=pix)
+    return fn(*args, x.astype(np.float64), w.astype(np.float64), pix=pix, **kw)

@@ -96,20 +96,24 @@ PLAN_CASES = [
 ]
 
 
-def _dense_check(case, transpose):
+def _dense_check(case, transpose, sampling=0, basis=0):
     a, b, c, d = case
-    tc = 3 * math.pi / min(a, c)
+    K = 4 if basis == 1 else 9
+    # theta_c = 3 pixels of the coarser grid (the pole-including grid has
+    # nlat - 1 ring spacings).
+    tc = 3 * math.pi / (min(a, c) - (1 if sampling == 1 else 0))
     o = oracle.default()
-    psi = o.psi_dense(a, b, c, d, tc)      # [Nout_plan, Nin_plan, 9]
+    psi = o.psi_dense(a, b, c, d, tc, sampling=sampling, basis=basis)  # [Nout_plan, Nin_plan, K]
     if not transpose:
         nlat_o, nlon_o, nlat_i, nlon_i = c, d, a, b
-        q = o.quadrature(a, b)
-        dense = psi                           # [op out pixel, op in pixel, 9]
+        q = o.quadrature(a, b, sampling=sampling)
+        dense = psi                           # [op out pixel, op in pixel, K]
     else:
         nlat_o, nlon_o, nlat_i, nlon_i = a, b, c, d
-        q = o.quadrature(c, d)
+        q = o.quadrature(c, d, sampling=sampling)
         dense = psi.transpose(1, 0, 2)        # filter centred at the op's input points
-    ent = disco.psi_entries(a, b, c, d, tc, transpose=transpose)
+    ent = disco.psi_entries(a, b, c, d, tc, transpose=transpose, basis=basis, sampling=sampling)
+    assert not ent["values"][:, K:].any()
     P, s = ent["phases"], ent["stride"]
     assert (P, s) == ((1, nlon_i // nlon_o) if nlon_i % nlon_o == 0 else (nlon_o // nlon_i, 1))
     n = ent["values"].shape[0]
@@ -123,7 +127,7 @@ def _dense_check(case, transpose):
         jo = to * nlon_o + r                  # output pixel q = 0 of the pattern
         ii = ti * nlon_i + dd % nlon_i        # input pixel (stride * 0 + d) mod nlon
         ref = dense[jo, ii] * q[ti]
-        got = ent["values"][e].astype(np.float64)
+        got = ent["values"][e, :K].astype(np.float64)
         assert np.abs(got - ref).max() <= 2e-7 * abs(q[ti]) + 1e-30, (key, got, ref)
     # Completeness: every non-zero dense element of the q = 0 outputs is stored
     # (the two geometry routes may disagree on exact zeros at hat edges by
@@ -141,8 +145,8 @@ def _dense_check(case, transpose):
             for qq in (1, nlon_o // P - 1):
                 jo = to * nlon_o + P * qq + r
                 jr = to * nlon_o + r
-                shifted = np.roll(dense[jr].reshape(nlat_i, nlon_i, 9), s * qq, axis=1)
-                assert np.abs(dense[jo] - shifted.reshape(-1, 9)).max() <= 1e-13
+                shifted = np.roll(dense[jr].reshape(nlat_i, nlon_i, K), s * qq, axis=1)
+                assert np.abs(dense[jo] - shifted.reshape(-1, K)).max() <= 1e-13
 
 
 @pytest.mark.parametrize("case", PLAN_CASES)
@@ -153,6 +157,47 @@ def test_plan_entries_forward_match_dense_psi(case):
 @pytest.mark.parametrize("case", PLAN_CASES)
 def test_plan_entries_transpose_match_dense_psi(case):
     _dense_check(case, True)
+
+
+# The paper's own pole-including (L + 1) x 2L grid (Sec. 4.2) and the
+# axisymmetric basis (Sec. 3.4), on either grid.
+POLE_CASES = [
+    (9, 16, 9, 16),       # L = 8
+    (17, 32, 9, 16),      # 2x downsampling L = 16 -> 8
+    (9, 16, 17, 32),      # forward that upsamples (2 longitude phases)
+    (13, 24, 13, 24),     # L = 12
+]
+
+
+@pytest.mark.parametrize("transpose", [False, True])
+@pytest.mark.parametrize("case", POLE_CASES)
+def test_plan_entries_poles_axisym_match_dense_psi(case, transpose):
+    _dense_check(case, transpose, sampling=1, basis=1)
+
+
+@pytest.mark.parametrize("transpose", [False, True])
+@pytest.mark.parametrize("case", POLE_CASES[:2])
+def test_plan_entries_poles_bilinear_match_dense_psi(case, transpose):
+    _dense_check(case, transpose, sampling=1, basis=0)
+
+
+@pytest.mark.parametrize("transpose", [False, True])
+@pytest.mark.parametrize("case", PLAN_CASES[:3])
+def test_plan_entries_axisym_cell_centred_match_dense_psi(case, transpose):
+    _dense_check(case, transpose, sampling=0, basis=1)
+
+
+def test_pole_grid_validation():
+    B = disco.Basis
+    # nlon must be 2 (nlat - 1); cell areas are not offered there; reserved must be 0.
+    rc, _ = _create(9, 18, 9, 18, 0.3, basis=B(1, 0, 0.0, 1, 0))
+    assert rc == disco.DISCO_ERR_INVALID_ARGUMENT
+    rc, _ = _create(9, 16, 9, 16, 0.3, basis=B(1, 1, 0.0, 1, 0))
+    assert rc == disco.DISCO_ERR_UNSUPPORTED
+    rc, _ = _create(9, 16, 9, 16, 0.3, basis=B(1, 0, 0.0, 2, 0))
+    assert rc == disco.DISCO_ERR_UNSUPPORTED
+    rc, _ = _create(9, 16, 9, 16, 0.3, basis=B(1, 0, 0.0, 1, 3))
+    assert rc == disco.DISCO_ERR_INVALID_ARGUMENT
 
 
 def test_psi_entries_validation():

@@ -56,11 +56,11 @@ def _workload_check(name, pix_per_ring=6):
     wl = synth.WORKLOADS[name]
     say("workload", name)
     x, w = synth.make_inputs(wl)
-    y, plan = run_gpu(wl.plan_args(), x, w, wl.op, wl.dtype)
+    y, plan = run_gpu(wl.plan_args(), x, w, wl.op, wl.dtype, plan_kw=wl.plan_kwargs())
     nlat, nlon = wl.y_shape[2], wl.y_shape[3]
     full = nlat * nlon <= 64 * 128
     pix = None if full else sample_pixels(nlat, nlon, pix_per_ring)
-    ref = run_oracle(wl.plan_args(), x, w, wl.op, pix=pix)
+    ref = run_oracle(wl.plan_args(), x, w, wl.op, pix=pix, **wl.oracle_kwargs())
     got = y if full else y.reshape(y.shape[0], y.shape[1], -1)[:, :, pix]
     err = rel_l2(got, ref)
     tol = BF16_TOL if wl.dtype == "bf16" else FP32_TOL
@@ -160,4 +160,101 @@ def test_bf16_small_grids(chans, op, algo):
     say("  rel_l2 %.3e" % err)
     assert err <= BF16_TOL
     assert np.abs(y - ref).max() <= 3e-2 * np.abs(ref).max()
+    plan.close()
+
+
+# --------------------------------------------------------------------------- #
+# The paper's own timed configuration (App. B): the axisymmetric four-node
+# basis on the pole-including (L + 1) x 2L grid with App. A's quadrature, and
+# the same basis on the cell-centred grid.
+# --------------------------------------------------------------------------- #
+AXISYM_SMALL = [
+    # (nlat_in, nlon_in, nlat_out, nlon_out, sampling)
+    (9, 16, 9, 16, "poles"),
+    (17, 32, 9, 16, "poles"),
+    (9, 16, 17, 32, "poles"),
+    (41, 80, 41, 80, "poles"),        # not a multiple of the 256-lane tile
+    (151, 300, 151, 300, "poles"),    # ragged tail over two tiles
+    (16, 32, 8, 16, "cell_centred"),
+    (33, 300, 33, 300, "cell_centred"),
+]
+
+
+def _axisym_case(case, op, chans, dtype, seed, algo="auto"):
+    a, b, c, d, smp = case
+    L = min(a, c) - 1 if smp == "poles" else min(a, c)
+    tc = 3 * math.pi / L
+    Ci, Co = chans
+    xs = (2, Ci, a, b) if op == "forward" else (2, Ci, c, d)
+    ws = (Co, Ci, 4) if op == "forward" else (Ci, Co, 4)
+    x, w = synth.random_inputs(seed, xs, ws, dtype=dtype)
+    say("axisym", case, op, chans, dtype, algo)
+    y, plan = run_gpu((a, b, c, d, tc), x, w, op, dtype=dtype, algo=algo,
+                      plan_kw={"basis": "axisym4", "sampling": smp})
+    assert plan.info()["K"] == 4
+    ref = run_oracle((a, b, c, d, tc), x, w, op, basis=1, sampling=1 if smp == "poles" else 0)
+    err = rel_l2(y, ref)
+    say("  rel_l2 %.3e" % err)
+    plan.close()
+    return y, ref, err
+
+
+@pytest.mark.parametrize("chans", [(1, 1), (3, 1), (2, 3), (3, 5), (9, 12)], ids=lambda c: "%dto%d" % c)
+@pytest.mark.parametrize("op", ["forward", "transpose"])
+@pytest.mark.parametrize("case", AXISYM_SMALL, ids=lambda c: "%dx%d_%dx%d_%s" % c)
+def test_axisym_small_grids_full(case, op, chans):
+    y, ref, err = _axisym_case(case, op, chans, "fp32", 31)
+    assert err <= FP32_TOL
+    assert np.abs(y - ref).max() <= 1e-5 * np.abs(ref).max()
+
+
+@pytest.mark.parametrize("op", ["forward", "transpose"])
+@pytest.mark.parametrize("case", AXISYM_SMALL[:3], ids=lambda c: "%dx%d_%dx%d_%s" % c)
+@pytest.mark.parametrize("chans", [(3, 5), (1, 1)], ids=lambda c: "%dto%d" % c)
+def test_axisym_bf16(case, op, chans):
+    y, ref, err = _axisym_case(case, op, chans, "bf16", 32)
+    assert err <= BF16_TOL
+
+
+@pytest.mark.parametrize("algo", ["fused", "fused_direct"])
+def test_axisym_algos_agree(algo):
+    """Every accepted execution variant runs the one axisymmetric schedule."""
+    case = AXISYM_SMALL[1]
+    y0, _, _ = _axisym_case(case, "forward", (2, 3), "fp32", 33)
+    y1, _, _ = _axisym_case(case, "forward", (2, 3), "fp32", 33, algo=algo)
+    assert np.array_equal(y0, y1)
+
+
+@pytest.mark.parametrize("algo", ["gather_then_contract", "contract_then_gather"])
+def test_axisym_two_kernel_schedules_unsupported(algo):
+    a, b = 9, 16
+    plan = disco.Plan(a, b, a, b, 3 * math.pi / 8, basis="axisym4", sampling="poles")
+    x, w = synth.random_inputs(34, (1, 1, a, b), (1, 1, 4))
+    with pytest.raises(disco.DiscoError) as ei:
+        run_gpu(None, x, w, "forward", algo=algo, plan=plan)
+    assert ei.value.status == disco.DISCO_ERR_UNSUPPORTED
+    with pytest.raises(disco.DiscoError) as ei:
+        run_gpu(None, x, np.zeros((1, 1, 9), np.float32), "forward", plan=plan)
+    assert ei.value.status == disco.DISCO_ERR_SHAPE
+    plan.close()
+
+
+@pytest.mark.parametrize("L", [1024, 2048, 4096])
+def test_workload_poles_axisym(L):
+    """The paper's timed layer, one channel, on sampled outputs (rings next to
+    both poles included)."""
+    _workload_check("poles_axisym_L%d" % L, pix_per_ring=4 if L < 4096 else 2)
+
+
+def test_poles_axisym_pole_rings_constant():
+    """A pole ring is one point: its outputs agree along longitude to fp32
+    rounding (each lane sums the same entries in its own cyclic order)."""
+    wl = synth.WORKLOADS["poles_axisym_L2048"]
+    x, w = synth.make_inputs(wl)
+    y, plan = run_gpu(wl.plan_args(), x, w, "forward", plan_kw=wl.plan_kwargs())
+    for t in (0, wl.nlat_out - 1):
+        ring = y[0, 0, t]
+        spread = float(np.abs(ring - ring.mean()).max())
+        say("  pole ring %d spread %.3e of %.3e" % (t, spread, abs(ring.mean())))
+        assert spread <= 1e-5 * max(abs(ring.mean()), np.abs(y).max() * 1e-2)
     plan.close()
