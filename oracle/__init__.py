@@ -92,6 +92,13 @@ class Oracle:
             f = getattr(lib, name)
             f.restype = ctypes.c_int
             f.argtypes = sig_ex
+        for name in ("oracle_forward_adjoint_ex", "oracle_transpose_adjoint_ex"):
+            f = getattr(lib, name)
+            f.restype = ctypes.c_int
+            f.argtypes = sig_ex
+        lib.oracle_weight_grad_ex.restype = ctypes.c_int
+        lib.oracle_weight_grad_ex.argtypes = ([ctypes.c_int] * 7 + [ctypes.c_double] * 2
+                                              + [ctypes.c_int] * 4 + [_dp] * 3)
         lib.oracle_max_threads.restype = ctypes.c_int
         self.lib = lib
 
@@ -196,6 +203,51 @@ class Oracle:
         if pix is None:
             y = y.reshape(y.shape[0], y.shape[1], nlat_in, nlon_in)
         return y
+
+    # -- gradients (App. C) ------------------------------------------------------
+    def input_grad(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, dy, w, *, transpose=False,
+                   h=None, quad=QUAD_FEJER1, window=True, pix=None, sampling=SAMPLING_CELL_CENTRED,
+                   basis=BASIS_BILINEAR):
+        """A^T dy for the forward op (dy[B, Cout, out-grid], w[Cout, Cin, K] ->
+        dx[B, Cin, in-grid]) or, with transpose=True, for the transposed op
+        (dyT[B, CoutT, in-grid], w[CinT, CoutT, K] -> dxT[B, CinT, out-grid])."""
+        dy = np.ascontiguousarray(dy, dtype=np.float64)
+        w = np.ascontiguousarray(w, dtype=np.float64)
+        if w.shape[2] != basis_size(basis):
+            raise ValueError("w last extent must be %d" % basis_size(basis))
+        B, C_dy = dy.shape[0], dy.shape[1]
+        C_dx = w.shape[1] if not transpose else w.shape[0]
+        grid = (nlat_out, nlon_out) if transpose else (nlat_in, nlon_in)
+        full = pix is None
+        if full:
+            pix = np.arange(grid[0] * grid[1], dtype=np.int64)
+        pix = np.ascontiguousarray(pix, dtype=np.int64)
+        dx = np.zeros((B, C_dx, pix.size))
+        h = default_h(theta_c, basis) if not h else h
+        fn = self.lib.oracle_transpose_adjoint_ex if transpose else self.lib.oracle_forward_adjoint_ex
+        rc = fn(nlat_in, nlon_in, nlat_out, nlon_out, sampling, basis, theta_c, h, quad, B, C_dy, C_dx,
+                _ptr(dy), _ptr(w), _ptr(dx), int(window), pix.size, _ptr(pix, _i64p))
+        if rc:
+            raise ValueError("input_grad failed (%d)" % rc)
+        return dx.reshape(B, C_dx, grid[0], grid[1]) if full else dx
+
+    def weight_grad(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, x, dy, *, transpose=False,
+                    h=None, quad=QUAD_FEJER1, sampling=SAMPLING_CELL_CENTRED, basis=BASIS_BILINEAR):
+        """dW of the forward op (x[B, Cin, in-grid], dy[B, Cout, out-grid] ->
+        [Cout, Cin, K]) or of the transposed op (xT[B, CinT, out-grid],
+        dyT[B, CoutT, in-grid] -> [CinT, CoutT, K])."""
+        x = np.ascontiguousarray(x, dtype=np.float64)
+        dy = np.ascontiguousarray(dy, dtype=np.float64)
+        B, C_x, C_dy = x.shape[0], x.shape[1], dy.shape[1]
+        K = basis_size(basis)
+        dw = np.zeros((C_x, C_dy, K) if transpose else (C_dy, C_x, K))
+        h = default_h(theta_c, basis) if not h else h
+        rc = self.lib.oracle_weight_grad_ex(int(transpose), nlat_in, nlon_in, nlat_out, nlon_out, sampling,
+                                            basis, theta_c, h, quad, B, C_x, C_dy, _ptr(x), _ptr(dy),
+                                            _ptr(dw))
+        if rc:
+            raise ValueError("weight_grad failed (%d)" % rc)
+        return dw
 
     def max_threads(self) -> int:
         return int(self.lib.oracle_max_threads())

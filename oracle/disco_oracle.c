@@ -474,6 +474,180 @@ int oracle_transpose(int nlat_in, int nlon_in, int nlat_out, int nlon_out, doubl
                                B, CinT, CoutT, xT, w, yT, window, n_pix, pix);
 }
 
+/* ------------------------------------------------------------------------- */
+/* Gradients (App. C).  Both ops are linear in x and in W.  For a scalar loss
+ * with upstream gradient dy = d loss / dy:
+ *   input gradient   dx = A^T dy, the product with Psi transposed in input
+ *                    and output coordinates (App. C, activation gradient);
+ *   weight gradient  dW = d <dy, y> / dW: the chain rule through the sparse
+ *                    values (App. C, kernel-tensor gradient) to the weights
+ *                    of the basis functions,
+ *     forward   dW[co][ci][k] = sum_{b,j} dy[b,co,j]  Z[b,ci,k](j)
+ *     transpose dW[c'][c][k]  = sum_{b,i} dyT[b,c,i]  Z'[b,c',k](i).
+ * Written out per pair of points: the filter is always centred at the
+ * plan's out-grid point j and evaluated at its in-grid point i; the forward
+ * op carries the quadrature weight q_in(i), the transposed op q_out(j), and
+ * each op's adjoint carries the same factor, so that
+ *   forward adjoint    dx[b,ci,i]  = sum_{co,k} W[co][ci][k] sum_j psi_k(R_j^{-1} w_i) q_in(i)  dy[b,co,j]
+ *   transpose adjoint  dxT[b,c',j] = sum_{c,k}  W[c'][c][k]  sum_i psi_k(R_j^{-1} w_i) q_out(j) dyT[b,c,i]
+ */
+/* ------------------------------------------------------------------------- */
+static int adjoint_sum(int of_transpose, grid_t g_in, grid_t g_out, double theta_c, double h,
+                       config_t cfg, int B, int C_dy, int C_dx, const double* dy,
+                       const double* w, double* dx, int window, int64_t n_pix, const int64_t* pix)
+{
+    if (!dy || !w || !dx || !pix || B < 0 || C_dy < 1 || C_dx < 1) return 1;
+    const int K = basis_size(cfg.basis);
+    const int smp = cfg.sampling;
+    /* Outputs: the in-grid for the forward op's adjoint, the out-grid for the
+     * transposed op's; the sum runs over the other grid. */
+    grid_t g_dst = of_transpose ? g_out : g_in;
+    grid_t g_src = of_transpose ? g_in : g_out;
+    double* q = (double*)malloc(sizeof(double) * (size_t)(of_transpose ? g_out.nlat : g_in.nlat));
+    if (!q) return 3;
+    if (oracle_quadrature_s(of_transpose ? g_out.nlat : g_in.nlat, of_transpose ? g_out.nlon : g_in.nlon,
+                            smp, cfg.quad_kind, q)) {
+        free(q);
+        return 2;
+    }
+    int64_t n_src = (int64_t)g_src.nlat * g_src.nlon, n_dst = (int64_t)g_dst.nlat * g_dst.nlon;
+    int bad = 0;
+#pragma omp parallel
+    {
+        double* Z = (double*)malloc(sizeof(double) * (size_t)B * C_dy * 9);
+#pragma omp for schedule(dynamic)
+        for (int64_t n = 0; n < n_pix; ++n) {
+            int64_t o = pix[n];
+            if (o < 0 || o >= n_dst || !Z) {
+#pragma omp atomic write
+                bad = 1;
+                continue;
+            }
+            int td = (int)(o / g_dst.nlon), pd = (int)(o % g_dst.nlon);
+            double th_d = oracle_colatitude_s(td, g_dst.nlat, smp), ph_d = oracle_longitude(pd, g_dst.nlon);
+            memset(Z, 0, sizeof(double) * (size_t)B * C_dy * 9);
+            double m_d[9], e_d[3];
+            inverse_rotation(th_d, ph_d, m_d);
+            unit_vector(th_d, ph_d, e_d);
+            for (int t = 0; t < g_src.nlat; ++t) {
+                double th_s = oracle_colatitude_s(t, g_src.nlat, smp);
+                if (window && fabs(th_s - th_d) > theta_c) continue;
+                for (int p = 0; p < g_src.nlon; ++p) {
+                    double ph_s = oracle_longitude(p, g_src.nlon);
+                    double val[9];
+                    int nz;
+                    if (!of_transpose) {
+                        /* centre at the source point j (out-grid), evaluate at the output i */
+                        double m_s[9];
+                        inverse_rotation(th_s, ph_s, m_s);
+                        nz = filter_values(cfg.basis, m_s, e_d, theta_c, h, val);
+                    } else {
+                        /* centre at the output j (out-grid), evaluate at the source i */
+                        double e_s[3];
+                        unit_vector(th_s, ph_s, e_s);
+                        nz = filter_values(cfg.basis, m_d, e_s, theta_c, h, val);
+                    }
+                    if (!nz) continue;
+                    for (int b = 0; b < B; ++b)
+                        for (int c = 0; c < C_dy; ++c) {
+                            double v = dy[((int64_t)b * C_dy + c) * n_src + (int64_t)t * g_src.nlon + p];
+                            double* zc = Z + ((size_t)b * C_dy + c) * 9;
+                            for (int k = 0; k < K; ++k) zc[k] += val[k] * v;
+                        }
+                }
+            }
+            double qw = q[td];
+            for (int b = 0; b < B; ++b)
+                for (int cx = 0; cx < C_dx; ++cx) {
+                    double s = 0.0;
+                    for (int cy = 0; cy < C_dy; ++cy)
+                        for (int k = 0; k < K; ++k) {
+                            /* forward op: W[co = cy][ci = cx][k]; transposed op: W[c' = cx][c = cy][k]. */
+                            double wv = of_transpose ? w[((int64_t)cx * C_dy + cy) * K + k]
+                                                     : w[((int64_t)cy * C_dx + cx) * K + k];
+                            s += wv * Z[((size_t)b * C_dy + cy) * 9 + k];
+                        }
+                    dx[((int64_t)b * C_dx + cx) * n_pix + n] = qw * s;
+                }
+        }
+        free(Z);
+    }
+    free(q);
+    return bad ? 4 : 0;
+}
+
+/* Forward op's input gradient: dy[B][Cout][nlat_out][nlon_out], w[Cout][Cin][K]
+ * -> dx[B][Cin][n_pix], pix over the in-grid. */
+int oracle_forward_adjoint_ex(int nlat_in, int nlon_in, int nlat_out, int nlon_out, int sampling,
+                              int basis, double theta_c, double h, int quad_kind, int B, int Cout,
+                              int Cin, const double* dy, const double* w, double* dx, int window,
+                              int64_t n_pix, const int64_t* pix)
+{
+    grid_t gi = {nlat_in, nlon_in}, go = {nlat_out, nlon_out};
+    config_t cfg = {sampling, basis, quad_kind};
+    return adjoint_sum(0, gi, go, theta_c, h, cfg, B, Cout, Cin, dy, w, dx, window, n_pix, pix);
+}
+
+/* Transposed op's input gradient: dyT[B][CoutT][nlat_in][nlon_in],
+ * w[CinT][CoutT][K] -> dxT[B][CinT][n_pix], pix over the out-grid. */
+int oracle_transpose_adjoint_ex(int nlat_in, int nlon_in, int nlat_out, int nlon_out, int sampling,
+                                int basis, double theta_c, double h, int quad_kind, int B, int CoutT,
+                                int CinT, const double* dyT, const double* w, double* dxT, int window,
+                                int64_t n_pix, const int64_t* pix)
+{
+    grid_t gi = {nlat_in, nlon_in}, go = {nlat_out, nlon_out};
+    config_t cfg = {sampling, basis, quad_kind};
+    return adjoint_sum(1, gi, go, theta_c, h, cfg, B, CoutT, CinT, dyT, w, dxT, window, n_pix, pix);
+}
+
+/* Weight gradient of either op: Z of every output pixel from the same sum as
+ * the op (disco_sum with the selection W[k'][0][k] = delta(k, k') per input
+ * channel would give it too; here it is accumulated directly), then
+ * dW += dy (x) Z over batch and output pixels.
+ *   forward:   x[B][Cin][in-grid],  dy[B][Cout][out-grid], dw[Cout][Cin][K]
+ *   transpose: xT[B][CinT][out-grid], dyT[B][CoutT][in-grid], dw[CinT][CoutT][K] */
+int oracle_weight_grad_ex(int transpose, int nlat_in, int nlon_in, int nlat_out, int nlon_out,
+                          int sampling, int basis, double theta_c, double h, int quad_kind, int B,
+                          int C_x, int C_dy, const double* x, const double* dy, double* dw)
+{
+    if (!x || !dy || !dw || B < 0 || C_x < 1 || C_dy < 1) return 1;
+    const int K = basis_size(basis);
+    grid_t gi = transpose ? (grid_t){nlat_out, nlon_out} : (grid_t){nlat_in, nlon_in};
+    grid_t go = transpose ? (grid_t){nlat_in, nlon_in} : (grid_t){nlat_out, nlon_out};
+    config_t cfg = {sampling, basis, quad_kind};
+    int64_t n_out = (int64_t)go.nlat * go.nlon;
+    int64_t* pix = (int64_t*)malloc(sizeof(int64_t) * (size_t)n_out);
+    /* Z for every (b, ci, k) through the op's own sum with a selection W:
+     * input channel c of batch item b becomes item b * C_x + c with one
+     * channel, and output channel k' of W_sel[k'][0][k] = delta picks Z_k. */
+    double* wsel = (double*)calloc((size_t)K * K, sizeof(double));
+    double* Z = (double*)malloc(sizeof(double) * (size_t)B * C_x * K * n_out);
+    if (!pix || !wsel || !Z) {
+        free(pix); free(wsel); free(Z);
+        return 3;
+    }
+    for (int64_t n = 0; n < n_out; ++n) pix[n] = n;
+    for (int k = 0; k < K; ++k) wsel[k * K + k] = 1.0;
+    int rc = disco_sum(transpose, gi, go, theta_c, h, cfg, B * C_x, 1, K, x, wsel, Z, 1, n_out, pix);
+    if (rc == 0) {
+        memset(dw, 0, sizeof(double) * (size_t)C_x * C_dy * K);
+        for (int b = 0; b < B; ++b)
+            for (int cx = 0; cx < C_x; ++cx)
+                for (int cy = 0; cy < C_dy; ++cy)
+                    for (int k = 0; k < K; ++k) {
+                        const double* zr = Z + (((int64_t)b * C_x + cx) * K + k) * n_out;
+                        const double* dr = dy + ((int64_t)b * C_dy + cy) * n_out;
+                        double s = 0.0;
+                        for (int64_t n = 0; n < n_out; ++n) s += dr[n] * zr[n];
+                        /* forward: dW[co = cy][ci = cx][k]; transpose: dW[c' = cx][c = cy][k] */
+                        int64_t at = transpose ? ((int64_t)cx * C_dy + cy) * K + k : ((int64_t)cy * C_x + cx) * K + k;
+                        dw[at] += s;
+                    }
+    }
+    free(pix); free(wsel); free(Z);
+    return rc;
+}
+
 int oracle_max_threads(void)
 {
 #ifdef _OPENMP

@@ -602,4 +602,129 @@ def pin_axisym_constant_input(o):
     assert errs[-1] <= 4e-3, errs
 
 
+# --------------------------------------------------------------------------- #
+# Gradients (App. C): the input gradient is the product with Psi transposed,
+# the weight gradient the chain rule through the sparse values.
+# --------------------------------------------------------------------------- #
+_GRAD_CASES = [
+    # (nlat_in, nlon_in, nlat_out, nlon_out, sampling, basis)
+    (16, 32, 8, 16, 0, 0),
+    (8, 16, 16, 32, 0, 0),
+    (9, 16, 9, 16, 1, 1),
+    (17, 32, 9, 16, 1, 0),
+    (12, 24, 6, 12, 0, 1),
+]
+
+
+def _grad_tc(a, c, smp):
+    return 3 * math.pi / (min(a, c) - (1 if smp == 1 else 0))
+
+
+def pin_gradients_match_dense_autograd(o):
+    """As the paper validated its sparse gradients: the same op written as a
+    dense product, y = W . (Psi diag(q) x) (forward) or W^T . (Psi^T diag(q_out)
+    xT) (transpose), differentiated by torch's autograd in fp64, gives the
+    input and weight gradients to machine precision."""
+    import torch
+    for (a, b, c, d, smp, bas) in _GRAD_CASES:
+        tc = _grad_tc(a, c, smp)
+        K = 4 if bas == 1 else 9
+        kw = dict(sampling=smp, basis=bas)
+        psi = torch.tensor(o.psi_dense(a, b, c, d, tc, **kw))            # [Nout, Nin, K]
+        qi = torch.tensor(np.repeat(o.quadrature(a, b, sampling=smp), b))
+        qo = torch.tensor(np.repeat(o.quadrature(c, d, sampling=smp), d))
+        r = _rng(50)
+        B, C1, C2 = 2, 3, 4
+        # forward: x[B, C1, in], w[C2, C1, K], y[B, C2, out]
+        x = torch.tensor(r.standard_normal((B, C1, a * b)), requires_grad=True)
+        w = torch.tensor(r.standard_normal((C2, C1, K)), requires_grad=True)
+        dy = torch.tensor(r.standard_normal((B, C2, c * d)))
+        Z = torch.einsum("jik,bci->bckj", psi, x * qi)
+        (torch.einsum("ock,bckj->boj", w, Z) * dy).sum().backward()
+        dx = o.input_grad(a, b, c, d, tc, dy.numpy().reshape(B, C2, c, d), w.detach().numpy(), **kw)
+        dw = o.weight_grad(a, b, c, d, tc, x.detach().numpy().reshape(B, C1, a, b),
+                           dy.numpy().reshape(B, C2, c, d), **kw)
+        gx, gw = x.grad.numpy().reshape(dx.shape), w.grad.numpy()
+        assert np.abs(dx - gx).max() <= 1e-13 * np.abs(gx).max(), (a, c, smp, bas)
+        assert np.abs(dw - gw).max() <= 1e-13 * np.abs(gw).max(), (a, c, smp, bas)
+        # transpose: xT[B, C1, out], w[C1, C2, K], yT[B, C2, in]
+        xT = torch.tensor(r.standard_normal((B, C1, c * d)), requires_grad=True)
+        wT = torch.tensor(r.standard_normal((C1, C2, K)), requires_grad=True)
+        dyT = torch.tensor(r.standard_normal((B, C2, a * b)))
+        ZT = torch.einsum("jik,bcj->bcki", psi, xT * qo)
+        (torch.einsum("cok,bcki->boi", wT, ZT) * dyT).sum().backward()
+        dxT = o.input_grad(a, b, c, d, tc, dyT.numpy().reshape(B, C2, a, b), wT.detach().numpy(),
+                           transpose=True, **kw)
+        dwT = o.weight_grad(a, b, c, d, tc, xT.detach().numpy().reshape(B, C1, c, d),
+                            dyT.numpy().reshape(B, C2, a, b), transpose=True, **kw)
+        gxT, gwT = xT.grad.numpy().reshape(dxT.shape), wT.grad.numpy()
+        assert np.abs(dxT - gxT).max() <= 1e-13 * np.abs(gxT).max(), (a, c, smp, bas)
+        assert np.abs(dwT - gwT).max() <= 1e-13 * np.abs(gwT).max(), (a, c, smp, bas)
+
+
+def pin_input_gradient_is_plain_adjoint(o):
+    """<A x, dy> = <x, A^T dy> in the plain (unweighted) inner product, for
+    the forward and the transposed op."""
+    for (a, b, c, d, smp, bas) in _GRAD_CASES:
+        tc = _grad_tc(a, c, smp)
+        K = 4 if bas == 1 else 9
+        kw = dict(sampling=smp, basis=bas)
+        r = _rng(51)
+        x = r.standard_normal((2, 3, a, b))
+        w = r.standard_normal((2, 3, K))
+        dy = r.standard_normal((2, 2, c, d))
+        lhs = float((o.forward(a, b, c, d, tc, x, w, **kw) * dy).sum())
+        rhs = float((x * o.input_grad(a, b, c, d, tc, dy, w, **kw)).sum())
+        assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs)), (lhs, rhs)
+        xT = r.standard_normal((2, 3, c, d))
+        dyT = r.standard_normal((2, 2, a, b))
+        wT = r.standard_normal((3, 2, K))
+        lhs = float((o.transpose(a, b, c, d, tc, xT, wT, **kw) * dyT).sum())
+        rhs = float((xT * o.input_grad(a, b, c, d, tc, dyT, wT, transpose=True, **kw)).sum())
+        assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs)), (lhs, rhs)
+
+
+def pin_weight_gradient_by_linearity(o):
+    """y is linear in W, so dW[co, ci, k] = <y(x; E_{co,ci,k}), dy> with E the
+    unit weight tensor: every element through the op itself."""
+    for (a, b, c, d, smp, bas) in _GRAD_CASES[:3]:
+        tc = _grad_tc(a, c, smp)
+        K = 4 if bas == 1 else 9
+        kw = dict(sampling=smp, basis=bas)
+        r = _rng(52)
+        x = r.standard_normal((2, 2, a, b))
+        dy = r.standard_normal((2, 3, c, d))
+        dw = o.weight_grad(a, b, c, d, tc, x, dy, **kw)
+        for (co, ci, k) in [(0, 0, 0), (2, 1, K - 1), (1, 0, K // 2)]:
+            E = np.zeros((3, 2, K))
+            E[co, ci, k] = 1.0
+            ref = float((o.forward(a, b, c, d, tc, x, E, **kw) * dy).sum())
+            assert abs(dw[co, ci, k] - ref) <= 1e-12 * max(1.0, abs(ref)), (co, ci, k, dw[co, ci, k], ref)
+        xT = r.standard_normal((2, 2, c, d))
+        dyT = r.standard_normal((2, 3, a, b))
+        dwT = o.weight_grad(a, b, c, d, tc, xT, dyT, transpose=True, **kw)
+        for (cp, cc, k) in [(0, 0, 0), (1, 2, K - 1)]:
+            E = np.zeros((2, 3, K))
+            E[cp, cc, k] = 1.0
+            ref = float((o.transpose(a, b, c, d, tc, xT, E, **kw) * dyT).sum())
+            assert abs(dwT[cp, cc, k] - ref) <= 1e-12 * max(1.0, abs(ref)), (cp, cc, k)
+
+
+def pin_forward_adjoint_from_transpose(o):
+    """The forward op's adjoint and the transposed op share the filter pairs
+    and differ only in where the quadrature sits: A^T dy = diag(q_in) T diag(1 / q_out) dy."""
+    for (a, b, c, d, smp, bas) in _GRAD_CASES:
+        tc = _grad_tc(a, c, smp)
+        K = 4 if bas == 1 else 9
+        kw = dict(sampling=smp, basis=bas)
+        r = _rng(53)
+        w = r.standard_normal((3, 2, K))
+        dy = r.standard_normal((1, 3, c, d))
+        qi = o.quadrature(a, b, sampling=smp)[None, None, :, None]
+        qo = o.quadrature(c, d, sampling=smp)[None, None, :, None]
+        got = o.input_grad(a, b, c, d, tc, dy, w, **kw)
+        ref = qi * o.transpose(a, b, c, d, tc, dy / qo, w, **kw)
+        assert np.abs(got - ref).max() <= 1e-12 * np.abs(ref).max()
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -52,6 +52,16 @@ MUTANTS = {
     "axisym_node_shift": ("psi[k] = hat(Theta / h - k);", "psi[k] = hat(Theta / h - k - 1);"),
     "axisym_signed_coordinate": ("oracle_basis_axisym(Th, h, psi);", "oracle_basis_axisym(u, h, psi);"),
     "axisym_drops_last_node": ("return basis == 1 ? 4 : 9;", "return basis == 1 ? 3 : 9;"),
+    # Gradients (App. C).
+    "adjoint_quadrature_of_source": ("            double qw = q[td];", "            double qw = q[td] * 0.0 + 1.0;"),
+    "adjoint_w_not_transposed": (": w[((int64_t)cy * C_dx + cx) * K + k];",
+                                 ": w[((int64_t)(cy % C_dx) * C_dy + (cx % C_dy)) * K + k];"),
+    "adjoint_centre_swapped": ("nz = filter_values(cfg.basis, m_s, e_d, theta_c, h, val);",
+                               "nz = filter_values(cfg.basis, m_d, e_s_t, theta_c, h, val);"),
+    "weight_grad_first_batch_only": ("        for (int b = 0; b < B; ++b)\n            for (int cx = 0; cx < C_x; ++cx)\n                for (int cy = 0; cy < C_dy; ++cy)",
+                                     "        for (int b = 0; b < 1; ++b)\n            for (int cx = 0; cx < C_x; ++cx)\n                for (int cy = 0; cy < C_dy; ++cy)"),
+    "weight_grad_layout_swapped": ("int64_t at = transpose ? ((int64_t)cx * C_dy + cy) * K + k : ((int64_t)cy * C_x + cx) * K + k;",
+                                   "int64_t at = transpose ? ((int64_t)cy * C_x + cx) * K + k : ((int64_t)cx * C_dy + cy) * K + k;"),
 }
 
 
@@ -61,6 +71,8 @@ def _mutant_source(name):
     old, new = MUTANTS[name]
     assert src.count(old) == 1, (name, src.count(old))
     src = src.replace(old, new)
+    if name == "adjoint_centre_swapped":
+        src = src.replace("double m_s[9];", "double m_s[9], e_s_t[3]; unit_vector(th_s, ph_s, e_s_t);")
     if name == "transpose_centre_swapped":
         # Evaluate the transposed op's filter centred at the output point.
         src = src.replace("double m_i[9];", "double m_i[9], e_i_t[3]; unit_vector(th_i, ph_i, e_i_t);")
