@@ -98,8 +98,12 @@ typedef struct {
     int32_t quadrature;  /* DISCO_QUAD_SAMPLING_THEOREM (default) or DISCO_QUAD_CELL_AREA */
     double node_spacing; /* h in radians; 0 selects theta_c / 3 (3x3) or theta_c / 4 (axisymmetric) */
     int32_t sampling;    /* DISCO_SAMPLING_CELL_CENTRED (default) or DISCO_SAMPLING_POLES */
-    int32_t reserved;    /* must be 0 */
+    int32_t flags;       /* 0 or DISCO_PLAN_BACKWARD */
 } disco_basis_t;
+
+/* Plan flag: also build the adjoint ops that disco_forward_backward and
+ * disco_transpose_backward need (about twice the plan's device memory). */
+enum { DISCO_PLAN_BACKWARD = 1 };
 
 typedef struct {
     void* data;       /* device pointer (may be NULL only when the tensor is empty) */
@@ -134,8 +138,8 @@ typedef struct {
  *   nlat_* >= 1, nlon_* >= 2, 0 < theta_c <= pi; basis may be NULL (defaults).
  *   The pole-including sampling needs nlat >= 2 and nlon = 2 (nlat - 1) on
  *   both grids.
- * Errors: INVALID_ARGUMENT (sizes, cutoff, negative node spacing, nonzero
- * reserved field, NULL plan_out), UNSUPPORTED (longitude ratio not an
+ * Errors: INVALID_ARGUMENT (sizes, cutoff, negative node spacing, unknown
+ * flags, NULL plan_out), UNSUPPORTED (longitude ratio not an
  * integer, unknown basis, sampling or quadrature, cell areas on the
  * pole-including grid), OUT_OF_MEMORY, DEVICE.  On success *plan_out owns the device
  * memory until disco_plan_destroy. */
@@ -177,6 +181,35 @@ disco_status_t disco_forward_algo(disco_plan_t plan, const disco_tensor_t* x,
 disco_status_t disco_transpose_algo(disco_plan_t plan, const disco_tensor_t* x,
                                     const disco_tensor_t* w, disco_tensor_t* y,
                                     hipStream_t stream, int32_t algo);
+
+/* Gradients of the forward op (App. C) for a scalar loss with upstream
+ * gradient dy = d loss / dy [B, Cout, nlat_out, nlon_out]:
+ *   dx [B, Cin, nlat_in, nlon_in] = A^T dy, the product with Psi transposed
+ *      in input and output coordinates:
+ *      dx[b,ci,i] = sum_{co,k} W[co,ci,k] sum_j psi_k(R_j^{-1} w_i) q_in(i) dy[b,co,j];
+ *   dw [Cout, Cin, K] = sum_{b,j} dy[b,co,j] Z[b,ci,k](j), Z the gathered
+ *      sums of the forward op (the chain rule through the sparse values to
+ *      the basis weights).
+ * x [B, Cin, nlat_in, nlon_in] is the forward input (read for dw only), w the
+ * forward weights (read for dx only).  dx or dw may be NULL (not computed);
+ * dx is overwritten, dw is overwritten (not accumulated).  The plan must have
+ * been created with DISCO_PLAN_BACKWARD.  dw is reduced over pixels in a fixed
+ * order (deterministic); with bf16 storage the gathered sums are rounded to
+ * bf16 before the reduction, which accumulates in fp32.  Errors as
+ * disco_forward, and UNSUPPORTED for a plan without DISCO_PLAN_BACKWARD. */
+disco_status_t disco_forward_backward(disco_plan_t plan, const disco_tensor_t* x,
+                                      const disco_tensor_t* w, const disco_tensor_t* dy,
+                                      disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream);
+
+/* Gradients of the transposed op: dy [B, CoutT, nlat_in, nlon_in],
+ * xT [B, CinT, nlat_out, nlon_out], w [CinT, CoutT, K];
+ *   dx [B, CinT, nlat_out, nlon_out]:
+ *      dx[b,c',j] = sum_{c,k} W[c',c,k] sum_i psi_k(R_j^{-1} w_i) q_out(j) dy[b,c,i];
+ *   dw [CinT, CoutT, K] = sum_{b,i} dy[b,c,i] Z'[b,c',k](i).
+ * Same conventions and errors as disco_forward_backward. */
+disco_status_t disco_transpose_backward(disco_plan_t plan, const disco_tensor_t* x,
+                                        const disco_tensor_t* w, const disco_tensor_t* dy,
+                                        disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream);
 
 /* Host-only export of the stored psi entries of one op, without any device
  * (Sec. 4.1: Psi is constructed explicitly, only where it is non-zero).

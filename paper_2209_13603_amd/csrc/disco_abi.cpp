@@ -22,6 +22,13 @@ struct disco_plan {
     PlanParams params{};
     disco_plan_info_t info{};
     DeviceOp fwd, tr;
+    // DISCO_PLAN_BACKWARD: the adjoint of each op (the other op's filter pairs
+    // weighted by the quadrature of the adjoint's output points, App. C) and
+    // K x K identity weights in fp32 and bf16 (the selection W that makes an
+    // op's kernels write its gathered sums Z).
+    DeviceOp fwd_adj, tr_adj;
+    void* wsel32 = nullptr;
+    void* wsel16 = nullptr;
     hipStream_t aux = nullptr;  // runs the spectral rings beside the direct kernels
 };
 
@@ -59,7 +66,7 @@ disco_status_t resolve_params(int nlat_in, int nlon_in, int nlat_out, int nlon_o
         return fail(DISCO_ERR_INVALID_ARGUMENT, "theta_c must lie in (0, pi]");
     disco_basis_t b{DISCO_BASIS_BILINEAR_3X3, DISCO_QUAD_SAMPLING_THEOREM, 0.0, DISCO_SAMPLING_CELL_CENTRED, 0};
     if (basis) b = *basis;
-    if (b.reserved != 0) return fail(DISCO_ERR_INVALID_ARGUMENT, "basis.reserved must be 0");
+    if ((b.flags & ~DISCO_PLAN_BACKWARD) != 0) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown basis.flags bits");
     if (b.kind != DISCO_BASIS_BILINEAR_3X3 && b.kind != DISCO_BASIS_AXISYMMETRIC_4)
         return fail(DISCO_ERR_UNSUPPORTED, "unknown basis kind");
     if (b.sampling != DISCO_SAMPLING_CELL_CENTRED && b.sampling != DISCO_SAMPLING_POLES)
@@ -83,6 +90,7 @@ disco_status_t resolve_params(int nlat_in, int nlon_in, int nlat_out, int nlon_o
     p->quadrature = b.quadrature;
     p->basis = b.kind;
     p->sampling = b.sampling;
+    p->flags = b.flags;
     return DISCO_OK;
 }
 
@@ -406,12 +414,24 @@ Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co, int32_t dtyp
     return d;
 }
 
+// Validates one application of `op` (x -> y with weights w, W laid out
+// [op Ci][op Co][K] when transpose, else [op Co][op Ci][K]) without launching.
+disco_status_t check_op_args(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
+                             const disco_tensor_t* w, const disco_tensor_t* y, int32_t algo);
+
+disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
+                      const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream, int32_t algo);
+
 disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
                    disco_tensor_t* y, hipStream_t stream, int32_t algo, bool transpose) {
     if (!plan) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan is NULL");
+    return run_op(plan, transpose ? plan->tr : plan->fwd, transpose, x, w, y, stream, algo);
+}
+
+disco_status_t check_op_args(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
+                             const disco_tensor_t* w, const disco_tensor_t* y, int32_t algo) {
     if (!x || !w || !y) return fail(DISCO_ERR_INVALID_ARGUMENT, "tensor descriptor is NULL");
     if (algo < DISCO_ALGO_AUTO || algo > DISCO_ALGO_FUSED_DIRECT) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown algo");
-    const DeviceOp& op = transpose ? plan->tr : plan->fwd;
     const OpGeom& g = op.g;
     if (x->ndim != 4 || y->ndim != 4 || w->ndim != 3)
         return fail(DISCO_ERR_SHAPE, "x and y must be 4-D [B, C, nlat, nlon], w 3-D");
@@ -440,7 +460,7 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
         return fail(DISCO_ERR_DTYPE, "x, w and y must share one dtype");
     if (x->dtype != DISCO_FLOAT32 && x->dtype != DISCO_BFLOAT16)
         return fail(DISCO_ERR_DTYPE, "dtype must be DISCO_FLOAT32 or DISCO_BFLOAT16");
-    if (B == 0) return ok();
+    if (B == 0) return DISCO_OK;
     if (!x->data || !w->data || !y->data) return fail(DISCO_ERR_INVALID_ARGUMENT, "NULL data pointer");
     if (overlaps(y, x) || overlaps(y, w)) return fail(DISCO_ERR_INVALID_ARGUMENT, "y overlaps x or w");
     // Index arithmetic inside the kernels keeps per-plane offsets in 64 bits;
@@ -449,6 +469,17 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
     if ((s = check_device_ptr(x->data, plan->device, "x")) != DISCO_OK) return s;
     if ((s = check_device_ptr(w->data, plan->device, "w")) != DISCO_OK) return s;
     if ((s = check_device_ptr(y->data, plan->device, "y")) != DISCO_OK) return s;
+    return DISCO_OK;
+}
+
+disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
+                      const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream, int32_t algo) {
+    disco_status_t s = check_op_args(plan, op, transpose, x, w, y, algo);
+    if (s != DISCO_OK) return s;
+    const int64_t B = x->shape[0], Ci = x->shape[1], Co = y->shape[1];
+    if (B == 0) return ok();
+    const OpGeom& g = op.g;
+    const bool axisym = op.basis == DISCO_BASIS_AXISYMMETRIC_4;
 
     ExecArgs a{};
     a.op = &op; a.x = x->data; a.w = w->data; a.y = y->data; a.dtype = x->dtype;
@@ -533,6 +564,119 @@ disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tenso
     return ok();
 }
 
+// Gradients of the forward (transpose = false) or transposed op, App. C.
+// The input gradient is one application of the adjoint op (built at plan
+// creation with DISCO_PLAN_BACKWARD; W is read in the other op's layout).
+// The weight gradient first runs the op's own kernels on x viewed as B * C_x
+// one-channel items with the K x K identity as W, which writes the gathered
+// sums Z [B * C_x][K][pixels] to a workspace, then reduces dy (x) Z over
+// pixels (disco_grad.hip).  Everything is validated before anything is
+// enqueued.
+disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t* x, const disco_tensor_t* w,
+                        const disco_tensor_t* dy, disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream) {
+    if (!plan) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (!(plan->params.flags & DISCO_PLAN_BACKWARD))
+        return fail(DISCO_ERR_UNSUPPORTED, "plan was created without DISCO_PLAN_BACKWARD");
+    if (!dy) return fail(DISCO_ERR_INVALID_ARGUMENT, "dy is NULL");
+    if (!dx && !dw) return ok();
+    const DeviceOp& op = transpose ? plan->tr : plan->fwd;
+    const DeviceOp& adj = transpose ? plan->tr_adj : plan->fwd_adj;
+    const int K = basis_size(op.basis);
+    disco_status_t s;
+    // Input gradient: dy -> dx through the adjoint op, whose W layout is the
+    // other op's.
+    if (dx && (s = check_op_args(plan, adj, !transpose, dy, w, dx, DISCO_ALGO_AUTO)) != DISCO_OK) return s;
+    // Weight gradient: shapes, then the Z pass's own arguments.
+    disco_tensor_t xz{}, wsel{}, zt{};
+    int64_t B = 0, C_x = 0, C_dy = 0, P = 0;
+    if (dw) {
+        if (!x) return fail(DISCO_ERR_INVALID_ARGUMENT, "x is NULL (needed for dw)");
+        if (x->ndim != 4 || dw->ndim != 3 || dy->ndim != 4) return fail(DISCO_ERR_SHAPE, "x and dy must be 4-D, dw 3-D");
+        B = x->shape[0]; C_x = x->shape[1]; C_dy = dy->shape[1];
+        if (dy->shape[0] != B) return fail(DISCO_ERR_SHAPE, "x and dy batch differ");
+        if (dy->shape[2] != op.g.nlat_o || dy->shape[3] != op.g.nlon_o)
+            return fail(DISCO_ERR_SHAPE, "dy grid must be the op's output grid");
+        const int64_t want0 = transpose ? C_x : C_dy, want1 = transpose ? C_dy : C_x;
+        if (dw->shape[0] != want0 || dw->shape[1] != want1 || dw->shape[2] != K)
+            return fail(DISCO_ERR_SHAPE, std::string("dw must be ") + (transpose ? "[CinT, CoutT, K]" : "[Cout, Cin, K]"));
+        if (dw->dtype != x->dtype || dy->dtype != x->dtype) return fail(DISCO_ERR_DTYPE, "x, dy and dw must share one dtype");
+        if (B * C_x > 65535) return fail(DISCO_ERR_SHAPE, "batch x channels too large for the weight gradient");
+        P = (int64_t)op.g.nlat_o * op.g.nlon_o;
+        if (B > 0) {
+            if (!dw->data || !dy->data) return fail(DISCO_ERR_INVALID_ARGUMENT, "NULL data pointer");
+            if ((s = check_device_ptr(dw->data, plan->device, "dw")) != DISCO_OK) return s;
+            if ((s = check_device_ptr(dy->data, plan->device, "dy")) != DISCO_OK) return s;
+            if (overlaps(dw, x) || overlaps(dw, dy) || (dx && overlaps(dw, dx)))
+                return fail(DISCO_ERR_INVALID_ARGUMENT, "dw overlaps another tensor");
+        }
+        xz = *x;
+        xz.shape[0] = B * C_x;
+        xz.shape[1] = 1;
+        wsel.data = x->dtype == DISCO_BFLOAT16 ? plan->wsel16 : plan->wsel32;
+        wsel.dtype = x->dtype;
+        wsel.ndim = 3;
+        wsel.shape[0] = transpose ? 1 : K;
+        wsel.shape[1] = transpose ? K : 1;
+        wsel.shape[2] = K;
+        zt.dtype = x->dtype;
+        zt.ndim = 4;
+        zt.shape[0] = B * C_x;
+        zt.shape[1] = K;
+        zt.shape[2] = op.g.nlat_o;
+        zt.shape[3] = op.g.nlon_o;
+        if (x->shape[2] != op.g.nlat_i || x->shape[3] != op.g.nlon_i)
+            return fail(DISCO_ERR_SHAPE, "x grid must be the op's input grid");
+        if (C_x < 1 || C_dy < 1 || C_dy > 4096) return fail(DISCO_ERR_SHAPE, "channel counts out of range");
+        if (x->dtype != DISCO_FLOAT32 && x->dtype != DISCO_BFLOAT16)
+            return fail(DISCO_ERR_DTYPE, "dtype must be DISCO_FLOAT32 or DISCO_BFLOAT16");
+        if (B > 0) {
+            if (!x->data) return fail(DISCO_ERR_INVALID_ARGUMENT, "NULL data pointer");
+            if ((s = check_device_ptr(x->data, plan->device, "x")) != DISCO_OK) return s;
+        }
+    }
+    if (dx && (s = run_op(plan, adj, !transpose, dy, w, dx, stream, DISCO_ALGO_AUTO)) != DISCO_OK) return s;
+    if (!dw || B == 0) return ok();
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return fail(DISCO_ERR_DEVICE, "hipGetDevice failed");
+    if (cur != plan->device && hipSetDevice(plan->device) != hipSuccess)
+        return fail(DISCO_ERR_DEVICE, "hipSetDevice failed");
+    struct Restore { int d; bool on; ~Restore() { if (on) (void)hipSetDevice(d); } } restore{cur, cur != plan->device};
+    // fp32 with the 3x3 basis: Z of all channels in one pass (sweep Z mode,
+    // spectral rings through a selection W); otherwise the op's own kernels
+    // once per input channel (items of B * C_x).
+    const bool onepass = x->dtype == DISCO_FLOAT32 && op.basis == DISCO_BASIS_BILINEAR_3X3;
+    ExecArgs za{};
+    za.op = &op; za.x = x->data; za.dtype = 0; za.B = (int)B; za.Ci = (int)C_x; za.Co = (int)C_x * K;
+    za.w_trans = transpose; za.stream = stream;
+    const size_t zbytes = ((size_t)(B * C_x) * K * (size_t)P * elem_bytes(x->dtype) + 255) & ~(size_t)255;
+    const size_t zws = onepass ? workspace_bytes_gather_z_all(za) : 0;
+    const size_t gbytes = weight_grad_ws_bytes((int)B, (int)C_dy, (int)(C_x * K), P);
+    void* zbuf = nullptr;
+    float* gws = nullptr;
+    hipError_t e = hipMallocAsync(&zbuf, zbytes + zws, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(gathered sums)");
+    e = hipMallocAsync((void**)&gws, gbytes, stream);
+    if (e != hipSuccess) {
+        (void)hipFreeAsync(zbuf, stream);
+        return hip_fail(e, "hipMallocAsync(weight gradient partials)");
+    }
+    zt.data = zbuf;
+    if (onepass) {
+        e = launch_gather_z_all(za, (float*)zbuf, (float*)((char*)zbuf + zbytes));
+        s = e == hipSuccess ? DISCO_OK : hip_fail(e, "kernel launch");
+    } else {
+        s = run_op(plan, op, transpose, &xz, &wsel, &zt, stream, DISCO_ALGO_AUTO);
+    }
+    if (s == DISCO_OK) {
+        e = launch_weight_grad(dy->data, zbuf, dw->data, gws, x->dtype, (int)B, (int)C_dy, (int)C_x, K, P,
+                               transpose, stream);
+        if (e != hipSuccess) s = hip_fail(e, "kernel launch");
+    }
+    (void)hipFreeAsync(gws, stream);
+    (void)hipFreeAsync(zbuf, stream);
+    return s == DISCO_OK ? ok() : s;
+}
+
 // ---- kernel timing (measurement tools only) --------------------------------
 struct TimedLaunch {
     std::string name;
@@ -614,11 +758,15 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
     PlanParams p{};
     disco_status_t s = resolve_params(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, basis, &p);
     if (s != DISCO_OK) return s;
-    HostOp hf, ht;
+    HostOp hf, ht, hfa, hta;
+    const bool with_backward = (p.flags & DISCO_PLAN_BACKWARD) != 0;
     std::string err;
     try {
         int rc = build_host_op(p, false, &hf, &err);
         if (rc == DISCO_OK) rc = build_host_op(p, true, &ht, &err);
+        // Adjoints: the other op's filter pairs, weighted at their output points.
+        if (rc == DISCO_OK && with_backward) rc = build_host_op(p, true, &hfa, &err, true);
+        if (rc == DISCO_OK && with_backward) rc = build_host_op(p, false, &hta, &err, true);
         if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
     } catch (const std::bad_alloc&) {
         return fail(DISCO_ERR_OUT_OF_MEMORY, "host allocation failed while building psi");
@@ -631,13 +779,34 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
         return fail(DISCO_ERR_DEVICE, "no HIP device available");
     }
     plan->params = p;
-    if ((s = upload_op(hf, &plan->fwd)) != DISCO_OK || (s = upload_op(ht, &plan->tr)) != DISCO_OK) {
+    s = upload_op(hf, &plan->fwd);
+    if (s == DISCO_OK) s = upload_op(ht, &plan->tr);
+    if (s == DISCO_OK && with_backward) s = upload_op(hfa, &plan->fwd_adj);
+    if (s == DISCO_OK && with_backward) s = upload_op(hta, &plan->tr_adj);
+    if (s == DISCO_OK && with_backward) {
+        const int K = basis_size(p.basis);
+        std::vector<float> id32((size_t)K * K, 0.0f);
+        std::vector<uint16_t> id16((size_t)K * K, 0);
+        for (int k = 0; k < K; ++k) {
+            id32[(size_t)k * K + k] = 1.0f;
+            id16[(size_t)k * K + k] = 0x3f80;  // 1.0 in bf16
+        }
+        int64_t dummy = 0;
+        s = upload_vec(id32, (float**)&plan->wsel32, &dummy, "hipMalloc(selection weights)");
+        if (s == DISCO_OK) s = upload_vec(id16, (uint16_t**)&plan->wsel16, &dummy, "hipMalloc(selection weights)");
+    }
+    if (s != DISCO_OK) {
         free_op(&plan->fwd);
         free_op(&plan->tr);
+        free_op(&plan->fwd_adj);
+        free_op(&plan->tr_adj);
+        if (plan->wsel32) (void)hipFree(plan->wsel32);
+        if (plan->wsel16) (void)hipFree(plan->wsel16);
         delete plan;
         return s;
     }
-    if (plan->fwd.spectral.n_rings > 0 || plan->tr.spectral.n_rings > 0) {
+    if (plan->fwd.spectral.n_rings > 0 || plan->tr.spectral.n_rings > 0 || plan->fwd_adj.spectral.n_rings > 0 ||
+        plan->tr_adj.spectral.n_rings > 0) {
         if (hipStreamCreateWithFlags(&plan->aux, hipStreamNonBlocking) != hipSuccess) plan->aux = nullptr;
     }
     // Keep freed workspace in the device's pool rather than returning it to
@@ -658,7 +827,7 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
     I.nnz_entries = (int64_t)hf.t_in.size();
     I.nnz_entries_transpose = (int64_t)ht.t_in.size();
     I.nnz_pairs_total = hf.nnz_pairs;
-    I.psi_bytes = plan->fwd.bytes + plan->tr.bytes;
+    I.psi_bytes = plan->fwd.bytes + plan->tr.bytes + plan->fwd_adj.bytes + plan->tr_adj.bytes;
     I.h = p.h;
     I.spectral_rings_forward = plan->fwd.spectral.n_rings;
     I.spectral_rings_transpose = plan->tr.spectral.n_rings;
@@ -679,6 +848,10 @@ disco_status_t disco_plan_destroy(disco_plan_t plan) {
     }
     free_op(&plan->fwd);
     free_op(&plan->tr);
+    free_op(&plan->fwd_adj);
+    free_op(&plan->tr_adj);
+    if (plan->wsel32) (void)hipFree(plan->wsel32);
+    if (plan->wsel16) (void)hipFree(plan->wsel16);
     if (cur != plan->device) (void)hipSetDevice(cur);
     delete plan;
     return ok();
@@ -766,6 +939,18 @@ disco_status_t disco_forward(disco_plan_t plan, const disco_tensor_t* x, const d
 disco_status_t disco_transpose(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
                                disco_tensor_t* y, hipStream_t stream) {
     return run(plan, x, w, y, stream, DISCO_ALGO_AUTO, true);
+}
+
+disco_status_t disco_forward_backward(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                                      const disco_tensor_t* dy, disco_tensor_t* dx, disco_tensor_t* dw,
+                                      hipStream_t stream) {
+    return backward(plan, false, x, w, dy, dx, dw, stream);
+}
+
+disco_status_t disco_transpose_backward(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                                        const disco_tensor_t* dy, disco_tensor_t* dx, disco_tensor_t* dw,
+                                        hipStream_t stream) {
+    return backward(plan, true, x, w, dy, dx, dw, stream);
 }
 
 disco_status_t disco_forward_algo(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,

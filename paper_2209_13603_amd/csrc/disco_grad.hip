@@ -1,0 +1,166 @@
+// disco_grad.hip -- the weight gradient's reduction over pixels (App. C).
+//
+// With the gathered sums Zs[b][(c_x, k)][p] of an op (computed by the op's
+// own kernels with a selection W) and the upstream gradient dy[b][m][p],
+//   G[m][n] = sum_b sum_p dy[b][m][p] Zs[b][n][p],   n = c_x K + k,
+// is a product of two short, very wide matrices.  k_weight_grad gives each
+// workgroup one batch item, one range of pixels and an 8 x 16 tile of G: every
+// lane accumulates the tile over its pixels (24 coalesced loads and 128 FMAs
+// per pixel), the lanes' tiles are summed across the wave with lane shuffles
+// and across the four waves in LDS, and the workgroup writes its partial tile.
+// k_weight_grad_reduce sums the partials of each element over (batch item,
+// pixel range) in a fixed order, so the result is deterministic, and writes
+// dW in the op's layout.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+
+#include "disco_internal.h"
+
+namespace disco {
+
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kTileM = 8;   // rows of dy per workgroup
+constexpr int kTileN = 16;  // rows of Zs per workgroup (dy is read N / kTileN times)
+
+__device__ __forceinline__ float load_val(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float load_val(const uint16_t* p, int64_t i) {
+    return __uint_as_float((uint32_t)p[i] << 16);
+}
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ void store_val(float* p, int64_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void store_val(uint16_t* p, int64_t i, float v) { p[i] = to_bf16(v); }
+
+// grid: (n_chunks, n_mt * n_nt, B).  partial: [B][n_chunks][M][N].
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_weight_grad(const T* __restrict__ dy, const T* __restrict__ zs,
+                                                        float* __restrict__ partial, int M, int N, int64_t P,
+                                                        int64_t chunk_len, int n_nt) {
+    __shared__ float red[kBlock / 64][kTileM * kTileN];
+    const int tid = threadIdx.x;
+    const int chunk = blockIdx.x;
+    const int m0 = (blockIdx.y / n_nt) * kTileM, n0 = (blockIdx.y % n_nt) * kTileN;
+    const int b = blockIdx.z;
+    const int64_t p0 = (int64_t)chunk * chunk_len;
+    const int64_t p1 = p0 + chunk_len < P ? p0 + chunk_len : P;
+    float acc[kTileM][kTileN];
+#pragma unroll
+    for (int i = 0; i < kTileM; ++i)
+#pragma unroll
+        for (int j = 0; j < kTileN; ++j) acc[i][j] = 0.0f;
+    const T* dyb = dy + (int64_t)b * M * P;
+    const T* zb = zs + (int64_t)b * N * P;
+    for (int64_t p = p0 + tid; p < p1; p += kBlock) {
+        float a[kTileM], z[kTileN];
+#pragma unroll
+        for (int i = 0; i < kTileM; ++i) a[i] = m0 + i < M ? load_val(dyb, (int64_t)(m0 + i) * P + p) : 0.0f;
+#pragma unroll
+        for (int j = 0; j < kTileN; ++j) z[j] = n0 + j < N ? load_val(zb, (int64_t)(n0 + j) * P + p) : 0.0f;
+#pragma unroll
+        for (int i = 0; i < kTileM; ++i)
+#pragma unroll
+            for (int j = 0; j < kTileN; ++j) acc[i][j] = fmaf(a[i], z[j], acc[i][j]);
+    }
+    // Sum over the 64 lanes of each wave, then over the waves.
+    const int lane = tid & 63, wave = tid >> 6;
+#pragma unroll
+    for (int i = 0; i < kTileM; ++i)
+#pragma unroll
+        for (int j = 0; j < kTileN; ++j) {
+            float v = acc[i][j];
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+            if (lane == 0) red[wave][i * kTileN + j] = v;
+        }
+    __syncthreads();
+    if (tid < kTileM * kTileN) {
+        const int i = tid / kTileN, j = tid % kTileN;
+        float v = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kBlock / 64; ++w) v += red[w][tid];
+        if (m0 + i < M && n0 + j < N)
+            partial[(((int64_t)b * gridDim.x + chunk) * M + m0 + i) * N + n0 + j] = v;
+    }
+}
+
+// One workgroup per dW element e = (m, n): lane t sums the partials
+// t, t + 256, ... of e over (b, chunk), then a fixed tree over the lanes.
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_weight_grad_reduce(const float* __restrict__ partial, T* __restrict__ dw,
+                                                               int B, int n_chunks, int M, int C_x, int K,
+                                                               bool transposed_layout) {
+    __shared__ float red[kBlock];
+    const int N = C_x * K;
+    const int e = blockIdx.x;
+    const int tid = threadIdx.x;
+    float v = 0.0f;
+    for (int s = tid; s < B * n_chunks; s += kBlock) v += partial[(int64_t)s * M * N + e];
+    red[tid] = v;
+    __syncthreads();
+    for (int half = kBlock / 2; half > 0; half >>= 1) {
+        if (tid < half) red[tid] += red[tid + half];
+        __syncthreads();
+    }
+    if (tid == 0) {
+        const int m = e / N, n = e - (e / N) * N;
+        const int cx = n / K, k = n - (n / K) * K;
+        const int64_t at = transposed_layout ? ((int64_t)cx * M + m) * K + k : ((int64_t)m * C_x + cx) * K + k;
+        store_val(dw, at, red[0]);
+    }
+}
+
+int64_t chunk_len_for(int B, int M, int N, int64_t P) {
+    const int tiles = ((M + kTileM - 1) / kTileM) * ((N + kTileN - 1) / kTileN) * B;
+    const int64_t want = std::max<int64_t>(1, 2048 / std::max(1, tiles));  // chunks per tile
+    int64_t len = (P + want - 1) / want;
+    len = std::max<int64_t>(len, 16 * kBlock);
+    return (len + kBlock - 1) / kBlock * kBlock;
+}
+
+template <typename T>
+hipError_t weight_grad(const T* dy, const T* zs, T* dw, float* ws, int B, int M, int C_x, int K, int64_t P,
+                       bool transposed_layout, hipStream_t s) {
+    const int N = C_x * K;
+    const int64_t len = chunk_len_for(B, M, N, P);
+    const int n_chunks = (int)std::max<int64_t>(1, (P + len - 1) / len);
+    const int n_mt = (M + kTileM - 1) / kTileM, n_nt = (N + kTileN - 1) / kTileN;
+    dim3 grid((unsigned)n_chunks, (unsigned)(n_mt * n_nt), (unsigned)B);
+    int tk = timing_begin("weight_grad", s);
+    hipLaunchKernelGGL((k_weight_grad<T>), grid, dim3(kBlock), 0, s, dy, zs, ws, M, N, P, len, n_nt);
+    timing_end(tk, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int ne = M * N;
+    tk = timing_begin("weight_grad_reduce", s);
+    hipLaunchKernelGGL((k_weight_grad_reduce<T>), dim3((unsigned)ne), dim3(kBlock), 0, s, ws, dw, B, n_chunks, M, C_x,
+                       K, transposed_layout);
+    timing_end(tk, s);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t weight_grad_ws_bytes(int B, int M, int N, int64_t P) {
+    const int64_t len = chunk_len_for(B, M, N, P);
+    const int64_t n_chunks = std::max<int64_t>(1, (P + len - 1) / len);
+    return sizeof(float) * (size_t)B * (size_t)n_chunks * (size_t)M * (size_t)N;
+}
+
+hipError_t launch_weight_grad(const void* dy, const void* zs, void* dw, float* ws, int dtype, int B, int M,
+                              int C_x, int K, int64_t P, bool transposed_layout, hipStream_t s) {
+    if (dtype == 1)
+        return weight_grad<uint16_t>((const uint16_t*)dy, (const uint16_t*)zs, (uint16_t*)dw, ws, B, M, C_x, K, P,
+                                     transposed_layout, s);
+    return weight_grad<float>((const float*)dy, (const float*)zs, (float*)dw, ws, B, M, C_x, K, P, transposed_layout,
+                              s);
+}
+
+}  // namespace disco

@@ -23,6 +23,7 @@ struct PlanParams {
     int quadrature;  // DISCO_QUAD_*
     int basis;       // DISCO_BASIS_*
     int sampling;    // DISCO_SAMPLING_*
+    int flags;       // DISCO_PLAN_*
 };
 
 // Basis size K of a DISCO_BASIS_* kind.
@@ -68,7 +69,10 @@ Work pattern_work(const HostOp& op, const std::vector<uint8_t>& include);
 
 // Returns 0 on success, otherwise a disco_status_t with *err set.
 int make_op_geom(const PlanParams& p, bool transpose, OpGeom* g, std::string* err);
-int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* err);
+// quad_at_output: weight each value with the quadrature of the op's output
+// ring instead of its input ring (the adjoint of the other op, App. C).
+int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* err,
+                  bool quad_at_output = false);
 
 // ---------------------------------------------------------------------------
 // Packed layout for the LDS-staged fused kernel (disco_fused.hip).
@@ -311,6 +315,12 @@ hipError_t launch_gather_then_contract(const ExecArgs& a, float* z_ws);
 hipError_t launch_sweep_z(const ExecArgs& a, float* z);   // disco_sweep.hip
 bool gather_z_split(const ExecArgs& a);                   // sweep + spectral Z schedule usable
 hipError_t launch_contract_then_gather(const ExecArgs& a, float* xc_ws);
+// Gathered sums Z[b][ci][k][pixel] (fp32 storage, 3x3 basis) of every output
+// ring into z (B * Ci * 9 * pixels floats): the sweep's Z mode, k_gather_z
+// for the other light rings, the spectral kernels with a selection W for the
+// heavy ones.  ws: workspace_bytes_gather_z_all bytes.
+size_t workspace_bytes_gather_z_all(const ExecArgs& a);
+hipError_t launch_gather_z_all(const ExecArgs& a, float* z, float* ws);
 size_t workspace_bytes_gather_then_contract(const ExecArgs& a);
 size_t workspace_bytes_contract_then_gather(const ExecArgs& a);
 hipError_t launch_fused(const ExecArgs& a, const PackedDev& P, float* partial_ws);
@@ -330,5 +340,14 @@ hipError_t launch_stencil(const ExecArgs& a, const PackedDev& P, float* partial_
 // The blocked kernel (one output channel, longitude stride 1); workspace
 // sizeof(float) * n_slots * B * nq.
 hipError_t launch_stencil_blocked(const ExecArgs& a, const StencilDev& S, float* partial_ws);
+
+// Weight gradient reduction (disco_grad.hip): G[m][n] = sum_{b,p} A[b][m][p]
+// Zs[b][n][p] over P pixels, A = dy [B][M][P] and Zs = the gathered sums
+// [B][N][P] (N = C_x * K, rows (c_x, k)), written as dW[m][c_x][k] (forward
+// layout) or dW[c_x][m][k] (transposed op's layout).  dtype 0 fp32, 1 bf16
+// (inputs and dW); partials in ws (weight_grad_ws_bytes).
+size_t weight_grad_ws_bytes(int B, int M, int N, int64_t P);
+hipError_t launch_weight_grad(const void* dy, const void* zs, void* dw, float* ws, int dtype, int B, int M,
+                              int C_x, int K, int64_t P, bool transposed_layout, hipStream_t s);
 
 }  // namespace disco

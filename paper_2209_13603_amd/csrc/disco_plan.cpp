@@ -159,7 +159,7 @@ int make_op_geom(const PlanParams& p, bool transpose, OpGeom* g, std::string* er
     return DISCO_OK;
 }
 
-int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* err) {
+int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* err, bool quad_at_output) {
     OpGeom g;
     int rc = make_op_geom(p, transpose, &g, err);
     if (rc) return rc;
@@ -169,6 +169,9 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
     // Quadrature of the op's input grid: the forward op sums over plan
     // in-grid points; the transposed op over plan out-grid points, its centres.
     const std::vector<double> q = ring_weights(g.nlat_i, g.nlon_i, p.quadrature, p.sampling);
+    // The adjoint ops weight by their output ring instead (App. C).
+    const std::vector<double> q_o =
+        quad_at_output ? ring_weights(g.nlat_o, g.nlon_o, p.quadrature, p.sampling) : std::vector<double>();
     const double h = p.h;
     // Basis support radius: the 3x3 hats vanish for max(|u|, |v|) >= 2h, the
     // axisymmetric ones for Theta >= 4h.
@@ -186,6 +189,7 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
     for (int to = 0; to < g.nlat_o; ++to) {
         for (int r = 0; r < g.P; ++r) {
             for (int ti = 0; ti < g.nlat_i; ++ti) {
+                const double qw = quad_at_output ? q_o[to] : q[ti];
                 // Colatitude difference (input - output) from integers.
                 const double dth_io = colat_diff(ti, g.nlat_i, to, g.nlat_o, p.sampling);
                 if (std::fabs(dth_io) > radius * (1.0 + 1e-12)) continue;
@@ -240,7 +244,7 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
                         for (int k = 0; k < kBasis; ++k) {
                             double psi = k < kAxisymBasis ? hat(Th / h - k) : 0.0;
                             if (psi < kPsiFloor) psi = 0.0;
-                            vals64[k] = psi * q[ti];
+                            vals64[k] = psi * qw;
                             vals[k] = (float)vals64[k];
                             if (psi != 0.0) { any = true; ++nzk; }
                         }
@@ -267,7 +271,7 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
                             // two node spacings away) comes out as rounding noise of
                             // the fp64 geometry (~1e-16); such values are exact zeros.
                             if (psi < kPsiFloor) psi = 0.0;
-                            vals64[3 * a + b] = psi * q[ti];
+                            vals64[3 * a + b] = psi * qw;
                             vals[3 * a + b] = (float)vals64[3 * a + b];
                             if (psi != 0.0) { any = true; ++nzk; }
                         }

@@ -34,6 +34,7 @@ DISCO_SAMPLING_CELL_CENTRED = 0
 DISCO_SAMPLING_POLES = 1
 BASES = {"bilinear3x3": DISCO_BASIS_BILINEAR_3X3, "axisym4": DISCO_BASIS_AXISYMMETRIC_4}
 SAMPLINGS = {"cell_centred": DISCO_SAMPLING_CELL_CENTRED, "poles": DISCO_SAMPLING_POLES}
+DISCO_PLAN_BACKWARD = 1
 
 ALGO_AUTO = 0
 ALGO_GATHER_THEN_CONTRACT = 1
@@ -46,7 +47,8 @@ ALGOS = {"auto": ALGO_AUTO, "gather_then_contract": ALGO_GATHER_THEN_CONTRACT,
 
 # Every exported symbol declared in include/disco.h.
 EXPORTS = ("disco_plan_create", "disco_plan_destroy", "disco_plan_query", "disco_forward",
-           "disco_transpose", "disco_forward_algo", "disco_transpose_algo", "disco_psi_entries",
+           "disco_transpose", "disco_forward_algo", "disco_transpose_algo", "disco_forward_backward",
+           "disco_transpose_backward", "disco_psi_entries",
            "disco_kernel_timing_enable", "disco_kernel_timing_read", "disco_kernel_work",
            "disco_status_string", "disco_last_error")
 
@@ -61,7 +63,7 @@ class DiscoError(RuntimeError):
 class Basis(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("quadrature", ctypes.c_int32),
                 ("node_spacing", ctypes.c_double), ("sampling", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("flags", ctypes.c_int32)]
 
 
 class Tensor(ctypes.Structure):
@@ -115,6 +117,10 @@ def library(path: str = LIB_PATH) -> ctypes.CDLL:
     for name in ("disco_forward_algo", "disco_transpose_algo"):
         getattr(lib, name).argtypes = [ctypes.c_void_p, P(Tensor), P(Tensor), P(Tensor),
                                        ctypes.c_void_p, ctypes.c_int32]
+    for name in ("disco_forward_backward", "disco_transpose_backward"):
+        getattr(lib, name).argtypes = [ctypes.c_void_p, P(Tensor), P(Tensor), P(Tensor), P(Tensor),
+                                       P(Tensor), ctypes.c_void_p]
+        getattr(lib, name).restype = ctypes.c_int
     lib.disco_psi_entries.argtypes = ([ctypes.c_int] * 4 + [ctypes.c_double, P(Basis), ctypes.c_int32,
                                       ctypes.c_int64] + [P(ctypes.c_int32)] * 4
                                       + [P(ctypes.c_float), P(ctypes.c_int64), P(ctypes.c_int32),
@@ -148,10 +154,10 @@ def _check(status: int):
 
 
 def _basis(node_spacing=0.0, quadrature=DISCO_QUAD_FEJER1, kind=DISCO_BASIS_BILINEAR_3X3,
-           sampling=DISCO_SAMPLING_CELL_CENTRED):
+           sampling=DISCO_SAMPLING_CELL_CENTRED, flags=0):
     kind = BASES[kind] if isinstance(kind, str) else int(kind)
     sampling = SAMPLINGS[sampling] if isinstance(sampling, str) else int(sampling)
-    return Basis(kind, quadrature, float(node_spacing), sampling, 0)
+    return Basis(kind, quadrature, float(node_spacing), sampling, int(flags))
 
 
 def _tensor(t) -> Tensor:
@@ -180,10 +186,10 @@ class Plan:
 
     def __init__(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, node_spacing=0.0,
                  quadrature=DISCO_QUAD_FEJER1, basis=DISCO_BASIS_BILINEAR_3X3,
-                 sampling=DISCO_SAMPLING_CELL_CENTRED):
+                 sampling=DISCO_SAMPLING_CELL_CENTRED, backward=False):
         lib = library()
         h = ctypes.c_void_p()
-        b = _basis(node_spacing, quadrature, basis, sampling)
+        b = _basis(node_spacing, quadrature, basis, sampling, DISCO_PLAN_BACKWARD if backward else 0)
         _check(lib.disco_plan_create(nlat_in, nlon_in, nlat_out, nlon_out, float(theta_c),
                                      ctypes.byref(b), ctypes.byref(h)))
         self._h = h
@@ -254,6 +260,39 @@ class Plan:
             y = torch.empty((x.shape[0], w.shape[1]) + self.grid_in, dtype=x.dtype,
                             device=x.device)
         return self._run("disco_transpose_algo", x, w, y, algo, stream)
+
+
+def _backward(plan, fn, x, w, dy, dx, dw, stream):
+    tx = _tensor(x) if x is not None else None
+    tw = _tensor(w) if w is not None else None
+    tdy = _tensor(dy)
+    tdx = _tensor(dx) if dx is not None else None
+    tdw = _tensor(dw) if dw is not None else None
+    ref = lambda t: ctypes.byref(t) if t is not None else None
+    _check(getattr(library(), fn)(plan._h, ref(tx), ref(tw), ref(tdy), ref(tdx), ref(tdw), _stream(stream)))
+    return dx, dw
+
+
+def forward_backward(plan, x, w, dy, want_dx=True, want_dw=True, stream=None):
+    """Gradients of the forward op (``disco_forward_backward``): returns (dx, dw),
+    None for the ones not asked for."""
+    import torch
+    dx = torch.empty((dy.shape[0], w.shape[1]) + plan.grid_in, dtype=dy.dtype, device=dy.device) \
+        if want_dx else None
+    dw = torch.empty_like(w) if want_dw else None
+    return _backward(plan, "disco_forward_backward", x if want_dw else None, w if want_dx else None,
+                     dy, dx, dw, stream)
+
+
+def transpose_backward(plan, x, w, dy, want_dx=True, want_dw=True, stream=None):
+    """Gradients of the transposed op (``disco_transpose_backward``): x[B, CinT,
+    out-grid], w[CinT, CoutT, K], dy[B, CoutT, in-grid] -> (dx, dw)."""
+    import torch
+    dx = torch.empty((dy.shape[0], w.shape[0]) + plan.grid_out, dtype=dy.dtype, device=dy.device) \
+        if want_dx else None
+    dw = torch.empty_like(w) if want_dw else None
+    return _backward(plan, "disco_transpose_backward", x if want_dw else None, w if want_dx else None,
+                     dy, dx, dw, stream)
 
 
 def kernel_timing(on: bool):

@@ -189,14 +189,14 @@ def test_plan_entries_axisym_cell_centred_match_dense_psi(case, transpose):
 
 def test_pole_grid_validation():
     B = disco.Basis
-    # nlon must be 2 (nlat - 1); cell areas are not offered there; reserved must be 0.
+    # nlon must be 2 (nlat - 1); cell areas are not offered there; unknown flag bits.
     rc, _ = _create(9, 18, 9, 18, 0.3, basis=B(1, 0, 0.0, 1, 0))
     assert rc == disco.DISCO_ERR_INVALID_ARGUMENT
     rc, _ = _create(9, 16, 9, 16, 0.3, basis=B(1, 1, 0.0, 1, 0))
     assert rc == disco.DISCO_ERR_UNSUPPORTED
     rc, _ = _create(9, 16, 9, 16, 0.3, basis=B(1, 0, 0.0, 2, 0))
     assert rc == disco.DISCO_ERR_UNSUPPORTED
-    rc, _ = _create(9, 16, 9, 16, 0.3, basis=B(1, 0, 0.0, 1, 3))
+    rc, _ = _create(9, 16, 9, 16, 0.3, basis=B(1, 0, 0.0, 1, 6))
     assert rc == disco.DISCO_ERR_INVALID_ARGUMENT
 
 

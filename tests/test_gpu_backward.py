@@ -1,0 +1,160 @@
+"""GPU parity of the gradients (App. C) through the C ABI against the fp64
+oracle: the input gradient (the adjoint op) and the weight gradient of the
+forward and the transposed op.
+
+Tolerances as the forward parity tests: relative L2 <= 1e-5 for fp32
+storage, <= 2e-2 for bf16.  Small grids are compared in full; on the
+2048 x 4096 sphere the input gradient is compared on sampled pixels, and the
+weight gradient exactly with an upstream gradient that is zero outside a
+sample of output pixels (the oracle then needs the gathered sums at those
+pixels only).
+"""
+import math
+
+import numpy as np
+import pytest
+
+from gpu_util import rel_l2, sample_pixels, say, to_numpy, torch_dev
+import oracle
+from paper_2209_13603_amd import disco, synth
+
+pytestmark = pytest.mark.gpu
+
+FP32_TOL = 1e-5
+BF16_TOL = 2e-2
+
+CASES = [
+    # (nlat_in, nlon_in, nlat_out, nlon_out, sampling, basis)
+    (16, 32, 8, 16, "cell_centred", "bilinear3x3"),
+    (8, 16, 16, 32, "cell_centred", "bilinear3x3"),
+    (33, 300, 33, 300, "cell_centred", "bilinear3x3"),
+    (64, 128, 64, 128, "cell_centred", "bilinear3x3"),
+    (17, 32, 9, 16, "poles", "bilinear3x3"),
+    (41, 80, 41, 80, "poles", "axisym4"),
+    (17, 32, 9, 16, "poles", "axisym4"),
+]
+
+
+def _codes(smp, bas):
+    return {"sampling": 1 if smp == "poles" else 0, "basis": 1 if bas == "axisym4" else 0}
+
+
+def _tc(a, c, smp):
+    return 3 * math.pi / (min(a, c) - (1 if smp == "poles" else 0))
+
+
+def _run(case, transpose, chans, dtype, seed):
+    a, b, c, d, smp, bas = case
+    tc = _tc(a, c, smp)
+    K = 4 if bas == "axisym4" else 9
+    C1, C2 = chans
+    # forward: x[B, C1, in], w[C2, C1, K], dy[B, C2, out]
+    # transpose: x[B, C1, out], w[C1, C2, K], dy[B, C2, in]
+    xs = (2, C1, c, d) if transpose else (2, C1, a, b)
+    ys = (2, C2, a, b) if transpose else (2, C2, c, d)
+    ws = (C1, C2, K) if transpose else (C2, C1, K)
+    r = np.random.default_rng(seed)
+    x = synth.to_storage(r.standard_normal(xs), dtype)
+    w = synth.to_storage(r.standard_normal(ws) / math.sqrt(C1 * K), dtype)
+    dy = synth.to_storage(r.standard_normal(ys), dtype)
+    say("backward", case, "transpose" if transpose else "forward", chans, dtype)
+    plan = disco.Plan(a, b, c, d, tc, basis=bas, sampling=smp, backward=True)
+    fn = disco.transpose_backward if transpose else disco.forward_backward
+    dx, dw = fn(plan, torch_dev(x, dtype), torch_dev(w, dtype), torch_dev(dy, dtype))
+    import torch
+    torch.cuda.synchronize()
+    o = oracle.default()
+    kw = _codes(smp, bas)
+    ref_dx = o.input_grad(a, b, c, d, tc, dy.astype(np.float64), w.astype(np.float64), transpose=transpose, **kw)
+    ref_dw = o.weight_grad(a, b, c, d, tc, x.astype(np.float64), dy.astype(np.float64), transpose=transpose, **kw)
+    plan.close()
+    return to_numpy(dx), to_numpy(dw), ref_dx, ref_dw
+
+
+@pytest.mark.parametrize("transpose", [False, True], ids=["forward", "transpose"])
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "%dx%d_%dx%d_%s_%s" % c)
+def test_gradients_small_grids(case, transpose):
+    dx, dw, rdx, rdw = _run(case, transpose, (3, 5), "fp32", 60)
+    ex, ew = rel_l2(dx, rdx), rel_l2(dw, rdw)
+    say("  dx rel_l2 %.3e  dw rel_l2 %.3e" % (ex, ew))
+    assert ex <= FP32_TOL and ew <= FP32_TOL
+    assert np.abs(dx - rdx).max() <= 1e-5 * np.abs(rdx).max()
+
+
+@pytest.mark.parametrize("chans", [(1, 1), (8, 8), (12, 20)], ids=lambda c: "%dto%d" % c)
+def test_gradients_channel_shapes(chans):
+    for transpose in (False, True):
+        dx, dw, rdx, rdw = _run(CASES[0], transpose, chans, "fp32", 61)
+        ex, ew = rel_l2(dx, rdx), rel_l2(dw, rdw)
+        say("  %s dx %.3e dw %.3e" % (chans, ex, ew))
+        assert ex <= FP32_TOL and ew <= FP32_TOL
+
+
+@pytest.mark.parametrize("transpose", [False, True], ids=["forward", "transpose"])
+def test_gradients_bf16(transpose):
+    dx, dw, rdx, rdw = _run(CASES[0], transpose, (3, 5), "bf16", 62)
+    ex, ew = rel_l2(dx, rdx), rel_l2(dw, rdw)
+    say("  bf16 dx %.3e dw %.3e" % (ex, ew))
+    assert ex <= BF16_TOL and ew <= BF16_TOL
+
+
+def test_backward_needs_the_plan_flag():
+    plan = disco.Plan(16, 32, 8, 16, 3 * math.pi / 8)
+    x, w = synth.random_inputs(63, (1, 2, 16, 32), (3, 2, 9))
+    dy = np.zeros((1, 3, 8, 16), np.float32)
+    with pytest.raises(disco.DiscoError) as ei:
+        disco.forward_backward(plan, torch_dev(x), torch_dev(w), torch_dev(dy))
+    assert ei.value.status == disco.DISCO_ERR_UNSUPPORTED
+    plan.close()
+    plan = disco.Plan(16, 32, 8, 16, 3 * math.pi / 8, backward=True)
+    import torch
+    bad_dw = torch.empty((3, 2, 4), device="cuda:0")
+    dx = torch.empty((1, 2, 16, 32), device="cuda:0")
+    with pytest.raises(disco.DiscoError) as ei:
+        disco._backward(plan, "disco_forward_backward", torch_dev(x), torch_dev(w), torch_dev(dy), dx, bad_dw,
+                        None)
+    assert ei.value.status == disco.DISCO_ERR_SHAPE
+    plan.close()
+
+
+@pytest.mark.parametrize("transpose", [False, True], ids=["forward", "transpose"])
+def test_gradients_sphere2048x4096(transpose):
+    """The 2048 x 4096 sphere, 8 -> 8 channels: dx on sampled pixels; dW with
+    dy supported on a sample of output pixels, against the oracle's gathered
+    sums at exactly those pixels."""
+    import torch
+    wl = synth.WORKLOADS["sphere2048x4096"]
+    n, m = wl.nlat_in, wl.nlon_in
+    tc = wl.theta_c
+    r = np.random.default_rng(64)
+    x = r.standard_normal((1, 8, n, m)).astype(np.float32)
+    w = (r.standard_normal((8, 8, 9)) / math.sqrt(72)).astype(np.float32)
+    pix = sample_pixels(n, m, 3, seed=7)
+    dy = np.zeros((1, 8, n * m), np.float32)
+    dy[:, :, pix] = r.standard_normal((1, 8, pix.size))
+    dy = dy.reshape(1, 8, n, m)
+    say("backward 2048x4096", "transpose" if transpose else "forward")
+    plan = disco.Plan(n, m, n, m, tc, backward=True)
+    fn = disco.transpose_backward if transpose else disco.forward_backward
+    dx, dw = fn(plan, torch_dev(x), torch_dev(w), torch_dev(dy))
+    torch.cuda.synchronize()
+    dx, dw = to_numpy(dx), to_numpy(dw)
+    o = oracle.default()
+    # dx at sampled pixels: the adjoint sums over the whole dy.
+    qpix = sample_pixels(n, m, 2, seed=8)
+    rdx = o.input_grad(n, m, n, m, tc, dy.astype(np.float64), w.astype(np.float64), transpose=transpose, pix=qpix)
+    ex = rel_l2(dx.reshape(1, 8, -1)[:, :, qpix], rdx)
+    # dW: Z of every input channel at the sampled pixels (selection W per channel).
+    sel = np.zeros((9, 1, 9))
+    for k in range(9):
+        sel[k, 0, k] = 1.0
+    xs = x.astype(np.float64).reshape(8, 1, n, m)
+    fn_o = o.transpose if transpose else o.forward
+    Z = fn_o(n, m, n, m, tc, xs, sel.transpose(1, 0, 2).copy() if transpose else sel, pix=pix)  # [8, 9, npix]
+    dyp = dy.reshape(8, -1)[:, pix].astype(np.float64)                                              # [8, npix]
+    G = np.einsum("mp,ckp->mck", dyp, Z)                                                            # [dy ch, x ch, k]
+    rdw = G.transpose(1, 0, 2) if transpose else G
+    ew = rel_l2(dw, rdw)
+    say("  dx rel_l2 %.3e over %d pixels, dw rel_l2 %.3e over %d pixels" % (ex, qpix.size, ew, pix.size))
+    assert ex <= FP32_TOL and ew <= FP32_TOL
+    plan.close()
