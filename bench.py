@@ -254,6 +254,92 @@ def kernel_report(plan, kt, wl, transpose, algo, es):
     return per_kernel, roof
 
 
+def _timed(torch, fn, steps):
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(steps):
+        fn()
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / steps
+
+
+def _events(torch, disco, fn, steps):
+    disco.kernel_timing(True)
+    disco.kernel_timing_read()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    kt = disco.kernel_timing_read()
+    disco.kernel_timing(False)
+    return kt
+
+
+def bench_backward(args, wl, plan, x, w, es, torch, disco):
+    """Gradient step of the workload's op (App. C): dx through the adjoint op
+    and dW from the gathered sums.  value = output pix x chan of the op per
+    second of one gradient step (dx and dW).  Kernel figures from two passes
+    with kernel events, dx alone and dW alone (their kernels share names)."""
+    from types import SimpleNamespace
+    transpose = wl.op != "forward"
+    fb = disco.transpose_backward if transpose else disco.forward_backward
+    dy = torch.randn(wl.y_shape, device=x.device).to(x.dtype)
+    both = lambda: fb(plan, x, w, dy)
+    for _ in range(args.warmup):
+        both()
+    ms = _timed(torch, both, args.steps)
+    kt_dx = _events(torch, disco, lambda: fb(plan, x, w, dy, want_dw=False), args.steps)
+    kt_dw = _events(torch, disco, lambda: fb(plan, x, w, dy, want_dx=False), args.steps)
+    log("backward step %.4f ms; dx kernels %s; dW kernels %s" % (ms, kt_dx, kt_dw))
+    B, Ci, Co, K = wl.batch, wl.c_in, wl.c_out, wl.K
+    P = wl.y_shape[2] * wl.y_shape[3]
+    kernels, cands = {}, []
+
+    def add(tag, kt, work, model_wl):
+        for k, (launches, tot_ms) in kt.items():
+            avg = tot_ms / launches
+            if k == "weight_grad":
+                b_ = B * Ci * K * P * (4 if (wl.dtype == "fp32" and wl.basis == "bilinear3x3") else es) + B * Co * P * es
+                f_, bd = 2.0 * B * Co * Ci * K * P, "hbm"
+            elif k == "weight_grad_reduce":
+                b_, f_, bd = 0, 0.0, "hbm"
+            else:
+                if k not in work:
+                    raise SystemExit("no work figures for kernel %s" % k)
+                b_, f_, bd = kernel_model(k, model_wl, work[k], es)
+            row = {"launches": launches, "avg_us": round(avg * 1e3, 2), "alg_bytes": int(b_), "alg_flops": f_,
+                   "bound": bd, "alg_gbs": round(b_ / (avg / 1e3) / 1e9, 1),
+                   "alg_tflops": round(f_ / (avg / 1e3) / 1e12, 2)}
+            if bd == "hbm":
+                row["hbm_frac"] = round(b_ / (avg / 1e3) / 1e9 / HBM_PEAK_GBS, 4)
+            kernels["%s:%s" % (tag, k)] = row
+            if not k.startswith("spectral_") and k != "weight_grad_reduce":
+                cands.append(("%s:%s" % (tag, k), tot_ms, b_, f_, bd, avg))
+
+    # dx: the adjoint op has the other op's filter pairs (its work figures).
+    work_dx = plan.kernel_work(not transpose, "auto", Co, Ci, wl.dtype)
+    add("dx", kt_dx, work_dx, SimpleNamespace(batch=B, c_in=Co, c_out=Ci))
+    # dW: one-pass gathered sums (fp32, 3x3 basis) or the op's kernels per channel.
+    if wl.dtype == "fp32" and wl.basis == "bilinear3x3":
+        work_dw = plan.kernel_work(transpose, "gather_then_contract", Ci, Ci * K, wl.dtype)
+        mwl = SimpleNamespace(batch=B, c_in=Ci, c_out=Ci * K)
+    else:
+        work_dw = plan.kernel_work(transpose, "auto", 1, K, wl.dtype)
+        mwl = SimpleNamespace(batch=B * Ci, c_in=1, c_out=K)
+    add("dw", kt_dw, work_dw, mwl)
+    name, tot, b_, f_, bd, avg = max(cands, key=lambda c: c[1])
+    if bd == "hbm":
+        achieved, peak, unit = b_ / (avg / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved, peak, unit = f_ / (avg / 1e3) / 1e12, FP32_VALU_PEAK_TFLOPS, "TFLOP/s"
+    roof = {"bound": bd, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": load_traffic(name.split(":")[1], wl.name + "_backward"),
+            "kernel": name, "kernel_avg_us": round(avg * 1e3, 2), "algorithmic_bytes": int(b_),
+            "algorithmic_flops": f_}
+    return ms, kernels, roof
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -274,6 +360,8 @@ def main(argv=None):
                     help="library kernel name for --traffic-summary")
     ap.add_argument("--command", action="append", default=[],
                     help="the command that produced each counter run (recorded verbatim)")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the op's gradient step (input and weight gradients) instead")
     ap.add_argument("--no-hbm-schedule", action="store_true",
                     help="skip the extra pass over the gather-then-contract schedule (whose "
                          "kernels are HBM-bound) that the JSON line reports as hbm_schedule")
@@ -309,10 +397,26 @@ def main(argv=None):
     w = torch.from_numpy(w_np).to(dev).to(tdt)
     y = torch.empty(wl.y_shape, dtype=tdt, device=dev)
     t0 = time.time()
-    plan = disco.Plan(*wl.plan_args(), **wl.plan_kwargs())
+    plan = disco.Plan(*wl.plan_args(), **wl.plan_kwargs(), backward=args.backward)
     plan_s = time.time() - t0
     info = plan.info()
     log("plan built in %.2fs: %s" % (plan_s, info))
+    if args.backward:
+        ms, kernels, roof = bench_backward(args, wl, plan, x, w, es, torch, disco)
+        out = {
+            "metric": "DISCO %s gradient (dx and dW) output pix*chan/s on %s" % (wl.op, wl.name),
+            "value": wl.out_pix_chan / (ms / 1e3), "unit": UNIT, "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "f32" if wl.dtype == "fp32" else "bf16", "data": "synthetic",
+            "config": {"workload": wl.name, "op": wl.op + "_backward", "nlat_in": wl.nlat_in,
+                       "nlon_in": wl.nlon_in, "nlat_out": wl.nlat_out, "nlon_out": wl.nlon_out,
+                       "theta_c": wl.theta_c, "batch": wl.batch, "c_in": wl.c_in, "c_out": wl.c_out,
+                       "basis": wl.basis, "sampling": wl.sampling, "storage": wl.dtype},
+            "kernels": kernels, "roofline": roof, "plan_seconds": round(plan_s, 3), "cpu_baseline": None,
+        }
+        plan.close()
+        print(json.dumps(out), flush=True)
+        return 0
     step = (lambda: plan.forward(x, w, y, algo=args.algo)) if wl.op == "forward" else \
         (lambda: plan.transpose(x, w, y, algo=args.algo))
 
