@@ -30,6 +30,7 @@ SAMPLING_CELL_CENTRED = 0
 SAMPLING_MW = 1        # pole-including (L + 1) x 2L grid of Sec. 4.2 / App. A
 BASIS_BILINEAR = 0     # 3x3 node grid, K = 9
 BASIS_AXISYM = 1       # 4 nodes along theta, K = 4
+BASIS_SEPARABLE = 2    # 4 nodes along theta x 4 along phi, K = 16
 
 
 def build(out: str = LIB_PATH, source: str = SOURCE, extra_flags=()) -> str:
@@ -68,6 +69,8 @@ class Oracle:
         lib.oracle_quadrature_s.argtypes = [ctypes.c_int] * 4 + [_dp]
         lib.oracle_basis_axisym.restype = None
         lib.oracle_basis_axisym.argtypes = [ctypes.c_double] * 2 + [_dp]
+        lib.oracle_basis_separable.restype = None
+        lib.oracle_basis_separable.argtypes = [ctypes.c_double] * 3 + [_dp]
         lib.oracle_psi_dense_ex.restype = ctypes.c_int
         lib.oracle_psi_dense_ex.argtypes = [ctypes.c_int] * 6 + [ctypes.c_double] * 2 + [_dp]
         lib.oracle_longitude.restype = ctypes.c_double
@@ -139,6 +142,11 @@ class Oracle:
         self.lib.oracle_basis_axisym(Theta, h, _ptr(out))
         return out
 
+    def basis_separable(self, Theta: float, Phi: float, h: float) -> np.ndarray:
+        out = np.zeros(16)
+        self.lib.oracle_basis_separable(Theta, Phi, h, _ptr(out))
+        return out
+
     def psi_dense(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, h=None, *,
                   sampling=SAMPLING_CELL_CENTRED, basis=BASIS_BILINEAR) -> np.ndarray:
         h = default_h(theta_c, basis) if not h else h
@@ -162,6 +170,8 @@ class Oracle:
         C_y = w.shape[0] if fn == "oracle_forward" else w.shape[1]
         if w.shape[2] != basis_size(basis):
             raise ValueError("w last extent must be %d" % basis_size(basis))
+        if (w.shape[1] if fn == "oracle_forward" else w.shape[0]) != C_x:
+            raise ValueError("w does not match the input channels")
         if pix is None:
             pix = np.arange(out_grid[0] * out_grid[1], dtype=np.int64)
         pix = np.ascontiguousarray(pix, dtype=np.int64)
@@ -217,6 +227,8 @@ class Oracle:
             raise ValueError("w last extent must be %d" % basis_size(basis))
         B, C_dy = dy.shape[0], dy.shape[1]
         C_dx = w.shape[1] if not transpose else w.shape[0]
+        if (w.shape[0] if not transpose else w.shape[1]) != C_dy:
+            raise ValueError("w does not match the channels of dy")
         grid = (nlat_out, nlon_out) if transpose else (nlat_in, nlon_in)
         full = pix is None
         if full:
@@ -270,13 +282,23 @@ def default_h(theta_c: float, basis: int = BASIS_BILINEAR) -> float:
     """Node spacing.  3x3 grid: theta_c / 3 (App. E.2 puts the edge nodes at
     pi/L with a cutoff of 3 pi/L).  Axisymmetric: theta_c / 4, four nodes at
     0, h, 2h, 3h whose last hat vanishes at the cutoff."""
-    return theta_c / 4.0 if basis == BASIS_AXISYM else theta_c / 3.0
+    return theta_c / 4.0 if basis in (BASIS_AXISYM, BASIS_SEPARABLE) else theta_c / 3.0
 
 
 def basis_size(basis: int) -> int:
-    return 4 if basis == BASIS_AXISYM else 9
+    return {BASIS_AXISYM: 4, BASIS_SEPARABLE: 16}.get(basis, 9)
+
+
+def depthwise_weights(w_dw: np.ndarray) -> np.ndarray:
+    """Depthwise channels (each channel filtered by its own filter, Sec. 4.2's
+    depthwise-separable layers): the op with W[c][c'][k] = delta(c, c') w[c][k]."""
+    C, K = w_dw.shape
+    w = np.zeros((C, C, K))
+    for c in range(C):
+        w[c, c] = w_dw[c]
+    return w
 
 
 __all__ = ["Oracle", "build", "default", "default_h", "basis_size", "QUAD_FEJER1",
            "QUAD_CELL_AREA", "SAMPLING_CELL_CENTRED", "SAMPLING_MW", "BASIS_BILINEAR",
-           "BASIS_AXISYM"]
+           "BASIS_AXISYM", "BASIS_SEPARABLE", "depthwise_weights"]

@@ -270,20 +270,46 @@ void oracle_basis_axisym(double Theta, double h, double psi[4])
     for (int k = 0; k < 4; ++k) psi[k] = hat(Theta / h - k);
 }
 
-/* basis 0 = the 3x3 grid (K = 9), 1 = axisymmetric (K = 4). */
-static int basis_size(int basis) { return basis == 1 ? 4 : 9; }
+/* Separable basis (Sec. 3.4: psi(theta, phi) = theta-part(theta) phi-part(phi),
+ * equally spaced nodes along both, linear interpolation; App. E uses four
+ * nodes along theta and along phi).  Along Theta the four hats of the
+ * axisymmetric basis; along the direction Phi = atan2(v, u) of the filter
+ * frame (0 south, pi/2 east) four periodic hats at Phi = b pi / 2,
+ *   mu_b(Phi) = max(0, 1 - |Phi - b pi/2|_{mod 2 pi} / (pi / 2)),
+ * and psi_{4a+b} = L(Theta / h - a) mu_b(Phi), K = 16.  The separable filter
+ * with node values t_a and p_b is W_{4a+b} = t_a p_b.  At the centre
+ * (Theta = 0) the direction is undefined; Phi = 0 is taken there (the value of
+ * atan2 at the origin), and any point within 1e-12 rad of the centre counts
+ * as the centre. */
+void oracle_basis_separable(double Theta, double Phi, double h, double psi[16])
+{
+    if (Theta <= 1e-12) Phi = 0.0;
+    for (int a = 0; a < 4; ++a) {
+        double la = hat(Theta / h - a);
+        for (int b = 0; b < 4; ++b) {
+            double d = fmod(fabs(Phi - b * 0.5 * M_PI), 2.0 * M_PI);
+            if (d > M_PI) d = 2.0 * M_PI - d;
+            psi[4 * a + b] = la * hat(d / (0.5 * M_PI));
+        }
+    }
+}
+
+/* basis 0 = the 3x3 grid (K = 9), 1 = axisymmetric (K = 4), 2 = separable (K = 16). */
+static int basis_size(int basis) { return basis == 1 ? 4 : basis == 2 ? 16 : 9; }
 
 /* Evaluate the K basis functions of the filter centred at (theta_j, phi_j)
  * at the input point e; returns 0 if the point is beyond the cutoff or all
  * values vanish, 1 otherwise. */
 static int filter_values(int basis, const double m[9], const double e[3], double theta_c,
-                         double h, double psi[9])
+                         double h, double psi[16])
 {
     double Th, u, v;
     frame_coords_m(m, e, &Th, &u, &v);
     if (Th > theta_c) return 0;
     if (basis == 1)
         oracle_basis_axisym(Th, h, psi);
+    else if (basis == 2)
+        oracle_basis_separable(Th, atan2(v, u), h, psi);
     else
         oracle_basis(u, v, h, psi);
     for (int k = 0; k < basis_size(basis); ++k)
@@ -308,7 +334,7 @@ int oracle_psi_dense_ex(int nlat_in, int nlon_in, int nlat_out, int nlon_out, in
         inverse_rotation(oracle_colatitude_s((int)(j / nlon_out), nlat_out, sampling),
                          oracle_longitude((int)(j % nlon_out), nlon_out), m);
         for (int64_t i = 0; i < n_in; ++i) {
-            double e[3], val[9];
+            double e[3], val[16];
             unit_vector(oracle_colatitude_s((int)(i / nlon_in), nlat_in, sampling),
                         oracle_longitude((int)(i % nlon_in), nlon_in), e);
             if (filter_values(basis, m, e, theta_c, h, val))
@@ -371,7 +397,7 @@ static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, d
     int bad = 0;
 #pragma omp parallel
     {
-        double* Z = (double*)malloc(sizeof(double) * (size_t)B * Cin * 9);
+        double* Z = (double*)malloc(sizeof(double) * (size_t)B * Cin * 16);
 #pragma omp for schedule(dynamic)
         for (int64_t n = 0; n < n_pix; ++n) {
             int64_t o = pix[n];
@@ -382,7 +408,7 @@ static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, d
             }
             int to = (int)(o / g_out.nlon), po = (int)(o % g_out.nlon);
             double th_o = oracle_colatitude_s(to, g_out.nlat, smp), ph_o = oracle_longitude(po, g_out.nlon);
-            memset(Z, 0, sizeof(double) * (size_t)B * Cin * 9);
+            memset(Z, 0, sizeof(double) * (size_t)B * Cin * 16);
             double m_o[9], e_o[3];
             inverse_rotation(th_o, ph_o, m_o);
             unit_vector(th_o, ph_o, e_o);
@@ -391,7 +417,7 @@ static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, d
                 if (window && fabs(th_i - th_o) > theta_c) continue;
                 for (int p = 0; p < g_in.nlon; ++p) {
                     double ph_i = oracle_longitude(p, g_in.nlon);
-                    double val[9];
+                    double val[16];
                     int nz;
                     if (!transpose) {
                         double e_i[3];
@@ -407,7 +433,7 @@ static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, d
                     for (int b = 0; b < B; ++b)
                         for (int c = 0; c < Cin; ++c) {
                             double xv = x[((int64_t)b * Cin + c) * n_in + (int64_t)t * g_in.nlon + p];
-                            double* zc = Z + ((size_t)b * Cin + c) * 9;
+                            double* zc = Z + ((size_t)b * Cin + c) * 16;
                             for (int k = 0; k < K; ++k) zc[k] += val[k] * qw * xv;
                         }
                 }
@@ -420,7 +446,7 @@ static int disco_sum(int transpose, grid_t g_in, grid_t g_out, double theta_c, d
                             /* forward: W[co][ci][k]; transpose: W[ci][co][k]. */
                             double wv = transpose ? w[((int64_t)ci * Cout + co) * K + k]
                                                   : w[((int64_t)co * Cin + ci) * K + k];
-                            s += wv * Z[((size_t)b * Cin + ci) * 9 + k];
+                            s += wv * Z[((size_t)b * Cin + ci) * 16 + k];
                         }
                     y[((int64_t)b * Cout + co) * n_pix + n] = s;
                 }
@@ -514,7 +540,7 @@ static int adjoint_sum(int of_transpose, grid_t g_in, grid_t g_out, double theta
     int bad = 0;
 #pragma omp parallel
     {
-        double* Z = (double*)malloc(sizeof(double) * (size_t)B * C_dy * 9);
+        double* Z = (double*)malloc(sizeof(double) * (size_t)B * C_dy * 16);
 #pragma omp for schedule(dynamic)
         for (int64_t n = 0; n < n_pix; ++n) {
             int64_t o = pix[n];
@@ -525,7 +551,7 @@ static int adjoint_sum(int of_transpose, grid_t g_in, grid_t g_out, double theta
             }
             int td = (int)(o / g_dst.nlon), pd = (int)(o % g_dst.nlon);
             double th_d = oracle_colatitude_s(td, g_dst.nlat, smp), ph_d = oracle_longitude(pd, g_dst.nlon);
-            memset(Z, 0, sizeof(double) * (size_t)B * C_dy * 9);
+            memset(Z, 0, sizeof(double) * (size_t)B * C_dy * 16);
             double m_d[9], e_d[3];
             inverse_rotation(th_d, ph_d, m_d);
             unit_vector(th_d, ph_d, e_d);
@@ -534,7 +560,7 @@ static int adjoint_sum(int of_transpose, grid_t g_in, grid_t g_out, double theta
                 if (window && fabs(th_s - th_d) > theta_c) continue;
                 for (int p = 0; p < g_src.nlon; ++p) {
                     double ph_s = oracle_longitude(p, g_src.nlon);
-                    double val[9];
+                    double val[16];
                     int nz;
                     if (!of_transpose) {
                         /* centre at the source point j (out-grid), evaluate at the output i */
@@ -551,7 +577,7 @@ static int adjoint_sum(int of_transpose, grid_t g_in, grid_t g_out, double theta
                     for (int b = 0; b < B; ++b)
                         for (int c = 0; c < C_dy; ++c) {
                             double v = dy[((int64_t)b * C_dy + c) * n_src + (int64_t)t * g_src.nlon + p];
-                            double* zc = Z + ((size_t)b * C_dy + c) * 9;
+                            double* zc = Z + ((size_t)b * C_dy + c) * 16;
                             for (int k = 0; k < K; ++k) zc[k] += val[k] * v;
                         }
                 }
@@ -565,7 +591,7 @@ static int adjoint_sum(int of_transpose, grid_t g_in, grid_t g_out, double theta
                             /* forward op: W[co = cy][ci = cx][k]; transposed op: W[c' = cx][c = cy][k]. */
                             double wv = of_transpose ? w[((int64_t)cx * C_dy + cy) * K + k]
                                                      : w[((int64_t)cy * C_dx + cx) * K + k];
-                            s += wv * Z[((size_t)b * C_dy + cy) * 9 + k];
+                            s += wv * Z[((size_t)b * C_dy + cy) * 16 + k];
                         }
                     dx[((int64_t)b * C_dx + cx) * n_pix + n] = qw * s;
                 }

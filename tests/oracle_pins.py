@@ -613,6 +613,8 @@ _GRAD_CASES = [
     (9, 16, 9, 16, 1, 1),
     (17, 32, 9, 16, 1, 0),
     (12, 24, 6, 12, 0, 1),
+    (16, 32, 8, 16, 0, 2),
+    (9, 16, 9, 16, 1, 2),
 ]
 
 
@@ -628,7 +630,7 @@ def pin_gradients_match_dense_autograd(o):
     import torch
     for (a, b, c, d, smp, bas) in _GRAD_CASES:
         tc = _grad_tc(a, c, smp)
-        K = 4 if bas == 1 else 9
+        K = {1: 4, 2: 16}.get(bas, 9)
         kw = dict(sampling=smp, basis=bas)
         psi = torch.tensor(o.psi_dense(a, b, c, d, tc, **kw))            # [Nout, Nin, K]
         qi = torch.tensor(np.repeat(o.quadrature(a, b, sampling=smp), b))
@@ -667,7 +669,7 @@ def pin_input_gradient_is_plain_adjoint(o):
     the forward and the transposed op."""
     for (a, b, c, d, smp, bas) in _GRAD_CASES:
         tc = _grad_tc(a, c, smp)
-        K = 4 if bas == 1 else 9
+        K = {1: 4, 2: 16}.get(bas, 9)
         kw = dict(sampling=smp, basis=bas)
         r = _rng(51)
         x = r.standard_normal((2, 3, a, b))
@@ -689,7 +691,7 @@ def pin_weight_gradient_by_linearity(o):
     unit weight tensor: every element through the op itself."""
     for (a, b, c, d, smp, bas) in _GRAD_CASES[:3]:
         tc = _grad_tc(a, c, smp)
-        K = 4 if bas == 1 else 9
+        K = {1: 4, 2: 16}.get(bas, 9)
         kw = dict(sampling=smp, basis=bas)
         r = _rng(52)
         x = r.standard_normal((2, 2, a, b))
@@ -715,7 +717,7 @@ def pin_forward_adjoint_from_transpose(o):
     and differ only in where the quadrature sits: A^T dy = diag(q_in) T diag(1 / q_out) dy."""
     for (a, b, c, d, smp, bas) in _GRAD_CASES:
         tc = _grad_tc(a, c, smp)
-        K = 4 if bas == 1 else 9
+        K = {1: 4, 2: 16}.get(bas, 9)
         kw = dict(sampling=smp, basis=bas)
         r = _rng(53)
         w = r.standard_normal((3, 2, K))
@@ -725,6 +727,106 @@ def pin_forward_adjoint_from_transpose(o):
         got = o.input_grad(a, b, c, d, tc, dy, w, **kw)
         ref = qi * o.transpose(a, b, c, d, tc, dy / qo, w, **kw)
         assert np.abs(got - ref).max() <= 1e-12 * np.abs(ref).max()
+
+
+# --------------------------------------------------------------------------- #
+# Separable basis (Sec. 3.4, App. E: four nodes along theta and along phi) and
+# depthwise channels (Sec. 4.2).
+# --------------------------------------------------------------------------- #
+_SEP = 2
+
+
+def pin_separable_basis(o):
+    """psi_{4a+b}(Theta, Phi) = L(Theta/h - a) mu_b(Phi): the theta factor is the
+    axisymmetric hat (pinned above); along Phi four periodic hats at b pi/2 with
+    the Kronecker property, a partition of unity at every direction, linear
+    reproduction between neighbouring nodes and period 2 pi.  At the centre
+    only node (0, 0) fires (direction taken as 0)."""
+    h = 0.0123
+    r = _rng(70)
+    for _ in range(300):
+        t = r.uniform(0, 4.2 * h)
+        ph = r.uniform(-3 * math.pi, 3 * math.pi)
+        psi = o.basis_separable(t, ph, h).reshape(4, 4)
+        lam = o.basis_axisym(t, h)
+        mu = psi.sum(axis=0) / max(lam.sum(), 1e-300) if lam.sum() > 0 else None
+        if lam.sum() > 0:
+            assert np.abs(psi - np.outer(lam, mu)).max() <= 1e-14
+            assert abs(mu.sum() - 1.0) <= 1e-13
+            assert np.count_nonzero(mu > 1e-15) <= 2
+            # linear between the two nodes around ph
+            base = math.floor((ph % (2 * math.pi)) / (math.pi / 2))
+            frac = (ph % (2 * math.pi)) / (math.pi / 2) - base
+            assert abs(mu[base % 4] - (1 - frac)) <= 1e-12 and abs(mu[(base + 1) % 4] - frac) <= 1e-12
+        psi2 = o.basis_separable(t, ph + 2 * math.pi, h)
+        assert np.abs(psi2 - psi.ravel()).max() <= 1e-12
+    for b in range(4):
+        e = np.zeros(4)
+        e[b] = 1.0
+        psi = o.basis_separable(h, b * math.pi / 2, h).reshape(4, 4)
+        assert np.abs(psi[1] - e).max() <= 1e-15 and np.abs(np.delete(psi, 1, axis=0)).max() == 0.0
+    c = o.basis_separable(0.0, 1.234, h)
+    e = np.zeros(16)
+    e[0] = 1.0
+    assert np.array_equal(c, e)
+
+
+def pin_separable_reduces_to_axisymmetric(o):
+    """With phi node values all equal the separable filter is the axisymmetric
+    one (the phi hats sum to one in every direction): W_sep[.,.,4a+b] = W_ax[.,.,a]
+    gives the axisymmetric op's output, forward and transposed, on both grids."""
+    for (a, b, c, d, smp) in ((16, 32, 8, 16, 0), (9, 16, 9, 16, 1), (17, 32, 9, 16, 1)):
+        tc = 3 * math.pi / (min(a, c) - (1 if smp == 1 else 0))
+        r = _rng(71)
+        x = r.standard_normal((2, 2, a, b))
+        w4 = r.standard_normal((3, 2, 4))
+        w16 = np.repeat(w4, 4, axis=2)
+        y4 = o.forward(a, b, c, d, tc, x, w4, sampling=smp, basis=_AX)
+        y16 = o.forward(a, b, c, d, tc, x, w16, sampling=smp, basis=_SEP)
+        assert np.abs(y16 - y4).max() <= 1e-13 * np.abs(y4).max()
+        xT = r.standard_normal((2, 3, c, d))
+        yT4 = o.transpose(a, b, c, d, tc, xT, w4, sampling=smp, basis=_AX)
+        yT16 = o.transpose(a, b, c, d, tc, xT, w16, sampling=smp, basis=_SEP)
+        assert np.abs(yT16 - yT4).max() <= 1e-13 * np.abs(yT4).max()
+
+
+def pin_separable_mirror_symmetry(o):
+    """phi -> -phi maps the phi node b to -b (1 <-> 3); theta -> pi - theta maps
+    b to 2 - b (0 <-> 2).  The flip is checked where no output meets an input
+    point (2x downsampling: the centre's direction convention is not
+    flip-symmetric)."""
+    a, b, c, d = 16, 32, 8, 16
+    tc = 3 * math.pi / c
+    r = _rng(72)
+    x = r.standard_normal((1, 2, a, b))
+    w = r.standard_normal((2, 2, 16))
+    y = o.forward(a, b, c, d, tc, x, w, basis=_SEP)
+    perm_m = [4 * (k // 4) + (-(k % 4)) % 4 for k in range(16)]
+    perm_f = [4 * (k // 4) + (2 - k % 4) % 4 for k in range(16)]
+    ym = o.forward(a, b, c, d, tc, x[..., (-np.arange(b)) % b], w[:, :, perm_m], basis=_SEP)
+    assert np.abs(ym - y[..., (-np.arange(d)) % d]).max() <= 1e-13 * np.abs(y).max()
+    yf = o.forward(a, b, c, d, tc, x[:, :, ::-1, :], w[:, :, perm_f], basis=_SEP)
+    assert np.abs(yf - y[:, :, ::-1, :]).max() <= 1e-12 * np.abs(y).max()
+    # same grid (outputs on input points): the mirror still holds exactly
+    y = o.forward(a, b, a, b, tc, x, w, basis=_SEP)
+    ym = o.forward(a, b, a, b, tc, x[..., (-np.arange(b)) % b], w[:, :, perm_m], basis=_SEP)
+    assert np.abs(ym - y[..., (-np.arange(b)) % b]).max() <= 1e-13 * np.abs(y).max()
+
+
+def pin_depthwise_is_per_channel(o):
+    """Depthwise channels: channel c of the output is channel c of the input
+    filtered by w[c] alone, i.e. each channel run as its own one-channel op."""
+    import oracle as _orc
+    a, b = 9, 16
+    tc = 3 * math.pi / 8
+    r = _rng(73)
+    for bas, K in ((_AX, 4), (_SEP, 16), (0, 9)):
+        x = r.standard_normal((2, 3, a, b))
+        wd = r.standard_normal((3, K))
+        y = o.forward(a, b, a, b, tc, x, _orc.depthwise_weights(wd), sampling=1, basis=bas)
+        for c in range(3):
+            yc = o.forward(a, b, a, b, tc, x[:, c:c + 1], wd[c][None, None, :], sampling=1, basis=bas)
+            assert np.abs(y[:, c:c + 1] - yc).max() <= 1e-13 * np.abs(y).max()
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -51,7 +51,13 @@ MUTANTS = {
                          "2.0 * M_PI / ((2.0 * L) * (2.0 * L + 1.0))"),
     "axisym_node_shift": ("psi[k] = hat(Theta / h - k);", "psi[k] = hat(Theta / h - k - 1);"),
     "axisym_signed_coordinate": ("oracle_basis_axisym(Th, h, psi);", "oracle_basis_axisym(u, h, psi);"),
-    "axisym_drops_last_node": ("return basis == 1 ? 4 : 9;", "return basis == 1 ? 3 : 9;"),
+    "axisym_drops_last_node": ("return basis == 1 ? 4 : basis", "return basis == 1 ? 3 : basis"),
+    "separable_phi_node_offset": ("double d = fmod(fabs(Phi - b * 0.5 * M_PI), 2.0 * M_PI);",
+                                  "double d = fmod(fabs(Phi + b * 0.5 * M_PI), 2.0 * M_PI);"),
+    "separable_phi_not_periodic": ("if (d > M_PI) d = 2.0 * M_PI - d;", "if (d > 4.0 * M_PI) d = 2.0 * M_PI - d;"),
+    "separable_index_order": ("psi[4 * a + b] = la * hat(d / (0.5 * M_PI));",
+                              "psi[4 * b + a] = la * hat(d / (0.5 * M_PI));"),
+    "separable_centre_direction": ("if (Theta <= 1e-12) Phi = 0.0;", "if (Theta <= 1e-12) Phi = 0.5 * M_PI;"),
     # Gradients (App. C).
     "adjoint_quadrature_of_source": ("            double qw = q[td];", "            double qw = q[td] * 0.0 + 1.0;"),
     "adjoint_w_not_transposed": (": w[((int64_t)cy * C_dx + cx) * K + k];",
