@@ -81,6 +81,9 @@ def kernel_model(name, wl, work, es):
     read.
     """
     B, Ci, Co = wl.batch, wl.c_in, wl.c_out
+    if getattr(wl, "depthwise", False):
+        # B x C one-channel items, each filtered by its channel's own filter.
+        B, Ci, Co = B * Ci, 1, 1
     outp, inp, pairs = work
     if name in ("stencil", "stencil_blocked"):
         # W folded into psi: 2 flop per stored (output pixel, input pixel)
@@ -194,6 +197,8 @@ def cpu_baseline(wl, x, w, seconds=15.0):
     fn = o.forward if wl.op == "forward" else o.transpose
     kw = wl.oracle_kwargs()
     x64, w64 = x.astype(np.float64), w.astype(np.float64)
+    if wl.depthwise:
+        w64 = oracle.depthwise_weights(w64)
     # Grow the sample until one timed call takes at least half the budget
     # (the first calls also pay thread start-up, so one calibration is short).
     n, dt = 256, 0.0
@@ -215,7 +220,8 @@ def kernel_report(plan, kt, wl, transpose, algo, es):
     """Per-kernel figures of one timed pass and the roofline object of the
     kernel with the largest total time (achieved against HBM peak for
     HBM-bound kernels, against the fp32 peak otherwise)."""
-    work = plan.kernel_work(transpose, algo, wl.c_in, wl.c_out, wl.dtype)
+    cin, cout = (1, 1) if wl.depthwise else (wl.c_in, wl.c_out)
+    work = plan.kernel_work(transpose, algo, cin, cout, wl.dtype)
     missing = sorted(set(kt) - set(work))
     if missing:
         raise SystemExit("no work figures for kernels %s" % missing)
@@ -401,6 +407,9 @@ def main(argv=None):
     plan_s = time.time() - t0
     info = plan.info()
     log("plan built in %.2fs: %s" % (plan_s, info))
+    if args.backward and wl.depthwise:
+        print("--backward: the depthwise calls have no gradient entry points", file=sys.stderr)
+        return 2
     if args.backward:
         ms, kernels, roof = bench_backward(args, wl, plan, x, w, es, torch, disco)
         out = {
@@ -417,8 +426,12 @@ def main(argv=None):
         plan.close()
         print(json.dumps(out), flush=True)
         return 0
-    step = (lambda: plan.forward(x, w, y, algo=args.algo)) if wl.op == "forward" else \
-        (lambda: plan.transpose(x, w, y, algo=args.algo))
+    if wl.depthwise:
+        step = (lambda: plan.forward_depthwise(x, w, y)) if wl.op == "forward" else \
+            (lambda: plan.transpose_depthwise(x, w, y))
+    else:
+        step = (lambda: plan.forward(x, w, y, algo=args.algo)) if wl.op == "forward" else \
+            (lambda: plan.transpose(x, w, y, algo=args.algo))
 
     for _ in range(args.warmup):
         step()
@@ -458,7 +471,8 @@ def main(argv=None):
     # move the gathered sums through HBM: their achieved GB/s against the
     # HBM peak (the default schedule's kernels are bound by arithmetic).
     hbm = None
-    if not args.no_hbm_schedule and args.algo != "gather_then_contract" and wl.basis == "bilinear3x3":
+    if not args.no_hbm_schedule and args.algo != "gather_then_contract" and wl.basis == "bilinear3x3" \
+            and not wl.depthwise:
         step2 = (lambda: plan.forward(x, w, y, algo="gather_then_contract")) if wl.op == "forward" else \
             (lambda: plan.transpose(x, w, y, algo="gather_then_contract"))
         for _ in range(2):
@@ -501,7 +515,8 @@ def main(argv=None):
         "config": {"workload": wl.name, "op": wl.op, "nlat_in": wl.nlat_in, "nlon_in": wl.nlon_in,
                    "nlat_out": wl.nlat_out, "nlon_out": wl.nlon_out, "theta_c": wl.theta_c,
                    "batch": wl.batch, "c_in": wl.c_in, "c_out": wl.c_out, "basis": wl.basis,
-                   "sampling": wl.sampling, "algo": args.algo, "storage": wl.dtype},
+                   "sampling": wl.sampling, "channels": wl.channels,
+                   "algo": "depthwise" if wl.depthwise else args.algo, "storage": wl.dtype},
         "paper_baseline": baseline,
         "op_algorithmic_gbs": round(op_bytes / (ms_per_step / 1e3) / 1e9, 2),
         "kernels": per_kernel,

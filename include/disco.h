@@ -34,7 +34,20 @@
  *   DISCO_BASIS_AXISYMMETRIC_4 (K = 4): the axisymmetric filter psi(theta)
  *     that App. B times, four nodes at geodesic distance k h, k = 0..3,
  *     psi_k(Theta) = max(0, 1 - |Theta / h - k|); the default h = theta_c / 4
- *     makes the last hat vanish at the cutoff.
+ *     makes the last hat vanish at the cutoff;
+ *   DISCO_BASIS_SEPARABLE_4X4 (K = 16): the separable filter
+ *     psi(theta, phi) = theta-part(theta) phi-part(phi) of Sec. 3.4 with four
+ *     nodes along each (App. E), as products of hats,
+ *     psi_{4a+b}(Theta, Phi) = max(0, 1 - |Theta / h - a|) mu_b(Phi),
+ *     mu_b(Phi) = max(0, 1 - |Phi - b pi / 2|_{mod 2 pi} / (pi / 2)),
+ *     Phi = atan2(v, u) the direction in the filter's tangent plane (0 south,
+ *     pi / 2 east; taken as 0 at the filter centre itself), default
+ *     h = theta_c / 4.  A separable filter with node values t_a and p_b is
+ *     W[., ., 4a+b] = t_a p_b.
+ *
+ * Channels: W[Cout][Cin][K] mixes every input channel into every output
+ * channel; the depthwise calls filter each channel by its own W[c][K]
+ * (the depthwise half of the paper's depthwise-separable layers, Sec. 4.2).
  *
  * Conventions for every call:
  *   - every call returns a disco_status_t; on failure nothing is enqueued on
@@ -75,7 +88,8 @@ typedef enum {
 typedef enum { DISCO_FLOAT32 = 0, DISCO_BFLOAT16 = 1 } disco_dtype_t;
 
 enum { DISCO_BASIS_BILINEAR_3X3 = 0,                /* K = 9 (App. E.2) */
-       DISCO_BASIS_AXISYMMETRIC_4 = 1 };             /* K = 4 (Sec. 3.4, App. B) */
+       DISCO_BASIS_AXISYMMETRIC_4 = 1,               /* K = 4 (Sec. 3.4, App. B) */
+       DISCO_BASIS_SEPARABLE_4X4 = 2 };              /* K = 16 (Sec. 3.4, App. E) */
 /* Quadrature: 0 = the sampling-theorem weights of the grid (Sec. 4.1): Fejer's
  * first rule in cos(theta) on the cell-centred grid, App. A's weights on the
  * pole-including grid; 1 = cell areas (cell-centred grid only). */
@@ -94,9 +108,9 @@ typedef enum {
 } disco_algo_t;
 
 typedef struct {
-    int32_t kind;        /* DISCO_BASIS_BILINEAR_3X3 or DISCO_BASIS_AXISYMMETRIC_4 */
+    int32_t kind;        /* DISCO_BASIS_BILINEAR_3X3, _AXISYMMETRIC_4 or _SEPARABLE_4X4 */
     int32_t quadrature;  /* DISCO_QUAD_SAMPLING_THEOREM (default) or DISCO_QUAD_CELL_AREA */
-    double node_spacing; /* h in radians; 0 selects theta_c / 3 (3x3) or theta_c / 4 (axisymmetric) */
+    double node_spacing; /* h in radians; 0 selects theta_c / 3 (3x3) or theta_c / 4 (the others) */
     int32_t sampling;    /* DISCO_SAMPLING_CELL_CENTRED (default) or DISCO_SAMPLING_POLES */
     int32_t flags;       /* 0 or DISCO_PLAN_BACKWARD */
 } disco_basis_t;
@@ -108,12 +122,12 @@ enum { DISCO_PLAN_BACKWARD = 1 };
 typedef struct {
     void* data;       /* device pointer (may be NULL only when the tensor is empty) */
     int32_t dtype;    /* disco_dtype_t */
-    int32_t ndim;     /* x, y: 4 ([B, C, nlat, nlon]); w: 3 ([C0, C1, K]) */
+    int32_t ndim;     /* x, y: 4 ([B, C, nlat, nlon]); w: 3 ([C0, C1, K]), or 2 ([C, K]) depthwise */
     int64_t shape[4];
 } disco_tensor_t;
 
 typedef struct {
-    int32_t K;                 /* basis size (9 or 4) */
+    int32_t K;                 /* basis size (9, 4 or 16) */
     int32_t nlat_in, nlon_in, nlat_out, nlon_out;
     int32_t phases_forward;    /* longitude phases of the forward op's patterns */
     int32_t phases_transpose;  /* ... and of the transposed op's */
@@ -170,11 +184,26 @@ disco_status_t disco_forward(disco_plan_t plan, const disco_tensor_t* x, const d
 disco_status_t disco_transpose(disco_plan_t plan, const disco_tensor_t* x,
                                const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream);
 
+/* Depthwise forward and transposed ops (Sec. 4.2, the depthwise half of a
+ * depthwise-separable layer): each channel is filtered by its own filter,
+ *   forward    y[b,c,j] = sum_k W[c,k] sum_i psi_k(R_j^{-1} w_i) q_in(i) x[b,c,i]
+ *   transpose  y[b,c,i] = sum_k W[c,k] sum_j psi_k(R_j^{-1} w_i) q_out(j) x[b,c,j]
+ * i.e. disco_forward / disco_transpose with W'[c][c'][k] = (c == c') W[c][k].
+ *   x [B, C, op input grid], w [C, K], y [B, C, op output grid]; any basis;
+ *   B * C <= 65535.
+ * W is folded into psi per call (one FMA per stored entry and channel).
+ * Errors as disco_forward (SHAPE for a w that is not [C, K]). */
+disco_status_t disco_forward_depthwise(disco_plan_t plan, const disco_tensor_t* x,
+                                       const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream);
+disco_status_t disco_transpose_depthwise(disco_plan_t plan, const disco_tensor_t* x,
+                                         const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream);
+
 /* disco_forward / disco_transpose with an explicit execution variant
  * (disco_algo_t).  Same arguments, errors and results.  With the
- * axisymmetric basis every variant runs the one schedule that basis has (W
- * folded into psi per call, see disco_kernel_work's "stencil" row) except
- * GATHER_THEN_CONTRACT and CONTRACT_THEN_GATHER, which return UNSUPPORTED. */
+ * axisymmetric and separable bases every variant runs the one schedule those
+ * bases have (W folded into psi per call, see disco_kernel_work's "stencil"
+ * row) except GATHER_THEN_CONTRACT and CONTRACT_THEN_GATHER, which return
+ * UNSUPPORTED. */
 disco_status_t disco_forward_algo(disco_plan_t plan, const disco_tensor_t* x,
                                   const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream,
                                   int32_t algo);
@@ -214,8 +243,9 @@ disco_status_t disco_transpose_backward(disco_plan_t plan, const disco_tensor_t*
 /* Host-only export of the stored psi entries of one op, without any device
  * (Sec. 4.1: Psi is constructed explicitly, only where it is non-zero).
  * transpose = 0 selects the forward op, 1 the transposed op.  Each entry is
- * (output ring, phase, input ring, longitude offset d, 9 values: psi_0..8 for
- * the 3x3 basis, psi_0..3 then five zeros for the axisymmetric one); an output
+ * (output ring, phase, input ring, longitude offset d, and a row of values:
+ * 9 for the 3x3 basis, psi_0..8; 9 for the axisymmetric one, psi_0..3 then
+ * five zeros; 16 for the separable one, psi_0..15); an output
  * pixel p_out = P * q + phase reads input pixel (stride * q + d) mod nlon of
  * the op's input grid, with P = phases and stride = nlon_in_op * P /
  * nlon_out_op.  Values are psi_k times the quadrature weight of the op's
@@ -251,9 +281,10 @@ disco_status_t disco_kernel_timing_read(int32_t capacity, char* names, int64_t* 
  * distinct input pixels it reads; pairs[i], the non-zero (output pixel,
  * input pixel, k) triples of the sparse tensor (Sec. 4.1 eq. 7, of the
  * forward or the transposed op) whose products it accounts for (for the
- * axisymmetric basis's "stencil" and "stencil_blocked" rows, whose psi has
- * W folded in, the
- * (output pixel, input pixel) pairs instead).  A kernel
+ * "stencil" and "stencil_blocked" rows of the axisymmetric and separable
+ * bases, whose psi has W folded in, the (output pixel, input pixel) pairs
+ * instead; with these two bases a depthwise call runs the rows of
+ * c_in = c_out = 1 once per channel).  A kernel
  * that only moves intermediate data reports zeros where it touches neither
  * x nor y.  Up to `capacity` rows are written (any output pointer may be
  * NULL) and *count receives the number of kernels.  Host only, no device

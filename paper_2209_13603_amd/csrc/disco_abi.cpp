@@ -67,7 +67,8 @@ disco_status_t resolve_params(int nlat_in, int nlon_in, int nlat_out, int nlon_o
     disco_basis_t b{DISCO_BASIS_BILINEAR_3X3, DISCO_QUAD_SAMPLING_THEOREM, 0.0, DISCO_SAMPLING_CELL_CENTRED, 0};
     if (basis) b = *basis;
     if ((b.flags & ~DISCO_PLAN_BACKWARD) != 0) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown basis.flags bits");
-    if (b.kind != DISCO_BASIS_BILINEAR_3X3 && b.kind != DISCO_BASIS_AXISYMMETRIC_4)
+    if (b.kind != DISCO_BASIS_BILINEAR_3X3 && b.kind != DISCO_BASIS_AXISYMMETRIC_4 &&
+        b.kind != DISCO_BASIS_SEPARABLE_4X4)
         return fail(DISCO_ERR_UNSUPPORTED, "unknown basis kind");
     if (b.sampling != DISCO_SAMPLING_CELL_CENTRED && b.sampling != DISCO_SAMPLING_POLES)
         return fail(DISCO_ERR_UNSUPPORTED, "unknown sampling");
@@ -85,7 +86,7 @@ disco_status_t resolve_params(int nlat_in, int nlon_in, int nlat_out, int nlon_o
         return fail(DISCO_ERR_UNSUPPORTED, "nlon_in / nlon_out or nlon_out / nlon_in must be an integer");
     p->nlat_in = nlat_in; p->nlon_in = nlon_in; p->nlat_out = nlat_out; p->nlon_out = nlon_out;
     p->theta_c = theta_c;
-    const double h_default = b.kind == DISCO_BASIS_AXISYMMETRIC_4 ? theta_c / 4.0 : theta_c / 3.0;
+    const double h_default = b.kind == DISCO_BASIS_BILINEAR_3X3 ? theta_c / 3.0 : theta_c / 4.0;
     p->h = b.node_spacing > 0.0 ? b.node_spacing : h_default;
     p->quadrature = b.quadrature;
     p->basis = b.kind;
@@ -209,6 +210,7 @@ disco_status_t upload_stencil(const HostOp& h, StencilDev* d) {
     if ((s = upload_vec(H.pieces, &d->pieces, &d->bytes, "hipMalloc(stencil pieces)")) != DISCO_OK) return s;
     if ((s = upload_vec(H.chunks, &d->chunks, &d->bytes, "hipMalloc(stencil chunks)")) != DISCO_OK) return s;
     if ((s = upload_vec(H.vals, &d->vals, &d->bytes, "hipMalloc(stencil values)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.cells, &d->cells, &d->bytes, "hipMalloc(stencil cells)")) != DISCO_OK) return s;
     PackedDev& P = d->P;
     if ((s = upload_vec(H.segs, &P.segs, &d->bytes, "hipMalloc(segments)")) != DISCO_OK) return s;
     if ((s = upload_vec(H.items, &P.items, &d->bytes, "hipMalloc(items)")) != DISCO_OK) return s;
@@ -257,18 +259,23 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
     d->bytes = (int64_t)(pb + eb);
     d->work_all = pattern_work(h, {});
     d->basis = h.basis;
-    disco_status_t s = upload_packed(h, {}, &d->packed);
+    const CellMap cm = cell_map(h.basis);
+    std::vector<int8_t> cmv(&cm.k[0][0], &cm.k[0][0] + sizeof(cm.k));
+    disco_status_t s = upload_vec(cmv, &d->cmap_dev, &d->bytes, "hipMalloc(cell map)");
+    if (s != DISCO_OK) return s;
+    s = upload_packed(h, {}, &d->packed);
     if (s != DISCO_OK) return s;
     d->bytes += d->packed.bytes;
-    // The axisymmetric basis has its stencil kernels (the blocked one when the
-    // longitude stride is 1); the spectral and sweep layouts are built for the
-    // 3x3 basis.
-    if (h.basis == DISCO_BASIS_AXISYMMETRIC_4) {
+    // Every basis has the folded-weight stencil kernels (all calls of the
+    // axisymmetric and separable bases, depthwise calls of any basis): the
+    // general one on the packed layout, the blocked one when the longitude
+    // stride is 1.  The spectral and sweep layouts are built for the 3x3 basis.
+    if (h.g.stride == 1) {
+        if ((s = upload_stencil(h, &d->stencil)) != DISCO_OK) return s;
+        d->bytes += d->stencil.bytes;
+    }
+    if (h.basis != DISCO_BASIS_BILINEAR_3X3) {
         d->work_light = d->work_all;
-        if (h.g.stride == 1) {
-            if ((s = upload_stencil(h, &d->stencil)) != DISCO_OK) return s;
-            d->bytes += d->stencil.bytes;
-        }
         return DISCO_OK;
     }
     SpectralHost sp;
@@ -327,7 +334,9 @@ void free_op(DeviceOp* d) {
     if (d->entries) (void)hipFree(d->entries);
     if (d->rest_pats) (void)hipFree(d->rest_pats);
     if (d->spectral_ring) (void)hipFree(d->spectral_ring);
+    if (d->cmap_dev) (void)hipFree(d->cmap_dev);
     d->spectral_ring = nullptr;
+    d->cmap_dev = nullptr;
     d->pat_ptr = nullptr;
     d->entries = nullptr;
     d->rest_pats = nullptr;
@@ -337,7 +346,7 @@ void free_op(DeviceOp* d) {
     free_packed(&d->packed_rest);
     free_spectral(&d->spectral);
     free_sweep(&d->sweep);
-    void* sp[] = {d->stencil.pieces, d->stencil.chunks, d->stencil.vals};
+    void* sp[] = {d->stencil.pieces, d->stencil.chunks, d->stencil.vals, d->stencil.cells};
     for (void* p : sp)
         if (p) (void)hipFree(p);
     free_packed(&d->stencil.P);
@@ -394,7 +403,7 @@ Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co, int32_t dtyp
         (void)Ci;
     }
     Dispatch d{algo, false, false, &op.packed, &op.work_all};
-    if (op.basis == DISCO_BASIS_AXISYMMETRIC_4) return d;
+    if (op.basis != DISCO_BASIS_BILINEAR_3X3) return d;
     d.spectral = algo == DISCO_ALGO_FUSED && op.spectral.n_rings > 0;
     // The sweep kernel addresses x and y through 32-bit buffer offsets: all
     // kCIC input channel planes and one output plane must stay below 2^31
@@ -419,13 +428,44 @@ Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co, int32_t dtyp
 disco_status_t check_op_args(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
                              const disco_tensor_t* w, const disco_tensor_t* y, int32_t algo);
 
+// depthwise: x [B, C, ...], w [C, K], y [B, C, ...] (channel c filtered by
+// w[c] alone); algo is then ignored.
 disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
-                      const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream, int32_t algo);
+                      const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream, int32_t algo,
+                      bool depthwise = false);
 
 disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
-                   disco_tensor_t* y, hipStream_t stream, int32_t algo, bool transpose) {
+                   disco_tensor_t* y, hipStream_t stream, int32_t algo, bool transpose, bool depthwise = false) {
     if (!plan) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan is NULL");
-    return run_op(plan, transpose ? plan->tr : plan->fwd, transpose, x, w, y, stream, algo);
+    return run_op(plan, transpose ? plan->tr : plan->fwd, transpose, x, w, y, stream, algo, depthwise);
+}
+
+disco_status_t check_common(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                            const disco_tensor_t* y);
+
+// Depthwise application of `op`: x [B, C, op input grid], w [C, K],
+// y [B, C, op output grid].
+disco_status_t check_dw_args(disco_plan_t plan, const DeviceOp& op, const disco_tensor_t* x,
+                             const disco_tensor_t* w, const disco_tensor_t* y) {
+    if (!x || !w || !y) return fail(DISCO_ERR_INVALID_ARGUMENT, "tensor descriptor is NULL");
+    const OpGeom& g = op.g;
+    if (x->ndim != 4 || y->ndim != 4 || w->ndim != 2)
+        return fail(DISCO_ERR_SHAPE, "x and y must be 4-D [B, C, nlat, nlon], depthwise w 2-D [C, K]");
+    for (int i = 0; i < 4; ++i)
+        if (x->shape[i] < 0 || y->shape[i] < 0 || (i < 2 && w->shape[i] < 0))
+            return fail(DISCO_ERR_SHAPE, "negative extent");
+    const int64_t B = x->shape[0], C = x->shape[1];
+    if (x->shape[2] != g.nlat_i || x->shape[3] != g.nlon_i)
+        return fail(DISCO_ERR_SHAPE, "x grid must be [" + std::to_string(g.nlat_i) + ", " + std::to_string(g.nlon_i) + "]");
+    if (y->shape[2] != g.nlat_o || y->shape[3] != g.nlon_o)
+        return fail(DISCO_ERR_SHAPE, "y grid must be [" + std::to_string(g.nlat_o) + ", " + std::to_string(g.nlon_o) + "]");
+    if (y->shape[0] != B || y->shape[1] != C) return fail(DISCO_ERR_SHAPE, "depthwise x and y must have the same [B, C]");
+    const int K = basis_size(op.basis);
+    if (w->shape[0] != C || w->shape[1] != K)
+        return fail(DISCO_ERR_SHAPE, "depthwise w must be [C, " + std::to_string(K) + "]");
+    if (C < 1) return fail(DISCO_ERR_SHAPE, "channel count must be >= 1");
+    if (B * C > 65535) return fail(DISCO_ERR_SHAPE, "batch x channels too large for a depthwise call");
+    return check_common(plan, x, w, y);
 }
 
 disco_status_t check_op_args(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
@@ -451,11 +491,18 @@ disco_status_t check_op_args(disco_plan_t plan, const DeviceOp& op, bool transpo
         return fail(DISCO_ERR_SHAPE, "forward w must be [Cout, Cin, " + ks + "]");
     if (transpose && (w->shape[0] != Ci || w->shape[1] != Co))
         return fail(DISCO_ERR_SHAPE, "transpose w must be [CinT, CoutT, " + ks + "]");
-    const bool axisym = op.basis == DISCO_BASIS_AXISYMMETRIC_4;
-    if (axisym && (algo == DISCO_ALGO_GATHER_THEN_CONTRACT || algo == DISCO_ALGO_CONTRACT_THEN_GATHER))
-        return fail(DISCO_ERR_UNSUPPORTED, "the axisymmetric basis has no two-kernel schedule");
+    const bool folded = op.basis != DISCO_BASIS_BILINEAR_3X3;
+    if (folded && (algo == DISCO_ALGO_GATHER_THEN_CONTRACT || algo == DISCO_ALGO_CONTRACT_THEN_GATHER))
+        return fail(DISCO_ERR_UNSUPPORTED, "only the 3x3 basis has the two-kernel schedules");
     if (Ci < 1 || Co < 1) return fail(DISCO_ERR_SHAPE, "channel counts must be >= 1");
     if (B > 65535 || Ci > 4096 || Co > 4096) return fail(DISCO_ERR_SHAPE, "batch or channels too large");
+    return check_common(plan, x, w, y);
+}
+
+// dtype, device residency and overlap checks shared by every application.
+disco_status_t check_common(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                            const disco_tensor_t* y) {
+    const int64_t B = x->shape[0];
     if (x->dtype != y->dtype || w->dtype != x->dtype)
         return fail(DISCO_ERR_DTYPE, "x, w and y must share one dtype");
     if (x->dtype != DISCO_FLOAT32 && x->dtype != DISCO_BFLOAT16)
@@ -473,22 +520,30 @@ disco_status_t check_op_args(disco_plan_t plan, const DeviceOp& op, bool transpo
 }
 
 disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
-                      const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream, int32_t algo) {
-    disco_status_t s = check_op_args(plan, op, transpose, x, w, y, algo);
+                      const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream, int32_t algo,
+                      bool depthwise) {
+    disco_status_t s = depthwise ? check_dw_args(plan, op, x, w, y) : check_op_args(plan, op, transpose, x, w, y, algo);
     if (s != DISCO_OK) return s;
-    const int64_t B = x->shape[0], Ci = x->shape[1], Co = y->shape[1];
+    int64_t B = x->shape[0], Ci = x->shape[1], Co = y->shape[1];
     if (B == 0) return ok();
-    const OpGeom& g = op.g;
-    const bool axisym = op.basis == DISCO_BASIS_AXISYMMETRIC_4;
+    // Folded-weight stencil kernels: every basis but the 3x3 grid, and
+    // depthwise calls (B * C one-channel items, item i filtered by w[i mod C]).
+    const bool axisym = op.basis != DISCO_BASIS_BILINEAR_3X3 || depthwise;
 
     ExecArgs a{};
     a.op = &op; a.x = x->data; a.w = w->data; a.y = y->data; a.dtype = x->dtype;
+    if (depthwise) {
+        a.dw_c = (int)Ci;
+        B *= Ci;
+        Ci = Co = 1;
+        algo = DISCO_ALGO_AUTO;
+    }
     a.B = (int)B; a.Ci = (int)Ci; a.Co = (int)Co; a.w_trans = transpose; a.stream = stream;
 
     const Dispatch dp = dispatch(op, algo, (int)Ci, (int)Co, x->dtype);
     algo = dp.algo;
     const bool spectral = dp.spectral, sweep = dp.sweep;
-    const PackedDev& packed = *dp.packed;
+    const PackedDev& packed = axisym ? op.packed : *dp.packed;
     // One output channel on a stride-1 op takes the blocked stencil kernel.
     const bool blocked = axisym && op.stencil.P.n_items > 0 && Co == 1;
     size_t ws_spec = 0, ws = 0;
@@ -881,7 +936,7 @@ disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t a
     ea.B = 1;
     ea.Ci = c_in;
     ea.Co = c_out;
-    if (op.basis == DISCO_BASIS_AXISYMMETRIC_4) {
+    if (op.basis != DISCO_BASIS_BILINEAR_3X3) {
         if (dp.algo != DISCO_ALGO_GATHER_THEN_CONTRACT && dp.algo != DISCO_ALGO_CONTRACT_THEN_GATHER) {
             // Folded psi: one value per (output pixel, input pixel) pair.
             const Work fw{all.out_pixels, all.in_pixels, op.n_entries * op.g.nq};
@@ -953,6 +1008,16 @@ disco_status_t disco_transpose_backward(disco_plan_t plan, const disco_tensor_t*
     return backward(plan, true, x, w, dy, dx, dw, stream);
 }
 
+disco_status_t disco_forward_depthwise(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                                       disco_tensor_t* y, hipStream_t stream) {
+    return run(plan, x, w, y, stream, DISCO_ALGO_AUTO, false, true);
+}
+
+disco_status_t disco_transpose_depthwise(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                                         disco_tensor_t* y, hipStream_t stream) {
+    return run(plan, x, w, y, stream, DISCO_ALGO_AUTO, true, true);
+}
+
 disco_status_t disco_forward_algo(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
                                   disco_tensor_t* y, hipStream_t stream, int32_t algo) {
     return run(plan, x, w, y, stream, algo, false);
@@ -986,13 +1051,25 @@ disco_status_t disco_psi_entries(int nlat_in, int nlon_in, int nlat_out, int nlo
     if (capacity < n) return ok();
     if (!out_ring || !phase || !in_ring || !offset || !values)
         return fail(DISCO_ERR_INVALID_ARGUMENT, "output array is NULL");
+    const bool sep = p.basis == DISCO_BASIS_SEPARABLE_4X4;
+    const int row = sep ? kSeparableBasis : kBasis;
+    const CellMap cm = cell_map(p.basis);
     for (int pat = 0; pat < op.g.n_patterns(); ++pat)
         for (int32_t e = op.pat_ptr[(size_t)pat]; e < op.pat_ptr[(size_t)pat + 1]; ++e) {
             out_ring[e] = pat / op.g.P;
             phase[e] = pat % op.g.P;
             in_ring[e] = op.t_in[(size_t)e];
             offset[e] = op.d[(size_t)e];
-            std::memcpy(values + (size_t)e * kBasis, &op.val[(size_t)e * kBasis], sizeof(float) * kBasis);
+            float* out = values + (size_t)e * row;
+            if (!sep) {
+                std::memcpy(out, &op.val[(size_t)e * kBasis], sizeof(float) * kBasis);
+                continue;
+            }
+            // The separable op stores its cell's four values: spread them.
+            for (int k = 0; k < row; ++k) out[k] = 0.0f;
+            const int c = op.cell[(size_t)e];
+            for (int m = 0; m < 4; ++m)
+                if (cm.k[c][m] >= 0) out[cm.k[c][m]] = op.val[(size_t)e * kBasis + m];
         }
     return ok();
 }

@@ -10,10 +10,13 @@
 
 namespace disco {
 
-// Values stored per psi entry: the nine functions of the 3x3 basis, or the
-// four of the axisymmetric basis followed by zeros.
+// Values stored per psi entry: the nine functions of the 3x3 basis, the four
+// of the axisymmetric basis followed by zeros, or, for the separable basis,
+// the (at most four) functions of the entry's cell (CellMap order) followed
+// by zeros.
 constexpr int kBasis = 9;
 constexpr int kAxisymBasis = 4;
+constexpr int kSeparableBasis = 16;
 
 // Parameters of a plan: the forward op maps the in-grid to the out-grid.
 struct PlanParams {
@@ -27,7 +30,7 @@ struct PlanParams {
 };
 
 // Basis size K of a DISCO_BASIS_* kind.
-inline int basis_size(int basis) { return basis == 1 ? kAxisymBasis : kBasis; }
+inline int basis_size(int basis) { return basis == 1 ? kAxisymBasis : basis == 2 ? kSeparableBasis : kBasis; }
 
 // Longitude structure of one op (forward or transposed) as a gather:
 // output pixel p_o = P * q + r (q in [0, nq), phase r in [0, P)) reads input
@@ -51,13 +54,30 @@ struct HostOp {
     std::vector<int32_t> t_in;     // per entry: input ring
     std::vector<int32_t> d;        // per entry: offset in [0, nlon_i)
     std::vector<int32_t> d_raw;    // per entry: unwrapped offset (contiguous along a window)
-    std::vector<uint8_t> cell;     // per entry: hat cell 4 * cu + cv, cu, cv in [0, 4) (3x3 basis; 0 otherwise)
-    std::vector<float> val;        // per entry: 9 values, psi_k * q(input ring) (axisymmetric: k < 4, then zeros)
+    std::vector<uint8_t> cell;     // per entry: hat cell (CellMap), 0 for the axisymmetric basis
+    std::vector<float> val;        // per entry: 9 values times q(input ring): psi_0..8 (3x3), psi_0..3 then
+                                   // zeros (axisymmetric), the cell's values then zeros (separable)
     std::vector<double> val64;     // the same values before rounding to fp32
     int32_t max_window = 0;
     int32_t full_ring_windows = 0;
     int64_t nnz_pairs = 0;  // non-zero (output pixel, input pixel, k) triples
 };
+
+// Hat cells.  Every basis is a sum of products of hats, so the support
+// splits into cells on which at most four basis functions are non-zero:
+//   3x3 grid: cell 4 cu + cv covers [(cu - 2) h, (cu - 1) h) x [(cv - 2) h,
+//     (cv - 1) h) of the tangent plane, with nodes a in {cu - 1, cu} and b in
+//     {cv - 1, cv} (those inside 0..2), listed a-major;
+//   axisymmetric: one cell holding all four functions;
+//   separable: cell 4 a + b is Theta in [a h, (a + 1) h) and direction in
+//     [b pi / 2, (b + 1) pi / 2), with functions 4 a' + b' for a' in {a, a + 1}
+//     (a' <= 3) and b' in {b, (b + 1) mod 4}, listed a'-major.
+// k[c][m] is the basis function of value m of an entry in cell c (-1: none).
+struct CellMap { int8_t k[16][4]; };
+CellMap cell_map(int basis);
+// The cell of entry e and its values in CellMap order (zeros where k < 0).
+// Returns false if the entry has a non-zero value outside its cell.
+bool entry_cell_values(const HostOp& op, int64_t e, int* cell, float v[4]);
 
 // Algorithmic work of a set of an op's patterns, per batch item and channel:
 // output pixels written, distinct input pixels read, non-zero (output pixel,
@@ -143,7 +163,8 @@ struct SChunk { int32_t piece_begin, piece_end, ent_begin, ent_end; };
 struct StencilHost {
     std::vector<SPiece> pieces;
     std::vector<SChunk> chunks;
-    std::vector<PVal> vals;             // per padded entry: psi_0..3 * q (zeros for padding)
+    std::vector<PVal> vals;             // per padded entry: its cell's values times q (zeros for padding)
+    std::vector<uint8_t> cells;         // per padded entry: its cell (CellMap)
     std::vector<PSeg> segs;             // chunk_begin / chunk_end index chunks
     std::vector<PItem> items;
     std::vector<int32_t> red_pattern, red_ptr, red_slots;
@@ -257,6 +278,7 @@ struct StencilDev {
     SPiece* pieces = nullptr;
     SChunk* chunks = nullptr;
     PVal* vals = nullptr;
+    uint8_t* cells = nullptr;
     PackedDev P;                        // segs, items and the reduction tables (no spans)
     int64_t n_padded = 0;
     int64_t bytes = 0;
@@ -273,12 +295,13 @@ static_assert(sizeof(DevEntry) == 48, "DevEntry is 12 dwords");
 
 struct DeviceOp {
     OpGeom g{};
-    int basis = 0;           // DISCO_BASIS_*: the axisymmetric basis runs only launch_stencil
+    int basis = 0;           // DISCO_BASIS_*: bases other than the 3x3 grid run only the stencil kernels
+    int8_t* cmap_dev = nullptr;  // device copy of cell_map(basis), 64 bytes
     PackedDev packed;        // every pattern through the direct kernel
     PackedDev packed_light;  // patterns not handled by the spectral path
     SpectralDev spectral;
     SweepDev sweep;          // light patterns walked by the sweep kernel (Ci <= kCIC)
-    StencilDev stencil;      // axisymmetric basis, longitude stride 1: the blocked layout
+    StencilDev stencil;      // longitude stride 1: the blocked layout of the stencil kernels
     PackedDev packed_rest;   // light patterns the sweep runs do not cover
     int32_t* rest_pats = nullptr;  // device: those patterns' indices (gather-then-contract schedule)
     int32_t n_rest_pats = 0;
@@ -304,6 +327,10 @@ struct ExecArgs {
     int B, Ci, Co;   // op's input / output channels
     bool w_trans;    // W is [Ci][Co][9] (transposed op) instead of [Co][Ci][9]
     hipStream_t stream;
+    // Depthwise channels (stencil kernels only): x and y are viewed as B * C
+    // one-channel items (B above is then B * C, Ci = Co = 1) and item i takes
+    // the filter W[i mod dw_c][.] of a [C][K] weight tensor; 0 = full W.
+    int dw_c = 0;
 };
 
 // Kernel timing hook: when enabled, brackets a launch with events on `s`.
@@ -333,9 +360,10 @@ hipError_t launch_sweep(const ExecArgs& a);
 size_t workspace_bytes_spectral(const ExecArgs& a);
 // Sums the partial outputs of split patterns (the fused and stencil kernels' slots).
 hipError_t launch_reduce_partials(const ExecArgs& a, const PackedDev& P, const float* partial);
-// Axisymmetric basis (disco_stencil.hip): W folded into the packed psi values
-// per call, one scalar weight per entry and channel pair, gathered directly
-// into y.  Workspace as launch_fused.
+// Folded-weight kernels (disco_stencil.hip), every basis: W folded into the
+// packed psi values per call (through the op's CellMap), one scalar weight per
+// entry and channel pair, gathered directly into y.  Workspace as
+// launch_fused.
 hipError_t launch_stencil(const ExecArgs& a, const PackedDev& P, float* partial_ws);
 // The blocked kernel (one output channel, longitude stride 1); workspace
 // sizeof(float) * n_slots * B * nq.

@@ -23,6 +23,60 @@ struct Piece {
 
 }  // namespace
 
+CellMap cell_map(int basis) {
+    CellMap m;
+    for (int c = 0; c < kCells; ++c)
+        for (int j = 0; j < 4; ++j) m.k[c][j] = -1;
+    if (basis == DISCO_BASIS_AXISYMMETRIC_4) {
+        for (int j = 0; j < kAxisymBasis; ++j) m.k[0][j] = (int8_t)j;
+    } else if (basis == DISCO_BASIS_SEPARABLE_4X4) {
+        for (int a = 0; a < 4; ++a)
+            for (int b = 0; b < 4; ++b)
+                for (int i = 0; i < 2; ++i)
+                    for (int j = 0; j < 2; ++j)
+                        if (a + i <= 3) m.k[4 * a + b][2 * i + j] = (int8_t)(4 * (a + i) + (b + j) % 4);
+    } else {
+        for (int cu = 0; cu < 4; ++cu)
+            for (int cv = 0; cv < 4; ++cv) {
+                int n = 0;
+                for (int a = cell_first(cu); a < cell_first(cu) + cell_count(cu); ++a)
+                    for (int b = cell_first(cv); b < cell_first(cv) + cell_count(cv); ++b)
+                        m.k[4 * cu + cv][n++] = (int8_t)(3 * a + b);
+            }
+    }
+    return m;
+}
+
+bool entry_cell_values(const HostOp& op, int64_t e, int* cell, float v[4]) {
+    const float* v9 = &op.val[(size_t)e * kBasis];
+    for (int j = 0; j < 4; ++j) v[j] = 0.0f;
+    if (op.basis == DISCO_BASIS_AXISYMMETRIC_4) {
+        *cell = 0;
+        for (int j = 0; j < kAxisymBasis; ++j) v[j] = v9[j];
+        return true;
+    }
+    *cell = op.cell[(size_t)e];
+    if (op.basis == DISCO_BASIS_SEPARABLE_4X4) {
+        for (int j = 0; j < 4; ++j) v[j] = v9[j];
+        for (int j = 4; j < kBasis; ++j)
+            if (v9[j] != 0.0f) return false;
+        return true;
+    }
+    const CellMap m = cell_map(op.basis);
+    float rest[kBasis];
+    for (int k = 0; k < kBasis; ++k) rest[k] = v9[k];
+    for (int j = 0; j < 4; ++j) {
+        const int k = m.k[*cell][j];
+        if (k >= 0) {
+            v[j] = v9[k];
+            rest[k] = 0.0f;
+        }
+    }
+    for (int k = 0; k < kBasis; ++k)
+        if (rest[k] != 0.0f) return false;
+    return true;
+}
+
 int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& skip, PackedHost* out,
             std::string* err) {
     const OpGeom& g = op.g;
@@ -79,29 +133,13 @@ int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& sk
                 const Piece& pc = pieces[(size_t)i];
                 PSpan sp{pc.ti * g.nlon_i, pc.d_first, halo + pc.d_last - pc.d_first + 1, lds};
                 for (int32_t e = pc.e_begin; e < pc.e_end; ++e) {
-                    const int cell = op.cell[(size_t)e];
-                    const int cu = cell / 4, cv = cell % 4;
                     PEntry E{};
                     E.off = lds + (op.d_raw[(size_t)e] - pc.d_first);
-                    int n = 0;
-                    const float* v9 = &op.val[(size_t)e * kBasis];
-                    if (op.basis == DISCO_BASIS_AXISYMMETRIC_4) {
-                        // All four values (one hat cell): the stencil kernel folds W into them.
-                        for (int k = 0; k < kAxisymBasis; ++k) E.v[k] = v9[k];
-                        ents.push_back({0, E});
-                        continue;
+                    int cell = 0;
+                    if (!entry_cell_values(op, e, &cell, E.v)) {
+                        if (err) *err = "internal: basis value outside its hat cell";
+                        return DISCO_ERR_DEVICE;
                     }
-                    for (int a = 0; a < 3; ++a)
-                        for (int b = 0; b < 3; ++b) {
-                            const bool in_cell = a >= cell_first(cu) && a < cell_first(cu) + cell_count(cu) &&
-                                                 b >= cell_first(cv) && b < cell_first(cv) + cell_count(cv);
-                            if (in_cell) {
-                                E.v[n++] = v9[3 * a + b];
-                            } else if (v9[3 * a + b] != 0.0f) {
-                                if (err) *err = "internal: basis value outside its hat cell";
-                                return DISCO_ERR_DEVICE;
-                            }
-                        }
                     ents.push_back({cell, E});
                 }
                 lds += sp.len;
@@ -361,6 +399,7 @@ int pack_stencil(const HostOp& op, int target_entries, StencilHost* out, std::st
     struct Run {
         int32_t ti, d_first, d_last;
         std::vector<PVal> v;
+        std::vector<uint8_t> c;
     };
     for (int pat = 0; pat < g.n_patterns(); ++pat) {
         const int32_t e0 = op.pat_ptr[(size_t)pat], e1 = op.pat_ptr[(size_t)pat + 1];
@@ -370,19 +409,30 @@ int pack_stencil(const HostOp& op, int target_entries, StencilHost* out, std::st
         for (int32_t e = e0; e < e1; ++e) {
             const int32_t ti = op.t_in[(size_t)e], dr = op.d_raw[(size_t)e];
             PVal pv{};
-            for (int k = 0; k < kAxisymBasis; ++k) pv.v[k] = op.val[(size_t)e * kBasis + k];
+            int cell = 0;
+            if (!entry_cell_values(op, e, &cell, pv.v)) {
+                if (err) *err = "internal: basis value outside its hat cell";
+                return DISCO_ERR_DEVICE;
+            }
             if (!runs.empty() && runs.back().ti == ti && dr > runs.back().d_last &&
                 dr - runs.back().d_last <= 4 && dr - runs.back().d_first + 1 <= kStencilMaxRun) {
                 Run& r = runs.back();
-                for (int32_t gap = r.d_last + 1; gap < dr; ++gap) r.v.push_back(PVal{});
+                for (int32_t gap = r.d_last + 1; gap < dr; ++gap) {
+                    r.v.push_back(PVal{});
+                    r.c.push_back(0);
+                }
                 r.v.push_back(pv);
+                r.c.push_back((uint8_t)cell);
                 r.d_last = dr;
             } else {
-                runs.push_back(Run{ti, dr, dr, {pv}});
+                runs.push_back(Run{ti, dr, dr, {pv}, {(uint8_t)cell}});
             }
         }
         for (Run& r : runs)
-            while (r.v.size() % 4) r.v.push_back(PVal{});
+            while (r.v.size() % 4) {
+                r.v.push_back(PVal{});
+                r.c.push_back(0);
+            }
         // 2. Chunks: runs packed greedily under the LDS column and entry budgets.
         const int32_t chunk_first = (int32_t)H.chunks.size();
         std::vector<int32_t> chunk_entries;
@@ -401,6 +451,7 @@ int pack_stencil(const HostOp& op, int target_entries, StencilHost* out, std::st
             SChunk& C = H.chunks.back();
             H.pieces.push_back(SPiece{runs[i].ti * g.nlon_i, runs[i].d_first, used, ne / 4});
             H.vals.insert(H.vals.end(), runs[i].v.begin(), runs[i].v.end());
+            H.cells.insert(H.cells.end(), runs[i].c.begin(), runs[i].c.end());
             C.piece_end = (int32_t)H.pieces.size();
             C.ent_end = (int32_t)H.vals.size();
             chunk_entries.back() += ne;

@@ -19,7 +19,8 @@
 //   z' = cos(ti - tj) - 2 sin(ti) sin(tj) sin^2(dphi/2)
 // Theta = atan2(|(x', y')|, z'), (u, v) = Theta (x', y') / |(x', y')|
 // (azimuthal equidistant tangent plane: u south, v east); the axisymmetric
-// basis needs Theta only.  Basis values below 1e-12 (rounding noise where a
+// basis needs Theta only, the separable one Theta and the direction
+// Phi = atan2(v, u) (0 south, pi / 2 east; 0 at the centre itself).  Basis values below 1e-12 (rounding noise where a
 // hat is evaluated at its own zero) are set to zero, and entries whose basis
 // values are all zero are dropped.  Values absorb the quadrature weight of the
 // op's input ring (Sec. 4.1: quadrature absorbed into f) and are then rounded
@@ -166,6 +167,7 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
     op->g = g;
     op->basis = p.basis;
     const bool axisym = p.basis == DISCO_BASIS_AXISYMMETRIC_4;
+    const bool separable = p.basis == DISCO_BASIS_SEPARABLE_4X4;
     // Quadrature of the op's input grid: the forward op sums over plan
     // in-grid points; the transposed op over plan out-grid points, its centres.
     const std::vector<double> q = ring_weights(g.nlat_i, g.nlon_i, p.quadrature, p.sampling);
@@ -174,8 +176,8 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
         quad_at_output ? ring_weights(g.nlat_o, g.nlon_o, p.quadrature, p.sampling) : std::vector<double>();
     const double h = p.h;
     // Basis support radius: the 3x3 hats vanish for max(|u|, |v|) >= 2h, the
-    // axisymmetric ones for Theta >= 4h.
-    const double radius = std::min(p.theta_c, axisym ? 4.0 * h : 2.0 * std::sqrt(2.0) * h);
+    // axisymmetric and separable ones for Theta >= 4h.
+    const double radius = std::min(p.theta_c, (axisym || separable) ? 4.0 * h : 2.0 * std::sqrt(2.0) * h);
     const int64_t M = (int64_t)g.nlon_i * g.nlon_o;  // longitude residues per 2 pi
 
     std::vector<double> sin_o(g.nlat_o), cos_o(g.nlat_o), sin_i(g.nlat_i), cos_i(g.nlat_i);
@@ -255,6 +257,45 @@ int build_host_op(const PlanParams& p, bool transpose, HostOp* op, std::string* 
                         op->d.push_back((int32_t)dnorm);
                         op->d_raw.push_back((int32_t)dd);
                         op->cell.push_back(0);
+                        op->val.insert(op->val.end(), vals, vals + kBasis);
+                        op->val64.insert(op->val64.end(), vals64, vals64 + kBasis);
+                        op->nnz_pairs += (int64_t)nzk * g.nq;
+                        ++kept;
+                        continue;
+                    }
+                    if (separable) {
+                        // psi_{4a+b} = hat(Theta / h - a) mu_b(Phi), mu_b the
+                        // periodic hat of width pi / 2 at node b pi / 2 (Sec. 3.4
+                        // with four nodes along theta and phi).  On the cell
+                        // (a, b) with a = floor(Theta / h), b the quadrant of Phi,
+                        // only a, a + 1 (if <= 3) and b, b + 1 (mod 4) fire;
+                        // their four products are stored in that order.
+                        double Phi = 0.0;
+                        if (Th > 1e-12) {
+                            Phi = std::atan2(ys, xs);
+                            if (Phi < 0.0) Phi += 2.0 * kPi;
+                        }
+                        const double sp = Phi / (0.5 * kPi);
+                        const int b = std::min(3, std::max(0, (int)std::floor(sp)));
+                        const int a = std::min(3, std::max(0, (int)std::floor(Th / h)));
+                        const double ta[2] = {hat(Th / h - a), a + 1 <= 3 ? hat(Th / h - (a + 1)) : 0.0};
+                        const double pb[2] = {hat(sp - b), hat(sp - (b + 1))};
+                        for (int k = 0; k < kBasis; ++k) { vals[k] = 0.0f; vals64[k] = 0.0; }
+                        for (int i = 0; i < 2; ++i)
+                            for (int j = 0; j < 2; ++j) {
+                                double psi = ta[i] * pb[j];
+                                if (psi < kPsiFloor) psi = 0.0;
+                                vals64[2 * i + j] = psi * qw;
+                                vals[2 * i + j] = (float)vals64[2 * i + j];
+                                if (psi != 0.0) { any = true; ++nzk; }
+                            }
+                        if (!any) continue;
+                        int64_t dnorm = dd % g.nlon_i;
+                        if (dnorm < 0) dnorm += g.nlon_i;
+                        op->t_in.push_back(ti);
+                        op->d.push_back((int32_t)dnorm);
+                        op->d_raw.push_back((int32_t)dd);
+                        op->cell.push_back((uint8_t)(4 * a + b));
                         op->val.insert(op->val.end(), vals, vals + kBasis);
                         op->val64.insert(op->val64.end(), vals64, vals64 + kBasis);
                         op->nnz_pairs += (int64_t)nzk * g.nq;

@@ -1,13 +1,21 @@
-// disco_stencil.hip -- the DISCO convolution with the axisymmetric basis
-// (Sec. 3.4), W folded into psi per call.
+// disco_stencil.hip -- the DISCO convolution with W folded into psi per call:
+// every call of the axisymmetric and separable bases (Sec. 3.4), and depthwise
+// channels (Sec. 4.2) with any basis.
 //
 // The paper writes the op as one sparse-dense product with
 // Psi_ji = psi(R_j^{-1} w_i) (Sec. 4.1 eq. 7), psi the interpolated filter
 // itself; with learnable node values p_k, psi = sum_k p_k psi_k, so for each
 // (output channel, input channel) pair the stored per-entry basis values fold
-// into one weight, c = sum_k W[co, ci, k] psi_k q.  With K = 4 and few
-// channels (App. B times one channel) that costs one FMA per stored entry and
-// output channel instead of a gather per basis function and a contraction.
+// into one weight, c = sum_k W[co, ci, k] psi_k q.  With few channels (App. B
+// times one channel; depthwise layers filter each channel alone) that costs
+// one FMA per stored entry and output channel instead of a gather per basis
+// function and a contraction.
+//
+// An entry stores the (at most four) basis values of its hat cell; the op's
+// cell map names the basis function of each.  Per input channel the kernels
+// stage a table T[j][cell][m] = W[co0 + j, ci, map[cell][m]] (0 where the map
+// has no function) in LDS, and fold c = sum_m T[j][cell][m] v[m] while an
+// entry is staged.
 //
 // Layout and walk are the packed one of the fused kernel (disco_fused.hip):
 // one workgroup = 256 consecutive output longitudes of one pattern (output
@@ -55,20 +63,44 @@ __device__ __forceinline__ int xcd_remap(int bid, int nb) {
     return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
+// Fills T[j][cell][m] (64 floats per output channel j of the tile) for input
+// channel ci.  dw_c > 0: depthwise, item b takes row b mod dw_c of a [C][K]
+// W (Ci = Co = 1).
+template <typename T, int COT>
+__device__ __forceinline__ void fill_fold_table(float* wt, const int8_t* __restrict__ cmap,
+                                                const T* __restrict__ w, int K, int b, int ci, int co0,
+                                                int Ci, int Co, bool w_trans, int dw_c) {
+    for (int idx = threadIdx.x; idx < COT * kCells * 4; idx += kBlock) {
+        const int j = idx / (kCells * 4), cm = idx - j * (kCells * 4);
+        const int k = cmap[cm];
+        const int co = co0 + j;
+        float v = 0.0f;
+        if (k >= 0 && co < Co) {
+            const int64_t base = dw_c > 0 ? (int64_t)(b % dw_c) * K
+                                 : w_trans ? ((int64_t)ci * Co + co) * K
+                                           : ((int64_t)co * Ci + ci) * K;
+            v = load_val(w, base + k);
+        }
+        wt[idx] = v;
+    }
+}
+
 template <typename T, int COT>
 __global__ __launch_bounds__(kBlock) void k_stencil(const PItem* __restrict__ items,
                                                     const PSeg* __restrict__ segs,
                                                     const PChunk* __restrict__ chunks,
                                                     const PSpan* __restrict__ spans,
                                                     const int32_t* __restrict__ offs,
-                                                    const PVal* __restrict__ vals, OpGeom g,
+                                                    const PVal* __restrict__ vals,
+                                                    const int8_t* __restrict__ cmap, OpGeom g,
                                                     const T* __restrict__ x, const T* __restrict__ w,
                                                     T* __restrict__ y, float* __restrict__ partial,
-                                                    int Ci, int Co, int n_qtiles, int n_cotiles,
-                                                    bool w_trans) {
+                                                    int Ci, int Co, int K, int n_qtiles, int n_cotiles,
+                                                    bool w_trans, int dw_c) {
     __shared__ float xs[kLdsCols];
     __shared__ __align__(16) int eoffs[kChunkEntries];
     __shared__ __align__(16) float ew[kChunkEntries * COT];  // [entry][j]
+    __shared__ __align__(16) float wt[COT * kCells * 4];     // [j][cell][m]
 
     const int tid = threadIdx.x;
     const int bid = xcd_remap(blockIdx.x, gridDim.x);
@@ -89,16 +121,11 @@ __global__ __launch_bounds__(kBlock) void k_stencil(const PItem* __restrict__ it
 #pragma unroll
         for (int j = 0; j < COT; ++j) acc[j] = 0.0f;
         for (int ci = 0; ci < Ci; ++ci) {
-            // W[co0 + j][ci][k] (forward) or W[ci][co0 + j][k] (transposed op).
-            float wk[COT][kAxisymBasis];
-#pragma unroll
-            for (int j = 0; j < COT; ++j) {
-                const int co = co0 + j;
-                const int64_t base = w_trans ? ((int64_t)ci * Co + co) * kAxisymBasis
-                                             : ((int64_t)co * Ci + ci) * kAxisymBasis;
-#pragma unroll
-                for (int k = 0; k < kAxisymBasis; ++k) wk[j][k] = co < Co ? load_val(w, base + k) : 0.0f;
-            }
+            // W[co0 + j][ci][.] (forward) or W[ci][co0 + j][.] (transposed op)
+            // through the cell map.  The previous readers of the table (the
+            // last chunk's staging) are behind that chunk's second barrier;
+            // the next chunk's first barrier orders these writes before use.
+            fill_fold_table<T, COT>(wt, cmap, w, K, b, ci, co0, Ci, Co, w_trans, dw_c);
             const T* xc = x + ((int64_t)b * Ci + ci) * n_in;
             for (int ch = sg.chunk_begin; ch < sg.chunk_end; ++ch) {
                 const PChunk C = chunks[ch];
@@ -117,10 +144,15 @@ __global__ __launch_bounds__(kBlock) void k_stencil(const PItem* __restrict__ it
                 for (int i = tid; i < ne; i += kBlock) {
                     eoffs[i] = offs[ebase + i];
                     const PVal pv = vals[ebase + i];
+                    // Entries are sorted by cell: cls[c] is the first of cell c.
+                    int cell = 0;
 #pragma unroll
-                    for (int j = 0; j < COT; ++j)
-                        ew[i * COT + j] = wk[j][0] * pv.v[0] + wk[j][1] * pv.v[1] + wk[j][2] * pv.v[2] +
-                                          wk[j][3] * pv.v[3];
+                    for (int c = 1; c < kCells; ++c) cell += ebase + i >= C.cls[c] ? 1 : 0;
+#pragma unroll
+                    for (int j = 0; j < COT; ++j) {
+                        const float4 t = *(const float4*)(wt + (j * kCells + cell) * 4);
+                        ew[i * COT + j] = t.x * pv.v[0] + t.y * pv.v[1] + t.z * pv.v[2] + t.w * pv.v[3];
+                    }
                 }
                 __syncthreads();
                 int e = 0;
@@ -170,8 +202,8 @@ hipError_t stencil_launch(const ExecArgs& a, const PackedDev& P, float* partial)
     dim3 grid((unsigned)(P.n_items * n_qtiles), (unsigned)(a.B * n_cot));
     const int tk = timing_begin("stencil", a.stream);
     hipLaunchKernelGGL((k_stencil<T, COT>), grid, dim3(kBlock), 0, a.stream, P.items, P.segs, P.chunks,
-                       P.spans, P.offs, P.vals, g, (const T*)a.x, (const T*)a.w, (T*)a.y, partial, a.Ci,
-                       a.Co, n_qtiles, n_cot, a.w_trans);
+                       P.spans, P.offs, P.vals, a.op->cmap_dev, g, (const T*)a.x, (const T*)a.w, (T*)a.y,
+                       partial, a.Ci, a.Co, basis_size(a.op->basis), n_qtiles, n_cot, a.w_trans, a.dw_c);
     timing_end(tk, a.stream);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -202,13 +234,16 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
                                                             const PSeg* __restrict__ segs,
                                                             const SChunk* __restrict__ chunks,
                                                             const SPiece* __restrict__ pieces,
-                                                            const PVal* __restrict__ vals, OpGeom g,
+                                                            const PVal* __restrict__ vals,
+                                                            const uint8_t* __restrict__ cells,
+                                                            const int8_t* __restrict__ cmap, OpGeom g,
                                                             const T* __restrict__ x,
                                                             const T* __restrict__ w, T* __restrict__ y,
-                                                            float* __restrict__ partial, int Ci,
-                                                            int n_qtiles) {
+                                                            float* __restrict__ partial, int Ci, int K,
+                                                            int n_qtiles, int dw_c) {
     __shared__ float4 xs4[kStencilCols / 4];
     __shared__ float4 ew4[kStencilEntries / 4 + 1];
+    __shared__ float4 wt4[kCells];  // [cell][m]
     float* xs = (float*)xs4;
     float* ew = (float*)ew4;
 
@@ -226,12 +261,9 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
         const PSeg sg = segs[si];
         float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
         for (int ci = 0; ci < Ci; ++ci) {
-            // One output channel: W[0][ci][k] and the transposed op's
-            // W[ci][0][k] are the same element.
-            const float w0 = load_val(w, (int64_t)ci * kAxisymBasis + 0);
-            const float w1 = load_val(w, (int64_t)ci * kAxisymBasis + 1);
-            const float w2 = load_val(w, (int64_t)ci * kAxisymBasis + 2);
-            const float w3 = load_val(w, (int64_t)ci * kAxisymBasis + 3);
+            // One output channel: W[0][ci][.] and the transposed op's
+            // W[ci][0][.] are the same row (ordered as k_stencil's table).
+            fill_fold_table<T, 1>((float*)wt4, cmap, w, K, b, ci, 0, Ci, 1, false, dw_c);
             const T* xc = x + ((int64_t)b * Ci + ci) * n_in;
             for (int ch = sg.chunk_begin; ch < sg.chunk_end; ++ch) {
                 const SChunk C = chunks[ch];
@@ -274,10 +306,15 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
                 }
                 const int ne = C.ent_end - C.ent_begin;
                 PVal pv[kEntriesPerThread];
+                int pc[kEntriesPerThread];
 #pragma unroll
                 for (int u = 0; u < kEntriesPerThread; ++u) {
                     const int i = tid + u * kBlock;
-                    if (i < ne) pv[u] = vals[C.ent_begin + i];
+                    pc[u] = 0;
+                    if (i < ne) {
+                        pv[u] = vals[C.ent_begin + i];
+                        pc[u] = cells[C.ent_begin + i];
+                    }
                 }
                 __syncthreads();  // readers of the previous chunk (or channel) are done
 #pragma unroll
@@ -288,8 +325,10 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
 #pragma unroll
                 for (int u = 0; u < kEntriesPerThread; ++u) {
                     const int i = tid + u * kBlock;
-                    if (i < ne)
-                        ew[i] = w0 * pv[u].v[0] + w1 * pv[u].v[1] + w2 * pv[u].v[2] + w3 * pv[u].v[3];
+                    if (i < ne) {
+                        const float4 t = wt4[pc[u]];
+                        ew[i] = t.x * pv[u].v[0] + t.y * pv[u].v[1] + t.z * pv[u].v[2] + t.w * pv[u].v[3];
+                    }
                 }
                 __syncthreads();
                 int cb = 0;  // the piece's first weight block
@@ -341,7 +380,8 @@ hipError_t stencil_blocked_launch(const ExecArgs& a, const StencilDev& S, float*
     dim3 grid((unsigned)(S.P.n_items * n_qtiles), (unsigned)a.B);
     const int tk = timing_begin("stencil_blocked", a.stream);
     hipLaunchKernelGGL((k_stencil_blocked<T>), grid, dim3(kBlock), 0, a.stream, S.P.items, S.P.segs, S.chunks,
-                       S.pieces, S.vals, g, (const T*)a.x, (const T*)a.w, (T*)a.y, partial, a.Ci, n_qtiles);
+                       S.pieces, S.vals, S.cells, a.op->cmap_dev, g, (const T*)a.x, (const T*)a.w, (T*)a.y,
+                       partial, a.Ci, basis_size(a.op->basis), n_qtiles, a.dw_c);
     timing_end(tk, a.stream);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

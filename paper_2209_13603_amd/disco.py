@@ -27,12 +27,15 @@ DISCO_BFLOAT16 = 1
 
 DISCO_BASIS_BILINEAR_3X3 = 0
 DISCO_BASIS_AXISYMMETRIC_4 = 1
+DISCO_BASIS_SEPARABLE_4X4 = 2
 DISCO_QUAD_FEJER1 = 0
 DISCO_QUAD_SAMPLING_THEOREM = 0
 DISCO_QUAD_CELL_AREA = 1
 DISCO_SAMPLING_CELL_CENTRED = 0
 DISCO_SAMPLING_POLES = 1
-BASES = {"bilinear3x3": DISCO_BASIS_BILINEAR_3X3, "axisym4": DISCO_BASIS_AXISYMMETRIC_4}
+BASES = {"bilinear3x3": DISCO_BASIS_BILINEAR_3X3, "axisym4": DISCO_BASIS_AXISYMMETRIC_4,
+         "separable4x4": DISCO_BASIS_SEPARABLE_4X4}
+BASIS_SIZE = {DISCO_BASIS_BILINEAR_3X3: 9, DISCO_BASIS_AXISYMMETRIC_4: 4, DISCO_BASIS_SEPARABLE_4X4: 16}
 SAMPLINGS = {"cell_centred": DISCO_SAMPLING_CELL_CENTRED, "poles": DISCO_SAMPLING_POLES}
 DISCO_PLAN_BACKWARD = 1
 
@@ -48,7 +51,8 @@ ALGOS = {"auto": ALGO_AUTO, "gather_then_contract": ALGO_GATHER_THEN_CONTRACT,
 # Every exported symbol declared in include/disco.h.
 EXPORTS = ("disco_plan_create", "disco_plan_destroy", "disco_plan_query", "disco_forward",
            "disco_transpose", "disco_forward_algo", "disco_transpose_algo", "disco_forward_backward",
-           "disco_transpose_backward", "disco_psi_entries",
+           "disco_transpose_backward", "disco_forward_depthwise", "disco_transpose_depthwise",
+           "disco_psi_entries",
            "disco_kernel_timing_enable", "disco_kernel_timing_read", "disco_kernel_work",
            "disco_status_string", "disco_last_error")
 
@@ -111,7 +115,7 @@ def library(path: str = LIB_PATH) -> ctypes.CDLL:
                                                            P(ctypes.c_void_p)]
     lib.disco_plan_destroy.argtypes = [ctypes.c_void_p]
     lib.disco_plan_query.argtypes = [ctypes.c_void_p, P(PlanInfo)]
-    for name in ("disco_forward", "disco_transpose"):
+    for name in ("disco_forward", "disco_transpose", "disco_forward_depthwise", "disco_transpose_depthwise"):
         getattr(lib, name).argtypes = [ctypes.c_void_p, P(Tensor), P(Tensor), P(Tensor),
                                        ctypes.c_void_p]
     for name in ("disco_forward_algo", "disco_transpose_algo"):
@@ -127,7 +131,7 @@ def library(path: str = LIB_PATH) -> ctypes.CDLL:
                                          P(ctypes.c_int32)])
     for name in ("disco_plan_create", "disco_plan_destroy", "disco_plan_query", "disco_forward",
                  "disco_transpose", "disco_forward_algo", "disco_transpose_algo",
-                 "disco_psi_entries"):
+                 "disco_forward_depthwise", "disco_transpose_depthwise", "disco_psi_entries"):
         getattr(lib, name).restype = ctypes.c_int
     lib.disco_kernel_timing_enable.argtypes = [ctypes.c_int32]
     lib.disco_kernel_timing_enable.restype = ctypes.c_int
@@ -261,6 +265,26 @@ class Plan:
                             device=x.device)
         return self._run("disco_transpose_algo", x, w, y, algo, stream)
 
+    def _run_dw(self, fn, x, w, y, stream):
+        tx, tw, ty = _tensor(x), _tensor(w), _tensor(y)
+        _check(getattr(library(), fn)(self._h, ctypes.byref(tx), ctypes.byref(tw), ctypes.byref(ty),
+                                      _stream(stream)))
+        return y
+
+    def forward_depthwise(self, x, w, y=None, stream=None):
+        """Depthwise forward op: y[B, C, out-grid], channel c = x[:, c] filtered by w[c] (w [C, K])."""
+        if y is None:
+            import torch
+            y = torch.empty((x.shape[0], x.shape[1]) + self.grid_out, dtype=x.dtype, device=x.device)
+        return self._run_dw("disco_forward_depthwise", x, w, y, stream)
+
+    def transpose_depthwise(self, x, w, y=None, stream=None):
+        """Depthwise transposed op: x[B, C, out-grid] -> y[B, C, in-grid], w [C, K]."""
+        if y is None:
+            import torch
+            y = torch.empty((x.shape[0], x.shape[1]) + self.grid_in, dtype=x.dtype, device=x.device)
+        return self._run_dw("disco_transpose_depthwise", x, w, y, stream)
+
 
 def _backward(plan, fn, x, w, dy, dx, dw, stream):
     tx = _tensor(x) if x is not None else None
@@ -332,7 +356,7 @@ def psi_entries(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, transpose=False, 
                                  ctypes.byref(stride)))
     n = count.value
     arrs = {k: np.zeros(n, dtype=np.int32) for k in ("out_ring", "phase", "in_ring", "offset")}
-    vals = np.zeros((n, 9), dtype=np.float32)
+    vals = np.zeros((n, 16 if basis == DISCO_BASIS_SEPARABLE_4X4 else 9), dtype=np.float32)
     ip = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
     _check(lib.disco_psi_entries(nlat_in, nlon_in, nlat_out, nlon_out, float(theta_c),
                                  ctypes.byref(b), int(transpose), n, ip(arrs["out_ring"]),

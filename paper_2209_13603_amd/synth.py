@@ -19,7 +19,9 @@ Recipe (per workload, one ``numpy.random.default_rng(seed)`` stream, PCG64):
   * the paper's own timed layer (one channel, batch 1, the axisymmetric
     four-node basis, theta_c = 3 pi / L on the pole-including (L + 1) x 2L
     grid, L = 1024, 2048, 4096) takes the same field evaluated on that grid,
-    and w ~ N(0, 1 / 4).
+    and w ~ N(0, 1 / 4);
+  * depthwise workloads (each channel filtered by its own w[c], the
+    depthwise half of a depthwise-separable layer) draw w [C, K] ~ N(0, 1 / K).
 """
 from __future__ import annotations
 
@@ -29,7 +31,8 @@ from dataclasses import dataclass
 import numpy as np
 
 K_BASIS = 9
-BASIS_K = {"bilinear3x3": 9, "axisym4": 4}
+BASIS_K = {"bilinear3x3": 9, "axisym4": 4, "separable4x4": 16}
+BASIS_CODE = {"bilinear3x3": 0, "axisym4": 1, "separable4x4": 2}
 
 
 @dataclass(frozen=True)
@@ -52,8 +55,9 @@ class Workload:
     op: str             # "forward" or "transpose"
     seed: int
     field: str = "normal"  # "normal" or "sh_field"
-    basis: str = "bilinear3x3"     # "bilinear3x3" (K = 9) or "axisym4" (K = 4)
+    basis: str = "bilinear3x3"     # "bilinear3x3" (K = 9), "axisym4" (K = 4) or "separable4x4" (K = 16)
     sampling: str = "cell_centred"  # "cell_centred" or "poles" ((L + 1) x 2L with both poles)
+    channels: str = "full"         # "full" (W [Cout, Cin, K]) or "depthwise" (w [C, K], Cin = Cout = C)
 
     @property
     def K(self) -> int:
@@ -65,8 +69,12 @@ class Workload:
 
     def oracle_kwargs(self) -> dict:
         """The same choice in the oracle's integer codes."""
-        return {"basis": 1 if self.basis == "axisym4" else 0,
+        return {"basis": BASIS_CODE[self.basis],
                 "sampling": 1 if self.sampling == "poles" else 0}
+
+    @property
+    def depthwise(self) -> bool:
+        return self.channels == "depthwise"
 
     @property
     def x_shape(self):
@@ -83,7 +91,9 @@ class Workload:
     @property
     def w_shape(self):
         # forward: W[Cout][Cin][K]; transpose: W[CinT][CoutT][K] (the adjoint
-        # pair shares one buffer).
+        # pair shares one buffer); depthwise: w[C][K].
+        if self.depthwise:
+            return (self.c_in, self.K)
         if self.op == "forward":
             return (self.c_out, self.c_in, self.K)
         return (self.c_in, self.c_out, self.K)
@@ -115,6 +125,15 @@ for _i, _L in enumerate((1024, 2048, 4096)):
     _n = "poles_axisym_L%d" % _L
     WORKLOADS[_n] = Workload(_n, _L + 1, 2 * _L, _L + 1, 2 * _L, 3 * math.pi / _L, 1, 1, 1, "fp32",
                              "forward", 5 + _i, "sh_field", "axisym4", "poles")
+# The separable four-by-four basis with depthwise channels (the filtering half
+# of the paper's depthwise-separable DISCO layers) on the 2048 x 4096 sphere,
+# eight channels, and its transpose on the 2x upsampling of the 256 x 512 grid.
+WORKLOADS["sphere2048x4096_separable_dw"] = Workload(
+    "sphere2048x4096_separable_dw", 2048, 4096, 2048, 4096, 3 * math.pi / 2048, 1, 8, 8, "fp32",
+    "forward", 8, "sh_field", "separable4x4", "cell_centred", "depthwise")
+WORKLOADS["up256x512_to_512x1024_separable_dw"] = Workload(
+    "up256x512_to_512x1024_separable_dw", 512, 1024, 256, 512, 3 * math.pi / 256, 4, 32, 32, "fp32",
+    "transpose", 9, "normal", "separable4x4", "cell_centred", "depthwise")
 
 # The headline workload: forward on the 2048 x 4096 sphere.
 HEADLINE = "sphere2048x4096"
@@ -206,7 +225,8 @@ def make_inputs(wl: Workload, batch: int | None = None):
                 x[b, c] = sh_field(rng, xs[2], xs[3], sampling=wl.sampling)
     else:
         x = rng.standard_normal(xs)
-    w = rng.standard_normal(wl.w_shape) * math.sqrt(1.0 / (wl.c_in * wl.K))
+    fan_in = wl.K if wl.depthwise else wl.c_in * wl.K
+    w = rng.standard_normal(wl.w_shape) * math.sqrt(1.0 / fan_in)
     return to_storage(x, wl.dtype), to_storage(w, wl.dtype)
 
 

@@ -98,7 +98,7 @@ PLAN_CASES = [
 
 def _dense_check(case, transpose, sampling=0, basis=0):
     a, b, c, d = case
-    K = 4 if basis == 1 else 9
+    K = {1: 4, 2: 16}.get(basis, 9)
     # theta_c = 3 pixels of the coarser grid (the pole-including grid has
     # nlat - 1 ring spacings).
     tc = 3 * math.pi / (min(a, c) - (1 if sampling == 1 else 0))
@@ -185,6 +185,43 @@ def test_plan_entries_poles_bilinear_match_dense_psi(case, transpose):
 @pytest.mark.parametrize("case", PLAN_CASES[:3])
 def test_plan_entries_axisym_cell_centred_match_dense_psi(case, transpose):
     _dense_check(case, transpose, sampling=0, basis=1)
+
+
+# The separable basis (Sec. 3.4: four nodes along theta times four periodic
+# nodes along the direction), both grids.
+@pytest.mark.parametrize("transpose", [False, True])
+@pytest.mark.parametrize("case", PLAN_CASES[:4])
+def test_plan_entries_separable_cell_centred_match_dense_psi(case, transpose):
+    _dense_check(case, transpose, sampling=0, basis=2)
+
+
+@pytest.mark.parametrize("transpose", [False, True])
+@pytest.mark.parametrize("case", POLE_CASES[:3])
+def test_plan_entries_separable_poles_match_dense_psi(case, transpose):
+    _dense_check(case, transpose, sampling=1, basis=2)
+
+
+def test_separable_entries_stay_in_their_cell():
+    """Every stored separable entry has at most four non-zero values, on at
+    most two neighbouring theta nodes and two neighbouring (periodic) phi
+    nodes, and its values sum to q times one minus the missing fifth theta
+    node's share (the theta hats are a partition of unity on [0, 3h])."""
+    a, b = 16, 32
+    tc = 3 * math.pi / a
+    ent = disco.psi_entries(a, b, a, b, tc, basis=2)
+    q = oracle.default().quadrature(a, b)
+    v = ent["values"].astype(np.float64).reshape(-1, 4, 4)
+    for e in range(v.shape[0]):
+        nz = np.argwhere(v[e] != 0)
+        assert 1 <= len(nz) <= 4
+        ta = sorted(set(nz[:, 0]))
+        pb = sorted(set(nz[:, 1]))
+        assert len(ta) <= 2 and (len(ta) < 2 or ta[1] == ta[0] + 1)
+        assert len(pb) <= 2 and (len(pb) < 2 or (pb[1] - pb[0]) in (1, 3))
+        s = v[e].sum() / q[int(ent["in_ring"][e])]
+        assert s <= 1.0 + 1e-6
+        if v[e, 3].sum() == 0.0:
+            assert abs(s - 1.0) <= 1e-6
 
 
 def test_pole_grid_validation():

@@ -32,11 +32,13 @@ CASES = [
     (17, 32, 9, 16, "poles", "bilinear3x3"),
     (41, 80, 41, 80, "poles", "axisym4"),
     (17, 32, 9, 16, "poles", "axisym4"),
+    (41, 80, 41, 80, "poles", "separable4x4"),
+    (16, 32, 8, 16, "cell_centred", "separable4x4"),
 ]
 
 
 def _codes(smp, bas):
-    return {"sampling": 1 if smp == "poles" else 0, "basis": 1 if bas == "axisym4" else 0}
+    return {"sampling": 1 if smp == "poles" else 0, "basis": synth.BASIS_CODE[bas]}
 
 
 def _tc(a, c, smp):
@@ -46,7 +48,7 @@ def _tc(a, c, smp):
 def _run(case, transpose, chans, dtype, seed):
     a, b, c, d, smp, bas = case
     tc = _tc(a, c, smp)
-    K = 4 if bas == "axisym4" else 9
+    K = synth.BASIS_K[bas]
     C1, C2 = chans
     # forward: x[B, C1, in], w[C2, C1, K], dy[B, C2, out]
     # transpose: x[B, C1, out], w[C1, C2, K], dy[B, C2, in]
