@@ -44,7 +44,7 @@ DEVICE_KERNEL = {"gather_z": "k_gather_z", "contract_z": "k_contract_z", "contra
 PAPER_SECONDS = {"poles_axisym_L1024": 0.0302, "poles_axisym_L2048": 0.0898,
                  "poles_axisym_L4096": 0.3255}
 # Template argument that tells two schedules' launches of one device function apart.
-KERNEL_VARIANT = {"sweep_gather_contract": ", false>", "sweep_gather_z": ", true>"}
+KERNEL_VARIANT = {"sweep_gather_contract": ", false, ", "sweep_gather_z": ", true, "}
 COPY_PROBE_BYTES = 256 << 20   # per direction, fp32 negation used as the plain copy kernel
 COPY_PROBE_KERNEL = "neg"
 
@@ -92,6 +92,9 @@ def kernel_model(name, wl, work, es):
         f_ = 2.0 * pairs * B * Ci * Co
         bound = "hbm" if b_ / (HBM_PEAK_GBS * 1e9) > f_ / (FP32_VALU_PEAK_TFLOPS * 1e12) else "alu"
         return (b_, f_, bound)
+    if name == "convert_y":
+        # fp32 partial sums read, bf16 output written, per covered pixel.
+        return (B * Co * outp * (4 + es), 0.0, "hbm")
     if name in ("gather_z", "sweep_gather_z"):
         return (B * Ci * inp * es + B * Ci * 9 * outp * 4, 2.0 * pairs * B * Ci, "hbm")
     if name == "contract_z":
@@ -216,19 +219,26 @@ def cpu_baseline(wl, x, w, seconds=15.0):
                       "channels, fp64 ring-window mode" % (n, wl.name, wl.batch, wl.c_out)}
 
 
-def kernel_report(plan, kt, wl, transpose, algo, es):
+def kernel_report(plan, kt, wl, transpose, algo, es, steps):
     """Per-kernel figures of one timed pass and the roofline object of the
     kernel with the largest total time (achieved against HBM peak for
-    HBM-bound kernels, against the fp32 peak otherwise)."""
+    HBM-bound kernels, against the fp32 peak otherwise).  A kernel launched
+    several times per step (the sweep over groups of eight input channels)
+    shares the step's algorithmic work equally between its launches."""
     cin, cout = (1, 1) if wl.depthwise else (wl.c_in, wl.c_out)
     work = plan.kernel_work(transpose, algo, cin, cout, wl.dtype)
     missing = sorted(set(kt) - set(work))
     if missing:
         raise SystemExit("no work figures for kernels %s" % missing)
     per_kernel = {}
+    def model(k):
+        b_, f_, bd = kernel_model(k, wl, work[k], es)
+        per_step = max(1, round(kt[k][0] / steps))
+        return b_ / per_step, f_ / per_step, bd
+
     for k, (launches, tot_ms) in kt.items():
         avg_ms = tot_ms / launches
-        b_, f_, bd = kernel_model(k, wl, work[k], es)
+        b_, f_, bd = model(k)
         per_kernel[k] = {"launches": launches, "avg_us": round(avg_ms * 1e3, 2),
                          "alg_bytes": int(b_), "alg_flops": f_, "bound": bd,
                          "alg_gbs": round(b_ / (avg_ms / 1e3) / 1e9, 1),
@@ -243,7 +253,7 @@ def kernel_report(plan, kt, wl, transpose, algo, es):
     name = max(direct, key=lambda k: kt[k][1])
     launches, tot_ms = kt[name]
     avg_ms = tot_ms / launches
-    bytes_, flops, bound = kernel_model(name, wl, work[name], es)
+    bytes_, flops, bound = model(name)
     if bound == "hbm":
         achieved = bytes_ / (avg_ms / 1e3) / 1e9
         peak, unit = HBM_PEAK_GBS, "GB/s"
@@ -465,7 +475,7 @@ def main(argv=None):
         copy_probe(torch, dev)
 
     transpose = wl.op != "forward"
-    per_kernel, roof = kernel_report(plan, kt, wl, transpose, args.algo, es)
+    per_kernel, roof = kernel_report(plan, kt, wl, transpose, args.algo, es, args.steps)
 
     # The same op through the gather-then-contract schedule, whose kernels
     # move the gathered sums through HBM: their achieved GB/s against the
@@ -492,7 +502,7 @@ def main(argv=None):
         kt2 = disco.kernel_timing_read()
         disco.kernel_timing(False)
         log("gather-then-contract step %.4f ms; kernels: %s" % (ms2, kt2))
-        pk2, roof2 = kernel_report(plan, kt2, wl, transpose, "gather_then_contract", es)
+        pk2, roof2 = kernel_report(plan, kt2, wl, transpose, "gather_then_contract", es, args.steps)
         hbm = {"algo": "gather_then_contract", "ms_per_step": ms2,
                "value": wl.out_pix_chan / (ms2 / 1e3), "kernels": pk2, "roofline": roof2}
     op_bytes = wl.batch * (wl.c_in * (wl.nlat_in * wl.nlon_in if wl.op == "forward" else

@@ -185,13 +185,18 @@ disco_status_t upload_sweep(const SweepHost& H, SweepDev* d) {
     if ((s = upload_vec(H.acts, &d->acts, &d->bytes, "hipMalloc(sweep spans)")) != DISCO_OK) return s;
     if ((s = upload_vec(offs, &d->offs, &d->bytes, "hipMalloc(sweep offsets)")) != DISCO_OK) return s;
     if ((s = upload_vec(vals, &d->vals, &d->bytes, "hipMalloc(sweep values)")) != DISCO_OK) return s;
+    std::vector<int32_t> cov;
+    for (size_t i = 0; i < H.covered.size(); ++i)
+        if (H.covered[i]) cov.push_back((int32_t)i);
+    if ((s = upload_vec(cov, &d->cov_pats, &d->bytes, "hipMalloc(sweep patterns)")) != DISCO_OK) return s;
     d->n_runs = (int32_t)H.runs.size();
     d->n_pats = (int32_t)H.pats.size();
+    d->n_cov = (int32_t)cov.size();
     return DISCO_OK;
 }
 
 void free_sweep(SweepDev* d) {
-    void* ptrs[] = {d->runs, d->pats, d->acts, d->offs, d->vals};
+    void* ptrs[] = {d->runs, d->pats, d->acts, d->offs, d->vals, d->cov_pats};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     *d = SweepDev{};
@@ -405,14 +410,19 @@ Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co, int32_t dtyp
     Dispatch d{algo, false, false, &op.packed, &op.work_all};
     if (op.basis != DISCO_BASIS_BILINEAR_3X3) return d;
     d.spectral = algo == DISCO_ALGO_FUSED && op.spectral.n_rings > 0;
-    // The sweep kernel addresses x and y through 32-bit buffer offsets: all
-    // kCIC input channel planes and one output plane must stay below 2^31
-    // bytes (2048 x 4096 fp32: 268 MB and 34 MB); larger grids take the
-    // general kernel.
+    // The sweep kernel addresses x and y through 32-bit buffer offsets: the
+    // kCIC input channel planes of one launch and one output plane (fp32 when
+    // partial sums accumulate) must stay below 2^31 bytes (2048 x 4096 fp32:
+    // 268 MB and 34 MB); larger grids take the general kernel.  More than
+    // kCIC input channels take one sweep launch per channel group.
     const int64_t es = (int64_t)elem_bytes(dtype);
     const bool sweep_offsets_fit = (int64_t)kCIC * g.nlat_i * g.nlon_i * es < ((int64_t)1 << 31) &&
-                                   (int64_t)g.nlat_o * g.nlon_o * es < ((int64_t)1 << 31);
-    d.sweep = algo == DISCO_ALGO_FUSED && op.sweep.n_runs > 0 && Ci <= kCIC && sweep_offsets_fit;
+                                   (int64_t)g.nlat_o * g.nlon_o * 4 < ((int64_t)1 << 31);
+    // Several channel groups pay off on single-phase ops (measured: 512 x
+    // 1024, 32 -> 32 channels, 0.76 -> 0.65 ms); on ops with longitude
+    // phases (the transposed upsampling op) one sweep launch costs about
+    // what the general kernel's whole channel pass does, so groups lose.
+    d.sweep = algo == DISCO_ALGO_FUSED && op.sweep.n_runs > 0 && sweep_offsets_fit && (Ci <= kCIC || g.P == 1);
     if (d.sweep) {
         d.packed = &op.packed_rest;
         d.packed_work = &op.work_rest;
@@ -546,7 +556,7 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
     const PackedDev& packed = axisym ? op.packed : *dp.packed;
     // One output channel on a stride-1 op takes the blocked stencil kernel.
     const bool blocked = axisym && op.stencil.P.n_items > 0 && Co == 1;
-    size_t ws_spec = 0, ws = 0;
+    size_t ws_spec = 0, ws_sweep = 0, ws = 0;
     if (blocked) {
         ws = workspace_bytes_fused(a, op.stencil.P);
     } else if (axisym) {
@@ -557,7 +567,8 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
         ws = workspace_bytes_gather_then_contract(a);
     } else {
         ws_spec = spectral ? (workspace_bytes_spectral(a) + 255) / 256 * 256 : 0;
-        ws = ws_spec + workspace_bytes_fused(a, packed);
+        ws_sweep = sweep ? (workspace_bytes_sweep(a) + 255) / 256 * 256 : 0;
+        ws = ws_spec + ws_sweep + workspace_bytes_fused(a, packed);
     }
     int cur = 0;
     if (hipGetDevice(&cur) != hipSuccess) return fail(DISCO_ERR_DEVICE, "hipGetDevice failed");
@@ -599,13 +610,14 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
             if (e == hipSuccess) e = hipEventRecord(fork, stream);
             if (e == hipSuccess) e = hipStreamWaitEvent(plan->aux, fork, 0);
             if (e == hipSuccess) e = launch_spectral(as, ws_ptr, kSpectralAll & ~1);
-            if (e == hipSuccess && sweep) e = launch_fused(as, packed, (float*)((char*)ws_ptr + ws_spec));
+            if (e == hipSuccess && sweep) e = launch_fused(as, packed, (float*)((char*)ws_ptr + ws_spec + ws_sweep));
             if (e == hipSuccess) e = hipEventRecord(join, plan->aux);
         } else if (spectral) {
             e = launch_spectral(a, ws_ptr);
         }
-        if (e == hipSuccess && sweep) e = launch_sweep(a);
-        if (e == hipSuccess && !(fork_aux && sweep)) e = launch_fused(a, packed, (float*)((char*)ws_ptr + ws_spec));
+        if (e == hipSuccess && sweep) e = launch_sweep(a, ws_sweep ? (float*)((char*)ws_ptr + ws_spec) : nullptr);
+        if (e == hipSuccess && !(fork_aux && sweep))
+            e = launch_fused(a, packed, (float*)((char*)ws_ptr + ws_spec + ws_sweep));
         if (join) {
             hipError_t ej = hipStreamWaitEvent(stream, join, 0);
             if (e == hipSuccess) e = ej;
@@ -969,6 +981,8 @@ disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t a
             rows.push_back({"spectral_irfft", Work{sw.out_pixels, 0, 0}});
         }
         if (dp.sweep) rows.push_back({"sweep_gather_contract", op.work_sweep});
+        if (dp.sweep && workspace_bytes_sweep(ea) > 0)
+            rows.push_back({"convert_y", Work{op.work_sweep.out_pixels, 0, 0}});
         if (dp.packed->n_items > 0) rows.push_back({"fused_gather_contract", *dp.packed_work});
         if (dp.packed->n_items > 0 && dp.packed->n_split > 0)
             rows.push_back({"reduce_partials", Work{0, 0, 0}});

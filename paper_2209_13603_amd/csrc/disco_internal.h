@@ -220,8 +220,10 @@ struct SweepDev {
     PSpan* acts = nullptr;
     int32_t* offs = nullptr;
     PVal* vals = nullptr;
+    int32_t* cov_pats = nullptr;  // patterns the runs cover (fp32 partial sums converted to bf16)
     int32_t n_runs = 0;
     int32_t n_pats = 0;
+    int32_t n_cov = 0;
     int64_t bytes = 0;
 };
 
@@ -356,7 +358,14 @@ size_t workspace_bytes_fused(const ExecArgs& a, const PackedDev& P);
 // products, bit 2 the inverse transforms (in that order on one stream).
 constexpr int kSpectralAll = 7;
 hipError_t launch_spectral(const ExecArgs& a, float* ws, int stages = kSpectralAll);
-hipError_t launch_sweep(const ExecArgs& a);
+// The sweep takes kCIC input channels per launch: more input channels run
+// one launch per group, the first storing y and the others adding their
+// partial sums into it (fp32 atomic adds, one per element and launch, in
+// launch order).  bf16 outputs accumulate in y32_ws (workspace_bytes_sweep
+// bytes, fp32 [B][Co][pixels]) and are converted for the covered patterns at
+// the end.
+size_t workspace_bytes_sweep(const ExecArgs& a);
+hipError_t launch_sweep(const ExecArgs& a, float* y32_ws);
 size_t workspace_bytes_spectral(const ExecArgs& a);
 // Sums the partial outputs of split patterns (the fused and stencil kernels' slots).
 hipError_t launch_reduce_partials(const ExecArgs& a, const PackedDev& P, const float* partial);

@@ -13,6 +13,13 @@
 // With ZOUT the same walk writes the gathered sums Z[b, c, k, pixel] (fp32)
 // instead of contracting them: the gather half of the gather-then-contract
 // schedule, one launch per group of kCIC input channels.
+//
+// More than kCIC input channels run one contracting launch per group of kCIC
+// channels: the first launch stores y, the later ones add their partial sums
+// with fp32 atomic adds (no return value, one add per element and launch, so
+// the order of the additions is the launch order and the result does not
+// vary between runs).  bf16 outputs accumulate in an fp32 workspace that a
+// last kernel rounds into y for the patterns the runs cover.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -60,6 +67,9 @@ __device__ __forceinline__ void buffer_store_val(float*, __amdgpu_buffer_rsrc_t 
 __device__ __forceinline__ void buffer_store_val(uint16_t*, __amdgpu_buffer_rsrc_t r, int off, float v) {
     __builtin_amdgcn_raw_buffer_store_b16(to_bf16(v), r, off, 0, 0);
 }
+// Output modes of the contracting sweep: store T into y, store fp32 into the
+// partial-sum buffer, or add fp32 into it.
+enum { kStoreY = 0, kStoreF32 = 1, kAddF32 = 2 };
 
 __host__ __device__ constexpr int cell_first(int c) { return c == 0 ? 0 : c - 1; }
 __host__ __device__ constexpr int cell_count(int c) { return (c == 0 || c == 3) ? 1 : 2; }
@@ -176,17 +186,21 @@ __device__ __forceinline__ void mfma_contract_k(v4f (&yacc)[NQ], const float (&w
     }
 }
 
-// grid: (n_runs * n_qtiles, B * n_cotiles); requires Ci <= kCIC.  With ZOUT
+// grid: (n_runs * n_qtiles, B * n_cotiles); the launch reads input channels
+// cg0 .. cg0 + kCIC - 1 (those below Ci; cg0 is 0 with YMODE kStoreY) and
+// writes y by YMODE (y32: the fp32 [B][Co][pixels] partial sums of kStoreF32
+// and kAddF32).  With ZOUT
 // the second grid dimension runs over (batch item, group of kCIC input
 // channels) instead (n_cotiles = number of channel groups) and z receives
 // Z[b, c, k, pixel] for the group's channels; w and y are not used.
-template <typename T, int COT, bool ZOUT>
+template <typename T, int COT, bool ZOUT, int YMODE>
 __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs, const SPat* __restrict__ pats,
                                                   const PSpan* __restrict__ acts, const int32_t* __restrict__ offs,
                                                   const PVal* __restrict__ vals, OpGeom g,
                                                   const T* __restrict__ x, const T* __restrict__ w,
                                                   T* __restrict__ y, float* __restrict__ zout, int Ci, int Co,
-                                                  int n_qtiles, int n_cotiles, bool w_trans) {
+                                                  int n_qtiles, int n_cotiles, bool w_trans, int cg0,
+                                                  float* __restrict__ y32) {
     __shared__ float4 xs[kNCQ * kSweepCols];
     __shared__ float4 evs[kSweepEntries + kEntryPad];
     __shared__ int eoffs[kSweepEntries + kEntryPad];
@@ -197,7 +211,7 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
     const int qt = bid - run * n_qtiles;
     const int b = blockIdx.y / n_cotiles;
     const int co0 = (blockIdx.y - b * n_cotiles) * COT;          // output channel tile
-    const int c0 = ZOUT ? (blockIdx.y - b * n_cotiles) * kCIC : 0;  // input channel group
+    const int c0 = ZOUT ? (blockIdx.y - b * n_cotiles) * kCIC : (YMODE == kStoreY ? 0 : cg0);  // input channel group
     const int q0 = qt * kBlock;
     const int q = q0 + tid;
     const int lane_col = g.stride * tid;
@@ -237,7 +251,7 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
 #pragma unroll
             for (int gg = 0; gg < kWG; ++gg) {
                 const int kk = 16 * gg + blk, co = co0 + 4 * qd + li;
-                const int c = kk / kBasis, k = kk % kBasis;
+                const int c = c0 + kk / kBasis, k = kk % kBasis;
                 float v = 0.0f;
                 if (kk < kKK && co < Co && c < Ci) {
                     const int64_t idx = w_trans ? ((int64_t)c * Co + co) * kBasis + k : ((int64_t)co * Ci + c) * kBasis + k;
@@ -444,45 +458,103 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
         // its wait does not cover the stores.
         if constexpr (ZOUT) continue;
         const int to = pattern / g.P, r = pattern - (pattern / g.P) * g.P;
-        const int pix_off = q < g.nq ? (to * g.nlon_o + q * g.P + r) * (int)sizeof(T) : kBufferOutOfRange;
+        const int pix = to * g.nlon_o + q * g.P + r;
+        if constexpr (YMODE == kStoreY) {
+            const int pix_off = q < g.nq ? pix * (int)sizeof(T) : kBufferOutOfRange;
 #pragma unroll
-        for (int j = 0; j < COT; ++j) {
-            const __amdgpu_buffer_rsrc_t yr =
-                buffer_of(y + ((int64_t)b * Co + co0 + j) * n_out, co0 + j < Co ? out_plane : 0);
-            buffer_store_val(y, yr, pix_off, yacc[j / 4][j % 4]);
+            for (int j = 0; j < COT; ++j) {
+                const __amdgpu_buffer_rsrc_t yr =
+                    buffer_of(y + ((int64_t)b * Co + co0 + j) * n_out, co0 + j < Co ? out_plane : 0);
+                buffer_store_val(y, yr, pix_off, yacc[j / 4][j % 4]);
+            }
+        } else {
+            const int off32 = q < g.nq ? pix * (int)sizeof(float) : kBufferOutOfRange;
+            const int plane32 = (int)(n_out * (int64_t)sizeof(float));
+#pragma unroll
+            for (int j = 0; j < COT; ++j) {
+                const __amdgpu_buffer_rsrc_t yr =
+                    buffer_of(y32 + ((int64_t)b * Co + co0 + j) * n_out, co0 + j < Co ? plane32 : 0);
+                if constexpr (YMODE == kAddF32)
+                    (void)__builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(yacc[j / 4][j % 4], yr, off32, 0, 0);
+                else
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(yacc[j / 4][j % 4]), yr, off32, 0, 0);
+            }
         }
     }
 }
 
+// y32[b][co][pixel] rounded to bf16 into y for the covered patterns.
+// grid: (ceil(nq / 256), n_cov, B * Co).
+__global__ __launch_bounds__(kBlock) void k_convert_y(const int32_t* __restrict__ pats, const float* __restrict__ y32,
+                                                     uint16_t* __restrict__ y, OpGeom g) {
+    const int q = blockIdx.x * kBlock + threadIdx.x;
+    if (q >= g.nq) return;
+    const int pattern = pats[blockIdx.y];
+    const int to = pattern / g.P, r = pattern - to * g.P;
+    const int64_t i = (int64_t)blockIdx.z * g.nlat_o * g.nlon_o + (int64_t)to * g.nlon_o + (int64_t)q * g.P + r;
+    y[i] = to_bf16(y32[i]);
+}
+
 template <typename T, int COT>
-hipError_t sweep_launch(const ExecArgs& a) {
+hipError_t sweep_launch(const ExecArgs& a, float* y32) {
     const OpGeom& g = a.op->g;
     const SweepDev& S = a.op->sweep;
     if (S.n_runs == 0) return hipSuccess;
     const int n_qtiles = (g.nq + kBlock - 1) / kBlock;
     const int n_cot = (a.Co + COT - 1) / COT;
+    const int n_grp = (a.Ci + kCIC - 1) / kCIC;
+    // fp32 outputs accumulate in y itself; bf16 ones in y32.
+    const bool f32 = a.dtype != 1;
+    float* acc = f32 ? (float*)a.y : y32;
+    if (n_grp > 1 && !acc) return hipErrorInvalidValue;
     dim3 grid((unsigned)(S.n_runs * n_qtiles), (unsigned)(a.B * n_cot));
-    int tk = timing_begin("sweep_gather_contract", a.stream);
-    hipLaunchKernelGGL((k_sweep<T, COT, false>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats, S.acts, S.offs,
-                       S.vals, g, (const T*)a.x, (const T*)a.w, (T*)a.y, (float*)nullptr, a.Ci, a.Co, n_qtiles, n_cot,
-                       a.w_trans);
-    timing_end(tk, a.stream);
+    for (int grp = 0; grp < n_grp; ++grp) {
+        const int ymode = grp > 0 ? kAddF32 : (n_grp > 1 && !f32 ? kStoreF32 : kStoreY);
+        const int tk = timing_begin("sweep_gather_contract", a.stream);
+        if (ymode == kStoreY)
+            hipLaunchKernelGGL((k_sweep<T, COT, false, kStoreY>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats,
+                               S.acts, S.offs, S.vals, g, (const T*)a.x, (const T*)a.w, (T*)a.y, (float*)nullptr, a.Ci,
+                               a.Co, n_qtiles, n_cot, a.w_trans, 0, (float*)nullptr);
+        else if (ymode == kStoreF32)
+            hipLaunchKernelGGL((k_sweep<T, COT, false, kStoreF32>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats,
+                               S.acts, S.offs, S.vals, g, (const T*)a.x, (const T*)a.w, (T*)a.y, (float*)nullptr, a.Ci,
+                               a.Co, n_qtiles, n_cot, a.w_trans, grp * kCIC, acc);
+        else
+            hipLaunchKernelGGL((k_sweep<T, COT, false, kAddF32>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats,
+                               S.acts, S.offs, S.vals, g, (const T*)a.x, (const T*)a.w, (T*)a.y, (float*)nullptr, a.Ci,
+                               a.Co, n_qtiles, n_cot, a.w_trans, grp * kCIC, acc);
+        timing_end(tk, a.stream);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (n_grp > 1 && !f32 && S.n_cov > 0) {
+        dim3 g2((unsigned)((g.nq + kBlock - 1) / kBlock), (unsigned)S.n_cov, (unsigned)(a.B * a.Co));
+        const int tk = timing_begin("convert_y", a.stream);
+        hipLaunchKernelGGL(k_convert_y, g2, dim3(kBlock), 0, a.stream, S.cov_pats, (const float*)y32,
+                           (uint16_t*)a.y, g);
+        timing_end(tk, a.stream);
+    }
     return hipGetLastError();
 }
 
 template <typename T>
-hipError_t sweep_dispatch(const ExecArgs& a) {
-    if (a.Co <= 4) return sweep_launch<T, 4>(a);
-    if (a.Co <= 8) return sweep_launch<T, 8>(a);
-    if (a.Co <= 16) return sweep_launch<T, 16>(a);
-    return sweep_launch<T, 32>(a);
+hipError_t sweep_dispatch(const ExecArgs& a, float* y32) {
+    if (a.Co <= 4) return sweep_launch<T, 4>(a, y32);
+    if (a.Co <= 8) return sweep_launch<T, 8>(a, y32);
+    if (a.Co <= 16) return sweep_launch<T, 16>(a, y32);
+    return sweep_launch<T, 32>(a, y32);
 }
 
 }  // namespace
 
-hipError_t launch_sweep(const ExecArgs& a) {
-    if (a.Ci > kCIC) return hipErrorInvalidValue;
-    return a.dtype == 1 ? sweep_dispatch<uint16_t>(a) : sweep_dispatch<float>(a);
+size_t workspace_bytes_sweep(const ExecArgs& a) {
+    if (a.dtype != 1 || a.Ci <= kCIC || a.op->sweep.n_runs == 0) return 0;
+    const OpGeom& g = a.op->g;
+    return sizeof(float) * (size_t)a.B * a.Co * (size_t)g.nlat_o * g.nlon_o;
+}
+
+hipError_t launch_sweep(const ExecArgs& a, float* y32_ws) {
+    return a.dtype == 1 ? sweep_dispatch<uint16_t>(a, y32_ws) : sweep_dispatch<float>(a, y32_ws);
 }
 
 hipError_t launch_sweep_z(const ExecArgs& a, float* z) {
@@ -494,13 +566,13 @@ hipError_t launch_sweep_z(const ExecArgs& a, float* z) {
     dim3 grid((unsigned)(S.n_runs * n_qtiles), (unsigned)(a.B * n_cg));
     const int tk = timing_begin("sweep_gather_z", a.stream);
     if (a.dtype == 1)
-        hipLaunchKernelGGL((k_sweep<uint16_t, 4, true>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats, S.acts,
-                           S.offs, S.vals, g, (const uint16_t*)a.x, (const uint16_t*)nullptr, (uint16_t*)nullptr, z,
-                           a.Ci, a.Co, n_qtiles, n_cg, a.w_trans);
+        hipLaunchKernelGGL((k_sweep<uint16_t, 4, true, kStoreY>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats,
+                           S.acts, S.offs, S.vals, g, (const uint16_t*)a.x, (const uint16_t*)nullptr,
+                           (uint16_t*)nullptr, z, a.Ci, a.Co, n_qtiles, n_cg, a.w_trans, 0, (float*)nullptr);
     else
-        hipLaunchKernelGGL((k_sweep<float, 4, true>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats, S.acts, S.offs,
-                           S.vals, g, (const float*)a.x, (const float*)nullptr, (float*)nullptr, z, a.Ci, a.Co,
-                           n_qtiles, n_cg, a.w_trans);
+        hipLaunchKernelGGL((k_sweep<float, 4, true, kStoreY>), grid, dim3(kBlock), 0, a.stream, S.runs, S.pats, S.acts,
+                           S.offs, S.vals, g, (const float*)a.x, (const float*)nullptr, (float*)nullptr, z, a.Ci, a.Co,
+                           n_qtiles, n_cg, a.w_trans, 0, (float*)nullptr);
     timing_end(tk, a.stream);
     return hipGetLastError();
 }

@@ -190,9 +190,13 @@ def test_kernel_work_covers_the_op(name):
                 if algo == "fused":
                     assert ("spectral_mac" in work) == (info["spectral_rings_transpose" if transpose
                                                               else "spectral_rings_forward"] > 0)
+                    # the sweep takes any channel count on single-phase ops (one
+                    # launch per group of eight), at most eight otherwise
+                    phases = info["phases_transpose" if transpose else "phases_forward"]
                     assert ("sweep_gather_contract" in work) == (
-                        ci <= 8 and info["sweep_patterns_transpose" if transpose
-                                         else "sweep_patterns_forward"] > 0)
+                        info["sweep_patterns_transpose" if transpose else "sweep_patterns_forward"] > 0
+                        and (ci <= 8 or phases == 1))
+                    assert ("convert_y" in work) == ("sweep_gather_contract" in work and ci > 8 and dt == "bf16")
     plan.close()
 
 
