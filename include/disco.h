@@ -240,6 +240,26 @@ disco_status_t disco_transpose_backward(disco_plan_t plan, const disco_tensor_t*
                                         const disco_tensor_t* w, const disco_tensor_t* dy,
                                         disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream);
 
+/* Gradients of the depthwise ops (disco_forward_depthwise and
+ * disco_transpose_depthwise; App. C applied to each channel's one-channel op):
+ *   dx [B, C, op input grid]: dx[b,c] = A_c^T dy[b,c] with A_c the one-channel op of filter W[c],
+ *      the adjoint of the depthwise op (the same as disco_forward_backward's
+ *      dx with the diagonal W'[c][c'][k] = (c == c') W[c][k]);
+ *   dw [C, K]:  dw[c,k] = sum_{b,j} dy[b,c,j] Z[b,c,k](j), Z the gathered sums
+ *      of channel c (the diagonal blocks of the full weight gradient).
+ * x [B, C, op input grid] is the depthwise op's input (read for dw only), w
+ * [C, K] its weights (read for dx only), dy [B, C, op output grid]; dx or dw
+ * may be NULL.  Same conventions as disco_forward_backward (plan created with
+ * DISCO_PLAN_BACKWARD, dw reduced in a fixed order, overwritten, bf16 sums
+ * rounded before the fp32 reduction); B * C <= 65535.  Errors as
+ * disco_forward_backward. */
+disco_status_t disco_forward_depthwise_backward(disco_plan_t plan, const disco_tensor_t* x,
+                                                const disco_tensor_t* w, const disco_tensor_t* dy,
+                                                disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream);
+disco_status_t disco_transpose_depthwise_backward(disco_plan_t plan, const disco_tensor_t* x,
+                                                  const disco_tensor_t* w, const disco_tensor_t* dy,
+                                                  disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream);
+
 /* Host-only export of the stored psi entries of one op, without any device
  * (Sec. 4.1: Psi is constructed explicitly, only where it is non-zero).
  * transpose = 0 selects the forward op, 1 the transposed op.  Each entry is

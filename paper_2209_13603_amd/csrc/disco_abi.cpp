@@ -639,8 +639,11 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
 // sums Z [B * C_x][K][pixels] to a workspace, then reduces dy (x) Z over
 // pixels (disco_grad.hip).  Everything is validated before anything is
 // enqueued.
+// depthwise: w and dw are [C, K] and every channel is its own one-channel op
+// (dx through the adjoint op run depthwise, dW the diagonal blocks only).
 disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t* x, const disco_tensor_t* w,
-                        const disco_tensor_t* dy, disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream) {
+                        const disco_tensor_t* dy, disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream,
+                        bool depthwise = false) {
     if (!plan) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (!(plan->params.flags & DISCO_PLAN_BACKWARD))
         return fail(DISCO_ERR_UNSUPPORTED, "plan was created without DISCO_PLAN_BACKWARD");
@@ -652,20 +655,29 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
     disco_status_t s;
     // Input gradient: dy -> dx through the adjoint op, whose W layout is the
     // other op's.
-    if (dx && (s = check_op_args(plan, adj, !transpose, dy, w, dx, DISCO_ALGO_AUTO)) != DISCO_OK) return s;
+    if (dx) {
+        s = depthwise ? check_dw_args(plan, adj, dy, w, dx) : check_op_args(plan, adj, !transpose, dy, w, dx, DISCO_ALGO_AUTO);
+        if (s != DISCO_OK) return s;
+    }
     // Weight gradient: shapes, then the Z pass's own arguments.
     disco_tensor_t xz{}, wsel{}, zt{};
     int64_t B = 0, C_x = 0, C_dy = 0, P = 0;
     if (dw) {
         if (!x) return fail(DISCO_ERR_INVALID_ARGUMENT, "x is NULL (needed for dw)");
-        if (x->ndim != 4 || dw->ndim != 3 || dy->ndim != 4) return fail(DISCO_ERR_SHAPE, "x and dy must be 4-D, dw 3-D");
+        if (x->ndim != 4 || dw->ndim != (depthwise ? 2 : 3) || dy->ndim != 4)
+            return fail(DISCO_ERR_SHAPE, depthwise ? "x and dy must be 4-D, depthwise dw 2-D" : "x and dy must be 4-D, dw 3-D");
         B = x->shape[0]; C_x = x->shape[1]; C_dy = dy->shape[1];
         if (dy->shape[0] != B) return fail(DISCO_ERR_SHAPE, "x and dy batch differ");
         if (dy->shape[2] != op.g.nlat_o || dy->shape[3] != op.g.nlon_o)
             return fail(DISCO_ERR_SHAPE, "dy grid must be the op's output grid");
-        const int64_t want0 = transpose ? C_x : C_dy, want1 = transpose ? C_dy : C_x;
-        if (dw->shape[0] != want0 || dw->shape[1] != want1 || dw->shape[2] != K)
-            return fail(DISCO_ERR_SHAPE, std::string("dw must be ") + (transpose ? "[CinT, CoutT, K]" : "[Cout, Cin, K]"));
+        if (depthwise) {
+            if (C_dy != C_x) return fail(DISCO_ERR_SHAPE, "depthwise x and dy must have the same channels");
+            if (dw->shape[0] != C_x || dw->shape[1] != K) return fail(DISCO_ERR_SHAPE, "depthwise dw must be [C, K]");
+        } else {
+            const int64_t want0 = transpose ? C_x : C_dy, want1 = transpose ? C_dy : C_x;
+            if (dw->shape[0] != want0 || dw->shape[1] != want1 || dw->shape[2] != K)
+                return fail(DISCO_ERR_SHAPE, std::string("dw must be ") + (transpose ? "[CinT, CoutT, K]" : "[Cout, Cin, K]"));
+        }
         if (dw->dtype != x->dtype || dy->dtype != x->dtype) return fail(DISCO_ERR_DTYPE, "x, dy and dw must share one dtype");
         if (B * C_x > 65535) return fail(DISCO_ERR_SHAPE, "batch x channels too large for the weight gradient");
         P = (int64_t)op.g.nlat_o * op.g.nlon_o;
@@ -701,7 +713,7 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
             if ((s = check_device_ptr(x->data, plan->device, "x")) != DISCO_OK) return s;
         }
     }
-    if (dx && (s = run_op(plan, adj, !transpose, dy, w, dx, stream, DISCO_ALGO_AUTO)) != DISCO_OK) return s;
+    if (dx && (s = run_op(plan, adj, !transpose, dy, w, dx, stream, DISCO_ALGO_AUTO, depthwise)) != DISCO_OK) return s;
     if (!dw || B == 0) return ok();
     int cur = 0;
     if (hipGetDevice(&cur) != hipSuccess) return fail(DISCO_ERR_DEVICE, "hipGetDevice failed");
@@ -717,7 +729,8 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
     za.w_trans = transpose; za.stream = stream;
     const size_t zbytes = ((size_t)(B * C_x) * K * (size_t)P * elem_bytes(x->dtype) + 255) & ~(size_t)255;
     const size_t zws = onepass ? workspace_bytes_gather_z_all(za) : 0;
-    const size_t gbytes = weight_grad_ws_bytes((int)B, (int)C_dy, (int)(C_x * K), P);
+    const size_t gbytes = depthwise ? weight_grad_ws_bytes_dw((int)B, (int)C_x, K, P)
+                                    : weight_grad_ws_bytes((int)B, (int)C_dy, (int)(C_x * K), P);
     void* zbuf = nullptr;
     float* gws = nullptr;
     hipError_t e = hipMallocAsync(&zbuf, zbytes + zws, stream);
@@ -735,8 +748,9 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
         s = run_op(plan, op, transpose, &xz, &wsel, &zt, stream, DISCO_ALGO_AUTO);
     }
     if (s == DISCO_OK) {
-        e = launch_weight_grad(dy->data, zbuf, dw->data, gws, x->dtype, (int)B, (int)C_dy, (int)C_x, K, P,
-                               transpose, stream);
+        e = depthwise ? launch_weight_grad_dw(dy->data, zbuf, dw->data, gws, x->dtype, (int)B, (int)C_x, K, P, stream)
+                      : launch_weight_grad(dy->data, zbuf, dw->data, gws, x->dtype, (int)B, (int)C_dy, (int)C_x, K, P,
+                                           transpose, stream);
         if (e != hipSuccess) s = hip_fail(e, "kernel launch");
     }
     (void)hipFreeAsync(gws, stream);
@@ -1030,6 +1044,18 @@ disco_status_t disco_forward_depthwise(disco_plan_t plan, const disco_tensor_t* 
 disco_status_t disco_transpose_depthwise(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
                                          disco_tensor_t* y, hipStream_t stream) {
     return run(plan, x, w, y, stream, DISCO_ALGO_AUTO, true, true);
+}
+
+disco_status_t disco_forward_depthwise_backward(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                                                const disco_tensor_t* dy, disco_tensor_t* dx, disco_tensor_t* dw,
+                                                hipStream_t stream) {
+    return backward(plan, false, x, w, dy, dx, dw, stream, true);
+}
+
+disco_status_t disco_transpose_depthwise_backward(disco_plan_t plan, const disco_tensor_t* x,
+                                                  const disco_tensor_t* w, const disco_tensor_t* dy,
+                                                  disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream) {
+    return backward(plan, true, x, w, dy, dx, dw, stream, true);
 }
 
 disco_status_t disco_forward_algo(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,

@@ -11,6 +11,11 @@
 // k_weight_grad_reduce sums the partials of each element over (batch item,
 // pixel range) in a fixed order, so the result is deterministic, and writes
 // dW in the op's layout.
+//
+// Depthwise channels need only the diagonal blocks, dW[c][k] = sum_b sum_p
+// dy[b][c][p] Zs[b][c][k][p]: k_weight_grad runs on B x C one-row items
+// (M = 1, N = K) and k_weight_grad_reduce_dw sums each channel's partials over
+// (batch item, pixel range) in a fixed order.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -117,6 +122,31 @@ __global__ __launch_bounds__(kBlock) void k_weight_grad_reduce(const float* __re
     }
 }
 
+// One workgroup per dW element e = (c, k) of a depthwise [C][K] dW: lane t
+// sums the partials of items b C + c over (b, chunk) pairs t, t + 256, ...,
+// then a fixed tree over the lanes.  partial: [B C][n_chunks][K].
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_weight_grad_reduce_dw(const float* __restrict__ partial,
+                                                                  T* __restrict__ dw, int B, int C, int n_chunks,
+                                                                  int K) {
+    __shared__ float red[kBlock];
+    const int e = blockIdx.x;
+    const int c = e / K, k = e - (e / K) * K;
+    const int tid = threadIdx.x;
+    float v = 0.0f;
+    for (int s = tid; s < B * n_chunks; s += kBlock) {
+        const int b = s / n_chunks, chunk = s - (s / n_chunks) * n_chunks;
+        v += partial[(((int64_t)b * C + c) * n_chunks + chunk) * K + k];
+    }
+    red[tid] = v;
+    __syncthreads();
+    for (int half = kBlock / 2; half > 0; half >>= 1) {
+        if (tid < half) red[tid] += red[tid + half];
+        __syncthreads();
+    }
+    if (tid == 0) store_val(dw, e, red[0]);
+}
+
 int64_t chunk_len_for(int B, int M, int N, int64_t P) {
     const int tiles = ((M + kTileM - 1) / kTileM) * ((N + kTileN - 1) / kTileN) * B;
     const int64_t want = std::max<int64_t>(1, 2048 / std::max(1, tiles));  // chunks per tile
@@ -146,7 +176,37 @@ hipError_t weight_grad(const T* dy, const T* zs, T* dw, float* ws, int B, int M,
     return hipGetLastError();
 }
 
+template <typename T>
+hipError_t weight_grad_dw(const T* dy, const T* zs, T* dw, float* ws, int B, int C, int K, int64_t P, hipStream_t s) {
+    const int items = B * C;
+    const int64_t len = chunk_len_for(items, 1, K, P);
+    const int n_chunks = (int)std::max<int64_t>(1, (P + len - 1) / len);
+    dim3 grid((unsigned)n_chunks, 1u, (unsigned)items);
+    int tk = timing_begin("weight_grad", s);
+    hipLaunchKernelGGL((k_weight_grad<T>), grid, dim3(kBlock), 0, s, dy, zs, ws, 1, K, P, len, 1);
+    timing_end(tk, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    tk = timing_begin("weight_grad_reduce", s);
+    hipLaunchKernelGGL((k_weight_grad_reduce_dw<T>), dim3((unsigned)(C * K)), dim3(kBlock), 0, s, ws, dw, B, C,
+                       n_chunks, K);
+    timing_end(tk, s);
+    return hipGetLastError();
+}
+
 }  // namespace
+
+size_t weight_grad_ws_bytes_dw(int B, int C, int K, int64_t P) {
+    return weight_grad_ws_bytes(B * C, 1, K, P);
+}
+
+hipError_t launch_weight_grad_dw(const void* dy, const void* zs, void* dw, float* ws, int dtype, int B, int C, int K,
+                                 int64_t P, hipStream_t s) {
+    if (K > kTileN) return hipErrorInvalidValue;
+    if (dtype == 1)
+        return weight_grad_dw<uint16_t>((const uint16_t*)dy, (const uint16_t*)zs, (uint16_t*)dw, ws, B, C, K, P, s);
+    return weight_grad_dw<float>((const float*)dy, (const float*)zs, (float*)dw, ws, B, C, K, P, s);
+}
 
 size_t weight_grad_ws_bytes(int B, int M, int N, int64_t P) {
     const int64_t len = chunk_len_for(B, M, N, P);

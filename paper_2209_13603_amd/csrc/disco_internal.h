@@ -384,6 +384,11 @@ hipError_t launch_stencil_blocked(const ExecArgs& a, const StencilDev& S, float*
 // layout) or dW[c_x][m][k] (transposed op's layout).  dtype 0 fp32, 1 bf16
 // (inputs and dW); partials in ws (weight_grad_ws_bytes).
 size_t weight_grad_ws_bytes(int B, int M, int N, int64_t P);
+// Depthwise dW[c][k] = sum_{b,p} dy[b][c][p] Zs[b][c][k][p] (K <= 16), partials
+// in ws (weight_grad_ws_bytes_dw), reduced in a fixed order.
+size_t weight_grad_ws_bytes_dw(int B, int C, int K, int64_t P);
+hipError_t launch_weight_grad_dw(const void* dy, const void* zs, void* dw, float* ws, int dtype, int B, int C, int K,
+                                 int64_t P, hipStream_t s);
 hipError_t launch_weight_grad(const void* dy, const void* zs, void* dw, float* ws, int dtype, int B, int M,
                               int C_x, int K, int64_t P, bool transposed_layout, hipStream_t s);
 

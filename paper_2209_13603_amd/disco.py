@@ -52,6 +52,7 @@ ALGOS = {"auto": ALGO_AUTO, "gather_then_contract": ALGO_GATHER_THEN_CONTRACT,
 EXPORTS = ("disco_plan_create", "disco_plan_destroy", "disco_plan_query", "disco_forward",
            "disco_transpose", "disco_forward_algo", "disco_transpose_algo", "disco_forward_backward",
            "disco_transpose_backward", "disco_forward_depthwise", "disco_transpose_depthwise",
+           "disco_forward_depthwise_backward", "disco_transpose_depthwise_backward",
            "disco_psi_entries",
            "disco_kernel_timing_enable", "disco_kernel_timing_read", "disco_kernel_work",
            "disco_status_string", "disco_last_error")
@@ -121,7 +122,8 @@ def library(path: str = LIB_PATH) -> ctypes.CDLL:
     for name in ("disco_forward_algo", "disco_transpose_algo"):
         getattr(lib, name).argtypes = [ctypes.c_void_p, P(Tensor), P(Tensor), P(Tensor),
                                        ctypes.c_void_p, ctypes.c_int32]
-    for name in ("disco_forward_backward", "disco_transpose_backward"):
+    for name in ("disco_forward_backward", "disco_transpose_backward", "disco_forward_depthwise_backward",
+                 "disco_transpose_depthwise_backward"):
         getattr(lib, name).argtypes = [ctypes.c_void_p, P(Tensor), P(Tensor), P(Tensor), P(Tensor),
                                        P(Tensor), ctypes.c_void_p]
         getattr(lib, name).restype = ctypes.c_int
@@ -316,6 +318,28 @@ def transpose_backward(plan, x, w, dy, want_dx=True, want_dw=True, stream=None):
         if want_dx else None
     dw = torch.empty_like(w) if want_dw else None
     return _backward(plan, "disco_transpose_backward", x if want_dw else None, w if want_dx else None,
+                     dy, dx, dw, stream)
+
+
+def forward_depthwise_backward(plan, x, w, dy, want_dx=True, want_dw=True, stream=None):
+    """Gradients of the depthwise forward op (``disco_forward_depthwise_backward``):
+    x[B, C, in-grid], w[C, K], dy[B, C, out-grid] -> (dx, dw)."""
+    import torch
+    dx = torch.empty((dy.shape[0], dy.shape[1]) + plan.grid_in, dtype=dy.dtype, device=dy.device) \
+        if want_dx else None
+    dw = torch.empty_like(w) if want_dw else None
+    return _backward(plan, "disco_forward_depthwise_backward", x if want_dw else None, w if want_dx else None,
+                     dy, dx, dw, stream)
+
+
+def transpose_depthwise_backward(plan, x, w, dy, want_dx=True, want_dw=True, stream=None):
+    """Gradients of the depthwise transposed op (``disco_transpose_depthwise_backward``):
+    x[B, C, out-grid], w[C, K], dy[B, C, in-grid] -> (dx, dw)."""
+    import torch
+    dx = torch.empty((dy.shape[0], dy.shape[1]) + plan.grid_out, dtype=dy.dtype, device=dy.device) \
+        if want_dx else None
+    dw = torch.empty_like(w) if want_dw else None
+    return _backward(plan, "disco_transpose_depthwise_backward", x if want_dw else None, w if want_dx else None,
                      dy, dx, dw, stream)
 
 

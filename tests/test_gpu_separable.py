@@ -202,3 +202,104 @@ def test_workload_separable_depthwise(name):
     assert err <= FP32_TOL
     assert np.isfinite(y).all()
     plan.close()
+
+
+# --------------------------------------------------------------------------- #
+# Gradients of the depthwise ops (App. C per channel): dx through the adjoint
+# run depthwise, dw the diagonal blocks of the full weight gradient.
+# --------------------------------------------------------------------------- #
+GRAD_CASES = [
+    (16, 32, 8, 16, "cell_centred"),
+    (33, 300, 33, 300, "cell_centred"),
+    (17, 32, 9, 16, "poles"),
+    (41, 80, 41, 80, "poles"),
+]
+
+
+def _dw_grad(case, transpose, basis, C, dtype, seed):
+    import torch
+    a, b, c, d, smp = case
+    tc = _tc(case)
+    code, K = BASES[basis]
+    xs = (2, C, c, d) if transpose else (2, C, a, b)
+    ys = (2, C, a, b) if transpose else (2, C, c, d)
+    r = np.random.default_rng(seed)
+    x = synth.to_storage(r.standard_normal(xs), dtype)
+    w = synth.to_storage(r.standard_normal((C, K)) / math.sqrt(K), dtype)
+    dy = synth.to_storage(r.standard_normal(ys), dtype)
+    say("depthwise backward", case, "transpose" if transpose else "forward", basis, C, dtype)
+    plan = disco.Plan(a, b, c, d, tc, basis=basis, sampling=smp, backward=True)
+    fn = disco.transpose_depthwise_backward if transpose else disco.forward_depthwise_backward
+    dx, dw = fn(plan, torch_dev(x, dtype), torch_dev(w, dtype), torch_dev(dy, dtype))
+    torch.cuda.synchronize()
+    o = oracle.default()
+    kw = {"sampling": 1 if smp == "poles" else 0, "basis": code}
+    wfull = oracle.depthwise_weights(w.astype(np.float64))
+    ref_dx = o.input_grad(a, b, c, d, tc, dy.astype(np.float64), wfull, transpose=transpose, **kw)
+    ref_full = o.weight_grad(a, b, c, d, tc, x.astype(np.float64), dy.astype(np.float64), transpose=transpose, **kw)
+    ref_dw = np.stack([ref_full[ch, ch] for ch in range(C)])
+    plan.close()
+    return to_numpy(dx), to_numpy(dw), ref_dx, ref_dw
+
+
+@pytest.mark.parametrize("basis", list(BASES))
+@pytest.mark.parametrize("transpose", [False, True], ids=["forward", "transpose"])
+@pytest.mark.parametrize("case", GRAD_CASES, ids=_ids)
+def test_depthwise_gradients(case, transpose, basis):
+    dx, dw, rdx, rdw = _dw_grad(case, transpose, basis, 3, "fp32", 61)
+    ex, ew = rel_l2(dx, rdx), rel_l2(dw, rdw)
+    say("  dx rel_l2 %.3e  dw rel_l2 %.3e" % (ex, ew))
+    assert ex <= FP32_TOL and ew <= FP32_TOL
+
+
+@pytest.mark.parametrize("basis", list(BASES))
+@pytest.mark.parametrize("transpose", [False, True], ids=["forward", "transpose"])
+def test_depthwise_gradients_bf16(transpose, basis):
+    dx, dw, rdx, rdw = _dw_grad(GRAD_CASES[0], transpose, basis, 5, "bf16", 62)
+    ex, ew = rel_l2(dx, rdx), rel_l2(dw, rdw)
+    say("  bf16 dx %.3e dw %.3e" % (ex, ew))
+    assert ex <= BF16_TOL and ew <= BF16_TOL
+
+
+def test_depthwise_gradients_match_the_full_op():
+    """On the GPU: the depthwise gradients equal the full-W gradients of the
+    diagonal W (dx to rounding, dw the diagonal blocks)."""
+    import torch
+    a, b = 33, 300
+    tc = 3 * math.pi / 33
+    plan = disco.Plan(a, b, a, b, tc, basis="separable4x4", backward=True)
+    r = np.random.default_rng(63)
+    C = 4
+    x = r.standard_normal((2, C, a, b)).astype(np.float32)
+    dy = r.standard_normal((2, C, a, b)).astype(np.float32)
+    w = (r.standard_normal((C, 16)) / 4).astype(np.float32)
+    dx, dw = disco.forward_depthwise_backward(plan, torch_dev(x), torch_dev(w), torch_dev(dy))
+    wf = oracle.depthwise_weights(w.astype(np.float64)).astype(np.float32)
+    dxf, dwf = disco.forward_backward(plan, torch_dev(x), torch_dev(wf), torch_dev(dy))
+    torch.cuda.synchronize()
+    assert rel_l2(to_numpy(dx), to_numpy(dxf)) <= 1e-6
+    full = to_numpy(dwf)
+    assert rel_l2(to_numpy(dw), np.stack([full[c, c] for c in range(C)])) <= 1e-6
+    plan.close()
+
+
+def test_depthwise_gradient_errors():
+    import torch
+    a, b = 16, 32
+    plan = disco.Plan(a, b, a, b, 3 * math.pi / 16, basis="axisym4", backward=True)
+    x = torch.zeros((2, 3, a, b), device="cuda:0")
+    dy = torch.zeros((2, 3, a, b), device="cuda:0")
+    w = torch.zeros((3, 4), device="cuda:0")
+    with pytest.raises(disco.DiscoError) as ei:       # dw of the full layout
+        disco._backward(plan, "disco_forward_depthwise_backward", x, w, dy, None,
+                        torch.zeros((3, 3, 4), device="cuda:0"), None)
+    assert ei.value.status == disco.DISCO_ERR_SHAPE
+    with pytest.raises(disco.DiscoError) as ei:       # dy with other channels
+        disco.forward_depthwise_backward(plan, x, w, torch.zeros((2, 4, a, b), device="cuda:0"))
+    assert ei.value.status == disco.DISCO_ERR_SHAPE
+    plan2 = disco.Plan(a, b, a, b, 3 * math.pi / 16, basis="axisym4")
+    with pytest.raises(disco.DiscoError) as ei:       # plan without the backward flag
+        disco.forward_depthwise_backward(plan2, x, w, dy)
+    assert ei.value.status == disco.DISCO_ERR_UNSUPPORTED
+    plan.close()
+    plan2.close()
