@@ -152,8 +152,11 @@ int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& sk
 // Each span carries one more block of columns than its entries read, and
 // the weight table four more entries, for the kernel's one-block-ahead reads.
 constexpr int kStencilTile = 1024;      // output longitudes per workgroup
-constexpr int kStencilCols = 8192;      // LDS floats staged per chunk
-constexpr int kStencilEntries = 1024;   // padded entries (weights) per chunk
+// Chunk budgets set for occupancy: 4096 staged floats and 512 entries keep
+// the blocked kernel at 91 VGPRs and 18.7 KB of LDS, five waves per SIMD
+// (8192 and 1024 gave 148 VGPRs, three waves, and 1.7x the time at L = 2048).
+constexpr int kStencilCols = 4096;      // LDS floats staged per chunk
+constexpr int kStencilEntries = 512;    // padded entries (weights) per chunk
 constexpr int kStencilMaxRun = 512;     // entries of one piece
 constexpr int kStencilSpan(int nblk) { return kStencilTile + 4 * nblk + 4; }
 
