@@ -205,11 +205,14 @@ void free_sweep(SweepDev* d) {
 disco_status_t upload_stencil(const HostOp& h, StencilDev* d) {
     // Entries per work item: enough workgroups (items x longitude tiles) to
     // fill the chip several times over, within [128, 1024].
-    const int64_t n_qt = (h.g.nq + kStencilTile - 1) / kStencilTile;
+    // The tile: 512 output longitudes when a pattern has no more (two-phase
+    // ops, small grids), so that no lanes idle; 1024 otherwise.
+    const int tile = h.g.nq <= kStencilSmallTile ? kStencilSmallTile : kStencilTile;
+    const int64_t n_qt = (h.g.nq + tile - 1) / tile;
     const int target = (int)std::min<int64_t>(1024, std::max<int64_t>(128, (int64_t)h.t_in.size() * n_qt / 4096));
     StencilHost H;
     std::string err;
-    int rc = pack_stencil(h, target, &H, &err);
+    int rc = pack_stencil(h, target, tile, &H, &err);
     if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
     disco_status_t s;
     if ((s = upload_vec(H.pieces, &d->pieces, &d->bytes, "hipMalloc(stencil pieces)")) != DISCO_OK) return s;
@@ -225,6 +228,7 @@ disco_status_t upload_stencil(const HostOp& h, StencilDev* d) {
     P.n_items = (int32_t)H.items.size();
     P.n_split = (int32_t)H.red_pattern.size();
     P.n_slots = H.n_slots;
+    d->tile = H.tile;
     d->n_padded = (int64_t)H.vals.size();
     return DISCO_OK;
 }

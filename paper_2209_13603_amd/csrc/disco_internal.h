@@ -138,32 +138,34 @@ int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& sk
             std::string* err);
 
 // ---------------------------------------------------------------------------
-// Blocked layout of the axisymmetric stencil kernel for ops with longitude
+// Blocked layout of the folded-weight stencil kernel for ops with longitude
 // stride 1 and one output channel (disco_stencil.hip): a workgroup owns
-// kStencilTile consecutive output longitudes (four per lane) of one pattern.
+// `tile` consecutive output longitudes (four per lane) of one pattern.
 // A pattern's entries on one input ring form runs of consecutive offsets
 // (the filter's disc meets a ring in one arc); each run ("piece") is padded
 // with zero entries to whole blocks of four, so a lane's four outputs take
 // the block's four weights against seven consecutive inputs read as two
 // aligned float4 (one of them kept from the previous block).  A chunk's
-// pieces are staged in LDS together (each span kStencilTile + 4 nblk
+// pieces are staged in LDS together (each span tile + 4 nblk
 // floats, 16-byte aligned); chunks form segments and work items as in the
 // fused layout (PSeg / PItem, split patterns summed by k_reduce_partials).
 // Each span carries one more block of columns than its entries read, and
 // the weight table four more entries, for the kernel's one-block-ahead reads.
-constexpr int kStencilTile = 1024;      // output longitudes per workgroup
-// Chunk budgets set for occupancy: 4096 staged floats and 512 entries keep
-// the blocked kernel at 91 VGPRs and 18.7 KB of LDS, five waves per SIMD
+constexpr int kStencilTile = 1024;      // output longitudes per workgroup (ops with nq > 512)
+constexpr int kStencilSmallTile = 512;  // ... for ops with at most 512 output longitudes per pattern
+// Chunk budgets scale with the tile (lanes = tile / 4) and are set for
+// occupancy: 4 tile staged floats and tile / 2 entries per chunk keep the
+// kernel at 91 VGPRs and five waves per SIMD for the 1024-longitude tile
 // (8192 and 1024 gave 148 VGPRs, three waves, and 1.7x the time at L = 2048).
-constexpr int kStencilCols = 4096;      // LDS floats staged per chunk
-constexpr int kStencilEntries = 512;    // padded entries (weights) per chunk
-constexpr int kStencilMaxRun = 512;     // entries of one piece
-constexpr int kStencilSpan(int nblk) { return kStencilTile + 4 * nblk + 4; }
-
-struct SPiece { int32_t row, dstart, lds_base, nblk; };           // row = ring * nlon_i; kStencilSpan(nblk) columns
+constexpr int stencil_cols(int tile) { return 4 * tile; }         // LDS floats staged per chunk
+constexpr int stencil_entries(int tile) { return tile / 2; }      // padded entries (weights) per chunk
+constexpr int stencil_max_run(int tile) { return tile / 2; }      // entries of one piece
+constexpr int stencil_span(int tile, int nblk) { return tile + 4 * nblk + 4; }
+struct SPiece { int32_t row, dstart, lds_base, nblk; };           // row = ring * nlon_i; stencil_span(tile, nblk) columns
 struct SChunk { int32_t piece_begin, piece_end, ent_begin, ent_end; };
 
 struct StencilHost {
+    int32_t tile = kStencilTile;        // output longitudes per workgroup
     std::vector<SPiece> pieces;
     std::vector<SChunk> chunks;
     std::vector<PVal> vals;             // per padded entry: its cell's values times q (zeros for padding)
@@ -173,7 +175,7 @@ struct StencilHost {
     std::vector<int32_t> red_pattern, red_ptr, red_slots;
     int32_t n_slots = 0;
 };
-int pack_stencil(const HostOp& op, int target_entries, StencilHost* out, std::string* err);
+int pack_stencil(const HostOp& op, int target_entries, int tile, StencilHost* out, std::string* err);
 
 // ---------------------------------------------------------------------------
 // Sweep layout (disco_sweep.hip): a workgroup walks a run of consecutive
@@ -285,6 +287,7 @@ struct StencilDev {
     PVal* vals = nullptr;
     uint8_t* cells = nullptr;
     PackedDev P;                        // segs, items and the reduction tables (no spans)
+    int32_t tile = kStencilTile;
     int64_t n_padded = 0;
     int64_t bytes = 0;
 };

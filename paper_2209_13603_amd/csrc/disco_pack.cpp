@@ -389,13 +389,19 @@ int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& sk
 
 namespace disco {
 
-int pack_stencil(const HostOp& op, int target_entries, StencilHost* out, std::string* err) {
+int pack_stencil(const HostOp& op, int target_entries, int tile, StencilHost* out, std::string* err) {
     const OpGeom& g = op.g;
     if (g.stride != 1) {
         if (err) *err = "the blocked stencil layout needs longitude stride 1";
         return DISCO_ERR_UNSUPPORTED;
     }
+    if (tile != kStencilTile && tile != kStencilSmallTile) {
+        if (err) *err = "internal: unknown stencil tile";
+        return DISCO_ERR_DEVICE;
+    }
+    const int cols = stencil_cols(tile), max_entries = stencil_entries(tile), max_run = stencil_max_run(tile);
     StencilHost H;
+    H.tile = tile;
     struct Run {
         int32_t ti, d_first, d_last;
         std::vector<PVal> v;
@@ -415,7 +421,7 @@ int pack_stencil(const HostOp& op, int target_entries, StencilHost* out, std::st
                 return DISCO_ERR_DEVICE;
             }
             if (!runs.empty() && runs.back().ti == ti && dr > runs.back().d_last &&
-                dr - runs.back().d_last <= 4 && dr - runs.back().d_first + 1 <= kStencilMaxRun) {
+                dr - runs.back().d_last <= 4 && dr - runs.back().d_first + 1 <= max_run) {
                 Run& r = runs.back();
                 for (int32_t gap = r.d_last + 1; gap < dr; ++gap) {
                     r.v.push_back(PVal{});
@@ -439,9 +445,8 @@ int pack_stencil(const HostOp& op, int target_entries, StencilHost* out, std::st
         int used = 0, used_e = 0;
         for (size_t i = 0; i < runs.size(); ++i) {
             const int ne = (int)runs[i].v.size();
-            const int len = kStencilSpan(ne / 4);  // staged columns, a multiple of 4
-            if (H.chunks.size() == (size_t)chunk_first || used + len > kStencilCols ||
-                used_e + ne > kStencilEntries) {
+            const int len = stencil_span(tile, ne / 4);  // staged columns, a multiple of 4
+            if (H.chunks.size() == (size_t)chunk_first || used + len > cols || used_e + ne > max_entries) {
                 const int32_t pb = (int32_t)H.pieces.size(), eb = (int32_t)H.vals.size();
                 H.chunks.push_back(SChunk{pb, pb, eb, eb});
                 chunk_entries.push_back(0);
@@ -498,7 +503,7 @@ int pack_stencil(const HostOp& op, int target_entries, StencilHost* out, std::st
         for (int32_t c = sg.chunk_begin; c < sg.chunk_end; ++c) {
             const SChunk& C = H.chunks[(size_t)c];
             n += C.ent_end - C.ent_begin;
-            n += (C.piece_end - C.piece_begin) * kStencilTile / 32;
+            n += (C.piece_end - C.piece_begin) * tile / 32;
         }
         if (H.items.empty() || acc + n > target_entries || H.items.back().seg_end - H.items.back().seg_begin >= 64) {
             H.items.push_back(PItem{i, i + 1});

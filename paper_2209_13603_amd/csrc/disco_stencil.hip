@@ -66,11 +66,11 @@ __device__ __forceinline__ int xcd_remap(int bid, int nb) {
 // Fills T[j][cell][m] (64 floats per output channel j of the tile) for input
 // channel ci.  dw_c > 0: depthwise, item b takes row b mod dw_c of a [C][K]
 // W (Ci = Co = 1).
-template <typename T, int COT>
+template <typename T, int COT, int NT>
 __device__ __forceinline__ void fill_fold_table(float* wt, const int8_t* __restrict__ cmap,
                                                 const T* __restrict__ w, int K, int b, int ci, int co0,
                                                 int Ci, int Co, bool w_trans, int dw_c) {
-    for (int idx = threadIdx.x; idx < COT * kCells * 4; idx += kBlock) {
+    for (int idx = threadIdx.x; idx < COT * kCells * 4; idx += NT) {
         const int j = idx / (kCells * 4), cm = idx - j * (kCells * 4);
         const int k = cmap[cm];
         const int co = co0 + j;
@@ -125,7 +125,7 @@ __global__ __launch_bounds__(kBlock) void k_stencil(const PItem* __restrict__ it
             // through the cell map.  The previous readers of the table (the
             // last chunk's staging) are behind that chunk's second barrier;
             // the next chunk's first barrier orders these writes before use.
-            fill_fold_table<T, COT>(wt, cmap, w, K, b, ci, co0, Ci, Co, w_trans, dw_c);
+            fill_fold_table<T, COT, kBlock>(wt, cmap, w, K, b, ci, co0, Ci, Co, w_trans, dw_c);
             const T* xc = x + ((int64_t)b * Ci + ci) * n_in;
             for (int ch = sg.chunk_begin; ch < sg.chunk_end; ++ch) {
                 const PChunk C = chunks[ch];
@@ -224,13 +224,11 @@ hipError_t stencil_dispatch(const ExecArgs& a, const PackedDev& P, float* partia
 // x[q0 + 4l + dstart + 4b + m], m = 0..6: the aligned float4 V0 (m < 4) and
 // V1 (m >= 4) at LDS columns 4l + 4b and 4l + 4b + 4 of the piece's span;
 // V1 is the next block's V0.  Per block: one float4 of x and one float4 of
-// folded weights (the same for every lane) from LDS for 16 FMAs.
-constexpr int kMaxPieces = kStencilCols / kStencilTile;       // every span is >= one tile
-constexpr int kColsPerThread = kStencilCols / kBlock;
-constexpr int kEntriesPerThread = kStencilEntries / kBlock;
-
-template <typename T>
-__global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restrict__ items,
+// folded weights (the same for every lane) from LDS for 16 FMAs.  TILE
+// output longitudes per workgroup of TILE / 4 lanes; the chunk budgets scale
+// with it, so every tile stages 16 columns and 2 entries per lane.
+template <typename T, int TILE>
+__global__ __launch_bounds__(TILE / 4) void k_stencil_blocked(const PItem* __restrict__ items,
                                                             const PSeg* __restrict__ segs,
                                                             const SChunk* __restrict__ chunks,
                                                             const SPiece* __restrict__ pieces,
@@ -241,8 +239,14 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
                                                             const T* __restrict__ w, T* __restrict__ y,
                                                             float* __restrict__ partial, int Ci, int K,
                                                             int n_qtiles, int dw_c) {
-    __shared__ float4 xs4[kStencilCols / 4];
-    __shared__ float4 ew4[kStencilEntries / 4 + 1];
+    constexpr int NT = TILE / 4;
+    constexpr int kCols = stencil_cols(TILE);
+    constexpr int kEntries = stencil_entries(TILE);
+    constexpr int kMaxPieces = kCols / TILE;  // every span is >= one tile
+    constexpr int kColsPerThread = kCols / NT;
+    constexpr int kEntriesPerThread = kEntries / NT;
+    __shared__ float4 xs4[kCols / 4];
+    __shared__ float4 ew4[kEntries / 4 + 1];
     __shared__ float4 wt4[kCells];  // [cell][m]
     float* xs = (float*)xs4;
     float* ew = (float*)ew4;
@@ -252,7 +256,7 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
     const int item = bid / n_qtiles;
     const int qt = bid - item * n_qtiles;
     const int b = blockIdx.y;
-    const int q0 = qt * kStencilTile;
+    const int q0 = qt * TILE;
     const int64_t n_in = (int64_t)g.nlat_i * g.nlon_i;
     const int64_t n_out = (int64_t)g.nlat_o * g.nlon_o;
     const PItem it = items[item];
@@ -263,12 +267,12 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
         for (int ci = 0; ci < Ci; ++ci) {
             // One output channel: W[0][ci][.] and the transposed op's
             // W[ci][0][.] are the same row (ordered as k_stencil's table).
-            fill_fold_table<T, 1>((float*)wt4, cmap, w, K, b, ci, 0, Ci, 1, false, dw_c);
+            fill_fold_table<T, 1, NT>((float*)wt4, cmap, w, K, b, ci, 0, Ci, 1, false, dw_c);
             const T* xc = x + ((int64_t)b * Ci + ci) * n_in;
             for (int ch = sg.chunk_begin; ch < sg.chunk_end; ++ch) {
                 const SChunk C = chunks[ch];
                 // The chunk's spans fill LDS columns [0, used) back to back
-                // (at most kStencilCols / kStencilTile pieces).  Every thread
+                // (at most kCols / TILE pieces).  Every thread
                 // first issues the loads of all its columns and entries, then
                 // stores them, so that a chunk costs one memory latency.
                 const int np = C.piece_end - C.piece_begin;
@@ -276,7 +280,7 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
                 int used = 0;
 #pragma unroll
                 for (int pp = 0; pp < kMaxPieces; ++pp) {
-                    pbase[pp] = kStencilCols;
+                    pbase[pp] = kCols;
                     prow[pp] = 0;
                     pstart[pp] = 0;
                     if (pp < np) {
@@ -286,13 +290,13 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
                         pbase[pp] = S.lds_base;
                         prow[pp] = S.row;
                         pstart[pp] = st;
-                        used = S.lds_base + kStencilSpan(S.nblk);
+                        used = S.lds_base + stencil_span(TILE, S.nblk);
                     }
                 }
                 float v[kColsPerThread];
 #pragma unroll
                 for (int u = 0; u < kColsPerThread; ++u) {
-                    const int c = tid + u * kBlock;
+                    const int c = tid + u * NT;
                     v[u] = 0.0f;
                     if (c < used) {
                         int base = pbase[0], row = prow[0], st = pstart[0];
@@ -309,7 +313,7 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
                 int pc[kEntriesPerThread];
 #pragma unroll
                 for (int u = 0; u < kEntriesPerThread; ++u) {
-                    const int i = tid + u * kBlock;
+                    const int i = tid + u * NT;
                     pc[u] = 0;
                     if (i < ne) {
                         pv[u] = vals[C.ent_begin + i];
@@ -319,12 +323,12 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
                 __syncthreads();  // readers of the previous chunk (or channel) are done
 #pragma unroll
                 for (int u = 0; u < kColsPerThread; ++u) {
-                    const int c = tid + u * kBlock;
+                    const int c = tid + u * NT;
                     if (c < used) xs[c] = v[u];
                 }
 #pragma unroll
                 for (int u = 0; u < kEntriesPerThread; ++u) {
-                    const int i = tid + u * kBlock;
+                    const int i = tid + u * NT;
                     if (i < ne) {
                         const float4 t = wt4[pc[u]];
                         ew[i] = t.x * pv[u].v[0] + t.y * pv[u].v[1] + t.z * pv[u].v[2] + t.w * pv[u].v[3];
@@ -372,16 +376,16 @@ __global__ __launch_bounds__(kBlock) void k_stencil_blocked(const PItem* __restr
     }
 }
 
-template <typename T>
+template <typename T, int TILE>
 hipError_t stencil_blocked_launch(const ExecArgs& a, const StencilDev& S, float* partial) {
     const OpGeom& g = a.op->g;
     if (S.P.n_items == 0) return hipSuccess;
-    const int n_qtiles = (g.nq + kStencilTile - 1) / kStencilTile;
+    const int n_qtiles = (g.nq + TILE - 1) / TILE;
     dim3 grid((unsigned)(S.P.n_items * n_qtiles), (unsigned)a.B);
     const int tk = timing_begin("stencil_blocked", a.stream);
-    hipLaunchKernelGGL((k_stencil_blocked<T>), grid, dim3(kBlock), 0, a.stream, S.P.items, S.P.segs, S.chunks,
-                       S.pieces, S.vals, S.cells, a.op->cmap_dev, g, (const T*)a.x, (const T*)a.w, (T*)a.y,
-                       partial, a.Ci, basis_size(a.op->basis), n_qtiles, a.dw_c);
+    hipLaunchKernelGGL((k_stencil_blocked<T, TILE>), grid, dim3(TILE / 4), 0, a.stream, S.P.items, S.P.segs,
+                       S.chunks, S.pieces, S.vals, S.cells, a.op->cmap_dev, g, (const T*)a.x, (const T*)a.w,
+                       (T*)a.y, partial, a.Ci, basis_size(a.op->basis), n_qtiles, a.dw_c);
     timing_end(tk, a.stream);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -391,8 +395,12 @@ hipError_t stencil_blocked_launch(const ExecArgs& a, const StencilDev& S, float*
 }  // namespace
 
 hipError_t launch_stencil_blocked(const ExecArgs& a, const StencilDev& S, float* partial_ws) {
-    return a.dtype == 1 ? stencil_blocked_launch<uint16_t>(a, S, partial_ws)
-                        : stencil_blocked_launch<float>(a, S, partial_ws);
+    if (S.tile == kStencilSmallTile)
+        return a.dtype == 1 ? stencil_blocked_launch<uint16_t, kStencilSmallTile>(a, S, partial_ws)
+                            : stencil_blocked_launch<float, kStencilSmallTile>(a, S, partial_ws);
+    if (S.tile != kStencilTile) return hipErrorInvalidValue;
+    return a.dtype == 1 ? stencil_blocked_launch<uint16_t, kStencilTile>(a, S, partial_ws)
+                        : stencil_blocked_launch<float, kStencilTile>(a, S, partial_ws);
 }
 
 hipError_t launch_stencil(const ExecArgs& a, const PackedDev& P, float* partial_ws) {
