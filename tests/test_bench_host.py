@@ -1,0 +1,96 @@
+"""Host-side checks of bench.py's measurement logic (no GPU): the algorithmic
+work model per kernel, the sharing of a step's work between the launches of a
+kernel that runs several times per step, the counter-summary writer and
+reader, and the refusal of more than one GPU."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import bench
+from paper_2209_13603_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_fused_model_counts_gather_and_contraction():
+    wl = synth.WORKLOADS["sphere2048x4096"]
+    outp, inp, pairs = 1000, 900, 50000
+    b, f, bound = bench.kernel_model("sweep_gather_contract", wl, (outp, inp, pairs), 4)
+    assert bound == "alu"
+    assert b == wl.batch * (wl.c_in * inp + wl.c_out * outp) * 4
+    assert f == 2.0 * pairs * wl.batch * wl.c_in + 2.0 * wl.batch * wl.c_in * 9 * wl.c_out * outp
+
+
+def test_depthwise_stencil_model_is_one_channel_per_item():
+    wl = synth.WORKLOADS["sphere2048x4096_separable_dw"]
+    outp, inp, pairs = 4096, 4096, 100000
+    b, f, _ = bench.kernel_model("stencil_blocked", wl, (outp, inp, pairs), 4)
+    items = wl.batch * wl.c_in
+    assert b == items * (inp + outp) * 4
+    assert f == 2.0 * pairs * items
+
+
+def test_convert_model_is_hbm():
+    wl = synth.WORKLOADS["up256x512_to_512x1024_bf16"]
+    b, f, bound = bench.kernel_model("convert_y", wl, (777, 0, 0), 2)
+    assert bound == "hbm" and f == 0.0
+    assert b == wl.batch * wl.c_out * 777 * (4 + 2)
+
+
+class _FakePlan:
+    def __init__(self, work):
+        self.work = work
+
+    def kernel_work(self, transpose, algo, cin, cout, dtype):
+        return self.work
+
+
+def test_multi_launch_kernel_shares_the_step():
+    """A kernel launched four times per step reports a quarter of the step's
+    work per launch; the time per launch is the total over launches."""
+    wl = synth.WORKLOADS["sphere512x1024"]
+    work = {"sweep_gather_contract": (1000, 1000, 20000), "spectral_mac": (0, 0, 5000)}
+    steps = 10
+    kt = {"sweep_gather_contract": (4 * steps, 40.0), "spectral_mac": (steps, 5.0)}
+    per, roof = bench.kernel_report(_FakePlan(work), kt, wl, False, "auto", 4, steps)
+    b_full, f_full, _ = bench.kernel_model("sweep_gather_contract", wl, work["sweep_gather_contract"], 4)
+    assert per["sweep_gather_contract"]["alg_bytes"] == int(b_full / 4)
+    assert per["sweep_gather_contract"]["alg_flops"] == pytest.approx(f_full / 4)
+    assert per["sweep_gather_contract"]["avg_us"] == pytest.approx(1000.0)
+    assert roof["kernel"] == "sweep_gather_contract"
+    assert roof["achieved"] == pytest.approx(round(f_full / 4 / 1e-3 / 1e12, 2))
+
+
+def _write_csv(path, rows):
+    with open(path, "w") as f:
+        f.write("Dispatch_Id,Kernel_Name,Counter_Name,Counter_Value\n")
+        for r in rows:
+            f.write('%d,"%s",%s,%s\n' % r)
+
+
+def test_traffic_summary_round_trip(tmp_path, monkeypatch):
+    """Counters scaled by the copy probe: FETCH_SIZE reads half the moved
+    bytes, WRITE_SIZE all of them; the summary carries the source digest and
+    load_traffic returns its per-launch bytes."""
+    monkeypatch.setattr(bench, "traffic_path", lambda k, w: str(tmp_path / ("t_%s_%s.txt" % (k, w))))
+    probe_kib = bench.COPY_PROBE_BYTES / 1024.0
+    sweep = "void disco::k_sweep<float, 8, false, 0>(int)"
+    fetch = [(1, sweep, "FETCH_SIZE", 1000.0), (2, sweep, "FETCH_SIZE", 1200.0),
+             (3, "neg_kernel(float)", "FETCH_SIZE", probe_kib / 2)]
+    write = [(1, sweep, "WRITE_SIZE", 3000.0), (2, sweep, "WRITE_SIZE", 3000.0),
+             (3, "neg_kernel(float)", "WRITE_SIZE", probe_kib)]
+    fc, wc = tmp_path / "f.csv", tmp_path / "w.csv"
+    _write_csv(fc, fetch)
+    _write_csv(wc, write)
+    bench.traffic_summary(str(fc), str(wc), "sweep_gather_contract", "sphere2048x4096", ["cmd"])
+    got = bench.load_traffic("sweep_gather_contract", "sphere2048x4096")
+    assert got == pytest.approx((1100.0 * 2 + 3000.0) * 1024.0)
+
+
+def test_bench_refuses_more_than_one_gpu():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, cwd=ROOT, timeout=300)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
