@@ -149,7 +149,8 @@ typedef struct {
  * in fp64 (per output ring: neighbour search over input rings within theta_c,
  * closed-form longitude window, rotation, basis, quadrature; Sec. 4.1 and
  * 4.2), rounds them to fp32 and uploads them to the current device.
- *   nlat_* >= 1, nlon_* >= 2, 0 < theta_c <= pi; basis may be NULL (defaults).
+ *   nlat_* >= 1, nlon_* >= 2, 0 < theta_c <= pi; basis may be NULL (defaults);
+ *   each op has at most 65535 (output ring, longitude phase) patterns.
  *   The pole-including sampling needs nlat >= 2 and nlon = 2 (nlat - 1) on
  *   both grids.
  * Errors: INVALID_ARGUMENT (sizes, cutoff, negative node spacing, unknown
@@ -171,8 +172,9 @@ disco_status_t disco_plan_query(disco_plan_t plan, disco_plan_info_t* info);
 
 /* Forward op (Sec. 3.2 eq. 4 on SO(3)/SO(2), Sec. 4.2 compressed product):
  *   x [B, Cin, nlat_in, nlon_in], w [Cout, Cin, K], y [B, Cout, nlat_out, nlon_out].
- * B may be 0 (nothing is enqueued).  Errors: INVALID_ARGUMENT, SHAPE, DTYPE,
- * OUT_OF_MEMORY (workspace), DEVICE. */
+ * B may be 0 (nothing is enqueued); B * max(Cin, Cout) <= 65535, channels
+ * <= 4096.  Errors: INVALID_ARGUMENT, SHAPE, DTYPE, OUT_OF_MEMORY
+ * (workspace), DEVICE. */
 disco_status_t disco_forward(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
                              disco_tensor_t* y, hipStream_t stream);
 
@@ -224,7 +226,8 @@ disco_status_t disco_transpose_algo(disco_plan_t plan, const disco_tensor_t* x,
  * dx is overwritten, dw is overwritten (not accumulated).  The plan must have
  * been created with DISCO_PLAN_BACKWARD.  dw is reduced over pixels in a fixed
  * order (deterministic); with bf16 storage the gathered sums are rounded to
- * bf16 before the reduction, which accumulates in fp32.  Errors as
+ * bf16 before the reduction, which accumulates in fp32; dw needs
+ * B * Cin * K <= 65535 (the input channels of dw's layout).  Errors as
  * disco_forward, and UNSUPPORTED for a plan without DISCO_PLAN_BACKWARD. */
 disco_status_t disco_forward_backward(disco_plan_t plan, const disco_tensor_t* x,
                                       const disco_tensor_t* w, const disco_tensor_t* dy,
@@ -251,8 +254,8 @@ disco_status_t disco_transpose_backward(disco_plan_t plan, const disco_tensor_t*
  * [C, K] its weights (read for dx only), dy [B, C, op output grid]; dx or dw
  * may be NULL.  Same conventions as disco_forward_backward (plan created with
  * DISCO_PLAN_BACKWARD, dw reduced in a fixed order, overwritten, bf16 sums
- * rounded before the fp32 reduction); B * C <= 65535.  Errors as
- * disco_forward_backward. */
+ * rounded before the fp32 reduction); B * C * K <= 65535 when dw is asked
+ * for.  Errors as disco_forward_backward. */
 disco_status_t disco_forward_depthwise_backward(disco_plan_t plan, const disco_tensor_t* x,
                                                 const disco_tensor_t* w, const disco_tensor_t* dy,
                                                 disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream);

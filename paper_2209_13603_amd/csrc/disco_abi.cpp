@@ -84,6 +84,12 @@ disco_status_t resolve_params(int nlat_in, int nlon_in, int nlat_out, int nlon_o
         return fail(DISCO_ERR_INVALID_ARGUMENT, "node_spacing must be >= 0");
     if (nlon_in % nlon_out != 0 && nlon_out % nlon_in != 0)
         return fail(DISCO_ERR_UNSUPPORTED, "nlon_in / nlon_out or nlon_out / nlon_in must be an integer");
+    // One pattern per (output ring, longitude phase) of each op; kernels put
+    // patterns in a 16-bit grid dimension.
+    const int64_t pat_fwd = (int64_t)nlat_out * (nlon_out % nlon_in == 0 ? nlon_out / nlon_in : 1);
+    const int64_t pat_tr = (int64_t)nlat_in * (nlon_in % nlon_out == 0 ? nlon_in / nlon_out : 1);
+    if (pat_fwd > 65535 || pat_tr > 65535)
+        return fail(DISCO_ERR_UNSUPPORTED, "more than 65535 latitude rings x longitude phases in one op");
     p->nlat_in = nlat_in; p->nlon_in = nlon_in; p->nlat_out = nlat_out; p->nlon_out = nlon_out;
     p->theta_c = theta_c;
     const double h_default = b.kind == DISCO_BASIS_BILINEAR_3X3 ? theta_c / 3.0 : theta_c / 4.0;
@@ -517,6 +523,9 @@ disco_status_t check_op_args(disco_plan_t plan, const DeviceOp& op, bool transpo
 disco_status_t check_common(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
                             const disco_tensor_t* y) {
     const int64_t B = x->shape[0];
+    // Kernels put (batch item, channel) pairs in a 16-bit grid dimension.
+    if (B * std::max(x->shape[1], y->shape[1]) > 65535)
+        return fail(DISCO_ERR_SHAPE, "batch x channels above 65535");
     if (x->dtype != y->dtype || w->dtype != x->dtype)
         return fail(DISCO_ERR_DTYPE, "x, w and y must share one dtype");
     if (x->dtype != DISCO_FLOAT32 && x->dtype != DISCO_BFLOAT16)
@@ -683,7 +692,8 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
                 return fail(DISCO_ERR_SHAPE, std::string("dw must be ") + (transpose ? "[CinT, CoutT, K]" : "[Cout, Cin, K]"));
         }
         if (dw->dtype != x->dtype || dy->dtype != x->dtype) return fail(DISCO_ERR_DTYPE, "x, dy and dw must share one dtype");
-        if (B * C_x > 65535) return fail(DISCO_ERR_SHAPE, "batch x channels too large for the weight gradient");
+        if (B * C_x * K > 65535)
+            return fail(DISCO_ERR_SHAPE, "batch x channels x basis functions too large for the weight gradient");
         P = (int64_t)op.g.nlat_o * op.g.nlon_o;
         if (B > 0) {
             if (!dw->data || !dy->data) return fail(DISCO_ERR_INVALID_ARGUMENT, "NULL data pointer");

@@ -251,3 +251,19 @@ def test_psi_entries_validation():
     rc = lib.disco_psi_entries(8, 16, 8, 16, 0.3, None, 0, 0, null, null, null, null, nullf,
                                None, None, None)
     assert rc == disco.DISCO_ERR_INVALID_ARGUMENT
+
+
+def test_pattern_count_limit():
+    """Kernels index (output ring, longitude phase) patterns in a 16-bit grid
+    dimension: ops with more are rejected before any device work."""
+    lib = disco.library()
+    b = disco._basis()
+    count = ctypes.c_int64()
+    null_i = ctypes.POINTER(ctypes.c_int32)()
+    null_f = ctypes.POINTER(ctypes.c_float)()
+    def entries(a, bb, c, d):
+        return lib.disco_psi_entries(a, bb, c, d, 0.01, ctypes.byref(b), 0, 0, null_i, null_i, null_i, null_i,
+                                     null_f, ctypes.byref(count), None, None)
+    assert entries(65536, 2, 65536, 2) == disco.DISCO_ERR_UNSUPPORTED
+    assert entries(40000, 2, 40000, 4) == disco.DISCO_ERR_UNSUPPORTED   # forward op: 2 phases x 40000 rings
+    assert "65535" in lib.disco_last_error().decode()

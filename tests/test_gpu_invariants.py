@@ -218,3 +218,25 @@ def test_kernel_work_names_match_timing():
         say(algo, sorted(kt), sorted(work))
         assert set(kt) <= set(work) and kt
     plan.close()
+
+
+def test_batch_times_channels_limit():
+    """(Batch item, channel) pairs index a 16-bit grid dimension: a call with
+    more than 65535 of them is rejected with a shape error before launch."""
+    import torch
+    a, b = 8, 16
+    plan = disco.Plan(a, b, a, b, 3 * math.pi / a, backward=True)
+    x = torch.zeros((16385, 1, a, b), device="cuda:0")
+    y = torch.zeros((16385, 4, a, b), device="cuda:0")
+    w = torch.zeros((4, 1, 9), device="cuda:0")
+    with pytest.raises(disco.DiscoError) as ei:
+        plan.forward(x, w, y)
+    assert ei.value.status == disco.DISCO_ERR_SHAPE
+    # the weight gradient's gathered sums: B * Cin * K pairs
+    x2 = torch.zeros((8000, 1, a, b), device="cuda:0")
+    dy2 = torch.zeros((8000, 1, a, b), device="cuda:0")
+    w2 = torch.zeros((1, 1, 9), device="cuda:0")
+    with pytest.raises(disco.DiscoError) as ei:
+        disco.forward_backward(plan, x2, w2, dy2, want_dx=False)
+    assert ei.value.status == disco.DISCO_ERR_SHAPE
+    plan.close()
