@@ -695,9 +695,11 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
         if (B * C_x * K > 65535)
             return fail(DISCO_ERR_SHAPE, "batch x channels x basis functions too large for the weight gradient");
         P = (int64_t)op.g.nlat_o * op.g.nlon_o;
+        // dw is written even for an empty batch (a sum over nothing: zeros).
+        if (!dw->data) return fail(DISCO_ERR_INVALID_ARGUMENT, "NULL data pointer");
+        if ((s = check_device_ptr(dw->data, plan->device, "dw")) != DISCO_OK) return s;
         if (B > 0) {
-            if (!dw->data || !dy->data) return fail(DISCO_ERR_INVALID_ARGUMENT, "NULL data pointer");
-            if ((s = check_device_ptr(dw->data, plan->device, "dw")) != DISCO_OK) return s;
+            if (!dy->data) return fail(DISCO_ERR_INVALID_ARGUMENT, "NULL data pointer");
             if ((s = check_device_ptr(dy->data, plan->device, "dy")) != DISCO_OK) return s;
             if (overlaps(dw, x) || overlaps(dw, dy) || (dx && overlaps(dw, dx)))
                 return fail(DISCO_ERR_INVALID_ARGUMENT, "dw overlaps another tensor");
@@ -728,11 +730,16 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
         }
     }
     if (dx && (s = run_op(plan, adj, !transpose, dy, w, dx, stream, DISCO_ALGO_AUTO, depthwise)) != DISCO_OK) return s;
-    if (!dw || B == 0) return ok();
+    if (!dw) return ok();
     int cur = 0;
     if (hipGetDevice(&cur) != hipSuccess) return fail(DISCO_ERR_DEVICE, "hipGetDevice failed");
     if (cur != plan->device && hipSetDevice(plan->device) != hipSuccess)
         return fail(DISCO_ERR_DEVICE, "hipSetDevice failed");
+    if (B == 0) {
+        struct Restore0 { int d; bool on; ~Restore0() { if (on) (void)hipSetDevice(d); } } r0{cur, cur != plan->device};
+        const hipError_t ez = launch_zero_fill(dw->data, (size_t)numel(dw) * elem_bytes(dw->dtype), stream);
+        return ez == hipSuccess ? ok() : hip_fail(ez, "kernel launch");
+    }
     struct Restore { int d; bool on; ~Restore() { if (on) (void)hipSetDevice(d); } } restore{cur, cur != plan->device};
     // fp32 with the 3x3 basis: Z of all channels in one pass (sweep Z mode,
     // spectral rings through a selection W); otherwise the op's own kernels

@@ -196,6 +196,20 @@ hipError_t weight_grad_dw(const T* dy, const T* zs, T* dw, float* ws, int B, int
 
 }  // namespace
 
+namespace {
+__global__ __launch_bounds__(kBlock) void k_zero_fill(uint16_t* __restrict__ p, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock) p[i] = 0;
+}
+}  // namespace
+
+hipError_t launch_zero_fill(void* p, size_t bytes, hipStream_t s) {
+    const int64_t n = (int64_t)(bytes / 2);
+    if (n == 0) return hipSuccess;
+    const unsigned blocks = (unsigned)std::min<int64_t>(1024, (n + kBlock - 1) / kBlock);
+    hipLaunchKernelGGL(k_zero_fill, dim3(blocks), dim3(kBlock), 0, s, (uint16_t*)p, n);
+    return hipGetLastError();
+}
+
 size_t weight_grad_ws_bytes_dw(int B, int C, int K, int64_t P) {
     return weight_grad_ws_bytes(B * C, 1, K, P);
 }

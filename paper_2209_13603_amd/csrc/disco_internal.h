@@ -390,6 +390,9 @@ hipError_t launch_stencil_blocked(const ExecArgs& a, const StencilDev& S, float*
 // layout) or dW[c_x][m][k] (transposed op's layout).  dtype 0 fp32, 1 bf16
 // (inputs and dW); partials in ws (weight_grad_ws_bytes).
 size_t weight_grad_ws_bytes(int B, int M, int N, int64_t P);
+// Zeros `bytes` (a multiple of 2) of device memory with a kernel (no memset
+// node when the caller captures a graph).
+hipError_t launch_zero_fill(void* p, size_t bytes, hipStream_t s);
 // Depthwise dW[c][k] = sum_{b,p} dy[b][c][p] Zs[b][c][k][p] (K <= 16), partials
 // in ws (weight_grad_ws_bytes_dw), reduced in a fixed order.
 size_t weight_grad_ws_bytes_dw(int B, int C, int K, int64_t P);

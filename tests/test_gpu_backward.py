@@ -160,3 +160,20 @@ def test_gradients_sphere2048x4096(transpose):
     say("  dx rel_l2 %.3e over %d pixels, dw rel_l2 %.3e over %d pixels" % (ex, qpix.size, ew, pix.size))
     assert ex <= FP32_TOL and ew <= FP32_TOL
     plan.close()
+
+
+@pytest.mark.parametrize("depthwise", [False, True], ids=["full", "depthwise"])
+def test_empty_batch_weight_gradient_is_zero(depthwise):
+    """dw is overwritten even for an empty batch: the sum over no pixels."""
+    import torch
+    a, b = 16, 32
+    plan = disco.Plan(a, b, a, b, 3 * math.pi / 16, backward=True)
+    x = torch.zeros((0, 3, a, b), device="cuda:0")
+    dy = torch.zeros((0, 3, a, b), device="cuda:0")
+    w = torch.full((3, 9) if depthwise else (3, 3, 9), 7.0, device="cuda:0")
+    dw = torch.full_like(w, 7.0)
+    fn = "disco_forward_depthwise_backward" if depthwise else "disco_forward_backward"
+    disco._backward(plan, fn, x, None, dy, None, dw, None)
+    torch.cuda.synchronize()
+    assert bool((dw == 0).all())
+    plan.close()
