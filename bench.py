@@ -46,6 +46,7 @@ PAPER_SECONDS = {"poles_axisym_L1024": 0.0302, "poles_axisym_L2048": 0.0898,
 # Template argument that tells two schedules' launches of one device function apart.
 KERNEL_VARIANT = {"sweep_gather_contract": ", false, ", "sweep_gather_z": ", true, "}
 COPY_PROBE_BYTES = 256 << 20   # per direction, fp32 negation used as the plain copy kernel
+EVICT_BYTES = 512 << 20       # larger than the 256 MB last-level cache (MALL)
 COPY_PROBE_KERNEL = "neg"
 
 
@@ -189,8 +190,10 @@ def copy_probe(torch, dev, reps=3):
     del a, b
 
 
-def cpu_baseline(wl, x, w, seconds=15.0):
-    """Time the oracle (as it stands) on a bounded random sample of output pixels."""
+def cpu_baseline(wl, x, w, seconds=15.0, y=None):
+    """Time the oracle (as it stands) on a bounded random sample of output
+    pixels; with ``y`` (the GPU output on the same inputs) also report the
+    parity of that output at the sampled pixels."""
     import numpy as np
     import oracle
     o = oracle.default()
@@ -208,15 +211,54 @@ def cpu_baseline(wl, x, w, seconds=15.0):
     for _ in range(6):
         pix = rng.choice(nlat * nlon, size=n, replace=False)
         t0 = time.perf_counter()
-        fn(*args, x64, w64, pix=pix, **kw)
+        ref = fn(*args, x64, w64, pix=pix, **kw)
         dt = time.perf_counter() - t0
         if dt >= 0.5 * seconds or n == nlat * nlon:
             break
         n = int(min(nlat * nlon, max(2 * n, n * seconds / max(dt, 1e-6))))
-    return {"value": n * wl.batch * wl.c_out / dt, "unit": UNIT, "cores": o.max_threads(),
-            "kind": "oracle", "seconds": round(dt, 3),
+    out = {"value": n * wl.batch * wl.c_out / dt, "unit": UNIT, "cores": o.max_threads(),
+           "kind": "oracle", "seconds": round(dt, 3),
             "sample": "%d output pixels drawn uniformly (seed 12345) of %s, all %d batch x %d "
                       "channels, fp64 ring-window mode" % (n, wl.name, wl.batch, wl.c_out)}
+    if y is not None:
+        out["parity"] = sample_parity(y, ref, pix, wl.dtype)
+    return out
+
+
+def step_percentiles(torch, step, reps, evict=None):
+    """Per-step GPU times (events on the calling stream around each step):
+    median, p10 and p90 in microseconds.  With ``evict`` (a byte tensor
+    larger than the last-level cache) every step is preceded by an untimed
+    fill of it, so the step starts with its inputs out of the caches."""
+    import numpy as np
+    if reps <= 0:
+        return None
+    times = []
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    for r in range(reps):
+        if evict is not None:
+            evict.fill_(r & 0xFF)
+        ev[0].record()
+        step()
+        ev[1].record()
+        ev[1].synchronize()
+        times.append(ev[0].elapsed_time(ev[1]) * 1e3)
+    t = np.asarray(times)
+    return {"reps": reps, "time_us_median": round(float(np.median(t)), 2),
+            "p10": round(float(np.percentile(t, 10)), 2), "p90": round(float(np.percentile(t, 90)), 2)}
+
+
+def sample_parity(y, ref, pix, dtype):
+    """Relative L2 and largest error (relative to the sample's largest
+    reference value) of the GPU output at the oracle's sampled pixels."""
+    import numpy as np
+    got = y.reshape(y.shape[0], y.shape[1], -1)[:, :, pix].astype(np.float64)
+    err = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300))
+    mx = float(np.abs(got - ref).max() / max(np.abs(ref).max(), 1e-300))
+    return {"rel_l2": err, "max_rel": mx, "pixels": int(len(pix)),
+            "tol_rel_l2": 1e-5 if dtype == "fp32" else 2e-2,
+            "pass": err <= (1e-5 if dtype == "fp32" else 2e-2)}
 
 
 def kernel_report(plan, kt, wl, transpose, algo, es, steps):
@@ -364,6 +406,10 @@ def main(argv=None):
     ap.add_argument("--workload", default=None)
     ap.add_argument("--algo", default="auto")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--reps", type=int, default=50,
+                    help="steps timed one by one for the median / p10 / p90")
+    ap.add_argument("--cold-reps", type=int, default=20,
+                    help="steps timed after a 512 MiB cache-evicting fill (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after the timed steps, run a plain copy kernel of known size "
@@ -471,6 +517,15 @@ def main(argv=None):
     log("step %.4f ms (with kernel events %.4f ms); kernels: %s"
         % (ms_per_step, ms_total / args.steps, kt))
 
+    dist = step_percentiles(torch, step, args.reps)
+    cold = None
+    if args.cold_reps > 0 and dist is not None:
+        evict = torch.empty(EVICT_BYTES, dtype=torch.uint8, device=dev)
+        cold = step_percentiles(torch, step, args.cold_reps, evict)
+        cold["evict_bytes"] = EVICT_BYTES
+        del evict
+    log("per step: warm %s; cold %s" % (dist, cold))
+
     if args.copy_probe:
         copy_probe(torch, dev)
 
@@ -531,12 +586,21 @@ def main(argv=None):
         "op_algorithmic_gbs": round(op_bytes / (ms_per_step / 1e3) / 1e9, 2),
         "kernels": per_kernel,
         "roofline": roof,
+        "step_distribution": dist,
+        "cold_cache": cold,
         "hbm_schedule": hbm,
         "plan_seconds": round(plan_s, 3),
     }
     if not args.no_cpu_baseline:
         log("timing the oracle on a bounded sample ...")
-        out["cpu_baseline"] = cpu_baseline(wl, x_np, w_np, args.cpu_seconds)
+        # The oracle reads the values the GPU holds (bf16-rounded for bf16
+        # storage), so the sample also checks the timed output.
+        step()
+        torch.cuda.synchronize()
+        xs = x.float().cpu().numpy()
+        ws = w.float().cpu().numpy()
+        ys = y.float().cpu().numpy()
+        out["cpu_baseline"] = cpu_baseline(wl, xs, ws, args.cpu_seconds, ys)
     else:
         out["cpu_baseline"] = None
     plan.close()

@@ -94,3 +94,67 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, cwd=ROOT, timeout=300)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_sample_parity_reads_the_sampled_pixels():
+    """The GPU output is compared at the flat pixels the oracle evaluated, in
+    the oracle's (batch, channel, pixel) order; a planted error at one of them
+    is seen, one at an unsampled pixel is not."""
+    import numpy as np
+    rng = np.random.default_rng(0)
+    y = rng.standard_normal((2, 3, 4, 8)).astype(np.float32)
+    pix = np.array([5, 0, 31, 17])
+    ref = y.reshape(2, 3, 32)[:, :, pix].astype(np.float64)
+    assert bench.sample_parity(y, ref, pix, "fp32")["rel_l2"] < 1e-7
+    bad = y.copy()
+    bad[1, 2, 3, 7] += 1.0                     # flat pixel 31: sampled
+    p = bench.sample_parity(bad, ref, pix, "fp32")
+    assert p["rel_l2"] > 1e-3 and not p["pass"]
+    ok = y.copy()
+    ok[0, 0, 0, 1] += 1.0                      # flat pixel 1: not sampled
+    assert bench.sample_parity(ok, ref, pix, "fp32")["pass"]
+
+
+class _FakeEvent:
+    clock = [0.0]
+
+    def __init__(self, enable_timing=True):
+        self.t = None
+
+    def record(self):
+        self.t = _FakeEvent.clock[0]
+
+    def synchronize(self):
+        pass
+
+    def elapsed_time(self, other):
+        return other.t - self.t
+
+
+class _FakeTorch:
+    class cuda:
+        Event = _FakeEvent
+
+        @staticmethod
+        def synchronize():
+            pass
+
+
+def test_step_percentiles_and_eviction():
+    """Steps of 1..10 ms give median 5.5 ms, p10 1.9 ms, p90 9.1 ms; the
+    eviction buffer is filled before every step, outside the timed span."""
+    durations = iter(range(1, 11))
+    fills = []
+
+    def step():
+        _FakeEvent.clock[0] += next(durations)
+
+    class Evict:
+        def fill_(self, v):
+            fills.append(v)
+            _FakeEvent.clock[0] += 100.0
+
+    d = bench.step_percentiles(_FakeTorch, step, 10, Evict())
+    assert d["reps"] == 10 and fills == list(range(10))
+    assert d["time_us_median"] == pytest.approx(5500.0)
+    assert d["p10"] == pytest.approx(1900.0) and d["p90"] == pytest.approx(9100.0)
