@@ -220,9 +220,23 @@ def cpu_baseline(wl, x, w, seconds=15.0, y=None):
            "kind": "oracle", "seconds": round(dt, 3),
             "sample": "%d output pixels drawn uniformly (seed 12345) of %s, all %d batch x %d "
                       "channels, fp64 ring-window mode" % (n, wl.name, wl.batch, wl.c_out)}
+    out["host_cpu"] = host_cpu()
+    out["nproc"] = os.cpu_count()
     if y is not None:
         out["parity"] = sample_parity(y, ref, pix, wl.dtype)
     return out
+
+
+def host_cpu():
+    """The host's CPU model as /proc/cpuinfo names it (None elsewhere)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def step_percentiles(torch, step, reps, evict=None):
