@@ -220,6 +220,13 @@ def cpu_baseline(wl, x, w, seconds=15.0, y=None):
            "kind": "oracle", "seconds": round(dt, 3),
             "sample": "%d output pixels drawn uniformly (seed 12345) of %s, all %d batch x %d "
                       "channels, fp64 ring-window mode" % (n, wl.name, wl.batch, wl.c_out)}
+    if nlat * nlon * wl.nlat_in * wl.nlon_in <= (128 * 256) ** 2:
+        # Small grids: the same sample without the ring window (every input
+        # pixel against every sampled output pixel), the cost the window saves.
+        t0 = time.perf_counter()
+        full = fn(*args, x64, w64, pix=pix, window=False, **kw)
+        out["all_pairs_seconds"] = round(time.perf_counter() - t0, 3)
+        out["all_pairs_max_diff"] = float(np.abs(full - ref).max())
     out["host_cpu"] = host_cpu()
     out["nproc"] = os.cpu_count()
     if y is not None:
