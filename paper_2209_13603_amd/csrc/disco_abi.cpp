@@ -448,11 +448,19 @@ Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co, int32_t dtyp
 disco_status_t check_op_args(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
                              const disco_tensor_t* w, const disco_tensor_t* y, int32_t algo);
 
+// Scratch memory the caller provides (the non-allocating entry point): the
+// kernels' workspace is taken from it and nothing is allocated; the spectral
+// rings then run on the caller's stream (no helper stream, no events).
+struct ExtScratch {
+    void* ptr;
+    size_t bytes;
+};
+
 // depthwise: x [B, C, ...], w [C, K], y [B, C, ...] (channel c filtered by
 // w[c] alone); algo is then ignored.
 disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
                       const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream, int32_t algo,
-                      bool depthwise = false);
+                      bool depthwise = false, const ExtScratch* ext = nullptr);
 
 disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
                    disco_tensor_t* y, hipStream_t stream, int32_t algo, bool transpose, bool depthwise = false) {
@@ -544,7 +552,7 @@ disco_status_t check_common(disco_plan_t plan, const disco_tensor_t* x, const di
 
 disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
                       const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream, int32_t algo,
-                      bool depthwise) {
+                      bool depthwise, const ExtScratch* ext) {
     disco_status_t s = depthwise ? check_dw_args(plan, op, x, w, y) : check_op_args(plan, op, transpose, x, w, y, algo);
     if (s != DISCO_OK) return s;
     int64_t B = x->shape[0], Ci = x->shape[1], Co = y->shape[1];
@@ -583,16 +591,20 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
         ws_sweep = sweep ? (workspace_bytes_sweep(a) + 255) / 256 * 256 : 0;
         ws = ws_spec + ws_sweep + workspace_bytes_fused(a, packed);
     }
+    if (ext && ws > ext->bytes)
+        return fail(DISCO_ERR_UNSUPPORTED, "this call needs " + std::to_string(ws) + " bytes of scratch memory; the "
+                    "non-allocating entry point has " + std::to_string(ext->bytes));
     int cur = 0;
     if (hipGetDevice(&cur) != hipSuccess) return fail(DISCO_ERR_DEVICE, "hipGetDevice failed");
     if (cur != plan->device && hipSetDevice(plan->device) != hipSuccess)
         return fail(DISCO_ERR_DEVICE, "hipSetDevice failed");
     struct Restore { int d; bool on; ~Restore() { if (on) (void)hipSetDevice(d); } } restore{cur, cur != plan->device};
 
-    if (fault_inject_alloc()) return fail(DISCO_ERR_OUT_OF_MEMORY, "allocation failure injected (DISCO_FAULT_INJECT=alloc)");
-    float* ws_ptr = nullptr;
+    if (!ext && fault_inject_alloc())
+        return fail(DISCO_ERR_OUT_OF_MEMORY, "allocation failure injected (DISCO_FAULT_INJECT=alloc)");
+    float* ws_ptr = ext ? (float*)ext->ptr : nullptr;
     hipError_t e = hipSuccess;
-    if (ws > 0) {
+    if (ws > 0 && !ext) {
         e = hipMallocAsync((void**)&ws_ptr, ws, stream);
         if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(workspace)");
     }
@@ -613,7 +625,7 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
         // the light rings, the general kernel's remaining rings follow the
         // spectral ones there.
         hipEvent_t fork = nullptr, join = nullptr;
-        const bool fork_aux = spectral && plan->aux;
+        const bool fork_aux = spectral && plan->aux && !ext;
         ExecArgs as = a;
         if (fork_aux) {
             as.stream = plan->aux;
@@ -638,7 +650,7 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
         if (fork) (void)hipEventDestroy(fork);
         if (join) (void)hipEventDestroy(join);
     }
-    hipError_t e2 = ws_ptr ? hipFreeAsync(ws_ptr, stream) : hipSuccess;
+    hipError_t e2 = ws_ptr && !ext ? hipFreeAsync(ws_ptr, stream) : hipSuccess;
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     if (e2 != hipSuccess) return hip_fail(e2, "hipFreeAsync(workspace)");
     return ok();
@@ -703,6 +715,9 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
             if ((s = check_device_ptr(dy->data, plan->device, "dy")) != DISCO_OK) return s;
             if (overlaps(dw, x) || overlaps(dw, dy) || (dx && overlaps(dw, dx)))
                 return fail(DISCO_ERR_INVALID_ARGUMENT, "dw overlaps another tensor");
+            // dx is written before the weight gradient's pass reads x.
+            if (dx && dx->data && overlaps(dx, x))
+                return fail(DISCO_ERR_INVALID_ARGUMENT, "dx overlaps x (x is read for dw after dx is written)");
         }
         xz = *x;
         xz.shape[0] = B * C_x;
@@ -791,6 +806,17 @@ std::vector<TimedLaunch> g_timed;
 }  // namespace
 
 namespace disco {
+
+int plan_device(const disco_plan* plan) { return plan->device; }
+
+disco_status_t set_last_error(disco_status_t s, const char* msg) { return fail(s, msg); }
+
+disco_status_t forward_with_scratch(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                                    disco_tensor_t* y, hipStream_t stream, void* scratch, size_t bytes) {
+    if (!plan) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan is NULL");
+    const ExtScratch ext{scratch, bytes};
+    return run_op(plan, plan->fwd, false, x, w, y, stream, DISCO_ALGO_AUTO, false, &ext);
+}
 
 int timing_begin(const char* name, hipStream_t s) {
     if (!g_timing_on.load(std::memory_order_relaxed)) return -1;

@@ -44,15 +44,18 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
 __device__ __forceinline__ void store_val(float* p, int64_t i, float v) { p[i] = v; }
 __device__ __forceinline__ void store_val(uint16_t* p, int64_t i, float v) { p[i] = to_bf16(v); }
 
-// grid: (n_chunks, n_mt * n_nt, B).  partial: [B][n_chunks][M][N].
+// grid: (n_chunks * n_mt * n_nt, 1, B), the pixel chunk fastest in x (grid x
+// has no 16-bit limit, so any number of tiles fits).  partial:
+// [B][n_chunks][M][N].
 template <typename T>
 __global__ __launch_bounds__(kBlock) void k_weight_grad(const T* __restrict__ dy, const T* __restrict__ zs,
                                                         float* __restrict__ partial, int M, int N, int64_t P,
-                                                        int64_t chunk_len, int n_nt) {
+                                                        int64_t chunk_len, int n_nt, int n_chunks) {
     __shared__ float red[kBlock / 64][kTileM * kTileN];
     const int tid = threadIdx.x;
-    const int chunk = blockIdx.x;
-    const int m0 = (blockIdx.y / n_nt) * kTileM, n0 = (blockIdx.y % n_nt) * kTileN;
+    const int chunk = (int)(blockIdx.x % (unsigned)n_chunks);
+    const int tile = (int)(blockIdx.x / (unsigned)n_chunks);
+    const int m0 = (tile / n_nt) * kTileM, n0 = (tile % n_nt) * kTileN;
     const int b = blockIdx.z;
     const int64_t p0 = (int64_t)chunk * chunk_len;
     const int64_t p1 = p0 + chunk_len < P ? p0 + chunk_len : P;
@@ -92,7 +95,7 @@ __global__ __launch_bounds__(kBlock) void k_weight_grad(const T* __restrict__ dy
 #pragma unroll
         for (int w = 0; w < kBlock / 64; ++w) v += red[w][tid];
         if (m0 + i < M && n0 + j < N)
-            partial[(((int64_t)b * gridDim.x + chunk) * M + m0 + i) * N + n0 + j] = v;
+            partial[(((int64_t)b * n_chunks + chunk) * M + m0 + i) * N + n0 + j] = v;
     }
 }
 
@@ -162,9 +165,9 @@ hipError_t weight_grad(const T* dy, const T* zs, T* dw, float* ws, int B, int M,
     const int64_t len = chunk_len_for(B, M, N, P);
     const int n_chunks = (int)std::max<int64_t>(1, (P + len - 1) / len);
     const int n_mt = (M + kTileM - 1) / kTileM, n_nt = (N + kTileN - 1) / kTileN;
-    dim3 grid((unsigned)n_chunks, (unsigned)(n_mt * n_nt), (unsigned)B);
+    dim3 grid((unsigned)((int64_t)n_chunks * n_mt * n_nt), 1u, (unsigned)B);
     int tk = timing_begin("weight_grad", s);
-    hipLaunchKernelGGL((k_weight_grad<T>), grid, dim3(kBlock), 0, s, dy, zs, ws, M, N, P, len, n_nt);
+    hipLaunchKernelGGL((k_weight_grad<T>), grid, dim3(kBlock), 0, s, dy, zs, ws, M, N, P, len, n_nt, n_chunks);
     timing_end(tk, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -183,7 +186,7 @@ hipError_t weight_grad_dw(const T* dy, const T* zs, T* dw, float* ws, int B, int
     const int n_chunks = (int)std::max<int64_t>(1, (P + len - 1) / len);
     dim3 grid((unsigned)n_chunks, 1u, (unsigned)items);
     int tk = timing_begin("weight_grad", s);
-    hipLaunchKernelGGL((k_weight_grad<T>), grid, dim3(kBlock), 0, s, dy, zs, ws, 1, K, P, len, 1);
+    hipLaunchKernelGGL((k_weight_grad<T>), grid, dim3(kBlock), 0, s, dy, zs, ws, 1, K, P, len, 1, n_chunks);
     timing_end(tk, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

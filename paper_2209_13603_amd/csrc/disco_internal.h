@@ -8,6 +8,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include "disco.h"
+
 namespace disco {
 
 // Values stored per psi entry: the nine functions of the 3x3 basis, the four
@@ -340,6 +342,18 @@ struct ExecArgs {
     // the filter W[i mod dw_c][.] of a [C][K] weight tensor; 0 = full W.
     int dw_c = 0;
 };
+
+// The plan's device (the one that created it).
+int plan_device(const disco_plan* plan);
+// Records msg as this thread's last error and returns s.
+disco_status_t set_last_error(disco_status_t s, const char* msg);
+// disco_forward with every kernel's workspace taken from `scratch` (`bytes`
+// bytes of device memory on the plan's device) instead of the stream-ordered
+// pool: nothing is allocated and the spectral rings run on `stream` itself.
+// A call that needs more than `bytes` fails with DISCO_ERR_UNSUPPORTED before
+// anything is enqueued.
+disco_status_t forward_with_scratch(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                                    disco_tensor_t* y, hipStream_t stream, void* scratch, size_t bytes);
 
 // Kernel timing hook: when enabled, brackets a launch with events on `s`.
 // Returns the token to pass to timing_end (or -1 when disabled).

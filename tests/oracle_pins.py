@@ -81,6 +81,77 @@ def pin_quadrature_unique(o):
         assert np.allclose(q, w, rtol=0, atol=1e-12), (n, np.abs(q - w).max())
 
 
+def _cell_area_weights(n, nlon):
+    """Area of the cell of ring t of the cell-centred grid divided among the
+    ring's nlon pixels: the spherical band between colatitudes t pi / n and
+    (t + 1) pi / n has area 2 pi (cos(t pi / n) - cos((t + 1) pi / n))."""
+    t = np.arange(n)
+    return (2 * math.pi / nlon) * (np.cos(t * math.pi / n) - np.cos((t + 1) * math.pi / n))
+
+
+def pin_quadrature_cell_area(o):
+    """Cell-area quadrature (the alternative rule the plan can select on the
+    cell-centred grid): each ring's weight is the area of its latitude band
+    divided by nlon (a difference of cosines, computed here independently),
+    the weights total 4 pi, and the forward and transposed ops apply exactly
+    these weights (dense products with Psi against the looped sums, and the
+    centre value of a delta input)."""
+    for n in (1, 2, 3, 7, 32, 129, 2048):
+        for nlon in (2, 64, 4096):
+            q = o.quadrature(n, nlon, kind=1)
+            ref = _cell_area_weights(n, nlon)
+            # the cosine difference cancels: its error is a few ulps of 2 pi / nlon
+            assert np.abs(q - ref).max() <= 8 * np.finfo(float).eps * 2 * math.pi / nlon, (n, nlon)
+            assert abs(q.sum() * nlon - 4 * math.pi) <= 1e-13 * 4 * math.pi, (n, nlon)
+    for (a, b, c, d) in _DENSE_CASES:
+        tc = 3 * math.pi / min(a, c)
+        psi = o.psi_dense(a, b, c, d, tc)                  # [Nout, Nin, 9]
+        qi = np.repeat(_cell_area_weights(a, b), b)
+        qo = np.repeat(_cell_area_weights(c, d), d)
+        x, w = _xw(40, 2, 3, a, b, 4)
+        Z = np.einsum("jik,bci->bckj", psi, x.reshape(2, 3, -1) * qi)
+        y_dense = np.einsum("ock,bckj->boj", w, Z).reshape(2, 4, c, d)
+        y = o.forward(a, b, c, d, tc, x, w, quad=1)
+        assert np.abs(y - y_dense).max() <= 1e-13 * np.abs(y_dense).max()
+        xT, wT = _xw(41, 2, 4, c, d, 4)
+        wT = wT.reshape(4, 4, 9)[:, :3]
+        ZT = np.einsum("jik,bcj->bcki", psi, xT.reshape(2, 4, -1) * qo)
+        yT_dense = np.einsum("cok,bcki->boi", wT, ZT).reshape(2, 3, a, b)
+        yT = o.transpose(a, b, c, d, tc, xT, wT, quad=1)
+        assert np.abs(yT - yT_dense).max() <= 1e-13 * np.abs(yT_dense).max()
+    a, b = 16, 32
+    x = np.zeros((1, 1, a, b))
+    x[0, 0, 3, 7] = 1.0
+    Z = o.forward(a, b, a, b, 3 * math.pi / a, x, _select_w(), quad=1)[0]
+    assert abs(Z[4, 3, 7] - _cell_area_weights(a, b)[3]) <= 1e-14 * _cell_area_weights(a, b)[3]
+
+
+def pin_node_spacing_override(o):
+    """A node spacing h other than the default moves the hats' nodes (Sec. 3.4:
+    equally spaced nodes, linear interpolation): with a delta input one ring
+    south of the output point, on the same meridian, the tangent-plane point
+    is (u, v) = (d, 0) with d the ring step, so the 3x3 basis gives
+    psi_4 = 1 - d / h and psi_7 = d / h for h >= d (closed form), and the
+    axisymmetric basis psi_1 = 2 - d / h, psi_2 = d / h - 1 for h <= d < 2 h,
+    all times the input ring's quadrature weight."""
+    a, b = 16, 32
+    tc = 3 * math.pi / a
+    d = math.pi / a
+    q = o.quadrature(a, b)
+    x = np.zeros((1, 1, a, b))
+    x[0, 0, 7, 5] = 1.0
+    for h in (tc / 2, 0.4 * tc):
+        Z = o.forward(a, b, a, b, tc, x, _select_w(), h=h)[0]
+        e = np.zeros(9)
+        e[4] = (1 - d / h) * q[7]
+        e[7] = d / h * q[7]
+        assert np.abs(Z[:, 6, 5] - e).max() <= 1e-14 * q[7], (h, Z[:, 6, 5], e)
+    h = 0.6 * d
+    Z = o.forward(a, b, a, b, tc, x, np.eye(4).reshape(4, 1, 4), h=h, basis=1)[0]
+    e = np.array([0.0, 2 - d / h, d / h - 1, 0.0]) * q[7]
+    assert np.abs(Z[:, 6, 5] - e).max() <= 1e-14 * q[7], (Z[:, 6, 5], e)
+
+
 def pin_grid(o):
     """Cell-centred equiangular grid: colatitude (t + 1/2) pi / nlat,
     longitude 2 pi p / nlon."""

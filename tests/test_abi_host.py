@@ -96,23 +96,26 @@ PLAN_CASES = [
 ]
 
 
-def _dense_check(case, transpose, sampling=0, basis=0):
+def _dense_check(case, transpose, sampling=0, basis=0, quad=0, h_scale=None):
+    """h_scale: node spacing as a multiple of theta_c (None: the default)."""
     a, b, c, d = case
     K = {1: 4, 2: 16}.get(basis, 9)
     # theta_c = 3 pixels of the coarser grid (the pole-including grid has
     # nlat - 1 ring spacings).
     tc = 3 * math.pi / (min(a, c) - (1 if sampling == 1 else 0))
+    h = 0.0 if h_scale is None else h_scale * tc
     o = oracle.default()
-    psi = o.psi_dense(a, b, c, d, tc, sampling=sampling, basis=basis)  # [Nout_plan, Nin_plan, K]
+    psi = o.psi_dense(a, b, c, d, tc, h=h or None, sampling=sampling, basis=basis)  # [Nout_plan, Nin_plan, K]
     if not transpose:
         nlat_o, nlon_o, nlat_i, nlon_i = c, d, a, b
-        q = o.quadrature(a, b, sampling=sampling)
+        q = o.quadrature(a, b, kind=quad, sampling=sampling)
         dense = psi                           # [op out pixel, op in pixel, K]
     else:
         nlat_o, nlon_o, nlat_i, nlon_i = a, b, c, d
-        q = o.quadrature(c, d, sampling=sampling)
+        q = o.quadrature(c, d, kind=quad, sampling=sampling)
         dense = psi.transpose(1, 0, 2)        # filter centred at the op's input points
-    ent = disco.psi_entries(a, b, c, d, tc, transpose=transpose, basis=basis, sampling=sampling)
+    ent = disco.psi_entries(a, b, c, d, tc, transpose=transpose, basis=basis, sampling=sampling,
+                            quadrature=quad, node_spacing=h)
     assert not ent["values"][:, K:].any()
     P, s = ent["phases"], ent["stride"]
     assert (P, s) == ((1, nlon_i // nlon_o) if nlon_i % nlon_o == 0 else (nlon_o // nlon_i, 1))
@@ -185,6 +188,23 @@ def test_plan_entries_poles_bilinear_match_dense_psi(case, transpose):
 @pytest.mark.parametrize("case", PLAN_CASES[:3])
 def test_plan_entries_axisym_cell_centred_match_dense_psi(case, transpose):
     _dense_check(case, transpose, sampling=0, basis=1)
+
+
+# Cell-area quadrature and node spacings other than the default (the
+# options disco_basis_t carries).  No spacing puts a node or a hat edge exactly
+# at the cutoff, where fp64 rounding of the two geometry routes decides.
+@pytest.mark.parametrize("transpose", [False, True])
+@pytest.mark.parametrize("case", PLAN_CASES[:3])
+@pytest.mark.parametrize("basis", [0, 1])
+def test_plan_entries_cell_area_match_dense_psi(case, transpose, basis):
+    _dense_check(case, transpose, sampling=0, basis=basis, quad=1)
+
+
+@pytest.mark.parametrize("transpose", [False, True])
+@pytest.mark.parametrize("case", PLAN_CASES[:3])
+@pytest.mark.parametrize("basis,h_scale", [(0, 0.5), (0, 0.25), (1, 0.22), (2, 0.2)])
+def test_plan_entries_node_spacing_match_dense_psi(case, transpose, basis, h_scale):
+    _dense_check(case, transpose, sampling=0, basis=basis, h_scale=h_scale)
 
 
 # The separable basis (Sec. 3.4: four nodes along theta times four periodic

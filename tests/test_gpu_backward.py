@@ -119,6 +119,57 @@ def test_backward_needs_the_plan_flag():
     plan.close()
 
 
+def test_dx_aliasing_x_is_rejected_when_dw_is_asked_for():
+    """dx is written before x is read for dw: a dx that overlaps x is an
+    argument error then (nothing enqueued), and allowed when dw is not asked
+    for (x is not read)."""
+    import torch
+    plan = disco.Plan(16, 32, 16, 32, 3 * math.pi / 16, backward=True)
+    x, w = synth.random_inputs(71, (1, 2, 16, 32), (2, 2, 9))
+    dy = synth.random_inputs(72, (1, 2, 16, 32), (1,))[0]
+    xt, wt, dyt = torch_dev(x), torch_dev(w), torch_dev(dy)
+    dw = torch.empty((2, 2, 9), device="cuda:0")
+    with pytest.raises(disco.DiscoError) as ei:
+        disco._backward(plan, "disco_forward_backward", xt, wt, dyt, xt, dw, None)
+    assert ei.value.status == disco.DISCO_ERR_INVALID_ARGUMENT
+    torch.cuda.synchronize()
+    assert np.array_equal(to_numpy(xt), x.astype(np.float64))  # nothing was written
+    disco._backward(plan, "disco_forward_backward", None, wt, dyt, xt, None, None)
+    torch.cuda.synchronize()
+    ref = oracle.default().input_grad(16, 32, 16, 32, 3 * math.pi / 16, dy.astype(np.float64),
+                                      w.astype(np.float64))
+    assert rel_l2(to_numpy(xt), ref) <= FP32_TOL
+    plan.close()
+
+
+def test_weight_gradient_1024_channels():
+    """1024 -> 1024 channels: the weight gradient's tiles (128 x 576 of them)
+    exceed a 16-bit grid dimension, which the kernel's grid does not use."""
+    import torch
+    a, b, c, d = 16, 32, 8, 16
+    tc = 3 * math.pi / c
+    C = 1024
+    r = np.random.default_rng(73)
+    x = r.standard_normal((1, C, a, b)).astype(np.float32)
+    dy = r.standard_normal((1, C, c, d)).astype(np.float32)
+    w = np.zeros((C, C, 9), np.float32)
+    plan = disco.Plan(a, b, c, d, tc, backward=True)
+    say("weight gradient", C, "channels")
+    _, dw = disco.forward_backward(plan, torch_dev(x), torch_dev(w), torch_dev(dy), want_dx=False)
+    torch.cuda.synchronize()
+    got = to_numpy(dw)
+    # Z of every input channel through the oracle (one-channel items, identity W).
+    sel = np.zeros((9, 1, 9))
+    for k in range(9):
+        sel[k, 0, k] = 1.0
+    Z = oracle.default().forward(a, b, c, d, tc, x.reshape(C, 1, a, b).astype(np.float64), sel)
+    ref = np.einsum("op,ikp->oik", dy.reshape(C, -1).astype(np.float64), Z.reshape(C, 9, -1))
+    err = rel_l2(got, ref)
+    say("  rel_l2 %.3e" % err)
+    assert err <= FP32_TOL
+    plan.close()
+
+
 @pytest.mark.parametrize("transpose", [False, True], ids=["forward", "transpose"])
 def test_gradients_sphere2048x4096(transpose):
     """The 2048 x 4096 sphere, 8 -> 8 channels: dx on sampled pixels; dW with

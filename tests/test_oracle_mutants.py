@@ -18,6 +18,12 @@ MUTANTS = {
     "fejer_denominator": ("(4.0 * (double)m * (double)m - 1.0)",
                           "(4.0 * (double)m * (double)m + 1.0)"),
     "fejer_last_term": ("m <= nlat / 2;", "m < nlat / 2;"),
+    "cell_area_full_step": ("w = 2.0 * sin(th) * sin(0.5 * M_PI / nlat);",
+                            "w = 2.0 * sin(th) * sin(M_PI / nlat);"),
+    "cell_area_cosine": ("w = 2.0 * sin(th) * sin(0.5 * M_PI / nlat);",
+                         "w = 2.0 * cos(th) * sin(0.5 * M_PI / nlat);"),
+    "quadrature_kind_ignored": ("oracle_quadrature_s(g_in.nlat, g_in.nlon, smp, cfg.quad_kind, q_in)",
+                                "oracle_quadrature_s(g_in.nlat, g_in.nlon, smp, 0, q_in)"),
     "colatitude_scale": ("(t + 0.5) * M_PI / (double)nlat", "(t + 0.5) * M_PI / (double)(nlat + 1)"),
     "longitude_direction": ("2.0 * M_PI * (double)p / (double)nlon",
                             "-2.0 * M_PI * (double)p / (double)nlon"),
@@ -28,6 +34,9 @@ MUTANTS = {
     "transpose_w_not_transposed": ("double wv = transpose ? w[((int64_t)ci * Cout + co) * K + k]",
                                    "double wv = transpose ? w[((int64_t)co * Cin + ci) * K + k]"),
     "basis_index_order": ("psi[3 * a + b] = hat", "psi[3 * b + a] = hat"),
+    "node_spacing_ignored": ("        oracle_basis(u, v, h, psi);", "        oracle_basis(u, v, theta_c / 3.0, psi);"),
+    "axisym_node_spacing_ignored": ("        oracle_basis_axisym(Th, h, psi);",
+                                    "        oracle_basis_axisym(Th, theta_c / 4.0, psi);"),
     "hat_shape": ("return a < 1.0 ? 1.0 - a : 0.0;", "return a < 1.0 ? 1.0 - a * a : 0.0;"),
     "cutoff_too_small": ("if (Th > theta_c) return 0;", "if (Th > 0.5 * theta_c) return 0;"),
     "window_too_narrow": ("if (window && fabs(th_i - th_o) > theta_c) continue;",
