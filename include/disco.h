@@ -265,6 +265,25 @@ disco_status_t disco_transpose_depthwise_backward(disco_plan_t plan, const disco
                                                   const disco_tensor_t* w, const disco_tensor_t* dy,
                                                   disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream);
 
+/* disco_forward for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, result and errors as disco_forward, except that the
+ * kernels' scratch memory (the spectral rings' transforms, the fp32 partial
+ * outputs of channel groups and of split patterns) comes from one fixed
+ * device array of 64 MiB (67108864 bytes) per GPU, which the library holds
+ * from the first call on that GPU until the process ends, and that the
+ * spectral rings run on `stream` itself instead of beside it.  The call
+ * allocates nothing (no hipMalloc, hipMallocAsync, hipFree or event).  A call
+ * that needs more scratch than that (2048 x 4096 with 8 -> 8 channels and
+ * batch 1 needs about 43 MB) fails with DISCO_ERR_UNSUPPORTED, naming both
+ * sizes, before anything is enqueued.  Every call on one GPU shares that
+ * GPU's array: calls that overlap in time on one GPU (several streams or
+ * host threads) race and must be serialised by the caller.  Every kernel
+ * writes the part of the array it reads before reading it, so nothing needs
+ * clearing between calls. */
+disco_status_t disco_forward_noalloc(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
+                                     disco_tensor_t* y, hipStream_t stream);
+
 /* Host-only export of the stored psi entries of one op, without any device
  * (Sec. 4.1: Psi is constructed explicitly, only where it is non-zero).
  * transpose = 0 selects the forward op, 1 the transposed op.  Each entry is

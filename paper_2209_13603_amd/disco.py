@@ -53,7 +53,7 @@ EXPORTS = ("disco_plan_create", "disco_plan_destroy", "disco_plan_query", "disco
            "disco_transpose", "disco_forward_algo", "disco_transpose_algo", "disco_forward_backward",
            "disco_transpose_backward", "disco_forward_depthwise", "disco_transpose_depthwise",
            "disco_forward_depthwise_backward", "disco_transpose_depthwise_backward",
-           "disco_psi_entries",
+           "disco_psi_entries", "disco_forward_noalloc",
            "disco_kernel_timing_enable", "disco_kernel_timing_read", "disco_kernel_work",
            "disco_status_string", "disco_last_error")
 
@@ -116,7 +116,8 @@ def library(path: str = LIB_PATH) -> ctypes.CDLL:
                                                            P(ctypes.c_void_p)]
     lib.disco_plan_destroy.argtypes = [ctypes.c_void_p]
     lib.disco_plan_query.argtypes = [ctypes.c_void_p, P(PlanInfo)]
-    for name in ("disco_forward", "disco_transpose", "disco_forward_depthwise", "disco_transpose_depthwise"):
+    for name in ("disco_forward", "disco_transpose", "disco_forward_depthwise", "disco_transpose_depthwise",
+                 "disco_forward_noalloc"):
         getattr(lib, name).argtypes = [ctypes.c_void_p, P(Tensor), P(Tensor), P(Tensor),
                                        ctypes.c_void_p]
     for name in ("disco_forward_algo", "disco_transpose_algo"):
@@ -133,7 +134,8 @@ def library(path: str = LIB_PATH) -> ctypes.CDLL:
                                          P(ctypes.c_int32)])
     for name in ("disco_plan_create", "disco_plan_destroy", "disco_plan_query", "disco_forward",
                  "disco_transpose", "disco_forward_algo", "disco_transpose_algo",
-                 "disco_forward_depthwise", "disco_transpose_depthwise", "disco_psi_entries"):
+                 "disco_forward_depthwise", "disco_transpose_depthwise", "disco_psi_entries",
+                 "disco_forward_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     lib.disco_kernel_timing_enable.argtypes = [ctypes.c_int32]
     lib.disco_kernel_timing_enable.restype = ctypes.c_int
@@ -258,6 +260,14 @@ class Plan:
             y = torch.empty((x.shape[0], w.shape[0]) + self.grid_out, dtype=x.dtype,
                             device=x.device)
         return self._run("disco_forward_algo", x, w, y, algo, stream)
+
+    def forward_noalloc(self, x, w, y, stream=None):
+        """disco_forward_noalloc: the forward op with its scratch memory in the
+        library's fixed per-GPU array (nothing allocated; y must be given)."""
+        tx, tw, ty = _tensor(x), _tensor(w), _tensor(y)
+        _check(library().disco_forward_noalloc(self._h, ctypes.byref(tx), ctypes.byref(tw),
+                                               ctypes.byref(ty), _stream(stream)))
+        return y
 
     def transpose(self, x, w, y=None, algo="auto", stream=None):
         """y[B, CoutT, nlat_in, nlon_in] = DISCO^T(x[B, CinT, nlat_out, nlon_out]; w[CinT, CoutT, K])."""
