@@ -69,44 +69,114 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def kernel_model(name, wl, work, es):
-    """Algorithmic (bytes, flops, bound) of one launch of kernel `name`.
+PEAK_TFLOPS = {"valu": FP32_VALU_PEAK_TFLOPS, "mfma_f32": FP32_MFMA_PEAK_TFLOPS,
+               "mfma_bf16": BF16_MFMA_PEAK_TFLOPS}
+
+
+def fft_flops(n):
+    """Flops of one real n-point FFT (half the 5 n log2 n of a complex one)."""
+    return 2.5 * n * math.log2(n) if n > 1 else 0.0
+
+
+def kernel_model(name, wl, work, es, spec=None):
+    """Algorithmic work of one launch of kernel `name`: a dict with `bytes`,
+    the flops per execution unit (`valu`: fp32 vector FMAs; `mfma_f32` /
+    `mfma_bf16`: matrix-core products of that input type), and `bound`.
 
     `work` = (out_pixels, in_pixels, pairs) per batch item and channel, as
     the library reports it for this kernel.  Per unit figures: every output
     pixel x channel written costs es bytes, every input pixel x channel read
     es bytes; the sparse gather costs 2 flop per non-zero (pixel pair, k) per
-    gathered channel, the channel contraction 2 * 9 * Cin flop per output
-    pixel x output channel.  The two-kernel path also moves its fp32
-    intermediate (9 planes per channel), which its kernels must write and
-    read.
+    gathered channel (VALU), the channel contraction 2 * 9 * Cin flop per
+    output pixel x output channel (matrix cores: fp32 in the ring sweep,
+    bf16 in the general kernel with bf16 storage).  The two-kernel path also
+    moves its fp32 intermediate (9 planes per channel), which its kernels must
+    write and read.  The spectral kernels count their own work: a real FFT of
+    each ring (2.5 N log2 N flop) and, per (ring pair, frequency), 36 flop per
+    input channel for the three basis rows plus 36 per (input, output
+    channel) pair and output frequency for the weights; `spec` gives the op's
+    spectral structure from the plan ({"rings", "pairs", "slots"}: output
+    rings, (output ring, input ring) pairs, input rings transformed).
     """
     B, Ci, Co = wl.batch, wl.c_in, wl.c_out
     if getattr(wl, "depthwise", False):
         # B x C one-channel items, each filtered by its channel's own filter.
         B, Ci, Co = B * Ci, 1, 1
     outp, inp, pairs = work
+    fwd = getattr(wl, "op", "forward") == "forward"
+    n_in = wl.nlon_in if fwd else wl.nlon_out     # ring length of the op's input grid
+    n_out = wl.nlon_out if fwd else wl.nlon_in
+    m = dict(bytes=0.0, valu=0.0, mfma_f32=0.0, mfma_bf16=0.0, bound="alu")
     if name in ("stencil", "stencil_blocked"):
         # W folded into psi: 2 flop per stored (output pixel, input pixel)
         # pair per channel pair; bound by whichever roof is lower.
-        b_ = B * Ci * inp * es + B * Co * outp * es
-        f_ = 2.0 * pairs * B * Ci * Co
-        bound = "hbm" if b_ / (HBM_PEAK_GBS * 1e9) > f_ / (FP32_VALU_PEAK_TFLOPS * 1e12) else "alu"
-        return (b_, f_, bound)
-    if name == "convert_y":
+        m["bytes"] = B * Ci * inp * es + B * Co * outp * es
+        m["valu"] = 2.0 * pairs * B * Ci * Co
+        m["bound"] = "hbm" if m["bytes"] / (HBM_PEAK_GBS * 1e9) > m["valu"] / (FP32_VALU_PEAK_TFLOPS * 1e12) \
+            else "alu"
+    elif name == "convert_y":
         # fp32 partial sums read, bf16 output written, per covered pixel.
-        return (B * Co * outp * (4 + es), 0.0, "hbm")
-    if name in ("gather_z", "sweep_gather_z"):
-        return (B * Ci * inp * es + B * Ci * 9 * outp * 4, 2.0 * pairs * B * Ci, "hbm")
-    if name == "contract_z":
-        return (B * Ci * 9 * outp * 4 + B * Co * outp * es, 2.0 * B * Ci * 9 * Co * outp, "hbm")
-    if name == "contract_x":
-        return (B * Ci * inp * es + B * Co * 9 * inp * 4, 2.0 * B * Ci * 9 * Co * inp, "hbm")
-    if name == "gather_y":
-        return (B * Co * 9 * inp * 4 + B * Co * outp * es, 2.0 * pairs * B * Co, "hbm")
-    # fused kernels: x in, y out, gather over the input channels, contraction per output
-    fl = 2.0 * pairs * B * Ci + 2.0 * B * Ci * 9 * Co * outp
-    return (B * Ci * inp * es + B * Co * outp * es, fl, "alu")
+        m.update(bytes=B * Co * outp * (4 + es), bound="hbm")
+    elif name in ("gather_z", "sweep_gather_z"):
+        m.update(bytes=B * Ci * inp * es + B * Ci * 9 * outp * 4, valu=2.0 * pairs * B * Ci, bound="hbm")
+    elif name == "contract_z":
+        m.update(bytes=B * Ci * 9 * outp * 4 + B * Co * outp * es, valu=2.0 * B * Ci * 9 * Co * outp, bound="hbm")
+    elif name == "contract_x":
+        m.update(bytes=B * Ci * inp * es + B * Co * 9 * inp * 4, valu=2.0 * B * Ci * 9 * Co * inp, bound="hbm")
+    elif name == "gather_y":
+        m.update(bytes=B * Co * 9 * inp * 4 + B * Co * outp * es, valu=2.0 * pairs * B * Co, bound="hbm")
+    elif name.startswith("spectral_"):
+        if not spec:
+            raise SystemExit("kernel %s needs the plan's spectral structure" % name)
+        mi, mo = n_in // 2 + 1, n_out // 2 + 1
+        if name == "spectral_rfft":
+            m["bytes"] = B * Ci * spec["slots"] * (n_in * es + mi * 8)
+            m["valu"] = B * Ci * spec["slots"] * fft_flops(n_in)
+        elif name == "spectral_mac":
+            # per (ring pair, frequency): the input transform of each input
+            # channel and 9 psi values read; per output bin: Yhat written
+            m["bytes"] = (B * Ci * 8 + 9 * 4) * spec["pairs"] * mi + B * Co * spec["rings"] * mi * 8
+            m["valu"] = 36.0 * B * Ci * spec["pairs"] * mi + 36.0 * B * Ci * Co * spec["rings"] * mi
+        else:
+            m["bytes"] = B * Co * spec["rings"] * (mo * 8 + n_out * es)
+            m["valu"] = B * Co * spec["rings"] * fft_flops(n_out)
+    elif name in ("fused_gather_contract", "sweep_gather_contract"):
+        # x in, y out, gather over the input channels (VALU), contraction per
+        # output (matrix cores).
+        m["bytes"] = B * Ci * inp * es + B * Co * outp * es
+        m["valu"] = 2.0 * pairs * B * Ci
+        dt = "mfma_bf16" if (name == "fused_gather_contract" and es == 2) else "mfma_f32"
+        m[dt] = 2.0 * B * Ci * 9 * Co * outp
+    elif name == "reduce_partials":
+        m.update(bound="hbm")
+    else:
+        raise SystemExit("no work model for kernel %s" % name)
+    m["flops"] = m["valu"] + m["mfma_f32"] + m["mfma_bf16"]
+    return m
+
+
+def spectral_spec(plan, transpose):
+    """The op's spectral structure from the plan's info."""
+    info = plan.info()
+    sfx = "transpose" if transpose else "forward"
+    return {"rings": info["spectral_rings_" + sfx], "pairs": info["spectral_pairs_" + sfx],
+            "slots": info["spectral_slots_" + sfx]}
+
+
+def model_roof(m, avg_s):
+    """Achieved rate of one launch of modelled work `m` lasting avg_s seconds,
+    against the bound: HBM bytes at the HBM peak, or the arithmetic at each
+    unit's own peak (VALU fp32, fp32 and bf16 matrix cores), the unit times
+    added (they share one issue port).  `peak` is then the rate the kernel's
+    mix of work would reach with every unit at its peak."""
+    if m["bound"] == "hbm":
+        ach = m["bytes"] / avg_s / 1e9
+        return {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS}
+    t_bound = sum(m[u] / (PEAK_TFLOPS[u] * 1e12) for u in PEAK_TFLOPS)
+    ach = m["flops"] / avg_s / 1e12
+    peak = m["flops"] / t_bound / 1e12 if t_bound > 0 else FP32_VALU_PEAK_TFLOPS
+    return {"bound": "alu", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+            "frac": (t_bound / avg_s) if t_bound > 0 else 0.0}
 
 
 def traffic_path(kernel, workload):
@@ -128,6 +198,65 @@ def load_traffic(kernel, workload):
     if kv.get("library_source_sha256_16") != kernel_source_digest():
         return None
     return float(kv["hbm_bytes_per_launch"])
+
+
+COUNTER_SET = ("MfmaUtil", "VALUBusy", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_WAIT_ANY", "SQ_WAVE_CYCLES")
+
+
+def counters_path(kernel, workload):
+    return os.path.join(ROOT, "profiles", "counters_%s_%s.txt" % (kernel, workload))
+
+
+def load_counters(kernel, workload):
+    """Matrix-core and VALU busy fractions of `kernel` from the committed
+    counter summary (None when absent or taken on different library sources)."""
+    out = {"mfma_busy": None, "valu_busy": None, "wait_frac": None}
+    path = counters_path(kernel, workload)
+    if not os.path.exists(path):
+        return out
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith((" ", "#", "-")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip().split()[0] if v.strip() else ""
+    if kv.get("library_source_sha256_16") != kernel_source_digest():
+        return out
+    for k in out:
+        out[k] = float(kv[k]) if k in kv else None
+    return out
+
+
+def counter_summary(csv_path, kernel, workload, commands):
+    """Write profiles/counters_<kernel>_<workload>.txt from one rocprofv3
+    --pmc run of COUNTER_SET: MfmaUtil and VALUBusy are rocprofv3's derived
+    metrics (matrix-core busy cycles per SIMD, VALU-active cycles per CU, as
+    percentages of the GPU's busy cycles), averaged over the kernel's
+    dispatches."""
+    dev = DEVICE_KERNEL[kernel]
+    sel = KERNEL_VARIANT.get(kernel, "")
+    rows = _pmc_rows(csv_path)
+    ks = [cs for n, cs in rows.values() if ((dev + "<") in n or n.split("(")[0].endswith(dev)) and sel in n]
+    if not ks:
+        raise SystemExit("%s: no %s dispatch" % (csv_path, dev))
+    avg = {c: sum(k.get(c, 0.0) for k in ks) / len(ks) for c in COUNTER_SET}
+    lines = ["# Counters of %s (%s) on %s, rocprofv3 --pmc, mean of %d dispatches" % (kernel, dev, workload, len(ks)),
+             "# mfma_busy = MfmaUtil / 100: SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs)",
+             "# valu_busy = VALUBusy / 100: SQ_ACTIVE_INST_VALU / (GRBM_GUI_ACTIVE x CUs)",
+             "# wait_frac = SQ_WAIT_ANY / SQ_WAVE_CYCLES: share of wave cycles spent waiting",
+             "kernel: %s" % kernel, "workload: %s" % workload,
+             "library_source_sha256_16: %s" % kernel_source_digest(),
+             "mfma_busy: %.4f" % (avg["MfmaUtil"] / 100.0),
+             "valu_busy: %.4f" % (avg["VALUBusy"] / 100.0),
+             "wait_frac: %.4f" % (avg["SQ_WAIT_ANY"] / max(avg["SQ_WAVE_CYCLES"], 1.0)),
+             "SQ_INSTS_VALU_per_dispatch: %.0f" % avg["SQ_INSTS_VALU"],
+             "SQ_INSTS_MFMA_per_dispatch: %.0f" % avg["SQ_INSTS_MFMA"],
+             "commands:"] + ["    " + c for c in commands]
+    path = counters_path(kernel, workload)
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(path)
+    print("\n".join(lines))
 
 
 def _pmc_rows(path):
@@ -290,46 +419,45 @@ def kernel_report(plan, kt, wl, transpose, algo, es, steps):
     shares the step's algorithmic work equally between its launches."""
     cin, cout = (1, 1) if wl.depthwise else (wl.c_in, wl.c_out)
     work = plan.kernel_work(transpose, algo, cin, cout, wl.dtype)
+    spec = spectral_spec(plan, transpose)
     missing = sorted(set(kt) - set(work))
     if missing:
         raise SystemExit("no work figures for kernels %s" % missing)
     per_kernel = {}
     def model(k):
-        b_, f_, bd = kernel_model(k, wl, work[k], es)
+        m = kernel_model(k, wl, work[k], es, spec)
         per_step = max(1, round(kt[k][0] / steps))
-        return b_ / per_step, f_ / per_step, bd
+        return {u: (v if u == "bound" else v / per_step) for u, v in m.items()}
 
     for k, (launches, tot_ms) in kt.items():
         avg_ms = tot_ms / launches
-        b_, f_, bd = model(k)
+        m = model(k)
+        r = model_roof(m, avg_ms / 1e3)
         per_kernel[k] = {"launches": launches, "avg_us": round(avg_ms * 1e3, 2),
-                         "alg_bytes": int(b_), "alg_flops": f_, "bound": bd,
-                         "alg_gbs": round(b_ / (avg_ms / 1e3) / 1e9, 1),
-                         "alg_tflops": round(f_ / (avg_ms / 1e3) / 1e12, 2)}
-        if bd == "hbm":
-            per_kernel[k]["hbm_frac"] = round(b_ / (avg_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)
+                         "alg_bytes": int(m["bytes"]), "alg_flops": m["flops"], "bound": m["bound"],
+                         "alg_gbs": round(m["bytes"] / (avg_ms / 1e3) / 1e9, 1),
+                         "alg_tflops": round(m["flops"] / (avg_ms / 1e3) / 1e12, 2),
+                         "frac": round(r["frac"], 4)}
+        if m["bound"] == "hbm":
+            per_kernel[k]["hbm_frac"] = round(r["frac"], 4)
     # The roofline names the direct kernel with the largest total time: the
-    # spectral kernels stand in for part of the direct product (their flops
-    # above are the direct method's they replace) and share the GPU with the
-    # sweep from the helper stream, which stretches their event-timed spans.
+    # spectral kernels share the GPU with the sweep from the helper stream,
+    # which stretches their event-timed spans over the sweep's.
     direct = [k for k in kt if not k.startswith("spectral_")] or list(kt)
     name = max(direct, key=lambda k: kt[k][1])
     launches, tot_ms = kt[name]
     avg_ms = tot_ms / launches
-    bytes_, flops, bound = model(name)
-    if bound == "hbm":
-        achieved = bytes_ / (avg_ms / 1e3) / 1e9
-        peak, unit = HBM_PEAK_GBS, "GB/s"
-    else:
-        achieved = flops / (avg_ms / 1e3) / 1e12
-        peak, unit = FP32_VALU_PEAK_TFLOPS, "TFLOP/s"
+    m = model(name)
+    r = model_roof(m, avg_ms / 1e3)
     traffic = load_traffic(name, wl.name)
-    roof = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-            "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": name,
-            "kernel_avg_us": round(avg_ms * 1e3, 2), "algorithmic_bytes": int(bytes_),
-            "algorithmic_flops": flops,
-            "algorithmic_gbs": round(bytes_ / (avg_ms / 1e3) / 1e9, 1),
+    roof = {"bound": r["bound"], "achieved": round(r["achieved"], 2), "peak": round(r["peak"], 2),
+            "unit": r["unit"], "frac": round(r["frac"], 4), "traffic": traffic, "kernel": name,
+            "kernel_avg_us": round(avg_ms * 1e3, 2), "algorithmic_bytes": int(m["bytes"]),
+            "algorithmic_flops": m["flops"],
+            "flops_by_unit": {u: m[u] for u in PEAK_TFLOPS if m[u] > 0},
+            "algorithmic_gbs": round(m["bytes"] / (avg_ms / 1e3) / 1e9, 1),
             "work_per_launch": dict(zip(("out_pixels", "in_pixels", "pairs"), work[name]))}
+    roof.update(load_counters(name, wl.name))
     return per_kernel, roof
 
 
@@ -375,7 +503,7 @@ def bench_backward(args, wl, plan, x, w, es, torch, disco):
     P = wl.y_shape[2] * wl.y_shape[3]
     kernels, cands = {}, []
 
-    def add(tag, kt, work, model_wl):
+    def add(tag, kt, work, model_wl, spec):
         for k, (launches, tot_ms) in kt.items():
             avg = tot_ms / launches
             if k == "weight_grad":
@@ -386,7 +514,8 @@ def bench_backward(args, wl, plan, x, w, es, torch, disco):
             else:
                 if k not in work:
                     raise SystemExit("no work figures for kernel %s" % k)
-                b_, f_, bd = kernel_model(k, model_wl, work[k], es)
+                mm = kernel_model(k, model_wl, work[k], es, spec)
+                b_, f_, bd = mm["bytes"], mm["flops"], mm["bound"]
             row = {"launches": launches, "avg_us": round(avg * 1e3, 2), "alg_bytes": int(b_), "alg_flops": f_,
                    "bound": bd, "alg_gbs": round(b_ / (avg / 1e3) / 1e9, 1),
                    "alg_tflops": round(f_ / (avg / 1e3) / 1e12, 2)}
@@ -398,15 +527,18 @@ def bench_backward(args, wl, plan, x, w, es, torch, disco):
 
     # dx: the adjoint op has the other op's filter pairs (its work figures).
     work_dx = plan.kernel_work(not transpose, "auto", Co, Ci, wl.dtype)
-    add("dx", kt_dx, work_dx, SimpleNamespace(batch=B, c_in=Co, c_out=Ci))
+    grids = dict(nlon_in=wl.nlon_in, nlon_out=wl.nlon_out)
+    # (the adjoint op's spectral rings are those of the other op's filter pairs)
+    add("dx", kt_dx, work_dx, SimpleNamespace(batch=B, c_in=Co, c_out=Ci, op="forward" if transpose else "transpose",
+                                              **grids), spectral_spec(plan, not transpose))
     # dW: one-pass gathered sums (fp32, 3x3 basis) or the op's kernels per channel.
     if wl.dtype == "fp32" and wl.basis == "bilinear3x3":
         work_dw = plan.kernel_work(transpose, "gather_then_contract", Ci, Ci * K, wl.dtype)
-        mwl = SimpleNamespace(batch=B, c_in=Ci, c_out=Ci * K)
+        mwl = SimpleNamespace(batch=B, c_in=Ci, c_out=Ci * K, op=wl.op, **grids)
     else:
         work_dw = plan.kernel_work(transpose, "auto", 1, K, wl.dtype)
-        mwl = SimpleNamespace(batch=B * Ci, c_in=1, c_out=K)
-    add("dw", kt_dw, work_dw, mwl)
+        mwl = SimpleNamespace(batch=B * Ci, c_in=1, c_out=K, op=wl.op, **grids)
+    add("dw", kt_dw, work_dw, mwl, spectral_spec(plan, transpose))
     name, tot, b_, f_, bd, avg = max(cands, key=lambda c: c[1])
     if bd == "hbm":
         achieved, peak, unit = b_ / (avg / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"
@@ -439,8 +571,11 @@ def main(argv=None):
                     help="write profiles/traffic_<kernel>_<workload>.txt from two rocprofv3 "
                          "counter runs (FETCH_SIZE, then WRITE_SIZE) of --copy-probe benches; "
                          "no GPU needed")
+    ap.add_argument("--counter-summary", metavar="CSV",
+                    help="write profiles/counters_<kernel>_<workload>.txt from a rocprofv3 --pmc run "
+                         "of %s; no GPU needed" % " ".join(COUNTER_SET))
     ap.add_argument("--kernel", default="sweep_gather_contract",
-                    help="library kernel name for --traffic-summary")
+                    help="library kernel name for --traffic-summary and --counter-summary")
     ap.add_argument("--command", action="append", default=[],
                     help="the command that produced each counter run (recorded verbatim)")
     ap.add_argument("--backward", action="store_true",
@@ -450,10 +585,13 @@ def main(argv=None):
                          "kernels are HBM-bound) that the JSON line reports as hbm_schedule")
     args = ap.parse_args(argv)
 
-    if args.traffic_summary:
+    if args.traffic_summary or args.counter_summary:
         from paper_2209_13603_amd import synth
         wl = synth.WORKLOADS[args.workload or synth.HEADLINE]
-        traffic_summary(*args.traffic_summary, args.kernel, wl.name, args.command)
+        if args.traffic_summary:
+            traffic_summary(*args.traffic_summary, args.kernel, wl.name, args.command)
+        else:
+            counter_summary(args.counter_summary, args.kernel, wl.name, args.command)
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:

@@ -143,6 +143,22 @@ typedef struct {
     int32_t sweep_patterns_forward;   /* (ring, phase) patterns of the forward op walked by the
                                          ring-sweep kernel (used when Cin <= 8) */
     int32_t sweep_patterns_transpose; /* ... of the transposed op */
+    int32_t spectral_pairs_forward;   /* (spectral output ring, input ring) pairs of the forward op:
+                                         one frequency-domain product per pair and frequency */
+    int32_t spectral_pairs_transpose; /* ... of the transposed op */
+    int32_t spectral_slots_forward;   /* input rings the forward op's spectral rings transform */
+    int32_t spectral_slots_transpose; /* ... of the transposed op */
+    /* Memory (App. B counts the non-zeros of Psi): the compressed psi of the
+     * forward op in its plain form (per stored entry an input ring, a
+     * longitude offset and K fp32 values, plus one pointer per pattern), and
+     * the device bytes of each kernel layout the plan holds, summed over its
+     * ops (psi_bytes is their total). */
+    int64_t psi_compressed_bytes;
+    int64_t bytes_entries;     /* the plain entry tables (two-kernel and contract-first schedules) */
+    int64_t bytes_general;     /* the general fused kernel's chunked layouts */
+    int64_t bytes_spectral;    /* the polar rings' frequency-domain psi rows and twiddles */
+    int64_t bytes_sweep;       /* the ring sweep's runs, spans and entries */
+    int64_t bytes_stencil;     /* the folded-weight stencil layouts */
 } disco_plan_info_t;
 
 /* Builds the sparse psi tensors of the forward and transposed ops on the host

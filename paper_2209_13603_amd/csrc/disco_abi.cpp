@@ -272,6 +272,7 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
         if (e != hipSuccess) return hip_fail(e, "hipMemcpy(psi entries)");
     }
     d->bytes = (int64_t)(pb + eb);
+    d->bytes_entries = d->bytes;
     d->work_all = pattern_work(h, {});
     d->basis = h.basis;
     const CellMap cm = cell_map(h.basis);
@@ -961,6 +962,19 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
     I.spectral_rings_transpose = plan->tr.spectral.n_rings;
     I.sweep_patterns_forward = plan->fwd.sweep.n_pats;
     I.sweep_patterns_transpose = plan->tr.sweep.n_pats;
+    I.spectral_pairs_forward = plan->fwd.spectral.n_pairs;
+    I.spectral_pairs_transpose = plan->tr.spectral.n_pairs;
+    I.spectral_slots_forward = plan->fwd.spectral.n_slots;
+    I.spectral_slots_transpose = plan->tr.spectral.n_slots;
+    I.psi_compressed_bytes = (int64_t)hf.t_in.size() * (8 + 4 * I.K) + 4 * (int64_t)hf.pat_ptr.size();
+    for (const DeviceOp* d : {&plan->fwd, &plan->tr, &plan->fwd_adj, &plan->tr_adj}) {
+        I.bytes_entries += d->bytes_entries;
+        I.bytes_general += d->packed.bytes + d->packed_light.bytes + d->packed_rest.bytes +
+                           (int64_t)sizeof(int32_t) * d->n_rest_pats;
+        I.bytes_spectral += d->spectral.bytes + (d->spectral.n_rings > 0 ? d->g.nlat_o : 0);
+        I.bytes_sweep += d->sweep.bytes;
+        I.bytes_stencil += d->stencil.bytes;
+    }
     *plan_out = plan;
     return ok();
 }
@@ -1002,6 +1016,12 @@ disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t a
     const Dispatch dp = dispatch(op, algo, c_in, c_out, dtype);
     struct Row { const char* name; Work w; };
     std::vector<Row> rows;
+    auto spectral_rows = [&op](const SpectralDev&, std::vector<Row>* r) {
+        const Work& sw = op.work_spectral;
+        r->push_back({"spectral_rfft", Work{0, sw.in_pixels, 0}});
+        r->push_back({"spectral_mac", Work{0, 0, sw.pairs}});
+        r->push_back({"spectral_irfft", Work{sw.out_pixels, 0, 0}});
+    };
     const Work& all = op.work_all;
     ExecArgs ea{};
     ea.op = &op;
@@ -1022,12 +1042,7 @@ disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t a
         rows.push_back({"sweep_gather_z", op.work_sweep});
         if (op.n_rest_pats > 0) rows.push_back({"gather_z", op.work_rest});
         rows.push_back({"contract_z", Work{all.out_pixels - op.work_spectral.out_pixels, 0, 0}});
-        if (op.spectral.n_rings > 0) {
-            const Work& sw = op.work_spectral;
-            rows.push_back({"spectral_rfft", Work{0, sw.in_pixels, 0}});
-            rows.push_back({"spectral_mac", Work{0, 0, sw.pairs}});
-            rows.push_back({"spectral_irfft", Work{sw.out_pixels, 0, 0}});
-        }
+        if (op.spectral.n_rings > 0) spectral_rows(op.spectral, &rows);
     } else if (dp.algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
         rows.push_back({"gather_z", all});
         rows.push_back({"contract_z", Work{all.out_pixels, 0, 0}});
@@ -1035,12 +1050,7 @@ disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t a
         rows.push_back({"contract_x", Work{0, all.in_pixels, 0}});
         rows.push_back({"gather_y", all});
     } else {
-        if (dp.spectral) {
-            const Work& sw = op.work_spectral;
-            rows.push_back({"spectral_rfft", Work{0, sw.in_pixels, 0}});
-            rows.push_back({"spectral_mac", Work{0, 0, sw.pairs}});
-            rows.push_back({"spectral_irfft", Work{sw.out_pixels, 0, 0}});
-        }
+        if (dp.spectral) spectral_rows(op.spectral, &rows);
         if (dp.sweep) rows.push_back({"sweep_gather_contract", op.work_sweep});
         if (dp.sweep && workspace_bytes_sweep(ea) > 0)
             rows.push_back({"convert_y", Work{op.work_sweep.out_pixels, 0, 0}});

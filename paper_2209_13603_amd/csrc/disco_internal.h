@@ -321,6 +321,7 @@ struct DeviceOp {
     int64_t n_entries = 0;
     int64_t nnz_pairs = 0;
     int64_t bytes = 0;
+    int64_t bytes_entries = 0;  // pat_ptr + entries (+ the cell map)
     // Work of the pattern sets above: all, spectral rings, the rest of them,
     // sweep-walked, and what the general kernel keeps beside the sweep.
     Work work_all, work_spectral, work_light, work_sweep, work_rest;

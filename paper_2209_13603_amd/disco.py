@@ -86,7 +86,12 @@ class PlanInfo(ctypes.Structure):
                 ("h", ctypes.c_double), ("spectral_rings_forward", ctypes.c_int32),
                 ("spectral_rings_transpose", ctypes.c_int32),
                 ("sweep_patterns_forward", ctypes.c_int32),
-                ("sweep_patterns_transpose", ctypes.c_int32)]
+                ("sweep_patterns_transpose", ctypes.c_int32),
+                ("spectral_pairs_forward", ctypes.c_int32), ("spectral_pairs_transpose", ctypes.c_int32),
+                ("spectral_slots_forward", ctypes.c_int32), ("spectral_slots_transpose", ctypes.c_int32),
+                ("psi_compressed_bytes", ctypes.c_int64), ("bytes_entries", ctypes.c_int64),
+                ("bytes_general", ctypes.c_int64), ("bytes_spectral", ctypes.c_int64),
+                ("bytes_sweep", ctypes.c_int64), ("bytes_stencil", ctypes.c_int64)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -17,26 +17,63 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def test_fused_model_counts_gather_and_contraction():
     wl = synth.WORKLOADS["sphere2048x4096"]
     outp, inp, pairs = 1000, 900, 50000
-    b, f, bound = bench.kernel_model("sweep_gather_contract", wl, (outp, inp, pairs), 4)
-    assert bound == "alu"
-    assert b == wl.batch * (wl.c_in * inp + wl.c_out * outp) * 4
-    assert f == 2.0 * pairs * wl.batch * wl.c_in + 2.0 * wl.batch * wl.c_in * 9 * wl.c_out * outp
+    m = bench.kernel_model("sweep_gather_contract", wl, (outp, inp, pairs), 4)
+    assert m["bound"] == "alu"
+    assert m["bytes"] == wl.batch * (wl.c_in * inp + wl.c_out * outp) * 4
+    assert m["valu"] == 2.0 * pairs * wl.batch * wl.c_in
+    assert m["mfma_f32"] == 2.0 * wl.batch * wl.c_in * 9 * wl.c_out * outp and m["mfma_bf16"] == 0.0
+    assert m["flops"] == m["valu"] + m["mfma_f32"]
+
+
+def test_bf16_general_kernel_contracts_on_bf16_matrix_cores():
+    """The general kernel with bf16 storage contracts on bf16 matrix cores:
+    those flops count against 2.5 PFLOP/s, the gather against the fp32 VALU
+    peak, and the bound is the sum of the two times."""
+    wl = synth.WORKLOADS["up256x512_to_512x1024_bf16"]
+    m = bench.kernel_model("fused_gather_contract", wl, (1000, 900, 50000), 2)
+    assert m["mfma_f32"] == 0.0 and m["mfma_bf16"] == 2.0 * wl.batch * wl.c_in * 9 * wl.c_out * 1000
+    t = m["valu"] / 157.3e12 + m["mfma_bf16"] / 2500e12
+    r = bench.model_roof(m, 2 * t)
+    assert r["frac"] == pytest.approx(0.5)
+    assert r["peak"] == pytest.approx(m["flops"] / t / 1e12)
+    assert r["achieved"] == pytest.approx(r["frac"] * r["peak"])
+
+
+def test_spectral_models_count_their_own_work():
+    """rfft / irfft: 2.5 N log2 N flop per ring transform; the products: 36
+    flop per (ring pair, frequency, input channel) and 36 per (output
+    frequency, input channel, output channel).  No spectral row claims the
+    direct sum it replaces, so none exceeds its unit's peak by construction."""
+    wl = synth.WORKLOADS["sphere2048x4096"]
+    N = wl.nlon_in
+    spec = {"rings": 162, "pairs": 1000, "slots": 170}
+    B, Ci, Co = wl.batch, wl.c_in, wl.c_out
+    m = bench.kernel_model("spectral_rfft", wl, (0, 170 * N, 0), 4, spec)
+    assert m["valu"] == pytest.approx(B * Ci * 170 * 2.5 * N * 12)
+    m = bench.kernel_model("spectral_irfft", wl, (162 * N, 0, 0), 4, spec)
+    assert m["valu"] == pytest.approx(B * Co * 162 * 2.5 * N * 12)
+    m = bench.kernel_model("spectral_mac", wl, (0, 0, 10 ** 9), 4, spec)
+    bins = N // 2 + 1
+    assert m["valu"] == 36.0 * B * Ci * 1000 * bins + 36.0 * B * Ci * Co * 162 * bins
+    assert m["mfma_f32"] == 0.0
+    with pytest.raises(SystemExit):
+        bench.kernel_model("spectral_mac", wl, (0, 0, 10 ** 9), 4)
 
 
 def test_depthwise_stencil_model_is_one_channel_per_item():
     wl = synth.WORKLOADS["sphere2048x4096_separable_dw"]
     outp, inp, pairs = 4096, 4096, 100000
-    b, f, _ = bench.kernel_model("stencil_blocked", wl, (outp, inp, pairs), 4)
+    m = bench.kernel_model("stencil_blocked", wl, (outp, inp, pairs), 4)
     items = wl.batch * wl.c_in
-    assert b == items * (inp + outp) * 4
-    assert f == 2.0 * pairs * items
+    assert m["bytes"] == items * (inp + outp) * 4
+    assert m["flops"] == 2.0 * pairs * items
 
 
 def test_convert_model_is_hbm():
     wl = synth.WORKLOADS["up256x512_to_512x1024_bf16"]
-    b, f, bound = bench.kernel_model("convert_y", wl, (777, 0, 0), 2)
-    assert bound == "hbm" and f == 0.0
-    assert b == wl.batch * wl.c_out * 777 * (4 + 2)
+    m = bench.kernel_model("convert_y", wl, (777, 0, 0), 2)
+    assert m["bound"] == "hbm" and m["flops"] == 0.0
+    assert m["bytes"] == wl.batch * wl.c_out * 777 * (4 + 2)
 
 
 class _FakePlan:
@@ -45,6 +82,10 @@ class _FakePlan:
 
     def kernel_work(self, transpose, algo, cin, cout, dtype):
         return self.work
+
+    def info(self):
+        return {"spectral_%s_%s" % (k, op): n for k, n in (("rings", 40), ("pairs", 300), ("slots", 44))
+                for op in ("forward", "transpose")}
 
 
 def test_multi_launch_kernel_shares_the_step():
@@ -55,7 +96,8 @@ def test_multi_launch_kernel_shares_the_step():
     steps = 10
     kt = {"sweep_gather_contract": (4 * steps, 40.0), "spectral_mac": (steps, 5.0)}
     per, roof = bench.kernel_report(_FakePlan(work), kt, wl, False, "auto", 4, steps)
-    b_full, f_full, _ = bench.kernel_model("sweep_gather_contract", wl, work["sweep_gather_contract"], 4)
+    m_full = bench.kernel_model("sweep_gather_contract", wl, work["sweep_gather_contract"], 4)
+    b_full, f_full = m_full["bytes"], m_full["flops"]
     assert per["sweep_gather_contract"]["alg_bytes"] == int(b_full / 4)
     assert per["sweep_gather_contract"]["alg_flops"] == pytest.approx(f_full / 4)
     assert per["sweep_gather_contract"]["avg_us"] == pytest.approx(1000.0)
@@ -87,6 +129,23 @@ def test_traffic_summary_round_trip(tmp_path, monkeypatch):
     bench.traffic_summary(str(fc), str(wc), "sweep_gather_contract", "sphere2048x4096", ["cmd"])
     got = bench.load_traffic("sweep_gather_contract", "sphere2048x4096")
     assert got == pytest.approx((1100.0 * 2 + 3000.0) * 1024.0)
+
+
+def test_counter_summary_round_trip(tmp_path, monkeypatch):
+    """Derived metrics averaged over the kernel's dispatches (other kernels
+    ignored), written with the source digest and read back as fractions."""
+    monkeypatch.setattr(bench, "counters_path", lambda k, w: str(tmp_path / ("c_%s_%s.txt" % (k, w))))
+    sweep = "void disco::k_sweep<float, 8, false, 0>(int)"
+    rows = []
+    for d, (mf, vb) in enumerate([(30.0, 40.0), (34.0, 44.0)]):
+        rows += [(d, sweep, "MfmaUtil", mf), (d, sweep, "VALUBusy", vb), (d, sweep, "SQ_INSTS_VALU", 1e6),
+                 (d, sweep, "SQ_INSTS_MFMA", 2e5), (d, sweep, "SQ_WAIT_ANY", 25.0), (d, sweep, "SQ_WAVE_CYCLES", 100.0)]
+    rows += [(9, "void disco::k_spectral<float, 8>(int)", "MfmaUtil", 99.0)]
+    c = tmp_path / "c.csv"
+    _write_csv(c, rows)
+    bench.counter_summary(str(c), "sweep_gather_contract", "sphere2048x4096", ["cmd"])
+    got = bench.load_counters("sweep_gather_contract", "sphere2048x4096")
+    assert got == {"mfma_busy": pytest.approx(0.32), "valu_busy": pytest.approx(0.42), "wait_frac": pytest.approx(0.25)}
 
 
 def test_bench_refuses_more_than_one_gpu():
