@@ -114,8 +114,21 @@ disco_status_t upload_vec(const std::vector<V>& v, V** dst, int64_t* bytes, cons
     return DISCO_OK;
 }
 
-// Entries per work item of the fused kernel (balances workgroups).
+// Entries per work item of the fused kernel (balances workgroups): 512,
+// and fewer on small ops, where the launch is a handful of workgroups and
+// the longest one's serial chain of staging and gathering is the time
+// (measured: 32 x 64, 4 -> 4 channels: 41.5 us at 512, 17.6 us at 64 with the
+// 64-lane tile; 128 x 256 -> 64 x 128, 16 -> 16 channels: 112 us at 512, 71 us
+// at 128).  Environment DISCO_FUSED_TARGET_ENTRIES overrides, for tuning.
 constexpr int kTargetEntries = 512;
+int fused_target_entries(const HostOp& h, int tile) {
+    const char* v = std::getenv("DISCO_FUSED_TARGET_ENTRIES");
+    if (v && *v) return std::max(16, std::atoi(v));
+    if (tile == 64) return 64;
+    const int64_t tiles = (h.g.nq + tile - 1) / tile;
+    if ((int64_t)h.t_in.size() * tiles < 65536) return 128;
+    return kTargetEntries;
+}
 
 // Output rings with at least this many entries take the spectral path
 // (environment DISCO_SPECTRAL_MIN_ENTRIES overrides, for tuning).
@@ -151,7 +164,12 @@ void free_spectral(SpectralDev* d) {
 disco_status_t upload_packed(const HostOp& h, const std::vector<uint8_t>& skip, PackedDev* d) {
     PackedHost P;
     std::string err;
-    int rc = pack_op(h, kTargetEntries, skip, &P, &err);
+    // A 64-lane tile when a pattern has at most 64 output longitudes, so
+    // that the lanes of a 256-lane tile do not idle (measured on 32 x 64);
+    // 256 otherwise (on 128 x 256 -> 64 x 128, whose patterns have 128, the
+    // 128-lane tile was slower: 104 against 71 us, fewer waves in flight).
+    const int tile = h.g.nq <= 64 ? 64 : kTileQ;
+    int rc = pack_op(h, fused_target_entries(h, tile), skip, &P, &err, tile);
     if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
     disco_status_t s;
     if ((s = upload_vec(P.spans, &d->spans, &d->bytes, "hipMalloc(spans)")) != DISCO_OK) return s;
@@ -172,6 +190,7 @@ disco_status_t upload_packed(const HostOp& h, const std::vector<uint8_t>& skip, 
     d->n_items = (int32_t)P.items.size();
     d->n_split = (int32_t)P.red_pattern.size();
     d->n_slots = P.n_slots;
+    d->tile = P.tile;
     return DISCO_OK;
 }
 
@@ -431,8 +450,9 @@ Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co, int32_t dtyp
                                    (int64_t)g.nlat_o * g.nlon_o * 4 < ((int64_t)1 << 31);
     // Several channel groups pay off on single-phase ops (measured: 512 x
     // 1024, 32 -> 32 channels, 0.76 -> 0.65 ms); on ops with longitude
-    // phases (the transposed upsampling op) one sweep launch costs about
-    // what the general kernel's whole channel pass does, so groups lose.
+    // phases (the transposed upsampling op, 64 -> 32 channels in bf16) the
+    // groups' fp32 atomic merges dominate (eight launches of 0.5 ms against
+    // the general kernel's 3.2 ms for the whole op), so groups lose.
     d.sweep = algo == DISCO_ALGO_FUSED && op.sweep.n_runs > 0 && sweep_offsets_fit && (Ci <= kCIC || g.P == 1);
     if (d.sweep) {
         d.packed = &op.packed_rest;

@@ -120,8 +120,10 @@ __device__ __forceinline__ void run_cell(int eb, int ee, const int* __restrict__
     }
 }
 
-template <typename T, int COT>
-__global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ items,
+// TQ: output longitudes (lanes) per workgroup, the width the op's spans were
+// packed for (PackedDev::tile).
+template <typename T, int COT, int TQ>
+__global__ __launch_bounds__(TQ) void k_fused(const PItem* __restrict__ items,
                                                   const PSeg* __restrict__ segs,
                                                   const PChunk* __restrict__ chunks,
                                                   const PSpan* __restrict__ spans,
@@ -143,7 +145,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
     const int qt = bid - item * n_qtiles;
     const int b = blockIdx.y / n_cotiles;
     const int co0 = (blockIdx.y - b * n_cotiles) * COT;
-    const int q0 = qt * kBlock;
+    const int q0 = qt * TQ;
     const int q = q0 + tid;
     const int lane_col = g.stride * tid;
     const int64_t n_in = (int64_t)g.nlat_i * g.nlon_i;
@@ -162,7 +164,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
 #pragma unroll
                 for (int k = 0; k < kBasis; ++k) z[c][k] = 0.0f;
             __syncthreads();  // previous users of ws / xs are done
-            for (int i = tid; i < kCIC * kBasis * COT; i += kBlock) {
+            for (int i = tid; i < kCIC * kBasis * COT; i += TQ) {
                 // ws[j][c][k]: output channel j of the tile, pass channel c, basis k
                 // (bf16 storage: the raw bf16 values, packed two per word).
                 const int j = i / (kCIC * kBasis), ck = i % (kCIC * kBasis), c = ck / kBasis, k = ck % kBasis;
@@ -182,7 +184,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
                     const PSpan S = spans[sp];
                     int start = (g.stride * q0 + S.dstart) % g.nlon_i;
                     if (start < 0) start += g.nlon_i;
-                    for (int j = tid; j < S.len; j += kBlock) {
+                    for (int j = tid; j < S.len; j += TQ) {
                         int idx = start + j;
                         if (idx >= g.nlon_i) idx = idx % g.nlon_i;
 #pragma unroll
@@ -200,7 +202,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
                 }
                 {
                     const int ebase = C.cls[0], ne = C.cls[kCells] - C.cls[0];
-                    for (int i = tid; i < ne; i += kBlock) {
+                    for (int i = tid; i < ne; i += TQ) {
                         eoffs[i] = offs[ebase + i];
                         const PVal pv = vals[ebase + i];
                         evs[i] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
@@ -308,19 +310,26 @@ __global__ __launch_bounds__(kBlock) void k_reduce_partials(const int32_t* __res
     store_val(y, ((int64_t)b * Co + co) * n_out + pix, acc);
 }
 
-template <typename T, int COT>
-hipError_t fused_launch(const ExecArgs& a, const PackedDev& P, float* partial) {
+template <typename T, int COT, int TQ>
+hipError_t fused_launch_tq(const ExecArgs& a, const PackedDev& P, float* partial) {
     const OpGeom& g = a.op->g;
-    if (P.n_items == 0) return hipSuccess;
-    const int n_qtiles = (g.nq + kBlock - 1) / kBlock;
+    const int n_qtiles = (g.nq + TQ - 1) / TQ;
     const int n_cot = (a.Co + COT - 1) / COT;
     dim3 grid((unsigned)(P.n_items * n_qtiles), (unsigned)(a.B * n_cot));
     int tk = timing_begin("fused_gather_contract", a.stream);
-    hipLaunchKernelGGL((k_fused<T, COT>), grid, dim3(kBlock), 0, a.stream, P.items, P.segs, P.chunks,
+    hipLaunchKernelGGL((k_fused<T, COT, TQ>), grid, dim3(TQ), 0, a.stream, P.items, P.segs, P.chunks,
                        P.spans, P.offs, P.vals, g, (const T*)a.x, (const T*)a.w, (T*)a.y, partial, a.Ci,
                        a.Co, n_qtiles, n_cot, a.w_trans);
     timing_end(tk, a.stream);
-    hipError_t e = hipGetLastError();
+    return hipGetLastError();
+}
+
+template <typename T, int COT>
+hipError_t fused_launch(const ExecArgs& a, const PackedDev& P, float* partial) {
+    if (P.n_items == 0) return hipSuccess;
+    hipError_t e = P.tile == 64    ? fused_launch_tq<T, COT, 64>(a, P, partial)
+                   : P.tile == 128 ? fused_launch_tq<T, COT, 128>(a, P, partial)
+                                   : fused_launch_tq<T, COT, kTileQ>(a, P, partial);
     if (e != hipSuccess) return e;
     return launch_reduce_partials(a, P, partial);
 }

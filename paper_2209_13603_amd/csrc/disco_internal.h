@@ -124,6 +124,7 @@ static_assert(sizeof(PChunk) == 80, "PChunk layout");
 static_assert(sizeof(PEntry) == 20, "PEntry layout");
 
 struct PackedHost {
+    int32_t tile = kTileQ;              // output longitudes (lanes) per workgroup: 64, 128 or 256
     std::vector<PSpan> spans;
     std::vector<PChunk> chunks;
     std::vector<PEntry> entries;
@@ -136,8 +137,10 @@ struct PackedHost {
 };
 // skip[pattern] != 0 leaves the pattern out of the segments and work items
 // (its output is produced elsewhere); skip may be empty.
+// tile: output longitudes (lanes) per workgroup, 64, 128 or kTileQ; the
+// spans carry the halo of that width.
 int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& skip, PackedHost* out,
-            std::string* err);
+            std::string* err, int tile = kTileQ);
 
 // ---------------------------------------------------------------------------
 // Blocked layout of the folded-weight stencil kernel for ops with longitude
@@ -270,6 +273,7 @@ struct SpectralDev {
 };
 
 struct PackedDev {
+    int32_t tile = kTileQ;       // lanes per workgroup the spans were cut for
     PSpan* spans = nullptr;
     PChunk* chunks = nullptr;
     int32_t* offs = nullptr;     // per entry: LDS column at lane 0

@@ -78,16 +78,21 @@ bool entry_cell_values(const HostOp& op, int64_t e, int* cell, float v[4]) {
 }
 
 int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& skip, PackedHost* out,
-            std::string* err) {
+            std::string* err, int tile) {
     const OpGeom& g = op.g;
     const int s = g.stride;
-    const int halo = s * (kTileQ - 1);  // extra columns a tile reads beyond one entry
+    if (tile != 64 && tile != 128 && tile != kTileQ) {
+        if (err) *err = "internal: unknown tile width";
+        return DISCO_ERR_DEVICE;
+    }
+    const int halo = s * (tile - 1);  // extra columns a tile reads beyond one entry
     if (halo + 1 > kLdsCols) {
         if (err) *err = "longitude stride too large for the staged kernel";
         return DISCO_ERR_UNSUPPORTED;
     }
     const int max_extent = kLdsCols - halo;  // max (d_last - d_first + 1) of one piece
     PackedHost P;
+    P.tile = tile;
     std::vector<int32_t> pattern_seg_count(g.n_patterns(), 0);
 
     for (int pat = 0; pat < g.n_patterns(); ++pat) {

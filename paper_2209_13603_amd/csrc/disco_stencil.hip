@@ -85,8 +85,10 @@ __device__ __forceinline__ void fill_fold_table(float* wt, const int8_t* __restr
     }
 }
 
-template <typename T, int COT>
-__global__ __launch_bounds__(kBlock) void k_stencil(const PItem* __restrict__ items,
+// TQ: output longitudes (lanes) per workgroup, the width the op's spans were
+// packed for (PackedDev::tile).
+template <typename T, int COT, int TQ>
+__global__ __launch_bounds__(TQ) void k_stencil(const PItem* __restrict__ items,
                                                     const PSeg* __restrict__ segs,
                                                     const PChunk* __restrict__ chunks,
                                                     const PSpan* __restrict__ spans,
@@ -108,7 +110,7 @@ __global__ __launch_bounds__(kBlock) void k_stencil(const PItem* __restrict__ it
     const int qt = bid - item * n_qtiles;
     const int b = blockIdx.y / n_cotiles;
     const int co0 = (blockIdx.y - b * n_cotiles) * COT;
-    const int q0 = qt * kBlock;
+    const int q0 = qt * TQ;
     const int q = q0 + tid;
     const int lane_col = g.stride * tid;
     const int64_t n_in = (int64_t)g.nlat_i * g.nlon_i;
@@ -125,7 +127,7 @@ __global__ __launch_bounds__(kBlock) void k_stencil(const PItem* __restrict__ it
             // through the cell map.  The previous readers of the table (the
             // last chunk's staging) are behind that chunk's second barrier;
             // the next chunk's first barrier orders these writes before use.
-            fill_fold_table<T, COT, kBlock>(wt, cmap, w, K, b, ci, co0, Ci, Co, w_trans, dw_c);
+            fill_fold_table<T, COT, TQ>(wt, cmap, w, K, b, ci, co0, Ci, Co, w_trans, dw_c);
             const T* xc = x + ((int64_t)b * Ci + ci) * n_in;
             for (int ch = sg.chunk_begin; ch < sg.chunk_end; ++ch) {
                 const PChunk C = chunks[ch];
@@ -134,14 +136,14 @@ __global__ __launch_bounds__(kBlock) void k_stencil(const PItem* __restrict__ it
                     const PSpan S = spans[sp];
                     int start = (g.stride * q0 + S.dstart) % g.nlon_i;
                     if (start < 0) start += g.nlon_i;
-                    for (int j = tid; j < S.len; j += kBlock) {
+                    for (int j = tid; j < S.len; j += TQ) {
                         int idx = start + j;
                         if (idx >= g.nlon_i) idx = idx % g.nlon_i;
                         xs[S.lds_base + j] = load_val(xc, (int64_t)S.row + idx);
                     }
                 }
                 const int ebase = C.cls[0], ne = C.cls[kCells] - C.cls[0];
-                for (int i = tid; i < ne; i += kBlock) {
+                for (int i = tid; i < ne; i += TQ) {
                     eoffs[i] = offs[ebase + i];
                     const PVal pv = vals[ebase + i];
                     // Entries are sorted by cell: cls[c] is the first of cell c.
@@ -193,19 +195,26 @@ __global__ __launch_bounds__(kBlock) void k_stencil(const PItem* __restrict__ it
     }
 }
 
-template <typename T, int COT>
-hipError_t stencil_launch(const ExecArgs& a, const PackedDev& P, float* partial) {
+template <typename T, int COT, int TQ>
+hipError_t stencil_launch_tq(const ExecArgs& a, const PackedDev& P, float* partial) {
     const OpGeom& g = a.op->g;
-    if (P.n_items == 0) return hipSuccess;
-    const int n_qtiles = (g.nq + kBlock - 1) / kBlock;
+    const int n_qtiles = (g.nq + TQ - 1) / TQ;
     const int n_cot = (a.Co + COT - 1) / COT;
     dim3 grid((unsigned)(P.n_items * n_qtiles), (unsigned)(a.B * n_cot));
     const int tk = timing_begin("stencil", a.stream);
-    hipLaunchKernelGGL((k_stencil<T, COT>), grid, dim3(kBlock), 0, a.stream, P.items, P.segs, P.chunks,
+    hipLaunchKernelGGL((k_stencil<T, COT, TQ>), grid, dim3(TQ), 0, a.stream, P.items, P.segs, P.chunks,
                        P.spans, P.offs, P.vals, a.op->cmap_dev, g, (const T*)a.x, (const T*)a.w, (T*)a.y,
                        partial, a.Ci, a.Co, basis_size(a.op->basis), n_qtiles, n_cot, a.w_trans, a.dw_c);
     timing_end(tk, a.stream);
-    hipError_t e = hipGetLastError();
+    return hipGetLastError();
+}
+
+template <typename T, int COT>
+hipError_t stencil_launch(const ExecArgs& a, const PackedDev& P, float* partial) {
+    if (P.n_items == 0) return hipSuccess;
+    hipError_t e = P.tile == 64    ? stencil_launch_tq<T, COT, 64>(a, P, partial)
+                   : P.tile == 128 ? stencil_launch_tq<T, COT, 128>(a, P, partial)
+                                   : stencil_launch_tq<T, COT, kTileQ>(a, P, partial);
     if (e != hipSuccess) return e;
     return launch_reduce_partials(a, P, partial);
 }

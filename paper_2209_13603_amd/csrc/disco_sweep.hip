@@ -186,6 +186,34 @@ __device__ __forceinline__ void mfma_contract_k(v4f (&yacc)[NQ], const float (&w
     }
 }
 
+// bf16 storage: the same contraction on the bf16 matrix cores
+// (v_mfma_f32_4x4x4_16b_bf16, four products per instruction, fp32
+// accumulation), with the gathered sums rounded to bf16 (round to nearest
+// even, v_cvt_pk_bf16_f32) like the general kernel does for bf16 storage.
+// The contraction index is kk' = 8 K + ci here, so that one basis function's
+// eight channels are two groups of four: group G = 2 K + (ci / 4) takes A
+// from block G % 16 (CBSZ = 4) of wb[qd][G / 16], where lane 4 b + i holds
+// W(co0 + 4 qd + i, kk' = 4 (16 h + b) + u) for u = 0..3 in register h.
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __bf16 bf4 __attribute__((ext_vector_type(4)));
+
+template <int G, int NQ>
+__device__ __forceinline__ void mfma_bf16_group(v4f (&yacc)[NQ], const v4s (&wb)[NQ][2], v4s zb) {
+#pragma unroll
+    for (int qd = 0; qd < NQ; ++qd)
+        yacc[qd] = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(wb[qd][G / 16], zb, yacc[qd], 4, G % 16, 0);
+}
+
+template <int K, int NQ>
+__device__ __forceinline__ void mfma_contract_k_bf16(v4f (&yacc)[NQ], const v4s (&wb)[NQ][2],
+                                                     const float (&z)[kCIC][kBasis]) {
+    static_assert(kCIC == 8, "two groups of four channels per basis function");
+    const v4f lo = {z[0][K], z[1][K], z[2][K], z[3][K]};
+    const v4f hi = {z[4][K], z[5][K], z[6][K], z[7][K]};
+    mfma_bf16_group<2 * K, NQ>(yacc, wb, __builtin_bit_cast(v4s, __builtin_convertvector(lo, bf4)));
+    mfma_bf16_group<2 * K + 1, NQ>(yacc, wb, __builtin_bit_cast(v4s, __builtin_convertvector(hi, bf4)));
+}
+
 // grid: (n_runs * n_qtiles, B * n_cotiles); the launch reads input channels
 // cg0 .. cg0 + kCIC - 1 (those below Ci; cg0 is 0 with YMODE kStoreY) and
 // writes y by YMODE (y32: the fp32 [B][Co][pixels] partial sums of kStoreF32
@@ -243,8 +271,30 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
     // v_mfma_f32_4x4x1_16b_f32 is taken from block ABID and broadcast to all
     // 16 blocks, so wv[qd][g] at lane 4b + i holds W(co0 + 4 qd + i, kk =
     // 16 g + b) and one register serves 16 values of kk.
-    float wv[COT / 4][kWG];
-    if constexpr (!ZOUT) {
+    constexpr bool kMM16 = sizeof(T) == 2 && !ZOUT;  // bf16 matrix-core contraction
+    float wv[kMM16 ? 1 : COT / 4][kMM16 ? 1 : kWG];
+    v4s wb[kMM16 ? COT / 4 : 1][2];
+    if constexpr (kMM16) {
+        const int li = tid & 3, blk = (tid & 63) >> 2;
+#pragma unroll
+        for (int qd = 0; qd < COT / 4; ++qd)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                v4s r;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int kk = 4 * (16 * h + blk) + u, co = co0 + 4 * qd + li;
+                    const int c = c0 + kk % kCIC, k = kk / kCIC;
+                    short v = 0;
+                    if (kk < kKK && co < Co && c < Ci) {
+                        const int64_t idx = w_trans ? ((int64_t)c * Co + co) * kBasis + k : ((int64_t)co * Ci + c) * kBasis + k;
+                        v = (short)((const uint16_t*)w)[idx];
+                    }
+                    r[u] = v;
+                }
+                wb[qd][h] = r;
+            }
+    } else if constexpr (!ZOUT) {
         const int li = tid & 3, blk = (tid & 63) >> 2;
 #pragma unroll
         for (int qd = 0; qd < COT / 4; ++qd)
@@ -419,38 +469,38 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
         run_cell<4>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         ce += (int)((SP.ncell[1] >> 8) & 255u);
         run_cell<5>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<0>(zr, zoff, zplane, z); else mfma_contract_k<0, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<0>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<0, COT / 4>(yacc, wb, z); else mfma_contract_k<0, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[1] >> 16) & 255u);
         run_cell<6>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<1>(zr, zoff, zplane, z); else mfma_contract_k<1, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<1>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<1, COT / 4>(yacc, wb, z); else mfma_contract_k<1, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[1] >> 24) & 255u);
         run_cell<7>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<2>(zr, zoff, zplane, z); else mfma_contract_k<2, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<2>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<2, COT / 4>(yacc, wb, z); else mfma_contract_k<2, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[2] >> 0) & 255u);
         run_cell<8>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         ce += (int)((SP.ncell[2] >> 8) & 255u);
         run_cell<9>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<3>(zr, zoff, zplane, z); else mfma_contract_k<3, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<3>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<3, COT / 4>(yacc, wb, z); else mfma_contract_k<3, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[2] >> 16) & 255u);
         run_cell<10>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<4>(zr, zoff, zplane, z); else mfma_contract_k<4, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<4>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<4, COT / 4>(yacc, wb, z); else mfma_contract_k<4, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[2] >> 24) & 255u);
         run_cell<11>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<5>(zr, zoff, zplane, z); else mfma_contract_k<5, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<5>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<5, COT / 4>(yacc, wb, z); else mfma_contract_k<5, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[3] >> 0) & 255u);
         run_cell<12>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         ce += (int)((SP.ncell[3] >> 8) & 255u);
         run_cell<13>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<6>(zr, zoff, zplane, z); else mfma_contract_k<6, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<6>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<6, COT / 4>(yacc, wb, z); else mfma_contract_k<6, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[3] >> 16) & 255u);
         run_cell<14>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<7>(zr, zoff, zplane, z); else mfma_contract_k<7, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<7>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<7, COT / 4>(yacc, wb, z); else mfma_contract_k<7, 0, COT / 4>(yacc, wv, z);
         ce += (int)((SP.ncell[3] >> 24) & 255u);
         run_cell<15>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         const int pattern = SP.pattern;
         SP = SPn;
         SPn = pats[pi + 2 < R.pat_end ? pi + 2 : pi];
-        if constexpr (ZOUT) store_z_k<8>(zr, zoff, zplane, z); else mfma_contract_k<8, 0, COT / 4>(yacc, wv, z);
+        if constexpr (ZOUT) store_z_k<8>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<8, COT / 4>(yacc, wb, z); else mfma_contract_k<8, 0, COT / 4>(yacc, wv, z);
         // Every lane issues the same COT stores (outputs that do not exist are
         // dropped by the buffer range check: an out-of-range offset for
         // longitudes past the ring, an empty buffer for channels past Cout),
