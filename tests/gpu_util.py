@@ -31,11 +31,13 @@ def rel_l2(got: np.ndarray, ref: np.ndarray) -> float:
     return float(np.linalg.norm((got - ref).ravel())) / (den if den > 0 else 1.0)
 
 
-def sample_pixels(nlat: int, nlon: int, per_ring: int = 6, seed: int = 0) -> np.ndarray:
+def sample_pixels(nlat: int, nlon: int, per_ring: int = 6, seed: int = 0, extra_rings=()) -> np.ndarray:
     """Flat pixel indices: the 6 rings next to each pole, every (nlat/12)-th ring,
-    and on each a few longitudes including the seam (0, nlon - 1)."""
+    the extra rings asked for, and on each a few longitudes including the
+    seam (0, nlon - 1)."""
     rings = set(range(min(6, nlat))) | set(range(max(0, nlat - 6), nlat))
     rings |= set(range(0, nlat, max(1, nlat // 12)))
+    rings |= set(int(t) for t in extra_rings if 0 <= t < nlat)
     r = np.random.default_rng(seed)
     pix = []
     for t in sorted(rings):
@@ -61,3 +63,37 @@ def run_oracle(args, x, w, op, pix=None, **kw):
     o = oracle.default()
     fn = o.forward if op == "forward" else o.transpose
     return fn(*args, x.astype(np.float64), w.astype(np.float64), pix=pix, **kw)
+
+
+def kernel_boundary_rings(plan_args, transpose: bool, plan_kw=None, min_entries: int = 128) -> list:
+    """Output rings on both sides of every change of kernel along latitude:
+    the op's rings with at least `min_entries` stored entries take the
+    spectral path (the library's default threshold), the others the direct
+    kernels; from the host-side export of the op's entries."""
+    kw = {k: v for k, v in (plan_kw or {}).items() if k in ("node_spacing", "quadrature", "basis", "sampling")}
+    e = disco.psi_entries(*plan_args, transpose=transpose, **kw)
+    nlat_o = plan_args[0] if transpose else plan_args[2]
+    counts = np.zeros((nlat_o, e["phases"]), dtype=np.int64)
+    np.add.at(counts, (e["out_ring"], e["phase"]), 1)
+    heavy = (counts >= min_entries).any(axis=1)
+    out = []
+    for t in range(1, nlat_o):
+        if heavy[t] != heavy[t - 1]:
+            out += [t - 1, t]
+    return out
+
+
+def per_ring_max_error(got: np.ndarray, ref: np.ndarray, pix: np.ndarray, nlon: int):
+    """Largest |got - ref| on each sampled ring relative to that ring's largest
+    |ref| (over batch and channels): (worst ratio, its ring, rings checked).
+    got and ref are [B, C, n] at the flat pixels pix."""
+    rings = pix // nlon
+    worst, worst_ring = 0.0, -1
+    for t in np.unique(rings):
+        sel = rings == t
+        scale = float(np.abs(ref[:, :, sel]).max())
+        err = float(np.abs(got[:, :, sel] - ref[:, :, sel]).max())
+        r = err / scale if scale > 0 else err
+        if r > worst:
+            worst, worst_ring = r, int(t)
+    return worst, worst_ring, int(np.unique(rings).size)

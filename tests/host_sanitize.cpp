@@ -1,0 +1,175 @@
+// host_sanitize.cpp -- drives every host-side step of a plan (grid and
+// quadrature, neighbour search, basis evaluation, the packed, sweep,
+// spectral and stencil layouts, the work figures) on the CPU, for a build
+// with AddressSanitizer and UndefinedBehaviorSanitizer.  No device call is
+// made: the layouts are built exactly as plan creation builds them before
+// uploading.  Exits non-zero on the first step that fails; a sanitizer
+// finding aborts the process.
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "disco.h"
+#include "disco_internal.h"
+
+using namespace disco;
+
+namespace {
+
+int failures = 0;
+
+void check(int rc, const std::string& what, const std::string& err) {
+    if (rc != DISCO_OK) {
+        std::printf("FAIL %s: status %d (%s)\n", what.c_str(), rc, err.c_str());
+        ++failures;
+    }
+}
+
+void run_op(const PlanParams& p, bool transpose, bool quad_at_output, const char* tag) {
+    HostOp op;
+    std::string err;
+    const std::string what = std::string(tag) + (transpose ? " transpose" : " forward") +
+                             (quad_at_output ? " adjoint" : "");
+    int rc = build_host_op(p, transpose, &op, &err, quad_at_output);
+    check(rc, what + " build_host_op", err);
+    if (rc != DISCO_OK) return;
+    (void)pattern_work(op, {});
+    const CellMap cm = cell_map(op.basis);
+    (void)cm;
+    for (int64_t e = 0; e < (int64_t)op.t_in.size(); ++e) {
+        int cell = 0;
+        float v[4];
+        if (!entry_cell_values(op, e, &cell, v)) {
+            std::printf("FAIL %s: entry %lld has a value outside its cell\n", what.c_str(), (long long)e);
+            ++failures;
+            break;
+        }
+    }
+    for (int tile : {64, 128, kTileQ}) {
+        for (int target : {64, 512}) {
+            PackedHost P;
+            check(pack_op(op, target, {}, &P, &err, tile), what + " pack_op", err);
+        }
+    }
+    if (op.g.stride == 1) {
+        for (int tile : {kStencilSmallTile, kStencilTile}) {
+            StencilHost S;
+            check(pack_stencil(op, 256, tile, &S, &err), what + " pack_stencil", err);
+        }
+    }
+    if (op.basis != DISCO_BASIS_BILINEAR_3X3) return;
+    SpectralHost sp;
+    std::vector<uint8_t> heavy;
+    check(build_spectral(op, 128, &sp, &heavy, &err), what + " build_spectral", err);
+    std::vector<uint8_t> light(heavy.size());
+    for (size_t i = 0; i < heavy.size(); ++i) light[i] = !heavy[i];
+    (void)pattern_work(op, heavy);
+    (void)pattern_work(op, light);
+    PackedHost PL;
+    check(pack_op(op, 512, heavy, &PL, &err), what + " pack_op (light)", err);
+    SweepHost sw;
+    check(pack_sweep(op, 768, heavy, &sw, &err), what + " pack_sweep", err);
+    std::vector<uint8_t> rest(sw.covered);
+    for (size_t i = 0; i < rest.size() && i < heavy.size(); ++i) rest[i] |= heavy[i];
+    PackedHost PR;
+    check(pack_op(op, 512, rest, &PR, &err), what + " pack_op (rest)", err);
+}
+
+void run_plan(int nlat_in, int nlon_in, int nlat_out, int nlon_out, double tc, int basis, int quad, int sampling,
+              double h) {
+    PlanParams p{};
+    p.nlat_in = nlat_in; p.nlon_in = nlon_in; p.nlat_out = nlat_out; p.nlon_out = nlon_out;
+    p.theta_c = tc;
+    p.h = h > 0 ? h : (basis == DISCO_BASIS_BILINEAR_3X3 ? tc / 3.0 : tc / 4.0);
+    p.quadrature = quad;
+    p.basis = basis;
+    p.sampling = sampling;
+    p.flags = DISCO_PLAN_BACKWARD;
+    char tag[160];
+    std::snprintf(tag, sizeof(tag), "%dx%d->%dx%d basis %d quad %d sampling %d h %.4g", nlat_in, nlon_in, nlat_out,
+                  nlon_out, basis, quad, sampling, p.h);
+    for (bool tr : {false, true})
+        for (bool adj : {false, true}) run_op(p, tr, adj, tag);
+}
+
+// The C ABI's host-side paths: argument validation of plan creation (every
+// rejected case returns before any device call), the host-only export of the
+// stored entries, and the status strings.  Plan creation with valid
+// arguments builds every op on the host and then needs a device; without one
+// it must fail cleanly with DISCO_ERR_DEVICE.
+void run_abi() {
+    const double pi = 3.14159265358979323846;
+    disco_plan_t plan = nullptr;
+    struct Bad { int a, b, c, d; double tc; int expect; } bad[] = {
+        {0, 16, 8, 16, 0.5, DISCO_ERR_INVALID_ARGUMENT}, {8, 1, 8, 16, 0.5, DISCO_ERR_INVALID_ARGUMENT},
+        {8, 16, 8, 16, 0.0, DISCO_ERR_INVALID_ARGUMENT}, {8, 16, 8, 16, 4.0, DISCO_ERR_INVALID_ARGUMENT},
+        {8, 16, 8, 24, 0.5, DISCO_ERR_UNSUPPORTED}};
+    for (auto& c : bad) {
+        const disco_status_t s = disco_plan_create(c.a, c.b, c.c, c.d, c.tc, nullptr, &plan);
+        if (s != c.expect) {
+            std::printf("FAIL plan_create(%d,%d,%d,%d,%g): %d, expected %d\n", c.a, c.b, c.c, c.d, c.tc, (int)s,
+                        c.expect);
+            ++failures;
+        }
+        (void)disco_last_error();
+    }
+    disco_basis_t b{DISCO_BASIS_BILINEAR_3X3, 7, 0.0, 0, 0};
+    if (disco_plan_create(8, 16, 8, 16, 0.5, &b, &plan) != DISCO_ERR_UNSUPPORTED) ++failures;
+    b = disco_basis_t{DISCO_BASIS_BILINEAR_3X3, 0, -1.0, 0, 0};
+    if (disco_plan_create(8, 16, 8, 16, 0.5, &b, &plan) != DISCO_ERR_INVALID_ARGUMENT) ++failures;
+    if (disco_plan_create(8, 16, 8, 16, 0.5, nullptr, nullptr) != DISCO_ERR_INVALID_ARGUMENT) ++failures;
+    // Valid arguments: host build of all four ops, then no device.
+    b = disco_basis_t{DISCO_BASIS_BILINEAR_3X3, 0, 0.0, 0, DISCO_PLAN_BACKWARD};
+    const disco_status_t sv = disco_plan_create(32, 64, 16, 32, 3 * pi / 16, &b, &plan);
+    if (sv == DISCO_OK) (void)disco_plan_destroy(plan);
+    (void)disco_plan_destroy(nullptr);
+    // Entry export on several grids and bases, sized then filled.
+    const int cases[][4] = {{16, 32, 8, 16}, {8, 16, 16, 32}, {33, 300, 33, 300}};
+    for (auto& c : cases)
+        for (int basis : {0, 1, 2})
+            for (int tr : {0, 1}) {
+                disco_basis_t bb{basis, 0, 0.0, 0, 0};
+                int64_t n = 0;
+                int32_t P = 0, S = 0;
+                const double tc = 3 * pi / std::min(c[0], c[2]);
+                disco_status_t s = disco_psi_entries(c[0], c[1], c[2], c[3], tc, &bb, tr, 0, nullptr, nullptr, nullptr,
+                                                     nullptr, nullptr, &n, &P, &S);
+                if (s != DISCO_OK || n <= 0) { ++failures; continue; }
+                std::vector<int32_t> r((size_t)n), ph((size_t)n), ri((size_t)n), off((size_t)n);
+                std::vector<float> v((size_t)n * 16);
+                s = disco_psi_entries(c[0], c[1], c[2], c[3], tc, &bb, tr, n, r.data(), ph.data(), ri.data(), off.data(),
+                                      v.data(), &n, &P, &S);
+                if (s != DISCO_OK) ++failures;
+            }
+    for (int s = 0; s <= 7; ++s) (void)disco_status_string((disco_status_t)s);
+}
+
+}  // namespace
+
+int main(int argc, char** argv) {
+    const bool big = argc > 1 && std::string(argv[1]) == "--big";
+    const double pi = 3.14159265358979323846;
+    // Cell-centred grids: same grid, downsampling, upsampling, odd sizes,
+    // latitude-only change, several tiles with a ragged tail.
+    const int cases[][4] = {{8, 16, 8, 16},   {16, 32, 8, 16},  {12, 24, 6, 12},   {8, 16, 16, 32},
+                            {32, 64, 32, 64}, {10, 20, 5, 20},  {33, 300, 33, 300}, {128, 256, 64, 128},
+                            {64, 128, 64, 128}, {256, 512, 512, 1024}};
+    for (auto& c : cases) {
+        const double tc = 3 * pi / std::min(c[0], c[2]);
+        for (int basis : {0, 1, 2}) run_plan(c[0], c[1], c[2], c[3], tc, basis, 0, 0, 0.0);
+        run_plan(c[0], c[1], c[2], c[3], tc, 0, 1, 0, 0.0);
+        run_plan(c[0], c[1], c[2], c[3], tc, 0, 0, 0, tc / 2);
+    }
+    // The pole-including grid (App. A).
+    const int poles[][4] = {{9, 16, 9, 16}, {17, 32, 9, 16}, {9, 16, 17, 32}, {41, 80, 41, 80}};
+    for (auto& c : poles) {
+        const double tc = 3 * pi / (std::min(c[0], c[2]) - 1);
+        for (int basis : {0, 1, 2}) run_plan(c[0], c[1], c[2], c[3], tc, basis, 0, 1, 0.0);
+    }
+    if (big) run_plan(2048, 4096, 2048, 4096, 3 * pi / 2048, 0, 0, 0, 0.0);
+    run_abi();
+    std::printf("%s (%d failures)\n", failures ? "FAILED" : "OK", failures);
+    return failures ? 1 : 0;
+}
