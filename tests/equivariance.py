@@ -23,9 +23,20 @@ Pieces:
   * rotation: (Q f)(w) = f(Q^{-1} w), evaluated exactly from the expansion at
     the rotated grid points; Q = Z(alpha) Y(beta) Z(gamma), active,
     right-handed;
+  * rotation in harmonic space (the fast path): Wigner D matrices
+    D_{m'm} = e^{-i m' alpha} d_{m'm}(beta) e^{-i m gamma}, d(beta) =
+    exp(-i beta J_y) from the eigenvectors of J_y in the |l m> basis
+    (computed once per degree), in this basis (no Condon-Shortley phase, so
+    conjugated by (-1)^m for m > 0); pinned against the point evaluation
+    above;
   * the error (App. D): mean over signals and rotations of
-    ||D(Q f) - Q(D f)|| / ||D(Q f)||, norms from the grid's quadrature, where
-    Q(D f) rotates the analysed (projected) output.
+    ||P D(Q f) - Q P D(f)|| / ||P D(Q f)||, norms from the grid's quadrature,
+    with P the projection onto degrees below L (analysis then synthesis) on
+    both sides: the grid holds a signal band-limited at L exactly, and what
+    the convolution puts at higher degrees is not a rotation error (with
+    both sides projected a rotation about z is exact at any angle, because
+    the op commutes with whole-pixel longitude shifts and so keeps each
+    longitudinal frequency below L).
 Filters (App. D): cutoff 5 pi / L, four nodes along theta (and four along
 phi for the directional, separable filter); best case the smooth
 psi_S(theta) = exp(-c^2 / (c^2 - theta^2)) at the nodes (times cos(phi) for
@@ -161,6 +172,80 @@ def rotate_grid(b: np.ndarray, Q: np.ndarray, L: int) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------- #
+# Batched synthesis, analysis and rotation in harmonic space (fast path)
+# --------------------------------------------------------------------------- #
+_JY = {}
+
+
+def jy_eigen(l: int):
+    """Eigenvalues and eigenvectors of J_y on the degree-l space (basis
+    m = -l..l): J_y = (J_+ - J_-) / 2i with <m+1|J_+|m> = sqrt(l(l+1) - m(m+1))."""
+    if l not in _JY:
+        n = 2 * l + 1
+        m = np.arange(-l, l)
+        Jp = np.zeros((n, n))
+        Jp[np.arange(1, n), np.arange(n - 1)] = np.sqrt(l * (l + 1) - m * (m + 1.0))
+        _JY[l] = np.linalg.eigh((Jp - Jp.T) / 2j)
+    return _JY[l]
+
+
+class Harmonics:
+    """Degrees below L on the (L + 1) x 2L pole-including grid, for batches of
+    S signals held as coefficients b[l, m, s] (0 <= m <= l < L, the
+    convention above): synthesis by a Legendre table and an FFT along
+    longitude, analysis by per-m weighted least squares (pseudo-inverses
+    computed once), rotation by Wigner D matrices."""
+
+    def __init__(self, L: int, q: np.ndarray):
+        self.L = L
+        th, _ = pole_grid(L)
+        P = legendre_table(L, np.cos(th))                  # [l, m, t]
+        sq = np.sqrt(np.asarray(q, dtype=np.float64))
+        self.Pt = [np.ascontiguousarray(P[m:, m].T) for m in range(L)]            # [t, l]
+        self.pinv = [np.linalg.pinv(self.Pt[m] * sq[:, None]) * sq[None, :] for m in range(L)]
+
+    def synth(self, b: np.ndarray) -> np.ndarray:
+        """f[s, t, p] from b[l, m, s]: per m the ring values of the m-th
+        longitudinal frequency, then a real inverse FFT along longitude."""
+        from scipy import fft
+        L = self.L
+        X = np.zeros((L + 1, L + 1, b.shape[2]), dtype=np.complex128)   # [m, t, s]
+        for m in range(L):
+            X[m] = self.Pt[m] @ b[m:, m]
+        f = fft.irfft(X, n=2 * L, axis=0, workers=-1) * (2 * L)         # [p, t, s]
+        return np.ascontiguousarray(f.transpose(2, 1, 0))
+
+    def analyse(self, f: np.ndarray) -> np.ndarray:
+        """b[l, m, s] of real signals f[s, t, p] (the quadrature-weighted
+        least-squares projection onto degrees below L)."""
+        from scipy import fft
+        L = self.L
+        F = fft.rfft(np.ascontiguousarray(f.transpose(2, 1, 0)), axis=0, workers=-1) / (2 * L)  # [m, t, s]
+        b = np.zeros((L, L, f.shape[0]), dtype=np.complex128)
+        for m in range(L):
+            b[m:, m] = self.pinv[m] @ (F[m].real if m == 0 else F[m])
+        return b
+
+    def rotate(self, b: np.ndarray, alpha: float, beta: float, gamma: float) -> np.ndarray:
+        """Coefficients of (Q f)(w) = f(Q^{-1} w), Q = Z(alpha) Y(beta) Z(gamma)."""
+        out = np.zeros_like(b)
+        for l in range(self.L):
+            lam, V = jy_eigen(l)
+            m = np.arange(-l, l + 1)
+            eps = np.where(m > 0, (-1.0) ** m, 1.0)
+            c = np.concatenate([np.conj(b[l, 1:l + 1][::-1]), b[l, :l + 1]], axis=0)   # m = -l..l
+            c = c * (eps * np.exp(-1j * m * gamma))[:, None]
+            c = V @ (np.exp(-1j * beta * lam)[:, None] * (V.conj().T @ c))
+            c = c * (eps * np.exp(-1j * m * alpha))[:, None]
+            out[l, :l + 1] = c[l:]
+        return out
+
+
+def random_coefficients_batch(L: int, S: int, rng: np.random.Generator) -> np.ndarray:
+    return np.stack([random_coefficients(L, rng) for _ in range(S)], axis=2)
+
+
+# --------------------------------------------------------------------------- #
 # Filters and the error
 # --------------------------------------------------------------------------- #
 def smooth_profile(theta: np.ndarray, cutoff: float) -> np.ndarray:
@@ -189,57 +274,70 @@ def norm_q(g: np.ndarray, q: np.ndarray) -> float:
     return math.sqrt(float((q[:, None] * g * g).sum()))
 
 
-def equivariance_error(op, L: int, q: np.ndarray, rotations, n_signals: int, seed: int):
+def equivariance_error(op, L: int, q: np.ndarray, angles, n_signals: int, seed: int, H=None):
     """Mean and standard deviation (over signals x rotations) of the relative
-    equivariance error of `op` (a callable f[L+1, 2L] -> y[L+1, 2L]) under
-    the given rotation matrices; q the grid's ring quadrature weights."""
+    equivariance error of `op` (a callable f[S, L+1, 2L] -> y[S, L+1, 2L]
+    applied to a batch of signals) under the rotations Z(a) Y(b) Z(g) given
+    as (a, b, g) triples; q the grid's ring quadrature weights.  Both sides
+    are projected onto degrees below L: ||P op(Q f) - Q P op(f)|| /
+    ||P op(Q f)||."""
+    H = H or Harmonics(L, q)
     rng = np.random.default_rng(seed)
+    b = random_coefficients_batch(L, n_signals, rng)
+    bd = H.analyse(op(H.synth(b)))
     errs = []
-    for _ in range(n_signals):
-        b = random_coefficients(L, rng)
-        f = synthesize_grid(b, L)
-        bd = analyse_grid(op(f), L, q)
-        for Q in rotations:
-            lhs = op(rotate_grid(b, Q, L))
-            rhs = rotate_grid(bd, Q, L)
-            errs.append(norm_q(lhs - rhs, q) / norm_q(lhs, q))
+    for ang in angles:
+        lhs = H.synth(H.analyse(op(H.synth(H.rotate(b, *ang)))))
+        rhs = H.synth(H.rotate(bd, *ang))
+        for s in range(n_signals):
+            errs.append(norm_q(lhs[s] - rhs[s], q) / norm_q(lhs[s], q))
     e = np.array(errs)
     return float(e.mean()), float(e.std())
 
 
-def rotations(kind: str, beta_deg, n: int, seed: int):
-    """App. D's rotations: for the axisymmetric filter uniform on
-    SO(3)/SO(2) (Z(alpha) Y(beta), cos(beta) uniform); for the directional one
-    Z(alpha) Y(beta) Z(gamma) with random alpha, gamma and a fixed beta."""
+def rotation_angles(kind: str, beta_deg, n: int, seed: int):
+    """App. D's rotations as Euler triples (alpha, beta, gamma) of
+    Z(alpha) Y(beta) Z(gamma): for the axisymmetric filter uniform on
+    SO(3)/SO(2) (gamma = 0, cos(beta) uniform); for the directional one
+    random alpha, gamma and a fixed beta."""
     rng = np.random.default_rng(seed)
     out = []
     for _ in range(n):
         a, g = rng.uniform(0.0, 2.0 * math.pi, 2)
         if kind == "axisym":
-            out.append(euler_zyz(a, math.acos(rng.uniform(-1.0, 1.0)), 0.0))
+            out.append((a, math.acos(rng.uniform(-1.0, 1.0)), 0.0))
         else:
-            out.append(euler_zyz(a, math.radians(beta_deg), g))
+            out.append((a, math.radians(beta_deg), g))
     return out
 
 
-def table(op_factory, Ls, n_signals: int = 5, n_rotations: int = 5, seed: int = 0):
+def rotations(kind: str, beta_deg, n: int, seed: int):
+    """The same rotations as 3 x 3 matrices."""
+    return [euler_zyz(*t) for t in rotation_angles(kind, beta_deg, n, seed)]
+
+
+def table(op_factory, Ls, n_signals: int = 5, n_rotations: int = 5, seed: int = 0, on_row=None):
     """Rows (L, filter, case, beta, mean %, std %) of a Table-5-shaped run.
     op_factory(L, cutoff, kind, w) returns the one-channel convolution on the
     (L + 1) x 2L grid with the axisymmetric ("axisym") or separable
     ("directional") basis and weights w [1, 1, K]; op_factory.quadrature(L)
-    gives the grid's ring weights."""
+    gives the grid's ring weights; on_row, if given, is called with each row
+    as it is finished."""
     rows = []
     for L in Ls:
         cutoff = 5.0 * math.pi / L
         q = op_factory.quadrature(L)
+        H = Harmonics(L, q)
         for kind, betas in (("axisym", [None]), ("directional", [0.0, 5.0, 10.0])):
             for case in ("best", "worst"):
                 w = filter_weights(kind, case, cutoff, np.random.default_rng(seed + 1))
                 op = op_factory(L, cutoff, kind, w)
                 for beta in betas:
-                    R = rotations(kind, beta, n_rotations, seed + 2)
-                    m, s = equivariance_error(op, L, q, R, n_signals, seed + 3)
+                    R = rotation_angles(kind, beta, n_rotations, seed + 2)
+                    m, s = equivariance_error(op, L, q, R, n_signals, seed + 3, H)
                     rows.append((L, kind, case, beta, 100.0 * m, 100.0 * s))
+                    if on_row:
+                        on_row(rows[-1])
     return rows
 
 
@@ -267,9 +365,9 @@ class GpuOps:
         wt = torch.from_numpy(np.asarray(w, dtype=np.float32)).to("cuda:0")
 
         def op(f):
-            x = torch.from_numpy(np.asarray(f, dtype=np.float32)[None, None]).to("cuda:0")
+            x = torch.from_numpy(np.asarray(f, dtype=np.float32)[:, None]).to("cuda:0")
             y = plan.forward(x, wt)
-            return y[0, 0].double().cpu().numpy()
+            return y[:, 0].double().cpu().numpy()
         return op
 
 
@@ -288,8 +386,8 @@ class OracleOps:
         o = self._o
 
         def op(f):
-            return o.forward(L + 1, 2 * L, L + 1, 2 * L, cutoff, np.asarray(f)[None, None], w,
-                             sampling=1, basis=basis)[0, 0]
+            return o.forward(L + 1, 2 * L, L + 1, 2 * L, cutoff, np.asarray(f)[:, None], w,
+                             sampling=1, basis=basis)[:, 0]
         return op
 
 
@@ -313,6 +411,7 @@ if __name__ == "__main__":
     ap.add_argument("--rotations", type=int, default=5)
     a = ap.parse_args()
     ops = GpuOps() if a.device == "gpu" else OracleOps()
-    for L in a.L:
-        rows = table(ops, [L], a.signals, a.rotations)
-        print(format_rows(rows), flush=True)
+    print("N_f = %d signals, N_Q = %d rotations, device %s" % (a.signals, a.rotations, a.device), flush=True)
+    rows = table(ops, a.L, a.signals, a.rotations,
+                 on_row=lambda r: print("  " + format_rows([r]).splitlines()[-1], flush=True))
+    print(format_rows(rows), flush=True)

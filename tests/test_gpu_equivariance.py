@@ -1,6 +1,7 @@
 """The equivariance harness (App. D) run on the library's op on the GPU: its
-errors equal the oracle's (the same op to fp32 rounding) and have the shape
-of Table 5 at L = 64."""
+errors equal the oracle's (the same op to fp32 rounding: rows the oracle
+puts at rounding level, the rotations about z, are at fp32 rounding level on
+the GPU) and have the shape of Table 5 at L = 64."""
 import numpy as np
 import pytest
 
@@ -16,7 +17,7 @@ def test_gpu_equivariance_errors_match_the_oracle():
     for g, c in zip(gpu, cpu):
         say("  %s %s %s: gpu %.5f%% oracle %.5f%%" % (g[1], g[2], g[3], g[4], c[4]))
         assert g[:4] == c[:4]
-        assert abs(g[4] - c[4]) <= 1e-3 * c[4] + 1e-5
+        assert abs(g[4] - c[4]) <= 1e-3 * c[4] + 1e-3     # percent: fp32 rounding is ~1e-5 relative
 
 
 def test_gpu_equivariance_table_shape():
