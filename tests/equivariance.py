@@ -274,13 +274,12 @@ def norm_q(g: np.ndarray, q: np.ndarray) -> float:
     return math.sqrt(float((q[:, None] * g * g).sum()))
 
 
-def equivariance_error(op, L: int, q: np.ndarray, angles, n_signals: int, seed: int, H=None):
-    """Mean and standard deviation (over signals x rotations) of the relative
-    equivariance error of `op` (a callable f[S, L+1, 2L] -> y[S, L+1, 2L]
-    applied to a batch of signals) under the rotations Z(a) Y(b) Z(g) given
-    as (a, b, g) triples; q the grid's ring quadrature weights.  Both sides
-    are projected onto degrees below L: ||P op(Q f) - Q P op(f)|| /
-    ||P op(Q f)||."""
+def equivariance_errors(op, L: int, q: np.ndarray, angles, n_signals: int, seed: int, H=None) -> np.ndarray:
+    """The relative equivariance error of `op` (a callable f[S, L+1, 2L] ->
+    y[S, L+1, 2L] applied to a batch of signals) for every signal and
+    rotation Z(a) Y(b) Z(g) given as (a, b, g) triples; q the grid's ring
+    quadrature weights.  Both sides are projected onto degrees below L:
+    ||P op(Q f) - Q P op(f)|| / ||P op(Q f)||."""
     H = H or Harmonics(L, q)
     rng = np.random.default_rng(seed)
     b = random_coefficients_batch(L, n_signals, rng)
@@ -291,7 +290,12 @@ def equivariance_error(op, L: int, q: np.ndarray, angles, n_signals: int, seed: 
         rhs = H.synth(H.rotate(bd, *ang))
         for s in range(n_signals):
             errs.append(norm_q(lhs[s] - rhs[s], q) / norm_q(lhs[s], q))
-    e = np.array(errs)
+    return np.array(errs)
+
+
+def equivariance_error(op, L: int, q: np.ndarray, angles, n_signals: int, seed: int, H=None):
+    """Mean and standard deviation over signals x rotations of the errors above."""
+    e = equivariance_errors(op, L, q, angles, n_signals, seed, H)
     return float(e.mean()), float(e.std())
 
 
@@ -317,7 +321,11 @@ def rotations(kind: str, beta_deg, n: int, seed: int):
 
 
 def table(op_factory, Ls, n_signals: int = 5, n_rotations: int = 5, seed: int = 0, on_row=None):
-    """Rows (L, filter, case, beta, mean %, std %) of a Table-5-shaped run.
+    """Rows (L, filter, case, beta, mean %, std %, sq mean %, sq std %) of a
+    Table-5-shaped run; the last two are the same statistics of the squared
+    ratio (||P op(Q f) - Q P op(f)||^2 / ||P op(Q f)||^2), reported beside
+    the ratio of norms because the printed table's magnitudes and its
+    quadratic growth with beta are those of the squared ratio.
     op_factory(L, cutoff, kind, w) returns the one-channel convolution on the
     (L + 1) x 2L grid with the axisymmetric ("axisym") or separable
     ("directional") basis and weights w [1, 1, K]; op_factory.quadrature(L)
@@ -334,8 +342,10 @@ def table(op_factory, Ls, n_signals: int = 5, n_rotations: int = 5, seed: int = 
                 op = op_factory(L, cutoff, kind, w)
                 for beta in betas:
                     R = rotation_angles(kind, beta, n_rotations, seed + 2)
-                    m, s = equivariance_error(op, L, q, R, n_signals, seed + 3, H)
-                    rows.append((L, kind, case, beta, 100.0 * m, 100.0 * s))
+                    e = equivariance_errors(op, L, q, R, n_signals, seed + 3, H)
+                    e2 = e * e
+                    rows.append((L, kind, case, beta, 100.0 * float(e.mean()), 100.0 * float(e.std()),
+                                 100.0 * float(e2.mean()), 100.0 * float(e2.std())))
                     if on_row:
                         on_row(rows[-1])
     return rows
@@ -392,10 +402,11 @@ class OracleOps:
 
 
 def format_rows(rows) -> str:
-    out = ["| L | filter | case | beta | error % (mean +- std) |", "|---|---|---|---|---|"]
-    for L, kind, case, beta, m, s in rows:
+    out = ["| L | filter | case | beta | error % (mean +- std) | squared ratio % (mean +- std) |",
+           "|---|---|---|---|---|---|"]
+    for L, kind, case, beta, m, s, m2, s2 in rows:
         b = "-" if beta is None else "%g deg" % beta
-        out.append("| %d | %s | %s | %s | %.3f +- %.3f |" % (L, kind, case, b, m, s))
+        out.append("| %d | %s | %s | %s | %.3f +- %.3f | %.3f +- %.3f |" % (L, kind, case, b, m, s, m2, s2))
     return "\n".join(out)
 
 

@@ -149,7 +149,7 @@ def test_table_shape_on_the_oracle():
     beta, starting from rounding level at beta = 0; the smooth axisymmetric
     filter errs less than the directional one at beta > 0."""
     rows = E.table(E.OracleOps(), [16], n_signals=3, n_rotations=3)
-    err = {(k, c, b): m for (_, k, c, b, m, _) in rows}
+    err = {(k, c, b): m for (_, k, c, b, m, *_) in rows}
     assert err[("axisym", "best", None)] < err[("axisym", "worst", None)]
     for c in ("best", "worst"):
         assert err[("directional", c, 0.0)] < err[("directional", c, 5.0)] < err[("directional", c, 10.0)]

@@ -23,7 +23,7 @@ def test_gpu_equivariance_errors_match_the_oracle():
 def test_gpu_equivariance_table_shape():
     rows = E.table(E.GpuOps(), [32, 64], n_signals=3, n_rotations=3)
     say(E.format_rows(rows))
-    err = {(L, k, c, b): m for (L, k, c, b, m, _) in rows}
+    err = {(L, k, c, b): m for (L, k, c, b, m, *_) in rows}
     for L in (32, 64):
         assert err[(L, "axisym", "best", None)] < err[(L, "axisym", "worst", None)]
         for c in ("best", "worst"):
