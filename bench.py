@@ -37,7 +37,8 @@ DEVICE_KERNEL = {"gather_z": "k_gather_z", "contract_z": "k_contract_z", "contra
                  "sweep_gather_z": "k_sweep",
                  "spectral_rfft": "k_rfft_rings", "spectral_mac": "k_spectral",
                  "spectral_irfft": "k_irfft_rings", "stencil": "k_stencil",
-                 "stencil_blocked": "k_stencil_blocked"}
+                 "stencil_blocked": "k_stencil_blocked", "mfma_gather_contract": "k_mfma",
+                 "mfma_weights": "k_mfma_wop"}
 # The paper's wall-clock for its timed layer (App. B: one channel, batch 1,
 # axisymmetric four-node filter, theta_c = 3 pi / L, (L + 1) x 2L pixels; NVIDIA
 # RTX 3090, TensorFlow sparse-dense products, mean of 10 runs), in seconds.
@@ -147,6 +148,15 @@ def kernel_model(name, wl, work, es, spec=None):
         m["valu"] = 2.0 * pairs * B * Ci
         dt = "mfma_bf16" if (name == "fused_gather_contract" and es == 2) else "mfma_f32"
         m[dt] = 2.0 * B * Ci * 9 * Co * outp
+    elif name == "mfma_gather_contract":
+        # x in, y out; the gather and the contraction both on bf16 matrix
+        # cores (counted at their algorithmic size: the non-zero triples and
+        # 9 basis functions, not the padded instruction shapes).
+        m["bytes"] = B * Ci * inp * es + B * Co * outp * es
+        m["mfma_bf16"] = 2.0 * pairs * B * Ci + 2.0 * B * Ci * 9 * Co * outp
+    elif name == "mfma_weights":
+        # W read, its operand table (8 bf16 per lane, 16 k per 9) written.
+        m.update(bytes=Ci * Co * 9 * es + Ci * Co * 16 * 2, bound="hbm")
     elif name == "reduce_partials":
         m.update(bound="hbm")
     else:
@@ -175,7 +185,8 @@ def model_roof(m, avg_s):
     t_bound = sum(m[u] / (PEAK_TFLOPS[u] * 1e12) for u in PEAK_TFLOPS)
     ach = m["flops"] / avg_s / 1e12
     peak = m["flops"] / t_bound / 1e12 if t_bound > 0 else FP32_VALU_PEAK_TFLOPS
-    return {"bound": "alu", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+    bound = "mfma" if m["flops"] > 0 and m["valu"] == 0 else "alu"
+    return {"bound": bound, "achieved": ach, "peak": peak, "unit": "TFLOP/s",
             "frac": (t_bound / avg_s) if t_bound > 0 else 0.0}
 
 

@@ -104,7 +104,15 @@ typedef enum {
     DISCO_ALGO_CONTRACT_THEN_GATHER = 2, /* W contraction on the input grid -> psi gather */
     DISCO_ALGO_FUSED = 3,       /* gather and contraction in one kernel; rings whose windows
                                    wrap whole input rings take the exact spectral (DFT) form */
-    DISCO_ALGO_FUSED_DIRECT = 4 /* the fused kernel for every ring (no spectral form) */
+    DISCO_ALGO_FUSED_DIRECT = 4, /* the fused kernel for every ring (no spectral form) */
+    DISCO_ALGO_MATRIX_CORE = 5   /* bf16 storage, 3x3 basis: the gather and the contraction both on
+                                    bf16 matrix cores, the values rounded to bf16 (Sec. 4.2, eq. 9);
+                                    AUTO takes it for bf16 storage where the op allows it (at most two
+                                    longitude phases, stride <= 4, nlon_in a multiple of 8, x 16-byte
+                                    and y 4-byte aligned).  The first bf16 call of an op builds its
+                                    tables (host packing and a synchronous upload, once per op); a
+                                    caller that captures graphs makes one such call first.  The
+                                    non-allocating entry point uses the tables only once built. */
 } disco_algo_t;
 
 typedef struct {

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(BUILD_DIR, "libdisco.so")
 
 SOURCES = ["disco_plan.cpp", "disco_pack.cpp", "disco_spectral_plan.cpp", "disco_abi.cpp", "disco_kernels.hip",
            "disco_fused.hip", "disco_spectral.hip", "disco_sweep.hip", "disco_stencil.hip", "disco_grad.hip",
-           "disco_noalloc.hip"]
+           "disco_noalloc.hip", "disco_mfma.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -30,6 +30,7 @@ struct disco_plan {
     void* wsel32 = nullptr;
     void* wsel16 = nullptr;
     hipStream_t aux = nullptr;  // runs the spectral rings beside the direct kernels
+    std::mutex lazy_mu;         // tables built on first use (the bf16 matrix-core layout)
 };
 
 namespace {
@@ -258,6 +259,33 @@ disco_status_t upload_stencil(const HostOp& h, StencilDev* d) {
     return DISCO_OK;
 }
 
+disco_status_t upload_mfma(const MfmaHost& H, MfmaDev* d) {
+    disco_status_t s;
+    if ((s = upload_vec(H.spans, &d->spans, &d->bytes, "hipMalloc(matrix-core spans)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.segs, &d->segs, &d->bytes, "hipMalloc(matrix-core segments)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.chunks, &d->chunks, &d->bytes, "hipMalloc(matrix-core chunks)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.aop, &d->aop, &d->bytes, "hipMalloc(matrix-core values)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.order, &d->order, &d->bytes, "hipMalloc(matrix-core order)")) != DISCO_OK) return s;
+    PackedDev& P = d->P;
+    if ((s = upload_vec(H.red_pattern, &P.red_pattern, &d->bytes, "hipMalloc(reduce)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.red_ptr, &P.red_ptr, &d->bytes, "hipMalloc(reduce)")) != DISCO_OK) return s;
+    if ((s = upload_vec(H.red_slots, &P.red_slots, &d->bytes, "hipMalloc(reduce)")) != DISCO_OK) return s;
+    d->n_segs = (int32_t)H.segs.size();
+    d->n_order = (int32_t)H.order.size();
+    d->n_qtiles = H.n_qtiles;
+    P.n_items = d->n_segs;
+    P.n_split = (int32_t)H.red_pattern.size();
+    P.n_slots = H.n_slots;
+    return DISCO_OK;
+}
+
+void free_mfma(MfmaDev* d) {
+    void* ptrs[] = {d->spans, d->segs, d->chunks, d->aop, d->order, d->P.red_pattern, d->P.red_ptr, d->P.red_slots};
+    for (void* p : ptrs)
+        if (p) (void)hipFree(p);
+    *d = MfmaDev{};
+}
+
 void free_packed(PackedDev* d) {
     void* ptrs[] = {d->spans, d->chunks, d->offs, d->vals, d->segs, d->items, d->red_pattern, d->red_ptr, d->red_slots};
     for (void* p : ptrs)
@@ -381,6 +409,8 @@ void free_op(DeviceOp* d) {
     free_packed(&d->packed_rest);
     free_spectral(&d->spectral);
     free_sweep(&d->sweep);
+    free_mfma(&d->mfma);
+    d->mfma_state = 0;
     void* sp[] = {d->stencil.pieces, d->stencil.chunks, d->stencil.vals, d->stencil.cells};
     for (void* p : sp)
         if (p) (void)hipFree(p);
@@ -520,7 +550,7 @@ disco_status_t check_dw_args(disco_plan_t plan, const DeviceOp& op, const disco_
 disco_status_t check_op_args(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
                              const disco_tensor_t* w, const disco_tensor_t* y, int32_t algo) {
     if (!x || !w || !y) return fail(DISCO_ERR_INVALID_ARGUMENT, "tensor descriptor is NULL");
-    if (algo < DISCO_ALGO_AUTO || algo > DISCO_ALGO_FUSED_DIRECT) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown algo");
+    if (algo < DISCO_ALGO_AUTO || algo > DISCO_ALGO_MATRIX_CORE) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown algo");
     const OpGeom& g = op.g;
     if (x->ndim != 4 || y->ndim != 4 || w->ndim != 3)
         return fail(DISCO_ERR_SHAPE, "x and y must be 4-D [B, C, nlat, nlon], w 3-D");
@@ -541,8 +571,9 @@ disco_status_t check_op_args(disco_plan_t plan, const DeviceOp& op, bool transpo
     if (transpose && (w->shape[0] != Ci || w->shape[1] != Co))
         return fail(DISCO_ERR_SHAPE, "transpose w must be [CinT, CoutT, " + ks + "]");
     const bool folded = op.basis != DISCO_BASIS_BILINEAR_3X3;
-    if (folded && (algo == DISCO_ALGO_GATHER_THEN_CONTRACT || algo == DISCO_ALGO_CONTRACT_THEN_GATHER))
-        return fail(DISCO_ERR_UNSUPPORTED, "only the 3x3 basis has the two-kernel schedules");
+    if (folded && (algo == DISCO_ALGO_GATHER_THEN_CONTRACT || algo == DISCO_ALGO_CONTRACT_THEN_GATHER ||
+                   algo == DISCO_ALGO_MATRIX_CORE))
+        return fail(DISCO_ERR_UNSUPPORTED, "only the 3x3 basis has the two-kernel and matrix-core schedules");
     if (Ci < 1 || Co < 1) return fail(DISCO_ERR_SHAPE, "channel counts must be >= 1");
     if (B > 65535 || Ci > 4096 || Co > 4096) return fail(DISCO_ERR_SHAPE, "batch or channels too large");
     return check_common(plan, x, w, y);
@@ -571,6 +602,42 @@ disco_status_t check_common(disco_plan_t plan, const disco_tensor_t* x, const di
     return DISCO_OK;
 }
 
+// Builds the op's bf16 matrix-core tables on first use (once per op; the
+// host op is rebuilt from the plan's parameters).  An op the layout does not
+// cover is marked so and left to the other kernels.
+disco_status_t ensure_mfma(disco_plan_t plan, const DeviceOp& cop) {
+    DeviceOp& op = const_cast<DeviceOp&>(cop);
+    std::lock_guard<std::mutex> lock(plan->lazy_mu);
+    if (op.mfma_state != 0) return DISCO_OK;
+    HostOp h;
+    MfmaHost H;
+    std::string err;
+    try {
+        int rc = build_host_op(plan->params, op.src_transpose, &h, &err, op.src_adjoint);
+        if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
+        rc = pack_mfma(h, &H, &err);
+        if (rc == DISCO_ERR_UNSUPPORTED) {
+            op.mfma_state = -1;
+            return DISCO_OK;
+        }
+        if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
+    } catch (const std::bad_alloc&) {
+        return fail(DISCO_ERR_OUT_OF_MEMORY, "host allocation failed while packing the matrix-core tables");
+    }
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return fail(DISCO_ERR_DEVICE, "hipGetDevice failed");
+    if (cur != plan->device && hipSetDevice(plan->device) != hipSuccess)
+        return fail(DISCO_ERR_DEVICE, "hipSetDevice failed");
+    disco_status_t s = upload_mfma(H, &op.mfma);
+    if (cur != plan->device) (void)hipSetDevice(cur);
+    if (s != DISCO_OK) {
+        free_mfma(&op.mfma);
+        return s;
+    }
+    op.mfma_state = 1;
+    return DISCO_OK;
+}
+
 disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
                       const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream, int32_t algo,
                       bool depthwise, const ExtScratch* ext) {
@@ -592,8 +659,23 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
     }
     a.B = (int)B; a.Ci = (int)Ci; a.Co = (int)Co; a.w_trans = transpose; a.stream = stream;
 
-    const Dispatch dp = dispatch(op, algo, (int)Ci, (int)Co, x->dtype);
-    algo = dp.algo;
+    // bf16 storage with the 3x3 basis: the matrix-core kernel where the op
+    // has its layout (built here on the first such call, never by the
+    // non-allocating entry point) and x and y are aligned for its vector
+    // accesses.
+    bool mfma = false;
+    if (!axisym && x->dtype == DISCO_BFLOAT16 &&
+        (algo == DISCO_ALGO_AUTO || algo == DISCO_ALGO_FUSED || algo == DISCO_ALGO_MATRIX_CORE)) {
+        if (!ext && op.mfma_state == 0 && (s = ensure_mfma(plan, op)) != DISCO_OK) return s;
+        mfma = op.mfma_state == 1 && ((uintptr_t)x->data % 16) == 0 && ((uintptr_t)y->data % 4) == 0;
+    }
+    if (algo == DISCO_ALGO_MATRIX_CORE && !mfma)
+        return fail(DISCO_ERR_UNSUPPORTED, "the matrix-core kernel needs bf16 storage, the 3x3 basis, at most two "
+                                           "longitude phases, stride <= 4, nlon_in a multiple of 8 and aligned x "
+                                           "(16 bytes) and y (4 bytes)");
+    if (mfma) algo = DISCO_ALGO_MATRIX_CORE;
+    const Dispatch dp = dispatch(op, mfma ? DISCO_ALGO_FUSED_DIRECT : algo, (int)Ci, (int)Co, x->dtype);
+    if (!mfma) algo = dp.algo;
     const bool spectral = dp.spectral, sweep = dp.sweep;
     const PackedDev& packed = axisym ? op.packed : *dp.packed;
     // One output channel on a stride-1 op takes the blocked stencil kernel.
@@ -603,6 +685,8 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
         ws = workspace_bytes_fused(a, op.stencil.P);
     } else if (axisym) {
         ws = workspace_bytes_fused(a, packed);
+    } else if (mfma) {
+        ws = workspace_bytes_mfma(a);
     } else if (algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {
         ws = workspace_bytes_contract_then_gather(a);
     } else if (algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
@@ -633,6 +717,8 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
         e = launch_stencil_blocked(a, op.stencil, ws_ptr);
     } else if (axisym) {
         e = launch_stencil(a, packed, ws_ptr);
+    } else if (mfma) {
+        e = launch_mfma(a, ws_ptr);
     } else if (algo == DISCO_ALGO_CONTRACT_THEN_GATHER) {
         e = launch_contract_then_gather(a, ws_ptr);
     } else if (algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
@@ -928,6 +1014,8 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
         return fail(DISCO_ERR_DEVICE, "no HIP device available");
     }
     plan->params = p;
+    plan->tr.src_transpose = plan->fwd_adj.src_transpose = true;
+    plan->fwd_adj.src_adjoint = plan->tr_adj.src_adjoint = true;
     s = upload_op(hf, &plan->fwd);
     if (s == DISCO_OK) s = upload_op(ht, &plan->tr);
     if (s == DISCO_OK && with_backward) s = upload_op(hfa, &plan->fwd_adj);
@@ -1029,11 +1117,17 @@ disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t a
                                  int32_t c_out, int32_t dtype, int32_t capacity, char* names,
                                  int64_t* out_pixels, int64_t* in_pixels, int64_t* pairs, int32_t* count) {
     if (!plan || !count) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan or count is NULL");
-    if (algo < DISCO_ALGO_AUTO || algo > DISCO_ALGO_FUSED_DIRECT) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown algo");
+    if (algo < DISCO_ALGO_AUTO || algo > DISCO_ALGO_MATRIX_CORE) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown algo");
     if (c_in < 1 || c_out < 1) return fail(DISCO_ERR_SHAPE, "channel counts must be >= 1");
     if (dtype != DISCO_FLOAT32 && dtype != DISCO_BFLOAT16) return fail(DISCO_ERR_DTYPE, "unknown dtype");
     const DeviceOp& op = transpose ? plan->tr : plan->fwd;
-    const Dispatch dp = dispatch(op, algo, c_in, c_out, dtype);
+    // The matrix-core kernel: what a bf16 call with this algo runs (its
+    // tables are not built by this query).
+    const bool mfma = dtype == DISCO_BFLOAT16 && mfma_supported(op.g, op.basis) && op.mfma_state >= 0 &&
+                      (algo == DISCO_ALGO_AUTO || algo == DISCO_ALGO_FUSED || algo == DISCO_ALGO_MATRIX_CORE);
+    if (algo == DISCO_ALGO_MATRIX_CORE && !mfma)
+        return fail(DISCO_ERR_UNSUPPORTED, "no matrix-core kernel for this op and dtype");
+    const Dispatch dp = dispatch(op, mfma ? DISCO_ALGO_FUSED_DIRECT : algo, c_in, c_out, dtype);
     struct Row { const char* name; Work w; };
     std::vector<Row> rows;
     auto spectral_rows = [&op](const SpectralDev&, std::vector<Row>* r) {
@@ -1049,7 +1143,11 @@ disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t a
     ea.B = 1;
     ea.Ci = c_in;
     ea.Co = c_out;
-    if (op.basis != DISCO_BASIS_BILINEAR_3X3) {
+    if (mfma) {
+        rows.push_back({"mfma_weights", Work{0, 0, 0}});
+        rows.push_back({"mfma_gather_contract", all});
+        if (op.mfma.P.n_split > 0) rows.push_back({"reduce_partials", Work{0, 0, 0}});
+    } else if (op.basis != DISCO_BASIS_BILINEAR_3X3) {
         if (dp.algo != DISCO_ALGO_GATHER_THEN_CONTRACT && dp.algo != DISCO_ALGO_CONTRACT_THEN_GATHER) {
             // Folded psi: one value per (output pixel, input pixel) pair.
             const Work fw{all.out_pixels, all.in_pixels, op.n_entries * op.g.nq};

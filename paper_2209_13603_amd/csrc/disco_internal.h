@@ -272,6 +272,56 @@ struct SpectralDev {
     int64_t bytes = 0;
 };
 
+// ---------------------------------------------------------------------------
+// Matrix-core layout (disco_mfma.hip) for bf16 storage: the 3x3 basis, at
+// most two longitude phases, stride <= 4, nlon_in a multiple of 8.
+//
+// Both steps of the gather-then-contract product run on bf16 matrix cores.
+// For one output ring, the entries of all its phases on one input ring are
+// laid on the shortest arc of offsets that covers them, cut into groups of
+// eight consecutive offsets (d0 .. d0 + 7); four groups make a chunk, the
+// 32-long reduction of one v_mfma_f32_16x16x32_bf16:
+//   Z[phase][k][q] += sum_{group, u} V[phase][k][group][u] x[ring][s q + d0 + u]
+// with the values V (rows k = 0..8, rows 9..15 zero) as the A operand and the
+// staged input as the B operand.  The second product
+//   y[co][q] += sum_{ci, k} W[co][ci][k] Z[ci][k][q]
+// takes two input channels per instruction.  A workgroup (4 waves, 16 output
+// longitudes per block, four blocks per wave) runs one segment of an output
+// ring (consecutive groups within the chunk and staged-element budgets) for
+// kMfmaTile output longitudes; rings cut into several segments write fp32
+// partial outputs to a slot per (segment, phase), summed by
+// k_reduce_partials.
+constexpr int kMfmaTile = 256;       // output longitudes per workgroup
+constexpr int kMfmaCis = 8;          // input channels staged per pass
+constexpr int kMfmaMaxChunks = 8;    // chunks (32 offsets each) of one segment
+constexpr int kMfmaMaxElems = 1280;  // staged elements per channel of one segment
+// Spans use PSpan: row = ring * nlon_i, dstart (a multiple of 8), len and
+// lds_base in staged elements (element e of a span holds the two inputs at
+// longitudes s q0 + dstart + e and + 1, q0 the tile's first output longitude).
+struct MSeg { int32_t ring, chunk_begin, chunk_end, span_begin, span_end, n_elems, slot, pad; };
+struct MChunkHdr { int32_t grp[4]; };  // staged element of each group's offset d0 at q = q0
+struct MfmaHost {
+    int32_t P = 1;
+    std::vector<PSpan> spans;
+    std::vector<MSeg> segs;
+    std::vector<MChunkHdr> chunks;
+    std::vector<uint16_t> aop;  // per chunk and phase: 64 lanes x 8 bf16 (lane i + 16 g: row i, group g)
+    std::vector<int32_t> red_pattern, red_ptr, red_slots;
+    int32_t n_slots = 0;
+    // Dispatch order: workgroup index -> work item (segment * n_qtiles +
+    // longitude tile) or -1 (nothing to do).  Workgroups go round-robin to
+    // the 8 XCDs, so entry x + 8 j is the j-th item of XCD x: each XCD gets a
+    // contiguous run of output rings (which share input rings in its L2) of
+    // about an eighth of the total work, heaviest items first.
+    std::vector<int32_t> order;
+    int32_t n_qtiles = 0;
+};
+// Whether pack_mfma covers an op of this geometry and basis.
+inline bool mfma_supported(const OpGeom& g, int basis) {
+    return basis == DISCO_BASIS_BILINEAR_3X3 && g.P <= 2 && g.stride <= 4 && g.nlon_i % 8 == 0;
+}
+int pack_mfma(const HostOp& op, MfmaHost* out, std::string* err);
+
 struct PackedDev {
     int32_t tile = kTileQ;       // lanes per workgroup the spans were cut for
     PSpan* spans = nullptr;
@@ -284,6 +334,17 @@ struct PackedDev {
     int32_t* red_ptr = nullptr;
     int32_t* red_slots = nullptr;
     int32_t n_items = 0, n_split = 0, n_slots = 0;
+    int64_t bytes = 0;
+};
+
+struct MfmaDev {
+    PSpan* spans = nullptr;
+    MSeg* segs = nullptr;
+    MChunkHdr* chunks = nullptr;
+    uint16_t* aop = nullptr;
+    int32_t* order = nullptr;
+    PackedDev P;                 // the reduction tables (red_*, n_split, n_slots)
+    int32_t n_segs = 0, n_order = 0, n_qtiles = 0;
     int64_t bytes = 0;
 };
 
@@ -316,6 +377,9 @@ struct DeviceOp {
     SpectralDev spectral;
     SweepDev sweep;          // light patterns walked by the sweep kernel (Ci <= kCIC)
     StencilDev stencil;      // longitude stride 1: the blocked layout of the stencil kernels
+    MfmaDev mfma;            // bf16 matrix-core layout, built at the op's first bf16 call
+    int8_t mfma_state = 0;   // 0 not built yet, 1 built, -1 the op has no such layout
+    bool src_transpose = false, src_adjoint = false;  // build_host_op arguments of this op
     PackedDev packed_rest;   // light patterns the sweep runs do not cover
     int32_t* rest_pats = nullptr;  // device: those patterns' indices (gather-then-contract schedule)
     int32_t n_rest_pats = 0;
@@ -378,6 +442,10 @@ hipError_t launch_gather_z_all(const ExecArgs& a, float* z, float* ws);
 size_t workspace_bytes_gather_then_contract(const ExecArgs& a);
 size_t workspace_bytes_contract_then_gather(const ExecArgs& a);
 hipError_t launch_fused(const ExecArgs& a, const PackedDev& P, float* partial_ws);
+// The matrix-core kernel (bf16 storage): workspace = the W operand table
+// (workspace_bytes_mfma_w) followed by the partial slots of split rings.
+size_t workspace_bytes_mfma(const ExecArgs& a);
+hipError_t launch_mfma(const ExecArgs& a, void* ws);
 size_t workspace_bytes_fused(const ExecArgs& a, const PackedDev& P);
 // stages: bit 0 the input-ring transforms, bit 1 the frequency-domain
 // products, bit 2 the inverse transforms (in that order on one stream).

@@ -2,6 +2,7 @@
 // fused kernel (layout described in disco_internal.h).
 #include <algorithm>
 #include <cstdio>
+#include <cstring>
 
 #include "disco.h"
 #include "disco_internal.h"
@@ -518,6 +519,199 @@ int pack_stencil(const HostOp& op, int target_entries, int tile, StencilHost* ou
             acc += n;
         }
     }
+    *out = std::move(H);
+    return DISCO_OK;
+}
+
+}  // namespace disco
+
+namespace disco {
+
+namespace {
+
+// fp32 -> bf16, round to nearest even (NaN kept quiet).
+uint16_t bf16_rne(float f) {
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// One group: eight consecutive offsets d0 .. d0 + 7 of input ring ti, with the
+// values of every phase (zero where a phase has no entry).
+struct MGroup {
+    int32_t ti, d0;
+    float v[2][kBasis][8];
+};
+
+}  // namespace
+
+int pack_mfma(const HostOp& op, MfmaHost* out, std::string* err) {
+    const OpGeom& g = op.g;
+    const int s = g.stride, P = g.P, N = g.nlon_i;
+    if (!mfma_supported(g, op.basis)) {
+        if (err) *err = "the matrix-core layout needs the 3x3 basis, at most two longitude phases, stride <= 4 "
+                        "and nlon_in a multiple of 8";
+        return DISCO_ERR_UNSUPPORTED;
+    }
+    const int halo = s * (kMfmaTile - 1);
+    MfmaHost H;
+    H.P = P;
+    for (int to = 0; to < g.nlat_o; ++to) {
+        // 1. Offsets (mod nlon_i) of every input ring, over all phases.
+        std::vector<std::vector<int32_t>> ring_d((size_t)g.nlat_i);
+        for (int r = 0; r < P; ++r) {
+            const int pat = to * P + r;
+            for (int32_t e = op.pat_ptr[(size_t)pat]; e < op.pat_ptr[(size_t)pat + 1]; ++e)
+                ring_d[(size_t)op.t_in[(size_t)e]].push_back(op.d[(size_t)e]);
+        }
+        // 2. Per input ring, the shortest arc of offsets covering them all,
+        // cut into groups of eight; each entry lands in exactly one slot.
+        std::vector<MGroup> groups;
+        std::vector<int32_t> arc_start((size_t)g.nlat_i, -1), first_group((size_t)g.nlat_i, -1);
+        for (int ti = 0; ti < g.nlat_i; ++ti) {
+            std::vector<int32_t>& ds = ring_d[(size_t)ti];
+            if (ds.empty()) continue;
+            std::sort(ds.begin(), ds.end());
+            ds.erase(std::unique(ds.begin(), ds.end()), ds.end());
+            int32_t a0 = ds[0], gap = N - ds.back() + ds[0];  // gap across the seam
+            for (size_t i = 1; i < ds.size(); ++i)
+                if (ds[i] - ds[i - 1] > gap) {
+                    gap = ds[i] - ds[i - 1];
+                    a0 = ds[i];
+                }
+            const int32_t width = N - gap + 1;
+            const int ng = (width + 7) / 8;
+            arc_start[(size_t)ti] = a0;
+            first_group[(size_t)ti] = (int32_t)groups.size();
+            for (int j = 0; j < ng; ++j) {
+                MGroup G{};
+                G.ti = ti;
+                G.d0 = a0 + 8 * j;
+                groups.push_back(G);
+            }
+        }
+        for (int r = 0; r < P; ++r) {
+            const int pat = to * P + r;
+            for (int32_t e = op.pat_ptr[(size_t)pat]; e < op.pat_ptr[(size_t)pat + 1]; ++e) {
+                const int ti = op.t_in[(size_t)e];
+                const int32_t pos = ((op.d[(size_t)e] - arc_start[(size_t)ti]) % N + N) % N;
+                MGroup& G = groups[(size_t)(first_group[(size_t)ti] + pos / 8)];
+                for (int k = 0; k < kBasis; ++k) G.v[r][k][pos % 8] = op.val[(size_t)e * kBasis + k];
+            }
+        }
+        // 3. Segments: runs of groups under the chunk and staged-element
+        // budgets; spans = per input ring, the offsets its groups read.
+        struct Seg { size_t g0, g1; };
+        std::vector<Seg> segs;
+        // Elements staged for groups d0 in [dmin, dmax]: a lane reads elements
+        // up to (dmax - dstart) + halo + 6, each holding two inputs.
+        auto span_len = [&](int32_t dmin, int32_t dmax) {
+            const int32_t dstart = dmin & ~7;
+            return (halo + (dmax - dstart) + 7 + 7) & ~7;
+        };
+        auto seg_elems = [&](size_t g0, size_t g1) {
+            int32_t total = 0;
+            for (size_t i = g0; i < g1;) {
+                size_t j = i;
+                while (j < g1 && groups[j].ti == groups[i].ti) ++j;
+                total += span_len(groups[i].d0, groups[j - 1].d0);
+                i = j;
+            }
+            return total;
+        };
+        for (size_t i = 0; i < groups.size(); ++i) {
+            if (!segs.empty() && (int)(i - segs.back().g0) < 4 * kMfmaMaxChunks &&
+                seg_elems(segs.back().g0, i + 1) <= kMfmaMaxElems) {
+                segs.back().g1 = i + 1;
+            } else {
+                segs.push_back(Seg{i, i + 1});
+            }
+        }
+        if (segs.empty()) segs.push_back(Seg{0, 0});  // no entries: the ring's outputs are zero
+        const bool split = segs.size() > 1;
+        int32_t slot0 = -1;
+        if (split) {
+            slot0 = H.n_slots;
+            H.n_slots += (int32_t)segs.size() * P;
+            for (int r = 0; r < P; ++r) {
+                H.red_pattern.push_back(to * P + r);
+                for (size_t k = 0; k < segs.size(); ++k) H.red_slots.push_back(slot0 + (int32_t)k * P + r);
+                H.red_ptr.push_back((int32_t)H.red_slots.size());
+            }
+        }
+        // 4. Emit spans, chunk headers and the A operands.
+        for (size_t si = 0; si < segs.size(); ++si) {
+            const Seg& sg = segs[si];
+            MSeg M{};
+            M.ring = to;
+            M.span_begin = (int32_t)H.spans.size();
+            M.chunk_begin = (int32_t)H.chunks.size();
+            M.slot = split ? slot0 + (int32_t)si * P : -1;
+            std::vector<int32_t> grp_elem;
+            int32_t lds = 0;
+            for (size_t i = sg.g0; i < sg.g1;) {
+                size_t j = i;
+                while (j < sg.g1 && groups[j].ti == groups[i].ti) ++j;
+                const int32_t dstart = groups[i].d0 & ~7;
+                const int32_t len = span_len(groups[i].d0, groups[j - 1].d0);
+                H.spans.push_back(PSpan{groups[i].ti * N, dstart, len, lds});
+                for (size_t k = i; k < j; ++k) grp_elem.push_back(lds + groups[k].d0 - dstart);
+                lds += len;
+                i = j;
+            }
+            M.span_end = (int32_t)H.spans.size();
+            M.n_elems = lds;
+            const size_t ng = sg.g1 - sg.g0;
+            const size_t nch = (ng + 3) / 4;
+            for (size_t c = 0; c < nch; ++c) {
+                MChunkHdr hd{};
+                for (int gq = 0; gq < 4; ++gq) {
+                    const size_t gi = 4 * c + gq;
+                    hd.grp[gq] = gi < ng ? grp_elem[gi] : 0;  // padding group: any staged element, values zero
+                }
+                H.chunks.push_back(hd);
+                for (int r = 0; r < P; ++r)
+                    for (int lane = 0; lane < 64; ++lane) {
+                        const int row = lane % 16, gq = lane / 16;
+                        const size_t gi = 4 * c + gq;
+                        for (int u = 0; u < 8; ++u) {
+                            const float v = (gi < ng && row < kBasis) ? groups[sg.g0 + gi].v[r][row][u] : 0.0f;
+                            H.aop.push_back(bf16_rne(v));
+                        }
+                    }
+            }
+            M.chunk_end = (int32_t)H.chunks.size();
+            H.segs.push_back(M);
+        }
+    }
+    H.red_ptr.insert(H.red_ptr.begin(), 0);
+    // 5. Dispatch order.  Work of an item ~ its chunks plus a fixed share
+    // (staging and the contraction); contiguous runs of items cut at equal
+    // shares of the total, each run sorted heaviest first.
+    const int nqt = (g.nq + kMfmaTile - 1) / kMfmaTile;
+    H.n_qtiles = nqt;
+    std::vector<int64_t> cost;
+    for (const MSeg& S : H.segs)
+        for (int t = 0; t < nqt; ++t) cost.push_back(S.chunk_end - S.chunk_begin + 2);
+    int64_t total = 0;
+    for (int64_t c : cost) total += c;
+    std::vector<std::vector<int32_t>> runs(8);
+    int64_t acc = 0;
+    for (size_t i = 0; i < cost.size(); ++i) {
+        const int x = (int)std::min<int64_t>(7, (acc + cost[i] / 2) * 8 / std::max<int64_t>(total, 1));
+        runs[(size_t)x].push_back((int32_t)i);
+        acc += cost[i];
+    }
+    size_t longest = 0;
+    for (auto& r : runs) {
+        std::stable_sort(r.begin(), r.end(), [&](int32_t a, int32_t b) { return cost[(size_t)a] > cost[(size_t)b]; });
+        longest = std::max(longest, r.size());
+    }
+    H.order.assign(8 * longest, -1);
+    for (int x = 0; x < 8; ++x)
+        for (size_t j = 0; j < runs[(size_t)x].size(); ++j) H.order[8 * j + (size_t)x] = runs[(size_t)x][j];
     *out = std::move(H);
     return DISCO_OK;
 }

@@ -44,9 +44,10 @@ ALGO_GATHER_THEN_CONTRACT = 1
 ALGO_CONTRACT_THEN_GATHER = 2
 ALGO_FUSED = 3
 ALGO_FUSED_DIRECT = 4
+ALGO_MATRIX_CORE = 5
 ALGOS = {"auto": ALGO_AUTO, "gather_then_contract": ALGO_GATHER_THEN_CONTRACT,
          "contract_then_gather": ALGO_CONTRACT_THEN_GATHER, "fused": ALGO_FUSED,
-         "fused_direct": ALGO_FUSED_DIRECT}
+         "fused_direct": ALGO_FUSED_DIRECT, "matrix_core": ALGO_MATRIX_CORE}
 
 # Every exported symbol declared in include/disco.h.
 EXPORTS = ("disco_plan_create", "disco_plan_destroy", "disco_plan_query", "disco_forward",

@@ -8,7 +8,10 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstring>
+#include <map>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "disco.h"
@@ -23,6 +26,122 @@ int failures = 0;
 void check(int rc, const std::string& what, const std::string& err) {
     if (rc != DISCO_OK) {
         std::printf("FAIL %s: status %d (%s)\n", what.c_str(), rc, err.c_str());
+        ++failures;
+    }
+}
+
+uint16_t bf16_of(float f) {
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// The matrix-core layout holds every entry's nine values (rounded to bf16)
+// exactly once, at its (output ring, phase, input ring, offset), and nothing
+// else; every staged element a lane reads lies inside its segment.
+void check_mfma(const HostOp& op, const std::string& what) {
+    MfmaHost M;
+    std::string err;
+    const int rc = pack_mfma(op, &M, &err);
+    if (!mfma_supported(op.g, op.basis)) {
+        if (rc != DISCO_ERR_UNSUPPORTED) {
+            std::printf("FAIL %s: pack_mfma accepted an uncovered op\n", what.c_str());
+            ++failures;
+        }
+        return;
+    }
+    check(rc, what + " pack_mfma", err);
+    if (rc != DISCO_OK) return;
+    const OpGeom& g = op.g;
+    const int N = g.nlon_i, P = g.P;
+    std::map<std::tuple<int, int, int, int, int>, uint16_t> want, got;
+    for (int pat = 0; pat < g.n_patterns(); ++pat)
+        for (int32_t e = op.pat_ptr[(size_t)pat]; e < op.pat_ptr[(size_t)pat + 1]; ++e)
+            for (int k = 0; k < kBasis; ++k) {
+                const uint16_t v = bf16_of(op.val[(size_t)e * kBasis + k]);
+                if (v != 0) want[{pat / P, pat % P, op.t_in[(size_t)e], op.d[(size_t)e], k}] = v;
+            }
+    std::vector<int> ring_segs((size_t)g.nlat_o, 0);
+    for (const MSeg& S : M.segs) {
+        ring_segs[(size_t)S.ring]++;
+        if (S.chunk_end - S.chunk_begin > kMfmaMaxChunks || S.n_elems > kMfmaMaxElems ||
+            S.span_end - S.span_begin > 4 * kMfmaMaxChunks) {
+            std::printf("FAIL %s: segment over its budgets\n", what.c_str());
+            ++failures;
+            return;
+        }
+        for (int c = S.chunk_begin; c < S.chunk_end; ++c)
+            for (int gq = 0; gq < 4; ++gq) {
+                const int ge = M.chunks[(size_t)c].grp[gq];
+                // largest element a lane reads: ge + stride * (tile - 1) + 6
+                if (ge < 0 || ge + g.stride * (kMfmaTile - 1) + 6 >= S.n_elems) {
+                    std::printf("FAIL %s: group reads outside its segment\n", what.c_str());
+                    ++failures;
+                    return;
+                }
+                int sp = S.span_begin;
+                while (sp + 1 < S.span_end && M.spans[(size_t)sp + 1].lds_base <= ge) ++sp;
+                const PSpan& SP = M.spans[(size_t)sp];
+                if (SP.dstart % 8 != 0 || SP.len % 8 != 0 || ge + g.stride * (kMfmaTile - 1) + 6 >= SP.lds_base + SP.len) {
+                    std::printf("FAIL %s: span misaligned or too short\n", what.c_str());
+                    ++failures;
+                    return;
+                }
+                const int ti = SP.row / N, d0 = ge - SP.lds_base + SP.dstart;
+                for (int r = 0; r < P; ++r)
+                    for (int k = 0; k < 16; ++k)
+                        for (int u = 0; u < 8; ++u) {
+                            const size_t idx = (((size_t)c * P + r) * 64 + (size_t)(k + 16 * gq)) * 8 + (size_t)u;
+                            const uint16_t v = M.aop[idx];
+                            if (v == 0) continue;
+                            if (k >= kBasis) {
+                                std::printf("FAIL %s: value in a padding row\n", what.c_str());
+                                ++failures;
+                                return;
+                            }
+                            auto key = std::make_tuple(S.ring, r, ti, (d0 + u) % N, k);
+                            if (got.count(key)) {
+                                std::printf("FAIL %s: value stored twice\n", what.c_str());
+                                ++failures;
+                                return;
+                            }
+                            got[key] = v;
+                        }
+            }
+    }
+    // The dispatch order lists every (segment, longitude tile) exactly once.
+    const size_t n_items = M.segs.size() * (size_t)M.n_qtiles;
+    std::vector<int> seen(n_items, 0);
+    if (M.order.size() % 8 != 0 || M.n_qtiles != (g.nq + kMfmaTile - 1) / kMfmaTile) {
+        std::printf("FAIL %s: dispatch order shape\n", what.c_str());
+        ++failures;
+        return;
+    }
+    for (int32_t it : M.order)
+        if (it >= 0) {
+            if ((size_t)it >= n_items || seen[(size_t)it]++) {
+                std::printf("FAIL %s: dispatch order repeats or overruns an item\n", what.c_str());
+                ++failures;
+                return;
+            }
+        }
+    for (int v : seen)
+        if (v != 1) {
+            std::printf("FAIL %s: dispatch order misses an item\n", what.c_str());
+            ++failures;
+            return;
+        }
+    for (int t = 0; t < g.nlat_o; ++t)
+        if (ring_segs[(size_t)t] == 0) {
+            std::printf("FAIL %s: output ring %d has no segment\n", what.c_str(), t);
+            ++failures;
+            return;
+        }
+    if (got != want) {
+        std::printf("FAIL %s: matrix-core values differ from the entries (%zu against %zu)\n", what.c_str(),
+                    got.size(), want.size());
         ++failures;
     }
 }
@@ -60,6 +179,7 @@ void run_op(const PlanParams& p, bool transpose, bool quad_at_output, const char
         }
     }
     if (op.basis != DISCO_BASIS_BILINEAR_3X3) return;
+    check_mfma(op, what);
     SpectralHost sp;
     std::vector<uint8_t> heavy;
     check(build_spectral(op, 128, &sp, &heavy, &err), what + " build_spectral", err);

@@ -22,6 +22,8 @@ hipError_t launch_weight_grad_dw(const void*, const void*, void*, float*, int, i
     return hipErrorNotSupported;
 }
 size_t workspace_bytes_fused(const ExecArgs&, const PackedDev&) { return 0; }
+size_t workspace_bytes_mfma(const ExecArgs&) { return 0; }
+hipError_t launch_mfma(const ExecArgs&, void*) { return hipErrorNotSupported; }
 size_t workspace_bytes_sweep(const ExecArgs&) { return 0; }
 hipError_t launch_stencil_blocked(const ExecArgs&, const StencilDev&, float*) { return hipErrorNotSupported; }
 size_t weight_grad_ws_bytes_dw(int, int, int, int64_t) { return 0; }
