@@ -120,12 +120,20 @@ typedef struct {
     int32_t quadrature;  /* DISCO_QUAD_SAMPLING_THEOREM (default) or DISCO_QUAD_CELL_AREA */
     double node_spacing; /* h in radians; 0 selects theta_c / 3 (3x3) or theta_c / 4 (the others) */
     int32_t sampling;    /* DISCO_SAMPLING_CELL_CENTRED (default) or DISCO_SAMPLING_POLES */
-    int32_t flags;       /* 0 or DISCO_PLAN_BACKWARD */
+    int32_t flags;       /* 0, DISCO_PLAN_BACKWARD, DISCO_PLAN_EAGER or both */
 } disco_basis_t;
 
-/* Plan flag: also build the adjoint ops that disco_forward_backward and
- * disco_transpose_backward need (about twice the plan's device memory). */
-enum { DISCO_PLAN_BACKWARD = 1 };
+/* Plan flags.  DISCO_PLAN_BACKWARD: also prepare the adjoint ops that
+ * disco_forward_backward and disco_transpose_backward need.
+ * Layouts: plan creation packs every layout of every op on the host but puts
+ * on the device only what disco_forward with DISCO_ALGO_AUTO runs on; the
+ * first call that runs on another layout (the transposed op, the adjoints,
+ * another algo, depthwise calls of the 3x3 basis) uploads it, with
+ * synchronous copies, once per plan.  DISCO_PLAN_EAGER uploads everything
+ * at creation (for callers that capture graphs or must not see the first
+ * call's upload); the bf16 matrix-core tables are built by the first bf16
+ * call in either case. */
+enum { DISCO_PLAN_BACKWARD = 1, DISCO_PLAN_EAGER = 2 };
 
 typedef struct {
     void* data;       /* device pointer (may be NULL only when the tensor is empty) */
@@ -144,7 +152,7 @@ typedef struct {
     int64_t nnz_entries;       /* stored (pattern, input pixel) entries, forward op */
     int64_t nnz_entries_transpose;
     int64_t nnz_pairs_total;   /* non-zero (output pixel, input pixel, k) triples, forward */
-    int64_t psi_bytes;         /* device bytes held by the plan */
+    int64_t psi_bytes;         /* device bytes the plan holds now (see DISCO_PLAN_EAGER) */
     double h;                  /* node spacing actually used */
     int32_t spectral_rings_forward;   /* output rings of the forward op on the spectral path */
     int32_t spectral_rings_transpose; /* ... of the transposed op */
@@ -167,6 +175,9 @@ typedef struct {
     int64_t bytes_spectral;    /* the polar rings' frequency-domain psi rows and twiddles */
     int64_t bytes_sweep;       /* the ring sweep's runs, spans and entries */
     int64_t bytes_stencil;     /* the folded-weight stencil layouts */
+    int64_t bytes_matrix_core; /* the bf16 matrix-core tables (built by the first bf16 call) */
+    int64_t psi_bytes_all_layouts; /* device bytes once every layout of every op is built
+                                      (matrix-core tables excluded) */
 } disco_plan_info_t;
 
 /* Builds the sparse psi tensors of the forward and transposed ops on the host

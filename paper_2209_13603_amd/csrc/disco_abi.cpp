@@ -30,7 +30,7 @@ struct disco_plan {
     void* wsel32 = nullptr;
     void* wsel16 = nullptr;
     hipStream_t aux = nullptr;  // runs the spectral rings beside the direct kernels
-    std::mutex lazy_mu;         // tables built on first use (the bf16 matrix-core layout)
+    std::mutex lazy_mu;         // serialises the uploads of layouts on first use
 };
 
 namespace {
@@ -67,7 +67,8 @@ disco_status_t resolve_params(int nlat_in, int nlon_in, int nlat_out, int nlon_o
         return fail(DISCO_ERR_INVALID_ARGUMENT, "theta_c must lie in (0, pi]");
     disco_basis_t b{DISCO_BASIS_BILINEAR_3X3, DISCO_QUAD_SAMPLING_THEOREM, 0.0, DISCO_SAMPLING_CELL_CENTRED, 0};
     if (basis) b = *basis;
-    if ((b.flags & ~DISCO_PLAN_BACKWARD) != 0) return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown basis.flags bits");
+    if ((b.flags & ~(DISCO_PLAN_BACKWARD | DISCO_PLAN_EAGER)) != 0)
+        return fail(DISCO_ERR_INVALID_ARGUMENT, "unknown basis.flags bits");
     if (b.kind != DISCO_BASIS_BILINEAR_3X3 && b.kind != DISCO_BASIS_AXISYMMETRIC_4 &&
         b.kind != DISCO_BASIS_SEPARABLE_4X4)
         return fail(DISCO_ERR_UNSUPPORTED, "unknown basis kind");
@@ -162,16 +163,19 @@ void free_spectral(SpectralDev* d) {
     *d = SpectralDev{};
 }
 
-disco_status_t upload_packed(const HostOp& h, const std::vector<uint8_t>& skip, PackedDev* d) {
-    PackedHost P;
+disco_status_t pack_general(const HostOp& h, const std::vector<uint8_t>& skip, PackedHost* P) {
     std::string err;
     // A 64-lane tile when a pattern has at most 64 output longitudes, so
     // that the lanes of a 256-lane tile do not idle (measured on 32 x 64);
     // 256 otherwise (on 128 x 256 -> 64 x 128, whose patterns have 128, the
     // 128-lane tile was slower: 104 against 71 us, fewer waves in flight).
     const int tile = h.g.nq <= 64 ? 64 : kTileQ;
-    int rc = pack_op(h, fused_target_entries(h, tile), skip, &P, &err, tile);
+    int rc = pack_op(h, fused_target_entries(h, tile), skip, P, &err, tile);
     if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
+    return DISCO_OK;
+}
+
+disco_status_t upload_packed(const PackedHost& P, PackedDev* d) {
     disco_status_t s;
     if ((s = upload_vec(P.spans, &d->spans, &d->bytes, "hipMalloc(spans)")) != DISCO_OK) return s;
     if ((s = upload_vec(P.chunks, &d->chunks, &d->bytes, "hipMalloc(chunks)")) != DISCO_OK) return s;
@@ -193,6 +197,16 @@ disco_status_t upload_packed(const HostOp& h, const std::vector<uint8_t>& skip, 
     d->n_slots = P.n_slots;
     d->tile = P.tile;
     return DISCO_OK;
+}
+
+// Device bytes upload_packed would allocate (each table at least one element).
+template <typename V>
+int64_t vec_bytes(const std::vector<V>& v) { return (int64_t)(sizeof(V) * std::max<size_t>(v.size(), 1)); }
+int64_t packed_bytes(const PackedHost& P) {
+    const int64_t ne = (int64_t)std::max<size_t>(P.entries.size(), 1);
+    return vec_bytes(P.spans) + vec_bytes(P.chunks) + ne * (int64_t)(sizeof(int32_t) + sizeof(PVal)) +
+           vec_bytes(P.segs) + vec_bytes(P.items) + vec_bytes(P.red_pattern) + vec_bytes(P.red_ptr) +
+           vec_bytes(P.red_slots);
 }
 
 // Cost of one sweep run (entries plus fixed per-pattern work).
@@ -228,7 +242,7 @@ void free_sweep(SweepDev* d) {
     *d = SweepDev{};
 }
 
-disco_status_t upload_stencil(const HostOp& h, StencilDev* d) {
+disco_status_t pack_stencil_host(const HostOp& h, StencilHost* H) {
     // Entries per work item: enough workgroups (items x longitude tiles) to
     // fill the chip several times over, within [128, 1024].
     // The tile: 512 output longitudes when a pattern has no more (two-phase
@@ -236,10 +250,13 @@ disco_status_t upload_stencil(const HostOp& h, StencilDev* d) {
     const int tile = h.g.nq <= kStencilSmallTile ? kStencilSmallTile : kStencilTile;
     const int64_t n_qt = (h.g.nq + tile - 1) / tile;
     const int target = (int)std::min<int64_t>(1024, std::max<int64_t>(128, (int64_t)h.t_in.size() * n_qt / 4096));
-    StencilHost H;
     std::string err;
-    int rc = pack_stencil(h, target, tile, &H, &err);
+    int rc = pack_stencil(h, target, tile, H, &err);
     if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
+    return DISCO_OK;
+}
+
+disco_status_t upload_stencil(const StencilHost& H, StencilDev* d) {
     disco_status_t s;
     if ((s = upload_vec(H.pieces, &d->pieces, &d->bytes, "hipMalloc(stencil pieces)")) != DISCO_OK) return s;
     if ((s = upload_vec(H.chunks, &d->chunks, &d->bytes, "hipMalloc(stencil chunks)")) != DISCO_OK) return s;
@@ -257,6 +274,11 @@ disco_status_t upload_stencil(const HostOp& h, StencilDev* d) {
     d->tile = H.tile;
     d->n_padded = (int64_t)H.vals.size();
     return DISCO_OK;
+}
+
+int64_t stencil_bytes(const StencilHost& H) {
+    return vec_bytes(H.pieces) + vec_bytes(H.chunks) + vec_bytes(H.vals) + vec_bytes(H.cells) + vec_bytes(H.segs) +
+           vec_bytes(H.items) + vec_bytes(H.red_pattern) + vec_bytes(H.red_ptr) + vec_bytes(H.red_slots);
 }
 
 disco_status_t upload_mfma(const MfmaHost& H, MfmaDev* d) {
@@ -293,70 +315,93 @@ void free_packed(PackedDev* d) {
     *d = PackedDev{};
 }
 
-disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
+}  // namespace
+
+namespace disco {
+
+// Host tables of one op's layout groups (see kPart*), packed at plan
+// creation and uploaded on first use.
+struct OpTables {
+    // kPartEntries: the plain entry tables.
+    std::vector<int32_t> pat_ptr;
+    std::vector<DevEntry> ent;
+    // kPartDirect: the general kernel over every pattern.
+    PackedHost packed;
+    // kPartStencil (longitude stride 1): the blocked stencil layout.
+    bool has_stencil = false;
+    StencilHost stencil;
+    // kPartCore (3x3 basis): spectral rings, their flags, the general kernel
+    // for the light rings, the sweep and the general kernel for the rest.
+    SpectralHost sp;
+    std::vector<uint8_t> spectral_flag;
+    bool has_light = false, has_sweep = false;
+    PackedHost light, rest;
+    SweepHost sw;
+    std::vector<int32_t> rest_pats;
+    int64_t bytes[4] = {0, 0, 0, 0};  // device bytes of each group (core, direct, entries, stencil)
+};
+
+}  // namespace disco
+
+namespace {
+
+int part_index(int part) { return part == kPartCore ? 0 : part == kPartDirect ? 1 : part == kPartEntries ? 2 : 3; }
+
+// Host side of one op: every group's tables packed, the op's metadata and
+// work figures set, the cell map uploaded (64 bytes).  Nothing else on the
+// device yet.
+disco_status_t prepare_op(const HostOp& h, DeviceOp* d) {
+    if (fault_inject_alloc()) return fail(DISCO_ERR_OUT_OF_MEMORY, "allocation failure injected (DISCO_FAULT_INJECT=alloc)");
     d->g = h.g;
+    d->basis = h.basis;
     d->n_entries = (int64_t)h.t_in.size();
     d->nnz_pairs = h.nnz_pairs;
-    std::vector<DevEntry> ent((size_t)d->n_entries);
+    d->work_all = pattern_work(h, {});
+    auto T = std::make_shared<OpTables>();
+    T->pat_ptr = h.pat_ptr;
+    T->ent.resize((size_t)d->n_entries);
     for (int64_t e = 0; e < d->n_entries; ++e) {
-        DevEntry& E = ent[(size_t)e];
+        DevEntry& E = T->ent[(size_t)e];
         E.row = h.t_in[(size_t)e] * h.g.nlon_i;
         E.d = h.d[(size_t)e];
         for (int k = 0; k < kBasis; ++k) E.v[k] = h.val[(size_t)e * kBasis + k];
         E.pad = 0;
     }
-    const size_t pb = sizeof(int32_t) * h.pat_ptr.size();
-    const size_t eb = sizeof(DevEntry) * std::max<size_t>(ent.size(), 1);
-    if (fault_inject_alloc()) return fail(DISCO_ERR_OUT_OF_MEMORY, "allocation failure injected (DISCO_FAULT_INJECT=alloc)");
-    hipError_t e = hipMalloc((void**)&d->pat_ptr, pb);
-    if (e != hipSuccess) { d->pat_ptr = nullptr; return hip_fail(e, "hipMalloc(pattern table)"); }
-    e = hipMalloc((void**)&d->entries, eb);
-    if (e != hipSuccess) { d->entries = nullptr; return hip_fail(e, "hipMalloc(psi entries)"); }
-    e = hipMemcpy(d->pat_ptr, h.pat_ptr.data(), pb, hipMemcpyHostToDevice);
-    if (e != hipSuccess) return hip_fail(e, "hipMemcpy(pattern table)");
-    if (!ent.empty()) {
-        e = hipMemcpy(d->entries, ent.data(), sizeof(DevEntry) * ent.size(), hipMemcpyHostToDevice);
-        if (e != hipSuccess) return hip_fail(e, "hipMemcpy(psi entries)");
-    }
-    d->bytes = (int64_t)(pb + eb);
-    d->bytes_entries = d->bytes;
-    d->work_all = pattern_work(h, {});
-    d->basis = h.basis;
-    const CellMap cm = cell_map(h.basis);
-    std::vector<int8_t> cmv(&cm.k[0][0], &cm.k[0][0] + sizeof(cm.k));
-    disco_status_t s = upload_vec(cmv, &d->cmap_dev, &d->bytes, "hipMalloc(cell map)");
-    if (s != DISCO_OK) return s;
-    s = upload_packed(h, {}, &d->packed);
-    if (s != DISCO_OK) return s;
-    d->bytes += d->packed.bytes;
+    T->bytes[2] = vec_bytes(T->pat_ptr) + vec_bytes(T->ent);
+    disco_status_t s;
+    if ((s = pack_general(h, {}, &T->packed)) != DISCO_OK) return s;
+    T->bytes[1] = packed_bytes(T->packed);
     // Every basis has the folded-weight stencil kernels (all calls of the
     // axisymmetric and separable bases, depthwise calls of any basis): the
     // general one on the packed layout, the blocked one when the longitude
     // stride is 1.  The spectral and sweep layouts are built for the 3x3 basis.
     if (h.g.stride == 1) {
-        if ((s = upload_stencil(h, &d->stencil)) != DISCO_OK) return s;
-        d->bytes += d->stencil.bytes;
+        if ((s = pack_stencil_host(h, &T->stencil)) != DISCO_OK) return s;
+        T->has_stencil = true;
+        T->bytes[3] = stencil_bytes(T->stencil);
     }
+    const CellMap cm = cell_map(h.basis);
+    std::vector<int8_t> cmv(&cm.k[0][0], &cm.k[0][0] + sizeof(cm.k));
+    if ((s = upload_vec(cmv, &d->cmap_dev, &d->bytes, "hipMalloc(cell map)")) != DISCO_OK) return s;
     if (h.basis != DISCO_BASIS_BILINEAR_3X3) {
         d->work_light = d->work_all;
+        d->tables = T;
+        d->built.store(kPartCore);  // nothing in the group for these bases
         return DISCO_OK;
     }
-    SpectralHost sp;
     std::vector<uint8_t> heavy;
     std::string err;
-    int rc = build_spectral(h, spectral_min_entries(), &sp, &heavy, &err);
+    int rc = build_spectral(h, spectral_min_entries(), &T->sp, &heavy, &err);
     if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
-    if (!sp.rings.empty()) {
-        if ((s = upload_spectral(sp, &d->spectral)) != DISCO_OK) return s;
-        std::vector<uint8_t> flag((size_t)h.g.nlat_o, 0);
-        for (int32_t r : sp.rings) flag[(size_t)r] = 1;
-        e = hipMalloc((void**)&d->spectral_ring, flag.size());
-        if (e != hipSuccess) { d->spectral_ring = nullptr; return hip_fail(e, "hipMalloc(spectral ring flags)"); }
-        e = hipMemcpy(d->spectral_ring, flag.data(), flag.size(), hipMemcpyHostToDevice);
-        if (e != hipSuccess) return hip_fail(e, "hipMemcpy(spectral ring flags)");
-        d->bytes += (int64_t)flag.size();
-        if ((s = upload_packed(h, heavy, &d->packed_light)) != DISCO_OK) return s;
-        d->bytes += d->spectral.bytes + d->packed_light.bytes;
+    int64_t core = 0;
+    if (!T->sp.rings.empty()) {
+        T->spectral_flag.assign((size_t)h.g.nlat_o, 0);
+        for (int32_t r : T->sp.rings) T->spectral_flag[(size_t)r] = 1;
+        if ((s = pack_general(h, heavy, &T->light)) != DISCO_OK) return s;
+        T->has_light = true;
+        core += vec_bytes(T->sp.rings) + vec_bytes(T->sp.pair_ptr) + vec_bytes(T->sp.pair_slot) +
+                vec_bytes(T->sp.slot_ring) + vec_bytes(T->sp.vs) + vec_bytes(T->sp.tw) + h.g.nlat_o +
+                packed_bytes(T->light);
         std::vector<uint8_t> light(heavy.size());
         for (size_t i = 0; i < heavy.size(); ++i) light[i] = !heavy[i];
         d->work_spectral = pattern_work(h, heavy);
@@ -365,30 +410,76 @@ disco_status_t upload_op(const HostOp& h, DeviceOp* d) {
         d->work_light = d->work_all;
     }
     // Sweep runs over the light patterns; the rest go to the general kernel.
-    SweepHost sw;
-    rc = pack_sweep(h, kSweepTarget, heavy, &sw, &err);
+    rc = pack_sweep(h, kSweepTarget, heavy, &T->sw, &err);
     if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
-    if (!sw.runs.empty()) {
-        std::vector<uint8_t> rest_skip(sw.covered);
+    if (!T->sw.runs.empty()) {
+        std::vector<uint8_t> rest_skip(T->sw.covered);
         for (size_t i = 0; i < rest_skip.size() && i < heavy.size(); ++i) rest_skip[i] |= heavy[i];
-        if ((s = upload_sweep(sw, &d->sweep)) != DISCO_OK) return s;
-        if ((s = upload_packed(h, rest_skip, &d->packed_rest)) != DISCO_OK) return s;
-        d->bytes += d->sweep.bytes + d->packed_rest.bytes;
+        if ((s = pack_general(h, rest_skip, &T->rest)) != DISCO_OK) return s;
+        T->has_sweep = true;
         for (size_t i = 0; i < rest_skip.size(); ++i) rest_skip[i] = !rest_skip[i];
-        d->work_sweep = pattern_work(h, sw.covered);
+        d->work_sweep = pattern_work(h, T->sw.covered);
         d->work_rest = pattern_work(h, rest_skip);
-        std::vector<int32_t> rest;
         for (size_t i = 0; i < rest_skip.size(); ++i)
-            if (rest_skip[i]) rest.push_back((int32_t)i);
-        if (!rest.empty()) {
-            e = hipMalloc((void**)&d->rest_pats, sizeof(int32_t) * rest.size());
-            if (e != hipSuccess) { d->rest_pats = nullptr; return hip_fail(e, "hipMalloc(rest patterns)"); }
-            e = hipMemcpy(d->rest_pats, rest.data(), sizeof(int32_t) * rest.size(), hipMemcpyHostToDevice);
-            if (e != hipSuccess) return hip_fail(e, "hipMemcpy(rest patterns)");
-            d->n_rest_pats = (int32_t)rest.size();
-            d->bytes += (int64_t)(sizeof(int32_t) * rest.size());
-        }
+            if (rest_skip[i]) T->rest_pats.push_back((int32_t)i);
+        int64_t cov = 0;
+        for (uint8_t c : T->sw.covered) cov += c;
+        const int64_t ne = (int64_t)std::max<size_t>(T->sw.entries.size(), 1);
+        core += vec_bytes(T->sw.runs) + vec_bytes(T->sw.pats) + vec_bytes(T->sw.acts) +
+                ne * (int64_t)(sizeof(int32_t) + sizeof(PVal)) + (int64_t)sizeof(int32_t) * std::max<int64_t>(cov, 1) +
+                packed_bytes(T->rest) + (T->rest_pats.empty() ? 0 : vec_bytes(T->rest_pats));
     }
+    T->bytes[0] = core;
+    d->tables = T;
+    return DISCO_OK;
+}
+
+// Uploads the groups in `parts` that are not on the device yet (the caller
+// holds the plan's lock, with the plan's device current).
+disco_status_t upload_parts(DeviceOp* d, int parts) {
+    const int todo = parts & ~d->built;
+    if (!todo) return DISCO_OK;
+    if (fault_inject_alloc()) return fail(DISCO_ERR_OUT_OF_MEMORY, "allocation failure injected (DISCO_FAULT_INJECT=alloc)");
+    const OpTables* T = d->tables.get();
+    if (!T) return fail(DISCO_ERR_DEVICE, "internal: layout tables released before upload");
+    disco_status_t s;
+    if (todo & kPartEntries) {
+        if ((s = upload_vec(T->pat_ptr, &d->pat_ptr, &d->bytes_entries, "hipMalloc(pattern table)")) != DISCO_OK) return s;
+        if ((s = upload_vec(T->ent, &d->entries, &d->bytes_entries, "hipMalloc(psi entries)")) != DISCO_OK) return s;
+        d->built.fetch_or(kPartEntries);
+    }
+    if (todo & kPartDirect) {
+        if ((s = upload_packed(T->packed, &d->packed)) != DISCO_OK) return s;
+        d->built.fetch_or(kPartDirect);
+    }
+    if (todo & kPartStencil) {
+        if (T->has_stencil && (s = upload_stencil(T->stencil, &d->stencil)) != DISCO_OK) return s;
+        d->built.fetch_or(kPartStencil);
+    }
+    if (todo & kPartCore) {
+        if (!T->sp.rings.empty()) {
+            if ((s = upload_spectral(T->sp, &d->spectral)) != DISCO_OK) return s;
+            int64_t b = 0;
+            if ((s = upload_vec(T->spectral_flag, &d->spectral_ring, &b, "hipMalloc(spectral ring flags)")) != DISCO_OK)
+                return s;
+            d->spectral.bytes += b;
+        }
+        if (T->has_light && (s = upload_packed(T->light, &d->packed_light)) != DISCO_OK) return s;
+        if (T->has_sweep) {
+            if ((s = upload_sweep(T->sw, &d->sweep)) != DISCO_OK) return s;
+            if ((s = upload_packed(T->rest, &d->packed_rest)) != DISCO_OK) return s;
+            if (!T->rest_pats.empty()) {
+                int64_t b = 0;
+                if ((s = upload_vec(T->rest_pats, &d->rest_pats, &b, "hipMalloc(rest patterns)")) != DISCO_OK) return s;
+                d->packed_rest.bytes += b;
+                d->n_rest_pats = (int32_t)T->rest_pats.size();
+            }
+        }
+        d->built.fetch_or(kPartCore);
+    }
+    d->bytes = d->bytes_entries + d->packed.bytes + d->stencil.bytes + d->spectral.bytes + d->packed_light.bytes +
+               d->sweep.bytes + d->packed_rest.bytes + 64;
+    if (d->built == kPartAll) d->tables.reset();
     return DISCO_OK;
 }
 
@@ -416,6 +507,9 @@ void free_op(DeviceOp* d) {
         if (p) (void)hipFree(p);
     free_packed(&d->stencil.P);
     d->stencil = StencilDev{};
+    d->built.store(0);
+    d->bytes = d->bytes_entries = 0;
+    d->tables.reset();
 }
 
 int64_t numel(const disco_tensor_t* t) {
@@ -457,16 +551,21 @@ struct Dispatch {
     const Work* packed_work;
 };
 
+// The small-op rule of AUTO: below 2^18 output pixel-channels one launch of
+// the general kernel over every ring (launch latency dominates), else the
+// fused schedule.
+int32_t resolve_auto(const DeviceOp& op, int32_t algo, int64_t Co) {
+    if (algo != DISCO_ALGO_AUTO) return algo;
+    const double out_pix_chan = (double)Co * op.g.nlat_o * op.g.nlon_o;
+    return out_pix_chan < (double)(1 << 18) ? DISCO_ALGO_FUSED_DIRECT : DISCO_ALGO_FUSED;
+}
+
 Dispatch dispatch(const DeviceOp& op, int32_t algo, int Ci, int Co, int32_t dtype) {
     const OpGeom& g = op.g;
-    if (algo == DISCO_ALGO_AUTO) {
-        // Small ops are bound by launch latency: one direct fused kernel.
-        // Otherwise the fused schedule (spectral polar rings, ring sweep,
-        // general kernel for the rest).
-        const double out_pix_chan = (double)Co * g.nlat_o * g.nlon_o;
-        algo = out_pix_chan < (double)(1 << 18) ? DISCO_ALGO_FUSED_DIRECT : DISCO_ALGO_FUSED;
-        (void)Ci;
-    }
+    // Small ops are bound by launch latency: one direct fused kernel.
+    // Otherwise the fused schedule (spectral polar rings, ring sweep, general
+    // kernel for the rest).
+    algo = resolve_auto(op, algo, Co);
     Dispatch d{algo, false, false, &op.packed, &op.work_all};
     if (op.basis != DISCO_BASIS_BILINEAR_3X3) return d;
     d.spectral = algo == DISCO_ALGO_FUSED && op.spectral.n_rings > 0;
@@ -638,6 +737,32 @@ disco_status_t ensure_mfma(disco_plan_t plan, const DeviceOp& cop) {
     return DISCO_OK;
 }
 
+// Uploads the op's layout groups in `parts` that are not on the device yet
+// (host tables packed at plan creation; synchronous copies).
+disco_status_t ensure_parts(disco_plan_t plan, const DeviceOp& cop, int parts) {
+    DeviceOp& op = const_cast<DeviceOp&>(cop);
+    std::lock_guard<std::mutex> lock(plan->lazy_mu);
+    if (!(parts & ~op.built)) return DISCO_OK;
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return fail(DISCO_ERR_DEVICE, "hipGetDevice failed");
+    if (cur != plan->device && hipSetDevice(plan->device) != hipSuccess)
+        return fail(DISCO_ERR_DEVICE, "hipSetDevice failed");
+    const disco_status_t s = upload_parts(&op, parts);
+    if (cur != plan->device) (void)hipSetDevice(cur);
+    return s;
+}
+
+// Layout groups a call runs on (3x3 basis unless `folded`).
+int needed_parts(const DeviceOp& op, int32_t algo, bool folded) {
+    if (folded) return kPartDirect | (op.g.stride == 1 ? kPartStencil : 0);
+    switch (algo) {
+        case DISCO_ALGO_GATHER_THEN_CONTRACT: return kPartEntries | kPartCore;
+        case DISCO_ALGO_CONTRACT_THEN_GATHER: return kPartEntries;
+        case DISCO_ALGO_FUSED_DIRECT: return kPartDirect;
+        default: return kPartCore;
+    }
+}
+
 disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, const disco_tensor_t* x,
                       const disco_tensor_t* w, disco_tensor_t* y, hipStream_t stream, int32_t algo,
                       bool depthwise, const ExtScratch* ext) {
@@ -674,8 +799,28 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
                                            "longitude phases, stride <= 4, nlon_in a multiple of 8 and aligned x "
                                            "(16 bytes) and y (4 bytes)");
     if (mfma) algo = DISCO_ALGO_MATRIX_CORE;
+    if (!mfma) {
+        algo = resolve_auto(op, algo, Co);
+        const int parts = needed_parts(op, algo, axisym);
+        if (parts & ~op.built) {
+            if (ext)
+                return fail(DISCO_ERR_UNSUPPORTED, "the tables this call runs on are not on the device yet and the "
+                                                   "non-allocating entry point does not build them: make one "
+                                                   "ordinary call with the same shapes first");
+            if ((s = ensure_parts(plan, op, parts)) != DISCO_OK) return s;
+        }
+    }
     const Dispatch dp = dispatch(op, mfma ? DISCO_ALGO_FUSED_DIRECT : algo, (int)Ci, (int)Co, x->dtype);
     if (!mfma) algo = dp.algo;
+    // The fused schedule of an op with neither spectral rings nor a sweep for
+    // these channels runs the general kernel over every ring.
+    if (!mfma && !axisym && dp.packed == &op.packed && !(op.built & kPartDirect)) {
+        if (ext)
+            return fail(DISCO_ERR_UNSUPPORTED, "the tables this call runs on are not on the device yet and the "
+                                               "non-allocating entry point does not build them: make one ordinary "
+                                               "call with the same shapes first");
+        if ((s = ensure_parts(plan, op, kPartDirect)) != DISCO_OK) return s;
+    }
     const bool spectral = dp.spectral, sweep = dp.sweep;
     const PackedDev& packed = axisym ? op.packed : *dp.packed;
     // One output channel on a stride-1 op takes the blocked stencil kernel.
@@ -867,6 +1012,7 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
     // spectral rings through a selection W); otherwise the op's own kernels
     // once per input channel (items of B * C_x).
     const bool onepass = x->dtype == DISCO_FLOAT32 && op.basis == DISCO_BASIS_BILINEAR_3X3;
+    if (onepass && (s = ensure_parts(plan, op, kPartCore | kPartEntries)) != DISCO_OK) return s;
     ExecArgs za{};
     za.op = &op; za.x = x->data; za.dtype = 0; za.B = (int)B; za.Ci = (int)C_x; za.Co = (int)C_x * K;
     za.w_trans = transpose; za.stream = stream;
@@ -1016,10 +1162,35 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
     plan->params = p;
     plan->tr.src_transpose = plan->fwd_adj.src_transpose = true;
     plan->fwd_adj.src_adjoint = plan->tr_adj.src_adjoint = true;
-    s = upload_op(hf, &plan->fwd);
-    if (s == DISCO_OK) s = upload_op(ht, &plan->tr);
-    if (s == DISCO_OK && with_backward) s = upload_op(hfa, &plan->fwd_adj);
-    if (s == DISCO_OK && with_backward) s = upload_op(hta, &plan->tr_adj);
+    try {
+        s = prepare_op(hf, &plan->fwd);
+        if (s == DISCO_OK) s = prepare_op(ht, &plan->tr);
+        if (s == DISCO_OK && with_backward) s = prepare_op(hfa, &plan->fwd_adj);
+        if (s == DISCO_OK && with_backward) s = prepare_op(hta, &plan->tr_adj);
+    } catch (const std::bad_alloc&) {
+        s = fail(DISCO_ERR_OUT_OF_MEMORY, "host allocation failed while packing psi");
+    }
+    // On the device now: what a forward call with AUTO runs on (the fused
+    // schedule's groups; the general kernel over every ring as well when some
+    // channel count makes the op small; the folded-weight layouts for the
+    // other bases), or every group with DISCO_PLAN_EAGER.  The rest is
+    // uploaded by the first call that runs on it.
+    const bool eager = (p.flags & DISCO_PLAN_EAGER) != 0;
+    auto eager_parts = [&](const DeviceOp& d) {
+        if (eager) return (int)kPartAll;
+        if (&d != &plan->fwd) return 0;
+        // The general kernel over every ring as well: for small grids (AUTO
+        // takes it below 2^18 output pixel-channels) and for ops whose fused
+        // schedule has no spectral rings and, for some channel counts, no
+        // sweep (two longitude phases and more than 8 input channels).
+        const bool small = (double)d.g.nlat_o * d.g.nlon_o < (double)(1 << 18);
+        const OpTables* T = d.tables.get();
+        const bool bare = T && T->sp.rings.empty() && (!T->has_sweep || d.g.P > 1);
+        return d.basis != DISCO_BASIS_BILINEAR_3X3 ? needed_parts(d, DISCO_ALGO_AUTO, true)
+                                                   : (kPartCore | (small || bare ? kPartDirect : 0));
+    };
+    for (DeviceOp* d : {&plan->fwd, &plan->tr, &plan->fwd_adj, &plan->tr_adj})
+        if (s == DISCO_OK && d->tables) s = upload_parts(d, eager_parts(*d));
     if (s == DISCO_OK && with_backward) {
         const int K = basis_size(p.basis);
         std::vector<float> id32((size_t)K * K, 0.0f);
@@ -1042,10 +1213,10 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
         delete plan;
         return s;
     }
-    if (plan->fwd.spectral.n_rings > 0 || plan->tr.spectral.n_rings > 0 || plan->fwd_adj.spectral.n_rings > 0 ||
-        plan->tr_adj.spectral.n_rings > 0) {
-        if (hipStreamCreateWithFlags(&plan->aux, hipStreamNonBlocking) != hipSuccess) plan->aux = nullptr;
-    }
+    bool any_spectral = false;
+    for (const DeviceOp* d : {&plan->fwd, &plan->tr, &plan->fwd_adj, &plan->tr_adj})
+        any_spectral |= d->spectral.n_rings > 0 || (d->tables && !d->tables->sp.rings.empty());
+    if (any_spectral && hipStreamCreateWithFlags(&plan->aux, hipStreamNonBlocking) != hipSuccess) plan->aux = nullptr;
     // Keep freed workspace in the device's pool rather than returning it to
     // the driver at every synchronisation.
     hipMemPool_t pool;
@@ -1064,24 +1235,24 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
     I.nnz_entries = (int64_t)hf.t_in.size();
     I.nnz_entries_transpose = (int64_t)ht.t_in.size();
     I.nnz_pairs_total = hf.nnz_pairs;
-    I.psi_bytes = plan->fwd.bytes + plan->tr.bytes + plan->fwd_adj.bytes + plan->tr_adj.bytes;
     I.h = p.h;
-    I.spectral_rings_forward = plan->fwd.spectral.n_rings;
-    I.spectral_rings_transpose = plan->tr.spectral.n_rings;
-    I.sweep_patterns_forward = plan->fwd.sweep.n_pats;
-    I.sweep_patterns_transpose = plan->tr.sweep.n_pats;
-    I.spectral_pairs_forward = plan->fwd.spectral.n_pairs;
-    I.spectral_pairs_transpose = plan->tr.spectral.n_pairs;
-    I.spectral_slots_forward = plan->fwd.spectral.n_slots;
-    I.spectral_slots_transpose = plan->tr.spectral.n_slots;
+    // Structure counts from the host tables (every op's are packed).
+    auto structure = [](const DeviceOp& d, int32_t* rings, int32_t* pats, int32_t* pairs, int32_t* slots) {
+        const OpTables* T = d.tables.get();
+        *rings = T ? (int32_t)T->sp.rings.size() : d.spectral.n_rings;
+        *pats = T ? (int32_t)T->sw.pats.size() : d.sweep.n_pats;
+        *pairs = T ? (int32_t)T->sp.pair_slot.size() : d.spectral.n_pairs;
+        *slots = T ? (int32_t)T->sp.slot_ring.size() : d.spectral.n_slots;
+    };
+    structure(plan->fwd, &I.spectral_rings_forward, &I.sweep_patterns_forward, &I.spectral_pairs_forward,
+              &I.spectral_slots_forward);
+    structure(plan->tr, &I.spectral_rings_transpose, &I.sweep_patterns_transpose, &I.spectral_pairs_transpose,
+              &I.spectral_slots_transpose);
     I.psi_compressed_bytes = (int64_t)hf.t_in.size() * (8 + 4 * I.K) + 4 * (int64_t)hf.pat_ptr.size();
     for (const DeviceOp* d : {&plan->fwd, &plan->tr, &plan->fwd_adj, &plan->tr_adj}) {
-        I.bytes_entries += d->bytes_entries;
-        I.bytes_general += d->packed.bytes + d->packed_light.bytes + d->packed_rest.bytes +
-                           (int64_t)sizeof(int32_t) * d->n_rest_pats;
-        I.bytes_spectral += d->spectral.bytes + (d->spectral.n_rings > 0 ? d->g.nlat_o : 0);
-        I.bytes_sweep += d->sweep.bytes;
-        I.bytes_stencil += d->stencil.bytes;
+        const OpTables* T = d->tables.get();
+        if (!T && d->bytes == 0) continue;  // an adjoint the plan does not have
+        I.psi_bytes_all_layouts += T ? 64 + T->bytes[0] + T->bytes[1] + T->bytes[2] + T->bytes[3] : d->bytes;
     }
     *plan_out = plan;
     return ok();
@@ -1109,7 +1280,22 @@ disco_status_t disco_plan_destroy(disco_plan_t plan) {
 
 disco_status_t disco_plan_query(disco_plan_t plan, disco_plan_info_t* info) {
     if (!plan || !info) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan or info is NULL");
-    *info = plan->info;
+    std::lock_guard<std::mutex> lock(plan->lazy_mu);
+    disco_plan_info_t I = plan->info;
+    // Device memory as it stands (groups and matrix-core tables built since
+    // creation included).
+    I.psi_bytes = I.bytes_entries = I.bytes_general = I.bytes_spectral = I.bytes_sweep = I.bytes_stencil = 0;
+    I.bytes_matrix_core = 0;
+    for (const DeviceOp* d : {&plan->fwd, &plan->tr, &plan->fwd_adj, &plan->tr_adj}) {
+        I.bytes_entries += d->bytes_entries;
+        I.bytes_general += d->packed.bytes + d->packed_light.bytes + d->packed_rest.bytes;
+        I.bytes_spectral += d->spectral.bytes;
+        I.bytes_sweep += d->sweep.bytes;
+        I.bytes_stencil += d->stencil.bytes;
+        I.bytes_matrix_core += d->mfma.bytes;
+        I.psi_bytes += d->bytes + d->mfma.bytes;
+    }
+    *info = I;
     return ok();
 }
 
@@ -1127,7 +1313,18 @@ disco_status_t disco_kernel_work(disco_plan_t plan, int32_t transpose, int32_t a
                       (algo == DISCO_ALGO_AUTO || algo == DISCO_ALGO_FUSED || algo == DISCO_ALGO_MATRIX_CORE);
     if (algo == DISCO_ALGO_MATRIX_CORE && !mfma)
         return fail(DISCO_ERR_UNSUPPORTED, "no matrix-core kernel for this op and dtype");
+    if (!mfma) {
+        // The figures need the groups the call would run on (uploaded here
+        // if a call has not done so yet).
+        const disco_status_t s = ensure_parts(plan, op, needed_parts(op, resolve_auto(op, algo, c_out),
+                                                                     op.basis != DISCO_BASIS_BILINEAR_3X3));
+        if (s != DISCO_OK) return s;
+    }
     const Dispatch dp = dispatch(op, mfma ? DISCO_ALGO_FUSED_DIRECT : algo, c_in, c_out, dtype);
+    if (!mfma && dp.packed == &op.packed) {
+        const disco_status_t s = ensure_parts(plan, op, kPartDirect);
+        if (s != DISCO_OK) return s;
+    }
     struct Row { const char* name; Work w; };
     std::vector<Row> rows;
     auto spectral_rows = [&op](const SpectralDev&, std::vector<Row>* r) {

@@ -2,7 +2,9 @@
 // and C ABI layer.  Not installed; the public interface is include/disco.h.
 #pragma once
 
+#include <atomic>
 #include <cstdint>
+#include <memory>
 #include <string>
 #include <vector>
 
@@ -359,6 +361,13 @@ struct StencilDev {
     int64_t bytes = 0;
 };
 
+// Host-side tables of one op's layouts, kept until uploaded (disco_abi.cpp).
+struct OpTables;
+// Layout groups of an op, uploaded on first use: the fused schedule's
+// (spectral rings, ring sweep, general kernel for the rest), the general
+// kernel over every pattern, the plain entry tables, the stencil layout.
+enum : int { kPartCore = 1, kPartDirect = 2, kPartEntries = 4, kPartStencil = 8, kPartAll = 15 };
+
 // Device-side layout of one op (see disco_kernels.hip).
 struct DevEntry {
     int32_t row;  // input ring * nlon_i
@@ -380,6 +389,8 @@ struct DeviceOp {
     MfmaDev mfma;            // bf16 matrix-core layout, built at the op's first bf16 call
     int8_t mfma_state = 0;   // 0 not built yet, 1 built, -1 the op has no such layout
     bool src_transpose = false, src_adjoint = false;  // build_host_op arguments of this op
+    std::atomic<int> built{0};  // kPart* groups on the device (set after their upload completes)
+    std::shared_ptr<OpTables> tables;  // host tables of the groups not uploaded yet
     PackedDev packed_rest;   // light patterns the sweep runs do not cover
     int32_t* rest_pats = nullptr;  // device: those patterns' indices (gather-then-contract schedule)
     int32_t n_rest_pats = 0;

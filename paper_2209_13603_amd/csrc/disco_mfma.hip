@@ -181,6 +181,10 @@ __global__ __launch_bounds__(kMfmaTile, 2) void k_mfma(const MSeg* __restrict__ 
     }
     __syncthreads();
     const uint16_t* xb = x + (int64_t)b * Ci * n_in;
+    // The first chunk's values stay in registers for the whole workgroup.
+    bf8 A0[NPH];
+#pragma unroll
+    for (int r = 0; r < NPH; ++r) A0[r] = __builtin_bit_cast(bf8, as[r * 64 + lane]);
 
     // W operands of pass ci0: item i = tid + j kMfmaTile = (pair p, block
     // cb, lane l) < nw stages those of input-channel pair ci0 / 2 + p for
@@ -228,7 +232,7 @@ __global__ __launch_bounds__(kMfmaTile, 2) void k_mfma(const MSeg* __restrict__ 
                 const uint32_t* xb = xc + hs[4 * c + gq];
                 bf8 A[NPH];
 #pragma unroll
-                for (int r = 0; r < NPH; ++r) A[r] = __builtin_bit_cast(bf8, as[(c * NPH + r) * 64 + lane]);
+                for (int r = 0; r < NPH; ++r) A[r] = first ? A0[r] : __builtin_bit_cast(bf8, as[(c * NPH + r) * 64 + lane]);
                 bf8 Bv[2][kNB];
 #pragma unroll
                 for (int h = 0; h < 2; ++h)
@@ -248,7 +252,7 @@ __global__ __launch_bounds__(kMfmaTile, 2) void k_mfma(const MSeg* __restrict__ 
                 // All of the chunk's LDS reads first, then its products, so
                 // that one wait covers them (the scheduler otherwise reuses one
                 // register set and waits before every product pair).
-                __builtin_amdgcn_sched_group_barrier(0x100, NPH + 4 * kNB, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 4 * kNB, 0);
                 __builtin_amdgcn_sched_group_barrier(0x008, 2 * kNB * NPH, 0);
             };
             chunk(0, true);

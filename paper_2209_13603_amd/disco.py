@@ -38,6 +38,7 @@ BASES = {"bilinear3x3": DISCO_BASIS_BILINEAR_3X3, "axisym4": DISCO_BASIS_AXISYMM
 BASIS_SIZE = {DISCO_BASIS_BILINEAR_3X3: 9, DISCO_BASIS_AXISYMMETRIC_4: 4, DISCO_BASIS_SEPARABLE_4X4: 16}
 SAMPLINGS = {"cell_centred": DISCO_SAMPLING_CELL_CENTRED, "poles": DISCO_SAMPLING_POLES}
 DISCO_PLAN_BACKWARD = 1
+DISCO_PLAN_EAGER = 2
 
 ALGO_AUTO = 0
 ALGO_GATHER_THEN_CONTRACT = 1
@@ -92,7 +93,8 @@ class PlanInfo(ctypes.Structure):
                 ("spectral_slots_forward", ctypes.c_int32), ("spectral_slots_transpose", ctypes.c_int32),
                 ("psi_compressed_bytes", ctypes.c_int64), ("bytes_entries", ctypes.c_int64),
                 ("bytes_general", ctypes.c_int64), ("bytes_spectral", ctypes.c_int64),
-                ("bytes_sweep", ctypes.c_int64), ("bytes_stencil", ctypes.c_int64)]
+                ("bytes_sweep", ctypes.c_int64), ("bytes_stencil", ctypes.c_int64),
+                ("bytes_matrix_core", ctypes.c_int64), ("psi_bytes_all_layouts", ctypes.c_int64)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -200,10 +202,11 @@ class Plan:
 
     def __init__(self, nlat_in, nlon_in, nlat_out, nlon_out, theta_c, node_spacing=0.0,
                  quadrature=DISCO_QUAD_FEJER1, basis=DISCO_BASIS_BILINEAR_3X3,
-                 sampling=DISCO_SAMPLING_CELL_CENTRED, backward=False):
+                 sampling=DISCO_SAMPLING_CELL_CENTRED, backward=False, eager=False):
         lib = library()
         h = ctypes.c_void_p()
-        b = _basis(node_spacing, quadrature, basis, sampling, DISCO_PLAN_BACKWARD if backward else 0)
+        b = _basis(node_spacing, quadrature, basis, sampling,
+                   (DISCO_PLAN_BACKWARD if backward else 0) | (DISCO_PLAN_EAGER if eager else 0))
         _check(lib.disco_plan_create(nlat_in, nlon_in, nlat_out, nlon_out, float(theta_c),
                                      ctypes.byref(b), ctypes.byref(h)))
         self._h = h

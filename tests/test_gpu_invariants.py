@@ -180,14 +180,18 @@ def test_kernel_work_covers_the_op(name):
                 work = plan.kernel_work(transpose, algo, ci, co, dt)
                 say(name, transpose, algo, ci, co, dt, work)
                 gather = [k for k in work if k in ("gather_z", "gather_y", "spectral_mac", "sweep_gather_z",
-                                                    "sweep_gather_contract", "fused_gather_contract")]
+                                                    "sweep_gather_contract", "fused_gather_contract",
+                                                    "mfma_gather_contract")]
                 assert sum(work[k][2] for k in gather) == total
                 writers = [k for k in work if k in ("contract_z", "gather_y", "spectral_irfft",
-                                                     "sweep_gather_contract", "fused_gather_contract")]
+                                                     "sweep_gather_contract", "fused_gather_contract",
+                                                     "mfma_gather_contract")]
                 assert sum(work[k][0] for k in writers) == n_out
                 for k, (o, i, p) in work.items():
                     assert 0 <= o <= n_out and 0 <= i <= n_in and p >= 0
-                if algo == "fused":
+                # bf16 storage with auto / fused: the matrix-core kernel over every ring
+                assert ("mfma_gather_contract" in work) == (dt == "bf16" and algo in ("auto", "fused"))
+                if algo == "fused" and dt != "bf16":
                     assert ("spectral_mac" in work) == (info["spectral_rings_transpose" if transpose
                                                               else "spectral_rings_forward"] > 0)
                     # the sweep takes any channel count on single-phase ops (one
