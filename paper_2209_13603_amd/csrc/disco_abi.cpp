@@ -209,8 +209,12 @@ int64_t packed_bytes(const PackedHost& P) {
            vec_bytes(P.red_slots);
 }
 
-// Cost of one sweep run (entries plus fixed per-pattern work).
+// Cost of one sweep run (entries plus fixed per-pattern work).  The Z mode
+// (all-HBM schedule) runs shorter runs: more workgroups keep more stores in
+// flight (2048 x 4096, 8 channels: 520 us at 768, 502 us at 256), where the
+// contracting sweep loses (357 -> 363 us at 512).
 constexpr int kSweepTarget = 768;
+constexpr int kSweepZTarget = 256;
 
 disco_status_t upload_sweep(const SweepHost& H, SweepDev* d) {
     disco_status_t s;
@@ -337,6 +341,7 @@ struct OpTables {
     bool has_light = false, has_sweep = false;
     PackedHost light, rest;
     SweepHost sw;
+    SweepHost sw_z;  // kPartEntries: the Z mode's shorter runs (when there is a sweep)
     std::vector<int32_t> rest_pats;
     int64_t bytes[4] = {0, 0, 0, 0};  // device bytes of each group (core, direct, entries, stencil)
 };
@@ -424,10 +429,16 @@ disco_status_t prepare_op(const HostOp& h, DeviceOp* d) {
             if (rest_skip[i]) T->rest_pats.push_back((int32_t)i);
         int64_t cov = 0;
         for (uint8_t c : T->sw.covered) cov += c;
-        const int64_t ne = (int64_t)std::max<size_t>(T->sw.entries.size(), 1);
-        core += vec_bytes(T->sw.runs) + vec_bytes(T->sw.pats) + vec_bytes(T->sw.acts) +
-                ne * (int64_t)(sizeof(int32_t) + sizeof(PVal)) + (int64_t)sizeof(int32_t) * std::max<int64_t>(cov, 1) +
-                packed_bytes(T->rest) + (T->rest_pats.empty() ? 0 : vec_bytes(T->rest_pats));
+        auto sweep_bytes = [cov](const SweepHost& W) {
+            const int64_t ne = (int64_t)std::max<size_t>(W.entries.size(), 1);
+            return vec_bytes(W.runs) + vec_bytes(W.pats) + vec_bytes(W.acts) +
+                   ne * (int64_t)(sizeof(int32_t) + sizeof(PVal)) + (int64_t)sizeof(int32_t) * std::max<int64_t>(cov, 1);
+        };
+        core += sweep_bytes(T->sw) + packed_bytes(T->rest) + (T->rest_pats.empty() ? 0 : vec_bytes(T->rest_pats));
+        rc = pack_sweep(h, kSweepZTarget, heavy, &T->sw_z, &err);
+        if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
+        if (T->sw_z.covered != T->sw.covered) return fail(DISCO_ERR_DEVICE, "internal: sweep layouts cover different rings");
+        T->bytes[2] += sweep_bytes(T->sw_z);
     }
     T->bytes[0] = core;
     d->tables = T;
@@ -446,6 +457,7 @@ disco_status_t upload_parts(DeviceOp* d, int parts) {
     if (todo & kPartEntries) {
         if ((s = upload_vec(T->pat_ptr, &d->pat_ptr, &d->bytes_entries, "hipMalloc(pattern table)")) != DISCO_OK) return s;
         if ((s = upload_vec(T->ent, &d->entries, &d->bytes_entries, "hipMalloc(psi entries)")) != DISCO_OK) return s;
+        if (T->has_sweep && (s = upload_sweep(T->sw_z, &d->sweep_z)) != DISCO_OK) return s;
         d->built.fetch_or(kPartEntries);
     }
     if (todo & kPartDirect) {
@@ -478,7 +490,7 @@ disco_status_t upload_parts(DeviceOp* d, int parts) {
         d->built.fetch_or(kPartCore);
     }
     d->bytes = d->bytes_entries + d->packed.bytes + d->stencil.bytes + d->spectral.bytes + d->packed_light.bytes +
-               d->sweep.bytes + d->packed_rest.bytes + 64;
+               d->sweep.bytes + d->sweep_z.bytes + d->packed_rest.bytes + 64;
     if (d->built == kPartAll) d->tables.reset();
     return DISCO_OK;
 }
@@ -500,6 +512,7 @@ void free_op(DeviceOp* d) {
     free_packed(&d->packed_rest);
     free_spectral(&d->spectral);
     free_sweep(&d->sweep);
+    free_sweep(&d->sweep_z);
     free_mfma(&d->mfma);
     d->mfma_state = 0;
     void* sp[] = {d->stencil.pieces, d->stencil.chunks, d->stencil.vals, d->stencil.cells};
@@ -869,13 +882,11 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
     } else if (algo == DISCO_ALGO_GATHER_THEN_CONTRACT) {
         e = launch_gather_then_contract(a, ws_ptr);
     } else {
-        // The spectral rings' input transforms run first on the caller's
-        // stream; their products and inverse transforms then run on the
-        // plan's helper stream, forked from and joined back into the
-        // caller's stream, beside the direct kernels (they take the slots the
-        // sweep's last workgroups leave free); when the sweep kernel takes
-        // the light rings, the general kernel's remaining rings follow the
-        // spectral ones there.
+        // The spectral rings (input transforms, products, inverse
+        // transforms) run on the plan's helper stream, forked from and joined
+        // back into the caller's stream, beside the direct kernels on the
+        // caller's stream; when the sweep kernel takes the light rings, the
+        // general kernel's remaining rings follow the spectral ones there.
         hipEvent_t fork = nullptr, join = nullptr;
         const bool fork_aux = spectral && plan->aux && !ext;
         ExecArgs as = a;
@@ -883,10 +894,9 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
             as.stream = plan->aux;
             e = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
             if (e == hipSuccess) e = hipEventCreateWithFlags(&join, hipEventDisableTiming);
-            if (e == hipSuccess) e = launch_spectral(a, ws_ptr, 1);
             if (e == hipSuccess) e = hipEventRecord(fork, stream);
             if (e == hipSuccess) e = hipStreamWaitEvent(plan->aux, fork, 0);
-            if (e == hipSuccess) e = launch_spectral(as, ws_ptr, kSpectralAll & ~1);
+            if (e == hipSuccess) e = launch_spectral(as, ws_ptr, kSpectralAll);
             if (e == hipSuccess && sweep) e = launch_fused(as, packed, (float*)((char*)ws_ptr + ws_spec + ws_sweep));
             if (e == hipSuccess) e = hipEventRecord(join, plan->aux);
         } else if (spectral) {
@@ -1290,7 +1300,7 @@ disco_status_t disco_plan_query(disco_plan_t plan, disco_plan_info_t* info) {
         I.bytes_entries += d->bytes_entries;
         I.bytes_general += d->packed.bytes + d->packed_light.bytes + d->packed_rest.bytes;
         I.bytes_spectral += d->spectral.bytes;
-        I.bytes_sweep += d->sweep.bytes;
+        I.bytes_sweep += d->sweep.bytes + d->sweep_z.bytes;
         I.bytes_stencil += d->stencil.bytes;
         I.bytes_matrix_core += d->mfma.bytes;
         I.psi_bytes += d->bytes + d->mfma.bytes;

@@ -385,6 +385,7 @@ struct DeviceOp {
     PackedDev packed_light;  // patterns not handled by the spectral path
     SpectralDev spectral;
     SweepDev sweep;          // light patterns walked by the sweep kernel (Ci <= kCIC)
+    SweepDev sweep_z;        // the same patterns in shorter runs, for the sweep's Z mode
     StencilDev stencil;      // longitude stride 1: the blocked layout of the stencil kernels
     MfmaDev mfma;            // bf16 matrix-core layout, built at the op's first bf16 call
     int8_t mfma_state = 0;   // 0 not built yet, 1 built, -1 the op has no such layout

@@ -235,8 +235,12 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
 
     const int tid = threadIdx.x;
     const int bid = xcd_remap(blockIdx.x, gridDim.x);
-    const int run = bid / n_qtiles;
-    const int qt = bid - run * n_qtiles;
+    // Work item = (longitude tile, run), runs fastest: the workgroups in
+    // flight on one XCD cover consecutive runs of the same tile, which share
+    // the input rings at their boundaries in that XCD's L2.
+    const int n_runs = gridDim.x / n_qtiles;
+    const int qt = bid / n_runs;
+    const int run = bid - qt * n_runs;
     const int b = blockIdx.y / n_cotiles;
     const int co0 = (blockIdx.y - b * n_cotiles) * COT;          // output channel tile
     const int c0 = ZOUT ? (blockIdx.y - b * n_cotiles) * kCIC : (YMODE == kStoreY ? 0 : cg0);  // input channel group
@@ -609,7 +613,7 @@ hipError_t launch_sweep(const ExecArgs& a, float* y32_ws) {
 
 hipError_t launch_sweep_z(const ExecArgs& a, float* z) {
     const OpGeom& g = a.op->g;
-    const SweepDev& S = a.op->sweep;
+    const SweepDev& S = a.op->sweep_z.n_runs > 0 ? a.op->sweep_z : a.op->sweep;
     if (S.n_runs == 0) return hipSuccess;
     const int n_qtiles = (g.nq + kBlock - 1) / kBlock;
     const int n_cg = (a.Ci + kCIC - 1) / kCIC;
