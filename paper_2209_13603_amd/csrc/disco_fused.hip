@@ -209,6 +209,9 @@ __global__ __launch_bounds__(TQ) void k_fused(const PItem* __restrict__ items,
                     }
                 }
                 __syncthreads();
+                // Waves whose output longitudes all lie past the ring's end
+                // stage but do not gather.
+                if (q0 + (tid & ~63) >= g.nq) continue;
                 run_cell<0>(C.cls[0] - C.cls[0], C.cls[1] - C.cls[0], eoffs, evs, xs, lane_col, z);
                 run_cell<1>(C.cls[1] - C.cls[0], C.cls[2] - C.cls[0], eoffs, evs, xs, lane_col, z);
                 run_cell<2>(C.cls[2] - C.cls[0], C.cls[3] - C.cls[0], eoffs, evs, xs, lane_col, z);
