@@ -199,22 +199,37 @@ constexpr int kSweepCols = 1152;  // LDS columns (per channel) of all slots of a
 constexpr int kSweepEntries = 128;  // entries of one pattern on the sweep path
 
 struct SRun { int32_t pat_begin, pat_end; };             // [begin, end) into SPat
+// Entry groups of a sweep pattern, in the order the kernel walks them: the 16
+// hat cells row by row, and after cell (a + 1, b + 1), the last cell that
+// touches basis function K = 3 a + b, the group of entries whose only
+// non-zero value is K's (a single product per channel instead of the 2 or 4
+// of their cell).  Group ids: cell c is c, K's group is 16 + K.
+constexpr int kSweepGroups = 25;
+constexpr int sweep_last_cell(int K) { return 4 * (K / 3 + 1) + K % 3 + 1; }
+constexpr int sweep_group_pos(int grp) {
+    return grp >= 16 ? sweep_last_cell(grp - 16) + (grp - 16) + 1
+                     : grp + (grp > 5) + (grp > 6) + (grp > 7) + (grp > 9) + (grp > 10) + (grp > 11) +
+                           (grp > 13) + (grp > 14) + (grp > 15);
+}
 // One pattern of a run, 12 dwords (the kernel keeps two in scalar registers):
-// the entries are [ent, ent + nent), sorted by hat cell, ncell[c / 4] byte
-// c % 4 = entries in cell c; the spans first read here are acts[act_begin,
-// act_begin + nact), the first of them copied inline.
+// the entries are [ent, ent + nent) in walk order; byte c % 4 of ncell[c / 4]
+// = entries in hat cell c, bit 16 + K of nact_nent = one entry in basis
+// function K's single-value group (a second one stays in its cell); the
+// spans first read here are acts[act_begin, act_begin + nact), the first of
+// them copied inline.
 struct SPat {
     int32_t pattern;
     int32_t act_begin;
-    int32_t nact_nent;           // nact in bits 0..7, nent in bits 8..23
+    int32_t nact_nent;           // nact in bits 0..7, nent in bits 8..15, singles in bits 16..24
     int32_t ent;
     uint32_t ncell[4];
     PSpan first;                 // acts[act_begin] (zeros when nact == 0)
 };
 static_assert(sizeof(SPat) == 48, "SPat layout");
-static_assert(kSweepEntries <= 255, "per-cell entry counts are bytes");
+static_assert(kSweepEntries <= 255, "per-cell and per-pattern entry counts are bytes");
 constexpr int spat_nact(const SPat& P) { return P.nact_nent & 255; }
-constexpr int spat_nent(const SPat& P) { return (P.nact_nent >> 8) & 0xffff; }
+constexpr int spat_nent(const SPat& P) { return (P.nact_nent >> 8) & 255; }
+constexpr int spat_single(const SPat& P, int K) { return (P.nact_nent >> (16 + K)) & 1; }
 
 struct SweepHost {
     std::vector<SRun> runs;

@@ -251,9 +251,47 @@ int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& sk
         }
         return u;
     };
+    // A pattern's entries in walk order: each entry goes to its hat cell with
+    // the cell's 1, 2 or 4 values, or, when only one of those values is not
+    // zero and that basis function's single-value group is still empty, to
+    // that group with that value alone; entries without a non-zero value are
+    // left out.
+    struct GEnt { int grp; int32_t e; float v[4]; };
+    auto group_entries = [&](int pat) {
+        std::vector<GEnt> out;
+        int count[kSweepGroups] = {0};
+        for (int32_t e = op.pat_ptr[(size_t)pat]; e < op.pat_ptr[(size_t)pat + 1]; ++e) {
+            const int cell = op.cell[(size_t)e];
+            const int cu = cell / 4, cv = cell % 4;
+            const int fa = cu == 0 ? 0 : cu - 1, na = (cu == 0 || cu == 3) ? 1 : 2;
+            const int fb = cv == 0 ? 0 : cv - 1, nb = (cv == 0 || cv == 3) ? 1 : 2;
+            const float* v9 = &op.val[(size_t)e * kBasis];
+            GEnt G{cell, e, {0.0f, 0.0f, 0.0f, 0.0f}};
+            int k = 0, nz = 0, kz = 0;
+            for (int a = fa; a < fa + na; ++a)
+                for (int b = fb; b < fb + nb; ++b) {
+                    G.v[k++] = v9[3 * a + b];
+                    if (v9[3 * a + b] != 0.0f) { ++nz; kz = 3 * a + b; }
+                }
+            if (nz == 0) continue;
+            if (nz == 1 && k > 1 && count[16 + kz] == 0) G = GEnt{16 + kz, e, {v9[kz], 0.0f, 0.0f, 0.0f}};
+            ++count[G.grp];
+            out.push_back(G);
+        }
+        std::stable_sort(out.begin(), out.end(), [](const GEnt& x, const GEnt& y) {
+            return sweep_group_pos(x.grp) < sweep_group_pos(y.grp);
+        });
+        return out;
+    };
+    std::vector<int32_t> n_grouped((size_t)g.n_patterns(), -1);
+    auto n_entries = [&](int pat) {
+        int32_t& n = n_grouped[(size_t)pat];
+        if (n < 0) n = (int32_t)group_entries(pat).size();
+        return (int)n;
+    };
     auto eligible = [&](int pat) {
         if (!skip.empty() && skip[(size_t)pat]) return false;
-        const int n = op.pat_ptr[(size_t)pat + 1] - op.pat_ptr[(size_t)pat];
+        const int n = n_entries(pat);
         return n > 0 && n <= kSweepEntries;
     };
 
@@ -286,8 +324,7 @@ int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& sk
                     if (first[(size_t)t] >= 0 && first[(size_t)t] <= (int)i && last[(size_t)t] >= (int)i) ++live;
                 live_max = std::max(live_max, live);
             }
-            const int n_e = op.pat_ptr[(size_t)end + 1] - op.pat_ptr[(size_t)end];
-            const int c = n_e + 24 + (int)u.size() * 2;
+            const int c = n_entries(end) + 24 + (int)u.size() * 2;
             if (end > pat && ((int64_t)live_max * cap > kSweepCols || cost + c > target_cost)) {
                 uses.pop_back();
                 break;
@@ -334,33 +371,23 @@ int pack_sweep(const HostOp& op, int target_cost, const std::vector<uint8_t>& sk
                 H.acts.push_back(PSpan{r.ti * g.nlon_i, dmin[(size_t)r.ti], halo + dmax[(size_t)r.ti] - dmin[(size_t)r.ti] + 1, sl * cap});
             }
             const int nact = (int)H.acts.size() - SP.act_begin;
-            if (nact > 0) SP.first = H.acts[(size_t)SP.act_begin];
-            // Entries, sorted by cell.
-            std::vector<std::pair<int, PEntry>> ents;
-            for (int32_t e = op.pat_ptr[(size_t)p]; e < op.pat_ptr[(size_t)p + 1]; ++e) {
-                const int32_t ti = op.t_in[(size_t)e];
-                const int cell = op.cell[(size_t)e];
-                const int cu = cell / 4, cv = cell % 4;
-                PEntry E{};
-                E.off = slot[(size_t)ti] * cap + (op.d_raw[(size_t)e] - dmin[(size_t)ti]);
-                int k = 0;
-                const float* v9 = &op.val[(size_t)e * kBasis];
-                for (int a = 0; a < 3; ++a)
-                    for (int b = 0; b < 3; ++b) {
-                        const int fa = cu == 0 ? 0 : cu - 1, na = (cu == 0 || cu == 3) ? 1 : 2;
-                        const int fb = cv == 0 ? 0 : cv - 1, nb = (cv == 0 || cv == 3) ? 1 : 2;
-                        if (a >= fa && a < fa + na && b >= fb && b < fb + nb) E.v[k++] = v9[3 * a + b];
-                    }
-                ents.push_back({cell, E});
+            if (nact > 255) {
+                if (err) *err = "internal: more than 255 new spans in one sweep pattern";
+                return DISCO_ERR_DEVICE;
             }
-            std::stable_sort(ents.begin(), ents.end(),
-                             [](const std::pair<int, PEntry>& x, const std::pair<int, PEntry>& y) { return x.first < y.first; });
+            if (nact > 0) SP.first = H.acts[(size_t)SP.act_begin];
+            // Entries in walk order.
+            const std::vector<GEnt> ents = group_entries(p);
             SP.ent = (int32_t)H.entries.size();
             SP.nact_nent = nact | ((int32_t)ents.size() << 8);
-            for (auto& pe : ents) {
-                const int c = pe.first;
-                SP.ncell[c / 4] += 1u << (8 * (c % 4));
-                H.entries.push_back(pe.second);
+            for (const GEnt& G : ents) {
+                const int32_t ti = op.t_in[(size_t)G.e];
+                if (G.grp < 16)
+                    SP.ncell[G.grp / 4] += 1u << (8 * (G.grp % 4));
+                else
+                    SP.nact_nent |= 1 << G.grp;  // bit 16 + K
+                H.entries.push_back(PEntry{slot[(size_t)ti] * cap + (op.d_raw[(size_t)G.e] - dmin[(size_t)ti]),
+                                           {G.v[0], G.v[1], G.v[2], G.v[3]}});
             }
             H.pats.push_back(SP);
             H.covered[(size_t)p] = 1;

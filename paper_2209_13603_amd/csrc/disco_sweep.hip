@@ -23,6 +23,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "disco_internal.h"
 
@@ -90,11 +91,38 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-template <int CELL>
+// The entry group at position pos of the walk, and the walk itself: f is
+// called with each position in order, as a compile-time constant.
+constexpr int sweep_group_at(int pos) {
+    for (int g = 0; g < kSweepGroups; ++g)
+        if (sweep_group_pos(g) == pos) return g;
+    return -1;
+}
+constexpr bool sweep_walk_is_a_permutation() {
+    for (int p = 0; p < kSweepGroups; ++p)
+        if (sweep_group_at(p) < 0) return false;
+    return true;
+}
+static_assert(sweep_walk_is_a_permutation(), "every walk position holds one group");
+template <int POS, class F>
+__device__ __forceinline__ void walk_groups(F& f) {
+    if constexpr (POS < kSweepGroups) {
+        f(std::integral_constant<int, POS>{});
+        walk_groups<POS + 1>(f);
+    }
+}
+
+// Basis functions touched by entry group G (a hat cell, or a basis
+// function's single-value group): rows A0 .. A0 + NA - 1, columns B0 .. B0 +
+// NB - 1 of the 3 x 3 grid, the entry's values in row-major order.
+constexpr int grp_a0(int G) { return G < 16 ? cell_first(G / 4) : (G - 16) / 3; }
+constexpr int grp_na(int G) { return G < 16 ? cell_count(G / 4) : 1; }
+constexpr int grp_b0(int G) { return G < 16 ? cell_first(G % 4) : (G - 16) % 3; }
+constexpr int grp_nb(int G) { return G < 16 ? cell_count(G % 4) : 1; }
+
+template <int G>
 __device__ __forceinline__ void fma_cell(const float4& v, const float4 (&xv)[kNCQ], float (&z)[kCIC][kBasis]) {
-    constexpr int CU = CELL / 4, CV = CELL % 4;
-    constexpr int A0 = cell_first(CU), NA = cell_count(CU);
-    constexpr int B0 = cell_first(CV), NB = cell_count(CV);
+    constexpr int A0 = grp_a0(G), NA = grp_na(G), B0 = grp_b0(G), NB = grp_nb(G);
     const float vn[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int ia = 0; ia < NA; ++ia)
@@ -112,17 +140,28 @@ __device__ __forceinline__ void fma_cell(const float4& v, const float4 (&xv)[kNC
         }
 }
 
-// Entries [e, ee) of one cell, with the input and values of the next entry
+// Entries [e, ee) of one group, with the input and values of the next entry
 // already in flight while an entry's FMAs run.  On entry (and on return) x0
 // and v0 hold the input and values of entry e and o1 the LDS column offset of
 // entry e + 1; entries are taken in pairs so that the two register sets swap
-// roles statically instead of being copied.  Cells are contiguous in the
-// entry array, so the lookahead runs across cell boundaries; the array ends
+// roles statically instead of being copied.  Groups are contiguous in the
+// entry array, so the lookahead runs across group boundaries; the array ends
 // with kEntryPad padding entries (offset 0, values 0), so the lookahead reads need
 // no bounds test.  The scheduling barriers keep the compiler from sinking
 // the next entry's LDS reads below the current entry's FMAs (which it does to
 // save registers, leaving the read latency exposed).
-template <int CELL>
+template <int G>
+__device__ __forceinline__ void entry_one(int e, float4 (&x0)[kNCQ], float4& v0, int& o1,
+                                          const int* __restrict__ eoffs, const float4* __restrict__ evs,
+                                          const float4* __restrict__ xs, int lane_col, float (&z)[kCIC][kBasis]) {
+    fma_cell<G>(v0, x0, z);
+#pragma unroll
+    for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kSweepCols + lane_col + o1];
+    v0 = evs[e + 1];
+    o1 = eoffs[e + 2];
+}
+
+template <int G>
 __device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], float4& v0, int& o1,
                                          const int* __restrict__ eoffs, const float4* __restrict__ evs,
                                          const float4* __restrict__ xs, int lane_col, float (&z)[kCIC][kBasis]) {
@@ -133,22 +172,18 @@ __device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], flo
         const float4 v1 = evs[e + 1];
         const int o2 = eoffs[e + 2];
         __builtin_amdgcn_sched_barrier(0);
-        fma_cell<CELL>(v0, x0, z);
+        fma_cell<G>(v0, x0, z);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kSweepCols + lane_col + o2];
         v0 = evs[e + 2];
         o1 = eoffs[e + 3];
         __builtin_amdgcn_sched_barrier(0);
-        fma_cell<CELL>(v1, x1, z);
+        fma_cell<G>(v1, x1, z);
         __builtin_amdgcn_sched_barrier(0);
     }
     if (e < ee) {
-        fma_cell<CELL>(v0, x0, z);
-#pragma unroll
-        for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kSweepCols + lane_col + o1];
-        v0 = evs[e + 1];
-        o1 = eoffs[e + 2];
+        entry_one<G>(e, x0, v0, o1, eoffs, evs, xs, lane_col, z);
         ++e;
     }
 }
@@ -221,8 +256,10 @@ __device__ __forceinline__ void mfma_contract_k_bf16(v4f (&yacc)[NQ], const v4s 
 // the second grid dimension runs over (batch item, group of kCIC input
 // channels) instead (n_cotiles = number of channel groups) and z receives
 // Z[b, c, k, pixel] for the group's channels; w and y are not used.
+// Up to 8 output channels per launch the registers are held to 128 VGPRs, so
+// that the four workgroups the LDS admits per CU are all resident.
 template <typename T, int COT, bool ZOUT, int YMODE>
-__global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs, const SPat* __restrict__ pats,
+__global__ __launch_bounds__(kBlock, COT <= 8 ? 4 : 1) void k_sweep(const SRun* __restrict__ runs, const SPat* __restrict__ pats,
                                                   const PSpan* __restrict__ acts, const int32_t* __restrict__ offs,
                                                   const PVal* __restrict__ vals, OpGeom g,
                                                   const T* __restrict__ x, const T* __restrict__ w,
@@ -454,57 +491,36 @@ __global__ __launch_bounds__(kBlock) void k_sweep(const SRun* __restrict__ runs,
             zoff = q < g.nq ? (tz * g.nlon_o + q * g.P + pz) * (int)sizeof(float) : kBufferOutOfRange;
         }
         // Contraction on the matrix cores: lane l ends with y[co0 + 4 quad +
-        // r][its pixel] in register r of yacc[quad].  Cells are walked row by
-        // row over the 4 x 4 grid, so basis function (a, b) is complete after
-        // cell (a + 1, b + 1) and is contracted right there.
+        // r][its pixel] in register r of yacc[quad].
         v4f yacc[COT / 4];
 #pragma unroll
         for (int j = 0; j < COT / 4; ++j) yacc[j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-        int ce = 0;  // end of the current cell in the pattern's entries
-        ce += (int)((SP.ncell[0] >> 0) & 255u);
-        run_cell<0>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        ce += (int)((SP.ncell[0] >> 8) & 255u);
-        run_cell<1>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        ce += (int)((SP.ncell[0] >> 16) & 255u);
-        run_cell<2>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        ce += (int)((SP.ncell[0] >> 24) & 255u);
-        run_cell<3>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        ce += (int)((SP.ncell[1] >> 0) & 255u);
-        run_cell<4>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        ce += (int)((SP.ncell[1] >> 8) & 255u);
-        run_cell<5>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<0>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<0, COT / 4>(yacc, wb, z); else mfma_contract_k<0, 0, COT / 4>(yacc, wv, z);
-        ce += (int)((SP.ncell[1] >> 16) & 255u);
-        run_cell<6>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<1>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<1, COT / 4>(yacc, wb, z); else mfma_contract_k<1, 0, COT / 4>(yacc, wv, z);
-        ce += (int)((SP.ncell[1] >> 24) & 255u);
-        run_cell<7>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<2>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<2, COT / 4>(yacc, wb, z); else mfma_contract_k<2, 0, COT / 4>(yacc, wv, z);
-        ce += (int)((SP.ncell[2] >> 0) & 255u);
-        run_cell<8>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        ce += (int)((SP.ncell[2] >> 8) & 255u);
-        run_cell<9>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<3>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<3, COT / 4>(yacc, wb, z); else mfma_contract_k<3, 0, COT / 4>(yacc, wv, z);
-        ce += (int)((SP.ncell[2] >> 16) & 255u);
-        run_cell<10>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<4>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<4, COT / 4>(yacc, wb, z); else mfma_contract_k<4, 0, COT / 4>(yacc, wv, z);
-        ce += (int)((SP.ncell[2] >> 24) & 255u);
-        run_cell<11>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<5>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<5, COT / 4>(yacc, wb, z); else mfma_contract_k<5, 0, COT / 4>(yacc, wv, z);
-        ce += (int)((SP.ncell[3] >> 0) & 255u);
-        run_cell<12>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        ce += (int)((SP.ncell[3] >> 8) & 255u);
-        run_cell<13>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<6>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<6, COT / 4>(yacc, wb, z); else mfma_contract_k<6, 0, COT / 4>(yacc, wv, z);
-        ce += (int)((SP.ncell[3] >> 16) & 255u);
-        run_cell<14>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
-        if constexpr (ZOUT) store_z_k<7>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<7, COT / 4>(yacc, wb, z); else mfma_contract_k<7, 0, COT / 4>(yacc, wv, z);
-        ce += (int)((SP.ncell[3] >> 24) & 255u);
-        run_cell<15>(e, ce, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+        // The entry groups in walk order; after basis function K's
+        // single-value group its sums are complete and are contracted (or
+        // stored) right there.  The next pattern's descriptor is requested
+        // before the last contraction.
         const int pattern = SP.pattern;
-        SP = SPn;
-        SPn = pats[pi + 2 < R.pat_end ? pi + 2 : pi];
-        if constexpr (ZOUT) store_z_k<8>(zr, zoff, zplane, z); else if constexpr (kMM16) mfma_contract_k_bf16<8, COT / 4>(yacc, wb, z); else mfma_contract_k<8, 0, COT / 4>(yacc, wv, z);
+        auto step = [&](auto pos_c) {
+            constexpr int grp = sweep_group_at(decltype(pos_c)::value);
+            if constexpr (grp < 16) {
+                run_cell<grp>(e, e + (int)((SP.ncell[grp / 4] >> (8 * (grp % 4))) & 255u), x0, v0, o1, eoffs, evs, xs,
+                              lane_col, z);
+            } else {
+                constexpr int K = grp - 16;
+                if (spat_single(SP, K)) {
+                    entry_one<grp>(e, x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                    ++e;
+                }
+                if constexpr (K == kBasis - 1) {
+                    SP = SPn;
+                    SPn = pats[pi + 2 < R.pat_end ? pi + 2 : pi];
+                }
+                if constexpr (ZOUT) store_z_k<K>(zr, zoff, zplane, z);
+                else if constexpr (kMM16) mfma_contract_k_bf16<K, COT / 4>(yacc, wb, z);
+                else mfma_contract_k<K, 0, COT / 4>(yacc, wv, z);
+            }
+        };
+        walk_groups<0>(step);
         // Every lane issues the same COT stores (outputs that do not exist are
         // dropped by the buffer range check: an out-of-range offset for
         // longitudes past the ring, an empty buffer for channels past Cout),

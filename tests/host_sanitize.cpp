@@ -41,6 +41,71 @@ uint16_t bf16_of(float f) {
 // The matrix-core layout holds every entry's nine values (rounded to bf16)
 // exactly once, at its (output ring, phase, input ring, offset), and nothing
 // else; every staged element a lane reads lies inside its segment.
+// The sweep layout holds every non-zero value of the patterns it covers
+// exactly once, at the input column and basis function of the op's entry:
+// entries are mapped back through the spans resident in the run's LDS slots
+// and decoded by their group (hat cell or single-value group); no entry is
+// without a non-zero value.
+void check_sweep(const HostOp& op, const SweepHost& sw, const std::string& what) {
+    const OpGeom& g = op.g;
+    std::map<std::tuple<int, int, int, int>, float> want, got;
+    for (int pat = 0; pat < g.n_patterns(); ++pat) {
+        if (!sw.covered[(size_t)pat]) continue;
+        for (int32_t e = op.pat_ptr[(size_t)pat]; e < op.pat_ptr[(size_t)pat + 1]; ++e)
+            for (int k = 0; k < kBasis; ++k) {
+                const float v = op.val[(size_t)e * kBasis + k];
+                if (v != 0.0f) want[{pat, op.t_in[(size_t)e], op.d_raw[(size_t)e], k}] = v;
+            }
+    }
+    auto fail = [&](const char* m) {
+        std::printf("FAIL %s: sweep layout: %s\n", what.c_str(), m);
+        ++failures;
+    };
+    for (const SRun& R : sw.runs) {
+        std::map<int, PSpan> resident;  // by lds_base
+        for (int32_t pi = R.pat_begin; pi < R.pat_end; ++pi) {
+            const SPat& P = sw.pats[(size_t)pi];
+            for (int a = P.act_begin; a < P.act_begin + spat_nact(P); ++a) resident[sw.acts[(size_t)a].lds_base] = sw.acts[(size_t)a];
+            int e = P.ent, n_groups = 0;
+            for (int pos = 0; pos < kSweepGroups; ++pos) {
+                int grp = -1;
+                for (int q = 0; q < kSweepGroups; ++q)
+                    if (sweep_group_pos(q) == pos) grp = q;
+                const int n = grp < 16 ? (int)((P.ncell[grp / 4] >> (8 * (grp % 4))) & 255u) : spat_single(P, grp - 16);
+                const int a0 = grp < 16 ? (grp / 4 == 0 ? 0 : grp / 4 - 1) : (grp - 16) / 3;
+                const int na = grp < 16 ? ((grp / 4 == 0 || grp / 4 == 3) ? 1 : 2) : 1;
+                const int b0 = grp < 16 ? (grp % 4 == 0 ? 0 : grp % 4 - 1) : (grp - 16) % 3;
+                const int nb = grp < 16 ? ((grp % 4 == 0 || grp % 4 == 3) ? 1 : 2) : 1;
+                for (int i = 0; i < n; ++i, ++e) {
+                    const PEntry& E = sw.entries[(size_t)e];
+                    auto it = resident.upper_bound(E.off);
+                    if (it == resident.begin()) return fail("an entry before every slot");
+                    --it;
+                    const PSpan& S = it->second;
+                    if (E.off >= S.lds_base + S.len) return fail("an entry outside its slot's span");
+                    const int ti = S.row / g.nlon_i, d_raw = S.dstart + (E.off - S.lds_base);
+                    bool any = false;
+                    for (int ia = 0; ia < na; ++ia)
+                        for (int ib = 0; ib < nb; ++ib) {
+                            const float v = E.v[ia * nb + ib];
+                            if (v == 0.0f) continue;
+                            any = true;
+                            auto key = std::make_tuple(P.pattern, ti, d_raw, 3 * (a0 + ia) + b0 + ib);
+                            if (got.count(key)) return fail("a value stored twice");
+                            got[key] = v;
+                        }
+                    for (int j = na * nb; j < 4; ++j)
+                        if (E.v[j] != 0.0f) return fail("a value past the group's basis functions");
+                    if (!any) return fail("an entry without a non-zero value");
+                }
+                n_groups += n;
+            }
+            if (n_groups != spat_nent(P)) return fail("group counts do not add up to the pattern's entries");
+        }
+    }
+    if (got != want) fail("values differ from the op's");
+}
+
 void check_mfma(const HostOp& op, const std::string& what) {
     MfmaHost M;
     std::string err;
@@ -191,6 +256,7 @@ void run_op(const PlanParams& p, bool transpose, bool quad_at_output, const char
     check(pack_op(op, 512, heavy, &PL, &err), what + " pack_op (light)", err);
     SweepHost sw;
     check(pack_sweep(op, 768, heavy, &sw, &err), what + " pack_sweep", err);
+    check_sweep(op, sw, what);
     std::vector<uint8_t> rest(sw.covered);
     for (size_t i = 0; i < rest.size() && i < heavy.size(); ++i) rest[i] |= heavy[i];
     PackedHost PR;
