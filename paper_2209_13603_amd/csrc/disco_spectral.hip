@@ -184,9 +184,10 @@ __global__ __launch_bounds__(kFftBlock) void k_spectral(const int32_t* __restric
                                                        const T* __restrict__ w, float2* __restrict__ yh,
                                                        int B, int Ci, int Co, int M, int n_cotiles,
                                                        bool w_trans) {
-    // Input channels per accumulation pass: four for up to 8 output
-    // channels, two above (the accumulators would cost occupancy).
-    constexpr int SC = COT <= 8 ? 4 : 2;
+    // Input channels per accumulation pass (output tiles have at most 8
+    // channels).
+    static_assert(COT <= 8, "output tiles of at most 8 channels");
+    constexpr int SC = 4;
     // This pass's weights as (W_3a + W_3a+2, W_3a+2 - W_3a, W_3a+1) for each
     // (input channel, output channel, a), staged in LDS and read back by
     // broadcast (as uniform scalar loads they would need more SGPRs than
@@ -352,10 +353,12 @@ hipError_t spectral_launch(const ExecArgs& a, float* ws, int stages) {
 
 template <typename T>
 hipError_t spectral_dispatch(const ExecArgs& a, float* ws, int stages) {
+    // Output channels in tiles of at most 8: wider tiles leave too few
+    // workgroups (512 x 1024, 32 -> 32 channels: 240 with tiles of 32, the
+    // products 207 -> 136 us with tiles of 8, where each tile redoes the
+    // cheap per-pair sums).
     if (a.Co <= 4) return spectral_launch<T, 4>(a, ws, stages);
-    if (a.Co <= 8) return spectral_launch<T, 8>(a, ws, stages);
-    if (a.Co <= 16) return spectral_launch<T, 16>(a, ws, stages);
-    return spectral_launch<T, 32>(a, ws, stages);
+    return spectral_launch<T, 8>(a, ws, stages);
 }
 
 }  // namespace
