@@ -165,11 +165,10 @@ void free_spectral(SpectralDev* d) {
 
 disco_status_t pack_general(const HostOp& h, const std::vector<uint8_t>& skip, PackedHost* P) {
     std::string err;
-    // A 64-lane tile when a pattern has at most 64 output longitudes, so
-    // that the lanes of a 256-lane tile do not idle (measured on 32 x 64);
-    // 256 otherwise (on 128 x 256 -> 64 x 128, whose patterns have 128, the
-    // 128-lane tile was slower: 104 against 71 us, fewer waves in flight).
-    const int tile = h.g.nq <= 64 ? 64 : kTileQ;
+    // The narrowest tile that covers a pattern's output longitudes (64, 128
+    // or 256): the general kernel's 256 threads then split each chunk's
+    // entries between 4, 2 or 1 groups of lanes instead of idling.
+    const int tile = h.g.nq <= 64 ? 64 : h.g.nq <= 128 ? 128 : kTileQ;
     int rc = pack_op(h, fused_target_entries(h, tile), skip, P, &err, tile);
     if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
     return DISCO_OK;

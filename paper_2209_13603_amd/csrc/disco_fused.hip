@@ -120,10 +120,14 @@ __device__ __forceinline__ void run_cell(int eb, int ee, const int* __restrict__
     }
 }
 
-// TQ: output longitudes (lanes) per workgroup, the width the op's spans were
-// packed for (PackedDev::tile).
+// TQ: output longitudes per workgroup, the width the op's spans were packed
+// for (PackedDev::tile).  A workgroup always has kBlock threads: with TQ <
+// kBlock they form kParts = kBlock / TQ groups of TQ lanes over the same
+// longitudes, each group gathering an equal share of every chunk's entries
+// (in entry order, so within whole cells or parts of one), and the groups'
+// contracted outputs are summed in group order at the end of a segment.
 template <typename T, int COT, int TQ>
-__global__ __launch_bounds__(TQ) void k_fused(const PItem* __restrict__ items,
+__global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ items,
                                                   const PSeg* __restrict__ segs,
                                                   const PChunk* __restrict__ chunks,
                                                   const PSpan* __restrict__ spans,
@@ -139,15 +143,19 @@ __global__ __launch_bounds__(TQ) void k_fused(const PItem* __restrict__ items,
     __shared__ float ws[kCIC * kBasis * COT];
     constexpr bool kBf16 = sizeof(T) == 2;
 
+    constexpr int kParts = kBlock / TQ;
+    static_assert(kParts * TQ == kBlock && TQ >= 64, "tiles of 64, 128 or 256 longitudes");
     const int tid = threadIdx.x;
+    const int lane = tid & (TQ - 1);  // output longitude within the tile
+    const int part = tid / TQ;        // share of the entries
     const int bid = xcd_remap(blockIdx.x, gridDim.x);
     const int item = bid / n_qtiles;
     const int qt = bid - item * n_qtiles;
     const int b = blockIdx.y / n_cotiles;
     const int co0 = (blockIdx.y - b * n_cotiles) * COT;
     const int q0 = qt * TQ;
-    const int q = q0 + tid;
-    const int lane_col = g.stride * tid;
+    const int q = q0 + lane;
+    const int lane_col = g.stride * lane;
     const int64_t n_in = (int64_t)g.nlat_i * g.nlon_i;
     const int64_t n_out = (int64_t)g.nlat_o * g.nlon_o;
     const PItem it = items[item];
@@ -164,7 +172,7 @@ __global__ __launch_bounds__(TQ) void k_fused(const PItem* __restrict__ items,
 #pragma unroll
                 for (int k = 0; k < kBasis; ++k) z[c][k] = 0.0f;
             __syncthreads();  // previous users of ws / xs are done
-            for (int i = tid; i < kCIC * kBasis * COT; i += TQ) {
+            for (int i = tid; i < kCIC * kBasis * COT; i += kBlock) {
                 // ws[j][c][k]: output channel j of the tile, pass channel c, basis k
                 // (bf16 storage: the raw bf16 values, packed two per word).
                 const int j = i / (kCIC * kBasis), ck = i % (kCIC * kBasis), c = ck / kBasis, k = ck % kBasis;
@@ -184,7 +192,7 @@ __global__ __launch_bounds__(TQ) void k_fused(const PItem* __restrict__ items,
                     const PSpan S = spans[sp];
                     int start = (g.stride * q0 + S.dstart) % g.nlon_i;
                     if (start < 0) start += g.nlon_i;
-                    for (int j = tid; j < S.len; j += TQ) {
+                    for (int j = tid; j < S.len; j += kBlock) {
                         int idx = start + j;
                         if (idx >= g.nlon_i) idx = idx % g.nlon_i;
 #pragma unroll
@@ -202,7 +210,7 @@ __global__ __launch_bounds__(TQ) void k_fused(const PItem* __restrict__ items,
                 }
                 {
                     const int ebase = C.cls[0], ne = C.cls[kCells] - C.cls[0];
-                    for (int i = tid; i < ne; i += TQ) {
+                    for (int i = tid; i < ne; i += kBlock) {
                         eoffs[i] = offs[ebase + i];
                         const PVal pv = vals[ebase + i];
                         evs[i] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
@@ -211,23 +219,26 @@ __global__ __launch_bounds__(TQ) void k_fused(const PItem* __restrict__ items,
                 __syncthreads();
                 // Waves whose output longitudes all lie past the ring's end
                 // stage but do not gather.
-                if (q0 + (tid & ~63) >= g.nq) continue;
-                run_cell<0>(C.cls[0] - C.cls[0], C.cls[1] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<1>(C.cls[1] - C.cls[0], C.cls[2] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<2>(C.cls[2] - C.cls[0], C.cls[3] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<3>(C.cls[3] - C.cls[0], C.cls[4] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<4>(C.cls[4] - C.cls[0], C.cls[5] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<5>(C.cls[5] - C.cls[0], C.cls[6] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<6>(C.cls[6] - C.cls[0], C.cls[7] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<7>(C.cls[7] - C.cls[0], C.cls[8] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<8>(C.cls[8] - C.cls[0], C.cls[9] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<9>(C.cls[9] - C.cls[0], C.cls[10] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<10>(C.cls[10] - C.cls[0], C.cls[11] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<11>(C.cls[11] - C.cls[0], C.cls[12] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<12>(C.cls[12] - C.cls[0], C.cls[13] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<13>(C.cls[13] - C.cls[0], C.cls[14] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<14>(C.cls[14] - C.cls[0], C.cls[15] - C.cls[0], eoffs, evs, xs, lane_col, z);
-                run_cell<15>(C.cls[15] - C.cls[0], C.cls[16] - C.cls[0], eoffs, evs, xs, lane_col, z);
+                if (q0 + (lane & ~63) >= g.nq) continue;
+                const int ne = C.cls[kCells] - C.cls[0];
+                const int lo = ne * part / kParts, hi = ne * (part + 1) / kParts;
+                auto share = [&](int c) { return C.cls[c] - C.cls[0] < lo ? lo : C.cls[c] - C.cls[0] > hi ? hi : C.cls[c] - C.cls[0]; };
+                run_cell<0>(share(0), share(1), eoffs, evs, xs, lane_col, z);
+                run_cell<1>(share(1), share(2), eoffs, evs, xs, lane_col, z);
+                run_cell<2>(share(2), share(3), eoffs, evs, xs, lane_col, z);
+                run_cell<3>(share(3), share(4), eoffs, evs, xs, lane_col, z);
+                run_cell<4>(share(4), share(5), eoffs, evs, xs, lane_col, z);
+                run_cell<5>(share(5), share(6), eoffs, evs, xs, lane_col, z);
+                run_cell<6>(share(6), share(7), eoffs, evs, xs, lane_col, z);
+                run_cell<7>(share(7), share(8), eoffs, evs, xs, lane_col, z);
+                run_cell<8>(share(8), share(9), eoffs, evs, xs, lane_col, z);
+                run_cell<9>(share(9), share(10), eoffs, evs, xs, lane_col, z);
+                run_cell<10>(share(10), share(11), eoffs, evs, xs, lane_col, z);
+                run_cell<11>(share(11), share(12), eoffs, evs, xs, lane_col, z);
+                run_cell<12>(share(12), share(13), eoffs, evs, xs, lane_col, z);
+                run_cell<13>(share(13), share(14), eoffs, evs, xs, lane_col, z);
+                run_cell<14>(share(14), share(15), eoffs, evs, xs, lane_col, z);
+                run_cell<15>(share(15), share(16), eoffs, evs, xs, lane_col, z);
             }
             if (sg.chunk_begin == sg.chunk_end) __syncthreads();  // ws visible
             // Contraction of this pass on the matrix cores:
@@ -273,7 +284,25 @@ __global__ __launch_bounds__(TQ) void k_fused(const PItem* __restrict__ items,
                 }
             }
         }
-        if (q < g.nq) {
+        if constexpr (kParts > 1) {
+            // The groups' outputs, summed in group order through LDS (the
+            // staging buffer, free until the next segment's first barrier).
+            float* red = (float*)xs;
+            static_assert((kParts - 1) * COT * TQ <= kNCQ * kLdsCols * 4, "reduction fits the staging buffer");
+            __syncthreads();  // the contraction's reads of ws and the gather's of xs are done
+            if (part > 0) {
+#pragma unroll
+                for (int j = 0; j < COT; ++j) red[((part - 1) * COT + j) * TQ + lane] = yacc[j / 4][j % 4];
+            }
+            __syncthreads();
+            if (part == 0) {
+#pragma unroll
+                for (int p = 1; p < kParts; ++p)
+#pragma unroll
+                    for (int j = 0; j < COT; ++j) yacc[j / 4][j % 4] += red[((p - 1) * COT + j) * TQ + lane];
+            }
+        }
+        if (part == 0 && q < g.nq) {
             const int to = sg.pattern / g.P, r = sg.pattern - (sg.pattern / g.P) * g.P;
             if (sg.slot < 0) {
                 const int64_t pix = (int64_t)to * g.nlon_o + (int64_t)q * g.P + r;
@@ -320,7 +349,7 @@ hipError_t fused_launch_tq(const ExecArgs& a, const PackedDev& P, float* partial
     const int n_cot = (a.Co + COT - 1) / COT;
     dim3 grid((unsigned)(P.n_items * n_qtiles), (unsigned)(a.B * n_cot));
     int tk = timing_begin("fused_gather_contract", a.stream);
-    hipLaunchKernelGGL((k_fused<T, COT, TQ>), grid, dim3(TQ), 0, a.stream, P.items, P.segs, P.chunks,
+    hipLaunchKernelGGL((k_fused<T, COT, TQ>), grid, dim3(kBlock), 0, a.stream, P.items, P.segs, P.chunks,
                        P.spans, P.offs, P.vals, g, (const T*)a.x, (const T*)a.w, (T*)a.y, partial, a.Ci,
                        a.Co, n_qtiles, n_cot, a.w_trans);
     timing_end(tk, a.stream);
