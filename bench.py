@@ -211,7 +211,8 @@ def load_traffic(kernel, workload):
     return float(kv["hbm_bytes_per_launch"])
 
 
-COUNTER_SET = ("MfmaUtil", "VALUBusy", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_WAIT_ANY", "SQ_WAVE_CYCLES")
+COUNTER_SET = ("MfmaUtil", "VALUBusy", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_WAIT_ANY", "SQ_WAVE_CYCLES",
+               "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_VALU_MFMA_COEXEC_CYCLES")
 
 
 def counters_path(kernel, workload):
@@ -255,11 +256,14 @@ def counter_summary(csv_path, kernel, workload, commands):
              "# mfma_busy = MfmaUtil / 100: SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs)",
              "# valu_busy = VALUBusy / 100: SQ_ACTIVE_INST_VALU / (GRBM_GUI_ACTIVE x CUs)",
              "# wait_frac = SQ_WAIT_ANY / SQ_WAVE_CYCLES: share of wave cycles spent waiting",
+             "# mfma_valu_coexec = SQ_VALU_MFMA_COEXEC_CYCLES / SQ_VALU_MFMA_BUSY_CYCLES: share of the",
+             "#   matrix cores' busy cycles in which a VALU instruction issued beside them",
              "kernel: %s" % kernel, "workload: %s" % workload,
              "library_source_sha256_16: %s" % kernel_source_digest(),
              "mfma_busy: %.4f" % (avg["MfmaUtil"] / 100.0),
              "valu_busy: %.4f" % (avg["VALUBusy"] / 100.0),
              "wait_frac: %.4f" % (avg["SQ_WAIT_ANY"] / max(avg["SQ_WAVE_CYCLES"], 1.0)),
+             "mfma_valu_coexec: %.4f" % (avg["SQ_VALU_MFMA_COEXEC_CYCLES"] / max(avg["SQ_VALU_MFMA_BUSY_CYCLES"], 1.0)),
              "SQ_INSTS_VALU_per_dispatch: %.0f" % avg["SQ_INSTS_VALU"],
              "SQ_INSTS_MFMA_per_dispatch: %.0f" % avg["SQ_INSTS_MFMA"],
              "commands:"] + ["    " + c for c in commands]
