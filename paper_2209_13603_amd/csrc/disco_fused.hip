@@ -86,37 +86,45 @@ __device__ __forceinline__ void fma_cell(const float4& v, const float4 (&xv)[kNC
         }
 }
 
-// Entries [eb, ee) of one cell, all staged in LDS; four at a time so that
-// the LDS reads of several entries are in flight together.
+constexpr int kEntryPad = 3;  // padding entries after a chunk's entries (lookahead reads)
+
+// Entries [e, ee) of one cell, with the input and values of the next entry
+// already in flight while an entry's FMAs run.  On entry (and on return) x0
+// and v0 hold the input and values of entry e and o1 the LDS column offset of
+// entry e + 1; entries are taken in pairs so that the two register sets swap
+// roles statically instead of being copied.  A lane group's entries are
+// contiguous across cells, so the lookahead runs across cell boundaries (and
+// into the next group's entries or the kEntryPad padding entries after the
+// chunk, which are read but never used).  The scheduling barriers keep the
+// next entry's LDS reads above the current entry's FMAs.
 template <int CELL>
-__device__ __forceinline__ void run_cell(int eb, int ee, const int* __restrict__ eoffs,
-                                         const float4* __restrict__ evs,
-                                         const float4* __restrict__ xs, int lane_col,
-                                         float (&z)[kCIC][kBasis]) {
-    int e = eb;
-    for (; e + 4 <= ee; e += 4) {
-        int o[4];
-        float4 v[4];
+__device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], float4& v0, int& o1,
+                                         const int* __restrict__ eoffs, const float4* __restrict__ evs,
+                                         const float4* __restrict__ xs, int lane_col, float (&z)[kCIC][kBasis]) {
+    for (; e + 1 < ee; e += 2) {
+        float4 x1[kNCQ];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            o[u] = eoffs[e + u];
-            v[u] = evs[e + u];
-        }
-        float4 xv[4][kNCQ];
+        for (int g = 0; g < kNCQ; ++g) x1[g] = xs[g * kLdsCols + lane_col + o1];
+        const float4 v1 = evs[e + 1];
+        const int o2 = eoffs[e + 2];
+        __builtin_amdgcn_sched_barrier(0);
+        fma_cell<CELL>(v0, x0, z);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int g = 0; g < kNCQ; ++g) xv[u][g] = xs[g * kLdsCols + lane_col + o[u]];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) fma_cell<CELL>(v[u], xv[u], z);
+        for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kLdsCols + lane_col + o2];
+        v0 = evs[e + 2];
+        o1 = eoffs[e + 3];
+        __builtin_amdgcn_sched_barrier(0);
+        fma_cell<CELL>(v1, x1, z);
+        __builtin_amdgcn_sched_barrier(0);
     }
-    for (; e < ee; ++e) {
-        const int o = eoffs[e];
-        const float4 v = evs[e];
-        float4 xv[kNCQ];
+    if (e < ee) {
+        fma_cell<CELL>(v0, x0, z);
 #pragma unroll
-        for (int g = 0; g < kNCQ; ++g) xv[g] = xs[g * kLdsCols + lane_col + o];
-        fma_cell<CELL>(v, xv, z);
+        for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kLdsCols + lane_col + o1];
+        v0 = evs[e + 1];
+        o1 = eoffs[e + 2];
+        ++e;
     }
 }
 
@@ -138,8 +146,8 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
                                                   int Ci, int Co, int n_qtiles, int n_cotiles,
                                                   bool w_trans) {
     __shared__ float4 xs[kNCQ * kLdsCols];
-    __shared__ float4 evs[kChunkEntries];
-    __shared__ int eoffs[kChunkEntries];
+    __shared__ float4 evs[kChunkEntries + kEntryPad];
+    __shared__ int eoffs[kChunkEntries + kEntryPad];
     __shared__ float ws[kCIC * kBasis * COT];
     constexpr bool kBf16 = sizeof(T) == 2;
 
@@ -215,6 +223,10 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
                         const PVal pv = vals[ebase + i];
                         evs[i] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
                     }
+                    if (tid < kEntryPad) {
+                        eoffs[ne + tid] = 0;
+                        evs[ne + tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                    }
                 }
                 __syncthreads();
                 // Waves whose output longitudes all lie past the ring's end
@@ -223,22 +235,30 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
                 const int ne = C.cls[kCells] - C.cls[0];
                 const int lo = ne * part / kParts, hi = ne * (part + 1) / kParts;
                 auto share = [&](int c) { return C.cls[c] - C.cls[0] < lo ? lo : C.cls[c] - C.cls[0] > hi ? hi : C.cls[c] - C.cls[0]; };
-                run_cell<0>(share(0), share(1), eoffs, evs, xs, lane_col, z);
-                run_cell<1>(share(1), share(2), eoffs, evs, xs, lane_col, z);
-                run_cell<2>(share(2), share(3), eoffs, evs, xs, lane_col, z);
-                run_cell<3>(share(3), share(4), eoffs, evs, xs, lane_col, z);
-                run_cell<4>(share(4), share(5), eoffs, evs, xs, lane_col, z);
-                run_cell<5>(share(5), share(6), eoffs, evs, xs, lane_col, z);
-                run_cell<6>(share(6), share(7), eoffs, evs, xs, lane_col, z);
-                run_cell<7>(share(7), share(8), eoffs, evs, xs, lane_col, z);
-                run_cell<8>(share(8), share(9), eoffs, evs, xs, lane_col, z);
-                run_cell<9>(share(9), share(10), eoffs, evs, xs, lane_col, z);
-                run_cell<10>(share(10), share(11), eoffs, evs, xs, lane_col, z);
-                run_cell<11>(share(11), share(12), eoffs, evs, xs, lane_col, z);
-                run_cell<12>(share(12), share(13), eoffs, evs, xs, lane_col, z);
-                run_cell<13>(share(13), share(14), eoffs, evs, xs, lane_col, z);
-                run_cell<14>(share(14), share(15), eoffs, evs, xs, lane_col, z);
-                run_cell<15>(share(15), share(16), eoffs, evs, xs, lane_col, z);
+                // Prime: entry lo in (x0, v0), the offset of entry lo + 1 in o1.
+                int e = lo;
+                float4 x0[kNCQ];
+                const int o0 = eoffs[e];
+#pragma unroll
+                for (int gq = 0; gq < kNCQ; ++gq) x0[gq] = xs[gq * kLdsCols + lane_col + o0];
+                float4 v0 = evs[e];
+                int o1 = eoffs[e + 1];
+                run_cell<0>(e, share(1), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<1>(e, share(2), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<2>(e, share(3), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<3>(e, share(4), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<4>(e, share(5), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<5>(e, share(6), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<6>(e, share(7), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<7>(e, share(8), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<8>(e, share(9), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<9>(e, share(10), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<10>(e, share(11), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<11>(e, share(12), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<12>(e, share(13), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<13>(e, share(14), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<14>(e, share(15), x0, v0, o1, eoffs, evs, xs, lane_col, z);
+                run_cell<15>(e, share(16), x0, v0, o1, eoffs, evs, xs, lane_col, z);
             }
             if (sg.chunk_begin == sg.chunk_end) __syncthreads();  // ws visible
             // Contraction of this pass on the matrix cores:

@@ -92,6 +92,10 @@ int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& sk
         return DISCO_ERR_UNSUPPORTED;
     }
     const int max_extent = kLdsCols - halo;  // max (d_last - d_first + 1) of one piece
+    // Entries of one chunk: the work-item target times the lane groups that
+    // share a chunk (tiles narrower than a workgroup), at most kChunkEntries,
+    // so that no chunk outweighs the work items by more than that.
+    const int chunk_cap = std::max(1, std::min(kChunkEntries, target_entries * (kTileQ / tile)));
     PackedHost P;
     P.tile = tile;
     std::vector<int32_t> pattern_seg_count(g.n_patterns(), 0);
@@ -104,7 +108,7 @@ int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& sk
         for (int32_t e = e0; e < e1; ++e) {
             const int32_t ti = op.t_in[(size_t)e], dr = op.d_raw[(size_t)e];
             if (!pieces.empty() && pieces.back().ti == ti && dr - pieces.back().d_first + 1 <= max_extent &&
-                dr > pieces.back().d_last && pieces.back().n() < kChunkEntries) {
+                dr > pieces.back().d_last && pieces.back().n() < chunk_cap) {
                 pieces.back().d_last = dr;
                 pieces.back().e_end = e + 1;
             } else {
@@ -117,7 +121,7 @@ int pack_op(const HostOp& op, int target_entries, const std::vector<uint8_t>& sk
         for (int i = 0; i < (int)pieces.size(); ++i) {
             const int len = halo + pieces[(size_t)i].d_last - pieces[(size_t)i].d_first + 1;
             const int ne = pieces[(size_t)i].n();
-            if (chunk_pieces.empty() || used + len > kLdsCols || used_e + ne > kChunkEntries) {
+            if (chunk_pieces.empty() || used + len > kLdsCols || used_e + ne > chunk_cap) {
                 chunk_pieces.push_back({i, i + 1});
                 used = len;
                 used_e = ne;
