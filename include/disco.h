@@ -192,7 +192,12 @@ typedef struct {
  * flags, NULL plan_out), UNSUPPORTED (longitude ratio not an
  * integer, unknown basis, sampling or quadrature, cell areas on the
  * pole-including grid), OUT_OF_MEMORY, DEVICE.  On success *plan_out owns the device
- * memory until disco_plan_destroy. */
+ * memory until disco_plan_destroy.
+ * With DISCO_LOG=1 in the environment the plan's statistics go to stderr
+ * (per op: patterns, stored entries, non-zero triples, the largest window,
+ * full-ring windows, compressed psi; then the schedule's structure, device
+ * bytes and build time).  This call, the ops and the gradients each run
+ * inside a roctx range named after them (rocprofv3 --marker-trace). */
 disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlon_out,
                                  double theta_c, const disco_basis_t* basis,
                                  disco_plan_t* plan_out);
@@ -349,6 +354,16 @@ disco_status_t disco_psi_entries(int nlat_in, int nlon_in, int nlat_out, int nlo
 disco_status_t disco_kernel_timing_enable(int32_t on);
 disco_status_t disco_kernel_timing_read(int32_t capacity, char* names, int64_t* launches,
                                         double* total_ms, int32_t* count);
+
+/* Range checks of the psi indices, for a library built with
+ * DISCO_DEBUG_BOUNDS (python -m paper_2209_13603_amd.build --debug-bounds
+ * writes libdisco_debug_bounds.so): the kernels check every LDS index they
+ * derive from the stored entries (input columns, entry slots, staged
+ * elements) against the buffer it indexes and record a failure.  Waits for
+ * the current device, then returns the number of kernel files (sweep,
+ * general, matrix-core, stencil) that recorded one since the last call and
+ * clears them; -1 for a library built without the checks. */
+int32_t disco_debug_bounds_violations(void);
 
 /* Algorithmic work of the kernels that one call of disco_forward_algo
  * (transpose == 0) or disco_transpose_algo (transpose != 0) with `algo`,

@@ -2,9 +2,13 @@
 // argument validation, plan construction and upload, workspace management
 // and dispatch to the kernels.  Validation is synchronous and happens before
 // anything is enqueued; a failed call enqueues nothing.
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <cmath>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <map>
@@ -16,6 +20,41 @@
 #include "disco_internal.h"
 
 using namespace disco;
+
+namespace {
+
+// A roctx range around a library call (plan creation, an op, a gradient),
+// seen by rocprofv3 --marker-trace; without a profiler it costs a call.
+struct TraceRange {
+    explicit TraceRange(const char* name) { roctxRangePushA(name); }
+    ~TraceRange() { roctxRangePop(); }
+    TraceRange(const TraceRange&) = delete;
+    TraceRange& operator=(const TraceRange&) = delete;
+};
+
+// DISCO_LOG=1 in the environment: plan statistics on stderr.
+bool log_enabled() {
+    static const bool on = [] {
+        const char* v = std::getenv("DISCO_LOG");
+        return v && v[0] && std::strcmp(v, "0") != 0;
+    }();
+    return on;
+}
+
+void log_host_op(const char* name, const HostOp& h) {
+    const OpGeom& g = h.g;
+    const int K = basis_size(h.basis);
+    const double compressed = (double)h.t_in.size() * (8 + 4 * K) + 4.0 * (double)h.pat_ptr.size();
+    std::fprintf(stderr,
+                 "disco: %s op %dx%d -> %dx%d: %d patterns (%d rings x %d phases, stride %d), %lld stored entries, "
+                 "%lld non-zero (pixel pair, k) triples, largest window %d entries, %d full-ring windows, "
+                 "compressed psi %.2f MB\n",
+                 name, g.nlat_i, g.nlon_i, g.nlat_o, g.nlon_o, g.n_patterns(), g.nlat_o, g.P, g.stride,
+                 (long long)h.t_in.size(), (long long)h.nnz_pairs, h.max_window, h.full_ring_windows,
+                 compressed / 1e6);
+}
+
+}  // namespace
 
 struct disco_plan {
     int device = 0;
@@ -626,6 +665,8 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
 
 disco_status_t run(disco_plan_t plan, const disco_tensor_t* x, const disco_tensor_t* w,
                    disco_tensor_t* y, hipStream_t stream, int32_t algo, bool transpose, bool depthwise = false) {
+    TraceRange range(transpose ? (depthwise ? "disco_transpose_depthwise" : "disco_transpose")
+                               : (depthwise ? "disco_forward_depthwise" : "disco_forward"));
     if (!plan) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan is NULL");
     return run_op(plan, transpose ? plan->tr : plan->fwd, transpose, x, w, y, stream, algo, depthwise);
 }
@@ -930,6 +971,7 @@ disco_status_t run_op(disco_plan_t plan, const DeviceOp& op, bool transpose, con
 disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t* x, const disco_tensor_t* w,
                         const disco_tensor_t* dy, disco_tensor_t* dx, disco_tensor_t* dw, hipStream_t stream,
                         bool depthwise = false) {
+    TraceRange range(transpose ? "disco_transpose_backward" : "disco_forward_backward");
     if (!plan) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (!(plan->params.flags & DISCO_PLAN_BACKWARD))
         return fail(DISCO_ERR_UNSUPPORTED, "plan was created without DISCO_PLAN_BACKWARD");
@@ -1101,6 +1143,18 @@ void timing_end(int token, hipStream_t s) {
 
 extern "C" {
 
+int32_t disco_debug_bounds_violations(void) {
+#ifdef DISCO_DEBUG_BOUNDS
+    (void)hipDeviceSynchronize();
+    int32_t n = 0;
+    for (unsigned int f : {bounds_flag_sweep(), bounds_flag_fused(), bounds_flag_mfma(), bounds_flag_stencil()})
+        n += f != 0u;
+    return n;
+#else
+    return -1;
+#endif
+}
+
 disco_status_t disco_kernel_timing_enable(int32_t on) {
     g_timing_on.store(on != 0);
     return ok();
@@ -1145,6 +1199,8 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
                                  const disco_basis_t* basis, disco_plan_t* plan_out) {
     if (!plan_out) return fail(DISCO_ERR_INVALID_ARGUMENT, "plan_out is NULL");
     *plan_out = nullptr;
+    TraceRange range("disco_plan_create");
+    const auto t0 = std::chrono::steady_clock::now();
     PlanParams p{};
     disco_status_t s = resolve_params(nlat_in, nlon_in, nlat_out, nlon_out, theta_c, basis, &p);
     if (s != DISCO_OK) return s;
@@ -1160,6 +1216,16 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
         if (rc != DISCO_OK) return fail((disco_status_t)rc, err);
     } catch (const std::bad_alloc&) {
         return fail(DISCO_ERR_OUT_OF_MEMORY, "host allocation failed while building psi");
+    }
+    if (log_enabled()) {
+        std::fprintf(stderr, "disco: plan theta_c %.6g, basis %d, quadrature %d, sampling %d, node spacing %.6g\n",
+                     p.theta_c, p.basis, p.quadrature, p.sampling, p.h);
+        log_host_op("forward", hf);
+        log_host_op("transpose", ht);
+        if (with_backward) {
+            log_host_op("forward adjoint", hfa);
+            log_host_op("transpose adjoint", hta);
+        }
     }
     disco_plan* plan = new (std::nothrow) disco_plan();
     if (!plan) return fail(DISCO_ERR_OUT_OF_MEMORY, "host allocation failed");
@@ -1262,6 +1328,17 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
         const OpTables* T = d->tables.get();
         if (!T && d->bytes == 0) continue;  // an adjoint the plan does not have
         I.psi_bytes_all_layouts += T ? 64 + T->bytes[0] + T->bytes[1] + T->bytes[2] + T->bytes[3] : d->bytes;
+    }
+    if (log_enabled()) {
+        int64_t live = 0;
+        for (const DeviceOp* d : {&plan->fwd, &plan->tr, &plan->fwd_adj, &plan->tr_adj}) live += d->bytes;
+        const double sec = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+        std::fprintf(stderr,
+                     "disco: plan built in %.3f s: forward op %d spectral rings, %d sweep patterns; transpose op %d "
+                     "spectral rings, %d sweep patterns; device tables %.2f MB now (%s), %.2f MB with every layout\n",
+                     sec, I.spectral_rings_forward, I.sweep_patterns_forward, I.spectral_rings_transpose,
+                     I.sweep_patterns_transpose, live / 1e6, eager ? "all layouts" : "the rest on first use",
+                     I.psi_bytes_all_layouts / 1e6);
     }
     *plan_out = plan;
     return ok();

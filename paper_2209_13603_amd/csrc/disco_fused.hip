@@ -29,6 +29,8 @@ namespace disco {
 
 namespace {
 
+DISCO_BOUNDS_FLAG
+
 constexpr int kBlock = kTileQ;
 constexpr int kNCQ = kCIC / 4;  // float4 channel groups per pass
 typedef float v4f __attribute__((ext_vector_type(4)));
@@ -103,6 +105,7 @@ __device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], flo
                                          const float4* __restrict__ xs, int lane_col, float (&z)[kCIC][kBasis]) {
     for (; e + 1 < ee; e += 2) {
         float4 x1[kNCQ];
+        DISCO_CHECK(lane_col + o1 >= 0 && lane_col + o1 < kLdsCols && e + 3 < kChunkEntries + kEntryPad);
 #pragma unroll
         for (int g = 0; g < kNCQ; ++g) x1[g] = xs[g * kLdsCols + lane_col + o1];
         const float4 v1 = evs[e + 1];
@@ -110,6 +113,7 @@ __device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], flo
         __builtin_amdgcn_sched_barrier(0);
         fma_cell<CELL>(v0, x0, z);
         __builtin_amdgcn_sched_barrier(0);
+        DISCO_CHECK(lane_col + o2 >= 0 && lane_col + o2 < kLdsCols);
 #pragma unroll
         for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kLdsCols + lane_col + o2];
         v0 = evs[e + 2];
@@ -120,6 +124,7 @@ __device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], flo
     }
     if (e < ee) {
         fma_cell<CELL>(v0, x0, z);
+        DISCO_CHECK(lane_col + o1 >= 0 && lane_col + o1 < kLdsCols && e + 2 < kChunkEntries + kEntryPad);
 #pragma unroll
         for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kLdsCols + lane_col + o1];
         v0 = evs[e + 1];
@@ -212,6 +217,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
                             v.y = c + 1 < Ci ? load_val(xp, (int64_t)(c + 1) * n_in) : 0.0f;
                             v.z = c + 2 < Ci ? load_val(xp, (int64_t)(c + 2) * n_in) : 0.0f;
                             v.w = c + 3 < Ci ? load_val(xp, (int64_t)(c + 3) * n_in) : 0.0f;
+                            DISCO_CHECK(S.lds_base + j >= 0 && S.lds_base + j < kLdsCols);
                             xs[gq * kLdsCols + S.lds_base + j] = v;
                         }
                     }
@@ -219,6 +225,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
                 {
                     const int ebase = C.cls[0], ne = C.cls[kCells] - C.cls[0];
                     for (int i = tid; i < ne; i += kBlock) {
+                        DISCO_CHECK(i < kChunkEntries);
                         eoffs[i] = offs[ebase + i];
                         const PVal pv = vals[ebase + i];
                         evs[i] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
@@ -239,6 +246,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const PItem* __restrict__ item
                 int e = lo;
                 float4 x0[kNCQ];
                 const int o0 = eoffs[e];
+                DISCO_CHECK(lane_col + o0 >= 0 && lane_col + o0 < kLdsCols);
 #pragma unroll
                 for (int gq = 0; gq < kNCQ; ++gq) x0[gq] = xs[gq * kLdsCols + lane_col + o0];
                 float4 v0 = evs[e];
@@ -395,6 +403,8 @@ hipError_t fused_dispatch(const ExecArgs& a, const PackedDev& P, float* partial)
 }
 
 }  // namespace
+
+DISCO_BOUNDS_READER(bounds_flag_fused)
 
 hipError_t launch_reduce_partials(const ExecArgs& a, const PackedDev& P, const float* partial) {
     const OpGeom& g = a.op->g;

@@ -12,6 +12,36 @@
 
 #include "disco.h"
 
+// Device-side range checks of the psi indices against the buffers they
+// index (a build with -DDISCO_DEBUG_BOUNDS; the default build has none).
+// Each kernel file keeps a flag that a failed check sets; the flags are read
+// and cleared through disco_debug_bounds_violations().  A check reports, it
+// does not skip the access: the accesses it covers are LDS reads and writes
+// inside the workgroup's allocation by the layouts' construction, which is
+// what the check verifies.
+#ifdef DISCO_DEBUG_BOUNDS
+#define DISCO_BOUNDS_FLAG static __device__ unsigned int disco_bounds_flag = 0u;
+#define DISCO_CHECK(cond)                                        \
+    do {                                                         \
+        if (!(cond)) atomicOr(&disco_bounds_flag, 1u);           \
+    } while (0)
+#define DISCO_BOUNDS_READER(fn)                                                              \
+    unsigned int fn() {                                                                      \
+        unsigned int v = 0u, z = 0u;                                                         \
+        if (hipMemcpyFromSymbol(&v, HIP_SYMBOL(disco_bounds_flag), sizeof(v)) != hipSuccess) \
+            v = 1u;                                                                          \
+        (void)hipMemcpyToSymbol(HIP_SYMBOL(disco_bounds_flag), &z, sizeof(z));              \
+        return v;                                                                            \
+    }
+#else
+#define DISCO_BOUNDS_FLAG
+#define DISCO_CHECK(cond) \
+    do {                  \
+    } while (0)
+#define DISCO_BOUNDS_READER(fn) \
+    unsigned int fn() { return 0u; }
+#endif
+
 namespace disco {
 
 // Values stored per psi entry: the nine functions of the 3x3 basis, the four
@@ -507,6 +537,12 @@ size_t weight_grad_ws_bytes(int B, int M, int N, int64_t P);
 // Zeros `bytes` (a multiple of 2) of device memory with a kernel (no memset
 // node when the caller captures a graph).
 hipError_t launch_zero_fill(void* p, size_t bytes, hipStream_t s);
+// The range-check flags of the kernel files (0 without DISCO_DEBUG_BOUNDS);
+// each call reads and clears its file's flag.
+unsigned int bounds_flag_sweep();
+unsigned int bounds_flag_fused();
+unsigned int bounds_flag_mfma();
+unsigned int bounds_flag_stencil();
 // Depthwise dW[c][k] = sum_{b,p} dy[b][c][p] Zs[b][c][k][p] (K <= 16), partials
 // in ws (weight_grad_ws_bytes_dw), reduced in a fixed order.
 size_t weight_grad_ws_bytes_dw(int B, int C, int K, int64_t P);

@@ -29,6 +29,8 @@ namespace disco {
 
 namespace {
 
+DISCO_BOUNDS_FLAG
+
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef float f8 __attribute__((ext_vector_type(8)));
@@ -229,6 +231,7 @@ __global__ __launch_bounds__(kMfmaTile, 2) void k_mfma(const MSeg* __restrict__ 
             // One chunk: its LDS reads, then its products (the first chunk
             // starts the accumulators from zero).
             auto chunk = [&](int c, bool first) {
+                DISCO_CHECK(hs[4 * c + gq] >= 0 && s * lq + hs[4 * c + gq] + 16 * s * (kNB - 1) + 6 < kMfmaMaxElems);
                 const uint32_t* xb = xc + hs[4 * c + gq];
                 bf8 A[NPH];
 #pragma unroll
@@ -327,6 +330,8 @@ hipError_t mfma_launch(const ExecArgs& a, const uint4* wop, float* partial) {
 }
 
 }  // namespace
+
+DISCO_BOUNDS_READER(bounds_flag_mfma)
 
 size_t workspace_bytes_mfma(const ExecArgs& a) {
     return mfma_wop_bytes(a) + sizeof(float) * (size_t)a.op->mfma.P.n_slots * a.B * a.Co * a.op->g.nq;

@@ -40,6 +40,8 @@ namespace disco {
 
 namespace {
 
+DISCO_BOUNDS_FLAG
+
 constexpr int kBlock = kTileQ;
 
 __device__ __forceinline__ float load_val(const float* p, int64_t i) { return p[i]; }
@@ -139,6 +141,7 @@ __global__ __launch_bounds__(TQ) void k_stencil(const PItem* __restrict__ items,
                     for (int j = tid; j < S.len; j += TQ) {
                         int idx = start + j;
                         if (idx >= g.nlon_i) idx = idx % g.nlon_i;
+                        DISCO_CHECK(S.lds_base + j >= 0 && S.lds_base + j < kLdsCols);
                         xs[S.lds_base + j] = load_val(xc, (int64_t)S.row + idx);
                     }
                 }
@@ -160,6 +163,8 @@ __global__ __launch_bounds__(TQ) void k_stencil(const PItem* __restrict__ items,
                 int e = 0;
                 for (; e + 4 <= ne; e += 4) {
                     const int4 o = *(const int4*)(eoffs + e);
+                    DISCO_CHECK(lane_col + o.x >= 0 && lane_col + o.x < kLdsCols && lane_col + o.y >= 0 && lane_col + o.y < kLdsCols &&
+                                lane_col + o.z >= 0 && lane_col + o.z < kLdsCols && lane_col + o.w >= 0 && lane_col + o.w < kLdsCols);
                     const float x0 = xs[lane_col + o.x], x1 = xs[lane_col + o.y];
                     const float x2 = xs[lane_col + o.z], x3 = xs[lane_col + o.w];
 #pragma unroll
@@ -171,6 +176,7 @@ __global__ __launch_bounds__(TQ) void k_stencil(const PItem* __restrict__ items,
                     }
                 }
                 for (; e < ne; ++e) {
+                    DISCO_CHECK(lane_col + eoffs[e] >= 0 && lane_col + eoffs[e] < kLdsCols);
                     const float xv = xs[lane_col + eoffs[e]];
 #pragma unroll
                     for (int j = 0; j < COT; ++j) acc[j] = fmaf(ew[e * COT + j], xv, acc[j]);
@@ -353,6 +359,7 @@ __global__ __launch_bounds__(TILE / 4) void k_stencil_blocked(const PItem* __res
                     // ahead (the span and the weight table carry one spare
                     // block for the last).
                     const int xb = (S.lds_base >> 2) + tid;
+                    DISCO_CHECK(xb >= 0 && xb + S.nblk + 1 < kCols / 4 && cb + S.nblk < kEntries / 4 + 1);
                     float4 V0 = xs4[xb], V1 = xs4[xb + 1];
                     float4 c = ew4[cb];
 #pragma unroll 2
@@ -402,6 +409,8 @@ hipError_t stencil_blocked_launch(const ExecArgs& a, const StencilDev& S, float*
 }
 
 }  // namespace
+
+DISCO_BOUNDS_READER(bounds_flag_stencil)
 
 hipError_t launch_stencil_blocked(const ExecArgs& a, const StencilDev& S, float* partial_ws) {
     if (S.tile == kStencilSmallTile)

@@ -31,6 +31,8 @@ namespace disco {
 
 namespace {
 
+DISCO_BOUNDS_FLAG
+
 constexpr int kBlock = kSweepTile;
 constexpr int kNCQ = kCIC / 4;
 constexpr int kPF = (kBlock + 8 + kBlock - 1) / kBlock;  // prefetched span columns per lane
@@ -155,6 +157,7 @@ __device__ __forceinline__ void entry_one(int e, float4 (&x0)[kNCQ], float4& v0,
                                           const int* __restrict__ eoffs, const float4* __restrict__ evs,
                                           const float4* __restrict__ xs, int lane_col, float (&z)[kCIC][kBasis]) {
     fma_cell<G>(v0, x0, z);
+    DISCO_CHECK(lane_col + o1 >= 0 && lane_col + o1 < kSweepCols && e + 2 < kSweepEntries + kEntryPad);
 #pragma unroll
     for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kSweepCols + lane_col + o1];
     v0 = evs[e + 1];
@@ -167,6 +170,7 @@ __device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], flo
                                          const float4* __restrict__ xs, int lane_col, float (&z)[kCIC][kBasis]) {
     for (; e + 1 < ee; e += 2) {
         float4 x1[kNCQ];
+        DISCO_CHECK(lane_col + o1 >= 0 && lane_col + o1 < kSweepCols && e + 3 < kSweepEntries + kEntryPad);
 #pragma unroll
         for (int g = 0; g < kNCQ; ++g) x1[g] = xs[g * kSweepCols + lane_col + o1];
         const float4 v1 = evs[e + 1];
@@ -174,6 +178,7 @@ __device__ __forceinline__ void run_cell(int& e, int ee, float4 (&x0)[kNCQ], flo
         __builtin_amdgcn_sched_barrier(0);
         fma_cell<G>(v0, x0, z);
         __builtin_amdgcn_sched_barrier(0);
+        DISCO_CHECK(lane_col + o2 >= 0 && lane_col + o2 < kSweepCols);
 #pragma unroll
         for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kSweepCols + lane_col + o2];
         v0 = evs[e + 2];
@@ -425,6 +430,7 @@ __global__ __launch_bounds__(kBlock, COT <= 8 ? 4 : 1) void k_sweep(const SRun* 
                 for (int i = 0; i < kPF; ++i) {
                     const int j = tid + i * kBlock;
                     if (j < S.len) {
+                        DISCO_CHECK(S.lds_base + j >= 0 && S.lds_base + j < kSweepCols);
 #pragma unroll
                         for (int gq = 0; gq < kNCQ; ++gq) xs[gq * kSweepCols + S.lds_base + j] = pf[i][gq];
                     }
@@ -434,6 +440,7 @@ __global__ __launch_bounds__(kBlock, COT <= 8 ? 4 : 1) void k_sweep(const SRun* 
                 for (int j = kPF * kBlock + tid; j < S.len; j += kBlock) {
                     float4 v[kNCQ];
                     load_col(S, start, j, v);
+                    DISCO_CHECK(S.lds_base + j >= 0 && S.lds_base + j < kSweepCols);
 #pragma unroll
                     for (int gq = 0; gq < kNCQ; ++gq) xs[gq * kSweepCols + S.lds_base + j] = v[gq];
                 }
@@ -443,6 +450,7 @@ __global__ __launch_bounds__(kBlock, COT <= 8 ? 4 : 1) void k_sweep(const SRun* 
             for (int i = 0; i < kPFE; ++i) {
                 const int k = tid + i * kBlock;
                 if (k < ne) {
+                    DISCO_CHECK(k < kSweepEntries);
                     eoffs[k] = pf_off[i];
                     evs[k] = pf_val[i];
                 }
@@ -455,11 +463,13 @@ __global__ __launch_bounds__(kBlock, COT <= 8 ? 4 : 1) void k_sweep(const SRun* 
             for (int j = tid; j < S.len; j += kBlock) {
                 float4 v[kNCQ];
                 load_col(S, start, j, v);
+                DISCO_CHECK(S.lds_base + j >= 0 && S.lds_base + j < kSweepCols);
 #pragma unroll
                 for (int gq = 0; gq < kNCQ; ++gq) xs[gq * kSweepCols + S.lds_base + j] = v[gq];
             }
         }
         for (int k = (have_pf ? kPFE * kBlock : 0) + tid; k < ne; k += kBlock) {
+            DISCO_CHECK(k < kSweepEntries);
             eoffs[k] = offs[SP.ent + k];
             const PVal pv = vals[SP.ent + k];
             evs[k] = make_float4(pv.v[0], pv.v[1], pv.v[2], pv.v[3]);
@@ -480,6 +490,7 @@ __global__ __launch_bounds__(kBlock, COT <= 8 ? 4 : 1) void k_sweep(const SRun* 
         // entries when the pattern has fewer).
         float4 x0[kNCQ];
         const int o0 = eoffs[0];
+        DISCO_CHECK(lane_col + o0 >= 0 && lane_col + o0 < kSweepCols);
 #pragma unroll
         for (int g = 0; g < kNCQ; ++g) x0[g] = xs[g * kSweepCols + lane_col + o0];
         float4 v0 = evs[0];
@@ -616,6 +627,8 @@ hipError_t sweep_dispatch(const ExecArgs& a, float* y32) {
 }
 
 }  // namespace
+
+DISCO_BOUNDS_READER(bounds_flag_sweep)
 
 size_t workspace_bytes_sweep(const ExecArgs& a) {
     if (a.dtype != 1 || a.Ci <= kCIC || a.op->sweep.n_runs == 0) return 0;

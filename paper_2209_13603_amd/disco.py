@@ -57,7 +57,13 @@ EXPORTS = ("disco_plan_create", "disco_plan_destroy", "disco_plan_query", "disco
            "disco_forward_depthwise_backward", "disco_transpose_depthwise_backward",
            "disco_psi_entries", "disco_forward_noalloc",
            "disco_kernel_timing_enable", "disco_kernel_timing_read", "disco_kernel_work",
-           "disco_status_string", "disco_last_error")
+           "disco_status_string", "disco_last_error", "disco_debug_bounds_violations")
+
+
+def debug_bounds_violations() -> int:
+    """Kernel files whose psi-index range checks failed since the last call
+    (waits for the device; -1 for a library built without the checks)."""
+    return int(library().disco_debug_bounds_violations())
 
 
 class DiscoError(RuntimeError):
@@ -110,11 +116,15 @@ def _status_name(s):
     return names.get(s, "DISCO_ERR_%d" % s)
 
 
-def library(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load libdisco.so (once); raises if it has not been built."""
+def library(path: str = None) -> ctypes.CDLL:
+    """Load libdisco.so (once); raises if it has not been built.  The
+    environment variable DISCO_LIBRARY names another build of it (for
+    instance the range-checking libdisco_debug_bounds.so)."""
     global _lib
     if _lib is not None:
         return _lib
+    if path is None:
+        path = os.environ.get("DISCO_LIBRARY") or LIB_PATH
     if not os.path.exists(path):
         raise FileNotFoundError("libdisco.so not built at %s: run `python -m "
                                 "paper_2209_13603_amd.build` (there is no CPU fallback)" % path)
@@ -159,6 +169,8 @@ def library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.disco_status_string.restype = ctypes.c_char_p
     lib.disco_last_error.argtypes = []
     lib.disco_last_error.restype = ctypes.c_char_p
+    lib.disco_debug_bounds_violations.argtypes = []
+    lib.disco_debug_bounds_violations.restype = ctypes.c_int32
     _lib = lib
     return lib
 

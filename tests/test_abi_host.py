@@ -287,3 +287,44 @@ def test_pattern_count_limit():
     assert entries(65536, 2, 65536, 2) == disco.DISCO_ERR_UNSUPPORTED
     assert entries(40000, 2, 40000, 4) == disco.DISCO_ERR_UNSUPPORTED   # forward op: 2 phases x 40000 rings
     assert "65535" in lib.disco_last_error().decode()
+
+
+def _plan_stderr(env_log):
+    """stderr of a fresh process that creates a 32 x 64 plan (without a
+    device the creation stops after the host build)."""
+    import subprocess
+    import sys
+    env = dict(os.environ)
+    env.pop("DISCO_LOG", None)
+    if env_log is not None:
+        env["DISCO_LOG"] = env_log
+    code = ("import ctypes; from paper_2209_13603_amd import disco; lib = disco.library(); "
+            "h = ctypes.c_void_p(); rc = lib.disco_plan_create(32, 64, 32, 64, 3 * 3.141592653589793 / 32, None, "
+            "ctypes.byref(h)); print(rc); rc == 0 and lib.disco_plan_destroy(h)")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    return r.stderr
+
+
+def test_plan_statistics_are_logged_with_disco_log():
+    err = _plan_stderr("1")
+    fwd = [l for l in err.splitlines() if l.startswith("disco: forward op 32x64 -> 32x64")]
+    assert len(fwd) == 1, err
+    m = re.search(r"(\d+) stored entries, (\d+) non-zero .*largest window (\d+) entries, (\d+) full-ring windows, "
+                  r"compressed psi ([0-9.]+) MB", fwd[0])
+    assert m, fwd[0]
+    entries, pairs, window, full, mb = int(m.group(1)), int(m.group(2)), int(m.group(3)), int(m.group(4)), \
+        float(m.group(5))
+    assert entries > 0 and pairs >= entries and 0 < window <= entries and 0 <= full <= 32
+    assert abs(mb - (entries * (8 + 4 * 9) + 4 * 33) / 1e6) < 0.01
+    assert any(l.startswith("disco: transpose op") for l in err.splitlines())
+
+
+def test_plan_log_is_off_by_default():
+    assert "disco:" not in _plan_stderr(None)
+    assert "disco:" not in _plan_stderr("0")
+
+
+def test_default_build_has_no_range_checks():
+    """The production library compiles the psi-index range checks out."""
+    assert disco.library().disco_debug_bounds_violations() == -1

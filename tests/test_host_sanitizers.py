@@ -28,7 +28,7 @@ def test_host_code_is_clean_under_asan_and_ubsan(tmp_path):
         [os.path.join(CSRC, f) for f in ("disco_plan.cpp", "disco_pack.cpp", "disco_spectral_plan.cpp",
                                          "disco_abi.cpp")]
     cmd = [HIPCC, "-O1", "-g", "-std=c++17", *san, "-I", os.path.join(ROOT, "include"), "-I", CSRC, *srcs,
-           "-o", exe]
+           "-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx", "-o", exe]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
     assert r.returncode == 0, r.stdout + r.stderr
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1",
