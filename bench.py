@@ -135,8 +135,11 @@ def kernel_model(name, wl, work, es, spec=None):
             m["valu"] = B * Ci * spec["slots"] * fft_flops(n_in)
         elif name == "spectral_mac":
             # per (ring pair, frequency): the input transform of each input
-            # channel and 9 psi values read; per output bin: Yhat written
-            m["bytes"] = (B * Ci * 8 + 9 * 4) * spec["pairs"] * mi + B * Co * spec["rings"] * mi * 8
+            # channel read; per (psi table, frequency) its 9 values (pairs
+            # mirrored about the equator share a table); per output bin: Yhat
+            # written
+            m["bytes"] = (B * Ci * 8 * spec["pairs"] + 9 * 4 * spec.get("tables", spec["pairs"])) * mi \
+                + B * Co * spec["rings"] * mi * 8
             m["valu"] = 36.0 * B * Ci * spec["pairs"] * mi + 36.0 * B * Ci * Co * spec["rings"] * mi
         else:
             m["bytes"] = B * Co * spec["rings"] * (mo * 8 + n_out * es)
@@ -170,7 +173,8 @@ def spectral_spec(plan, transpose):
     info = plan.info()
     sfx = "transpose" if transpose else "forward"
     return {"rings": info["spectral_rings_" + sfx], "pairs": info["spectral_pairs_" + sfx],
-            "slots": info["spectral_slots_" + sfx]}
+            "slots": info["spectral_slots_" + sfx],
+            "tables": info.get("spectral_tables_" + sfx, info["spectral_pairs_" + sfx])}
 
 
 def model_roof(m, avg_s):

@@ -178,6 +178,10 @@ typedef struct {
     int64_t bytes_matrix_core; /* the bf16 matrix-core tables (built by the first bf16 call) */
     int64_t psi_bytes_all_layouts; /* device bytes once every layout of every op is built
                                       (matrix-core tables excluded) */
+    int32_t spectral_tables_forward;   /* frequency-domain psi tables of the forward op's pairs:
+                                          a pair mirrored about the equator from an earlier one
+                                          shares that pair's table */
+    int32_t spectral_tables_transpose; /* ... of the transposed op */
 } disco_plan_info_t;
 
 /* Builds the sparse psi tensors of the forward and transposed ops on the host

@@ -184,6 +184,7 @@ disco_status_t upload_spectral(const SpectralHost& S, SpectralDev* d) {
     if ((s = upload_vec(S.rings, &d->rings, &d->bytes, "hipMalloc(spectral rings)")) != DISCO_OK) return s;
     if ((s = upload_vec(S.pair_ptr, &d->pair_ptr, &d->bytes, "hipMalloc(spectral pairs)")) != DISCO_OK) return s;
     if ((s = upload_vec(S.pair_slot, &d->pair_slot, &d->bytes, "hipMalloc(spectral pairs)")) != DISCO_OK) return s;
+    if ((s = upload_vec(S.pair_tab, &d->pair_tab, &d->bytes, "hipMalloc(spectral pairs)")) != DISCO_OK) return s;
     if ((s = upload_vec(S.slot_ring, &d->slot_ring, &d->bytes, "hipMalloc(spectral slots)")) != DISCO_OK) return s;
     if ((s = upload_vec(S.vs, &d->vs, &d->bytes, "hipMalloc(spectral psi)")) != DISCO_OK) return s;
     if ((s = upload_vec(S.tw, &d->tw, &d->bytes, "hipMalloc(twiddles)")) != DISCO_OK) return s;
@@ -192,11 +193,12 @@ disco_status_t upload_spectral(const SpectralHost& S, SpectralDev* d) {
     d->n_rings = (int)S.rings.size();
     d->n_pairs = (int)S.pair_slot.size();
     d->n_slots = (int)S.slot_ring.size();
+    d->n_tables = S.n_tables;
     return DISCO_OK;
 }
 
 void free_spectral(SpectralDev* d) {
-    void* ptrs[] = {d->rings, d->pair_ptr, d->pair_slot, d->slot_ring, d->vs, d->tw};
+    void* ptrs[] = {d->rings, d->pair_ptr, d->pair_slot, d->pair_tab, d->slot_ring, d->vs, d->tw};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     *d = SpectralDev{};
@@ -443,7 +445,7 @@ disco_status_t prepare_op(const HostOp& h, DeviceOp* d) {
         if ((s = pack_general(h, heavy, &T->light)) != DISCO_OK) return s;
         T->has_light = true;
         core += vec_bytes(T->sp.rings) + vec_bytes(T->sp.pair_ptr) + vec_bytes(T->sp.pair_slot) +
-                vec_bytes(T->sp.slot_ring) + vec_bytes(T->sp.vs) + vec_bytes(T->sp.tw) + h.g.nlat_o +
+                vec_bytes(T->sp.pair_tab) + vec_bytes(T->sp.slot_ring) + vec_bytes(T->sp.vs) + vec_bytes(T->sp.tw) + h.g.nlat_o +
                 packed_bytes(T->light);
         std::vector<uint8_t> light(heavy.size());
         for (size_t i = 0; i < heavy.size(); ++i) light[i] = !heavy[i];
@@ -1312,17 +1314,19 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
     I.nnz_pairs_total = hf.nnz_pairs;
     I.h = p.h;
     // Structure counts from the host tables (every op's are packed).
-    auto structure = [](const DeviceOp& d, int32_t* rings, int32_t* pats, int32_t* pairs, int32_t* slots) {
+    auto structure = [](const DeviceOp& d, int32_t* rings, int32_t* pats, int32_t* pairs, int32_t* slots,
+                        int32_t* tables) {
         const OpTables* T = d.tables.get();
         *rings = T ? (int32_t)T->sp.rings.size() : d.spectral.n_rings;
         *pats = T ? (int32_t)T->sw.pats.size() : d.sweep.n_pats;
         *pairs = T ? (int32_t)T->sp.pair_slot.size() : d.spectral.n_pairs;
         *slots = T ? (int32_t)T->sp.slot_ring.size() : d.spectral.n_slots;
+        *tables = T ? T->sp.n_tables : d.spectral.n_tables;
     };
     structure(plan->fwd, &I.spectral_rings_forward, &I.sweep_patterns_forward, &I.spectral_pairs_forward,
-              &I.spectral_slots_forward);
+              &I.spectral_slots_forward, &I.spectral_tables_forward);
     structure(plan->tr, &I.spectral_rings_transpose, &I.sweep_patterns_transpose, &I.spectral_pairs_transpose,
-              &I.spectral_slots_transpose);
+              &I.spectral_slots_transpose, &I.spectral_tables_transpose);
     I.psi_compressed_bytes = (int64_t)hf.t_in.size() * (8 + 4 * I.K) + 4 * (int64_t)hf.pat_ptr.size();
     for (const DeviceOp* d : {&plan->fwd, &plan->tr, &plan->fwd_adj, &plan->tr_adj}) {
         const OpTables* T = d->tables.get();

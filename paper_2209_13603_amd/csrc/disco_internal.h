@@ -295,13 +295,17 @@ struct SweepDev {
 // East-west mirror symmetry of the 3x3 basis gives Vhat_{3a+2} =
 // conj(Vhat_{3a}) and a real Vhat_{3a+1}, so each (ring pair, frequency)
 // stores 9 floats: Re/Im Vhat_{3a} and Re Vhat_{3a+1} for a = 0, 1, 2.
+// Pairs mirrored about the equator share one table (rows a = 0 and a = 2
+// exchanged), which halves the tables of an op with both polar caps.
 struct SpectralHost {
     int N = 0, M = 0;                 // ring length and M = N / 2
     std::vector<int32_t> rings;       // heavy output rings
     std::vector<int32_t> pair_ptr;    // CSR over pairs, size rings + 1
     std::vector<int32_t> pair_slot;   // input-ring slot of each pair
+    std::vector<int32_t> pair_tab;    // table of each pair in vs; bit 31: read with rows a = 0, 2 exchanged
+    int32_t n_tables = 0;             // tables in vs (pairs that are no equator mirror of an earlier one)
     std::vector<int32_t> slot_ring;   // input ring of each slot
-    std::vector<float> vs;            // [pair][9][M + 1], scaled by 1 / N
+    std::vector<float> vs;            // [table][9][M + 1], scaled by 1 / N
     std::vector<float> tw;            // [N / 2][2]: exp(-2 pi i t / N)
 };
 // Fills *sp (possibly with no rings) and marks heavy patterns in *heavy.
@@ -309,10 +313,11 @@ int build_spectral(const HostOp& op, int min_entries, SpectralHost* sp, std::vec
                    std::string* err);
 
 struct SpectralDev {
-    int N = 0, M = 0, n_rings = 0, n_pairs = 0, n_slots = 0;
+    int N = 0, M = 0, n_rings = 0, n_pairs = 0, n_slots = 0, n_tables = 0;
     int32_t* rings = nullptr;
     int32_t* pair_ptr = nullptr;
     int32_t* pair_slot = nullptr;
+    int32_t* pair_tab = nullptr;
     int32_t* slot_ring = nullptr;
     float* vs = nullptr;
     float* tw = nullptr;

@@ -179,6 +179,7 @@ __global__ __launch_bounds__(kFftBlock) void k_rfft_rings(const int32_t* __restr
 template <typename T, int COT>
 __global__ __launch_bounds__(kFftBlock) void k_spectral(const int32_t* __restrict__ pair_ptr,
                                                        const int32_t* __restrict__ pair_slot,
+                                                       const int32_t* __restrict__ pair_tab,
                                                        const float* __restrict__ vs,
                                                        const float2* __restrict__ xh,
                                                        const T* __restrict__ w, float2* __restrict__ yh,
@@ -228,10 +229,18 @@ __global__ __launch_bounds__(kFftBlock) void k_spectral(const int32_t* __restric
                 G[c][a] = make_float2(0.0f, 0.0f);
             }
         for (int p = p0; p < p1; ++p) {
-            const float* v = vs + (int64_t)p * 9 * vstride + m;
+            // The pair's table; an equator mirror reads its rows a = 0 and
+            // a = 2 exchanged.
+            const int32_t tb = pair_tab[p];
+            const int r0 = tb < 0 ? 6 : 0;
+            const float* v = vs + (int64_t)(tb & 0x7fffffff) * 9 * vstride + m;
             float V[9];
 #pragma unroll
-            for (int i = 0; i < 9; ++i) V[i] = v[i * vstride];
+            for (int j = 0; j < 3; ++j) {
+                V[j] = v[(r0 + j) * vstride];
+                V[3 + j] = v[(3 + j) * vstride];
+                V[6 + j] = v[(6 - r0 + j) * vstride];
+            }
             const float2* xr = xh + (((int64_t)pair_slot[p] * B + b) * Ci) * vstride + m;
 #pragma unroll
             for (int c = 0; c < SC; ++c) {
@@ -335,7 +344,7 @@ hipError_t spectral_launch(const ExecArgs& a, float* ws, int stages) {
         const int n_cot = (a.Co + COT - 1) / COT;
         const int tk = timing_begin("spectral_mac", a.stream);
         hipLaunchKernelGGL((k_spectral<T, COT>), dim3((M + 1 + kFftBlock - 1) / kFftBlock, S.n_rings, a.B * n_cot),
-                           dim3(kFftBlock), 0, a.stream, S.pair_ptr, S.pair_slot, S.vs, xh, (const T*)a.w, yh,
+                           dim3(kFftBlock), 0, a.stream, S.pair_ptr, S.pair_slot, S.pair_tab, S.vs, xh, (const T*)a.w, yh,
                            a.B, a.Ci, a.Co, M, n_cot, a.w_trans);
         timing_end(tk, a.stream);
         const hipError_t e = hipGetLastError();

@@ -9,6 +9,14 @@
 // every output longitude by a shift).  This file computes Vhat_k in fp64 with
 // its own radix-2 FFT, checks the east-west mirror symmetry that lets 9 floats
 // per frequency describe all nine basis functions, and rounds to fp32.
+//
+// The grids are symmetric about the equator: reflecting both rings of a pair
+// (t_o -> nlat_o - 1 - t_o, t_i -> nlat_i - 1 - t_i) flips the sign of the
+// local coordinate along the meridian and keeps the one along the parallel and
+// the longitude offsets, so the reflected pair's psi rows are this pair's with
+// the radial index a of psi_{3a+b} replaced by 2 - a.  A pair whose stored
+// entries show exactly that relation to an earlier pair reads that pair's
+// table with its rows a = 0 and a = 2 exchanged instead of holding its own.
 #include <algorithm>
 #include <cmath>
 #include <complex>
@@ -114,24 +122,74 @@ int build_spectral(const HostOp& op, int min_entries, SpectralHost* sp, std::vec
         sp->pair_ptr.push_back((int32_t)sp->pair_slot.size());
         (*heavy)[(size_t)to] = 1;
     }
-    // Vhat per pair: b = 0 (complex) and b = 1 (real) columns, scaled by 1/N
+    // Entry range of every pair, and the table each pair reads: its own, or
+    // (bit 31) the equator mirror's with rows a = 0 and a = 2 exchanged.
+    struct PairEnt { int32_t to, ti, e0, e1; };
+    std::vector<PairEnt> pe;
+    for (int32_t to : rings) {
+        const int32_t e1 = op.pat_ptr[(size_t)to + 1];
+        for (int32_t e = op.pat_ptr[(size_t)to]; e < e1;) {
+            const int32_t ti = op.t_in[(size_t)e];
+            int32_t eend = e;
+            while (eend < e1 && op.t_in[(size_t)eend] == ti) ++eend;
+            pe.push_back({to, ti, e, eend});
+            e = eend;
+        }
+    }
+    const size_t n_pairs = pe.size();
+    std::vector<int32_t> ring_first((size_t)g.nlat_o, -1);  // first pair of each spectral ring
+    for (size_t p = n_pairs; p-- > 0;) ring_first[(size_t)pe[p].to] = (int32_t)p;
+    sp->pair_tab.assign(n_pairs, -1);
+    std::vector<int32_t> owners;  // pair whose entries make each table
+    auto mirrors = [&](const PairEnt& p, const PairEnt& q) {
+        if (p.e1 - p.e0 != q.e1 - q.e0) return false;
+        double vmax = 0.0;
+        for (const PairEnt* r : {&p, &q})
+            for (int32_t e = r->e0; e < r->e1; ++e)
+                for (int k = 0; k < kBasis; ++k) vmax = std::max(vmax, std::fabs(op.val64[(size_t)e * kBasis + k]));
+        for (int32_t e = q.e0; e < q.e1; ++e) at[(size_t)op.d[(size_t)e]] = e;
+        bool same = true;
+        for (int32_t e = p.e0; e < p.e1 && same; ++e) {
+            const int32_t f = at[(size_t)op.d[(size_t)e]];
+            if (f < 0) { same = false; break; }
+            for (int a = 0; a < 3 && same; ++a)
+                for (int b = 0; b < 3; ++b)
+                    if (std::fabs(op.val64[(size_t)e * kBasis + 3 * a + b] -
+                                  op.val64[(size_t)f * kBasis + 3 * (2 - a) + b]) > 1e-12 * vmax) {
+                        same = false;
+                        break;
+                    }
+        }
+        for (int32_t e = q.e0; e < q.e1; ++e) at[(size_t)op.d[(size_t)e]] = -1;
+        return same;
+    };
+    for (size_t p = 0; p < n_pairs; ++p) {
+        const PairEnt& P = pe[p];
+        // The mirror pair, if it is an earlier one with a table of its own.
+        int32_t mq = -1;
+        const int32_t mto = g.nlat_o - 1 - P.to, mti = g.nlat_i - 1 - P.ti;
+        for (int32_t q = ring_first[(size_t)mto]; q >= 0 && q < (int32_t)p && pe[(size_t)q].to == mto; ++q)
+            if (pe[(size_t)q].ti == mti) mq = q;
+        if (mq >= 0 && sp->pair_tab[(size_t)mq] >= 0 && mirrors(P, pe[(size_t)mq])) {
+            sp->pair_tab[p] = sp->pair_tab[(size_t)mq] | (int32_t)0x80000000u;
+        } else {
+            sp->pair_tab[p] = (int32_t)owners.size();
+            owners.push_back((int32_t)p);
+        }
+    }
+    // Vhat per table: b = 0 (complex) and b = 1 (real) columns, scaled by 1/N
     // (the inverse transform on the device is unnormalised).
-    const size_t n_pairs = sp->pair_slot.size();
-    sp->vs.assign(n_pairs * 9 * (size_t)(M + 1), 0.0f);
-    size_t pair = 0;
+    sp->n_tables = (int32_t)owners.size();
+    sp->vs.assign(owners.size() * 9 * (size_t)(M + 1), 0.0f);
     std::vector<cd> buf((size_t)N), wtab((size_t)M);
     for (int t = 0; t < M; ++t) {
         const double ang = -2.0 * 3.14159265358979323846 * (double)t / (double)N;
         wtab[(size_t)t] = cd(std::cos(ang), std::sin(ang));
     }
-    for (int32_t to : rings) {
-        const int32_t e0 = op.pat_ptr[(size_t)to], e1 = op.pat_ptr[(size_t)to + 1];
-        int32_t e = e0;
-        while (e < e1) {
-            const int32_t ti = op.t_in[(size_t)e];
-            int32_t eend = e;
-            while (eend < e1 && op.t_in[(size_t)eend] == ti) ++eend;
-            float* dst = &sp->vs[pair * 9 * (size_t)(M + 1)];
+    for (size_t tb = 0; tb < owners.size(); ++tb) {
+        {
+            const int32_t e = pe[(size_t)owners[tb]].e0, eend = pe[(size_t)owners[tb]].e1;
+            float* dst = &sp->vs[tb * 9 * (size_t)(M + 1)];
             for (int a = 0; a < 3; ++a) {
                 // Two real sequences in one complex FFT: v_{3a} + i v_{3a+1}.
                 std::fill(buf.begin(), buf.end(), cd(0.0, 0.0));
@@ -149,8 +207,6 @@ int build_spectral(const HostOp& op, int min_entries, SpectralHost* sp, std::vec
                     dst[(size_t)(3 * a + 2) * (M + 1) + m] = (float)(v1.real() / N);
                 }
             }
-            ++pair;
-            e = eend;
         }
     }
     sp->tw.resize((size_t)N);

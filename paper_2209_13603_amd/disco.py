@@ -100,7 +100,8 @@ class PlanInfo(ctypes.Structure):
                 ("psi_compressed_bytes", ctypes.c_int64), ("bytes_entries", ctypes.c_int64),
                 ("bytes_general", ctypes.c_int64), ("bytes_spectral", ctypes.c_int64),
                 ("bytes_sweep", ctypes.c_int64), ("bytes_stencil", ctypes.c_int64),
-                ("bytes_matrix_core", ctypes.c_int64), ("psi_bytes_all_layouts", ctypes.c_int64)]
+                ("bytes_matrix_core", ctypes.c_int64), ("psi_bytes_all_layouts", ctypes.c_int64),
+                ("spectral_tables_forward", ctypes.c_int32), ("spectral_tables_transpose", ctypes.c_int32)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -38,6 +38,85 @@ uint16_t bf16_of(float f) {
     return (uint16_t)(u >> 16);
 }
 
+// Spectral tables: every pair's frequency-domain psi rows, read as the
+// product kernel reads them (its table, rows a = 0 and a = 2 exchanged for an
+// equator mirror), equal the DFT of the pair's own entries at a few
+// frequencies, evaluated directly in fp64; and when the spectral rings are
+// symmetric about the equator, every pair of the southern half reads a
+// northern table.
+void check_spectral(const HostOp& op, const SpectralHost& sp, const std::string& what) {
+    if (sp.rings.empty()) return;
+    const int N = sp.N, M = sp.M;
+    const double pi = 3.14159265358979323846;
+    size_t p = 0;
+    int south = 0;
+    std::vector<uint8_t> is_heavy((size_t)op.g.nlat_o, 0);
+    for (int32_t to : sp.rings) is_heavy[(size_t)to] = 1;
+    bool symmetric = true;
+    for (int t = 0; t < op.g.nlat_o; ++t) symmetric &= is_heavy[(size_t)t] == is_heavy[(size_t)(op.g.nlat_o - 1 - t)];
+    for (int32_t to : sp.rings) {
+        const int32_t e1 = op.pat_ptr[(size_t)to + 1];
+        for (int32_t e = op.pat_ptr[(size_t)to]; e < e1; ++p) {
+            const int32_t ti = op.t_in[(size_t)e];
+            int32_t eend = e;
+            while (eend < e1 && op.t_in[(size_t)eend] == ti) ++eend;
+            if (p >= sp.pair_tab.size()) {
+                std::printf("FAIL %s: spectral pair table too short\n", what.c_str());
+                ++failures;
+                return;
+            }
+            const int32_t tb = sp.pair_tab[p];
+            const int32_t tab = tb & 0x7fffffff, r0 = tb < 0 ? 6 : 0;
+            if (tab >= sp.n_tables || (size_t)(tab + 1) * 9 * (M + 1) > sp.vs.size()) {
+                std::printf("FAIL %s: pair %zu reads table %d of %d\n", what.c_str(), p, tab, sp.n_tables);
+                ++failures;
+                return;
+            }
+            if (to > op.g.nlat_o - 1 - to) south += tb < 0;
+            double scale = 0.0;
+            for (int32_t k = e; k < eend; ++k)
+                for (int kk = 0; kk < kBasis; ++kk) scale += std::fabs(op.val64[(size_t)k * kBasis + kk]);
+            scale /= N;
+            for (int m : {0, 1, M / 3, M}) {
+                for (int a = 0; a < 3; ++a) {
+                    double re0 = 0, im0 = 0, re1 = 0;
+                    for (int32_t k = e; k < eend; ++k) {
+                        const double ang = -2.0 * pi * (double)m * op.d[(size_t)k] / N;
+                        re0 += op.val64[(size_t)k * kBasis + 3 * a] * std::cos(ang);
+                        im0 += op.val64[(size_t)k * kBasis + 3 * a] * std::sin(ang);
+                        re1 += op.val64[(size_t)k * kBasis + 3 * a + 1] * std::cos(ang);
+                    }
+                    const int row = a == 0 ? r0 : a == 2 ? 6 - r0 : 3;
+                    const float* v = &sp.vs[(size_t)tab * 9 * (M + 1)];
+                    const double got[3] = {v[(size_t)(row + 0) * (M + 1) + m], v[(size_t)(row + 1) * (M + 1) + m],
+                                           v[(size_t)(row + 2) * (M + 1) + m]};
+                    const double want[3] = {re0 / N, im0 / N, re1 / N};
+                    for (int j = 0; j < 3; ++j)
+                        if (std::fabs(got[j] - want[j]) > 1e-6 * scale + 1e-30) {
+                            std::printf("FAIL %s: pair %zu (rings %d, %d) row %d freq %d: table %.9g, DFT %.9g\n",
+                                        what.c_str(), p, to, ti, 3 * a + j, m, got[j], want[j]);
+                            ++failures;
+                            return;
+                        }
+                }
+            }
+            e = eend;
+        }
+    }
+    if (p != sp.pair_tab.size()) {
+        std::printf("FAIL %s: %zu pairs, table of %zu\n", what.c_str(), p, sp.pair_tab.size());
+        ++failures;
+    }
+    int south_pairs = 0;
+    for (size_t r = 0; r < sp.rings.size(); ++r)
+        if (sp.rings[r] > op.g.nlat_o - 1 - sp.rings[r]) south_pairs += sp.pair_ptr[r + 1] - sp.pair_ptr[r];
+    if (symmetric && south != south_pairs) {
+        std::printf("FAIL %s: %d of %d southern spectral pairs share a northern table\n", what.c_str(), south,
+                    south_pairs);
+        ++failures;
+    }
+}
+
 // The matrix-core layout holds every entry's nine values (rounded to bf16)
 // exactly once, at its (output ring, phase, input ring, offset), and nothing
 // else; every staged element a lane reads lies inside its segment.
@@ -248,6 +327,14 @@ void run_op(const PlanParams& p, bool transpose, bool quad_at_output, const char
     SpectralHost sp;
     std::vector<uint8_t> heavy;
     check(build_spectral(op, 128, &sp, &heavy, &err), what + " build_spectral", err);
+    check_spectral(op, sp, what);
+    {
+        // Most rings of a small grid on the spectral path.
+        SpectralHost sp8;
+        std::vector<uint8_t> heavy8;
+        check(build_spectral(op, 8, &sp8, &heavy8, &err), what + " build_spectral (8)", err);
+        check_spectral(op, sp8, what + " (8 entries)");
+    }
     std::vector<uint8_t> light(heavy.size());
     for (size_t i = 0; i < heavy.size(); ++i) light[i] = !heavy[i];
     (void)pattern_work(op, heavy);

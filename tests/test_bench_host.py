@@ -56,6 +56,10 @@ def test_spectral_models_count_their_own_work():
     bins = N // 2 + 1
     assert m["valu"] == 36.0 * B * Ci * 1000 * bins + 36.0 * B * Ci * Co * 162 * bins
     assert m["mfma_f32"] == 0.0
+    # psi tables are read once per table, input transforms once per pair
+    m2 = bench.kernel_model("spectral_mac", wl, (0, 0, 10 ** 9), 4, dict(spec, tables=500))
+    assert m2["bytes"] == (B * Ci * 8 * 1000 + 36 * 500) * bins + B * Co * 162 * bins * 8
+    assert m["bytes"] - m2["bytes"] == 36 * 500 * bins
     with pytest.raises(SystemExit):
         bench.kernel_model("spectral_mac", wl, (0, 0, 10 ** 9), 4)
 
