@@ -140,7 +140,11 @@ def kernel_model(name, wl, work, es, spec=None):
             # written
             m["bytes"] = (B * Ci * 8 * spec["pairs"] + 9 * 4 * spec.get("tables", spec["pairs"])) * mi \
                 + B * Co * spec["rings"] * mi * 8
-            m["valu"] = 36.0 * B * Ci * spec["pairs"] * mi + 36.0 * B * Ci * Co * spec["rings"] * mi
+            m["valu"] = 36.0 * B * Ci * spec["pairs"] * mi
+            if not spec.get("z_mode"):
+                # the contraction with W per output bin (the weight gradient's
+                # pass writes the planes of Z instead: Co = Ci * 9, no W)
+                m["valu"] += 36.0 * B * Ci * Co * spec["rings"] * mi
         else:
             m["bytes"] = B * Co * spec["rings"] * (mo * 8 + n_out * es)
             m["valu"] = B * Co * spec["rings"] * fft_flops(n_out)
@@ -559,10 +563,12 @@ def bench_backward(args, wl, plan, x, w, es, torch, disco):
     if wl.dtype == "fp32" and wl.basis == "bilinear3x3":
         work_dw = plan.kernel_work(transpose, "gather_then_contract", Ci, Ci * K, wl.dtype)
         mwl = SimpleNamespace(batch=B, c_in=Ci, c_out=Ci * K, op=wl.op, **grids)
+        spec_dw = dict(spectral_spec(plan, transpose), z_mode=True)
     else:
         work_dw = plan.kernel_work(transpose, "auto", 1, K, wl.dtype)
         mwl = SimpleNamespace(batch=B * Ci, c_in=1, c_out=K, op=wl.op, **grids)
-    add("dw", kt_dw, work_dw, mwl, spectral_spec(plan, transpose))
+        spec_dw = spectral_spec(plan, transpose)
+    add("dw", kt_dw, work_dw, mwl, spec_dw)
     name, tot, b_, f_, bd, avg = max(cands, key=lambda c: c[1])
     if bd == "hbm":
         achieved, peak, unit = b_ / (avg / 1e3) / 1e9, HBM_PEAK_GBS, "GB/s"

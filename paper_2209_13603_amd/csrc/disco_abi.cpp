@@ -1062,7 +1062,7 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
     }
     struct Restore { int d; bool on; ~Restore() { if (on) (void)hipSetDevice(d); } } restore{cur, cur != plan->device};
     // fp32 with the 3x3 basis: Z of all channels in one pass (sweep Z mode,
-    // spectral rings through a selection W); otherwise the op's own kernels
+    // spectral rings' products without the contraction); otherwise the op's own kernels
     // once per input channel (items of B * C_x).
     const bool onepass = x->dtype == DISCO_FLOAT32 && op.basis == DISCO_BASIS_BILINEAR_3X3;
     if (onepass && (s = ensure_parts(plan, op, kPartCore | kPartEntries)) != DISCO_OK) return s;

@@ -497,8 +497,9 @@ bool gather_z_split(const ExecArgs& a);                   // sweep + spectral Z 
 hipError_t launch_contract_then_gather(const ExecArgs& a, float* xc_ws);
 // Gathered sums Z[b][ci][k][pixel] (fp32 storage, 3x3 basis) of every output
 // ring into z (B * Ci * 9 * pixels floats): the sweep's Z mode, k_gather_z
-// for the other light rings, the spectral kernels with a selection W for the
-// heavy ones.  ws: workspace_bytes_gather_z_all bytes.
+// for the other light rings, the spectral kernels' transforms and their
+// products without the contraction (kSpectralZ) for the heavy ones.  ws:
+// workspace_bytes_gather_z_all bytes.
 size_t workspace_bytes_gather_z_all(const ExecArgs& a);
 hipError_t launch_gather_z_all(const ExecArgs& a, float* z, float* ws);
 size_t workspace_bytes_gather_then_contract(const ExecArgs& a);
@@ -510,8 +511,11 @@ size_t workspace_bytes_mfma(const ExecArgs& a);
 hipError_t launch_mfma(const ExecArgs& a, void* ws);
 size_t workspace_bytes_fused(const ExecArgs& a, const PackedDev& P);
 // stages: bit 0 the input-ring transforms, bit 1 the frequency-domain
-// products, bit 2 the inverse transforms (in that order on one stream).
+// products, bit 2 the inverse transforms (in that order on one stream);
+// with kSpectralZ the products write the nine gathered planes of every input
+// channel (a.Co = a.Ci * 9, a.w unused) instead of contracting with W.
 constexpr int kSpectralAll = 7;
+constexpr int kSpectralZ = 8;
 hipError_t launch_spectral(const ExecArgs& a, float* ws, int stages = kSpectralAll);
 // The sweep takes kCIC input channels per launch: more input channels run
 // one launch per group, the first storing y and the others adding their

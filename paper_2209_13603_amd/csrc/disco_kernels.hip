@@ -252,16 +252,6 @@ hipError_t gather_then_contract(const ExecArgs& a, float* z, float* spec_ws) {
     return e;
 }
 
-// W[(ci K + k)][ci'][k'] = delta(ci, ci') delta(k, k'): with it the op's
-// output channel ci K + k is Z[ci][k].
-__global__ __launch_bounds__(kBlock) void k_fill_selection(float* __restrict__ w, int Ci) {
-    const int64_t n = (int64_t)Ci * kBasis * Ci * kBasis;
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock) {
-        const int64_t row = i / ((int64_t)Ci * kBasis), col = i - row * ((int64_t)Ci * kBasis);
-        w[i] = row == col ? 1.0f : 0.0f;
-    }
-}
-
 template <typename T>
 hipError_t contract_then_gather(const ExecArgs& a, float* xc) {
     const OpGeom& g = a.op->g;
@@ -312,16 +302,12 @@ size_t workspace_bytes_contract_then_gather(const ExecArgs& a) {
     return sizeof(float) * (size_t)a.B * a.Co * kBasis * (size_t)g.nlat_i * g.nlon_i;
 }
 
-static size_t selection_bytes(const ExecArgs& a) {
-    const size_t b = sizeof(float) * (size_t)a.Ci * kBasis * a.Ci * kBasis;
-    return (b + 255) & ~(size_t)255;
-}
-
 // The spectral rings' share of the gathered sums: the op's spectral kernels
-// with Co = Ci * 9 output channels and the selection W write Z directly.
-static ExecArgs z_as_output(const ExecArgs& a, const float* wsel, float* z) {
+// with Co = Ci * 9 output channels write the planes of Z directly (their
+// products without the contraction).
+static ExecArgs z_as_output(const ExecArgs& a, float* z) {
     ExecArgs s = a;
-    s.w = wsel;
+    s.w = nullptr;
     s.y = z;
     s.Co = a.Ci * kBasis;
     s.w_trans = false;
@@ -330,8 +316,7 @@ static ExecArgs z_as_output(const ExecArgs& a, const float* wsel, float* z) {
 
 size_t workspace_bytes_gather_z_all(const ExecArgs& a) {
     size_t b = 0;
-    if (gather_z_split(a) && a.op->spectral.n_rings > 0)
-        b = selection_bytes(a) + workspace_bytes_spectral(z_as_output(a, nullptr, nullptr));
+    if (gather_z_split(a) && a.op->spectral.n_rings > 0) b = workspace_bytes_spectral(z_as_output(a, nullptr));
     return b;
 }
 
@@ -361,14 +346,7 @@ hipError_t launch_gather_z_all(const ExecArgs& a, float* z, float* ws) {
         if (e != hipSuccess) return e;
     }
     if (op.spectral.n_rings == 0) return hipSuccess;
-    float* wsel = ws;
-    float* spec_ws = (float*)((char*)ws + selection_bytes(a));
-    const int64_t n = (int64_t)a.Ci * kBasis * a.Ci * kBasis;
-    hipLaunchKernelGGL(k_fill_selection, dim3((unsigned)std::min<int64_t>(1024, (n + kBlock - 1) / kBlock)),
-                       dim3(kBlock), 0, a.stream, wsel, a.Ci);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return launch_spectral(z_as_output(a, wsel, z), spec_ws);
+    return launch_spectral(z_as_output(a, z), ws, kSpectralAll | kSpectralZ);
 }
 
 hipError_t launch_gather_then_contract(const ExecArgs& a, float* z_ws) {

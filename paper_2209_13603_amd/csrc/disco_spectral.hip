@@ -277,6 +277,75 @@ __global__ __launch_bounds__(kFftBlock) void k_spectral(const int32_t* __restric
         if (co0 + j < Co) yh[(((int64_t)h * B + b) * Co + co0 + j) * vstride + m] = Y[j];
 }
 
+// The gathered sums of the heavy rings in the frequency domain: the products
+// of k_spectral without the channel contraction, Zhat[h][b][ci * 9 + k][m] =
+// sum over the ring's pairs of Xhat[slot][ci][m] conj(Vhat_k[pair][m]), the
+// nine planes of each input channel from the same E, F, G sums (k = 3a:
+// E - iF, 3a + 1: G, 3a + 2: E + iF in the conjugate convention of
+// k_spectral).  grid: (ceil((M+1)/256), n_rings, B * ceil(Ci / 4))
+__global__ __launch_bounds__(kFftBlock) void k_spectral_z(const int32_t* __restrict__ pair_ptr,
+                                                         const int32_t* __restrict__ pair_slot,
+                                                         const int32_t* __restrict__ pair_tab,
+                                                         const float* __restrict__ vs,
+                                                         const float2* __restrict__ xh, float2* __restrict__ zh,
+                                                         int B, int Ci, int M, int n_cg) {
+    constexpr int SC = 4;
+    const int m = blockIdx.x * kFftBlock + threadIdx.x;
+    if (m > M) return;  // no barriers below
+    const int h = blockIdx.y;
+    const int b = blockIdx.z / n_cg;
+    const int ci0 = (blockIdx.z - b * n_cg) * SC;
+    const int p0 = pair_ptr[h], p1 = pair_ptr[h + 1];
+    const int64_t vstride = (int64_t)(M + 1);
+    float2 E[SC][3], F[SC][3], G[SC][3];
+#pragma unroll
+    for (int c = 0; c < SC; ++c)
+#pragma unroll
+        for (int a = 0; a < 3; ++a) {
+            E[c][a] = make_float2(0.0f, 0.0f);
+            F[c][a] = make_float2(0.0f, 0.0f);
+            G[c][a] = make_float2(0.0f, 0.0f);
+        }
+    for (int p = p0; p < p1; ++p) {
+        const int32_t tb = pair_tab[p];
+        const int r0 = tb < 0 ? 6 : 0;
+        const float* v = vs + (int64_t)(tb & 0x7fffffff) * 9 * vstride + m;
+        float V[9];
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+            V[j] = v[(r0 + j) * vstride];
+            V[3 + j] = v[(3 + j) * vstride];
+            V[6 + j] = v[(6 - r0 + j) * vstride];
+        }
+        const float2* xr = xh + (((int64_t)pair_slot[p] * B + b) * Ci) * vstride + m;
+#pragma unroll
+        for (int c = 0; c < SC; ++c) {
+            const float2 X = ci0 + c < Ci ? xr[(int64_t)(ci0 + c) * vstride] : make_float2(0.0f, 0.0f);
+#pragma unroll
+            for (int a = 0; a < 3; ++a) {
+                E[c][a].x = fmaf(V[3 * a + 0], X.x, E[c][a].x);
+                E[c][a].y = fmaf(V[3 * a + 0], X.y, E[c][a].y);
+                F[c][a].x = fmaf(V[3 * a + 1], X.x, F[c][a].x);
+                F[c][a].y = fmaf(V[3 * a + 1], X.y, F[c][a].y);
+                G[c][a].x = fmaf(V[3 * a + 2], X.x, G[c][a].x);
+                G[c][a].y = fmaf(V[3 * a + 2], X.y, G[c][a].y);
+            }
+        }
+    }
+    const int Co = Ci * kBasis;
+#pragma unroll
+    for (int c = 0; c < SC; ++c) {
+        if (ci0 + c >= Ci) continue;
+        float2* zr = zh + (((int64_t)h * B + b) * Co + (int64_t)(ci0 + c) * kBasis) * vstride + m;
+#pragma unroll
+        for (int a = 0; a < 3; ++a) {
+            zr[(3 * a + 0) * vstride] = make_float2(E[c][a].x + F[c][a].y, E[c][a].y - F[c][a].x);
+            zr[(3 * a + 1) * vstride] = G[c][a];
+            zr[(3 * a + 2) * vstride] = make_float2(E[c][a].x - F[c][a].y, E[c][a].y + F[c][a].x);
+        }
+    }
+}
+
 // y[b][co][ring][:] = inverse real DFT of Yhat[h][b][co][:].  grid: (n_rings, B * Co)
 template <typename T>
 __global__ __launch_bounds__(kFftBlock) void k_irfft_rings(const int32_t* __restrict__ rings,
@@ -340,7 +409,17 @@ hipError_t spectral_launch(const ExecArgs& a, float* ws, int stages) {
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    if (stages & 2) {
+    if ((stages & 2) && (stages & kSpectralZ)) {
+        // a.Co = a.Ci * 9: the planes of every input channel, no W.
+        const int n_cg = (a.Ci + 3) / 4;
+        const int tk = timing_begin("spectral_mac", a.stream);
+        hipLaunchKernelGGL(k_spectral_z, dim3((M + 1 + kFftBlock - 1) / kFftBlock, S.n_rings, a.B * n_cg),
+                           dim3(kFftBlock), 0, a.stream, S.pair_ptr, S.pair_slot, S.pair_tab, S.vs, xh, yh, a.B, a.Ci,
+                           M, n_cg);
+        timing_end(tk, a.stream);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    } else if (stages & 2) {
         const int n_cot = (a.Co + COT - 1) / COT;
         const int tk = timing_begin("spectral_mac", a.stream);
         hipLaunchKernelGGL((k_spectral<T, COT>), dim3((M + 1 + kFftBlock - 1) / kFftBlock, S.n_rings, a.B * n_cot),

@@ -60,6 +60,9 @@ def test_spectral_models_count_their_own_work():
     m2 = bench.kernel_model("spectral_mac", wl, (0, 0, 10 ** 9), 4, dict(spec, tables=500))
     assert m2["bytes"] == (B * Ci * 8 * 1000 + 36 * 500) * bins + B * Co * 162 * bins * 8
     assert m["bytes"] - m2["bytes"] == 36 * 500 * bins
+    # the weight gradient's pass: the planes of Z, no contraction with W
+    m3 = bench.kernel_model("spectral_mac", wl, (0, 0, 10 ** 9), 4, dict(spec, z_mode=True))
+    assert m3["valu"] == 36.0 * B * Ci * 1000 * bins
     with pytest.raises(SystemExit):
         bench.kernel_model("spectral_mac", wl, (0, 0, 10 ** 9), 4)
 
