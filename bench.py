@@ -48,6 +48,7 @@ PAPER_SECONDS = {"poles_axisym_L1024": 0.0302, "poles_axisym_L2048": 0.0898,
 KERNEL_VARIANT = {"sweep_gather_contract": ", false, ", "sweep_gather_z": ", true, "}
 COPY_PROBE_BYTES = 256 << 20   # per direction, fp32 negation used as the plain copy kernel
 EVICT_BYTES = 512 << 20       # larger than the 256 MB last-level cache (MALL)
+COPY_KERNEL_BYTES = 1 << 30   # per direction, torch copy_ timed as the achievable streaming rate
 COPY_PROBE_KERNEL = "neg"
 
 
@@ -424,14 +425,60 @@ def step_percentiles(torch, step, reps, evict=None):
 
 def sample_parity(y, ref, pix, dtype):
     """Relative L2 and largest error (relative to the sample's largest
-    reference value) of the GPU output at the oracle's sampled pixels."""
+    reference value) of the GPU output at the oracle's sampled pixels, and
+    per output ring the largest error relative to that ring's largest
+    reference value (the worst ring reported)."""
     import numpy as np
     got = y.reshape(y.shape[0], y.shape[1], -1)[:, :, pix].astype(np.float64)
     err = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300))
     mx = float(np.abs(got - ref).max() / max(np.abs(ref).max(), 1e-300))
-    return {"rel_l2": err, "max_rel": mx, "pixels": int(len(pix)),
+    ring = np.asarray(pix) // y.shape[-1]
+    d = np.abs(got - ref).max(axis=(0, 1))
+    r = np.abs(ref).max(axis=(0, 1))
+    worst, worst_ring = 0.0, -1
+    for t in np.unique(ring):
+        sel = ring == t
+        v = float(d[sel].max() / max(r[sel].max(), 1e-300))
+        if v > worst:
+            worst, worst_ring = v, int(t)
+    return {"rel_l2": err, "max_rel": mx, "max_rel_worst_ring": worst, "worst_ring": worst_ring,
+            "rings": int(len(np.unique(ring))), "pixels": int(len(pix)),
             "tol_rel_l2": 1e-5 if dtype == "fp32" else 2e-2,
             "pass": err <= (1e-5 if dtype == "fp32" else 2e-2)}
+
+
+def copy_kernel_gbs(torch, dev, nbytes=COPY_KERNEL_BYTES, reps=5):
+    """Bandwidth of a plain device copy (torch's copy_ of nbytes of fp32 into
+    another buffer: nbytes read and nbytes written), the best of reps timed
+    launches: what a streaming kernel reaches on this GPU, beside the HBM
+    peak."""
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    best = None
+    for _ in range(reps):
+        ev[0].record()
+        b.copy_(a)
+        ev[1].record()
+        ev[1].synchronize()
+        ms = ev[0].elapsed_time(ev[1])
+        best = ms if best is None else min(best, ms)
+    del a, b
+    return {"gbs": round(2 * nbytes / (best / 1e3) / 1e9, 1), "bytes_per_launch": 2 * nbytes,
+            "kernel": "torch copy_ of %d MiB fp32 (read + write), best of %d" % (nbytes >> 20, reps)}
+
+
+def add_copy_fracs(obj, copy_gbs):
+    """Every HBM-bound kernel row and roofline in obj gains copy_frac: its
+    algorithmic GB/s over the copy kernel's."""
+    if isinstance(obj, dict):
+        if obj.get("bound") == "hbm":
+            gbs = obj.get("alg_gbs", obj.get("achieved") if obj.get("unit") == "GB/s" else None)
+            if gbs is not None:
+                obj["copy_frac"] = round(gbs / copy_gbs, 4)
+        for v in obj.values():
+            add_copy_fracs(v, copy_gbs)
 
 
 def kernel_report(plan, kt, wl, transpose, algo, es, steps):
@@ -539,6 +586,14 @@ def bench_backward(args, wl, plan, x, w, es, torch, disco):
                 f_, bd = 2.0 * B * Co * Ci * K * P, "hbm"
             elif k == "weight_grad_reduce":
                 b_, f_, bd = 0, 0.0, "hbm"
+            elif k == "spectral_rfft_dy":
+                # dy's transform on the op's spectral output rings (the
+                # weight gradient's frequency-domain share): dy read, the
+                # half spectrum written
+                n_o = wl.nlon_out if wl.op == "forward" else wl.nlon_in
+                rings = spec["rings"]
+                b_ = B * Co * rings * (n_o * 4 + (n_o // 2 + 1) * 8)
+                f_, bd = B * Co * rings * fft_flops(n_o), "alu"
             else:
                 if k not in work:
                     raise SystemExit("no work figures for kernel %s" % k)
@@ -760,6 +815,11 @@ def main(argv=None):
         vs_baseline = value / paper
         baseline = {"value": paper, "unit": UNIT, "seconds": PAPER_SECONDS[wl.name],
                     "hardware": "NVIDIA RTX 3090 (the paper's App. B; other hardware, context)"}
+    copy_k = copy_kernel_gbs(torch, dev)
+    add_copy_fracs(per_kernel, copy_k["gbs"])
+    add_copy_fracs(roof, copy_k["gbs"])
+    if hbm:
+        add_copy_fracs(hbm, copy_k["gbs"])
     out = {
         "metric": metric, "value": value, "unit": UNIT, "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
@@ -773,6 +833,7 @@ def main(argv=None):
                    "algo": "depthwise" if wl.depthwise else args.algo, "storage": wl.dtype},
         "paper_baseline": baseline,
         "op_algorithmic_gbs": round(op_bytes / (ms_per_step / 1e3) / 1e9, 2),
+        "copy_kernel": copy_k,
         "kernels": per_kernel,
         "roofline": roof,
         "step_distribution": dist,

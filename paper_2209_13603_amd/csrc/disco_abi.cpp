@@ -442,6 +442,13 @@ disco_status_t prepare_op(const HostOp& h, DeviceOp* d) {
     if (!T->sp.rings.empty()) {
         T->spectral_flag.assign((size_t)h.g.nlat_o, 0);
         for (int32_t r : T->sp.rings) T->spectral_flag[(size_t)r] = 1;
+        int32_t lo = 0, hi = h.g.nlat_o;
+        while (lo < h.g.nlat_o && T->spectral_flag[(size_t)lo]) ++lo;
+        while (hi > lo && T->spectral_flag[(size_t)hi - 1]) --hi;
+        if (lo < hi && lo + (h.g.nlat_o - hi) == (int32_t)T->sp.rings.size()) {
+            d->cap_lo = lo;
+            d->cap_hi = hi;
+        }
         if ((s = pack_general(h, heavy, &T->light)) != DISCO_OK) return s;
         T->has_light = true;
         core += vec_bytes(T->sp.rings) + vec_bytes(T->sp.pair_ptr) + vec_bytes(T->sp.pair_slot) +
@@ -1071,11 +1078,22 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
     za.w_trans = transpose; za.stream = stream;
     const size_t zbytes = ((size_t)(B * C_x) * K * (size_t)P * elem_bytes(x->dtype) + 255) & ~(size_t)255;
     const size_t zws = onepass ? workspace_bytes_gather_z_all(za) : 0;
+    // With the heavy rings forming the two polar caps, their share of dW is
+    // summed in the frequency domain (Parseval: per ring, sum_q dy Z = sum_m
+    // Re(conj(DYhat) Zhat) with the interior bins counted twice), so their Z
+    // needs no inverse transforms and is not written to HBM.
+    const bool split = onepass && !depthwise && gather_z_split(za) && op.spectral.n_rings > 0 && op.cap_lo < op.cap_hi;
+    const int64_t off_light = split ? (int64_t)op.cap_lo * op.g.nlon_o : 0;
+    const int64_t p_light = split ? (int64_t)(op.cap_hi - op.cap_lo) * op.g.nlon_o : P;
+    const int b_heavy = split ? op.spectral.n_rings * (int)B : 0;
+    const int64_t p_heavy = split ? 2 * (int64_t)(op.spectral.M + 1) : 0;
+    const size_t dyh_bytes = split ? (spectral_dyhat_bytes(za, (int)C_dy) + 255) / 256 * 256 : 0;
     const size_t gbytes = depthwise ? weight_grad_ws_bytes_dw((int)B, (int)C_x, K, P)
+                          : split   ? weight_grad_split_ws_bytes((int)B, (int)C_dy, (int)(C_x * K), p_light, b_heavy, p_heavy)
                                     : weight_grad_ws_bytes((int)B, (int)C_dy, (int)(C_x * K), P);
     void* zbuf = nullptr;
     float* gws = nullptr;
-    hipError_t e = hipMallocAsync(&zbuf, zbytes + zws, stream);
+    hipError_t e = hipMallocAsync(&zbuf, zbytes + zws + dyh_bytes, stream);
     if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(gathered sums)");
     e = hipMallocAsync((void**)&gws, gbytes, stream);
     if (e != hipSuccess) {
@@ -1083,6 +1101,21 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
         return hip_fail(e, "hipMallocAsync(weight gradient partials)");
     }
     zt.data = zbuf;
+    if (split) {
+        float2* zhat = nullptr;
+        float2* dyh = (float2*)((char*)zbuf + zbytes + zws);
+        const float* dy32 = (const float*)dy->data;
+        e = launch_gather_z_light(za, (float*)zbuf, (float*)((char*)zbuf + zbytes), &zhat);
+        if (e == hipSuccess) e = launch_spectral_dyhat(za, dy32, (int)C_dy, dyh);
+        if (e == hipSuccess)
+            e = launch_weight_grad_split(dy32 + off_light, (const float*)zbuf + off_light, (int)B, p_light, P,
+                                         (const float*)dyh, (const float*)zhat, b_heavy, p_heavy, (float*)dw->data,
+                                         gws, (int)C_dy, (int)C_x, K, transpose, stream);
+        s = e == hipSuccess ? DISCO_OK : hip_fail(e, "kernel launch");
+        (void)hipFreeAsync(gws, stream);
+        (void)hipFreeAsync(zbuf, stream);
+        return s == DISCO_OK ? ok() : s;
+    }
     if (onepass) {
         e = launch_gather_z_all(za, (float*)zbuf, (float*)((char*)zbuf + zbytes));
         s = e == hipSuccess ? DISCO_OK : hip_fail(e, "kernel launch");

@@ -110,12 +110,15 @@ constexpr int kPix = 64;         // pixels staged per step (one per lane and row
 constexpr int kLd = kPix + 2;    // LDS row stride in floats: operand reads free of bank conflicts
 
 // grid: (n_chunks * n_mt * n_nt, 1, B), n_mt = ceil(M / 16), n_nt = ceil(N /
-// (16 NB)).  LDS rows 0..15 hold dy rows m0.., rows 16.. the Zs rows n0..;
-// rows past M or N hold zeros.  partial: [B][n_chunks][M][N].
+// (16 NB)).  Row r of batch item b starts at (b rows + r) * stride and P of
+// its values are summed (P <= stride).  LDS rows 0..15 hold dy rows m0..,
+// rows 16.. the Zs rows n0..; rows past M or N hold zeros.  partial:
+// [B][n_chunks][M][N].
 template <typename T, int NB>
 __global__ __launch_bounds__(kBlock) void k_weight_grad_mfma(const T* __restrict__ dy, const T* __restrict__ zs,
                                                              float* __restrict__ partial, int M, int N, int64_t P,
-                                                             int64_t chunk_len, int n_nt, int n_chunks) {
+                                                             int64_t stride, int64_t chunk_len, int n_nt,
+                                                             int n_chunks) {
     constexpr int kRows = kMT + 16 * NB;
     constexpr int kIt = kRows / (kBlock / 64);  // staged rows per wave and step
     static_assert(kRows % (kBlock / 64) == 0, "the waves stage whole rows");
@@ -129,13 +132,13 @@ __global__ __launch_bounds__(kBlock) void k_weight_grad_mfma(const T* __restrict
     const int b = blockIdx.z;
     const int64_t p0 = (int64_t)chunk * chunk_len;
     const int64_t p1 = p0 + chunk_len < P ? p0 + chunk_len : P;
-    const T* dyb = dy + (int64_t)b * M * P;
-    const T* zb = zs + (int64_t)b * N * P;
+    const T* dyb = dy + (int64_t)b * M * stride;
+    const T* zb = zs + (int64_t)b * N * stride;
     // Staged row r = wave + 4 it of this lane: its source row (wave-uniform),
     // or none.
     auto row_src = [&](int r) -> const T* {
-        if (r < kMT) return r < mr ? dyb + (int64_t)(m0 + r) * P : nullptr;
-        return r - kMT < nr ? zb + (int64_t)(n0 + r - kMT) * P : nullptr;
+        if (r < kMT) return r < mr ? dyb + (int64_t)(m0 + r) * stride : nullptr;
+        return r - kMT < nr ? zb + (int64_t)(n0 + r - kMT) * stride : nullptr;
     };
     auto load_step = [&](int64_t ps, float (&v)[kIt]) {
         const int64_t p = ps + lane;
@@ -263,40 +266,59 @@ int64_t chunk_len_mfma(int B, int M, int N, int64_t P) {
 
 template <typename T, int NB>
 void launch_wg_mfma(dim3 grid, hipStream_t s, const T* dy, const T* zs, float* ws, int M, int N, int64_t P,
-                    int64_t len, int n_nt, int n_chunks) {
-    hipLaunchKernelGGL((k_weight_grad_mfma<T, NB>), grid, dim3(kBlock), 0, s, dy, zs, ws, M, N, P, len, n_nt,
+                    int64_t stride, int64_t len, int n_nt, int n_chunks) {
+    hipLaunchKernelGGL((k_weight_grad_mfma<T, NB>), grid, dim3(kBlock), 0, s, dy, zs, ws, M, N, P, stride, len, n_nt,
                        n_chunks);
+}
+
+// Partial slabs ([M][N] each) one launch of k_weight_grad_mfma writes.
+int64_t wg_slabs(int B, int M, int N, int64_t P) {
+    const int64_t len = chunk_len_mfma(B, M, N, P);
+    return (int64_t)B * std::max<int64_t>(1, (P + len - 1) / len);
+}
+
+// The partial tiles of G over B batch items of rows with P summed values
+// each (row stride `stride`), into wg_slabs(B, M, N, P) slabs at ws.
+template <typename T>
+hipError_t weight_grad_part(const T* dy, const T* zs, float* ws, int B, int M, int N, int64_t P, int64_t stride,
+                            hipStream_t s) {
+    const int64_t len = chunk_len_mfma(B, M, N, P);
+    const int n_chunks = (int)std::max<int64_t>(1, (P + len - 1) / len);
+    const int nb = mfma_nb(N);
+    const int n_mt = (M + kMT - 1) / kMT, n_nt = (N + 16 * nb - 1) / (16 * nb);
+    dim3 grid((unsigned)((int64_t)n_chunks * n_mt * n_nt), 1u, (unsigned)B);
+    switch (nb) {
+        case 1: launch_wg_mfma<T, 1>(grid, s, dy, zs, ws, M, N, P, stride, len, n_nt, n_chunks); break;
+        case 2: launch_wg_mfma<T, 2>(grid, s, dy, zs, ws, M, N, P, stride, len, n_nt, n_chunks); break;
+        case 3: launch_wg_mfma<T, 3>(grid, s, dy, zs, ws, M, N, P, stride, len, n_nt, n_chunks); break;
+        case 4: launch_wg_mfma<T, 4>(grid, s, dy, zs, ws, M, N, P, stride, len, n_nt, n_chunks); break;
+        case 5: launch_wg_mfma<T, 5>(grid, s, dy, zs, ws, M, N, P, stride, len, n_nt, n_chunks); break;
+        case 6: launch_wg_mfma<T, 6>(grid, s, dy, zs, ws, M, N, P, stride, len, n_nt, n_chunks); break;
+        case 7: launch_wg_mfma<T, 7>(grid, s, dy, zs, ws, M, N, P, stride, len, n_nt, n_chunks); break;
+        default: launch_wg_mfma<T, 8>(grid, s, dy, zs, ws, M, N, P, stride, len, n_nt, n_chunks); break;
+    }
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t weight_grad_reduce(const float* ws, T* dw, int64_t slabs, int M, int C_x, int K, bool transposed_layout,
+                              hipStream_t s) {
+    const int tk = timing_begin("weight_grad_reduce", s);
+    hipLaunchKernelGGL((k_weight_grad_reduce<T>), dim3((unsigned)(M * C_x * K)), dim3(kBlock), 0, s, ws, dw, 1,
+                       (int)slabs, M, C_x, K, transposed_layout);
+    timing_end(tk, s);
+    return hipGetLastError();
 }
 
 template <typename T>
 hipError_t weight_grad(const T* dy, const T* zs, T* dw, float* ws, int B, int M, int C_x, int K, int64_t P,
                        bool transposed_layout, hipStream_t s) {
     const int N = C_x * K;
-    const int64_t len = chunk_len_mfma(B, M, N, P);
-    const int n_chunks = (int)std::max<int64_t>(1, (P + len - 1) / len);
-    const int nb = mfma_nb(N);
-    const int n_mt = (M + kMT - 1) / kMT, n_nt = (N + 16 * nb - 1) / (16 * nb);
-    dim3 grid((unsigned)((int64_t)n_chunks * n_mt * n_nt), 1u, (unsigned)B);
-    int tk = timing_begin("weight_grad", s);
-    switch (nb) {
-        case 1: launch_wg_mfma<T, 1>(grid, s, dy, zs, ws, M, N, P, len, n_nt, n_chunks); break;
-        case 2: launch_wg_mfma<T, 2>(grid, s, dy, zs, ws, M, N, P, len, n_nt, n_chunks); break;
-        case 3: launch_wg_mfma<T, 3>(grid, s, dy, zs, ws, M, N, P, len, n_nt, n_chunks); break;
-        case 4: launch_wg_mfma<T, 4>(grid, s, dy, zs, ws, M, N, P, len, n_nt, n_chunks); break;
-        case 5: launch_wg_mfma<T, 5>(grid, s, dy, zs, ws, M, N, P, len, n_nt, n_chunks); break;
-        case 6: launch_wg_mfma<T, 6>(grid, s, dy, zs, ws, M, N, P, len, n_nt, n_chunks); break;
-        case 7: launch_wg_mfma<T, 7>(grid, s, dy, zs, ws, M, N, P, len, n_nt, n_chunks); break;
-        default: launch_wg_mfma<T, 8>(grid, s, dy, zs, ws, M, N, P, len, n_nt, n_chunks); break;
-    }
+    const int tk = timing_begin("weight_grad", s);
+    hipError_t e = weight_grad_part(dy, zs, ws, B, M, N, P, P, s);
     timing_end(tk, s);
-    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int ne = M * N;
-    tk = timing_begin("weight_grad_reduce", s);
-    hipLaunchKernelGGL((k_weight_grad_reduce<T>), dim3((unsigned)ne), dim3(kBlock), 0, s, ws, dw, B, n_chunks, M, C_x,
-                       K, transposed_layout);
-    timing_end(tk, s);
-    return hipGetLastError();
+    return weight_grad_reduce(ws, dw, wg_slabs(B, M, N, P), M, C_x, K, transposed_layout, s);
 }
 
 template <typename T>
@@ -349,9 +371,25 @@ hipError_t launch_weight_grad_dw(const void* dy, const void* zs, void* dw, float
 }
 
 size_t weight_grad_ws_bytes(int B, int M, int N, int64_t P) {
-    const int64_t len = chunk_len_mfma(B, M, N, P);
-    const int64_t n_chunks = std::max<int64_t>(1, (P + len - 1) / len);
-    return sizeof(float) * (size_t)B * (size_t)n_chunks * (size_t)M * (size_t)N;
+    return sizeof(float) * (size_t)wg_slabs(B, M, N, P) * (size_t)M * (size_t)N;
+}
+
+size_t weight_grad_split_ws_bytes(int B, int M, int N, int64_t P_light, int B_heavy, int64_t P_heavy) {
+    return sizeof(float) * (size_t)(wg_slabs(B, M, N, P_light) + wg_slabs(B_heavy, M, N, P_heavy)) * (size_t)M *
+           (size_t)N;
+}
+
+hipError_t launch_weight_grad_split(const float* dy, const float* zs, int B, int64_t P_light, int64_t stride,
+                                    const float* dyh, const float* zh, int B_heavy, int64_t P_heavy, float* dw,
+                                    float* ws, int M, int C_x, int K, bool transposed_layout, hipStream_t s) {
+    const int N = C_x * K;
+    const int64_t s1 = wg_slabs(B, M, N, P_light);
+    const int tk = timing_begin("weight_grad", s);
+    hipError_t e = weight_grad_part(dy, zs, ws, B, M, N, P_light, stride, s);
+    if (e == hipSuccess) e = weight_grad_part(dyh, zh, ws + s1 * M * N, B_heavy, M, N, P_heavy, P_heavy, s);
+    timing_end(tk, s);
+    if (e != hipSuccess) return e;
+    return weight_grad_reduce(ws, dw, s1 + wg_slabs(B_heavy, M, N, P_heavy), M, C_x, K, transposed_layout, s);
 }
 
 hipError_t launch_weight_grad(const void* dy, const void* zs, void* dw, float* ws, int dtype, int B, int M,

@@ -446,6 +446,9 @@ struct DeviceOp {
     int32_t* rest_pats = nullptr;  // device: those patterns' indices (gather-then-contract schedule)
     int32_t n_rest_pats = 0;
     uint8_t* spectral_ring = nullptr;  // device, nlat_o: 1 for output rings the spectral path writes
+    // The spectral rings are exactly the polar caps [0, cap_lo) and [cap_hi,
+    // nlat_o) (cap_lo < cap_hi), or cap_lo = cap_hi = 0.
+    int32_t cap_lo = 0, cap_hi = 0;
     int32_t* pat_ptr = nullptr;  // device, n_patterns + 1
     DevEntry* entries = nullptr;  // device
     int64_t n_entries = 0;
@@ -502,6 +505,10 @@ hipError_t launch_contract_then_gather(const ExecArgs& a, float* xc_ws);
 // workspace_bytes_gather_z_all bytes.
 size_t workspace_bytes_gather_z_all(const ExecArgs& a);
 hipError_t launch_gather_z_all(const ExecArgs& a, float* z, float* ws);
+// The same without the heavy rings' inverse transforms: their Z stays in
+// the frequency domain (spectral_yhat of the Z-as-output arguments, Ci * 9
+// channels) and z is not written on the spectral rings.
+hipError_t launch_gather_z_light(const ExecArgs& a, float* z, float* ws, float2** zhat);
 size_t workspace_bytes_gather_then_contract(const ExecArgs& a);
 size_t workspace_bytes_contract_then_gather(const ExecArgs& a);
 hipError_t launch_fused(const ExecArgs& a, const PackedDev& P, float* partial_ws);
@@ -517,6 +524,15 @@ size_t workspace_bytes_fused(const ExecArgs& a, const PackedDev& P);
 constexpr int kSpectralAll = 7;
 constexpr int kSpectralZ = 8;
 hipError_t launch_spectral(const ExecArgs& a, float* ws, int stages = kSpectralAll);
+// Where the products' output Yhat[h][b][co][m] (M + 1 bins) lies in the
+// spectral workspace ws of launch_spectral(a, ws, ...).
+float2* spectral_yhat(const ExecArgs& a, float* ws);
+// DYhat[h][b][c][m]: the real DFT of dy (fp32 [B][C][nlat_o][nlon_o]) on the
+// op's spectral output rings, bins 0 < m < M doubled, so that the sum over a
+// ring of dy times a signal with Yhat (as the products write it) is
+// sum_m Re(DYhat[m]) Re(Yhat[m]) + Im(DYhat[m]) Im(Yhat[m]).
+size_t spectral_dyhat_bytes(const ExecArgs& a, int C);
+hipError_t launch_spectral_dyhat(const ExecArgs& a, const float* dy, int C, float2* dyh);
 // The sweep takes kCIC input channels per launch: more input channels run
 // one launch per group, the first storing y and the others adding their
 // partial sums into it (fp32 atomic adds, one per element and launch, in
@@ -543,6 +559,14 @@ hipError_t launch_stencil_blocked(const ExecArgs& a, const StencilDev& S, float*
 // layout) or dW[c_x][m][k] (transposed op's layout).  dtype 0 fp32, 1 bf16
 // (inputs and dW); partials in ws (weight_grad_ws_bytes).
 size_t weight_grad_ws_bytes(int B, int M, int N, int64_t P);
+// fp32 only: G summed over two parts into one set of partials, the light
+// rings' pixels (B items, rows of P_light values at row stride `stride`) and
+// the heavy rings' frequency-domain rows (B_heavy = rings x B items, rows of
+// P_heavy values, e.g. spectral_dyhat against the spectral Zhat as floats).
+size_t weight_grad_split_ws_bytes(int B, int M, int N, int64_t P_light, int B_heavy, int64_t P_heavy);
+hipError_t launch_weight_grad_split(const float* dy, const float* zs, int B, int64_t P_light, int64_t stride,
+                                    const float* dyh, const float* zh, int B_heavy, int64_t P_heavy, float* dw,
+                                    float* ws, int M, int C_x, int K, bool transposed_layout, hipStream_t s);
 // Zeros `bytes` (a multiple of 2) of device memory with a kernel (no memset
 // node when the caller captures a graph).
 hipError_t launch_zero_fill(void* p, size_t bytes, hipStream_t s);

@@ -320,7 +320,7 @@ size_t workspace_bytes_gather_z_all(const ExecArgs& a) {
     return b;
 }
 
-hipError_t launch_gather_z_all(const ExecArgs& a, float* z, float* ws) {
+static hipError_t gather_z_all(const ExecArgs& a, float* z, float* ws, int spectral_stages) {
     const OpGeom& g = a.op->g;
     const DeviceOp& op = *a.op;
     constexpr int CG = 4;
@@ -346,7 +346,16 @@ hipError_t launch_gather_z_all(const ExecArgs& a, float* z, float* ws) {
         if (e != hipSuccess) return e;
     }
     if (op.spectral.n_rings == 0) return hipSuccess;
-    return launch_spectral(z_as_output(a, z), ws, kSpectralAll | kSpectralZ);
+    return launch_spectral(z_as_output(a, z), ws, spectral_stages);
+}
+
+hipError_t launch_gather_z_all(const ExecArgs& a, float* z, float* ws) {
+    return gather_z_all(a, z, ws, kSpectralAll | kSpectralZ);
+}
+
+hipError_t launch_gather_z_light(const ExecArgs& a, float* z, float* ws, float2** zhat) {
+    *zhat = spectral_yhat(z_as_output(a, z), ws);
+    return gather_z_all(a, z, ws, 1 | 2 | kSpectralZ);
 }
 
 hipError_t launch_gather_then_contract(const ExecArgs& a, float* z_ws) {

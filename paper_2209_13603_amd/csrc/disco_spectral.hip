@@ -129,12 +129,15 @@ __device__ __forceinline__ float2* fft_lds(float2* a, float2* b, int M, const fl
     return a;
 }
 
-// Xhat[slot][b][ci][m], m in [0, M]: real DFT of ring slot_ring[slot] of x.
+// Xhat[slot][b][ci][m], m in [0, M]: real DFT of ring slot_ring[slot] of x,
+// the bins 0 < m < M multiplied by `interior` (2 gives the weights of a sum
+// over the whole spectrum of a real signal, for Parseval's identity).
 // grid: (n_slots, B * Ci)
 template <typename T>
 __global__ __launch_bounds__(kFftBlock) void k_rfft_rings(const int32_t* __restrict__ slot_ring,
                                                          const T* __restrict__ x, const float2* __restrict__ tw,
-                                                         float2* __restrict__ xh, int B, int Ci, int nlat, int M) {
+                                                         float2* __restrict__ xh, int B, int Ci, int nlat, int M,
+                                                         float interior) {
     extern __shared__ float2 sm[];
     float2* a = sm;
     float2* bb = sm + M;
@@ -171,7 +174,9 @@ __global__ __launch_bounds__(kFftBlock) void k_rfft_rings(const int32_t* __restr
         const float2 dif = csub(zm, zc);
         const float2 o = make_float2(0.5f * dif.y, -0.5f * dif.x);  // (zm - zc) / (2i)
         const float2 w = tw_at(thi, tlo, m, M, false);  // m = M gives -1
-        out[m] = cadd(e, cmul(w, o));
+        const float2 v = cadd(e, cmul(w, o));
+        const float sc = m == 0 || m == M ? 1.0f : interior;
+        out[m] = make_float2(sc * v.x, sc * v.y);
     }
 }
 
@@ -404,7 +409,7 @@ hipError_t spectral_launch(const ExecArgs& a, float* ws, int stages) {
     if (stages & 1) {
         const int tk = timing_begin("spectral_rfft", a.stream);
         hipLaunchKernelGGL((k_rfft_rings<T>), dim3(S.n_slots, a.B * a.Ci), dim3(kFftBlock), lds, a.stream,
-                           S.slot_ring, (const T*)a.x, (const float2*)S.tw, xh, a.B, a.Ci, g.nlat_i, M);
+                           S.slot_ring, (const T*)a.x, (const float2*)S.tw, xh, a.B, a.Ci, g.nlat_i, M, 1.0f);
         timing_end(tk, a.stream);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -455,6 +460,28 @@ size_t workspace_bytes_spectral(const ExecArgs& a) {
     const SpectralDev& S = a.op->spectral;
     if (S.n_rings == 0) return 0;
     return sizeof(float2) * (size_t)(S.M + 1) * a.B * ((size_t)S.n_slots * a.Ci + (size_t)S.n_rings * a.Co);
+}
+
+float2* spectral_yhat(const ExecArgs& a, float* ws) {
+    const SpectralDev& S = a.op->spectral;
+    return (float2*)ws + (size_t)S.n_slots * a.B * a.Ci * (S.M + 1);
+}
+
+size_t spectral_dyhat_bytes(const ExecArgs& a, int C) {
+    const SpectralDev& S = a.op->spectral;
+    return sizeof(float2) * (size_t)S.n_rings * a.B * C * (S.M + 1);
+}
+
+hipError_t launch_spectral_dyhat(const ExecArgs& a, const float* dy, int C, float2* dyh) {
+    const SpectralDev& S = a.op->spectral;
+    if (S.n_rings == 0) return hipSuccess;
+    const int M = S.M;
+    const size_t lds = sizeof(float2) * (2 * (size_t)M + kTwLo + tw_hi_len(M));
+    const int tk = timing_begin("spectral_rfft_dy", a.stream);
+    hipLaunchKernelGGL((k_rfft_rings<float>), dim3(S.n_rings, a.B * C), dim3(kFftBlock), lds, a.stream, S.rings, dy,
+                       (const float2*)S.tw, dyh, a.B, C, a.op->g.nlat_o, M, 2.0f);
+    timing_end(tk, a.stream);
+    return hipGetLastError();
 }
 
 hipError_t launch_spectral(const ExecArgs& a, float* ws, int stages) {

@@ -179,6 +179,18 @@ def test_sample_parity_reads_the_sampled_pixels():
     ok = y.copy()
     ok[0, 0, 0, 1] += 1.0                      # flat pixel 1: not sampled
     assert bench.sample_parity(ok, ref, pix, "fp32")["pass"]
+    # per ring (8 longitudes per ring here): the planted error sits in ring 3
+    assert p["worst_ring"] == 3 and p["rings"] == 3
+    r3 = np.abs(ref[:, :, 2]).max()            # ring 3's only sampled pixel is 31
+    assert p["max_rel_worst_ring"] == pytest.approx(1.0 / r3)
+
+
+def test_copy_fraction_marks_hbm_rows_only():
+    rows = {"a": {"bound": "hbm", "alg_gbs": 4000.0}, "b": {"bound": "alu", "alg_gbs": 100.0},
+            "roof": {"bound": "hbm", "achieved": 3000.0, "unit": "GB/s"}}
+    bench.add_copy_fracs(rows, 5000.0)
+    assert rows["a"]["copy_frac"] == 0.8 and "copy_frac" not in rows["b"]
+    assert rows["roof"]["copy_frac"] == 0.6
 
 
 class _FakeEvent:

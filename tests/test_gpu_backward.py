@@ -83,6 +83,30 @@ def test_gradients_small_grids(case, transpose):
     assert np.abs(dx - rdx).max() <= 1e-5 * np.abs(rdx).max()
 
 
+@pytest.mark.parametrize("transpose", [False, True], ids=["forward", "transpose"])
+@pytest.mark.parametrize("grid,min_entries", [((64, 128), 64), ((64, 128), 160), ((96, 256), 96)],
+                         ids=lambda v: "x".join(map(str, v)) if isinstance(v, tuple) else str(v))
+def test_gradients_spectral_polar_caps(grid, min_entries, transpose, monkeypatch):
+    """The weight gradient's heavy rings summed in the frequency domain: with
+    the spectral threshold lowered so that both polar caps (and only they)
+    take the spectral path, dx and dW against the oracle in full."""
+    monkeypatch.setenv("DISCO_SPECTRAL_MIN_ENTRIES", str(min_entries))
+    n, m = grid
+    tc = 3 * math.pi / n
+    e = disco.psi_entries(n, m, n, m, tc, transpose=transpose)
+    counts = np.bincount(e["out_ring"], minlength=n)
+    heavy = counts >= min_entries
+    lo = int(np.argmin(heavy)) if not heavy.all() else n
+    hi = n - int(np.argmin(heavy[::-1])) if not heavy.all() else n
+    assert 0 < lo < hi < n and not heavy[lo:hi].any() and heavy[hi:].all(), (lo, hi)
+    say("spectral caps", grid, min_entries, "rings [0, %d) and [%d, %d)" % (lo, hi, n))
+    dx, dw, rdx, rdw = _run((n, m, n, m, "cell_centred", "bilinear3x3"), transpose, (3, 5), "fp32", 65)
+    ex, ew = rel_l2(dx, rdx), rel_l2(dw, rdw)
+    say("  dx rel_l2 %.3e  dw rel_l2 %.3e" % (ex, ew))
+    assert ex <= FP32_TOL and ew <= FP32_TOL
+    assert np.abs(dw - rdw).max() <= 1e-5 * np.abs(rdw).max()
+
+
 @pytest.mark.parametrize("chans", [(1, 1), (8, 8), (12, 20)], ids=lambda c: "%dto%d" % c)
 def test_gradients_channel_shapes(chans):
     for transpose in (False, True):
