@@ -33,5 +33,13 @@ hipError_t launch_gather_then_contract(const ExecArgs&, float*) { return hipErro
 size_t workspace_bytes_gather_z_all(const ExecArgs&) { return 0; }
 size_t workspace_bytes_contract_then_gather(const ExecArgs&) { return 0; }
 size_t workspace_bytes_gather_then_contract(const ExecArgs&) { return 0; }
+size_t spectral_dyhat_bytes(const ExecArgs&, int) { return 0; }
+size_t weight_grad_split_ws_bytes(int, int, int, int64_t, int, int64_t) { return 0; }
+hipError_t launch_gather_z_light(const ExecArgs&, float*, float*, float2**) { return hipErrorNotSupported; }
+hipError_t launch_spectral_dyhat(const ExecArgs&, const float*, int, float2*) { return hipErrorNotSupported; }
+hipError_t launch_weight_grad_split(const float*, const float*, int, int64_t, int64_t, const float*, const float*, int,
+                                    int64_t, float*, float*, int, int, int, bool, hipStream_t) {
+    return hipErrorNotSupported;
+}
 
 }  // namespace disco
