@@ -365,8 +365,19 @@ __global__ __launch_bounds__(kBlock) void k_reduce_partials(const int32_t* __res
     const int s0 = red_ptr[sp], s1 = red_ptr[sp + 1];
     const int64_t n_out = (int64_t)g.nlat_o * g.nlon_o;
     const int64_t pix = (int64_t)to * g.nlon_o + (int64_t)q * g.P + r;
+    // Loads of four slots issued together, then added in slot order.
+    const float* pq = partial + ((int64_t)b * Co + co) * g.nq + q;
+    const int64_t slot_stride = (int64_t)B * Co * g.nq;
     float acc = 0.0f;
-    for (int s = s0; s < s1; ++s) acc += partial[(((int64_t)red_slots[s] * B + b) * Co + co) * g.nq + q];
+    int s = s0;
+    for (; s + 4 <= s1; s += 4) {
+        float v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = pq[red_slots[s + u] * slot_stride];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc += v[u];
+    }
+    for (; s < s1; ++s) acc += pq[red_slots[s] * slot_stride];
     store_val(y, ((int64_t)b * Co + co) * n_out + pix, acc);
 }
 
