@@ -269,7 +269,10 @@ disco_status_t disco_transpose_algo(disco_plan_t plan, const disco_tensor_t* x,
  * forward weights (read for dx only).  dx or dw may be NULL (not computed);
  * dx is overwritten, dw is overwritten (not accumulated; zeros for B = 0).
  * dx must not overlap dy or w, dw none of x, dy and dx, and when dw is asked
- * for dx must not overlap x either (dx is written before x is read for dw).  The plan must have
+ * for dx must not overlap x either (dx may be written while x is read for
+ * dw: with both asked for, dw's pass runs on a plan-owned helper stream
+ * beside dx's, forked from stream and joined back into it, so the call's
+ * work is complete when stream's is).  The plan must have
  * been created with DISCO_PLAN_BACKWARD.  dw is reduced over pixels in a fixed
  * order (deterministic); with bf16 storage the gathered sums are rounded to
  * bf16 before the reduction, which accumulates in fp32; dw needs

@@ -69,6 +69,7 @@ struct disco_plan {
     void* wsel32 = nullptr;
     void* wsel16 = nullptr;
     hipStream_t aux = nullptr;  // runs the spectral rings beside the direct kernels
+    hipStream_t aux_dw = nullptr;  // runs the weight gradient's pass beside the input gradient's
     std::mutex lazy_mu;         // serialises the uploads of layouts on first use
 };
 
@@ -1027,9 +1028,9 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
             if ((s = check_device_ptr(dy->data, plan->device, "dy")) != DISCO_OK) return s;
             if (overlaps(dw, x) || overlaps(dw, dy) || (dx && overlaps(dw, dx)))
                 return fail(DISCO_ERR_INVALID_ARGUMENT, "dw overlaps another tensor");
-            // dx is written before the weight gradient's pass reads x.
+            // dx may be written while the weight gradient's pass reads x.
             if (dx && dx->data && overlaps(dx, x))
-                return fail(DISCO_ERR_INVALID_ARGUMENT, "dx overlaps x (x is read for dw after dx is written)");
+                return fail(DISCO_ERR_INVALID_ARGUMENT, "dx overlaps x (x is read for dw while dx is written)");
         }
         xz = *x;
         xz.shape[0] = B * C_x;
@@ -1056,6 +1057,42 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
             if ((s = check_device_ptr(x->data, plan->device, "x")) != DISCO_OK) return s;
         }
     }
+    // With both gradients asked for, the weight gradient's pass (bound by
+    // HBM: Z written, then reduced with dy) runs on the plan's second helper
+    // stream beside the input gradient (the adjoint op, bound by arithmetic),
+    // forked from the caller's stream and joined back into it on every return
+    // below.
+    hipStream_t ds = stream;
+    struct Join {
+        hipStream_t from = nullptr, to = nullptr;
+        hipEvent_t ev = nullptr;
+        ~Join() {
+            if (!ev) return;
+            (void)hipEventRecord(ev, from);
+            (void)hipStreamWaitEvent(to, ev, 0);
+            (void)hipEventDestroy(ev);
+        }
+    } join;
+    if (dx && dw && B > 0 && plan->aux_dw) {
+        int dev0 = 0;
+        (void)hipGetDevice(&dev0);
+        if (dev0 != plan->device) (void)hipSetDevice(plan->device);
+        hipEvent_t fork = nullptr, jev = nullptr;
+        hipError_t e = hipEventCreateWithFlags(&fork, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&jev, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventRecord(fork, stream);
+        if (e == hipSuccess) e = hipStreamWaitEvent(plan->aux_dw, fork, 0);
+        if (fork) (void)hipEventDestroy(fork);
+        if (dev0 != plan->device) (void)hipSetDevice(dev0);
+        if (e != hipSuccess) {
+            if (jev) (void)hipEventDestroy(jev);
+            return hip_fail(e, "stream fork");
+        }
+        join.from = plan->aux_dw;
+        join.to = stream;
+        join.ev = jev;
+        ds = plan->aux_dw;
+    }
     if (dx && (s = run_op(plan, adj, !transpose, dy, w, dx, stream, DISCO_ALGO_AUTO, depthwise)) != DISCO_OK) return s;
     if (!dw) return ok();
     int cur = 0;
@@ -1064,7 +1101,7 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
         return fail(DISCO_ERR_DEVICE, "hipSetDevice failed");
     if (B == 0) {
         struct Restore0 { int d; bool on; ~Restore0() { if (on) (void)hipSetDevice(d); } } r0{cur, cur != plan->device};
-        const hipError_t ez = launch_zero_fill(dw->data, (size_t)numel(dw) * elem_bytes(dw->dtype), stream);
+        const hipError_t ez = launch_zero_fill(dw->data, (size_t)numel(dw) * elem_bytes(dw->dtype), ds);
         return ez == hipSuccess ? ok() : hip_fail(ez, "kernel launch");
     }
     struct Restore { int d; bool on; ~Restore() { if (on) (void)hipSetDevice(d); } } restore{cur, cur != plan->device};
@@ -1075,7 +1112,7 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
     if (onepass && (s = ensure_parts(plan, op, kPartCore | kPartEntries)) != DISCO_OK) return s;
     ExecArgs za{};
     za.op = &op; za.x = x->data; za.dtype = 0; za.B = (int)B; za.Ci = (int)C_x; za.Co = (int)C_x * K;
-    za.w_trans = transpose; za.stream = stream;
+    za.w_trans = transpose; za.stream = ds;
     const size_t zbytes = ((size_t)(B * C_x) * K * (size_t)P * elem_bytes(x->dtype) + 255) & ~(size_t)255;
     const size_t zws = onepass ? workspace_bytes_gather_z_all(za) : 0;
     // With the heavy rings forming the two polar caps, their share of dW is
@@ -1093,11 +1130,11 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
                                     : weight_grad_ws_bytes((int)B, (int)C_dy, (int)(C_x * K), P);
     void* zbuf = nullptr;
     float* gws = nullptr;
-    hipError_t e = hipMallocAsync(&zbuf, zbytes + zws + dyh_bytes, stream);
+    hipError_t e = hipMallocAsync(&zbuf, zbytes + zws + dyh_bytes, ds);
     if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(gathered sums)");
-    e = hipMallocAsync((void**)&gws, gbytes, stream);
+    e = hipMallocAsync((void**)&gws, gbytes, ds);
     if (e != hipSuccess) {
-        (void)hipFreeAsync(zbuf, stream);
+        (void)hipFreeAsync(zbuf, ds);
         return hip_fail(e, "hipMallocAsync(weight gradient partials)");
     }
     zt.data = zbuf;
@@ -1110,26 +1147,26 @@ disco_status_t backward(disco_plan_t plan, bool transpose, const disco_tensor_t*
         if (e == hipSuccess)
             e = launch_weight_grad_split(dy32 + off_light, (const float*)zbuf + off_light, (int)B, p_light, P,
                                          (const float*)dyh, (const float*)zhat, b_heavy, p_heavy, (float*)dw->data,
-                                         gws, (int)C_dy, (int)C_x, K, transpose, stream);
+                                         gws, (int)C_dy, (int)C_x, K, transpose, ds);
         s = e == hipSuccess ? DISCO_OK : hip_fail(e, "kernel launch");
-        (void)hipFreeAsync(gws, stream);
-        (void)hipFreeAsync(zbuf, stream);
+        (void)hipFreeAsync(gws, ds);
+        (void)hipFreeAsync(zbuf, ds);
         return s == DISCO_OK ? ok() : s;
     }
     if (onepass) {
         e = launch_gather_z_all(za, (float*)zbuf, (float*)((char*)zbuf + zbytes));
         s = e == hipSuccess ? DISCO_OK : hip_fail(e, "kernel launch");
     } else {
-        s = run_op(plan, op, transpose, &xz, &wsel, &zt, stream, DISCO_ALGO_AUTO);
+        s = run_op(plan, op, transpose, &xz, &wsel, &zt, ds, DISCO_ALGO_AUTO);
     }
     if (s == DISCO_OK) {
-        e = depthwise ? launch_weight_grad_dw(dy->data, zbuf, dw->data, gws, x->dtype, (int)B, (int)C_x, K, P, stream)
+        e = depthwise ? launch_weight_grad_dw(dy->data, zbuf, dw->data, gws, x->dtype, (int)B, (int)C_x, K, P, ds)
                       : launch_weight_grad(dy->data, zbuf, dw->data, gws, x->dtype, (int)B, (int)C_dy, (int)C_x, K, P,
-                                           transpose, stream);
+                                           transpose, ds);
         if (e != hipSuccess) s = hip_fail(e, "kernel launch");
     }
-    (void)hipFreeAsync(gws, stream);
-    (void)hipFreeAsync(zbuf, stream);
+    (void)hipFreeAsync(gws, ds);
+    (void)hipFreeAsync(zbuf, ds);
     return s == DISCO_OK ? ok() : s;
 }
 
@@ -1327,6 +1364,8 @@ disco_status_t disco_plan_create(int nlat_in, int nlon_in, int nlat_out, int nlo
     for (const DeviceOp* d : {&plan->fwd, &plan->tr, &plan->fwd_adj, &plan->tr_adj})
         any_spectral |= d->spectral.n_rings > 0 || (d->tables && !d->tables->sp.rings.empty());
     if (any_spectral && hipStreamCreateWithFlags(&plan->aux, hipStreamNonBlocking) != hipSuccess) plan->aux = nullptr;
+    if ((p.flags & DISCO_PLAN_BACKWARD) && hipStreamCreateWithFlags(&plan->aux_dw, hipStreamNonBlocking) != hipSuccess)
+        plan->aux_dw = nullptr;
     // Keep freed workspace in the device's pool rather than returning it to
     // the driver at every synchronisation.
     hipMemPool_t pool;
@@ -1389,6 +1428,10 @@ disco_status_t disco_plan_destroy(disco_plan_t plan) {
     if (plan->aux) {
         (void)hipStreamSynchronize(plan->aux);
         (void)hipStreamDestroy(plan->aux);
+    }
+    if (plan->aux_dw) {
+        (void)hipStreamSynchronize(plan->aux_dw);
+        (void)hipStreamDestroy(plan->aux_dw);
     }
     free_op(&plan->fwd);
     free_op(&plan->tr);
