@@ -144,9 +144,9 @@ def test_backward_needs_the_plan_flag():
 
 
 def test_dx_aliasing_x_is_rejected_when_dw_is_asked_for():
-    """dx is written before x is read for dw: a dx that overlaps x is an
-    argument error then (nothing enqueued), and allowed when dw is not asked
-    for (x is not read)."""
+    """dx may be written while x is read for dw (the two passes run on
+    two streams): a dx that overlaps x is an argument error then (nothing
+    enqueued), and allowed when dw is not asked for (x is not read)."""
     import torch
     plan = disco.Plan(16, 32, 16, 32, 3 * math.pi / 16, backward=True)
     x, w = synth.random_inputs(71, (1, 2, 16, 32), (2, 2, 9))
