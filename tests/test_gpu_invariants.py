@@ -97,6 +97,23 @@ def test_empty_batch_and_plan_info():
     plan.close()
 
 
+def test_plan_memory_2048x4096():
+    """The 2048 x 4096 plan as created: the spectral pairs of the southern cap
+    read the northern tables (one table per mirrored pair), and the device
+    holds a small multiple of the compressed psi."""
+    wl = synth.WORKLOADS["sphere2048x4096"]
+    plan = disco.Plan(*wl.plan_args())
+    info = plan.info()
+    say("plan bytes %d, compressed %d, spectral pairs %d tables %d" % (
+        info["psi_bytes"], info["psi_compressed_bytes"], info["spectral_pairs_forward"],
+        info["spectral_tables_forward"]))
+    assert info["spectral_pairs_forward"] > 0
+    assert 2 * info["spectral_tables_forward"] == info["spectral_pairs_forward"]
+    assert 2 * info["spectral_tables_transpose"] == info["spectral_pairs_transpose"]
+    assert info["psi_bytes"] < 4 * info["psi_compressed_bytes"]
+    plan.close()
+
+
 def test_error_paths():
     import torch
     plan = disco.Plan(16, 32, 8, 16, 3 * math.pi / 8)
