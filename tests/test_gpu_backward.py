@@ -107,6 +107,33 @@ def test_gradients_spectral_polar_caps(grid, min_entries, transpose, monkeypatch
     assert np.abs(dw - rdw).max() <= 1e-5 * np.abs(rdw).max()
 
 
+@pytest.mark.parametrize("transpose", [False, True], ids=["forward", "transpose"])
+def test_gradient_passes_on_two_streams_match_each_alone(transpose):
+    """With dx and dW both asked for, dW's pass runs on a helper stream beside
+    dx's; the results equal, bitwise, those of each pass asked for alone (on
+    the caller's stream), repeated calls included, on a grid whose polar caps
+    take the spectral path."""
+    import torch
+    n, m = 128, 256
+    tc = 3 * math.pi / n
+    r = np.random.default_rng(66)
+    C1, C2 = 8, 8
+    x = torch_dev(r.standard_normal((2, C1, n, m)).astype(np.float32))
+    w = torch_dev((r.standard_normal((C1, C2, 9) if transpose else (C2, C1, 9)) / 8.0).astype(np.float32))
+    dy = torch_dev(r.standard_normal((2, C2, n, m)).astype(np.float32))
+    plan = disco.Plan(n, m, n, m, tc, backward=True)
+    assert plan.info()["spectral_rings_forward"] > 0
+    fn = disco.transpose_backward if transpose else disco.forward_backward
+    dx_only, _ = fn(plan, x, w, dy, want_dw=False)
+    _, dw_only = fn(plan, x, w, dy, want_dx=False)
+    for rep in range(3):
+        dx, dw = fn(plan, x, w, dy)
+        torch.cuda.synchronize()
+        say("two streams", "transpose" if transpose else "forward", "call", rep)
+        assert torch.equal(dx, dx_only) and torch.equal(dw, dw_only)
+    plan.close()
+
+
 @pytest.mark.parametrize("chans", [(1, 1), (8, 8), (12, 20)], ids=lambda c: "%dto%d" % c)
 def test_gradients_channel_shapes(chans):
     for transpose in (False, True):
