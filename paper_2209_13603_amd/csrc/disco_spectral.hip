@@ -180,9 +180,9 @@ __global__ __launch_bounds__(kFftBlock) void k_rfft_rings(const int32_t* __restr
     }
 }
 
-// Yhat[h][b][co][m] for heavy ring h.  grid: (ceil((M+1)/256), n_rings, B * n_cotiles)
-template <typename T, int COT>
-__global__ __launch_bounds__(kFftBlock) void k_spectral(const int32_t* __restrict__ pair_ptr,
+// Yhat[h][b][co][m] for heavy ring h.  grid: (ceil((M+1)/BLK), n_rings, B * n_cotiles)
+template <typename T, int COT, int BLK>
+__global__ __launch_bounds__(BLK) void k_spectral(const int32_t* __restrict__ pair_ptr,
                                                        const int32_t* __restrict__ pair_slot,
                                                        const int32_t* __restrict__ pair_tab,
                                                        const float* __restrict__ vs,
@@ -190,16 +190,15 @@ __global__ __launch_bounds__(kFftBlock) void k_spectral(const int32_t* __restric
                                                        const T* __restrict__ w, float2* __restrict__ yh,
                                                        int B, int Ci, int Co, int M, int n_cotiles,
                                                        bool w_trans) {
-    // Input channels per accumulation pass (output tiles have at most 8
-    // channels).
-    static_assert(COT <= 8, "output tiles of at most 8 channels");
+    // Input channels per accumulation pass.
+    static_assert(COT <= 32, "output tiles of at most 32 channels");
     constexpr int SC = 4;
     // This pass's weights as (W_3a + W_3a+2, W_3a+2 - W_3a, W_3a+1) for each
     // (input channel, output channel, a), staged in LDS and read back by
     // broadcast (as uniform scalar loads they would need more SGPRs than
     // there are and spill).
     __shared__ float wsd[SC * COT * 9];
-    const int m = blockIdx.x * kFftBlock + threadIdx.x;
+    const int m = blockIdx.x * BLK + threadIdx.x;
     const int h = blockIdx.y;
     const int b = blockIdx.z / n_cotiles;
     const int co0 = (blockIdx.z - b * n_cotiles) * COT;
@@ -211,7 +210,7 @@ __global__ __launch_bounds__(kFftBlock) void k_spectral(const int32_t* __restric
     for (int j = 0; j < COT; ++j) Y[j] = make_float2(0.0f, 0.0f);
     for (int ci0 = 0; ci0 < Ci; ci0 += SC) {
         __syncthreads();  // the previous pass's reads of wsd are done
-        for (int idx = threadIdx.x; idx < SC * COT * 3; idx += kFftBlock) {
+        for (int idx = threadIdx.x; idx < SC * COT * 3; idx += BLK) {
             const int c = idx / (COT * 3), r = idx - c * (COT * 3), j = r / 3, a = r - j * 3;
             const int ci = ci0 + c < Ci ? ci0 + c : Ci - 1;  // E, F, G are zero past Ci
             const int co = co0 + j < Co ? co0 + j : Co - 1;
@@ -398,7 +397,7 @@ __global__ __launch_bounds__(kFftBlock) void k_irfft_rings(const int32_t* __rest
     }
 }
 
-template <typename T, int COT>
+template <typename T, int COT, int BLK = kFftBlock>
 hipError_t spectral_launch(const ExecArgs& a, float* ws, int stages) {
     const SpectralDev& S = a.op->spectral;
     const OpGeom& g = a.op->g;
@@ -427,8 +426,8 @@ hipError_t spectral_launch(const ExecArgs& a, float* ws, int stages) {
     } else if (stages & 2) {
         const int n_cot = (a.Co + COT - 1) / COT;
         const int tk = timing_begin("spectral_mac", a.stream);
-        hipLaunchKernelGGL((k_spectral<T, COT>), dim3((M + 1 + kFftBlock - 1) / kFftBlock, S.n_rings, a.B * n_cot),
-                           dim3(kFftBlock), 0, a.stream, S.pair_ptr, S.pair_slot, S.pair_tab, S.vs, xh, (const T*)a.w, yh,
+        hipLaunchKernelGGL((k_spectral<T, COT, BLK>), dim3((M + 1 + BLK - 1) / BLK, S.n_rings, a.B * n_cot),
+                           dim3(BLK), 0, a.stream, S.pair_ptr, S.pair_slot, S.pair_tab, S.vs, xh, (const T*)a.w, yh,
                            a.B, a.Ci, a.Co, M, n_cot, a.w_trans);
         timing_end(tk, a.stream);
         const hipError_t e = hipGetLastError();
@@ -451,6 +450,11 @@ hipError_t spectral_dispatch(const ExecArgs& a, float* ws, int stages) {
     // products 207 -> 136 us with tiles of 8, where each tile redoes the
     // cheap per-pair sums).
     if (a.Co <= 4) return spectral_launch<T, 4>(a, ws, stages);
+    if (a.Co <= 8 || (stages & kSpectralZ)) return spectral_launch<T, 8>(a, ws, stages);
+    // More output channels: one tile of up to 32 (the per-pair sums done
+    // once), the frequencies in workgroups of 64 so that they still fill
+    // the chip.
+    if (a.Co <= 32) return spectral_launch<T, 32, 64>(a, ws, stages);
     return spectral_launch<T, 8>(a, ws, stages);
 }
 
